@@ -1,0 +1,332 @@
+// SparseCoder oracle: a plain, slow, obviously correct CPU implementation of
+// sliding-window + global-token sparse self-attention with learned-token-pruning
+// scores, threshold masking, compaction, and the attention-only encoder stack.
+//
+// TEST INFRASTRUCTURE ONLY.  Nothing on the product path may call this code:
+// only the tests, the smoke check and the benchmark's CPU-baseline leg do.  It
+// shares no code, header, table or helper with the HIP library.
+//
+// Everything is computed in double precision from the exact input values.
+// Sources (SparseCoder, arXiv 2310.07109):
+//   * sliding-window local attention: token i attends to its neighbours within
+//     the window (Sec. 4.2.1, Fig. 4); global ("special") tokens attend to every
+//     token and are attended to by every token (Sec. 3.1, Fig. 3b-c; Sec. 5.5);
+//   * importance score of a token: attention probabilities accumulated down the
+//     token's column after the row-wise softmax (Sec. 1, Fig. 1 caption;
+//     Sec. 3.2), for sparse attention the band's sub-diagonal plus the global
+//     rows and columns (Sec. 5.5); normalised here to the mean over heads and
+//     valid queries;
+//   * binarised mask: keep iff score > layer threshold, strictly (Sec. 4.2.2,
+//     the display equation of step 2); hard pruning removes masked tokens
+//     (Sec. 4.2.2 step 3) and later layers see the shorter sequence (Sec. 4.2).
+// Where the paper is silent the readings are: half-width r = floor(w/2) with
+// |i - j| <= r inclusive; the softmax scale is an argument; prefix padding
+// (tokens >= valid length are neither queries nor keys); scores divided by
+// H * valid length so that they sum to one over a sequence; kept tokens stay in
+// ascending order; global tokens are kept when keep_global is set.
+//
+// Pins: tests/test_oracle_pins.py checks every function here against brute
+// force, closed forms, library routines and invariants.
+#include <algorithm>
+#include <cmath>
+#include <cstdint>
+#include <cstring>
+#include <limits>
+#include <vector>
+#ifdef _OPENMP
+#include <omp.h>
+#endif
+
+namespace {
+
+int set_threads(int nthreads) {
+#ifdef _OPENMP
+  if (nthreads > 0) omp_set_num_threads(nthreads);
+  return omp_get_max_threads();
+#else
+  (void)nthreads;
+  return 1;
+#endif
+}
+
+// Round a double to the nearest bfloat16 value (8 significant bits), ties to
+// even, returned as a double.  bfloat16 keeps float32's exponent range.
+double round_bf16(double x) {
+  if (x == 0.0 || !std::isfinite(x)) return x;
+  int e;
+  std::frexp(x, &e);  // |x| = f * 2^e, f in [0.5, 1)
+  int ulp_exp = e - 8;
+  if (ulp_exp < -133) ulp_exp = -133;  // subnormal spacing of float32
+  double ulp = std::ldexp(1.0, ulp_exp);
+  double q = std::nearbyint(x / ulp) * ulp;  // default rounding mode: ties to even
+  const double maxbf = std::ldexp(255.0, 120);  // (2 - 2^-7) * 2^127
+  if (std::fabs(q) > maxbf) return std::copysign(std::numeric_limits<double>::infinity(), x);
+  return q;
+}
+
+// The attention of one (sequence, head).  Rows are tokens; row stride is `ld`
+// doubles between consecutive tokens.  Writes out rows (stride ld_out), the
+// per-query log-sum-exp, and adds every probability P[q][k] into colsum[k].
+void attend_one_head(int n, int d, int L, int r, const std::vector<char>& is_global, double alpha,
+                     const double* q, const double* k, const double* v, long ld, double* out, long ld_out,
+                     double* lse, double* colsum) {
+  std::vector<int> nbr;
+  std::vector<double> s;
+  nbr.reserve(n);
+  s.reserve(n);
+  for (int i = 0; i < n; ++i) {
+    double* o = out + (long)i * ld_out;
+    if (i >= L) {  // padding query: no token, no output
+      for (int c = 0; c < d; ++c) o[c] = 0.0;
+      lse[i] = -std::numeric_limits<double>::infinity();
+      continue;
+    }
+    // Allowed(i, j): both valid, and inside the window or either one global.
+    nbr.clear();
+    for (int j = 0; j < L; ++j)
+      if (std::abs(i - j) <= r || is_global[i] || is_global[j]) nbr.push_back(j);
+    s.assign(nbr.size(), 0.0);
+    double m = -std::numeric_limits<double>::infinity();
+    for (size_t t = 0; t < nbr.size(); ++t) {
+      const double* qi = q + (long)i * ld;
+      const double* kj = k + (long)nbr[t] * ld;
+      double acc = 0.0;
+      for (int c = 0; c < d; ++c) acc += qi[c] * kj[c];
+      s[t] = alpha * acc;
+      m = std::max(m, s[t]);
+    }
+    double z = 0.0;
+    for (size_t t = 0; t < nbr.size(); ++t) z += std::exp(s[t] - m);
+    for (int c = 0; c < d; ++c) o[c] = 0.0;
+    for (size_t t = 0; t < nbr.size(); ++t) {
+      double p = std::exp(s[t] - m) / z;
+      const double* vj = v + (long)nbr[t] * ld;
+      for (int c = 0; c < d; ++c) o[c] += p * vj[c];
+      colsum[nbr[t]] += p;
+    }
+    lse[i] = m + std::log(z);
+  }
+}
+
+std::vector<char> global_flags(int n, int L, int G, const int32_t* gp) {
+  std::vector<char> f(n, 0);
+  for (int j = 0; j < G; ++j) {
+    int p = gp[j];
+    if (p >= 0 && p < L) f[p] = 1;
+  }
+  return f;
+}
+
+}  // namespace
+
+extern "C" {
+
+// Exposed so the tests can pin the rounding against a library conversion.
+double orc_round_bf16(double x) { return round_bf16(x); }
+
+// Sparse attention over a padded batch, layout [B, n, H, d] (token-major).
+//   window: full width w; a query attends to keys with |i - j| <= floor(w/2).
+//   global_pos: [B, G]; entries outside [0, valid_len[b]) are unused slots.
+//   out [B, n, H, d]; lse [B, H, n] (-inf for padding rows); scores [B, n]:
+//   s_k = (1 / (H * L)) * sum_h sum_{q < L} P_h[q][k] for k < L, 0 otherwise.
+//   colsum (optional) [B, H, n]: the per-head column sums before averaging.
+int orc_sparse_attention(int B, int n, int H, int d, int window, int G, const int32_t* global_pos,
+                         const int32_t* valid_len, double alpha, const double* q, const double* k,
+                         const double* v, double* out, double* lse, double* scores, double* colsum,
+                         int nthreads) {
+  if (B < 0 || n < 0 || H <= 0 || d <= 0 || window < 0 || G < 0) return -1;
+  set_threads(nthreads);
+  const int r = window / 2;
+  const long ld = (long)H * d;
+  std::vector<double> cs((size_t)B * H * n, 0.0);
+#pragma omp parallel for schedule(dynamic, 1)
+  for (long bh = 0; bh < (long)B * H; ++bh) {
+    int b = (int)(bh / H), h = (int)(bh % H);
+    int L = std::min(std::max(valid_len[b], 0), n);
+    std::vector<char> g = global_flags(n, L, G, global_pos + (long)b * G);
+    long base = (long)b * n * ld + (long)h * d;
+    attend_one_head(n, d, L, r, g, alpha, q + base, k + base, v + base, ld, out + base, ld,
+                    lse + ((long)b * H + h) * n, cs.data() + ((size_t)b * H + h) * n);
+  }
+  for (int b = 0; b < B; ++b) {
+    int L = std::min(std::max(valid_len[b], 0), n);
+    for (int j = 0; j < n; ++j) {
+      double acc = 0.0;
+      if (j < L)
+        for (int h = 0; h < H; ++h) acc += cs[((size_t)b * H + h) * n + j];
+      scores[(long)b * n + j] = (j < L) ? acc / ((double)H * L) : 0.0;
+    }
+  }
+  if (colsum) std::memcpy(colsum, cs.data(), cs.size() * sizeof(double));
+  return 0;
+}
+
+// Binarised mask and hard pruning of one layer.  The decision is taken on the
+// float32 score against the float32 threshold: keep iff k < L and (s > theta
+// or (keep_global and k is global)).  Kept tokens keep their relative order.
+//   keep_idx [B, n]: input index of the j-th kept token, -1 for j >= new_len.
+//   new_global_pos [B, G]: surviving global tokens renumbered, -1 padded.
+//   orig_in (optional) [B, n] composes into orig_out [B, n] = orig_in[keep_idx]
+//   (identity when orig_in is NULL), -1 beyond new_len.
+int orc_ltp_prune(int B, int n, int G, const int32_t* global_pos, const int32_t* valid_len,
+                  const float* scores, float threshold, int keep_global, int32_t* keep_idx, int32_t* new_len,
+                  int32_t* new_global_pos, const int32_t* orig_in, int32_t* orig_out) {
+  if (B < 0 || n < 0 || G < 0) return -1;
+  for (int b = 0; b < B; ++b) {
+    int L = std::min(std::max(valid_len[b], 0), n);
+    std::vector<char> g = global_flags(n, L, G, global_pos + (long)b * G);
+    std::vector<int> new_index(n, -1);
+    int cnt = 0;
+    for (int k = 0; k < n; ++k) {
+      bool keep = k < L && (scores[(long)b * n + k] > threshold || (keep_global && g[k]));
+      if (keep) {
+        new_index[k] = cnt;
+        keep_idx[(long)b * n + cnt] = k;
+        ++cnt;
+      }
+    }
+    for (int j = cnt; j < n; ++j) keep_idx[(long)b * n + j] = -1;
+    new_len[b] = cnt;
+    int gc = 0;
+    for (int j = 0; j < G; ++j) {
+      int p = global_pos[(long)b * G + j];
+      if (p >= 0 && p < L && new_index[p] >= 0) new_global_pos[(long)b * G + gc++] = new_index[p];
+    }
+    for (int j = gc; j < G; ++j) new_global_pos[(long)b * G + j] = -1;
+    if (orig_out) {
+      for (int j = 0; j < n; ++j) {
+        int src = keep_idx[(long)b * n + j];
+        orig_out[(long)b * n + j] = src < 0 ? -1 : (orig_in ? orig_in[(long)b * n + src] : src);
+      }
+    }
+  }
+  return 0;
+}
+
+// Row gather of a padded [B, n, row_bytes] tensor: dst row j = src row
+// keep_idx[j] for j < new_len[b]; rows at or beyond new_len are left untouched.
+int orc_gather_rows(int B, int n, long row_bytes, const void* src, void* dst, const int32_t* keep_idx,
+                    const int32_t* new_len) {
+  const char* s = static_cast<const char*>(src);
+  char* t = static_cast<char*>(dst);
+  for (int b = 0; b < B; ++b)
+    for (int j = 0; j < new_len[b]; ++j) {
+      int k = keep_idx[(long)b * n + j];
+      std::memcpy(t + ((long)b * n + j) * row_bytes, s + ((long)b * n + k) * row_bytes, row_bytes);
+    }
+  return 0;
+}
+
+// One layer of the attention-only encoder stack (RoBERTa-shaped, no FFN):
+//   qkv = bf16(x . Wqkv)            [columns q | k | v, each head-major]
+//   O   = bf16(sparse attention(q, k, v))
+//   s   = float32(importance scores); keep / compaction as orc_ltp_prune
+//   y   = bf16(LayerNorm(x + O . Wo)) on the kept rows, gamma = 1, beta = 0,
+//         biased variance, eps inside the square root.
+// x: [B, n, D] exact bf16 values; Wqkv: [D, 3D] and Wo: [D, D] row-major.
+// Outputs: y [B, n, D] compacted (rows >= new_len zero), keep_idx [B, n],
+// new_len [B], new_global_pos [B, G], scores (optional) [B, n] float32.
+int orc_encoder_layer(int B, int n, int H, int d, int window, int G, const int32_t* global_pos,
+                      const int32_t* valid_len, double alpha, const double* x, const double* Wqkv,
+                      const double* Wo, float threshold, int keep_global, double ln_eps, double* y,
+                      int32_t* keep_idx, int32_t* new_len, int32_t* new_global_pos, float* scores_out,
+                      int nthreads) {
+  if (B < 0 || n < 0 || H <= 0 || d <= 0) return -1;
+  set_threads(nthreads);
+  const long D = (long)H * d, D3 = 3 * D;
+  std::vector<double> qv((size_t)B * n * D), kv((size_t)B * n * D), vv((size_t)B * n * D);
+  // a1: projection, double accumulation, bf16 storage.  Padding rows are
+  // projected too; the attention never reads them.
+#pragma omp parallel for schedule(static)
+  for (long row = 0; row < (long)B * n; ++row) {
+    const double* xr = x + row * D;
+    std::vector<double> acc(D3, 0.0);
+    for (long c = 0; c < D; ++c) {
+      double xv = xr[c];
+      const double* w = Wqkv + c * D3;
+      for (long j = 0; j < D3; ++j) acc[j] += xv * w[j];
+    }
+    for (long j = 0; j < D; ++j) {
+      qv[row * D + j] = round_bf16(acc[j]);
+      kv[row * D + j] = round_bf16(acc[D + j]);
+      vv[row * D + j] = round_bf16(acc[2 * D + j]);
+    }
+  }
+  std::vector<double> o((size_t)B * n * D), lse((size_t)B * H * n), sc((size_t)B * n);
+  int rc = orc_sparse_attention(B, n, H, d, window, G, global_pos, valid_len, alpha, qv.data(), kv.data(),
+                                vv.data(), o.data(), lse.data(), sc.data(), nullptr, nthreads);
+  if (rc) return rc;
+  for (auto& e : o) e = round_bf16(e);
+  std::vector<float> s32((size_t)B * n);
+  for (size_t i = 0; i < s32.size(); ++i) s32[i] = (float)sc[i];
+  if (scores_out) std::memcpy(scores_out, s32.data(), s32.size() * sizeof(float));
+  orc_ltp_prune(B, n, G, global_pos, valid_len, s32.data(), threshold, keep_global, keep_idx, new_len,
+                new_global_pos, nullptr, nullptr);
+  // a9 on the kept rows: residual + output projection + LayerNorm.
+#pragma omp parallel for schedule(dynamic, 4)
+  for (long row = 0; row < (long)B * n; ++row) {
+    int b = (int)(row / n), j = (int)(row % n);
+    double* yr = y + row * D;
+    if (j >= new_len[b]) {
+      for (long c = 0; c < D; ++c) yr[c] = 0.0;
+      continue;
+    }
+    long src = (long)b * n + keep_idx[row];
+    std::vector<double> t(D);
+    for (long c = 0; c < D; ++c) t[c] = x[src * D + c];
+    for (long c = 0; c < D; ++c) {
+      double ov = o[src * D + c];
+      const double* w = Wo + c * D;
+      for (long e = 0; e < D; ++e) t[e] += ov * w[e];
+    }
+    double mean = 0.0;
+    for (long c = 0; c < D; ++c) mean += t[c];
+    mean /= (double)D;
+    double var = 0.0;
+    for (long c = 0; c < D; ++c) var += (t[c] - mean) * (t[c] - mean);
+    var /= (double)D;
+    double inv = 1.0 / std::sqrt(var + ln_eps);
+    for (long c = 0; c < D; ++c) yr[c] = round_bf16((t[c] - mean) * inv);
+  }
+  return 0;
+}
+
+// The multi-layer stack: orc_encoder_layer applied n_layers times, each layer
+// on the previous layer's compacted output and renumbered global tokens.
+//   Wqkv: n_layers consecutive [D, 3D] matrices; Wo: n_layers consecutive [D, D].
+//   thresholds [n_layers]; y [B, n, D]; final_len [B]; orig_idx [B, n] (input
+//   position of each surviving row, -1 beyond final_len); kept_per_layer
+//   [n_layers, B] (sequence length after each layer's pruning).
+int orc_encoder_stack(int B, int n, int H, int d, int window, int G, const int32_t* global_pos,
+                      const int32_t* valid_len, double alpha, int n_layers, const double* x, const double* Wqkv,
+                      const double* Wo, const float* thresholds, int keep_global, double ln_eps, double* y,
+                      int32_t* final_len, int32_t* orig_idx, int32_t* kept_per_layer, int nthreads) {
+  const long D = (long)H * d;
+  std::vector<double> cur(x, x + (size_t)B * n * D), nxt((size_t)B * n * D);
+  std::vector<int32_t> len(valid_len, valid_len + B), gp(global_pos, global_pos + (size_t)B * G);
+  std::vector<int32_t> orig((size_t)B * n), orig2((size_t)B * n), kidx((size_t)B * n), nl(B), ngp((size_t)B * G);
+  for (int b = 0; b < B; ++b)
+    for (int j = 0; j < n; ++j) orig[(size_t)b * n + j] = j < len[b] ? j : -1;
+  for (int l = 0; l < n_layers; ++l) {
+    int rc = orc_encoder_layer(B, n, H, d, window, G, gp.data(), len.data(), alpha, cur.data(),
+                               Wqkv + (size_t)l * D * 3 * D, Wo + (size_t)l * D * D, thresholds[l], keep_global,
+                               ln_eps, nxt.data(), kidx.data(), nl.data(), ngp.data(), nullptr, nthreads);
+    if (rc) return rc;
+    for (int b = 0; b < B; ++b)
+      for (int j = 0; j < n; ++j) {
+        int s = kidx[(size_t)b * n + j];
+        orig2[(size_t)b * n + j] = s < 0 ? -1 : orig[(size_t)b * n + s];
+      }
+    orig.swap(orig2);
+    cur.swap(nxt);
+    len = nl;
+    gp = ngp;
+    for (int b = 0; b < B; ++b) kept_per_layer[(size_t)l * B + b] = len[b];
+  }
+  std::memcpy(y, cur.data(), cur.size() * sizeof(double));
+  std::memcpy(final_len, len.data(), (size_t)B * sizeof(int32_t));
+  std::memcpy(orig_idx, orig.data(), orig.size() * sizeof(int32_t));
+  return 0;
+}
+
+}  // extern "C"

@@ -1,0 +1,265 @@
+"""Seeded synthetic inputs for the sparse-attention + token-pruning path.
+
+This module is shared by both sides of every parity check (the CPU oracle
+and the HIP library) and therefore holds none of the method's arithmetic:
+only counter-based random draws, quantisation of those draws to the storage
+dtype, and the shapes / length mixes / global-token layouts of the workloads.
+
+Random numbers: splitmix64 (Steele, Lea, Flood, "Fast splittable
+pseudorandom number generators", OOPSLA 2014) evaluated on a counter, top 53
+bits -> uniform double in [0, 1), Box-Muller for normals.  Every tensor has
+its own stream id, so a tensor's values do not depend on what else was drawn.
+"""
+from __future__ import annotations
+
+import math
+from dataclasses import dataclass, field
+
+import numpy as np
+
+_GAMMA = np.uint64(0x9E3779B97F4A7C15)
+_M1 = np.uint64(0xBF58476D1CE4E5B9)
+_M2 = np.uint64(0x94D049BB133111EB)
+
+# Stream ids (one per drawn tensor / quantity).
+S_Q, S_K, S_V, S_LEN, S_GLOB, S_SPIKE_U, S_SPIKE_V, S_X = 1, 2, 3, 4, 5, 6, 7, 8
+S_SPIKE_UQ = 9
+S_WQKV0, S_WO0 = 100, 101  # + 2 * layer
+
+
+def _mix(z: np.ndarray) -> np.ndarray:
+    z = (z ^ (z >> np.uint64(30))) * _M1
+    z = (z ^ (z >> np.uint64(27))) * _M2
+    return z ^ (z >> np.uint64(31))
+
+
+def raw_u64(seed: int, stream: int, count: int, offset: int = 0) -> np.ndarray:
+    """splitmix64 outputs number offset..offset+count-1 of stream (seed, stream)."""
+    with np.errstate(over="ignore"):
+        base = _mix(np.array([(seed << 20) + stream], dtype=np.uint64))[0]
+        ctr = np.arange(offset + 1, offset + count + 1, dtype=np.uint64)
+        return _mix(base + ctr * _GAMMA)
+
+
+def uniform(seed: int, stream: int, count: int, offset: int = 0) -> np.ndarray:
+    """Doubles in [0, 1) with 53 random bits."""
+    return (raw_u64(seed, stream, count, offset) >> np.uint64(11)).astype(np.float64) * (2.0 ** -53)
+
+
+def normal(seed: int, stream: int, count: int) -> np.ndarray:
+    """Standard normal doubles by Box-Muller on consecutive uniform pairs."""
+    m = (count + 1) // 2
+    u = uniform(seed, stream, 2 * m)
+    u1 = 1.0 - u[0::2]  # (0, 1]
+    u2 = u[1::2]
+    rad = np.sqrt(-2.0 * np.log(u1))
+    z = np.empty(2 * m, dtype=np.float64)
+    z[0::2] = rad * np.cos(2.0 * math.pi * u2)
+    z[1::2] = rad * np.sin(2.0 * math.pi * u2)
+    return z[:count]
+
+
+def randint(seed: int, stream: int, count: int, lo: int, hi: int, offset: int = 0) -> np.ndarray:
+    """Integers uniform in [lo, hi] (inclusive)."""
+    u = uniform(seed, stream, count, offset)
+    return (lo + np.floor(u * (hi - lo + 1))).astype(np.int64)
+
+
+# ---------------------------------------------------------------- dtypes ----
+def f64_to_bf16_bits(x: np.ndarray) -> np.ndarray:
+    """Round doubles to float32 (RNE), then float32 to bfloat16 (RNE); uint16 bits."""
+    b = np.ascontiguousarray(x, dtype=np.float64).astype(np.float32).view(np.uint32)
+    lsb = (b >> np.uint32(16)) & np.uint32(1)
+    with np.errstate(over="ignore"):
+        r = (b + np.uint32(0x7FFF) + lsb) >> np.uint32(16)
+    return r.astype(np.uint16)
+
+
+def bf16_bits_to_f64(bits: np.ndarray) -> np.ndarray:
+    return (np.asarray(bits, dtype=np.uint16).astype(np.uint32) << np.uint32(16)).view(np.float32).astype(np.float64)
+
+
+def quantise(x: np.ndarray, dtype: str):
+    """(storage array, exact double values) for dtype 'f32' or 'bf16'."""
+    if dtype == "f32":
+        s = x.astype(np.float32)
+        return s, s.astype(np.float64)
+    if dtype == "bf16":
+        s = f64_to_bf16_bits(x)
+        return s, bf16_bits_to_f64(s)
+    raise ValueError(dtype)
+
+
+# --------------------------------------------------------------- configs ----
+@dataclass
+class AttnConfig:
+    """One single-layer (or multi-pass) attention workload."""
+    name: str
+    seed: int
+    B: int
+    n: int
+    H: int
+    d: int
+    dtype: str
+    window: int
+    len_range: tuple            # (lo, hi) inclusive; lo == hi == n means no padding
+    n_global: int               # global slots per sequence
+    global_mode: str            # "first" (position 0 only) or "random" (distinct, sorted)
+    thresholds: list = field(default_factory=list)  # one per prune pass; None = stored value
+    input_scale: float = 0.125  # Q, K, V ~ N(0,1) * input_scale
+    spike_rank: int = 0
+    spike_amp: float = 0.0
+    spike_on_q: bool = False
+    alpha: float = 0.125        # softmax scale 1/sqrt(d)
+
+
+@dataclass
+class StackConfig:
+    name: str
+    seed: int
+    B: int
+    n: int
+    H: int
+    d: int
+    n_layers: int
+    window: int
+    len_range: tuple
+    n_global: int
+    w_std: float
+    theta_max: float
+    alpha: float = 0.125
+    ln_eps: float = 1e-5
+
+    @property
+    def D(self):
+        return self.H * self.d
+
+    def thresholds(self):
+        """Per-layer thresholds increasing linearly from 0 to theta_max over the layers."""
+        if self.n_layers == 1:
+            return [0.0]
+        return [self.theta_max * l / (self.n_layers - 1) for l in range(self.n_layers)]
+
+
+CONFIGS = {
+    1: AttnConfig("fp32 single layer B1 n512 H12 w64", 0, 1, 512, 12, 64, "f32", 64, (512, 512), 1, "first",
+                  thresholds=[0.002]),
+    2: AttnConfig("bf16 single layer B8 n1024 H12 w256 varlen", 1, 8, 1024, 12, 64, "bf16", 256, (512, 1024), 1,
+                  "first", thresholds=[None]),
+    4: AttnConfig("bf16 single layer B8 n4096 H12 w512 G32 varlen", 3, 8, 4096, 12, 64, "bf16", 512, (2048, 4096), 32,
+                  "random", thresholds=[None]),
+    5: AttnConfig("bf16 three prune passes B2 n8192 H16 w1024 G64 K-spike", 4, 2, 8192, 16, 64, "bf16", 1024,
+                  (8192, 8192), 64, "random", thresholds=[0.0005, 0.001, 0.002], spike_rank=4, spike_amp=3.0),
+}
+CONFIGS["5b"] = AttnConfig("bf16 three prune passes B2 n8192 H16 w1024 G64 QK-spike", 4, 2, 8192, 16, 64, "bf16",
+                           1024, (8192, 8192), 64, "random", thresholds=[0.0005, 0.001, 0.002], spike_rank=4,
+                           spike_amp=3.0, spike_on_q=True)
+
+STACK_CONFIG = StackConfig("bf16 12-layer attention stack B16 n2048 D768 w512", 2, 16, 2048, 12, 64, 12, 512,
+                           (256, 2048), 1, 0.02, 0.01)
+
+
+def lengths(seed: int, B: int, lo: int, hi: int) -> np.ndarray:
+    if lo == hi:
+        return np.full(B, lo, dtype=np.int32)
+    return randint(seed, S_LEN, B, lo, hi).astype(np.int32)
+
+
+def global_positions(seed: int, valid_len: np.ndarray, G: int, mode: str) -> np.ndarray:
+    """[B, G] int32, ascending and distinct per row, each < valid_len[b]; -1 pads unused slots."""
+    B = len(valid_len)
+    out = np.full((B, G), -1, dtype=np.int32)
+    if G == 0:
+        return out
+    for b in range(B):
+        L = int(valid_len[b])
+        if L == 0:
+            continue
+        if mode == "first":
+            out[b, 0] = 0
+            continue
+        g = min(G, L)
+        u = uniform(seed, S_GLOB, g, offset=b * 1_000_003)
+        perm = np.arange(L, dtype=np.int64)
+        for i in range(g):  # partial Fisher-Yates
+            j = i + int(u[i] * (L - i))
+            perm[i], perm[j] = perm[j], perm[i]
+        out[b, :g] = np.sort(perm[:g])
+    return out
+
+
+def _low_rank(seed, su, sv, B, n, H, d, rank, amp):
+    """amp * U_h V_h^T per (b, h): U ~ N(0,1) [n, rank], V ~ N(0,1)/8 [d, rank]; shape [B, n, H, d]."""
+    U = normal(seed, su, B * H * n * rank).reshape(B, H, n, rank)
+    V = normal(seed, sv, B * H * d * rank).reshape(B, H, d, rank) / 8.0
+    return amp * np.einsum("bhnr,bhdr->bnhd", U, V)
+
+
+def make_attention_inputs(cfg: AttnConfig, seed: int | None = None, B=None, n=None, H=None, window=None,
+                          n_global=None, len_range=None, dtype=None):
+    """Q, K, V (storage + exact doubles), valid lengths and global positions for one workload.
+
+    Keyword overrides shrink or vary a config for tests; the draws stay seeded.
+    """
+    seed = cfg.seed if seed is None else seed
+    B = cfg.B if B is None else B
+    n = cfg.n if n is None else n
+    H = cfg.H if H is None else H
+    d = cfg.d
+    window = cfg.window if window is None else window
+    G = cfg.n_global if n_global is None else n_global
+    lo, hi = cfg.len_range if len_range is None else len_range
+    lo, hi = min(lo, n), min(hi, n)
+    dtype = cfg.dtype if dtype is None else dtype
+    shape = (B, n, H, d)
+    cnt = B * n * H * d
+    q = normal(seed, S_Q, cnt).reshape(shape) * cfg.input_scale
+    k = normal(seed, S_K, cnt).reshape(shape) * cfg.input_scale
+    v = normal(seed, S_V, cnt).reshape(shape) * cfg.input_scale
+    if cfg.spike_rank > 0:
+        k = k + _low_rank(seed, S_SPIKE_U, S_SPIKE_V, B, n, H, d, cfg.spike_rank, cfg.spike_amp)
+        if cfg.spike_on_q:
+            q = q + _low_rank(seed, S_SPIKE_UQ, S_SPIKE_V, B, n, H, d, cfg.spike_rank, cfg.spike_amp)
+    vl = lengths(seed, B, lo, hi)
+    gp = global_positions(seed, vl, G, cfg.global_mode)
+    out = dict(B=B, n=n, H=H, d=d, window=window, G=G, dtype=dtype, alpha=cfg.alpha, valid_len=vl, global_pos=gp)
+    for name, x in (("q", q), ("k", k), ("v", v)):
+        s, e = quantise(x, dtype)
+        out[name] = s
+        out[name + "64"] = e
+    return out
+
+
+def make_stack_inputs(cfg: StackConfig, seed: int | None = None, B=None, n=None, n_layers=None, len_range=None,
+                      H=None):
+    """Hidden states, per-layer weights (bf16 storage + exact doubles), lengths and global positions."""
+    seed = cfg.seed if seed is None else seed
+    B = cfg.B if B is None else B
+    n = cfg.n if n is None else n
+    H = cfg.H if H is None else H
+    D = H * cfg.d
+    nl = cfg.n_layers if n_layers is None else n_layers
+    lo, hi = cfg.len_range if len_range is None else len_range
+    lo, hi = min(lo, n), min(hi, n)
+    x = normal(seed, S_X, B * n * D).reshape(B, n, D)
+    xs, x64 = quantise(x, "bf16")
+    wqkv, wqkv64, wo, wo64 = [], [], [], []
+    for l in range(nl):
+        a = normal(seed, S_WQKV0 + 2 * l, D * 3 * D).reshape(D, 3 * D) * cfg.w_std
+        b = normal(seed, S_WO0 + 2 * l, D * D).reshape(D, D) * cfg.w_std
+        s, e = quantise(a, "bf16")
+        wqkv.append(s)
+        wqkv64.append(e)
+        s, e = quantise(b, "bf16")
+        wo.append(s)
+        wo64.append(e)
+    vl = lengths(seed, B, lo, hi)
+    gp = global_positions(seed, vl, cfg.n_global, "first")
+    return dict(B=B, n=n, H=H, d=cfg.d, D=D, n_layers=nl, window=cfg.window, G=cfg.n_global, alpha=cfg.alpha,
+                ln_eps=cfg.ln_eps, x=xs, x64=x64, wqkv=wqkv, wqkv64=wqkv64, wo=wo, wo64=wo64, valid_len=vl,
+                global_pos=gp)
+
+
+def paper_threshold_schedule(final_threshold: float, n_layers: int):
+    """Thresholds of layers 1..n_layers growing linearly with depth to final_threshold at the last layer."""
+    return [final_threshold * l / n_layers for l in range(1, n_layers + 1)]

@@ -1,0 +1,71 @@
+"""Plant plausible mistakes in copies of the oracle (CPU only) and show that the
+pins in test_oracle_pins.py catch every one of them.
+
+Each mutant is a textual edit of sc_oracle.cpp compiled to a temporary library;
+the pins then run against it and at least one must fail.
+"""
+import ctypes
+import os
+import subprocess
+
+import pytest
+
+import oracle
+import test_oracle_pins as pins
+
+SRC = os.path.join(os.path.dirname(os.path.dirname(os.path.abspath(__file__))), "oracle", "sc_oracle.cpp")
+
+MUTANTS = [
+    ("window off by one", "std::abs(i - j) <= r ||", "std::abs(i - j) < r ||"),
+    ("global columns dropped", "|| is_global[i] || is_global[j]", "|| is_global[i]"),
+    ("global rows dropped", "|| is_global[i] || is_global[j]", "|| is_global[j]"),
+    ("scores divided by padded length", "acc / ((double)H * L)", "acc / ((double)H * n)"),
+    ("column sum credited to the query", "colsum[nbr[t]] += p;", "colsum[i] += p;"),
+    ("softmax sum without the max shift", "z += std::exp(s[t] - m);", "z += std::exp(s[t]);"),
+    ("softmax scale ignored", "s[t] = alpha * acc;", "s[t] = acc;"),
+    ("lse without the max", "lse[i] = m + std::log(z);", "lse[i] = std::log(z);"),
+    ("padding row attends", "if (i >= L) {  // padding query", "if (i > L) {  // padding query"),
+    ("non-strict mask", "scores[(long)b * n + k] > threshold", "scores[(long)b * n + k] >= threshold"),
+    ("globals kept regardless of flag", "(keep_global && g[k])", "(g[k])"),
+    ("globals not renumbered", "new_global_pos[(long)b * G + gc++] = new_index[p];",
+     "new_global_pos[(long)b * G + gc++] = p;"),
+    ("orig index not composed", "orig_in[(long)b * n + src]", "orig_in[(long)b * n + j]"),
+    ("bf16 rounding truncates", "std::nearbyint(x / ulp) * ulp", "std::trunc(x / ulp) * ulp"),
+    ("k and v projections swapped", "kv[row * D + j] = round_bf16(acc[D + j]);",
+     "kv[row * D + j] = round_bf16(acc[2 * D + j]);"),
+    ("attention output not stored as bf16", "for (auto& e : o) e = round_bf16(e);", ""),
+    ("residual dropped", "t[c] = x[src * D + c];", "t[c] = 0.0;"),
+    ("unbiased variance", "var /= (double)D;", "var /= (double)(D - 1);"),
+    ("value of the query used", "const double* vj = v + (long)nbr[t] * ld;", "const double* vj = v + (long)i * ld;"),
+]
+
+
+def build_mutant(tmp_path, old, new):
+    src = open(SRC).read()
+    assert src.count(old) >= 1, f"mutation anchor not found: {old!r}"
+    path = tmp_path / "mut.cpp"
+    path.write_text(src.replace(old, new, 1))
+    so = tmp_path / "libmut.so"
+    subprocess.run(["g++", "-std=c++17", "-O1", "-fopenmp", "-fPIC", "-shared", str(path), "-o", str(so)],
+                   check=True)
+    return str(so)
+
+
+@pytest.mark.slow
+@pytest.mark.parametrize("name,old,new", MUTANTS, ids=[m[0] for m in MUTANTS])
+def test_mutant_is_caught(tmp_path, monkeypatch, name, old, new):
+    so = build_mutant(tmp_path, old, new)
+    saved = oracle._lib
+    oracle._lib = None
+    monkeypatch.setattr(oracle, "_LIB", so)
+    try:
+        oracle.lib()
+        caught = []
+        for check in pins.ALL_CHECKS:
+            try:
+                check()
+            except AssertionError:
+                caught.append(check.__name__)
+        assert caught, f"no pin caught mutant '{name}'"
+    finally:
+        oracle._lib = saved

@@ -1,0 +1,433 @@
+"""Pins of the CPU oracle against things other than itself (no GPU).
+
+Each check pins one or more parts of the oracle against brute force on tiny
+inputs, a library routine the method reduces to, a closed form, an invariant
+or a value the paper prints.  ``test_oracle_mutants.py`` re-runs these checks
+on deliberately broken copies of the oracle to show that each plausible
+mistake is caught by at least one of them.
+"""
+import json
+import math
+import os
+from fractions import Fraction
+
+import numpy as np
+import pytest
+import torch
+
+import oracle
+import sc_inputs as si
+
+GOLDEN = os.path.join(os.path.dirname(os.path.abspath(__file__)), "golden")
+
+
+# ----------------------------------------------------------------- helpers --
+def rand_case(seed, B=2, n=24, H=3, d=8, window=None, G=None, full=False, scale=0.7):
+    rng = np.random.default_rng(seed)
+    window = int(rng.integers(0, n)) if window is None else window
+    q = rng.standard_normal((B, n, H, d)) * scale
+    k = rng.standard_normal((B, n, H, d)) * scale
+    v = rng.standard_normal((B, n, H, d))
+    vl = np.full(B, n, np.int32) if full else rng.integers(1, n + 1, B).astype(np.int32)
+    G = int(rng.integers(0, 4)) if G is None else G
+    gp = np.full((B, max(G, 1)), -1, np.int32)
+    for b in range(B):
+        g = rng.choice(vl[b], size=min(G, vl[b]), replace=False) if G else []
+        gp[b, :len(g)] = np.sort(g)
+    return q, k, v, vl, gp, window
+
+
+def allowed_matrix(n, L, r, gflags):
+    i = np.arange(n)[:, None]
+    j = np.arange(n)[None, :]
+    m = (np.abs(i - j) <= r) | gflags[:, None] | gflags[None, :]
+    return m & (i < L) & (j < L)
+
+
+def brute_force(q, k, v, vl, gp, window, alpha):
+    """Explicit n x n masked softmax attention in numpy (tiny inputs only)."""
+    B, n, H, d = q.shape
+    r = window // 2
+    out = np.zeros_like(q)
+    lse = np.full((B, H, n), -np.inf)
+    colsum = np.zeros((B, H, n))
+    for b in range(B):
+        L = int(vl[b])
+        gf = np.zeros(n, bool)
+        for p in gp[b]:
+            if 0 <= p < L:
+                gf[p] = True
+        M = allowed_matrix(n, L, r, gf)
+        for h in range(H):
+            S = alpha * q[b, :, h, :] @ k[b, :, h, :].T
+            S = np.where(M, S, -np.inf)
+            for i in range(L):
+                m = S[i].max()
+                e = np.where(M[i], np.exp(S[i] - m), 0.0)
+                z = e.sum()
+                p = e / z
+                out[b, i, h] = p @ v[b, :, h, :]
+                lse[b, h, i] = m + math.log(z)
+                colsum[b, h] += p
+    scores = np.zeros((B, n))
+    for b in range(B):
+        L = int(vl[b])
+        if L:
+            scores[b, :L] = colsum[b, :, :L].sum(0) / (H * L)
+    return out, lse, scores
+
+
+def run(q, k, v, vl, gp, window, alpha=0.35, **kw):
+    return oracle.sparse_attention(q, k, v, vl, gp, window, alpha, **kw)
+
+
+# ------------------------------------------------------------------ checks --
+def check_brute_force():
+    for seed in range(12):
+        q, k, v, vl, gp, w = rand_case(seed)
+        o, l, s = run(q, k, v, vl, gp, w)
+        bo, bl, bs = brute_force(q, k, v, vl, gp, w, 0.35)
+        np.testing.assert_allclose(o, bo, rtol=0, atol=1e-12)
+        fin = np.isfinite(bl)
+        assert np.array_equal(fin, np.isfinite(l))
+        np.testing.assert_allclose(l[fin], bl[fin], rtol=0, atol=1e-12)
+        np.testing.assert_allclose(s, bs, rtol=0, atol=1e-13)
+
+
+def _sdpa(q, k, v, alpha):
+    """Dense attention by torch's library routine, float64; [B, n, H, d] layout."""
+    Q, K, V = (torch.from_numpy(x).permute(0, 2, 1, 3) for x in (q, k, v))
+    O = torch.nn.functional.scaled_dot_product_attention(Q, K, V, scale=alpha)
+    S = alpha * Q @ K.transpose(-1, -2)
+    lse = torch.logsumexp(S, -1)
+    P = torch.softmax(S, -1)
+    n = q.shape[1]
+    scores = P.sum(2).mean(1) / n  # sum over queries, mean over heads, / L
+    return O.permute(0, 2, 1, 3).numpy(), lse.numpy(), scores.numpy()
+
+
+def check_window_covers_sequence_is_dense():
+    q, k, v, vl, gp, _ = rand_case(100, n=20, full=True, G=0)
+    for w in (40, 41, 1000):
+        o, l, s = run(q, k, v, vl, gp, w)
+        ro, rl, rs = _sdpa(q, k, v, 0.35)
+        np.testing.assert_allclose(o, ro, atol=1e-12)
+        np.testing.assert_allclose(l, rl, atol=1e-12)
+        np.testing.assert_allclose(s, rs, atol=1e-14)
+
+
+def check_all_global_is_dense():
+    q, k, v, vl, _, _ = rand_case(101, n=16, full=True)
+    gp = np.tile(np.arange(16, dtype=np.int32), (q.shape[0], 1))
+    o, l, s = run(q, k, v, vl, gp, 2)
+    ro, rl, rs = _sdpa(q, k, v, 0.35)
+    np.testing.assert_allclose(o, ro, atol=1e-12)
+    np.testing.assert_allclose(s, rs, atol=1e-14)
+
+
+def check_zero_window_no_global():
+    """r = 0 and no global token: every query attends only to itself."""
+    q, k, v, vl, gp, _ = rand_case(102, G=0)
+    gp[:] = -1
+    for w in (0, 1):
+        o, l, s = run(q, k, v, vl, gp, w)
+        B, n = q.shape[:2]
+        for b in range(B):
+            L = int(vl[b])
+            assert np.array_equal(o[b, :L], v[b, :L])           # P = 1 exactly
+            assert np.all(o[b, L:] == 0)
+            assert np.all(s[b, :L] == 1.0 / L) and np.all(s[b, L:] == 0)
+            self_logit = 0.35 * np.einsum("nhd,nhd->hn", q[b, :L], k[b, :L])
+            np.testing.assert_allclose(l[b, :, :L], self_logit, rtol=1e-14, atol=1e-15)
+            assert np.all(np.isneginf(l[b, :, L:]))
+
+
+def check_constant_values():
+    q, k, v, vl, gp, w = rand_case(103)
+    c = np.linspace(-1, 1, q.shape[-1])
+    v[:] = c
+    o, _, _ = run(q, k, v, vl, gp, w)
+    for b in range(q.shape[0]):
+        np.testing.assert_allclose(o[b, :vl[b]], np.broadcast_to(c, o[b, :vl[b]].shape), atol=1e-14)
+
+
+def check_zero_queries_rational_scores():
+    """Q = 0 makes every row uniform over its neighbour set: exact rational scores by counting."""
+    for seed in (104, 105, 106):
+        q, k, v, vl, gp, w = rand_case(seed, n=20)
+        q[:] = 0.0
+        _, _, s = run(q, k, v, vl, gp, w)
+        r = w // 2
+        for b in range(q.shape[0]):
+            L = int(vl[b])
+            g = set(int(p) for p in gp[b] if 0 <= p < L)
+            nb = [[j for j in range(L) if abs(i - j) <= r or i in g or j in g] for i in range(L)]
+            for kk in range(L):
+                exact = sum((Fraction(1, len(nb[i])) for i in range(L) if kk in nb[i]), Fraction(0)) / L
+                assert abs(s[b, kk] - float(exact)) < 1e-15
+
+
+def check_score_invariants():
+    for seed in range(200, 206):
+        q, k, v, vl, gp, w = rand_case(seed, n=40)
+        o, l, s, cs = run(q, k, v, vl, gp, w, want_colsum=True)
+        for b in range(q.shape[0]):
+            L = int(vl[b])
+            np.testing.assert_allclose(s[b].sum(), 1.0, atol=1e-13)          # sum over tokens is one
+            np.testing.assert_allclose(cs[b].sum(-1), np.full(q.shape[2], L), atol=1e-11)  # rows sum to 1
+            assert np.all(s[b, L:] == 0) and np.all(s[b, :L] > 0)
+
+
+def check_reflection_symmetry():
+    q, k, v, vl, gp, w = rand_case(300, n=30, full=True, G=2)
+    o, l, s = run(q, k, v, vl, gp, w)
+    n = q.shape[1]
+    gpr = np.where(gp >= 0, n - 1 - gp, -1)
+    gpr = np.sort(np.where(gpr < 0, 10 ** 6, gpr), 1)
+    gpr = np.where(gpr == 10 ** 6, -1, gpr).astype(np.int32)
+    o2, l2, s2 = run(q[:, ::-1], k[:, ::-1], v[:, ::-1], vl, gpr, w)
+    np.testing.assert_allclose(o2[:, ::-1], o, atol=1e-13)
+    np.testing.assert_allclose(s2[:, ::-1], s, atol=1e-14)
+
+
+def check_head_permutation():
+    q, k, v, vl, gp, w = rand_case(301, H=4)
+    perm = [2, 0, 3, 1]
+    o, l, s = run(q, k, v, vl, gp, w)
+    o2, l2, s2 = run(q[:, :, perm], k[:, :, perm], v[:, :, perm], vl, gp, w)
+    np.testing.assert_allclose(o2, o[:, :, perm], atol=0)
+    np.testing.assert_allclose(s2, s, atol=1e-15)
+
+
+def check_sec55_example_structure():
+    """Paper's worked example (Sec. 5.5): ten tokens, specials 1st and 8th, window 3.
+
+    With Q = 0 the softmax is uniform over the allowed keys and V = identity
+    makes the output row i equal P[i, :], so the oracle's support is read off.
+    """
+    lines = [ln for ln in open(os.path.join(GOLDEN, "sec55_example_mask.txt")) if not ln.startswith("#")]
+    glob = [int(x) for x in lines[0].split()[1:]]
+    window = int(lines[1].split()[1])
+    M = np.array([[c == "1" for c in ln.strip()] for ln in lines[2:12]])
+    n = 10
+    q = np.zeros((1, n, 1, n))
+    k = np.random.default_rng(0).standard_normal((1, n, 1, n))
+    v = np.eye(n).reshape(1, n, 1, n)
+    o, _, _ = run(q, k, v, np.array([n], np.int32), np.array([glob], np.int32), window)
+    P = o[0, :, 0, :]
+    assert np.array_equal(P > 0, M)
+    np.testing.assert_allclose(P.sum(1), 1.0, atol=1e-15)
+    np.testing.assert_allclose(P[M], np.repeat(1.0 / M.sum(1), M.sum(1)), atol=1e-15)
+
+
+def check_padding_is_invisible():
+    """Padding tokens neither attend nor are attended: changing them changes nothing."""
+    q, k, v, vl, gp, w = rand_case(302, n=32)
+    vl[:] = [20, 9]
+    o, l, s = run(q, k, v, vl, gp, w)
+    q2, k2, v2 = q.copy(), k.copy(), v.copy()
+    for b, L in enumerate(vl):
+        q2[b, L:] = 7.0
+        k2[b, L:] = -3.0
+        v2[b, L:] = 11.0
+    o2, l2, s2 = run(q2, k2, v2, vl, gp, w)
+    assert np.array_equal(o, o2) and np.array_equal(s, s2)
+    # and a shorter padded copy gives the same valid outputs
+    o3, _, s3 = run(q[:1, :20], k[:1, :20], v[:1, :20], vl[:1], gp[:1], w)
+    np.testing.assert_allclose(o3[0], o[0, :20], atol=0)
+    np.testing.assert_allclose(s3[0], s[0, :20], atol=0)
+
+
+def brute_prune(s32, vl, gp, theta, keep_global, orig_in=None):
+    B, n = s32.shape
+    out = []
+    for b in range(B):
+        L = int(vl[b])
+        g = [int(p) for p in gp[b] if 0 <= p < L]
+        kept = [kk for kk in range(L) if s32[b, kk] > np.float32(theta) or (keep_global and kk in g)]
+        ng = [kept.index(p) for p in g if p in kept]
+        orig = [(orig_in[b, kk] if orig_in is not None else kk) for kk in kept]
+        out.append((kept, ng, orig))
+    return out
+
+
+def check_prune_brute_force():
+    rng = np.random.default_rng(7)
+    for trial in range(20):
+        B, n, G = 3, 50, 4
+        s = rng.random((B, n)).astype(np.float32) * 0.05
+        vl = rng.integers(0, n + 1, B).astype(np.int32)
+        gp = np.full((B, G), -1, np.int32)
+        for b in range(B):
+            g = rng.choice(max(vl[b], 1), size=min(G, vl[b]), replace=False) if vl[b] else []
+            gp[b, :len(g)] = np.sort(g)
+        theta = float(rng.choice([-1.0, 0.0, 0.01, 0.025, 0.049, float(s[0, 3])]))
+        kg = int(trial % 2)
+        orig_in = rng.integers(0, 1000, (B, n)).astype(np.int32) if trial % 3 == 0 else None
+        ki, nl, ngp, oo = oracle.ltp_prune(s, vl, gp, theta, kg, orig_in)
+        ref = brute_prune(s, vl, gp, theta, kg, orig_in)
+        for b, (kept, ng, orig) in enumerate(ref):
+            assert nl[b] == len(kept)
+            assert list(ki[b, :nl[b]]) == kept and np.all(ki[b, nl[b]:] == -1)
+            assert list(ngp[b, :len(ng)]) == ng and np.all(ngp[b, len(ng):] == -1)
+            assert list(oo[b, :nl[b]]) == orig and np.all(oo[b, nl[b]:] == -1)
+
+
+def check_prune_invariants():
+    q, k, v, vl, gp, w = rand_case(400, n=64, B=3)
+    _, _, s = run(q, k, v, vl, gp, w)
+    s32 = s.astype(np.float32)
+    prev = None
+    for theta in (-1.0, 0.0, 0.005, 0.01, 0.02, 0.05, 0.2):
+        ki, nl, ngp, _ = oracle.ltp_prune(s32, vl, gp, theta, 1)
+        for b in range(3):
+            kept = set(ki[b, :nl[b]].tolist())
+            g = set(int(p) for p in gp[b] if 0 <= p < vl[b])
+            assert g <= kept                                   # globals always kept
+            assert list(ki[b, :nl[b]]) == sorted(kept)         # stable order
+            if theta > 0:
+                assert len(kept - g) < 1.0 / theta             # scores sum to one
+            if theta < 0:
+                assert nl[b] == vl[b]                          # keeps every valid token
+            if prev is not None:
+                assert kept <= prev[b]                         # nested as theta grows
+        prev = [set(ki[b, :nl[b]].tolist()) for b in range(3)]
+
+
+def check_mask_rule_golden():
+    cases = json.load(open(os.path.join(GOLDEN, "mask_rule.json")))["cases"]
+    for c in cases:
+        s = np.array([[c["score"], 1.0]], np.float32)
+        ki, nl, _, _ = oracle.ltp_prune(s, np.array([2], np.int32), np.full((1, 1), -1, np.int32),
+                                        c["threshold"], 1)
+        assert int(0 in ki[0, :nl[0]]) == c["mask"]
+
+
+def check_gather_rows():
+    rng = np.random.default_rng(9)
+    src = rng.integers(0, 2 ** 16, (2, 10, 7), dtype=np.uint16)
+    ki = np.array([[1, 4, 9] + [-1] * 7, [0, 2] + [-1] * 8], np.int32)
+    nl = np.array([3, 2], np.int32)
+    dst = oracle.gather_rows(src, ki, nl)
+    assert np.array_equal(dst[0, :3], src[0, [1, 4, 9]]) and np.array_equal(dst[1, :2], src[1, [0, 2]])
+    assert np.all(dst[0, 3:] == 0)
+
+
+def _torch_bf16(x):
+    return torch.from_numpy(np.asarray(x, np.float64)).to(torch.float32).to(torch.bfloat16).to(torch.float64).numpy()
+
+
+def check_bf16_rounding():
+    rng = np.random.default_rng(11)
+    x = (rng.standard_normal(5000) * np.exp(rng.uniform(-20, 20, 5000))).astype(np.float32).astype(np.float64)
+    ours = np.array([oracle.round_bf16(t) for t in x])
+    assert np.array_equal(ours, _torch_bf16(x))
+    # ties go to even: 1 + 2^-8 is halfway between 1 and 1 + 2^-7
+    assert oracle.round_bf16(1 + 2 ** -8) == 1.0
+    assert oracle.round_bf16(1 + 3 * 2 ** -8) == 1 + 2 ** -6
+    assert oracle.round_bf16(-(1 + 2 ** -8)) == -1.0
+
+
+def _ref_layer(x, wqkv, wo, vl, gp, H, alpha, theta, eps):
+    """Library composition for dense windows: numpy matmul, torch SDPA, torch layer_norm, torch bf16."""
+    B, n, D = x.shape
+    d = D // H
+    qkv = _torch_bf16(x @ wqkv)
+    q, k, v = (qkv[..., i * D:(i + 1) * D].reshape(B, n, H, d) for i in range(3))
+    y = np.zeros_like(x)
+    kept_all, nl = [], []
+    for b in range(B):
+        L = int(vl[b])
+        Q, K, V = (torch.from_numpy(t[b:b + 1, :L]).permute(0, 2, 1, 3) for t in (q, k, v))
+        O = torch.nn.functional.scaled_dot_product_attention(Q, K, V, scale=alpha)
+        P = torch.softmax(alpha * Q @ K.transpose(-1, -2), -1)
+        s = (P.sum(2).mean(1)[0] / L).numpy().astype(np.float32)
+        g = [int(p) for p in gp[b] if 0 <= p < L]
+        kept = [j for j in range(L) if s[j] > np.float32(theta) or j in g]
+        O = _torch_bf16(O.permute(0, 2, 1, 3).reshape(L, D).numpy())
+        t = torch.from_numpy(x[b, :L] + O @ wo)
+        yy = _torch_bf16(torch.nn.functional.layer_norm(t, (D,), eps=eps).numpy())
+        y[b, :len(kept)] = yy[kept]
+        kept_all.append(kept)
+        nl.append(len(kept))
+    return y, kept_all, nl
+
+
+def stack_case(seed=500, B=2, n=24, H=2, d=8):
+    rng = np.random.default_rng(seed)
+    D = H * d
+    bf = _torch_bf16
+    x = bf(rng.standard_normal((B, n, D)))
+    wqkv = bf(rng.standard_normal((D, 3 * D)) * 0.3)
+    wo = bf(rng.standard_normal((D, D)) * 0.3)
+    vl = np.array([n, n - 7][:B], np.int32)
+    gp = np.array([[0], [3]][:B], np.int32)
+    return x, wqkv, wo, vl, gp, H
+
+
+def check_encoder_layer_against_libraries():
+    x, wqkv, wo, vl, gp, H = stack_case()
+    n = x.shape[1]
+    # scores here are about 1/L (~0.04-0.06): the threshold prunes some, keeps some
+    for theta in (-1.0, 0.045):
+        y, ki, nl, ngp, sc = oracle.encoder_layer(x, wqkv, wo, vl, gp, H, 2 * n, 0.6, theta)
+        ry, rkept, rnl = _ref_layer(x, wqkv, wo, vl, gp, H, 0.6, theta, 1e-5)
+        assert list(nl) == rnl
+        for b in range(x.shape[0]):
+            assert list(ki[b, :nl[b]]) == rkept[b]
+        diff = np.abs(y - ry)
+        ulp = np.maximum(np.abs(ry), 1e-30) * 2.0 ** -7
+        assert np.all(diff <= ulp)                    # at most one bf16 step apart ...
+        assert np.mean(diff == 0) > 0.995             # ... and nearly all identical
+
+
+def check_layernorm_statistics():
+    x, wqkv, wo, vl, gp, H = stack_case(501)
+    y, ki, nl, _, _ = oracle.encoder_layer(x, wqkv, wo, vl, gp, H, 6, 0.6, -1.0)
+    for b in range(x.shape[0]):
+        rows = y[b, :nl[b]]
+        assert np.all(np.abs(rows.mean(1)) < 2e-2)
+        assert np.all(np.abs(rows.var(1) - 1.0) < 3e-2)
+
+
+def check_stack_composition():
+    """Stack = layers applied in turn; theta = -1 keeps everything (identity orig_idx)."""
+    x, wqkv, wo, vl, gp, H = stack_case(502)
+    n = x.shape[1]
+    th = [0.0, 0.05, 0.06]
+    w1 = [wqkv, wqkv[:, ::-1].copy(), wqkv * 0.5]
+    w2 = [wo, wo.T.copy(), wo]
+    y, fl, oi, kpl = oracle.encoder_stack(x, w1, w2, vl, gp, H, 6, 0.6, th)
+    cur, cl, cg = x, vl, gp
+    orig = np.where(np.arange(n)[None, :] < vl[:, None], np.arange(n)[None, :], -1)
+    for l in range(3):
+        cur, ki, cl, cg, _ = oracle.encoder_layer(cur, w1[l], w2[l], cl, cg, H, 6, 0.6, th[l])
+        orig = np.where(ki >= 0, np.take_along_axis(orig, np.maximum(ki, 0), 1), -1)
+        assert list(kpl[l]) == list(cl)
+    assert np.array_equal(y, cur) and list(fl) == list(cl) and np.array_equal(oi, orig)
+    y0, fl0, oi0, _ = oracle.encoder_stack(x, w1, w2, vl, gp, H, 6, 0.6, [-1.0] * 3)
+    assert list(fl0) == list(vl)
+    for b in range(2):
+        assert list(oi0[b, :vl[b]]) == list(range(vl[b]))
+
+
+def check_paper_threshold_schedule():
+    g = json.load(open(os.path.join(GOLDEN, "paper_threshold_schedule.json")))
+    sched = si.paper_threshold_schedule(g["final_threshold"], g["n_layers"])
+    for layer, val in g["printed"].items():
+        assert abs(sched[int(layer) - 1] - val) < 1e-15
+
+
+ATTENTION_CHECKS = [check_brute_force, check_window_covers_sequence_is_dense, check_all_global_is_dense,
+                    check_zero_window_no_global, check_constant_values, check_zero_queries_rational_scores,
+                    check_score_invariants, check_reflection_symmetry, check_head_permutation,
+                    check_sec55_example_structure, check_padding_is_invisible]
+PRUNE_CHECKS = [check_prune_brute_force, check_prune_invariants, check_mask_rule_golden, check_gather_rows]
+STACK_CHECKS = [check_bf16_rounding, check_encoder_layer_against_libraries, check_layernorm_statistics,
+                check_stack_composition]
+ALL_CHECKS = ATTENTION_CHECKS + PRUNE_CHECKS + STACK_CHECKS + [check_paper_threshold_schedule]
+
+
+@pytest.mark.parametrize("check", ALL_CHECKS, ids=lambda f: f.__name__[6:])
+def test_pin(check):
+    check()
