@@ -1,0 +1,211 @@
+/*
+ * sc.h - C ABI of the SparseCoder hot path on MI355X (gfx950).
+ *
+ * SparseCoder (arXiv 2310.07109) prunes tokens layer by layer inside an encoder
+ * whose self-attention is a sliding window plus global tokens.  Per layer the
+ * library computes, on one GPU:
+ *
+ *   sc_window_attention   banded Q.K^T, masked softmax and P.V for the sliding
+ *                         window (Sec. 4.2.1, Fig. 4) plus the global tokens'
+ *                         dense rows and columns (Sec. 3.1 "Global attention",
+ *                         Fig. 3b-c; Sec. 5.5), and the per-query partial sums
+ *                         of the attention probabilities each key receives;
+ *   sc_ltp_score          the importance score of every token: probabilities
+ *                         accumulated down its column after the row softmax
+ *                         (Sec. 1, Fig. 1 caption; Sec. 3.2), i.e. the sum over
+ *                         the band's sub-diagonal plus the global strips
+ *                         (Sec. 5.5), averaged over heads and valid queries;
+ *   sc_ltp_prune_compact  the binarised mask (keep iff score > threshold,
+ *                         Sec. 4.2.2 step 2) and hard pruning: surviving tokens
+ *                         are compacted into a shorter sequence (Sec. 4.2.2
+ *                         step 3) for the next layer;
+ *   sc_encoder_attn_stack the attention-only encoder stack (QKV projection,
+ *                         the three steps above, output projection, residual
+ *                         and LayerNorm) over several layers, each layer on the
+ *                         previous layer's surviving tokens (Sec. 4.2, Fig. 5).
+ *
+ * Conventions shared by every entry point
+ *   - Tensor pointers are DEVICE pointers owned by the caller; the library never
+ *     allocates device memory.  Scratch memory comes from `workspace`, whose
+ *     size is returned by the matching *_workspace_size() call (may be 0, in
+ *     which case workspace may be NULL).
+ *   - `stream` is a hipStream_t passed as void* (NULL = the default stream).
+ *     All work is enqueued asynchronously on it; nothing synchronises.
+ *   - Arguments are validated on the host before anything is enqueued.  On any
+ *     error nothing is enqueued and a negative sc_status is returned.
+ *     Device-resident arguments (valid_len, global_pos) cannot be checked on
+ *     the host: values outside their documented range are clamped or ignored
+ *     by the kernels (memory-safe), with unspecified numerical results.
+ *   - Activations are token-major: [B, n, H, d] with d contiguous, so one token
+ *     of one sequence is one contiguous row of H*d elements.
+ *   - Sequence b holds valid_len[b] real tokens followed by padding.  Padding
+ *     tokens are neither queries nor keys; their outputs are zero.
+ */
+#ifndef SC_H_
+#define SC_H_
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef int32_t sc_status;
+#define SC_OK 0
+#define SC_EINVAL (-1)        /* invalid argument (null pointer, bad size, aliasing) */
+#define SC_EUNSUPPORTED (-2)  /* valid but not implemented (e.g. head dim != 64)     */
+#define SC_EWORKSPACE (-3)    /* workspace missing or smaller than required           */
+#define SC_EHIP (-4)          /* a HIP runtime call failed (launch error)              */
+
+#define SC_F32 0   /* float32 storage and arithmetic                               */
+#define SC_BF16 1  /* bfloat16 storage, float32 accumulation                        */
+
+#define SC_SCORE_FROM_PARTIALS 0   /* sc_ltp_score reads sc_window_attention's partials */
+#define SC_SCORE_FROM_BAND_PROBS 1 /* sc_ltp_score reads the band-stored probabilities   */
+
+/*
+ * Geometry of one attention layer over a padded batch.
+ *   B, n        batch size and padded length; B >= 1, n >= 1.
+ *   H, d        heads and head dimension; H >= 1, d must be 64.
+ *   window      full window width w >= 0: query i attends to key j when
+ *               |i - j| <= floor(w / 2) (both valid).  The paper states the
+ *               window both as i-w..i+w (Sec. 4.2.1) and as a band stored as
+ *               n x (2w - 1) (Sec. 5.5); this ABI takes w as the full width.
+ *   G           global-token slots per sequence, 0 <= G <= n.
+ *   global_pos  device int32 [B, G]: positions of the global tokens of each
+ *               sequence, ascending and distinct, each < valid_len[b];
+ *               -1 marks an unused slot.  May be NULL when G == 0.
+ *   valid_len   device int32 [B]: 0 <= valid_len[b] <= n.
+ *   softmax_scale  alpha applied to Q.K^T before the softmax (finite).
+ *   dtype       SC_F32 or SC_BF16 for q, k, v and outputs.
+ */
+typedef struct sc_attn_desc {
+  int32_t B, n, H, d;
+  int32_t window;
+  int32_t G;
+  const int32_t *global_pos;
+  const int32_t *valid_len;
+  float softmax_scale;
+  int32_t dtype;
+} sc_attn_desc;
+
+/* Human-readable text for a status code (static storage). */
+const char *sc_status_str(sc_status s);
+
+/* Bytes of the score partials written by sc_window_attention and read by
+ * sc_ltp_score(SC_SCORE_FROM_PARTIALS); 0 on an invalid descriptor.  The layout
+ * is private to the library: per (sequence, head, 64-query block) sums of the
+ * probabilities that block's queries give each key of its band and each
+ * global key, plus per (sequence, head) sums over the global queries. */
+size_t sc_score_partials_size(const sc_attn_desc *desc);
+
+/* Bytes of the band-stored probabilities (paper layout, Sec. 5.5 / Fig. 3d),
+ * three float32 arrays back to back, r = min(floor(w/2), n - 1):
+ *   band [B, H, n, 2r+1]: entry (i, j) = P[i][i - r + j] when query i and key
+ *        i - r + j are valid and neither is global, else 0 (the local part);
+ *   gcol [B, H, n, G]: P[i][global_pos[b,s]] for valid non-global queries i and
+ *        used slots s, else 0 (the global columns);
+ *   grow [B, H, G, n]: P[global_pos[b,s]][k] for used slots s and valid keys k,
+ *        else 0 (the global rows).
+ * A token's score is its band sub-diagonal plus its global column and its
+ * entries of the global rows.  0 on an invalid descriptor. */
+size_t sc_band_probs_size(const sc_attn_desc *desc);
+
+size_t sc_window_attention_workspace_size(const sc_attn_desc *desc);
+
+/*
+ * Sliding-window + global sparse attention of one layer (Sec. 4.2.1, Sec. 3.1,
+ * Sec. 5.5): for every valid query i of sequence b and head h,
+ *   N(i) = { j < L : |i - j| <= r  or  i global  or  j global },  r = floor(w/2)
+ *   out[b,i,h,:] = sum_{j in N(i)} softmax_j(alpha * q_i . k_j) * v_j
+ *   lse[b,h,i]   = log sum_{j in N(i)} exp(alpha * q_i . k_j)   (natural log)
+ * Padding queries get out = 0 and lse = -inf.
+ *   q, k, v     [B, n, H, d] in desc->dtype (read only).
+ *   out         [B, n, H, d] in desc->dtype; must not overlap q, k or v.
+ *   lse         float32 [B, H, n], or NULL.
+ *   score_partials  float32 buffer of sc_score_partials_size() bytes, or NULL
+ *               (skips the second pass that sums exact probabilities).
+ *   band_probs  float32 buffer of sc_band_probs_size() bytes, or NULL; when set
+ *               every probability is also stored in the paper's band layout.
+ * Softmax is computed in float32 (exp2 of log2-scaled logits, running max);
+ * in bf16 mode P is rounded to bf16 for the P.V product only.
+ */
+sc_status sc_window_attention(const sc_attn_desc *desc, const void *q, const void *k, const void *v, void *out,
+                              float *lse, float *score_partials, float *band_probs, void *workspace,
+                              size_t ws_bytes, void *stream);
+
+size_t sc_ltp_score_workspace_size(const sc_attn_desc *desc, int32_t mode);
+
+/*
+ * Importance score of every token (Sec. 1 Fig. 1; Sec. 3.2; Sec. 5.5):
+ *   scores[b,k] = 1/(H * L_b) * sum_h sum_{i < L_b} P_h[i][k]   for k < L_b,
+ *   scores[b,k] = 0                                              for k >= L_b,
+ * so the scores of one sequence sum to one.  Deterministic: fixed-order sums,
+ * no atomics.
+ *   mode  SC_SCORE_FROM_PARTIALS: src = score_partials of sc_window_attention
+ *         with the same desc; SC_SCORE_FROM_BAND_PROBS: src = band_probs.
+ *   scores  float32 [B, n].
+ */
+sc_status sc_ltp_score(const sc_attn_desc *desc, int32_t mode, const float *src, float *scores, void *workspace,
+                       size_t ws_bytes, void *stream);
+
+size_t sc_ltp_prune_compact_workspace_size(const sc_attn_desc *desc);
+
+/*
+ * Binarised mask and hard pruning of one layer (Sec. 4.2.2 steps 2-3):
+ *   keep(b,k) = k < L_b and (scores[b,k] > threshold  or  (keep_global and k global))
+ * compared in float32, strictly.  Surviving tokens keep their order.
+ *   scores          float32 [B, n] (e.g. from sc_ltp_score).
+ *   n_tensors       0..4 tensors to compact, each [B, n, row_bytes[t]] bytes.
+ *   src, dst        HOST arrays of n_tensors device pointers; dst row j of
+ *                   sequence b = src row keep_idx[b,j] for j < new_len[b]; dst
+ *                   rows at or beyond new_len are left untouched.  src[t] and
+ *                   dst[t] must not overlap.
+ *   row_bytes       HOST array of n_tensors row sizes in bytes (> 0).
+ *   keep_idx        int32 [B, n]: input position of the j-th survivor, -1 beyond.
+ *   new_len         int32 [B]: survivors per sequence.
+ *   new_global_pos  int32 [B, G]: surviving global tokens renumbered into the
+ *                   compacted sequence, ascending, -1 padded; may be NULL.
+ *   orig_idx_in     int32 [B, n] or NULL (identity): original positions of the
+ *                   layer's input tokens.
+ *   orig_idx_out    int32 [B, n] or NULL: orig_idx_in[keep_idx], -1 beyond
+ *                   new_len.  Must not overlap orig_idx_in.
+ */
+sc_status sc_ltp_prune_compact(const sc_attn_desc *desc, const float *scores, float threshold, int32_t keep_global,
+                               int32_t n_tensors, const void *const *src, void *const *dst, const int64_t *row_bytes,
+                               int32_t *keep_idx, int32_t *new_len, int32_t *new_global_pos,
+                               const int32_t *orig_idx_in, int32_t *orig_idx_out, void *workspace, size_t ws_bytes,
+                               void *stream);
+
+size_t sc_encoder_attn_stack_workspace_size(const sc_attn_desc *desc, int32_t n_layers);
+
+/*
+ * Attention-only encoder stack of n_layers RoBERTa-shaped layers without FFN
+ * (Sec. 4.2, Fig. 5; pruning after each layer, Sec. 4.2.2):
+ *   qkv = bf16(x . Wqkv[l])                 Wqkv [D, 3D] row-major, columns q|k|v,
+ *                                            each head-major (head h = cols h*d..)
+ *   O   = bf16(sc_window_attention(q,k,v))   with the layer's current lengths
+ *   keep, compaction as sc_ltp_prune_compact with thresholds[l]
+ *   x   = bf16(LayerNorm(x + O . Wo[l]))     on the survivors; Wo [D, D];
+ *                                            LayerNorm gamma 1, beta 0, eps ln_eps
+ * desc gives the layer-0 geometry (dtype must be SC_BF16, D = H*d); lengths and
+ * global positions shrink on the device from layer to layer, with no host
+ * synchronisation.
+ *   x_in            bf16 [B, n, D]; x_out bf16 [B, n, D] (survivors first).
+ *   Wqkv, Wo        HOST arrays of n_layers device pointers (bf16).
+ *   thresholds      HOST float [n_layers].
+ *   final_len       int32 [B]; orig_idx int32 [B, n] (input position of each
+ *                   surviving row, -1 beyond final_len); kept_per_layer int32
+ *                   [n_layers, B] (sequence length after each layer's pruning).
+ */
+sc_status sc_encoder_attn_stack(const sc_attn_desc *desc, int32_t n_layers, const void *x_in,
+                                const void *const *Wqkv, const void *const *Wo, const float *thresholds,
+                                int32_t keep_global, float ln_eps, void *x_out, int32_t *final_len,
+                                int32_t *orig_idx, int32_t *kept_per_layer, void *workspace, size_t ws_bytes,
+                                void *stream);
+
+#ifdef __cplusplus
+}
+#endif
+#endif /* SC_H_ */

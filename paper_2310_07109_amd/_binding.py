@@ -1,0 +1,217 @@
+"""ctypes binding of libsc.so (argument marshalling only)."""
+from __future__ import annotations
+
+import ctypes
+import os
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+_LIB_PATH = os.path.join(_HERE, "libsc.so")
+
+SC_OK, SC_EINVAL, SC_EUNSUPPORTED, SC_EWORKSPACE, SC_EHIP = 0, -1, -2, -3, -4
+SC_F32, SC_BF16 = 0, 1
+SC_SCORE_FROM_PARTIALS, SC_SCORE_FROM_BAND_PROBS = 0, 1
+
+_lib = None
+
+
+class ScError(RuntimeError):
+    def __init__(self, status: int, where: str):
+        self.status = status
+        super().__init__(f"{where}: {sc_status_str(status)} ({status})")
+
+
+class _Desc(ctypes.Structure):
+    _fields_ = [("B", ctypes.c_int32), ("n", ctypes.c_int32), ("H", ctypes.c_int32), ("d", ctypes.c_int32),
+                ("window", ctypes.c_int32), ("G", ctypes.c_int32), ("global_pos", ctypes.c_void_p),
+                ("valid_len", ctypes.c_void_p), ("softmax_scale", ctypes.c_float), ("dtype", ctypes.c_int32)]
+
+
+def lib_path() -> str:
+    return _LIB_PATH
+
+
+def load():
+    """Load libsc.so; raises if it has not been built (no fallback path exists)."""
+    global _lib
+    if _lib is not None:
+        return _lib
+    if not os.path.exists(_LIB_PATH):
+        raise RuntimeError(f"{_LIB_PATH} is missing: build it with `python -m paper_2310_07109_amd.build`")
+    L = ctypes.CDLL(_LIB_PATH)
+    vp, sz, i32, f32 = ctypes.c_void_p, ctypes.c_size_t, ctypes.c_int32, ctypes.c_float
+    dp = ctypes.POINTER(_Desc)
+    sig = {
+        "sc_status_str": (ctypes.c_char_p, [i32]),
+        "sc_score_partials_size": (sz, [dp]),
+        "sc_band_probs_size": (sz, [dp]),
+        "sc_window_attention_workspace_size": (sz, [dp]),
+        "sc_window_attention": (i32, [dp, vp, vp, vp, vp, vp, vp, vp, vp, sz, vp]),
+        "sc_ltp_score_workspace_size": (sz, [dp, i32]),
+        "sc_ltp_score": (i32, [dp, i32, vp, vp, vp, sz, vp]),
+        "sc_ltp_prune_compact_workspace_size": (sz, [dp]),
+        "sc_ltp_prune_compact": (i32, [dp, vp, f32, i32, i32, vp, vp, vp, vp, vp, vp, vp, vp, vp, sz, vp]),
+        "sc_encoder_attn_stack_workspace_size": (sz, [dp, i32]),
+        "sc_encoder_attn_stack": (i32, [dp, i32, vp, vp, vp, vp, i32, f32, vp, vp, vp, vp, vp, sz, vp]),
+    }
+    for name, (res, args) in sig.items():
+        f = getattr(L, name)
+        f.restype = res
+        f.argtypes = args
+    _lib = L
+    return L
+
+
+def sc_status_str(status: int) -> str:
+    return load().sc_status_str(int(status)).decode()
+
+
+def _check(status: int, where: str):
+    if status != SC_OK:
+        raise ScError(status, where)
+
+
+def _ptr(t):
+    return None if t is None else ctypes.c_void_p(t.data_ptr())
+
+
+def _stream(stream):
+    import torch
+    s = torch.cuda.current_stream() if stream is None else stream
+    return ctypes.c_void_p(s.cuda_stream)
+
+
+class Desc:
+    """Geometry of one attention layer (mirrors sc_attn_desc).
+
+    valid_len: int32 device tensor [B]; global_pos: int32 device tensor [B, G] or None.
+    """
+
+    def __init__(self, B, n, H, window, valid_len, global_pos=None, softmax_scale=0.125, dtype=SC_BF16, d=64):
+        self.B, self.n, self.H, self.d, self.window = int(B), int(n), int(H), int(d), int(window)
+        self.valid_len = valid_len
+        self.global_pos = global_pos
+        self.G = 0 if global_pos is None else int(global_pos.shape[1])
+        self.softmax_scale = float(softmax_scale)
+        self.dtype = int(dtype)
+
+    def c(self) -> _Desc:
+        return _Desc(self.B, self.n, self.H, self.d, self.window, self.G,
+                     None if self.global_pos is None else self.global_pos.data_ptr(),
+                     None if self.valid_len is None else self.valid_len.data_ptr(), self.softmax_scale, self.dtype)
+
+    def torch_dtype(self):
+        import torch
+        return torch.bfloat16 if self.dtype == SC_BF16 else torch.float32
+
+
+def _ws(nbytes, device):
+    import torch
+    return torch.empty(max(int(nbytes), 1), dtype=torch.uint8, device=device)
+
+
+def sc_score_partials_size(desc: Desc) -> int:
+    return load().sc_score_partials_size(ctypes.byref(desc.c()))
+
+
+def sc_band_probs_size(desc: Desc) -> int:
+    return load().sc_band_probs_size(ctypes.byref(desc.c()))
+
+
+def sc_window_attention_workspace_size(desc: Desc) -> int:
+    return load().sc_window_attention_workspace_size(ctypes.byref(desc.c()))
+
+
+def sc_window_attention(desc: Desc, q, k, v, out=None, lse=True, score_partials=True, band_probs=False,
+                        stream=None):
+    """Returns (out, lse, score_partials, band_probs); absent outputs are None."""
+    import torch
+    L = load()
+    cd = desc.c()
+    dev = q.device
+    out = torch.empty_like(q) if out is None else out
+    lse_t = torch.empty((desc.B, desc.H, desc.n), dtype=torch.float32, device=dev) if lse else None
+    sp = torch.empty(L.sc_score_partials_size(ctypes.byref(cd)) // 4, dtype=torch.float32, device=dev) \
+        if score_partials else None
+    bp = torch.empty(L.sc_band_probs_size(ctypes.byref(cd)) // 4, dtype=torch.float32, device=dev) \
+        if band_probs else None
+    wsb = L.sc_window_attention_workspace_size(ctypes.byref(cd))
+    ws = _ws(wsb, dev)
+    _check(L.sc_window_attention(ctypes.byref(cd), _ptr(q), _ptr(k), _ptr(v), _ptr(out), _ptr(lse_t), _ptr(sp),
+                                 _ptr(bp), _ptr(ws), wsb, _stream(stream)), "sc_window_attention")
+    return out, lse_t, sp, bp
+
+
+def sc_ltp_score_workspace_size(desc: Desc, mode: int = SC_SCORE_FROM_PARTIALS) -> int:
+    return load().sc_ltp_score_workspace_size(ctypes.byref(desc.c()), mode)
+
+
+def sc_ltp_score(desc: Desc, src, mode: int = SC_SCORE_FROM_PARTIALS, scores=None, stream=None):
+    import torch
+    L = load()
+    cd = desc.c()
+    scores = torch.empty((desc.B, desc.n), dtype=torch.float32, device=src.device) if scores is None else scores
+    wsb = L.sc_ltp_score_workspace_size(ctypes.byref(cd), mode)
+    ws = _ws(wsb, src.device)
+    _check(L.sc_ltp_score(ctypes.byref(cd), mode, _ptr(src), _ptr(scores), _ptr(ws), wsb, _stream(stream)),
+           "sc_ltp_score")
+    return scores
+
+
+def sc_ltp_prune_compact_workspace_size(desc: Desc) -> int:
+    return load().sc_ltp_prune_compact_workspace_size(ctypes.byref(desc.c()))
+
+
+def sc_ltp_prune_compact(desc: Desc, scores, threshold, keep_global=True, tensors=(), dsts=None, orig_idx_in=None,
+                         want_orig=True, stream=None):
+    """Returns (keep_idx, new_len, new_global_pos, orig_idx_out, dsts)."""
+    import torch
+    L = load()
+    cd = desc.c()
+    dev = scores.device
+    B, n, G = desc.B, desc.n, desc.G
+    keep_idx = torch.empty((B, n), dtype=torch.int32, device=dev)
+    new_len = torch.empty((B,), dtype=torch.int32, device=dev)
+    ngp = torch.empty((B, G), dtype=torch.int32, device=dev) if G > 0 else None
+    orig_out = torch.empty((B, n), dtype=torch.int32, device=dev) if want_orig else None
+    tensors = list(tensors)
+    if dsts is None:
+        dsts = [torch.empty_like(t) for t in tensors]
+    nt = len(tensors)
+    src_arr = (ctypes.c_void_p * max(nt, 1))(*[t.data_ptr() for t in tensors])
+    dst_arr = (ctypes.c_void_p * max(nt, 1))(*[t.data_ptr() for t in dsts])
+    rb_arr = (ctypes.c_int64 * max(nt, 1))(*[t.numel() * t.element_size() // (B * n) for t in tensors])
+    wsb = L.sc_ltp_prune_compact_workspace_size(ctypes.byref(cd))
+    ws = _ws(wsb, dev)
+    _check(L.sc_ltp_prune_compact(ctypes.byref(cd), _ptr(scores), ctypes.c_float(threshold), int(bool(keep_global)),
+                                  nt, src_arr, dst_arr, rb_arr, _ptr(keep_idx), _ptr(new_len), _ptr(ngp),
+                                  _ptr(orig_idx_in), _ptr(orig_out), _ptr(ws), wsb, _stream(stream)),
+           "sc_ltp_prune_compact")
+    return keep_idx, new_len, ngp, orig_out, dsts
+
+
+def sc_encoder_attn_stack_workspace_size(desc: Desc, n_layers: int) -> int:
+    return load().sc_encoder_attn_stack_workspace_size(ctypes.byref(desc.c()), int(n_layers))
+
+
+def sc_encoder_attn_stack(desc: Desc, x_in, wqkv, wo, thresholds, keep_global=True, ln_eps=1e-5, x_out=None,
+                          workspace=None, stream=None):
+    """Returns (x_out, final_len, orig_idx, kept_per_layer)."""
+    import torch
+    L = load()
+    cd = desc.c()
+    dev = x_in.device
+    nl = len(wqkv)
+    B, n = desc.B, desc.n
+    x_out = torch.empty_like(x_in) if x_out is None else x_out
+    final_len = torch.empty((B,), dtype=torch.int32, device=dev)
+    orig = torch.empty((B, n), dtype=torch.int32, device=dev)
+    kpl = torch.empty((nl, B), dtype=torch.int32, device=dev)
+    wq = (ctypes.c_void_p * nl)(*[w.data_ptr() for w in wqkv])
+    wo_ = (ctypes.c_void_p * nl)(*[w.data_ptr() for w in wo])
+    th = (ctypes.c_float * nl)(*[float(t) for t in thresholds])
+    wsb = L.sc_encoder_attn_stack_workspace_size(ctypes.byref(cd), nl)
+    ws = _ws(wsb, dev) if workspace is None else workspace
+    _check(L.sc_encoder_attn_stack(ctypes.byref(cd), nl, _ptr(x_in), wq, wo_, th, int(bool(keep_global)),
+                                   ctypes.c_float(ln_eps), _ptr(x_out), _ptr(final_len), _ptr(orig), _ptr(kpl),
+                                   _ptr(ws), wsb, _stream(stream)), "sc_encoder_attn_stack")
+    return x_out, final_len, orig, kpl

@@ -1,0 +1,400 @@
+// C ABI of the library (declared in include/sc.h): argument validation on the
+// host, workspace carving, and launch sequencing on the caller's stream.
+// Nothing here allocates device memory or synchronises.
+#include <cmath>
+#include <cstdint>
+#include <cstring>
+
+#include "../../include/sc.h"
+#include "sc_internal.h"
+
+namespace {
+
+using sc::AttnArgs;
+using sc::AttnGeom;
+
+bool overlaps(const void* a, size_t na, const void* b, size_t nb) {
+  if (!a || !b || na == 0 || nb == 0) return false;
+  const uintptr_t x = reinterpret_cast<uintptr_t>(a), y = reinterpret_cast<uintptr_t>(b);
+  return x < y + nb && y < x + na;
+}
+
+size_t elem_size(int dtype) { return dtype == SC_BF16 ? 2 : 4; }
+
+sc_status check_desc(const sc_attn_desc* d) {
+  if (!d) return SC_EINVAL;
+  if (d->B < 1 || d->n < 1 || d->H < 1 || d->window < 0 || d->G < 0 || d->G > d->n) return SC_EINVAL;
+  if (!d->valid_len) return SC_EINVAL;
+  if (d->G > 0 && !d->global_pos) return SC_EINVAL;
+  if (!std::isfinite(d->softmax_scale)) return SC_EINVAL;
+  if (d->dtype != SC_F32 && d->dtype != SC_BF16) return SC_EINVAL;
+  if (d->d != 64) return SC_EUNSUPPORTED;
+  // grid sizes must fit the launch limits
+  const long long blocks = (long long)((d->n + 63) / 64) * d->H * d->B;
+  if (blocks >= (1LL << 31)) return SC_EUNSUPPORTED;
+  if ((long long)d->B * d->n >= (1LL << 31)) return SC_EUNSUPPORTED;
+  return SC_OK;
+}
+
+size_t tensor_bytes(const sc_attn_desc* d) { return (size_t)d->B * d->n * d->H * d->d * elem_size(d->dtype); }
+
+// Carves 256-byte aligned pieces out of the caller's workspace.
+struct Carver {
+  char* base;
+  size_t off = 0;
+  explicit Carver(void* p) : base(static_cast<char*>(p)) {}
+  template <typename T>
+  T* take(size_t count) {
+    off = (off + 255) & ~size_t(255);
+    T* p = base ? reinterpret_cast<T*>(base + off) : nullptr;
+    off += count * sizeof(T);
+    return p;
+  }
+};
+
+AttnArgs make_attn_args(const sc_attn_desc* d, const AttnGeom& geo) {
+  AttnArgs a;
+  std::memset(&a, 0, sizeof(a));
+  a.valid_len = d->valid_len;
+  a.gpos = d->G > 0 ? d->global_pos : nullptr;
+  a.ld_in = (long long)d->H * d->d;
+  a.bs_in = a.ld_in * d->n;
+  a.ld_out = a.ld_in;
+  a.bs_out = a.bs_in;
+  a.B = d->B;
+  a.n = d->n;
+  a.H = d->H;
+  a.G = d->G;
+  a.r = geo.r;
+  a.c2 = d->softmax_scale * 1.4426950408889634f;
+  a.nqb = geo.nqb;
+  a.rwp = geo.rwp;
+  a.ngc = geo.ngc;
+  a.nkc = geo.nkc;
+  a.Gp = geo.Gp;
+  a.bw = geo.bw;
+  a.rb = geo.rb;
+  return a;
+}
+
+void carve_attn_ws(AttnArgs& a, Carver& c) {
+  const size_t per = (size_t)a.B * a.H * a.Gp;
+  a.gr_ml = c.take<float>(per * a.nkc * 2);
+  a.gr_o = c.take<float>(per * a.nkc * 64);
+  a.gr_lse2 = c.take<float>(per);
+}
+
+void set_partials(AttnArgs& a, float* sp) {
+  a.part_band = sp;
+  a.part_extra = sp ? sp + (size_t)a.B * a.H * a.nqb * a.rwp : nullptr;
+  a.part_grow = sp ? a.part_extra + (size_t)a.B * a.H * a.nqb * a.G : nullptr;
+}
+
+size_t attn_ws_size(const sc_attn_desc* d) {
+  const AttnGeom geo = sc::attn_geom(d->n, d->window, d->G);
+  if (geo.Gp == 0) return 0;
+  AttnArgs a = make_attn_args(d, geo);
+  Carver c(nullptr);
+  carve_attn_ws(a, c);
+  return c.off;
+}
+
+}  // namespace
+
+extern "C" {
+
+const char* sc_status_str(sc_status s) {
+  switch (s) {
+    case SC_OK: return "ok";
+    case SC_EINVAL: return "invalid argument";
+    case SC_EUNSUPPORTED: return "unsupported argument";
+    case SC_EWORKSPACE: return "workspace missing or too small";
+    case SC_EHIP: return "HIP runtime error";
+    default: return "unknown status";
+  }
+}
+
+size_t sc_score_partials_size(const sc_attn_desc* d) {
+  if (check_desc(d) != SC_OK) return 0;
+  const AttnGeom geo = sc::attn_geom(d->n, d->window, d->G);
+  return sizeof(float) * sc::partials_floats(d->B, d->H, d->n, geo, d->G);
+}
+
+size_t sc_band_probs_size(const sc_attn_desc* d) {
+  if (check_desc(d) != SC_OK) return 0;
+  const AttnGeom geo = sc::attn_geom(d->n, d->window, d->G);
+  return sizeof(float) * sc::band_probs_floats(d->B, d->H, d->n, geo, d->G);
+}
+
+size_t sc_window_attention_workspace_size(const sc_attn_desc* d) {
+  if (check_desc(d) != SC_OK) return 0;
+  return attn_ws_size(d);
+}
+
+sc_status sc_window_attention(const sc_attn_desc* d, const void* q, const void* k, const void* v, void* out,
+                              float* lse, float* score_partials, float* band_probs, void* workspace,
+                              size_t ws_bytes, void* stream) {
+  sc_status st = check_desc(d);
+  if (st != SC_OK) return st;
+  if (!q || !k || !v || !out) return SC_EINVAL;
+  const size_t tb = tensor_bytes(d);
+  if (overlaps(out, tb, q, tb) || overlaps(out, tb, k, tb) || overlaps(out, tb, v, tb)) return SC_EINVAL;
+  const size_t lse_b = sizeof(float) * d->B * d->H * d->n;
+  if (lse && (overlaps(lse, lse_b, out, tb) || overlaps(lse, lse_b, q, tb) || overlaps(lse, lse_b, k, tb) ||
+              overlaps(lse, lse_b, v, tb)))
+    return SC_EINVAL;
+  const size_t need = attn_ws_size(d);
+  if (need > 0 && (!workspace || ws_bytes < need)) return SC_EWORKSPACE;
+  const size_t sp_b = sc_score_partials_size(d), bp_b = sc_band_probs_size(d);
+  if (score_partials && (overlaps(score_partials, sp_b, out, tb) || overlaps(score_partials, sp_b, workspace, need)))
+    return SC_EINVAL;
+  if (band_probs && (overlaps(band_probs, bp_b, out, tb) || overlaps(band_probs, bp_b, score_partials, sp_b) ||
+                     overlaps(band_probs, bp_b, workspace, need)))
+    return SC_EINVAL;
+  const AttnGeom geo = sc::attn_geom(d->n, d->window, d->G);
+  AttnArgs a = make_attn_args(d, geo);
+  a.q = q;
+  a.k = k;
+  a.v = v;
+  a.out = out;
+  a.lse = lse;
+  Carver c(workspace);
+  if (geo.Gp > 0) carve_attn_ws(a, c);
+  set_partials(a, score_partials);
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  if (band_probs) {
+    a.bp_band = band_probs;
+    a.bp_gcol = band_probs + (size_t)d->B * d->H * d->n * geo.bw;
+    a.bp_grow = a.bp_gcol + (size_t)d->B * d->H * d->n * d->G;
+    if (sc::launch_fill_zero(band_probs, bp_b, s) != hipSuccess) return SC_EHIP;
+  }
+  return sc::launch_window_attention(d->dtype, a, s) == hipSuccess ? SC_OK : SC_EHIP;
+}
+
+size_t sc_ltp_score_workspace_size(const sc_attn_desc* d, int32_t mode) {
+  (void)d;
+  (void)mode;
+  return 0;
+}
+
+sc_status sc_ltp_score(const sc_attn_desc* d, int32_t mode, const float* src, float* scores, void* workspace,
+                       size_t ws_bytes, void* stream) {
+  (void)workspace;
+  (void)ws_bytes;
+  sc_status st = check_desc(d);
+  if (st != SC_OK) return st;
+  if (!src || !scores) return SC_EINVAL;
+  if (mode != SC_SCORE_FROM_PARTIALS && mode != SC_SCORE_FROM_BAND_PROBS) return SC_EINVAL;
+  const size_t src_b = mode == SC_SCORE_FROM_PARTIALS ? sc_score_partials_size(d) : sc_band_probs_size(d);
+  if (overlaps(src, src_b, scores, sizeof(float) * d->B * d->n)) return SC_EINVAL;
+  const AttnGeom geo = sc::attn_geom(d->n, d->window, d->G);
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  hipError_t e = mode == SC_SCORE_FROM_PARTIALS
+                     ? sc::launch_score_from_partials(src, d->valid_len, d->global_pos, d->B, d->n, d->H, d->G, geo,
+                                                      scores, s)
+                     : sc::launch_score_from_band(src, d->valid_len, d->global_pos, d->B, d->n, d->H, d->G, geo,
+                                                  scores, s);
+  return e == hipSuccess ? SC_OK : SC_EHIP;
+}
+
+size_t sc_ltp_prune_compact_workspace_size(const sc_attn_desc* d) {
+  if (check_desc(d) != SC_OK) return 0;
+  return sizeof(int32_t) * (size_t)d->B * d->n;
+}
+
+sc_status sc_ltp_prune_compact(const sc_attn_desc* d, const float* scores, float threshold, int32_t keep_global,
+                               int32_t n_tensors, const void* const* src, void* const* dst, const int64_t* row_bytes,
+                               int32_t* keep_idx, int32_t* new_len, int32_t* new_global_pos,
+                               const int32_t* orig_idx_in, int32_t* orig_idx_out, void* workspace, size_t ws_bytes,
+                               void* stream) {
+  sc_status st = check_desc(d);
+  if (st != SC_OK) return st;
+  if (!scores || !keep_idx || !new_len) return SC_EINVAL;
+  if (n_tensors < 0 || n_tensors > 4) return SC_EINVAL;
+  if (n_tensors > 0 && (!src || !dst || !row_bytes)) return SC_EINVAL;
+  const size_t need = sc_ltp_prune_compact_workspace_size(d);
+  if (!workspace || ws_bytes < need) return SC_EWORKSPACE;
+  const size_t bn = (size_t)d->B * d->n;
+  const size_t i32b = sizeof(int32_t) * bn;
+  sc::GatherArgs ga;
+  std::memset(&ga, 0, sizeof(ga));
+  ga.B = d->B;
+  ga.n = d->n;
+  ga.nt = n_tensors;
+  for (int t = 0; t < n_tensors; ++t) {
+    if (!src[t] || !dst[t] || row_bytes[t] <= 0) return SC_EINVAL;
+    const size_t tb = bn * (size_t)row_bytes[t];
+    if (overlaps(src[t], tb, dst[t], tb)) return SC_EINVAL;
+    if (overlaps(dst[t], tb, keep_idx, i32b) || overlaps(dst[t], tb, workspace, need)) return SC_EINVAL;
+    ga.src[t] = static_cast<const char*>(src[t]);
+    ga.dst[t] = static_cast<char*>(dst[t]);
+    ga.row_bytes[t] = row_bytes[t];
+  }
+  if (orig_idx_in && orig_idx_out && overlaps(orig_idx_in, i32b, orig_idx_out, i32b)) return SC_EINVAL;
+  if (overlaps(keep_idx, i32b, workspace, need) || overlaps(keep_idx, i32b, scores, sizeof(float) * bn))
+    return SC_EINVAL;
+  sc::PruneArgs p;
+  p.scores = scores;
+  p.valid_len = d->valid_len;
+  p.gpos = d->G > 0 ? d->global_pos : nullptr;
+  p.B = d->B;
+  p.n = d->n;
+  p.G = d->G;
+  p.threshold = threshold;
+  p.keep_global = keep_global ? 1 : 0;
+  p.keep_idx = keep_idx;
+  p.new_len = new_len;
+  p.new_gpos = new_global_pos;
+  p.orig_in = orig_idx_in;
+  p.orig_out = orig_idx_out;
+  p.new_index = static_cast<int*>(workspace);
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  if (sc::launch_prune(p, s) != hipSuccess) return SC_EHIP;
+  ga.keep_idx = keep_idx;
+  ga.new_len = new_len;
+  return sc::launch_gather(ga, s) == hipSuccess ? SC_OK : SC_EHIP;
+}
+
+// ------------------------------------------------------------------ stack --
+namespace {
+
+struct StackWs {
+  __bf16 *qkv, *o, *oc, *xc, *xa, *xb;
+  float *t, *scores, *partials;
+  int *len_a, *len_b, *gp_a, *gp_b, *orig_a, *orig_b, *keep_idx, *new_index;
+  AttnArgs attn;
+};
+
+size_t carve_stack(const sc_attn_desc* d, void* base, StackWs* ws) {
+  const AttnGeom geo = sc::attn_geom(d->n, d->window, d->G);
+  const size_t D = (size_t)d->H * d->d, bn = (size_t)d->B * d->n, G = (size_t)d->G;
+  Carver c(base);
+  StackWs w;
+  w.qkv = c.take<__bf16>(bn * 3 * D);
+  w.o = c.take<__bf16>(bn * D);
+  w.oc = c.take<__bf16>(bn * D);
+  w.xc = c.take<__bf16>(bn * D);
+  w.xa = c.take<__bf16>(bn * D);
+  w.xb = c.take<__bf16>(bn * D);
+  w.t = c.take<float>(bn * D);
+  w.scores = c.take<float>(bn);
+  w.partials = c.take<float>(sc::partials_floats(d->B, d->H, d->n, geo, d->G));
+  w.len_a = c.take<int>(d->B);
+  w.len_b = c.take<int>(d->B);
+  w.gp_a = c.take<int>(G > 0 ? d->B * G : 1);
+  w.gp_b = c.take<int>(G > 0 ? d->B * G : 1);
+  w.orig_a = c.take<int>(bn);
+  w.orig_b = c.take<int>(bn);
+  w.keep_idx = c.take<int>(bn);
+  w.new_index = c.take<int>(bn);
+  w.attn = make_attn_args(d, geo);
+  if (geo.Gp > 0) carve_attn_ws(w.attn, c);
+  if (ws) *ws = w;
+  return c.off;
+}
+
+}  // namespace
+
+size_t sc_encoder_attn_stack_workspace_size(const sc_attn_desc* d, int32_t n_layers) {
+  if (check_desc(d) != SC_OK || n_layers < 1) return 0;
+  return carve_stack(d, nullptr, nullptr);
+}
+
+sc_status sc_encoder_attn_stack(const sc_attn_desc* d, int32_t n_layers, const void* x_in,
+                                const void* const* Wqkv, const void* const* Wo, const float* thresholds,
+                                int32_t keep_global, float ln_eps, void* x_out, int32_t* final_len,
+                                int32_t* orig_idx, int32_t* kept_per_layer, void* workspace, size_t ws_bytes,
+                                void* stream) {
+  sc_status st = check_desc(d);
+  if (st != SC_OK) return st;
+  if (d->dtype != SC_BF16) return SC_EUNSUPPORTED;
+  if ((long long)d->H * d->d > 2048) return SC_EUNSUPPORTED;
+  if (n_layers < 1 || !x_in || !Wqkv || !Wo || !thresholds || !x_out || !final_len) return SC_EINVAL;
+  if (!(ln_eps > 0.f) || !std::isfinite(ln_eps)) return SC_EINVAL;
+  for (int l = 0; l < n_layers; ++l)
+    if (!Wqkv[l] || !Wo[l]) return SC_EINVAL;
+  const size_t need = sc_encoder_attn_stack_workspace_size(d, n_layers);
+  if (!workspace || ws_bytes < need) return SC_EWORKSPACE;
+  const size_t D = (size_t)d->H * d->d, bn = (size_t)d->B * d->n, xb = bn * D * 2;
+  if (overlaps(x_out, xb, x_in, xb) || overlaps(x_out, xb, workspace, need) || overlaps(x_in, xb, workspace, need))
+    return SC_EINVAL;
+  StackWs w;
+  carve_stack(d, workspace, &w);
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  const int B = d->B, n = d->n, H = d->H, G = d->G, Di = (int)D;
+  bool ok = true;
+  auto chk = [&](hipError_t e) { ok = ok && e == hipSuccess; };
+  int *len_cur = w.len_a, *len_nxt = w.len_b, *gp_cur = w.gp_a, *gp_nxt = w.gp_b;
+  int *orig_cur = w.orig_a, *orig_nxt = w.orig_b;
+  chk(sc::launch_copy_i32(d->valid_len, len_cur, B, s));
+  if (G > 0) chk(sc::launch_copy_i32(d->global_pos, gp_cur, (long long)B * G, s));
+  chk(sc::launch_iota_orig(d->valid_len, orig_cur, B, n, s));
+  const __bf16* cur = static_cast<const __bf16*>(x_in);
+  for (int l = 0; l < n_layers && ok; ++l) {
+    __bf16* nxt = (l == n_layers - 1) ? static_cast<__bf16*>(x_out) : ((l & 1) ? w.xb : w.xa);
+    // a1: qkv projection of the surviving rows
+    chk(sc::launch_gemm_bf16(cur, Wqkv[l], w.qkv, 0, B, n, Di, 3 * Di, len_cur, s));
+    // a2-a5: sparse attention reading q|k|v out of the fused projection
+    AttnArgs a = w.attn;
+    a.q = w.qkv;
+    a.k = w.qkv + D;
+    a.v = w.qkv + 2 * D;
+    a.ld_in = 3 * (long long)D;
+    a.bs_in = a.ld_in * n;
+    a.out = w.o;
+    a.ld_out = (long long)D;
+    a.bs_out = a.ld_out * n;
+    a.lse = nullptr;
+    a.valid_len = len_cur;
+    a.gpos = G > 0 ? gp_cur : nullptr;
+    set_partials(a, w.partials);
+    chk(sc::launch_window_attention(SC_BF16, a, s));
+    // a6: importance scores
+    const AttnGeom geo = sc::attn_geom(n, d->window, G);
+    chk(sc::launch_score_from_partials(w.partials, len_cur, G > 0 ? gp_cur : nullptr, B, n, H, G, geo, w.scores, s));
+    // a7-a8: threshold, scan, gather of O and of the residual input
+    sc::PruneArgs p;
+    p.scores = w.scores;
+    p.valid_len = len_cur;
+    p.gpos = G > 0 ? gp_cur : nullptr;
+    p.B = B;
+    p.n = n;
+    p.G = G;
+    p.threshold = thresholds[l];
+    p.keep_global = keep_global ? 1 : 0;
+    p.keep_idx = w.keep_idx;
+    p.new_len = len_nxt;
+    p.new_gpos = G > 0 ? gp_nxt : nullptr;
+    p.orig_in = orig_cur;
+    p.orig_out = orig_nxt;
+    p.new_index = w.new_index;
+    chk(sc::launch_prune(p, s));
+    sc::GatherArgs ga;
+    std::memset(&ga, 0, sizeof(ga));
+    ga.B = B;
+    ga.n = n;
+    ga.nt = 2;
+    ga.src[0] = reinterpret_cast<const char*>(w.o);
+    ga.dst[0] = reinterpret_cast<char*>(w.oc);
+    ga.src[1] = reinterpret_cast<const char*>(cur);
+    ga.dst[1] = reinterpret_cast<char*>(w.xc);
+    ga.row_bytes[0] = ga.row_bytes[1] = (long long)D * 2;
+    ga.keep_idx = w.keep_idx;
+    ga.new_len = len_nxt;
+    chk(sc::launch_gather(ga, s));
+    // a9: output projection, residual, LayerNorm on the survivors
+    chk(sc::launch_gemm_bf16(w.oc, Wo[l], w.t, 1, B, n, Di, Di, len_nxt, s));
+    chk(sc::launch_residual_layernorm(w.xc, w.t, nxt, B, n, Di, ln_eps, len_nxt, s));
+    if (kept_per_layer) chk(sc::launch_record_len(len_nxt, kept_per_layer + (size_t)l * B, B, s));
+    cur = nxt;
+    int* tmp;
+    tmp = len_cur; len_cur = len_nxt; len_nxt = tmp;
+    tmp = gp_cur; gp_cur = gp_nxt; gp_nxt = tmp;
+    tmp = orig_cur; orig_cur = orig_nxt; orig_nxt = tmp;
+  }
+  chk(sc::launch_copy_i32(len_cur, final_len, B, s));
+  if (orig_idx) chk(sc::launch_copy_i32(orig_cur, orig_idx, (long long)bn, s));
+  return ok ? SC_OK : SC_EHIP;
+}
+
+}  // extern "C"

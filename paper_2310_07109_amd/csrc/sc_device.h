@@ -1,0 +1,107 @@
+// Device-side building blocks of the gfx950 kernels: vector types, MFMA
+// fragment traits for the two storage types, cross-lane helpers.
+//
+// Lane conventions (wave64, v_mfma_f32_16x16x* family): lane l has row/column
+// index lr = l % 16 and lane group g = l / 16.  A 16x16 fp32 result tile puts
+// element (4g + i, lr) in lane l, register i.  Both operands of one MFMA are
+// loaded with the same per-lane pattern along the contraction dimension, so the
+// products pair up whatever order the hardware uses inside a lane group.
+#pragma once
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+#define SC_DEV __device__ __forceinline__
+
+namespace sc {
+
+typedef __attribute__((ext_vector_type(8))) __bf16 bf16x8;
+typedef __attribute__((ext_vector_type(4))) __bf16 bf16x4;
+typedef __attribute__((ext_vector_type(4))) float f32x4;
+
+constexpr int kHeadDim = 64;
+constexpr float kLog2e = 1.4426950408889634f;
+constexpr float kLn2 = 0.6931471805599453f;
+
+SC_DEV float fast_exp2(float x) { return __builtin_amdgcn_exp2f(x); }
+SC_DEV float fast_log2(float x) { return __builtin_amdgcn_logf(x); }
+
+SC_DEV float shfl_xor(float v, int m) { return __shfl_xor(v, m, 64); }
+SC_DEV float shfl(float v, int src) { return __shfl(v, src, 64); }
+
+// Sum over the four lane groups (lanes lr, lr+16, lr+32, lr+48); every lane
+// gets the same result, added in the same order.
+SC_DEV float group_sum(float v) {
+  v += shfl_xor(v, 16);
+  v += shfl_xor(v, 32);
+  return v;
+}
+SC_DEV float group_max(float v) {
+  v = fmaxf(v, shfl_xor(v, 16));
+  v = fmaxf(v, shfl_xor(v, 32));
+  return v;
+}
+
+// Workgroups are dispatched round-robin over the 8 XCDs (each with its own L2).
+// Renumber them so that consecutive logical blocks run on the same XCD: the
+// query blocks of one (sequence, head) then share K/V tiles in one L2.
+SC_DEV int xcd_remap(int i, int total) {
+  const int full = (total / 8) * 8;
+  if (i >= full) return i;
+  return (i % 8) * (full / 8) + i / 8;
+}
+
+template <int DT>
+struct Tr;
+
+// bfloat16: one MFMA v_mfma_f32_16x16x32_bf16 covers 32 of the 64 head dims;
+// a lane holds 8 consecutive dims (16 bytes) of its row.
+template <>
+struct Tr<1> {
+  using T = __bf16;
+  using Frag = bf16x8;
+  static constexpr int kChunks = 2;
+  static constexpr int kPitch = 72;  // LDS row pitch in elements: 144 B keeps 16 rows on distinct banks
+  SC_DEV static f32x4 mma(Frag a, Frag b, f32x4 c) {
+    return __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, b, c, 0, 0, 0);
+  }
+  SC_DEV static void load_frags(const T* rowp, int g, Frag (&f)[kChunks]) {
+    f[0] = *reinterpret_cast<const bf16x8*>(rowp + 8 * g);
+    f[1] = *reinterpret_cast<const bf16x8*>(rowp + 32 + 8 * g);
+  }
+};
+
+// float32: v_mfma_f32_16x16x4_f32 covers 4 dims per instruction, one per lane
+// group.  Chunk c = 4m + i gives lane group g the dim 16m + 4g + i, so one
+// 16-byte LDS read fills four chunks.
+template <>
+struct Tr<0> {
+  using T = float;
+  using Frag = float;
+  static constexpr int kChunks = 16;
+  static constexpr int kPitch = 68;  // 272 B
+  SC_DEV static f32x4 mma(Frag a, Frag b, f32x4 c) { return __builtin_amdgcn_mfma_f32_16x16x4f32(a, b, c, 0, 0, 0); }
+  SC_DEV static void load_frags(const T* rowp, int g, Frag (&f)[kChunks]) {
+#pragma unroll
+    for (int m = 0; m < 4; ++m) {
+      f32x4 v = *reinterpret_cast<const f32x4*>(rowp + 16 * m + 4 * g);
+      f[4 * m + 0] = v[0];
+      f[4 * m + 1] = v[1];
+      f[4 * m + 2] = v[2];
+      f[4 * m + 3] = v[3];
+    }
+  }
+};
+
+// 16-byte global <-> LDS copies of whole rows of 64 head dims.
+template <typename T>
+SC_DEV void copy16(T* dst, const T* src) {
+  *reinterpret_cast<uint4*>(dst) = *reinterpret_cast<const uint4*>(src);
+}
+template <typename T>
+SC_DEV void zero16(T* dst) {
+  *reinterpret_cast<uint4*>(dst) = make_uint4(0, 0, 0, 0);
+}
+
+SC_DEV int clampi(int x, int lo, int hi) { return x < lo ? lo : (x > hi ? hi : x); }
+
+}  // namespace sc

@@ -1,0 +1,98 @@
+// Internal launch interface between the C ABI (sc_api.hip) and the kernels.
+#pragma once
+#include <hip/hip_runtime.h>
+#include <stddef.h>
+#include <stdint.h>
+
+namespace sc {
+
+constexpr int kQueryBlock = 64;    // queries per window-attention workgroup
+constexpr int kKeyTile = 64;       // keys per LDS tile
+constexpr int kGlobalChunk = 64;   // global slots per workgroup of the global-row kernels
+constexpr int kGlobalKeySpan = 512;  // keys per split of the global-row kernels
+
+// Geometry + pointers of one attention launch sequence.  Element strides let
+// the same kernels read q/k/v out of a fused [tokens, 3*D] projection.
+struct AttnArgs {
+  const void* q;
+  const void* k;
+  const void* v;
+  void* out;
+  float* lse;             // [B, H, n] or null
+  const int* valid_len;   // [B]
+  const int* gpos;        // [B, G] or null
+  long long ld_in, bs_in;   // elements between tokens / sequences of q, k, v
+  long long ld_out, bs_out; // same for out
+  int B, n, H, G, r;      // r = half window, clamped to [0, n]
+  float c2;               // softmax scale * log2(e)
+  // score partials (null: skip the exact-probability pass)
+  float* part_band;       // [B, H, nqb, rwp]
+  float* part_extra;      // [B, H, nqb, G]
+  float* part_grow;       // [B, H, ngc, n]
+  int nqb, rwp, ngc, nkc, Gp;
+  // global-row split partials (workspace)
+  float* gr_ml;           // [B, H, nkc, Gp, 2]
+  float* gr_o;            // [B, H, nkc, Gp, 64]
+  float* gr_lse2;         // [B, H, Gp]
+  // paper band layout (null unless requested)
+  float* bp_band;         // [B, H, n, bw]
+  float* bp_gcol;         // [B, H, n, G]
+  float* bp_grow;         // [B, H, G, n]
+  int bw, rb;             // bw = 2 * rb + 1
+};
+
+struct AttnGeom {
+  int nqb, rwp, ngc, Gp, nkc, r, bw, rb;
+};
+
+AttnGeom attn_geom(int n, int window, int G);
+size_t partials_floats(int B, int H, int n, const AttnGeom& g, int G);
+size_t band_probs_floats(int B, int H, int n, const AttnGeom& g, int G);
+size_t attn_workspace_bytes(int B, int H, const AttnGeom& g);
+
+hipError_t launch_window_attention(int dtype, const AttnArgs& a, hipStream_t s);
+hipError_t launch_score_from_partials(const float* partials, const int* valid_len, const int* gpos, int B, int n,
+                                      int H, int G, const AttnGeom& g, float* scores, hipStream_t s);
+hipError_t launch_score_from_band(const float* bp, const int* valid_len, const int* gpos, int B, int n, int H, int G,
+                                  const AttnGeom& g, float* scores, hipStream_t s);
+
+struct PruneArgs {
+  const float* scores;     // [B, n]
+  const int* valid_len;    // [B]
+  const int* gpos;         // [B, G] or null
+  int B, n, G;
+  float threshold;
+  int keep_global;
+  int* keep_idx;           // [B, n]
+  int* new_len;            // [B]
+  int* new_gpos;           // [B, G] or null
+  const int* orig_in;      // [B, n] or null
+  int* orig_out;           // [B, n] or null
+  int* new_index;          // workspace [B, n]
+};
+hipError_t launch_prune(const PruneArgs& p, hipStream_t s);
+
+struct GatherArgs {
+  int B, n, nt;
+  const char* src[4];
+  char* dst[4];
+  long long row_bytes[4];
+  const int* keep_idx;
+  const int* new_len;
+};
+hipError_t launch_gather(const GatherArgs& g, hipStream_t s);
+
+// Stack pieces.
+// y[rows, N] = x[rows, K] . W[K, N] (bf16 in, fp32 accumulate), rows of
+// sequence b limited to len[b] (others untouched); output bf16 or fp32.
+hipError_t launch_gemm_bf16(const void* x, const void* w, void* y, int out_f32, int B, int n, int K, int N,
+                            const int* len, hipStream_t s);
+// y = bf16(LayerNorm(x_res + t)) per row, rows of sequence b < len[b].
+hipError_t launch_residual_layernorm(const void* x_res, const float* t, void* y, int B, int n, int D, float eps,
+                                     const int* len, hipStream_t s);
+hipError_t launch_fill_zero(void* p, size_t bytes, hipStream_t s);
+hipError_t launch_copy_i32(const int* src, int* dst, long long count, hipStream_t s);
+hipError_t launch_iota_orig(const int* valid_len, int* orig, int B, int n, hipStream_t s);
+hipError_t launch_record_len(const int* len, int* dst, int B, hipStream_t s);
+
+}  // namespace sc

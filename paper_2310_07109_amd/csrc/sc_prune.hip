@@ -1,0 +1,189 @@
+// Binarised mask and hard pruning (SparseCoder, arXiv 2310.07109, Sec. 4.2.2
+// steps 2-3): keep a token iff its score is strictly above the layer
+// threshold (or it is a global token and those are kept), then compact the
+// survivors, in order, into a shorter sequence.
+//
+// k_prune_scan   one workgroup of 1024 threads per sequence walks the tokens
+//                1024 at a time: a wavefront ballot + mbcnt gives each kept
+//                token its rank inside its wave, an LDS scan of the 16 wave
+//                totals gives the wave offsets, and a running carry links the
+//                chunks.  Exact and deterministic (integer work only).
+// k_gather_rows  one wavefront per output row copies the kept input row with
+//                16-byte lanes (coalesced), for up to four tensors at once.
+#include "sc_device.h"
+#include "sc_internal.h"
+
+namespace sc {
+namespace {
+
+constexpr int kScanThreads = 1024;
+constexpr int kScanWaves = kScanThreads / 64;
+
+// Exclusive rank of this lane among the lanes of its wave whose flag is set,
+// and the wave's total.
+SC_DEV int wave_rank(bool flag, int& total) {
+  const unsigned long long m = __ballot(flag);
+  total = __popcll(m);
+  return __builtin_amdgcn_mbcnt_hi((uint32_t)(m >> 32), __builtin_amdgcn_mbcnt_lo((uint32_t)m, 0u));
+}
+
+// Block-wide exclusive scan of one flag per thread; returns this thread's
+// offset and writes the block total to `total`.  Contains barriers.
+SC_DEV int block_rank(bool flag, int* s_wave, int& total) {
+  const int w = threadIdx.x >> 6, lane = threadIdx.x & 63;
+  int wt;
+  const int r = wave_rank(flag, wt);
+  if (lane == 0) s_wave[w] = wt;
+  __syncthreads();
+  if (w == 0) {
+    const int v = lane < kScanWaves ? s_wave[lane] : 0;
+    int incl = v;
+#pragma unroll
+    for (int off = 1; off < kScanWaves; off <<= 1) {
+      const int u = __shfl_up(incl, off, 64);
+      if (lane >= off) incl += u;
+    }
+    if (lane < kScanWaves) s_wave[kScanWaves + lane] = incl - v;
+    if (lane == kScanWaves - 1) s_wave[2 * kScanWaves] = incl;
+  }
+  __syncthreads();
+  total = s_wave[2 * kScanWaves];
+  const int off = s_wave[kScanWaves + w] + r;
+  __syncthreads();  // s_wave is reused by the next call
+  return off;
+}
+
+__global__ __launch_bounds__(kScanThreads) void k_prune_scan(PruneArgs p) {
+  __shared__ int s_wave[2 * kScanWaves + 1];
+  extern __shared__ uint32_t s_gbits[];  // global-token bitmask over [0, n)
+  const int b = blockIdx.x, tid = threadIdx.x, n = p.n;
+  const int L = clampi(p.valid_len[b], 0, n);
+  const int nwords = (n + 31) >> 5;
+  const int* gp = (p.gpos && p.G > 0) ? p.gpos + (long long)b * p.G : nullptr;
+  for (int i = tid; i < nwords; i += kScanThreads) s_gbits[i] = 0u;
+  __syncthreads();
+  if (gp)
+    for (int j = tid; j < p.G; j += kScanThreads) {
+      const int q = gp[j];
+      if (q >= 0 && q < L) atomicOr(&s_gbits[q >> 5], 1u << (q & 31));
+    }
+  __syncthreads();
+  const float* s = p.scores + (long long)b * n;
+  int* kidx = p.keep_idx + (long long)b * n;
+  int* nidx = p.new_index + (long long)b * n;
+  const int* oin = p.orig_in ? p.orig_in + (long long)b * n : nullptr;
+  int* oout = p.orig_out ? p.orig_out + (long long)b * n : nullptr;
+  int carry = 0;
+  for (int base = 0; base < n; base += kScanThreads) {
+    const int k = base + tid;
+    bool keep = false;
+    if (k < L) {
+      const bool glob = (s_gbits[k >> 5] >> (k & 31)) & 1u;
+      keep = s[k] > p.threshold || (p.keep_global && glob);
+    }
+    int total;
+    const int pos = carry + block_rank(keep, s_wave, total);
+    if (keep) {
+      kidx[pos] = k;
+      if (oout) oout[pos] = oin ? oin[k] : k;
+    }
+    if (k < n) nidx[k] = keep ? pos : -1;
+    carry += total;
+  }
+  if (tid == 0) p.new_len[b] = carry;
+  for (int j = carry + tid; j < n; j += kScanThreads) {
+    kidx[j] = -1;
+    if (oout) oout[j] = -1;
+  }
+  if (!p.new_gpos || p.G == 0) return;
+  __syncthreads();  // new_index written by this block is visible to it
+  int gcarry = 0;
+  int* ngp = p.new_gpos + (long long)b * p.G;
+  for (int base = 0; base < p.G; base += kScanThreads) {
+    const int j = base + tid;
+    int q = -1;
+    if (j < p.G) {
+      const int pos = gp[j];
+      if (pos >= 0 && pos < L) q = nidx[pos];
+    }
+    int total;
+    const int at = gcarry + block_rank(q >= 0, s_wave, total);
+    if (q >= 0) ngp[at] = q;
+    gcarry += total;
+  }
+  for (int j = gcarry + tid; j < p.G; j += kScanThreads) ngp[j] = -1;
+}
+
+// One wavefront per (sequence, output row); blockIdx.z selects the tensor.
+__global__ __launch_bounds__(256) void k_gather_rows(GatherArgs a) {
+  const int t = blockIdx.z, b = blockIdx.y;
+  const int j = blockIdx.x * 4 + (threadIdx.x >> 6), lane = threadIdx.x & 63;
+  if (j >= a.n || j >= a.new_len[b]) return;
+  const int k = a.keep_idx[(long long)b * a.n + j];
+  if (k < 0 || k >= a.n) return;
+  const long long rb = a.row_bytes[t];
+  const char* src = a.src[t] + ((long long)b * a.n + k) * rb;
+  char* dst = a.dst[t] + ((long long)b * a.n + j) * rb;
+  if (((rb | (long long)(uintptr_t)a.src[t] | (long long)(uintptr_t)a.dst[t]) & 15) == 0) {
+    for (long long o = 16LL * lane; o < rb; o += 16 * 64)
+      *reinterpret_cast<uint4*>(dst + o) = *reinterpret_cast<const uint4*>(src + o);
+  } else if (((rb | (long long)(uintptr_t)a.src[t] | (long long)(uintptr_t)a.dst[t]) & 3) == 0) {
+    for (long long o = 4LL * lane; o < rb; o += 4 * 64)
+      *reinterpret_cast<uint32_t*>(dst + o) = *reinterpret_cast<const uint32_t*>(src + o);
+  } else {
+    for (long long o = lane; o < rb; o += 64) dst[o] = src[o];
+  }
+}
+
+__global__ void k_fill_zero(uint32_t* p, long long words) {
+  const long long i = (long long)blockIdx.x * blockDim.x + threadIdx.x;
+  if (i < words) p[i] = 0u;
+}
+
+__global__ void k_copy_i32(const int* src, int* dst, long long count) {
+  const long long i = (long long)blockIdx.x * blockDim.x + threadIdx.x;
+  if (i < count) dst[i] = src[i];
+}
+
+__global__ void k_iota_orig(const int* valid_len, int* orig, int B, int n) {
+  const long long i = (long long)blockIdx.x * blockDim.x + threadIdx.x;
+  if (i >= (long long)B * n) return;
+  const int b = (int)(i / n), j = (int)(i % n);
+  orig[i] = j < clampi(valid_len[b], 0, n) ? j : -1;
+}
+
+}  // namespace
+
+hipError_t launch_prune(const PruneArgs& p, hipStream_t s) {
+  const size_t dyn = sizeof(uint32_t) * (((size_t)p.n + 31) / 32 + 1);
+  hipLaunchKernelGGL(k_prune_scan, dim3(p.B), dim3(kScanThreads), dyn, s, p);
+  return hipGetLastError();
+}
+
+hipError_t launch_gather(const GatherArgs& g, hipStream_t s) {
+  if (g.nt == 0) return hipSuccess;
+  hipLaunchKernelGGL(k_gather_rows, dim3((g.n + 3) / 4, g.B, g.nt), dim3(256), 0, s, g);
+  return hipGetLastError();
+}
+
+hipError_t launch_fill_zero(void* p, size_t bytes, hipStream_t s) {
+  const long long words = (long long)(bytes / 4);
+  if (words <= 0) return hipSuccess;
+  hipLaunchKernelGGL(k_fill_zero, dim3((unsigned)((words + 255) / 256)), dim3(256), 0, s, static_cast<uint32_t*>(p),
+                     words);
+  return hipGetLastError();
+}
+
+hipError_t launch_copy_i32(const int* src, int* dst, long long count, hipStream_t s) {
+  if (count <= 0) return hipSuccess;
+  hipLaunchKernelGGL(k_copy_i32, dim3((unsigned)((count + 255) / 256)), dim3(256), 0, s, src, dst, count);
+  return hipGetLastError();
+}
+
+hipError_t launch_iota_orig(const int* valid_len, int* orig, int B, int n, hipStream_t s) {
+  const long long count = (long long)B * n;
+  hipLaunchKernelGGL(k_iota_orig, dim3((unsigned)((count + 255) / 256)), dim3(256), 0, s, valid_len, orig, B, n);
+  return hipGetLastError();
+}
+
+}  // namespace sc

@@ -1,0 +1,153 @@
+"""C-ABI checks that need no GPU: the library loads, exports every entry point
+declared in include/sc.h, sizes its buffers consistently, and rejects invalid
+arguments on the host before touching the device."""
+import ctypes
+import os
+import re
+
+import pytest
+
+import paper_2310_07109_amd as sc
+from paper_2310_07109_amd import _binding as B
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "sc.h")
+
+pytestmark = pytest.mark.skipif(not os.path.exists(sc.lib_path()), reason="libsc.so not built")
+
+
+def declared_functions():
+    text = open(HEADER).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"\b(sc_[a-z_]+)\s*\(", text)))
+
+
+def test_exports_every_declared_symbol():
+    L = sc.load()
+    names = declared_functions()
+    assert len(names) == 11
+    for name in names:
+        assert hasattr(L, name), name
+
+
+def test_status_strings():
+    assert sc.sc_status_str(0) == "ok"
+    for code in (-1, -2, -3, -4):
+        assert sc.sc_status_str(code) not in ("ok", "unknown status")
+
+
+class FakeT:
+    """Stands in for a device tensor: only an address (never dereferenced)."""
+
+    def __init__(self, addr):
+        self.addr = addr
+
+    def data_ptr(self):
+        return self.addr
+
+
+def desc(**kw):
+    base = dict(B=2, n=256, H=4, window=64, valid_len=FakeT(0x10000), global_pos=None, softmax_scale=0.125,
+                dtype=B.SC_BF16)
+    base.update(kw)
+    gp = base.pop("global_pos")
+    G = base.pop("G", 0)
+    d = sc.Desc(**base)
+    d.global_pos, d.G = gp, G
+    return d
+
+
+def call_attn(d, q=0x100000, k=0x200000, v=0x300000, out=0x400000, lse=None, ws=None, ws_bytes=0):
+    L = sc.load()
+    return L.sc_window_attention(ctypes.byref(d.c()), q, k, v, out, lse, None, None, ws, ws_bytes, None)
+
+
+def test_invalid_descriptors_rejected_before_launch():
+    assert call_attn(desc(d=32)) == B.SC_EUNSUPPORTED
+    assert call_attn(desc(window=-1)) == B.SC_EINVAL
+    assert call_attn(desc(B=0)) == B.SC_EINVAL
+    assert call_attn(desc(n=0)) == B.SC_EINVAL
+    assert call_attn(desc(H=0)) == B.SC_EINVAL
+    assert call_attn(desc(dtype=7)) == B.SC_EINVAL
+    assert call_attn(desc(softmax_scale=float("nan"))) == B.SC_EINVAL
+    assert call_attn(desc(softmax_scale=float("inf"))) == B.SC_EINVAL
+    assert call_attn(desc(valid_len=None)) == B.SC_EINVAL
+    # G > 0 needs global positions, and G may not exceed n
+    assert call_attn(desc(G=3)) == B.SC_EINVAL
+    assert call_attn(desc(global_pos=FakeT(0x50000), G=257)) == B.SC_EINVAL
+
+
+def test_null_and_aliasing_rejected():
+    d = desc()
+    assert call_attn(d, q=None) == B.SC_EINVAL
+    assert call_attn(d, out=None) == B.SC_EINVAL
+    # out overlapping q (tensor is 2*256*4*64*2 bytes = 256 KiB)
+    assert call_attn(d, out=0x100000 + 4096) == B.SC_EINVAL
+    assert call_attn(d, lse=0x400000 + 64) == B.SC_EINVAL
+
+
+def test_workspace_checked():
+    d = desc(global_pos=FakeT(0x50000), G=4)
+    need = sc.sc_window_attention_workspace_size(d)
+    assert need > 0
+    assert call_attn(d, ws=None, ws_bytes=0) == B.SC_EWORKSPACE
+    assert call_attn(d, ws=0x900000, ws_bytes=need - 1) == B.SC_EWORKSPACE
+    assert sc.sc_window_attention_workspace_size(desc()) == 0  # no global tokens: no split partials
+
+
+def test_sizes():
+    d = desc()
+    # partials: per (b, h): nqb * (rwp + G) + ngc * n floats; rwp = min(64 + 2r, n)
+    nqb, rwp = 4, min(64 + 64, 256)
+    assert sc.sc_score_partials_size(d) == 4 * 2 * 4 * (nqb * rwp)
+    dg = desc(global_pos=FakeT(0x50000), G=3)
+    assert sc.sc_score_partials_size(dg) == 4 * 2 * 4 * (nqb * (rwp + 3) + 1 * 256)
+    # band layout: [B,H,n,2r+1] + [B,H,n,G] + [B,H,G,n]
+    assert sc.sc_band_probs_size(dg) == 4 * 2 * 4 * 256 * (65 + 2 * 3)
+    # huge window: r clamps to n - 1 for the band layout
+    assert sc.sc_band_probs_size(desc(window=10 ** 6)) == 4 * 2 * 4 * 256 * (2 * 255 + 1)
+    assert sc.sc_score_partials_size(desc(d=16)) == 0
+    assert sc.sc_encoder_attn_stack_workspace_size(desc(), 3) > 0
+    assert sc.sc_encoder_attn_stack_workspace_size(desc(), 0) == 0
+
+
+def test_prune_validation():
+    L = sc.load()
+    d = desc()
+    cd = d.c()
+    ws_need = sc.sc_ltp_prune_compact_workspace_size(d)
+    assert ws_need == 4 * 2 * 256
+
+    def call(scores=0x100000, nt=0, src=None, dst=None, rb=None, keep=0x200000, nl=0x300000, ws=0x800000,
+             wsb=ws_need, oin=None, oout=None):
+        return L.sc_ltp_prune_compact(ctypes.byref(cd), scores, ctypes.c_float(0.01), 1, nt, src, dst, rb, keep, nl,
+                                      None, oin, oout, ws, wsb, None)
+
+    assert call(scores=None) == B.SC_EINVAL
+    assert call(keep=None) == B.SC_EINVAL
+    assert call(nt=5) == B.SC_EINVAL
+    assert call(nt=1) == B.SC_EINVAL  # arrays missing
+    assert call(ws=None) == B.SC_EWORKSPACE
+    assert call(wsb=ws_need - 4) == B.SC_EWORKSPACE
+    one = lambda x: (ctypes.c_void_p * 1)(x)  # noqa: E731
+    rb = (ctypes.c_int64 * 1)(128)
+    assert call(nt=1, src=one(0x1000000), dst=one(0x1000000 + 128), rb=rb) == B.SC_EINVAL  # src/dst overlap
+    assert call(nt=1, src=one(0x1000000), dst=one(0x2000000), rb=(ctypes.c_int64 * 1)(0)) == B.SC_EINVAL
+    assert call(oin=0x3000000, oout=0x3000000 + 8) == B.SC_EINVAL
+
+
+def test_score_and_stack_validation():
+    L = sc.load()
+    d = desc()
+    cd = d.c()
+    assert L.sc_ltp_score(ctypes.byref(cd), 5, 0x100000, 0x200000, None, 0, None) == B.SC_EINVAL
+    assert L.sc_ltp_score(ctypes.byref(cd), 0, None, 0x200000, None, 0, None) == B.SC_EINVAL
+    dd = desc(dtype=B.SC_F32)
+    w = (ctypes.c_void_p * 1)(0x5000000)
+    th = (ctypes.c_float * 1)(0.0)
+    assert L.sc_encoder_attn_stack(ctypes.byref(dd.c()), 1, 0x100000, w, w, th, 1, ctypes.c_float(1e-5), 0x200000,
+                                   0x300000, None, None, 0x900000, 1 << 30, None) == B.SC_EUNSUPPORTED
+    assert L.sc_encoder_attn_stack(ctypes.byref(cd), 1, 0x100000, w, w, th, 1, ctypes.c_float(0.0), 0x200000,
+                                   0x300000, None, None, 0x900000, 1 << 30, None) == B.SC_EINVAL
+    assert L.sc_encoder_attn_stack(ctypes.byref(cd), 1, 0x100000, w, w, th, 1, ctypes.c_float(1e-5), 0x200000,
+                                   0x300000, None, None, None, 0, None) == B.SC_EWORKSPACE

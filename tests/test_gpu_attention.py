@@ -1,0 +1,208 @@
+"""GPU parity of sc_window_attention / sc_ltp_score / sc_ltp_prune_compact
+against the CPU oracle, through the C ABI, on seeded inputs."""
+import numpy as np
+import pytest
+import torch
+
+import oracle
+import sc_inputs as si
+from gpu_helpers import (NEAR_THETA, check_lse, check_out, check_scores, compare_keep, dev_i32, log, make_desc,
+                         run_attention, stored_threshold, to_dev_storage)
+
+pytestmark = pytest.mark.gpu
+
+import paper_2310_07109_amd as sc  # noqa: E402
+
+
+def small_case(name, dtype, B, n, H, window, G, len_range, mode="random", seed=7, lens=None, gp_override=None):
+    cfg = si.AttnConfig(name, seed, B, n, H, 64, dtype, window, len_range, G, mode)
+    inp = si.make_attention_inputs(cfg)
+    if lens is not None:
+        inp["valid_len"] = np.array(lens, np.int32)
+        inp["global_pos"] = si.global_positions(seed, inp["valid_len"], G, mode)
+    if gp_override is not None:
+        inp["global_pos"] = np.array(gp_override, np.int32)
+    return inp
+
+
+SMALL = [
+    # name, dtype, B, n, H, window, G, len range, extra
+    ("single token", "bf16", 2, 1, 2, 4, 1, (1, 1), {}),
+    ("ragged no global w0", "bf16", 2, 100, 3, 0, 0, (60, 100), {}),
+    ("w1 equals w0", "f32", 1, 70, 2, 1, 0, (70, 70), {}),
+    ("ragged varlen with empty seq", "bf16", 3, 200, 2, 16, 2, (0, 200), dict(lens=[0, 137, 200])),
+    ("dense window", "bf16", 2, 300, 2, 1000, 1, (250, 300), {}),
+    ("fp32 odd window G5", "f32", 2, 513, 2, 129, 5, (300, 513), {}),
+    ("two slot chunks", "bf16", 1, 700, 2, 256, 70, (650, 700), {}),
+    ("all tokens global", "bf16", 1, 96, 2, 8, 96, (96, 96), {}),
+    ("global at last valid token", "bf16", 2, 160, 2, 32, 2, (160, 160),
+     dict(gp_override=[[0, 159], [5, 159]])),
+    ("unused slots", "f32", 2, 140, 2, 40, 4, (140, 140), dict(gp_override=[[3, 77, -1, -1], [-1, -1, -1, -1]])),
+]
+
+
+@pytest.mark.parametrize("case", SMALL, ids=[c[0] for c in SMALL])
+def test_small_cases(case):
+    name, dtype, B, n, H, window, G, lr, extra = case
+    log(f"case {name}")
+    inp = small_case(name, dtype, B, n, H, window, G, lr, **extra)
+    ro, rl, rs = oracle.sparse_attention(inp["q64"], inp["k64"], inp["v64"], inp["valid_len"], inp["global_pos"],
+                                         window, inp["alpha"])
+    g = run_attention(inp, band=True)
+    check_out(g["out"], ro, dtype)
+    check_lse(g["lse"], rl, inp["valid_len"])
+    check_scores(g["scores"], rs, inp["valid_len"])
+    check_scores(g["band_scores"], rs, inp["valid_len"])
+
+
+def test_band_probs_layout_entries():
+    """Paper layout: band entry (i, j) is P[i][i - r + j]; checked against the oracle's P via V = identity."""
+    n, H, r = 64, 1, 5
+    cfg = si.AttnConfig("band", 3, 1, n, H, 64, "f32", 2 * r, (n, n), 2, "random")
+    inp = si.make_attention_inputs(cfg)
+    gp = inp["global_pos"]
+    # oracle probabilities: V = identity rows gives O[i] = P[i, :64]
+    eye = np.zeros((1, n, H, 64))
+    eye[0, :, 0, :] = np.eye(n, 64)
+    P, _, _ = oracle.sparse_attention(inp["q64"], inp["k64"], eye, inp["valid_len"], gp, 2 * r, inp["alpha"])
+    P = P[0, :, 0, :]
+    g = run_attention(inp, band=True)
+    bp = g["band_probs"].cpu().numpy()
+    bw = 2 * r + 1
+    band = bp[: n * bw].reshape(n, bw)
+    G = gp.shape[1]
+    gcol = bp[n * bw: n * bw + n * G].reshape(n, G)
+    grow = bp[n * bw + n * G:].reshape(G, n)
+    glob = set(gp[0].tolist())
+    for i in range(n):
+        for j in range(bw):
+            k = i - r + j
+            want = P[i, k] if (0 <= k < n and i not in glob and k not in glob) else 0.0
+            assert abs(band[i, j] - want) <= 1e-5 * abs(want) + 1e-9
+        for s, p in enumerate(gp[0]):
+            want = P[i, p] if i not in glob else 0.0
+            assert abs(gcol[i, s] - want) <= 1e-5 * abs(want) + 1e-9
+    for s, p in enumerate(gp[0]):
+        np.testing.assert_allclose(grow[s], P[p], rtol=1e-5, atol=1e-9)
+
+
+_CACHE = {}
+
+
+def config_run(cid):
+    if cid not in _CACHE:
+        cfg = si.CONFIGS[cid]
+        log(f"config {cid}: generating inputs")
+        inp = si.make_attention_inputs(cfg)
+        log(f"config {cid}: oracle")
+        ref = oracle.sparse_attention(inp["q64"], inp["k64"], inp["v64"], inp["valid_len"], inp["global_pos"],
+                                      inp["window"], inp["alpha"])
+        log(f"config {cid}: gpu")
+        g = run_attention(inp)
+        _CACHE[cid] = (inp, ref, g)
+    return _CACHE[cid]
+
+
+@pytest.mark.parametrize("cid", [1, 2, 4])
+def test_config_attention_and_scores(cid):
+    inp, (ro, rl, rs), g = config_run(cid)
+    err = check_out(g["out"], ro, inp["dtype"])
+    check_lse(g["lse"], rl, inp["valid_len"])
+    worst = check_scores(g["scores"], rs, inp["valid_len"])
+    log(f"config {cid}: max |dO| {err:.3g}, worst score rel err {worst:.3g}")
+
+
+@pytest.mark.parametrize("cid", [1, 2, 4])
+def test_config_prune_compact(cid):
+    inp, (ro, rl, rs), g = config_run(cid)
+    cfg = si.CONFIGS[cid]
+    theta = cfg.thresholds[0] if cfg.thresholds[0] is not None else stored_threshold(cid)
+    d = g["desc"]
+    # 1) the whole path: GPU scores -> GPU keep
+    keep, nl, ngp, orig, (oc,) = sc.sc_ltp_prune_compact(d, g["scores_t"], theta, True, [g["out_t"]])
+    keep, nl = keep.cpu().numpy(), nl.cpu().numpy()
+    excl, dis = compare_keep(keep, nl, rs, theta, inp["valid_len"], inp["global_pos"])
+    log(f"config {cid}: kept {nl.tolist()} of {inp['valid_len'].tolist()}, near-theta excluded {excl}, "
+        f"disagreements among them {dis}")
+    # 2) compaction on the oracle's float32 scores is bit-exact
+    s32 = torch.from_numpy(rs.astype(np.float32)).cuda()
+    keep2, nl2, ngp2, orig2, (oc2,) = sc.sc_ltp_prune_compact(d, s32, theta, True, [g["out_t"]])
+    rk, rnl, rngp, rorig = oracle.ltp_prune(rs.astype(np.float32), inp["valid_len"], inp["global_pos"], theta, 1)
+    assert np.array_equal(keep2.cpu().numpy(), rk) and np.array_equal(nl2.cpu().numpy(), rnl)
+    assert np.array_equal(ngp2.cpu().numpy(), rngp) and np.array_equal(orig2.cpu().numpy(), rorig)
+    src = g["out_t"].view(torch.int16).cpu().numpy() if inp["dtype"] == "bf16" else g["out_t"].cpu().numpy()
+    dst = oc2.view(torch.int16).cpu().numpy() if inp["dtype"] == "bf16" else oc2.cpu().numpy()
+    for b in range(d.B):
+        assert np.array_equal(dst[b, :rnl[b]], src[b, rk[b, :rnl[b]]])
+
+
+def test_config5_three_passes():
+    """Three successive prune passes on the compacted Q, K, V (renumbered positions, remapped globals)."""
+    cfg = si.CONFIGS[5]
+    log("config 5: generating inputs")
+    inp = si.make_attention_inputs(cfg)
+    q, k, v = (to_dev_storage(inp[x], "bf16") for x in ("q", "k", "v"))
+    q64, k64, v64 = inp["q64"], inp["k64"], inp["v64"]
+    vl, gp = inp["valid_len"].copy(), inp["global_pos"].copy()
+    for p, theta in enumerate(cfg.thresholds):
+        log(f"config 5 pass {p}: L={vl.tolist()}")
+        ro, rl, rs = oracle.sparse_attention(q64, k64, v64, vl, gp, cfg.window, cfg.alpha)
+        d = sc.Desc(cfg.B, cfg.n, cfg.H, cfg.window, dev_i32(vl), dev_i32(gp), cfg.alpha, sc.SC_BF16)
+        out, lse, sp, _ = sc.sc_window_attention(d, q, k, v)
+        scores = sc.sc_ltp_score(d, sp)
+        check_out(out.float().cpu().numpy(), ro, "bf16")
+        check_scores(scores.cpu().numpy(), rs, vl)
+        keep, nl, ngp, _, (q2, k2, v2) = sc.sc_ltp_prune_compact(d, scores, theta, True, [q, k, v])
+        keep_np, nl_np = keep.cpu().numpy(), nl.cpu().numpy()
+        excl, dis = compare_keep(keep_np, nl_np, rs, theta, vl, gp)
+        log(f"config 5 pass {p}: kept {nl_np.tolist()}, excluded {excl}, disagreements {dis}")
+        # continue the oracle on the GPU's kept lists (identical outside the near-theta band)
+        rk = keep_np
+        q64c, k64c, v64c = (np.zeros_like(x) for x in (q64, k64, v64))
+        for b in range(cfg.B):
+            idx = rk[b, :nl_np[b]]
+            q64c[b, :len(idx)], k64c[b, :len(idx)], v64c[b, :len(idx)] = q64[b, idx], k64[b, idx], v64[b, idx]
+        q64, k64, v64 = q64c, k64c, v64c
+        vl = nl_np.astype(np.int32)
+        gp = ngp.cpu().numpy()
+        q, k, v = q2, k2, v2
+
+
+def test_determinism():
+    inp = small_case("det", "bf16", 2, 777, 4, 200, 9, (500, 777))
+    a = run_attention(inp)
+    b = run_attention(inp)
+    for key in ("out", "lse", "scores"):
+        assert np.array_equal(a[key], b[key]), key
+
+
+def test_prune_edge_cases():
+    inp = small_case("edges", "bf16", 3, 300, 2, 64, 3, (0, 300), lens=[0, 1, 300])
+    g = run_attention(inp)
+    d = g["desc"]
+    ro, rl, rs = oracle.sparse_attention(inp["q64"], inp["k64"], inp["v64"], inp["valid_len"], inp["global_pos"],
+                                         64, inp["alpha"])
+    for theta, kg in ((-1.0, 1), (1.0, 1), (1.0, 0), (0.0, 0), (float(np.float32(rs[2, 10])), 1)):
+        s32 = torch.from_numpy(rs.astype(np.float32)).cuda()
+        keep, nl, ngp, orig, _ = sc.sc_ltp_prune_compact(d, s32, theta, kg)
+        rk, rnl, rngp, rorig = oracle.ltp_prune(rs.astype(np.float32), inp["valid_len"], inp["global_pos"], theta,
+                                                kg)
+        assert np.array_equal(keep.cpu().numpy(), rk) and np.array_equal(nl.cpu().numpy(), rnl)
+        assert np.array_equal(ngp.cpu().numpy(), rngp) and np.array_equal(orig.cpu().numpy(), rorig)
+
+
+def test_orig_index_composition_and_poisoned_tail():
+    """orig_idx_in composes; destination rows beyond new_len are left untouched."""
+    inp = small_case("orig", "bf16", 2, 256, 2, 32, 1, (200, 256), mode="first")
+    g = run_attention(inp)
+    d = g["desc"]
+    oin = torch.randint(0, 10000, (2, 256), dtype=torch.int32, device="cuda")
+    dst = torch.full_like(g["out_t"], float("nan"))
+    keep, nl, _, orig, (oc,) = sc.sc_ltp_prune_compact(d, g["scores_t"], 0.004, True, [g["out_t"]], dsts=[dst],
+                                                       orig_idx_in=oin)
+    keep, nl, orig, oin = keep.cpu().numpy(), nl.cpu().numpy(), orig.cpu().numpy(), oin.cpu().numpy()
+    oc = oc.float().cpu().numpy()
+    for b in range(2):
+        m = nl[b]
+        assert np.array_equal(orig[b, :m], oin[b, keep[b, :m]]) and np.all(orig[b, m:] == -1)
+        assert np.all(np.isnan(oc[b, m:])) and not np.isnan(oc[b, :m]).any()
