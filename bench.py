@@ -1,0 +1,170 @@
+#!/usr/bin/env python3
+"""Benchmark of the SparseCoder hot path on one MI355X.
+
+One step = one pass of the single-layer hot path over one batch resident in
+HBM: sliding-window + global sparse attention with the exact score partials
+(sc_window_attention), the importance scores (sc_ltp_score), and the
+threshold / scan / compaction of the attention output (sc_ltp_prune_compact).
+Default workload: batch 8, seq 4096, 12 heads x 64, bf16, window 512, 32
+global tokens at seeded positions, valid lengths uniform in [2048, 4096],
+threshold pruning about half of the valid tokens.
+
+Prints one JSON line.  `value` is kept-token-layers per second (valid tokens
+entering the layer, per second of wall time on the GPU stream).
+"""
+import argparse
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+METRIC = "kept-token-layers/sec per GPU; % MFMA (window attn) & % HBM peak (score/prune)"
+HBM_PEAK_GBS = 8000.0
+MFMA_PEAK_TFLOPS = {"bf16": 2500.0, "f32": 157.3}
+
+
+def algorithmic_counts(inp):
+    """Allowed (query, key) pairs of the window kernel (non-global valid queries) and of the global rows."""
+    import numpy as np
+    r = inp["window"] // 2
+    pairs_window = pairs_global = 0
+    for b in range(inp["B"]):
+        L = int(inp["valid_len"][b])
+        g = np.array(sorted(int(p) for p in inp["global_pos"][b] if 0 <= p < L), dtype=np.int64)
+        q = np.arange(L, dtype=np.int64)
+        lo, hi = np.maximum(0, q - r), np.minimum(L - 1, q + r)
+        band = hi - lo + 1
+        g_in = np.searchsorted(g, hi, side="right") - np.searchsorted(g, lo, side="left")
+        nonglob = np.ones(L, bool)
+        nonglob[g] = False
+        pairs_window += int(np.sum((band + len(g) - g_in)[nonglob]))
+        pairs_global += len(g) * L
+    return pairs_window, pairs_global
+
+
+def main():
+    ap = argparse.ArgumentParser(description=__doc__)
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=50)
+    ap.add_argument("--warmup", type=int, default=5)
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    args = ap.parse_args()
+    if args.gpus != 1:
+        print(f"bench.py measures one GPU only: the hot path runs on a single MI355X; --gpus {args.gpus} is not "
+              "supported (sharding across GPUs is described, not built).", file=sys.stderr)
+        sys.exit(2)
+
+    import numpy as np
+    import torch
+
+    import paper_2310_07109_amd as sc
+    import sc_inputs as si
+
+    cfg = si.CONFIGS[4]
+    with open(os.path.join(ROOT, "tests", "golden", "thresholds.json")) as f:
+        theta = json.load(f)["4"]["theta"]
+    t0 = time.time()
+    inp = si.make_attention_inputs(cfg)
+    gen_s = time.time() - t0
+    dev = "cuda:0"
+    torch.cuda.set_device(0)
+
+    def i32(a):
+        return torch.from_numpy(np.ascontiguousarray(a, dtype=np.int32)).to(dev)
+
+    def bf(a):
+        return torch.from_numpy(np.ascontiguousarray(a).view(np.int16)).to(dev).view(torch.bfloat16)
+
+    d = sc.Desc(cfg.B, cfg.n, cfg.H, cfg.window, i32(inp["valid_len"]), i32(inp["global_pos"]), cfg.alpha,
+                sc.SC_BF16)
+    q, k, v = bf(inp["q"]), bf(inp["k"]), bf(inp["v"])
+    out = torch.empty_like(q)
+    lse = torch.empty((cfg.B, cfg.H, cfg.n), dtype=torch.float32, device=dev)
+    sp = torch.empty(sc.sc_score_partials_size(d) // 4, dtype=torch.float32, device=dev)
+    ws_attn = torch.empty(max(sc.sc_window_attention_workspace_size(d), 1), dtype=torch.uint8, device=dev)
+    scores = torch.empty((cfg.B, cfg.n), dtype=torch.float32, device=dev)
+    oc = torch.empty_like(out)
+    outs = dict(keep_idx=torch.empty((cfg.B, cfg.n), dtype=torch.int32, device=dev),
+                new_len=torch.empty((cfg.B,), dtype=torch.int32, device=dev),
+                new_global_pos=torch.empty((cfg.B, cfg.n_global), dtype=torch.int32, device=dev),
+                orig_idx_out=torch.empty((cfg.B, cfg.n), dtype=torch.int32, device=dev))
+    ws_prune = torch.empty(sc.sc_ltp_prune_compact_workspace_size(d), dtype=torch.uint8, device=dev)
+
+    def step():
+        sc.sc_window_attention(d, q, k, v, out=out, lse=lse, score_partials=sp, workspace=ws_attn)
+        sc.sc_ltp_score(d, sp, scores=scores)
+        sc.sc_ltp_prune_compact(d, scores, theta, True, [out], dsts=[oc], outs=outs, workspace=ws_prune)
+
+    for _ in range(args.warmup):
+        step()
+    torch.cuda.synchronize()
+    sc.sc_profile_window_kernel(True)
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    w0 = time.perf_counter()
+    e0.record()
+    for _ in range(args.steps):
+        step()
+    e1.record()
+    torch.cuda.synchronize()
+    wall_ms = (time.perf_counter() - w0) * 1e3 / args.steps
+    ms = e0.elapsed_time(e1) / args.steps
+    kern_ms, launches = sc.sc_profile_window_kernel_read()
+    sc.sc_profile_window_kernel(False)
+    kern_ms /= max(launches, 1)
+
+    tokens = int(np.sum(inp["valid_len"]))
+    kept = outs["new_len"].cpu().tolist()
+    pairs_w, pairs_g = algorithmic_counts(inp)
+    hd = cfg.d
+    flops = 4.0 * hd * cfg.H * pairs_w                       # Q.K^T and P.V of the window kernel's queries
+    bytes_ = tokens * cfg.H * (4 * hd * 2 + 4)               # read Q, K, V; write O (bf16) and LSE (fp32)
+    t_mfma = flops / (MFMA_PEAK_TFLOPS["bf16"] * 1e12)
+    t_hbm = bytes_ / (HBM_PEAK_GBS * 1e9)
+    if t_mfma >= t_hbm:
+        achieved = flops / (kern_ms * 1e-3) / 1e12
+        roof = dict(bound="mfma", achieved=round(achieved, 2), peak=MFMA_PEAK_TFLOPS["bf16"], unit="TFLOP/s")
+    else:
+        achieved = bytes_ / (kern_ms * 1e-3) / 1e9
+        roof = dict(bound="hbm", achieved=round(achieved, 1), peak=HBM_PEAK_GBS, unit="GB/s")
+    roof["frac"] = round(roof["achieved"] / roof["peak"], 4)
+    roof["traffic"] = None
+    roof["kernel"] = "k_window_attn<bf16>"
+    roof["kernel_us"] = round(kern_ms * 1e3, 2)
+    roof["algorithmic_flop"] = flops
+    roof["algorithmic_bytes"] = bytes_
+
+    value = tokens / (ms * 1e-3)
+    result = {
+        "metric": METRIC, "value": round(value, 1), "unit": "kept-token-layers/s", "n_gpus": 1,
+        "steps": args.steps, "warmup": args.warmup, "ms_per_step": round(ms, 4), "higher_is_better": True,
+        "scaling": "weak", "vs_baseline": None, "dtype": "bf16", "data": "synthetic",
+        "config": {"workload": "single sparse-attention + LTP layer: B8 n4096 H12 d64 bf16, window 512, "
+                               "32 seeded global tokens, valid lengths U[2048,4096], threshold pruning ~50%",
+                   "batch": cfg.B, "seq_len": cfg.n, "heads": cfg.H, "head_dim": cfg.d, "window": cfg.window,
+                   "global_tokens": cfg.n_global, "valid_tokens": tokens, "threshold": theta,
+                   "parallelism": "none (1 GPU)"},
+        "roofline": roof,
+        "kept_per_sequence": kept,
+        "wall_ms_per_step": round(wall_ms, 4),
+    }
+    if not args.no_cpu_baseline:
+        import oracle
+        threads = oracle.default_threads()
+        c0 = time.perf_counter()
+        _, _, rs = oracle.sparse_attention(inp["q64"], inp["k64"], inp["v64"], inp["valid_len"], inp["global_pos"],
+                                           cfg.window, cfg.alpha, nthreads=threads)
+        oracle.ltp_prune(rs.astype(np.float32), inp["valid_len"], inp["global_pos"], theta, 1)
+        cpu_s = time.perf_counter() - c0
+        result["cpu_baseline"] = {"value": round(tokens / cpu_s, 1), "unit": "kept-token-layers/s", "cores": threads,
+                                  "kind": "oracle",
+                                  "sample": "the whole workload once (8 sequences, one layer: attention, scores, "
+                                            f"pruning) in double precision, {cpu_s:.2f} s"}
+    result["input_generation_s"] = round(gen_s, 1)
+    print(json.dumps(result), flush=True)
+
+
+if __name__ == "__main__":
+    main()

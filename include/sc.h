@@ -205,6 +205,18 @@ sc_status sc_encoder_attn_stack(const sc_attn_desc *desc, int32_t n_layers, cons
                                 int32_t *orig_idx, int32_t *kept_per_layer, void *workspace, size_t ws_bytes,
                                 void *stream);
 
+/*
+ * Kernel timing for benchmarks.  While enabled, every launch of the
+ * window-attention kernel (the dominant kernel of sc_window_attention and of
+ * each stack layer) is bracketed by a pair of hipEvents recorded on the
+ * caller's stream.  sc_profile_window_kernel_read() waits for the recorded
+ * events, returns the summed kernel time in milliseconds and the number of
+ * launches, and clears the record.  Enabling with a non-zero argument also
+ * clears it.  Not thread-safe; at most 4096 launches are recorded.
+ */
+sc_status sc_profile_window_kernel(int32_t enable);
+sc_status sc_profile_window_kernel_read(double *total_ms, int64_t *launches);
+
 #ifdef __cplusplus
 }
 #endif

@@ -73,7 +73,11 @@ def _f64(a):
 
 
 def default_threads() -> int:
-    return int(os.environ.get("SC_ORACLE_THREADS", "0")) or (os.cpu_count() or 1)
+    for var in ("SC_ORACLE_THREADS", "OMP_NUM_THREADS"):
+        v = os.environ.get(var, "")
+        if v.isdigit() and int(v) > 0:
+            return int(v)
+    return os.cpu_count() or 1
 
 
 def round_bf16(x: float) -> float:

@@ -52,6 +52,8 @@ def load():
         "sc_ltp_prune_compact": (i32, [dp, vp, f32, i32, i32, vp, vp, vp, vp, vp, vp, vp, vp, vp, sz, vp]),
         "sc_encoder_attn_stack_workspace_size": (sz, [dp, i32]),
         "sc_encoder_attn_stack": (i32, [dp, i32, vp, vp, vp, vp, i32, f32, vp, vp, vp, vp, vp, sz, vp]),
+        "sc_profile_window_kernel": (i32, [i32]),
+        "sc_profile_window_kernel_read": (i32, [ctypes.POINTER(ctypes.c_double), ctypes.POINTER(ctypes.c_int64)]),
     }
     for name, (res, args) in sig.items():
         f = getattr(L, name)
@@ -121,21 +123,33 @@ def sc_window_attention_workspace_size(desc: Desc) -> int:
     return load().sc_window_attention_workspace_size(ctypes.byref(desc.c()))
 
 
+def _opt(spec, make):
+    """Output argument: True -> allocate, False/None -> absent, tensor -> use it."""
+    if spec is True:
+        return make()
+    if spec is False or spec is None:
+        return None
+    return spec
+
+
 def sc_window_attention(desc: Desc, q, k, v, out=None, lse=True, score_partials=True, band_probs=False,
-                        stream=None):
-    """Returns (out, lse, score_partials, band_probs); absent outputs are None."""
+                        workspace=None, stream=None):
+    """Returns (out, lse, score_partials, band_probs); absent outputs are None.
+
+    lse / score_partials / band_probs: True (allocate), False (skip) or a preallocated tensor."""
     import torch
     L = load()
     cd = desc.c()
     dev = q.device
     out = torch.empty_like(q) if out is None else out
-    lse_t = torch.empty((desc.B, desc.H, desc.n), dtype=torch.float32, device=dev) if lse else None
-    sp = torch.empty(L.sc_score_partials_size(ctypes.byref(cd)) // 4, dtype=torch.float32, device=dev) \
-        if score_partials else None
-    bp = torch.empty(L.sc_band_probs_size(ctypes.byref(cd)) // 4, dtype=torch.float32, device=dev) \
-        if band_probs else None
+    lse_t = _opt(lse, lambda: torch.empty((desc.B, desc.H, desc.n), dtype=torch.float32, device=dev))
+    sp = _opt(score_partials, lambda: torch.empty(L.sc_score_partials_size(ctypes.byref(cd)) // 4,
+                                                  dtype=torch.float32, device=dev))
+    bp = _opt(band_probs, lambda: torch.empty(L.sc_band_probs_size(ctypes.byref(cd)) // 4, dtype=torch.float32,
+                                              device=dev))
     wsb = L.sc_window_attention_workspace_size(ctypes.byref(cd))
-    ws = _ws(wsb, dev)
+    ws = _ws(wsb, dev) if workspace is None else workspace
+    wsb = wsb if workspace is None else workspace.numel() * workspace.element_size()
     _check(L.sc_window_attention(ctypes.byref(cd), _ptr(q), _ptr(k), _ptr(v), _ptr(out), _ptr(lse_t), _ptr(sp),
                                  _ptr(bp), _ptr(ws), wsb, _stream(stream)), "sc_window_attention")
     return out, lse_t, sp, bp
@@ -162,17 +176,22 @@ def sc_ltp_prune_compact_workspace_size(desc: Desc) -> int:
 
 
 def sc_ltp_prune_compact(desc: Desc, scores, threshold, keep_global=True, tensors=(), dsts=None, orig_idx_in=None,
-                         want_orig=True, stream=None):
-    """Returns (keep_idx, new_len, new_global_pos, orig_idx_out, dsts)."""
+                         want_orig=True, outs=None, workspace=None, stream=None):
+    """Returns (keep_idx, new_len, new_global_pos, orig_idx_out, dsts).
+
+    outs: optional dict of preallocated keep_idx / new_len / new_global_pos / orig_idx_out."""
     import torch
     L = load()
     cd = desc.c()
     dev = scores.device
     B, n, G = desc.B, desc.n, desc.G
-    keep_idx = torch.empty((B, n), dtype=torch.int32, device=dev)
-    new_len = torch.empty((B,), dtype=torch.int32, device=dev)
-    ngp = torch.empty((B, G), dtype=torch.int32, device=dev) if G > 0 else None
-    orig_out = torch.empty((B, n), dtype=torch.int32, device=dev) if want_orig else None
+    outs = outs or {}
+    keep_idx = outs.get("keep_idx") if "keep_idx" in outs else torch.empty((B, n), dtype=torch.int32, device=dev)
+    new_len = outs.get("new_len") if "new_len" in outs else torch.empty((B,), dtype=torch.int32, device=dev)
+    ngp = outs.get("new_global_pos") if "new_global_pos" in outs else (
+        torch.empty((B, G), dtype=torch.int32, device=dev) if G > 0 else None)
+    orig_out = outs.get("orig_idx_out") if "orig_idx_out" in outs else (
+        torch.empty((B, n), dtype=torch.int32, device=dev) if want_orig else None)
     tensors = list(tensors)
     if dsts is None:
         dsts = [torch.empty_like(t) for t in tensors]
@@ -181,7 +200,8 @@ def sc_ltp_prune_compact(desc: Desc, scores, threshold, keep_global=True, tensor
     dst_arr = (ctypes.c_void_p * max(nt, 1))(*[t.data_ptr() for t in dsts])
     rb_arr = (ctypes.c_int64 * max(nt, 1))(*[t.numel() * t.element_size() // (B * n) for t in tensors])
     wsb = L.sc_ltp_prune_compact_workspace_size(ctypes.byref(cd))
-    ws = _ws(wsb, dev)
+    ws = _ws(wsb, dev) if workspace is None else workspace
+    wsb = wsb if workspace is None else workspace.numel() * workspace.element_size()
     _check(L.sc_ltp_prune_compact(ctypes.byref(cd), _ptr(scores), ctypes.c_float(threshold), int(bool(keep_global)),
                                   nt, src_arr, dst_arr, rb_arr, _ptr(keep_idx), _ptr(new_len), _ptr(ngp),
                                   _ptr(orig_idx_in), _ptr(orig_out), _ptr(ws), wsb, _stream(stream)),
@@ -215,3 +235,15 @@ def sc_encoder_attn_stack(desc: Desc, x_in, wqkv, wo, thresholds, keep_global=Tr
                                    ctypes.c_float(ln_eps), _ptr(x_out), _ptr(final_len), _ptr(orig), _ptr(kpl),
                                    _ptr(ws), wsb, _stream(stream)), "sc_encoder_attn_stack")
     return x_out, final_len, orig, kpl
+
+
+def sc_profile_window_kernel(enable: bool):
+    _check(load().sc_profile_window_kernel(int(bool(enable))), "sc_profile_window_kernel")
+
+
+def sc_profile_window_kernel_read():
+    """(total kernel milliseconds, launches) since the last enable/read."""
+    ms = ctypes.c_double(0.0)
+    cnt = ctypes.c_int64(0)
+    _check(load().sc_profile_window_kernel_read(ctypes.byref(ms), ctypes.byref(cnt)), "sc_profile_window_kernel_read")
+    return ms.value, cnt.value

@@ -397,4 +397,17 @@ sc_status sc_encoder_attn_stack(const sc_attn_desc* d, int32_t n_layers, const v
   return ok ? SC_OK : SC_EHIP;
 }
 
+sc_status sc_profile_window_kernel(int32_t enable) {
+  sc::profile_set(enable);
+  return SC_OK;
+}
+
+sc_status sc_profile_window_kernel_read(double* total_ms, int64_t* launches) {
+  if (!total_ms || !launches) return SC_EINVAL;
+  long long cnt = 0;
+  if (sc::profile_read(total_ms, &cnt) != 0) return SC_EHIP;
+  *launches = cnt;
+  return SC_OK;
+}
+
 }  // extern "C"

@@ -711,6 +711,51 @@ size_t attn_workspace_bytes(int B, int H, const AttnGeom& g) {
   return sizeof(float) * (per * g.nkc * (2 + kHeadDim) + per);
 }
 
+// ------------------------------------------------- benchmark kernel timing
+namespace {
+constexpr int kMaxProfiled = 4096;
+bool g_prof_on = false;
+int g_prof_count = 0;
+hipEvent_t g_prof_ev[2 * kMaxProfiled];
+bool g_prof_created[2 * kMaxProfiled] = {};
+
+void profile_begin(hipStream_t s) {
+  if (!g_prof_on || g_prof_count >= kMaxProfiled) return;
+  const int i = 2 * g_prof_count;
+  for (int j = i; j < i + 2; ++j)
+    if (!g_prof_created[j]) g_prof_created[j] = hipEventCreate(&g_prof_ev[j]) == hipSuccess;
+  if (g_prof_created[i]) hipEventRecord(g_prof_ev[i], s);
+}
+
+void profile_end(hipStream_t s) {
+  if (!g_prof_on || g_prof_count >= kMaxProfiled) return;
+  const int i = 2 * g_prof_count + 1;
+  if (g_prof_created[i]) hipEventRecord(g_prof_ev[i], s);
+  ++g_prof_count;
+}
+}  // namespace
+
+int profile_set(int enable) {
+  g_prof_on = enable != 0;
+  if (g_prof_on) g_prof_count = 0;
+  return 0;
+}
+
+int profile_read(double* total_ms, long long* launches) {
+  double tot = 0.0;
+  for (int i = 0; i < g_prof_count; ++i) {
+    if (!g_prof_created[2 * i] || !g_prof_created[2 * i + 1]) return -1;
+    if (hipEventSynchronize(g_prof_ev[2 * i + 1]) != hipSuccess) return -1;
+    float ms = 0.f;
+    if (hipEventElapsedTime(&ms, g_prof_ev[2 * i], g_prof_ev[2 * i + 1]) != hipSuccess) return -1;
+    tot += ms;
+  }
+  *total_ms = tot;
+  *launches = g_prof_count;
+  g_prof_count = 0;
+  return 0;
+}
+
 template <int DT>
 static hipError_t launch_window_t(const AttnArgs& a, hipStream_t s) {
   if (a.G > 0 && a.gpos) {
@@ -720,7 +765,9 @@ static hipError_t launch_window_t(const AttnArgs& a, hipStream_t s) {
     hipLaunchKernelGGL(k_global_rows_merge<DT>, dim3((unsigned)((waves + 3) / 4)), dim3(kThreads), 0, s, a);
   }
   const size_t dyn = sizeof(uint32_t) * ((size_t)a.rwp / 32 + 2);
+  profile_begin(s);
   hipLaunchKernelGGL(k_window_attn<DT>, dim3((unsigned)(a.nqb * a.H * a.B)), dim3(kThreads), dyn, s, a);
+  profile_end(s);
   if (a.G > 0 && a.gpos && (a.part_grow || a.bp_grow)) {
     const unsigned grid = (unsigned)(a.nkc * a.ngc * a.H * a.B);
     hipLaunchKernelGGL(k_global_rows_score<DT>, dim3(grid), dim3(kThreads), 0, s, a);

@@ -25,7 +25,7 @@ def declared_functions():
 def test_exports_every_declared_symbol():
     L = sc.load()
     names = declared_functions()
-    assert len(names) == 11
+    assert len(names) == 13
     for name in names:
         assert hasattr(L, name), name
 
