@@ -35,55 +35,93 @@ constexpr float kTau = 8.0f;       // lazy-rescale slack in log2 units
 constexpr float kNegBig = -1e30f;  // running-max sentinel (finite: avoids inf - inf)
 
 // --------------------------------------------------------------- staging ----
-// Copy 64 rows of one head (64 dims) into an LDS tile of pitch Tr::kPitch.
-// rowfn(row) gives the source token index, or -1 for a zero row.
-template <int DT, typename RowFn>
-SC_DEV void stage_rows(typename Tr<DT>::T* lds, const typename Tr<DT>::T* g, long long ld, RowFn rowfn) {
+// Tiles of 64 rows x 64 head dims move HBM -> registers -> LDS in two steps so
+// that the loads of tile t+1 are in flight while tile t is computed.  Each
+// thread moves kCpt 16-byte chunks of K (and of V).  rowfn(row) gives the
+// source token of a tile row, or -1 for a zero row.
+template <int DT>
+struct Stage {
   using T = typename Tr<DT>::T;
-  constexpr int kEpc = 16 / sizeof(T);        // elements per 16-byte chunk
-  constexpr int kCpr = kHeadDim / kEpc;       // chunks per row
-  for (int c = threadIdx.x; c < 64 * kCpr; c += kThreads) {
-    const int row = c / kCpr, part = c % kCpr;
-    const int src = rowfn(row);
-    T* d = lds + row * Tr<DT>::kPitch + part * kEpc;
-    if (src >= 0)
-      copy16(d, g + (long long)src * ld + part * kEpc);
-    else
-      zero16(d);
-  }
-}
+  static constexpr int kEpc = 16 / sizeof(T);              // elements per chunk
+  static constexpr int kCpr = kHeadDim / kEpc;             // chunks per row
+  static constexpr int kCpt = 64 * kCpr / kThreads;        // chunks per thread
+  static constexpr int P = Tr<DT>::kPitch;
+  uint4 kr[kCpt];
+  uint4 vr[kCpt];
 
-// Position of key kk (0..63) of a tile inside a transposed V row: within each
-// 32-key half, keys 4q..4q+3 and 16+4q..16+4q+3 become 8 adjacent entries, the
-// order in which one lane group holds P for the P.V MFMA.
-SC_DEV int vt_pos(int kk) {
-  const int half = kk >> 5, t = kk & 31;
-  return 32 * half + (t < 16 ? 8 * (t >> 2) + (t & 3) : 8 * ((t - 16) >> 2) + 4 + (t & 3));
-}
-
-// V tile.  bf16: transposed into [dim][key position] so that the P.V MFMA
-// reads 8 keys of one dim as one 16-byte LDS load.  f32: row-major like K.
-template <int DT, typename RowFn>
-SC_DEV void stage_v(typename Tr<DT>::T* lds, const typename Tr<DT>::T* g, long long ld, RowFn rowfn) {
-  if constexpr (DT == 0) {
-    stage_rows<DT>(lds, g, ld, rowfn);
-  } else {
-    const int t = threadIdx.x;  // 32 key pairs x 8 dim chunks
-    const int part = t & 7, k0 = 2 * (t >> 3);
-    const int r0 = rowfn(k0), r1 = rowfn(k0 + 1);
-    uint4 a = make_uint4(0, 0, 0, 0), b = make_uint4(0, 0, 0, 0);
-    if (r0 >= 0) a = *reinterpret_cast<const uint4*>(g + (long long)r0 * ld + 8 * part);
-    if (r1 >= 0) b = *reinterpret_cast<const uint4*>(g + (long long)r1 * ld + 8 * part);
-    const uint32_t av[4] = {a.x, a.y, a.z, a.w}, bv[4] = {b.x, b.y, b.z, b.w};
-    const int pos = vt_pos(k0);  // even; k0 + 1 lands at pos + 1
-    uint32_t* base = reinterpret_cast<uint32_t*>(lds);
+  template <typename RowFn>
+  SC_DEV void load_k(const T* g, long long ld, RowFn rowfn) {
 #pragma unroll
-    for (int j = 0; j < 8; ++j) {
-      const uint32_t lo = (av[j >> 1] >> (16 * (j & 1))) & 0xFFFFu;
-      const uint32_t hi = (bv[j >> 1] >> (16 * (j & 1))) & 0xFFFFu;
-      base[((8 * part + j) * Tr<1>::kPitch + pos) >> 1] = lo | (hi << 16);
+    for (int i = 0; i < kCpt; ++i) {
+      const int c = threadIdx.x + kThreads * i, row = c / kCpr, part = c % kCpr;
+      const int src = rowfn(row);
+      kr[i] = src >= 0 ? *reinterpret_cast<const uint4*>(g + (long long)src * ld + part * kEpc)
+                       : make_uint4(0, 0, 0, 0);
     }
   }
+  // V: f32 like K; bf16 as two consecutive rows x one chunk per thread (for
+  // the transposed LDS layout).
+  template <typename RowFn>
+  SC_DEV void load_v(const T* g, long long ld, RowFn rowfn) {
+    if constexpr (DT == 0) {
+#pragma unroll
+      for (int i = 0; i < kCpt; ++i) {
+        const int c = threadIdx.x + kThreads * i, row = c / kCpr, part = c % kCpr;
+        const int src = rowfn(row);
+        vr[i] = src >= 0 ? *reinterpret_cast<const uint4*>(g + (long long)src * ld + part * kEpc)
+                         : make_uint4(0, 0, 0, 0);
+      }
+    } else {
+      const int part = threadIdx.x & 7, k0 = 2 * (threadIdx.x >> 3);
+#pragma unroll
+      for (int i = 0; i < 2; ++i) {
+        const int src = rowfn(k0 + i);
+        vr[i] = src >= 0 ? *reinterpret_cast<const uint4*>(g + (long long)src * ld + 8 * part)
+                         : make_uint4(0, 0, 0, 0);
+      }
+    }
+  }
+  SC_DEV void store_k(T* lds) const {
+#pragma unroll
+    for (int i = 0; i < kCpt; ++i) {
+      const int c = threadIdx.x + kThreads * i, row = c / kCpr, part = c % kCpr;
+      *reinterpret_cast<uint4*>(lds + row * P + part * kEpc) = kr[i];
+    }
+  }
+  // bf16 V goes to LDS transposed, [dim][key position]: within each 32-key
+  // half, keys 4q..4q+3 and 16+4q..16+4q+3 become 8 adjacent entries, the order
+  // in which one lane group holds P for the P.V MFMA, so that one 16-byte LDS
+  // read feeds the MFMA.
+  SC_DEV void store_v(T* lds) const {
+    if constexpr (DT == 0) {
+#pragma unroll
+      for (int i = 0; i < kCpt; ++i) {
+        const int c = threadIdx.x + kThreads * i, row = c / kCpr, part = c % kCpr;
+        *reinterpret_cast<uint4*>(lds + row * P + part * kEpc) = vr[i];
+      }
+    } else {
+      const int part = threadIdx.x & 7, k0 = 2 * (threadIdx.x >> 3);
+      const int half = k0 >> 5, t = k0 & 31;
+      const int pos = 32 * half + (t < 16 ? 8 * (t >> 2) + (t & 3) : 8 * ((t - 16) >> 2) + 4 + (t & 3));
+      const uint32_t av[4] = {vr[0].x, vr[0].y, vr[0].z, vr[0].w};
+      const uint32_t bv[4] = {vr[1].x, vr[1].y, vr[1].z, vr[1].w};
+      uint32_t* base = reinterpret_cast<uint32_t*>(lds);
+#pragma unroll
+      for (int j = 0; j < 8; ++j) {
+        const uint32_t lo = (av[j >> 1] >> (16 * (j & 1))) & 0xFFFFu;
+        const uint32_t hi = (bv[j >> 1] >> (16 * (j & 1))) & 0xFFFFu;
+        base[((8 * part + j) * P + pos) >> 1] = lo | (hi << 16);  // pos even: k0 + 1 lands at pos + 1
+      }
+    }
+  }
+};
+
+// Direct (unpipelined) copy of 64 rows into LDS, for the query tile.
+template <int DT, typename RowFn>
+SC_DEV void stage_rows(typename Tr<DT>::T* lds, const typename Tr<DT>::T* g, long long ld, RowFn rowfn) {
+  Stage<DT> st;
+  st.load_k(g, ld, rowfn);
+  st.store_k(lds);
 }
 
 // ------------------------------------------------------------ pass 1 tile ---
@@ -222,11 +260,11 @@ __global__ __launch_bounds__(kThreads) void k_window_attn(AttnArgs a) {
   using Frag = typename TR::Frag;
   constexpr int P = TR::kPitch;
   __shared__ __attribute__((aligned(16))) T sQ[kBQ * P];
-  __shared__ __attribute__((aligned(16))) T sK[kBK * P];
-  __shared__ __attribute__((aligned(16))) T sV[kBK * P];
+  __shared__ __attribute__((aligned(16))) T sK[2][kBK * P];
+  __shared__ __attribute__((aligned(16))) T sV[2][kBK * P];
   __shared__ float sL2[kBQ];
-  __shared__ int sPos[kBK];
-  extern __shared__ uint32_t sBits[];
+  __shared__ int sPos[2][kBK];
+  extern __shared__ uint32_t sDyn[];  // [global bitmask over the band range][active global-slot chunks]
 
   const int total = a.nqb * a.H * a.B;
   const int lin = xcd_remap(blockIdx.x, total);
@@ -259,29 +297,46 @@ __global__ __launch_bounds__(kThreads) void k_window_attn(AttnArgs a) {
   const int nkt = (kt1 - kt0 + kBK - 1) / kBK;
   const int nwords = (kt1 - kt0 + 31) >> 5;
   const int nxc = gp ? (G + kBK - 1) / kBK : 0;
+  uint32_t* sBits = sDyn;                  // nwords
+  int* sXList = reinterpret_cast<int*>(sDyn + a.rwp / 32 + 2);  // nxc + 1 entries
+  __shared__ int sNx;
 
   for (int i = tid; i < nwords; i += kThreads) sBits[i] = 0u;
+  for (int i = tid; i < nxc; i += kThreads) sXList[i] = 0;
+  if (tid == 0) sNx = 0;
   __syncthreads();
+  // global keys inside the band range -> bitmask; outside -> mark their chunk
   for (int j = tid; j < (gp ? G : 0); j += kThreads) {
     const int p = gp[j];
-    if (p >= kt0 && p < kt1) atomicOr(&sBits[(p - kt0) >> 5], 1u << ((p - kt0) & 31));
+    if (p >= kt0 && p < kt1)
+      atomicOr(&sBits[(p - kt0) >> 5], 1u << ((p - kt0) & 31));
+    else if (p >= 0 && p < L)
+      sXList[j / kBK] = 1;
   }
   // padding query rows are staged as zeros: their (unused) logits stay finite
   stage_rows<DT>(sQ, Qg, a.ld_in, [&](int row) { const int q = q0 + row; return q < L ? q : -1; });
   __syncthreads();
+  if (tid == 0) {  // compact the list of chunks holding global keys outside the band
+    int m = 0;
+    for (int c = 0; c < nxc; ++c)
+      if (sXList[c]) sXList[m++] = c;
+    sNx = m;
+  }
+  __syncthreads();
+  const int ntile = nkt + sNx;
   auto gbit = [&](int k) -> bool {
     const int o = k - kt0;
     return (sBits[o >> 5] >> (o & 31)) & 1u;
   };
-  auto stage_slots = [&](int c) -> bool {  // positions of global slots outside the band
-    int ex = 0;
-    if (tid < kBK) {
-      const int j = kBK * c + tid;
-      const int p = j < G ? gp[j] : -1;
-      ex = p >= 0 && p < L && (p < kt0 || p >= kt1);
-      sPos[tid] = ex ? p : -1;
+  // source token of row `row` of tile t: band tiles first, then global-slot tiles
+  auto rowf = [&](int t, int row) -> int {
+    if (t < nkt) {
+      const int k = kt0 + t * kBK + row;
+      return k < kt1 ? k : -1;
     }
-    return __syncthreads_or(ex);
+    const int j = kBK * sXList[t - nkt] + row;
+    const int p = j < G ? gp[j] : -1;
+    return (p >= 0 && p < L && (p < kt0 || p >= kt1)) ? p : -1;
   };
 
   // ---- pass 1: softmax + P.V for this wave's 16 queries
@@ -294,41 +349,47 @@ __global__ __launch_bounds__(kThreads) void k_window_attn(AttnArgs a) {
 #pragma unroll
   for (int dt = 0; dt < 4; ++dt) o[dt] = f32x4{0.f, 0.f, 0.f, 0.f};
 
-  for (int t = 0; t < nkt + nxc; ++t) {
-    const bool band = t < nkt;
-    const int k0 = kt0 + t * kBK;
-    __syncthreads();
-    bool any = true;
-    if (band) {
-      auto rowfn = [&](int row) { const int k = k0 + row; return k < kt1 ? k : -1; };
-      stage_rows<DT>(sK, Kg, a.ld_in, rowfn);
-      stage_v<DT>(sV, Vg, a.ld_in, rowfn);
-    } else {
-      any = stage_slots(t - nkt);
-      if (any) {
-        auto rowfn = [&](int row) { return sPos[row]; };
-        stage_rows<DT>(sK, Kg, a.ld_in, rowfn);
-        stage_v<DT>(sV, Vg, a.ld_in, rowfn);
-      }
-    }
-    __syncthreads();
-    if (band) {
+  Stage<DT> st;
+  int pos_reg = -1;
+  auto load = [&](int t, bool with_v) {
+    st.load_k(Kg, a.ld_in, [&](int row) { return rowf(t, row); });
+    if (with_v) st.load_v(Vg, a.ld_in, [&](int row) { return rowf(t, row); });
+    if (tid < kBK) pos_reg = rowf(t, tid);
+  };
+  auto store = [&](int buf, bool with_v) {
+    st.store_k(sK[buf]);
+    if (with_v) st.store_v(sV[buf]);
+    if (tid < kBK) sPos[buf][tid] = pos_reg;
+  };
+
+  load(0, true);
+  store(0, true);
+  __syncthreads();
+  for (int t = 0; t < ntile; ++t) {
+    const int buf = t & 1;
+    if (t + 1 < ntile) load(t + 1, true);
+    if (t < nkt) {
+      const int k0 = kt0 + t * kBK;
       const uint32_t gw = sBits[2 * t] | (2 * t + 1 < nwords ? sBits[2 * t + 1] : 0u);
       const bool near = k0 <= qa + 15 + r && k0 + kBK - 1 >= qa - r;
-      if (!near && gw == 0u) continue;
-      const bool interior = k0 + kBK <= kt1 && k0 >= qa + 15 - r && k0 + kBK - 1 <= qa + r;
-      if (interior) {
-        softmax_tile<DT, false>(qf, sK, sV, a.c2, lr, g, m_use, l_run, o, [](int, int) { return true; });
-      } else {
-        softmax_tile<DT, true>(qf, sK, sV, a.c2, lr, g, m_use, l_run, o, [&](int st, int i) {
-          const int k = k0 + 16 * st + 4 * g + i;
-          return k < kt1 && (abs(qrow - k) <= r || gbit(k));
-        });
+      if (near || gw != 0u) {
+        const bool interior = k0 + kBK <= kt1 && k0 >= qa + 15 - r && k0 + kBK - 1 <= qa + r;
+        if (interior) {
+          softmax_tile<DT, false>(qf, sK[buf], sV[buf], a.c2, lr, g, m_use, l_run, o, [](int, int) { return true; });
+        } else {
+          softmax_tile<DT, true>(qf, sK[buf], sV[buf], a.c2, lr, g, m_use, l_run, o, [&](int s4, int i) {
+            const int k = k0 + 16 * s4 + 4 * g + i;
+            return k < kt1 && (abs(qrow - k) <= r || gbit(k));
+          });
+        }
       }
-    } else if (any) {
-      softmax_tile<DT, true>(qf, sK, sV, a.c2, lr, g, m_use, l_run, o,
-                             [&](int st, int i) { return sPos[16 * st + 4 * g + i] >= 0; });
+    } else {
+      const int* sp = sPos[buf];
+      softmax_tile<DT, true>(qf, sK[buf], sV[buf], a.c2, lr, g, m_use, l_run, o,
+                             [&](int s4, int i) { return sp[16 * s4 + 4 * g + i] >= 0; });
     }
+    if (t + 1 < ntile) store(buf ^ 1, true);
+    __syncthreads();
   }
 
   const float l_row = group_sum(l_run);
@@ -349,6 +410,8 @@ __global__ __launch_bounds__(kThreads) void k_window_attn(AttnArgs a) {
   if (!a.part_band && !a.bp_band) return;  // uniform across the block
 
   // ---- pass 2: exact probabilities, column sums per key
+  load(0, false);
+  store(0, false);
   __syncthreads();
   Frag qf2[4][TR::kChunks];
   float l2[4][4];
@@ -362,21 +425,16 @@ __global__ __launch_bounds__(kThreads) void k_window_attn(AttnArgs a) {
   float* pe = a.part_band ? a.part_extra + ((long long)bh * a.nqb + qb) * G : nullptr;
   float* bpb = a.bp_band ? a.bp_band + (long long)bh * n * a.bw : nullptr;
   float* bpc = a.bp_band ? a.bp_gcol + (long long)bh * n * G : nullptr;
+  // global-key partials of slots never visited stay zero
+  if (pe)
+    for (int j = tid; j < G; j += kThreads) pe[j] = 0.f;
 
-  for (int t = 0; t < nkt + nxc; ++t) {
-    const bool band = t < nkt;
-    const int k0 = kt0 + t * kBK;
-    __syncthreads();
-    bool any = true;
-    if (band) {
-      stage_rows<DT>(sK, Kg, a.ld_in, [&](int row) { const int k = k0 + row; return k < kt1 ? k : -1; });
-    } else {
-      any = stage_slots(t - nkt);
-      if (any) stage_rows<DT>(sK, Kg, a.ld_in, [&](int row) { return sPos[row]; });
-    }
-    __syncthreads();
+  for (int t = 0; t < ntile; ++t) {
+    const int buf = t & 1;
+    if (t + 1 < ntile) load(t + 1, false);
     float cs;
-    if (band) {
+    if (t < nkt) {
+      const int k0 = kt0 + t * kBK;
       const int key = k0 + 16 * w + lr;
       auto ok = [&](int qst, int i) {
         const int q = q0 + 16 * qst + 4 * g + i;
@@ -385,7 +443,7 @@ __global__ __launch_bounds__(kThreads) void k_window_attn(AttnArgs a) {
       if (bpb) {
         const bool kglob = key < kt1 && gbit(key);
         const int kslot = kglob ? find_slot(gp, G, key) : -1;
-        cs = score_tile<DT, true>(qf2, l2, sK, w, a.c2, lr, g, ok, [&](int qst, int i, float p) {
+        cs = score_tile<DT, true>(qf2, l2, sK[buf], w, a.c2, lr, g, ok, [&](int qst, int i, float p) {
           const int q = q0 + 16 * qst + 4 * g + i;
           if (!(q < L) || key >= kt1 || p == 0.f) return;
           if (kglob) {
@@ -396,27 +454,26 @@ __global__ __launch_bounds__(kThreads) void k_window_attn(AttnArgs a) {
         });
       } else {
         const bool interior = k0 + kBK <= kt1 && k0 >= q0 + kBQ - 1 - r && k0 + kBK - 1 <= q0 + r;
-        cs = interior ? score_tile<DT, false>(qf2, l2, sK, w, a.c2, lr, g, ok, NoEmit{})
-                      : score_tile<DT, true>(qf2, l2, sK, w, a.c2, lr, g, ok, NoEmit{});
+        cs = interior ? score_tile<DT, false>(qf2, l2, sK[buf], w, a.c2, lr, g, ok, NoEmit{})
+                      : score_tile<DT, true>(qf2, l2, sK[buf], w, a.c2, lr, g, ok, NoEmit{});
       }
       if (pb && g == 0 && key < kt1) pb[key - kt0] = cs;
     } else {
-      const int slot = kBK * (t - nkt) + 16 * w + lr;
-      cs = 0.f;
-      if (any) {
-        const bool kvalid = sPos[16 * w + lr] >= 0;
-        auto ok = [&](int, int) { return kvalid; };
-        if (bpc) {
-          cs = score_tile<DT, true>(qf2, l2, sK, w, a.c2, lr, g, ok, [&](int qst, int i, float p) {
-            const int q = q0 + 16 * qst + 4 * g + i;
-            if (kvalid && q < L && p != 0.f) bpc[(long long)q * G + slot] = p;
-          });
-        } else {
-          cs = score_tile<DT, true>(qf2, l2, sK, w, a.c2, lr, g, ok, NoEmit{});
-        }
+      const int slot = kBK * sXList[t - nkt] + 16 * w + lr;
+      const bool kvalid = sPos[buf][16 * w + lr] >= 0;
+      auto ok = [&](int, int) { return kvalid; };
+      if (bpc) {
+        cs = score_tile<DT, true>(qf2, l2, sK[buf], w, a.c2, lr, g, ok, [&](int qst, int i, float p) {
+          const int q = q0 + 16 * qst + 4 * g + i;
+          if (kvalid && q < L && p != 0.f) bpc[(long long)q * G + slot] = p;
+        });
+      } else {
+        cs = score_tile<DT, true>(qf2, l2, sK[buf], w, a.c2, lr, g, ok, NoEmit{});
       }
       if (pe && g == 0 && slot < G) pe[slot] = cs;
     }
+    if (t + 1 < ntile) store(buf ^ 1, false);
+    __syncthreads();
   }
 }
 
@@ -445,8 +502,8 @@ __global__ __launch_bounds__(kThreads) void k_global_rows_fwd(AttnArgs a) {
   using T = typename TR::T;
   constexpr int P = TR::kPitch;
   __shared__ __attribute__((aligned(16))) T sQ[kBQ * P];
-  __shared__ __attribute__((aligned(16))) T sK[kBK * P];
-  __shared__ __attribute__((aligned(16))) T sV[kBK * P];
+  __shared__ __attribute__((aligned(16))) T sK[2][kBK * P];
+  __shared__ __attribute__((aligned(16))) T sV[2][kBK * P];
   __shared__ int sPos[kGlobalChunk];
   const GrBlock blk = gr_block(a);
   const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6, g = lane >> 4, lr = lane & 15;
@@ -466,7 +523,17 @@ __global__ __launch_bounds__(kThreads) void k_global_rows_fwd(AttnArgs a) {
   const T* Qg = static_cast<const T*>(a.q) + blk.b * a.bs_in + blk.h * kHeadDim;
   const T* Kg = static_cast<const T*>(a.k) + blk.b * a.bs_in + blk.h * kHeadDim;
   const T* Vg = static_cast<const T*>(a.v) + blk.b * a.bs_in + blk.h * kHeadDim;
+  const int ntile = (kend - kbeg + kBK - 1) / kBK;
+  auto rowf = [&](int t, int row) { const int k = kbeg + t * kBK + row; return k < kend ? k : -1; };
+  Stage<DT> st;
+  auto load = [&](int t) {
+    st.load_k(Kg, a.ld_in, [&](int row) { return rowf(t, row); });
+    st.load_v(Vg, a.ld_in, [&](int row) { return rowf(t, row); });
+  };
   stage_rows<DT>(sQ, Qg, a.ld_in, [&](int row) { return sPos[row]; });
+  load(0);
+  st.store_k(sK[0]);
+  st.store_v(sV[0]);
   __syncthreads();
   typename TR::Frag qf[TR::kChunks];
   TR::load_frags(sQ + (16 * w + lr) * P, g, qf);
@@ -474,17 +541,19 @@ __global__ __launch_bounds__(kThreads) void k_global_rows_fwd(AttnArgs a) {
   f32x4 o[4];
 #pragma unroll
   for (int dt = 0; dt < 4; ++dt) o[dt] = f32x4{0.f, 0.f, 0.f, 0.f};
-  for (int k0 = kbeg; k0 < kend; k0 += kBK) {
-    __syncthreads();
-    auto rowfn = [&](int row) { const int k = k0 + row; return k < kend ? k : -1; };
-    stage_rows<DT>(sK, Kg, a.ld_in, rowfn);
-    stage_v<DT>(sV, Vg, a.ld_in, rowfn);
-    __syncthreads();
+  for (int t = 0; t < ntile; ++t) {
+    const int buf = t & 1, k0 = kbeg + t * kBK;
+    if (t + 1 < ntile) load(t + 1);
     if (k0 + kBK <= kend)
-      softmax_tile<DT, false>(qf, sK, sV, a.c2, lr, g, m_use, l_run, o, [](int, int) { return true; });
+      softmax_tile<DT, false>(qf, sK[buf], sV[buf], a.c2, lr, g, m_use, l_run, o, [](int, int) { return true; });
     else
-      softmax_tile<DT, true>(qf, sK, sV, a.c2, lr, g, m_use, l_run, o,
-                             [&](int st, int i) { return k0 + 16 * st + 4 * g + i < kend; });
+      softmax_tile<DT, true>(qf, sK[buf], sV[buf], a.c2, lr, g, m_use, l_run, o,
+                             [&](int s4, int i) { return k0 + 16 * s4 + 4 * g + i < kend; });
+    if (t + 1 < ntile) {
+      st.store_k(sK[buf ^ 1]);
+      st.store_v(sV[buf ^ 1]);
+    }
+    __syncthreads();
   }
   const float l_row = group_sum(l_run);
   const int slot = kGlobalChunk * blk.gc + 16 * w + lr;
@@ -538,7 +607,7 @@ __global__ __launch_bounds__(kThreads) void k_global_rows_score(AttnArgs a) {
   using T = typename TR::T;
   constexpr int P = TR::kPitch;
   __shared__ __attribute__((aligned(16))) T sQ[kBQ * P];
-  __shared__ __attribute__((aligned(16))) T sK[kBK * P];
+  __shared__ __attribute__((aligned(16))) T sK[2][kBK * P];
   __shared__ int sPos[kGlobalChunk];
   const GrBlock blk = gr_block(a);
   const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6, g = lane >> 4, lr = lane & 15;
@@ -563,7 +632,14 @@ __global__ __launch_bounds__(kThreads) void k_global_rows_score(AttnArgs a) {
   }
   const T* Qg = static_cast<const T*>(a.q) + blk.b * a.bs_in + blk.h * kHeadDim;
   const T* Kg = static_cast<const T*>(a.k) + blk.b * a.bs_in + blk.h * kHeadDim;
+  const int ntile = (kend - kbeg + kBK - 1) / kBK;
+  Stage<DT> st;
+  auto load = [&](int t) {
+    st.load_k(Kg, a.ld_in, [&](int row) { const int k = kbeg + t * kBK + row; return k < kend ? k : -1; });
+  };
   stage_rows<DT>(sQ, Qg, a.ld_in, [&](int row) { return sPos[row]; });
+  load(0);
+  st.store_k(sK[0]);
   __syncthreads();
   typename TR::Frag qf[4][TR::kChunks];
   float l2[4][4];
@@ -574,69 +650,81 @@ __global__ __launch_bounds__(kThreads) void k_global_rows_score(AttnArgs a) {
     for (int i = 0; i < 4; ++i)
       l2[qst][i] = a.gr_lse2[(long long)blk.bh * a.Gp + kGlobalChunk * blk.gc + 16 * qst + 4 * g + i];
   }
-  for (int k0 = kbeg; k0 < kend; k0 += kBK) {
-    __syncthreads();
-    stage_rows<DT>(sK, Kg, a.ld_in, [&](int row) { const int k = k0 + row; return k < kend ? k : -1; });
-    __syncthreads();
-    const int key = k0 + 16 * w + lr;
+  for (int t = 0; t < ntile; ++t) {
+    const int buf = t & 1;
+    if (t + 1 < ntile) load(t + 1);
+    const int key = kbeg + t * kBK + 16 * w + lr;
     auto ok = [&](int, int) { return key < kend; };
     float cs;
     if (bpr) {
-      cs = score_tile<DT, true>(qf, l2, sK, w, a.c2, lr, g, ok, [&](int qst, int i, float p) {
+      cs = score_tile<DT, true>(qf, l2, sK[buf], w, a.c2, lr, g, ok, [&](int qst, int i, float p) {
         const int slot = kGlobalChunk * blk.gc + 16 * qst + 4 * g + i;
         if (key < kend && slot < a.G && p != 0.f) bpr[(long long)slot * a.n + key] = p;
       });
     } else {
-      cs = score_tile<DT, true>(qf, l2, sK, w, a.c2, lr, g, ok, NoEmit{});
+      cs = score_tile<DT, true>(qf, l2, sK[buf], w, a.c2, lr, g, ok, NoEmit{});
     }
     if (pg && g == 0 && key < kend) pg[key] = cs;
+    if (t + 1 < ntile) st.store_k(sK[buf ^ 1]);
+    __syncthreads();
   }
 }
 
 // ------------------------------------------------------ score reduction ----
 // scores[b, k] = (sum over heads of: the band partials of every query block
 // whose band holds k, the global-key partials if k is global, and the
-// global-row sums) / (H * L).  One thread per key; fixed order; no atomics.
-__global__ __launch_bounds__(256) void k_score_from_partials(const float* part, const int* valid_len, const int* gpos,
-                                                              int B, int n, int H, int G, AttnGeom geo,
-                                                              float* scores) {
-  __shared__ int smap[256];
-  const int b = blockIdx.y, kb = blockIdx.x * 256, tid = threadIdx.x, k = kb + tid;
+// global-row sums) / (H * L).  Workgroup = 64 keys of one sequence; wave w
+// sums heads w, w + nw, ...; the nw wave sums are then added in wave order.
+// Fixed order everywhere; no atomics.
+constexpr int kScoreKeys = 64;
+constexpr int kScoreMaxWaves = 16;
+
+__global__ __launch_bounds__(64 * kScoreMaxWaves) void k_score_from_partials(const float* part, const int* valid_len,
+                                                                             const int* gpos, int B, int n, int H,
+                                                                             int G, AttnGeom geo, float* scores) {
+  __shared__ int smap[kScoreKeys];
+  __shared__ float red[kScoreMaxWaves][kScoreKeys];
+  const int b = blockIdx.y, kb = blockIdx.x * kScoreKeys, tid = threadIdx.x;
+  const int lane = tid & 63, w = tid >> 6, nw = blockDim.x >> 6;
+  const int k = kb + lane;
   const int L = clampi(valid_len[b], 0, n);
-  smap[tid] = -1;
+  if (tid < kScoreKeys) smap[tid] = -1;
   __syncthreads();
   if (gpos)
-    for (int j = tid; j < G; j += 256) {
+    for (int j = tid; j < G; j += blockDim.x) {
       const int p = gpos[(long long)b * G + j];
-      if (p >= kb && p < kb + 256 && p < L) smap[p - kb] = j;
+      if (p >= kb && p < kb + kScoreKeys && p < L) smap[p - kb] = j;
     }
   __syncthreads();
-  if (k >= n) return;
-  if (k >= L) {
-    scores[(long long)b * n + k] = 0.f;
-    return;
-  }
-  const float* band = part;
-  const float* extra = band + (size_t)B * H * geo.nqb * geo.rwp;
-  const float* grow = extra + (size_t)B * H * geo.nqb * G;
-  const int r = geo.r;
-  const int nqbv = (L + kBQ - 1) / kBQ;
-  // blocks whose key range [max(0, qb*64 - r), qb*64 + 64 + r) holds k
-  const int qlo = k - r - (kBQ - 1) <= 0 ? 0 : (k - r) / kBQ;
-  const int qhi = min(nqbv - 1, (k + r) / kBQ);
-  const int slot = smap[tid];
   float acc = 0.f;
-  for (int h = 0; h < H; ++h) {
-    const long long bh = (long long)b * H + h;
-    const float* pb = band + bh * geo.nqb * geo.rwp;
-    for (int qb = qlo; qb <= qhi; ++qb) acc += pb[(long long)qb * geo.rwp + (k - max(0, qb * kBQ - r))];
-    if (slot >= 0) {
-      const float* pe = extra + bh * geo.nqb * G + slot;
-      for (int qb = 0; qb < nqbv; ++qb) acc += pe[(long long)qb * G];
+  if (k < L) {
+    const float* band = part;
+    const float* extra = band + (size_t)B * H * geo.nqb * geo.rwp;
+    const float* grow = extra + (size_t)B * H * geo.nqb * G;
+    const int r = geo.r;
+    const int nqbv = (L + kBQ - 1) / kBQ;
+    // blocks whose key range [max(0, qb*64 - r), qb*64 + 64 + r) holds k
+    const int qlo = k - r - (kBQ - 1) <= 0 ? 0 : (k - r) / kBQ;
+    const int qhi = min(nqbv - 1, (k + r) / kBQ);
+    const int slot = smap[lane];
+    for (int h = w; h < H; h += nw) {
+      const long long bh = (long long)b * H + h;
+      const float* pb = band + bh * geo.nqb * geo.rwp;
+      for (int qb = qlo; qb <= qhi; ++qb) acc += pb[(long long)qb * geo.rwp + (k - max(0, qb * kBQ - r))];
+      if (slot >= 0) {
+        const float* pe = extra + bh * geo.nqb * G + slot;
+        for (int qb = 0; qb < nqbv; ++qb) acc += pe[(long long)qb * G];
+      }
+      for (int gc = 0; gc < geo.ngc; ++gc) acc += grow[(bh * geo.ngc + gc) * n + k];
     }
-    for (int gc = 0; gc < geo.ngc; ++gc) acc += grow[(bh * geo.ngc + gc) * n + k];
   }
-  scores[(long long)b * n + k] = acc / ((float)H * (float)L);
+  red[w][lane] = acc;
+  __syncthreads();
+  if (w == 0 && k < n) {
+    float tot = 0.f;
+    for (int i = 0; i < nw; ++i) tot += red[i][lane];
+    scores[(long long)b * n + k] = k < L ? tot / ((float)H * (float)L) : 0.f;
+  }
 }
 
 // Paper layout: the score of key k is its band sub-diagonal (entries (i, j)
@@ -724,13 +812,13 @@ void profile_begin(hipStream_t s) {
   const int i = 2 * g_prof_count;
   for (int j = i; j < i + 2; ++j)
     if (!g_prof_created[j]) g_prof_created[j] = hipEventCreate(&g_prof_ev[j]) == hipSuccess;
-  if (g_prof_created[i]) hipEventRecord(g_prof_ev[i], s);
+  if (g_prof_created[i]) (void)hipEventRecord(g_prof_ev[i], s);
 }
 
 void profile_end(hipStream_t s) {
   if (!g_prof_on || g_prof_count >= kMaxProfiled) return;
   const int i = 2 * g_prof_count + 1;
-  if (g_prof_created[i]) hipEventRecord(g_prof_ev[i], s);
+  if (g_prof_created[i]) (void)hipEventRecord(g_prof_ev[i], s);
   ++g_prof_count;
 }
 }  // namespace
@@ -764,7 +852,8 @@ static hipError_t launch_window_t(const AttnArgs& a, hipStream_t s) {
     const long long waves = (long long)a.B * a.H * a.Gp;
     hipLaunchKernelGGL(k_global_rows_merge<DT>, dim3((unsigned)((waves + 3) / 4)), dim3(kThreads), 0, s, a);
   }
-  const size_t dyn = sizeof(uint32_t) * ((size_t)a.rwp / 32 + 2);
+  const int nxc = a.G > 0 && a.gpos ? (a.G + kBK - 1) / kBK : 0;
+  const size_t dyn = sizeof(uint32_t) * ((size_t)a.rwp / 32 + 2 + nxc + 1);
   profile_begin(s);
   hipLaunchKernelGGL(k_window_attn<DT>, dim3((unsigned)(a.nqb * a.H * a.B)), dim3(kThreads), dyn, s, a);
   profile_end(s);
@@ -781,9 +870,10 @@ hipError_t launch_window_attention(int dtype, const AttnArgs& a, hipStream_t s) 
 
 hipError_t launch_score_from_partials(const float* partials, const int* valid_len, const int* gpos, int B, int n,
                                       int H, int G, const AttnGeom& g, float* scores, hipStream_t s) {
-  dim3 grid((n + 255) / 256, B);
-  hipLaunchKernelGGL(k_score_from_partials, grid, dim3(256), 0, s, partials, valid_len, G > 0 ? gpos : nullptr, B, n,
-                     H, G, g, scores);
+  dim3 grid((n + kScoreKeys - 1) / kScoreKeys, B);
+  const int nw = H < kScoreMaxWaves ? H : kScoreMaxWaves;
+  hipLaunchKernelGGL(k_score_from_partials, grid, dim3(64 * nw), 0, s, partials, valid_len, G > 0 ? gpos : nullptr, B,
+                     n, H, G, g, scores);
   return hipGetLastError();
 }
 

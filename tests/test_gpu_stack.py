@@ -1,0 +1,124 @@
+"""GPU parity of sc_encoder_attn_stack (QKV GEMM, sparse attention, scores,
+pruning, Wo GEMM, residual + LayerNorm, layer after layer) against the CPU
+oracle, compared layer by layer: each oracle layer starts from the GPU's
+previous-layer output (re-sync), so that one legitimate near-threshold flip
+cannot cascade through the later layers' geometry."""
+import numpy as np
+import pytest
+import torch
+
+import oracle
+import sc_inputs as si
+from gpu_helpers import DEV, NEAR_THETA, check_out, dev_i32, log
+
+import paper_2310_07109_amd as sc
+
+pytestmark = pytest.mark.gpu
+
+
+def bf16_dev(a_bits):
+    return torch.from_numpy(np.ascontiguousarray(a_bits).view(np.int16)).to(DEV).view(torch.bfloat16)
+
+
+def to_f64(t):
+    return t.float().cpu().numpy().astype(np.float64)
+
+
+def run_layer(x_t, wq_t, wo_t, vl, gp, H, window, alpha, theta):
+    B, n, D = x_t.shape
+    d = sc.Desc(B, n, H, window, dev_i32(vl), dev_i32(gp), alpha, sc.SC_BF16)
+    y, fl, orig, kpl = sc.sc_encoder_attn_stack(d, x_t, [wq_t], [wo_t], [theta])
+    torch.cuda.synchronize()
+    return y, fl.cpu().numpy(), orig.cpu().numpy()
+
+
+def remap_globals(gp, orig, new_len):
+    """Global positions after pruning (globals are kept): their index in the compacted sequence."""
+    out = np.full_like(gp, -1)
+    for b in range(gp.shape[0]):
+        pos = {int(o): j for j, o in enumerate(orig[b, :new_len[b]])}
+        new = sorted(pos[int(p)] for p in gp[b] if p >= 0 and int(p) in pos)
+        out[b, :len(new)] = new
+    return out
+
+
+def layerwise(x_bits, wq_bits, wo_bits, vl, gp, H, window, alpha, thetas, seqs=None, tag=""):
+    """Run the stack one layer at a time on the GPU; check each layer against the oracle on `seqs`."""
+    x_t = bf16_dev(x_bits)
+    seqs = list(range(x_bits.shape[0])) if seqs is None else seqs
+    excluded_total = 0
+    for l, theta in enumerate(thetas):
+        wq_t, wo_t = bf16_dev(wq_bits[l]), bf16_dev(wo_bits[l])
+        y_t, nl, orig = run_layer(x_t, wq_t, wo_t, vl, gp, H, window, alpha, theta)
+        x64 = to_f64(x_t)[seqs]
+        ry, rk, rnl, rngp, rs = oracle.encoder_layer(x64, si.bf16_bits_to_f64(wq_bits[l]),
+                                                     si.bf16_bits_to_f64(wo_bits[l]), vl[seqs], gp[seqs], H, window,
+                                                     alpha, theta)
+        y = to_f64(y_t)
+        for i, b in enumerate(seqs):
+            L = int(vl[b])
+            near = {k for k in range(L) if abs(float(rs[i, k]) - theta) <= NEAR_THETA}
+            g = {int(p) for p in gp[b] if 0 <= p < L}
+            kept_gpu = list(orig[b, :nl[b]])
+            kept_ref = list(rk[i, :rnl[i]])
+            excluded_total += len(near - g)
+            assert set(kept_gpu) - near == set(kept_ref) - near, f"layer {l} seq {b}: kept sets differ"
+            if set(kept_gpu) == set(kept_ref):
+                check_out(y[b, :nl[b]], ry[i, :rnl[i]], "bf16", what=f"layer {l} seq {b} hidden")
+        log(f"{tag} layer {l}: theta {theta:.5f} kept {nl.tolist()} (near-theta excluded so far {excluded_total})")
+        gp = remap_globals(gp, orig, nl)
+        vl = nl.astype(np.int32)
+        x_t = y_t
+    return x_t, vl
+
+
+def test_small_stack_layerwise_and_chained():
+    cfg = si.StackConfig("small", 21, 3, 300, 2, 64, 4, 64, (120, 300), 1, 0.05, 0.012)
+    inp = si.make_stack_inputs(cfg)
+    inp["valid_len"][1] = 1  # a one-token sequence
+    inp["global_pos"] = si.global_positions(cfg.seed, inp["valid_len"], 1, "first")
+    thetas = [0.0, 0.004, 0.008, 0.012]
+    xl, vl_final = layerwise(inp["x"], inp["wqkv"], inp["wo"], inp["valid_len"], inp["global_pos"], cfg.H,
+                             cfg.window, cfg.alpha, thetas, tag="small")
+    # the multi-layer call equals the chain of single-layer calls, bit for bit
+    d = sc.Desc(cfg.B, cfg.n, cfg.H, cfg.window, dev_i32(inp["valid_len"]), dev_i32(inp["global_pos"]), cfg.alpha,
+                sc.SC_BF16)
+    y, fl, orig, kpl = sc.sc_encoder_attn_stack(d, bf16_dev(inp["x"]), [bf16_dev(w) for w in inp["wqkv"]],
+                                                [bf16_dev(w) for w in inp["wo"]], thetas)
+    fl = fl.cpu().numpy()
+    assert np.array_equal(fl, vl_final)
+    assert np.array_equal(kpl.cpu().numpy()[-1], fl)
+    for b in range(cfg.B):
+        assert torch.equal(y[b, :fl[b]].view(torch.int16), xl[b, :fl[b]].view(torch.int16))
+        o = orig.cpu().numpy()[b]
+        assert np.all(o[fl[b]:] == -1) and np.all(np.diff(o[:fl[b]]) > 0)
+
+
+def test_stack_no_pruning_keeps_all():
+    cfg = si.StackConfig("nop", 22, 2, 130, 2, 64, 3, 32, (100, 130), 1, 0.05, 0.0)
+    inp = si.make_stack_inputs(cfg)
+    d = sc.Desc(cfg.B, cfg.n, cfg.H, cfg.window, dev_i32(inp["valid_len"]), dev_i32(inp["global_pos"]), cfg.alpha,
+                sc.SC_BF16)
+    y, fl, orig, kpl = sc.sc_encoder_attn_stack(d, bf16_dev(inp["x"]), [bf16_dev(w) for w in inp["wqkv"]],
+                                                [bf16_dev(w) for w in inp["wo"]], [-1.0] * 3)
+    assert np.array_equal(fl.cpu().numpy(), inp["valid_len"])
+    for b in range(cfg.B):
+        assert list(orig.cpu().numpy()[b, :inp["valid_len"][b]]) == list(range(inp["valid_len"][b]))
+    ry, rfl, roi, rkpl = oracle.encoder_stack(inp["x64"], inp["wqkv64"], inp["wo64"], inp["valid_len"],
+                                              inp["global_pos"], cfg.H, cfg.window, cfg.alpha, [-1.0] * 3)
+    yy = to_f64(y)
+    for b in range(cfg.B):
+        L = int(inp["valid_len"][b])
+        check_out(yy[b, :L], ry[b, :L], "bf16", what="unpruned stack")
+
+
+def test_config3_stack_sampled_sequences():
+    """RoBERTa-shaped 12-layer stack, B16 n2048: all sequences on the GPU, oracle on a sample of sequences."""
+    cfg = si.STACK_CONFIG
+    log("config 3: generating inputs")
+    inp = si.make_stack_inputs(cfg)
+    vl = inp["valid_len"]
+    seqs = [int(np.argmin(vl)), int(np.argmax(vl)), 5]
+    log(f"config 3: lengths {vl.tolist()}, oracle on sequences {seqs}")
+    layerwise(inp["x"], inp["wqkv"], inp["wo"], vl, inp["global_pos"], cfg.H, cfg.window, cfg.alpha,
+              cfg.thresholds(), seqs=seqs, tag="config 3")
