@@ -131,7 +131,7 @@ def main():
         roof = dict(bound="hbm", achieved=round(achieved, 1), peak=HBM_PEAK_GBS, unit="GB/s")
     roof["frac"] = round(roof["achieved"] / roof["peak"], 4)
     roof["traffic"] = None
-    roof["kernel"] = "k_window_attn<bf16>"
+    roof["kernel"] = "k_window_attn<bf16> + k_window_score<bf16> (the two passes of the window attention)"
     roof["kernel_us"] = round(kern_ms * 1e3, 2)
     roof["algorithmic_flop"] = flops
     roof["algorithmic_bytes"] = bytes_

@@ -77,7 +77,7 @@ typedef int32_t sc_status;
  *               sequence, ascending and distinct, each < valid_len[b];
  *               -1 marks an unused slot.  May be NULL when G == 0.
  *   valid_len   device int32 [B]: 0 <= valid_len[b] <= n.
- *   softmax_scale  alpha applied to Q.K^T before the softmax (finite).
+ *   softmax_scale  alpha >= 0 applied to Q.K^T before the softmax (finite).
  *   dtype       SC_F32 or SC_BF16 for q, k, v and outputs.
  */
 typedef struct sc_attn_desc {
@@ -206,10 +206,10 @@ sc_status sc_encoder_attn_stack(const sc_attn_desc *desc, int32_t n_layers, cons
                                 void *stream);
 
 /*
- * Kernel timing for benchmarks.  While enabled, every launch of the
- * window-attention kernel (the dominant kernel of sc_window_attention and of
- * each stack layer) is bracketed by a pair of hipEvents recorded on the
- * caller's stream.  sc_profile_window_kernel_read() waits for the recorded
+ * Kernel timing for benchmarks.  While enabled, the window-attention kernels
+ * (its two passes: softmax/P.V, then the exact-probability column sums; the
+ * dominant work of sc_window_attention and of each stack layer) are bracketed
+ * by a pair of hipEvents recorded on the caller's stream.  sc_profile_window_kernel_read() waits for the recorded
  * events, returns the summed kernel time in milliseconds and the number of
  * launches, and clears the record.  Enabling with a non-zero argument also
  * clears it.  Not thread-safe; at most 4096 launches are recorded.

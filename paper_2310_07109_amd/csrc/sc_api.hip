@@ -26,7 +26,7 @@ sc_status check_desc(const sc_attn_desc* d) {
   if (d->B < 1 || d->n < 1 || d->H < 1 || d->window < 0 || d->G < 0 || d->G > d->n) return SC_EINVAL;
   if (!d->valid_len) return SC_EINVAL;
   if (d->G > 0 && !d->global_pos) return SC_EINVAL;
-  if (!std::isfinite(d->softmax_scale)) return SC_EINVAL;
+  if (!std::isfinite(d->softmax_scale) || d->softmax_scale < 0.f) return SC_EINVAL;
   if (d->dtype != SC_F32 && d->dtype != SC_BF16) return SC_EINVAL;
   if (d->d != 64) return SC_EUNSUPPORTED;
   // grid sizes must fit the launch limits
@@ -78,6 +78,8 @@ AttnArgs make_attn_args(const sc_attn_desc* d, const AttnGeom& geo) {
 }
 
 void carve_attn_ws(AttnArgs& a, Carver& c) {
+  a.win_lse2 = c.take<float>((size_t)a.B * a.H * a.n);
+  if (a.Gp == 0) return;
   const size_t per = (size_t)a.B * a.H * a.Gp;
   a.gr_ml = c.take<float>(per * a.nkc * 2);
   a.gr_o = c.take<float>(per * a.nkc * 64);
@@ -92,7 +94,6 @@ void set_partials(AttnArgs& a, float* sp) {
 
 size_t attn_ws_size(const sc_attn_desc* d) {
   const AttnGeom geo = sc::attn_geom(d->n, d->window, d->G);
-  if (geo.Gp == 0) return 0;
   AttnArgs a = make_attn_args(d, geo);
   Carver c(nullptr);
   carve_attn_ws(a, c);
@@ -144,7 +145,7 @@ sc_status sc_window_attention(const sc_attn_desc* d, const void* q, const void* 
               overlaps(lse, lse_b, v, tb)))
     return SC_EINVAL;
   const size_t need = attn_ws_size(d);
-  if (need > 0 && (!workspace || ws_bytes < need)) return SC_EWORKSPACE;
+  if (!workspace || ws_bytes < need) return SC_EWORKSPACE;
   const size_t sp_b = sc_score_partials_size(d), bp_b = sc_band_probs_size(d);
   if (score_partials && (overlaps(score_partials, sp_b, out, tb) || overlaps(score_partials, sp_b, workspace, need)))
     return SC_EINVAL;
@@ -159,7 +160,7 @@ sc_status sc_window_attention(const sc_attn_desc* d, const void* q, const void* 
   a.out = out;
   a.lse = lse;
   Carver c(workspace);
-  if (geo.Gp > 0) carve_attn_ws(a, c);
+  carve_attn_ws(a, c);
   set_partials(a, score_partials);
   hipStream_t s = static_cast<hipStream_t>(stream);
   if (band_probs) {
@@ -288,7 +289,7 @@ size_t carve_stack(const sc_attn_desc* d, void* base, StackWs* ws) {
   w.keep_idx = c.take<int>(bn);
   w.new_index = c.take<int>(bn);
   w.attn = make_attn_args(d, geo);
-  if (geo.Gp > 0) carve_attn_ws(w.attn, c);
+  carve_attn_ws(w.attn, c);
   if (ws) *ws = w;
   return c.off;
 }

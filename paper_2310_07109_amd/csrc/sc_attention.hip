@@ -11,17 +11,19 @@
 //
 // Window kernel, one workgroup (4 waves) per (sequence, head, 64 queries):
 //   pass 1  each wave owns 16 queries; K/V tiles of 64 keys are staged in LDS
-//           and S^T = K.Q^T is computed on MFMA so that a lane holds one query
-//           and 4 keys of each 16-key sub-tile.  Online softmax in the log2
-//           domain with a lazily raised running max (rescale only when a tile
-//           max exceeds it by 8), P rounded to the storage type, O^T += V^T.P^T
-//           on MFMA.  Ends with O, and LSE for the exact second pass.
+//           (double-buffered, the next tile's loads in flight during the
+//           current tile's math) and S^T = K.Q^T is computed on MFMA so that a
+//           lane holds one query and 4 keys of each 16-key sub-tile.  Online
+//           softmax in the log2 domain with a lazily raised running max
+//           (rescale only when a tile max exceeds it by 8); P is rounded to the
+//           storage type and O^T += V^T.P^T runs on MFMA, with the V operand
+//           read from the row-major V tile by LDS transpose reads.
 //   pass 2  (only when score partials are requested) the same tiles again; each
 //           wave owns one 16-key sub-tile for all 64 queries, S = Q.K^T puts a
 //           key in each lane and 4 queries per register, P = exp2(S*c - LSE2)
 //           is exact, and the column sums are reduced inside the lane, then
-//           across the 4 lane groups with shuffles.  One float per (block,
-//           key) goes to HBM; no atomics, fixed summation order.
+//           across the 4 lane groups with permlane swaps.  One float per
+//           (block, key) goes to HBM; no atomics, fixed summation order.
 #include "sc_device.h"
 #include "sc_internal.h"
 
@@ -34,125 +36,85 @@ constexpr int kBK = kKeyTile;
 constexpr float kTau = 8.0f;       // lazy-rescale slack in log2 units
 constexpr float kNegBig = -1e30f;  // running-max sentinel (finite: avoids inf - inf)
 
+// Minimum resident waves per SIMD the register allocation must allow.
+#define SC_OCC(w) __attribute__((amdgpu_waves_per_eu(w)))
+
 // --------------------------------------------------------------- staging ----
 // Tiles of 64 rows x 64 head dims move HBM -> registers -> LDS in two steps so
 // that the loads of tile t+1 are in flight while tile t is computed.  Each
-// thread moves kCpt 16-byte chunks of K (and of V).  rowfn(row) gives the
-// source token of a tile row, or -1 for a zero row.
+// thread moves kCpt 16-byte chunks; consecutive threads cover consecutive
+// chunks of a row (coalesced loads, conflict-free LDS writes).
 template <int DT>
 struct Stage {
   using T = typename Tr<DT>::T;
-  static constexpr int kEpc = 16 / sizeof(T);              // elements per chunk
-  static constexpr int kCpr = kHeadDim / kEpc;             // chunks per row
-  static constexpr int kCpt = 64 * kCpr / kThreads;        // chunks per thread
+  static constexpr int kEpc = 16 / sizeof(T);        // elements per chunk
+  static constexpr int kCpr = kHeadDim / kEpc;       // chunks per row
+  static constexpr int kCpt = 64 * kCpr / kThreads;  // chunks per thread
   static constexpr int P = Tr<DT>::kPitch;
-  uint4 kr[kCpt];
-  uint4 vr[kCpt];
+  uint4 r[kCpt];
 
-  template <typename RowFn>
-  SC_DEV void load_k(const T* g, long long ld, RowFn rowfn) {
+  // rows k0 .. k0+63; rows at or beyond kend are zero (k0 < kend).  The
+  // loads are unconditional (row clamped to kend - 1) so that no exec-masked
+  // branch separates them from the math they overlap with.
+  SC_DEV void load_range(const T* g, long long ld, int k0, int kend) {
 #pragma unroll
     for (int i = 0; i < kCpt; ++i) {
       const int c = threadIdx.x + kThreads * i, row = c / kCpr, part = c % kCpr;
-      const int src = rowfn(row);
-      kr[i] = src >= 0 ? *reinterpret_cast<const uint4*>(g + (long long)src * ld + part * kEpc)
-                       : make_uint4(0, 0, 0, 0);
+      const int k = k0 + row;
+      const uint4 v = *reinterpret_cast<const uint4*>(g + (long long)min(k, kend - 1) * ld + part * kEpc);
+      r[i] = k < kend ? v : make_uint4(0, 0, 0, 0);
     }
   }
-  // V: f32 like K; bf16 as two consecutive rows x one chunk per thread (for
-  // the transposed LDS layout).
+  // row `row` comes from token rowfn(row), or is zero when that is -1
   template <typename RowFn>
-  SC_DEV void load_v(const T* g, long long ld, RowFn rowfn) {
-    if constexpr (DT == 0) {
-#pragma unroll
-      for (int i = 0; i < kCpt; ++i) {
-        const int c = threadIdx.x + kThreads * i, row = c / kCpr, part = c % kCpr;
-        const int src = rowfn(row);
-        vr[i] = src >= 0 ? *reinterpret_cast<const uint4*>(g + (long long)src * ld + part * kEpc)
-                         : make_uint4(0, 0, 0, 0);
-      }
-    } else {
-      const int part = threadIdx.x & 7, k0 = 2 * (threadIdx.x >> 3);
-#pragma unroll
-      for (int i = 0; i < 2; ++i) {
-        const int src = rowfn(k0 + i);
-        vr[i] = src >= 0 ? *reinterpret_cast<const uint4*>(g + (long long)src * ld + 8 * part)
-                         : make_uint4(0, 0, 0, 0);
-      }
-    }
-  }
-  SC_DEV void store_k(T* lds) const {
+  SC_DEV void load_rows(const T* g, long long ld, RowFn rowfn) {
 #pragma unroll
     for (int i = 0; i < kCpt; ++i) {
       const int c = threadIdx.x + kThreads * i, row = c / kCpr, part = c % kCpr;
-      *reinterpret_cast<uint4*>(lds + row * P + part * kEpc) = kr[i];
+      const int k = rowfn(row);
+      r[i] = k >= 0 ? *reinterpret_cast<const uint4*>(g + (long long)k * ld + part * kEpc) : make_uint4(0, 0, 0, 0);
     }
   }
-  // bf16 V goes to LDS transposed, [dim][key position]: within each 32-key
-  // half, keys 4q..4q+3 and 16+4q..16+4q+3 become 8 adjacent entries, the order
-  // in which one lane group holds P for the P.V MFMA, so that one 16-byte LDS
-  // read feeds the MFMA.
-  SC_DEV void store_v(T* lds) const {
-    if constexpr (DT == 0) {
+  SC_DEV void store(T* lds) const {
 #pragma unroll
-      for (int i = 0; i < kCpt; ++i) {
-        const int c = threadIdx.x + kThreads * i, row = c / kCpr, part = c % kCpr;
-        *reinterpret_cast<uint4*>(lds + row * P + part * kEpc) = vr[i];
-      }
-    } else {
-      const int part = threadIdx.x & 7, k0 = 2 * (threadIdx.x >> 3);
-      const int half = k0 >> 5, t = k0 & 31;
-      const int pos = 32 * half + (t < 16 ? 8 * (t >> 2) + (t & 3) : 8 * ((t - 16) >> 2) + 4 + (t & 3));
-      const uint32_t av[4] = {vr[0].x, vr[0].y, vr[0].z, vr[0].w};
-      const uint32_t bv[4] = {vr[1].x, vr[1].y, vr[1].z, vr[1].w};
-      uint32_t* base = reinterpret_cast<uint32_t*>(lds);
-#pragma unroll
-      for (int j = 0; j < 8; ++j) {
-        const uint32_t lo = (av[j >> 1] >> (16 * (j & 1))) & 0xFFFFu;
-        const uint32_t hi = (bv[j >> 1] >> (16 * (j & 1))) & 0xFFFFu;
-        base[((8 * part + j) * P + pos) >> 1] = lo | (hi << 16);  // pos even: k0 + 1 lands at pos + 1
-      }
+    for (int i = 0; i < kCpt; ++i) {
+      const int c = threadIdx.x + kThreads * i, row = c / kCpr, part = c % kCpr;
+      *reinterpret_cast<uint4*>(lds + row * P + part * kEpc) = r[i];
     }
   }
 };
 
-// Direct (unpipelined) copy of 64 rows into LDS, for the query tile.
-template <int DT, typename RowFn>
-SC_DEV void stage_rows(typename Tr<DT>::T* lds, const typename Tr<DT>::T* g, long long ld, RowFn rowfn) {
-  Stage<DT> st;
-  st.load_k(g, ld, rowfn);
-  st.store_k(lds);
-}
-
 // ------------------------------------------------------------ pass 1 tile ---
-// One 64-key tile for the 16 queries of a wave.  s holds S^T sub-tiles:
-// s[st][i] is (key 16*st + 4g + i, query lr).  ok(st, i) masks keys.
+// One 64-key tile for the 16 queries of a wave.  s[st][i] is the logit of
+// (key 16*st + 4g + i, query lr).  ok(st, i) masks keys (kMasked only).
+// The running max m_use is in scaled log2 units; softmax_scale >= 0, so the
+// tile max is taken on the raw logits and scaled once.
 template <int DT, bool kMasked, typename OkFn>
 SC_DEV void softmax_tile(const typename Tr<DT>::Frag (&qf)[Tr<DT>::kChunks], const typename Tr<DT>::T* sK,
                          const typename Tr<DT>::T* sV, float c2, int lr, int g, float& m_use, float& l_run,
                          f32x4 (&o)[4], OkFn ok) {
   using TR = Tr<DT>;
+  constexpr int P = TR::kPitch;
   f32x4 s[4];
 #pragma unroll
   for (int st = 0; st < 4; ++st) {
     typename TR::Frag kf[TR::kChunks];
-    TR::load_frags(sK + (16 * st + lr) * TR::kPitch, g, kf);
+    TR::load_frags(sK + (16 * st + lr) * P, g, kf);
     f32x4 acc = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
     for (int c = 0; c < TR::kChunks; ++c) acc = TR::mma(kf[c], qf[c], acc);
     s[st] = acc;
   }
+  bool valid[4][4];
   float tmax = -INFINITY;
 #pragma unroll
   for (int st = 0; st < 4; ++st)
 #pragma unroll
     for (int i = 0; i < 4; ++i) {
-      float x = s[st][i] * c2;
-      if (kMasked && !ok(st, i)) x = -INFINITY;
-      s[st][i] = x;
-      tmax = fmaxf(tmax, x);
+      valid[st][i] = !kMasked || ok(st, i);
+      tmax = fmaxf(tmax, valid[st][i] ? s[st][i] : -INFINITY);
     }
-  tmax = group_max(tmax);
+  tmax = group_max(tmax) * c2;
   if (tmax > m_use + kTau) {
     const float f = fast_exp2(m_use - tmax);
     l_run *= f;
@@ -165,10 +127,12 @@ SC_DEV void softmax_tile(const typename Tr<DT>::Frag (&qf)[Tr<DT>::kChunks], con
   for (int st = 0; st < 4; ++st)
 #pragma unroll
     for (int i = 0; i < 4; ++i) {
-      p[st][i] = fast_exp2(s[st][i] - m_use);
+      const float e = fast_exp2(fmaf(s[st][i], c2, -m_use));
+      p[st][i] = valid[st][i] ? e : 0.f;
       l_run += p[st][i];
     }
   if constexpr (DT == 1) {
+    // keys of lane group g in MFMA order: 32kc + 4g + (0..3), then 32kc + 16 + 4g + (0..3)
 #pragma unroll
     for (int kc = 0; kc < 2; ++kc) {
       bf16x8 pb;
@@ -177,10 +141,14 @@ SC_DEV void softmax_tile(const typename Tr<DT>::Frag (&qf)[Tr<DT>::kChunks], con
         pb[i] = (__bf16)p[2 * kc][i];
         pb[4 + i] = (__bf16)p[2 * kc + 1][i];
       }
+      const typename TR::T* v0 = sV + (32 * kc + 4 * g + (lr >> 2)) * P + 4 * (lr & 3);
+      const typename TR::T* v1 = v0 + 16 * P;
 #pragma unroll
       for (int dt = 0; dt < 4; ++dt) {
-        const bf16x8 va = *reinterpret_cast<const bf16x8*>(sV + (16 * dt + lr) * TR::kPitch + 32 * kc + 8 * g);
-        o[dt] = TR::mma(va, pb, o[dt]);
+        const i16x4 a0 = lds_read_tr16(v0 + 16 * dt);
+        const i16x4 a1 = lds_read_tr16(v1 + 16 * dt);
+        const i16x8 a = __builtin_shufflevector(a0, a1, 0, 1, 2, 3, 4, 5, 6, 7);
+        o[dt] = TR::mma(__builtin_bit_cast(bf16x8, a), pb, o[dt]);
       }
     }
   } else {
@@ -189,7 +157,7 @@ SC_DEV void softmax_tile(const typename Tr<DT>::Frag (&qf)[Tr<DT>::kChunks], con
 #pragma unroll
       for (int i = 0; i < 4; ++i)
 #pragma unroll
-        for (int dt = 0; dt < 4; ++dt) o[dt] = TR::mma(sV[(16 * st + 4 * g + i) * TR::kPitch + 16 * dt + lr], p[st][i], o[dt]);
+        for (int dt = 0; dt < 4; ++dt) o[dt] = TR::mma(sV[(16 * st + 4 * g + i) * P + 16 * dt + lr], p[st][i], o[dt]);
   }
 }
 
@@ -252,9 +220,98 @@ SC_DEV int find_slot(const int* gp, int G, int key) {
   return -1;
 }
 
-// ------------------------------------------------------- window kernel ------
+// ------------------------------------------------------- window kernels -----
+// Geometry of one window block (sequence b, head h, queries q0 .. q0+63) and
+// its LDS tables: the global-token bitmask over the key range [kt0, kt1) and
+// the list of 64-slot chunks that hold global keys outside that range.
+struct WinBlock {
+  int qb, bh, h, b, L, q0, kt0, kt1, nkt, nwords, nxc, ntile;
+};
+
+SC_DEV WinBlock win_block(const AttnArgs& a) {
+  WinBlock wb;
+  const int lin = xcd_remap(blockIdx.x, a.nqb * a.H * a.B);
+  wb.qb = lin % a.nqb;
+  wb.bh = lin / a.nqb;
+  wb.h = wb.bh % a.H;
+  wb.b = wb.bh / a.H;
+  wb.L = clampi(a.valid_len[wb.b], 0, a.n);
+  wb.q0 = wb.qb * kBQ;
+  wb.kt0 = max(0, wb.q0 - a.r);
+  wb.kt1 = min(wb.L, wb.q0 + kBQ + a.r);
+  wb.nkt = (wb.kt1 - wb.kt0 + kBK - 1) / kBK;
+  wb.nwords = (wb.kt1 - wb.kt0 + 31) >> 5;
+  wb.nxc = (a.gpos && a.G > 0) ? (a.G + kBK - 1) / kBK : 0;
+  wb.ntile = wb.nkt;
+  return wb;
+}
+
+// Fills the bitmask and the chunk list; returns the number of tiles (band
+// tiles, then global-slot tiles).  Contains barriers; call with q0 < L.
+SC_DEV int win_tables(const AttnArgs& a, const WinBlock& wb, uint32_t* sBits, int* sXList, int* sNx) {
+  const int tid = threadIdx.x;
+  const int* gp = wb.nxc ? a.gpos + (long long)wb.b * a.G : nullptr;
+  for (int i = tid; i < wb.nwords; i += kThreads) sBits[i] = 0u;
+  for (int i = tid; i < wb.nxc; i += kThreads) sXList[i] = 0;
+  __syncthreads();
+  for (int j = tid; j < (gp ? a.G : 0); j += kThreads) {
+    const int p = gp[j];
+    if (p >= wb.kt0 && p < wb.kt1)
+      atomicOr(&sBits[(p - wb.kt0) >> 5], 1u << ((p - wb.kt0) & 31));
+    else if (p >= 0 && p < wb.L)
+      sXList[j / kBK] = 1;
+  }
+  __syncthreads();
+  if (tid == 0) {
+    int m = 0;
+    for (int c = 0; c < wb.nxc; ++c)
+      if (sXList[c]) sXList[m++] = c;
+    *sNx = m;
+  }
+  __syncthreads();
+  return wb.nkt + *sNx;
+}
+
+// Tile loader shared by both passes: band tiles are contiguous key ranges,
+// global-slot tiles gather the rows of global keys outside the band.
 template <int DT>
-__global__ __launch_bounds__(kThreads) void k_window_attn(AttnArgs a) {
+struct WinLoader {
+  using T = typename Tr<DT>::T;
+  const AttnArgs& a;
+  const WinBlock& wb;
+  const int* gp;
+  const int* sXList;
+  Stage<DT> stk, stv;
+  int pos_reg = -1;
+
+  SC_DEV int slot_row(int c, int row) const {
+    const int j = kBK * c + row;
+    const int p = j < a.G ? gp[j] : -1;
+    return (p >= 0 && p < wb.L && (p < wb.kt0 || p >= wb.kt1)) ? p : -1;
+  }
+  SC_DEV void load(int t, const T* Kg, const T* Vg) {
+    if (t < wb.nkt) {
+      const int k0 = wb.kt0 + t * kBK;
+      stk.load_range(Kg, a.ld_in, k0, wb.kt1);
+      if (Vg) stv.load_range(Vg, a.ld_in, k0, wb.kt1);
+    } else {
+      const int c = sXList[t - wb.nkt];
+      stk.load_rows(Kg, a.ld_in, [&](int row) { return slot_row(c, row); });
+      if (Vg) stv.load_rows(Vg, a.ld_in, [&](int row) { return slot_row(c, row); });
+      if (threadIdx.x < kBK) pos_reg = slot_row(c, threadIdx.x);
+    }
+  }
+  SC_DEV void store(int t, T* sK, T* sV, int* sPos) const {
+    stk.store(sK);
+    if (sV) stv.store(sV);
+    if (t >= wb.nkt && threadIdx.x < kBK) sPos[threadIdx.x] = pos_reg;
+  }
+};
+
+// Pass 1: O, LSE (and the log2 LSE handed to pass 2) for the non-global
+// queries of the block; zero rows for padding queries.
+template <int DT>
+__global__ __launch_bounds__(kThreads) SC_OCC(3) void k_window_attn(AttnArgs a) {
   using TR = Tr<DT>;
   using T = typename TR::T;
   using Frag = typename TR::Frag;
@@ -262,23 +319,19 @@ __global__ __launch_bounds__(kThreads) void k_window_attn(AttnArgs a) {
   __shared__ __attribute__((aligned(16))) T sQ[kBQ * P];
   __shared__ __attribute__((aligned(16))) T sK[2][kBK * P];
   __shared__ __attribute__((aligned(16))) T sV[2][kBK * P];
-  __shared__ float sL2[kBQ];
   __shared__ int sPos[2][kBK];
+  __shared__ int sNx;
   extern __shared__ uint32_t sDyn[];  // [global bitmask over the band range][active global-slot chunks]
 
-  const int total = a.nqb * a.H * a.B;
-  const int lin = xcd_remap(blockIdx.x, total);
-  const int qb = lin % a.nqb, bh = lin / a.nqb, h = bh % a.H, b = bh / a.H;
+  const WinBlock wb = win_block(a);
   const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6, g = lane >> 4, lr = lane & 15;
-  const int n = a.n, r = a.r, G = a.G;
-  const int L = clampi(a.valid_len[b], 0, n);
-  const int q0 = qb * kBQ;
-  const T* Qg = static_cast<const T*>(a.q) + b * a.bs_in + h * kHeadDim;
-  const T* Kg = static_cast<const T*>(a.k) + b * a.bs_in + h * kHeadDim;
-  const T* Vg = static_cast<const T*>(a.v) + b * a.bs_in + h * kHeadDim;
-  T* Og = static_cast<T*>(a.out) + b * a.bs_out + h * kHeadDim;
-  float* lseg = a.lse ? a.lse + (long long)bh * n : nullptr;
-  const int* gp = (a.gpos && G > 0) ? a.gpos + (long long)b * G : nullptr;
+  const int n = a.n, r = a.r, L = wb.L, q0 = wb.q0, kt0 = wb.kt0, kt1 = wb.kt1, nkt = wb.nkt;
+  const T* Qg = static_cast<const T*>(a.q) + wb.b * a.bs_in + wb.h * kHeadDim;
+  const T* Kg = static_cast<const T*>(a.k) + wb.b * a.bs_in + wb.h * kHeadDim;
+  const T* Vg = static_cast<const T*>(a.v) + wb.b * a.bs_in + wb.h * kHeadDim;
+  T* Og = static_cast<T*>(a.out) + wb.b * a.bs_out + wb.h * kHeadDim;
+  float* lseg = a.lse ? a.lse + (long long)wb.bh * n : nullptr;
+  float* l2g = a.win_lse2 ? a.win_lse2 + (long long)wb.bh * n : nullptr;
 
   if (q0 >= L) {  // padding block: zero output rows
     constexpr int kEpc = 16 / sizeof(T), kCpr = kHeadDim / kEpc;
@@ -291,55 +344,20 @@ __global__ __launch_bounds__(kThreads) void k_window_attn(AttnArgs a) {
         if (q0 + i < n) lseg[q0 + i] = -INFINITY;
     return;
   }
-
-  const int kt0 = max(0, q0 - r);
-  const int kt1 = min(L, q0 + kBQ + r);
-  const int nkt = (kt1 - kt0 + kBK - 1) / kBK;
-  const int nwords = (kt1 - kt0 + 31) >> 5;
-  const int nxc = gp ? (G + kBK - 1) / kBK : 0;
-  uint32_t* sBits = sDyn;                  // nwords
-  int* sXList = reinterpret_cast<int*>(sDyn + a.rwp / 32 + 2);  // nxc + 1 entries
-  __shared__ int sNx;
-
-  for (int i = tid; i < nwords; i += kThreads) sBits[i] = 0u;
-  for (int i = tid; i < nxc; i += kThreads) sXList[i] = 0;
-  if (tid == 0) sNx = 0;
-  __syncthreads();
-  // global keys inside the band range -> bitmask; outside -> mark their chunk
-  for (int j = tid; j < (gp ? G : 0); j += kThreads) {
-    const int p = gp[j];
-    if (p >= kt0 && p < kt1)
-      atomicOr(&sBits[(p - kt0) >> 5], 1u << ((p - kt0) & 31));
-    else if (p >= 0 && p < L)
-      sXList[j / kBK] = 1;
+  uint32_t* sBits = sDyn;
+  int* sXList = reinterpret_cast<int*>(sDyn + a.rwp / 32 + 2);
+  {  // padding query rows are staged as zeros: their (unused) logits stay finite
+    Stage<DT> sq;
+    sq.load_range(Qg + (long long)q0 * a.ld_in, a.ld_in, 0, L - q0);
+    sq.store(sQ);
   }
-  // padding query rows are staged as zeros: their (unused) logits stay finite
-  stage_rows<DT>(sQ, Qg, a.ld_in, [&](int row) { const int q = q0 + row; return q < L ? q : -1; });
-  __syncthreads();
-  if (tid == 0) {  // compact the list of chunks holding global keys outside the band
-    int m = 0;
-    for (int c = 0; c < nxc; ++c)
-      if (sXList[c]) sXList[m++] = c;
-    sNx = m;
-  }
-  __syncthreads();
-  const int ntile = nkt + sNx;
+  const int ntile = win_tables(a, wb, sBits, sXList, &sNx);
   auto gbit = [&](int k) -> bool {
     const int o = k - kt0;
     return (sBits[o >> 5] >> (o & 31)) & 1u;
   };
-  // source token of row `row` of tile t: band tiles first, then global-slot tiles
-  auto rowf = [&](int t, int row) -> int {
-    if (t < nkt) {
-      const int k = kt0 + t * kBK + row;
-      return k < kt1 ? k : -1;
-    }
-    const int j = kBK * sXList[t - nkt] + row;
-    const int p = j < G ? gp[j] : -1;
-    return (p >= 0 && p < L && (p < kt0 || p >= kt1)) ? p : -1;
-  };
+  WinLoader<DT> ld{a, wb, wb.nxc ? a.gpos + (long long)wb.b * a.G : nullptr, sXList};
 
-  // ---- pass 1: softmax + P.V for this wave's 16 queries
   Frag qf[TR::kChunks];
   TR::load_frags(sQ + (16 * w + lr) * P, g, qf);
   const int qa = q0 + 16 * w;
@@ -349,46 +367,48 @@ __global__ __launch_bounds__(kThreads) void k_window_attn(AttnArgs a) {
 #pragma unroll
   for (int dt = 0; dt < 4; ++dt) o[dt] = f32x4{0.f, 0.f, 0.f, 0.f};
 
-  Stage<DT> st;
-  int pos_reg = -1;
-  auto load = [&](int t, bool with_v) {
-    st.load_k(Kg, a.ld_in, [&](int row) { return rowf(t, row); });
-    if (with_v) st.load_v(Vg, a.ld_in, [&](int row) { return rowf(t, row); });
-    if (tid < kBK) pos_reg = rowf(t, tid);
-  };
-  auto store = [&](int buf, bool with_v) {
-    st.store_k(sK[buf]);
-    if (with_v) st.store_v(sV[buf]);
-    if (tid < kBK) sPos[buf][tid] = pos_reg;
-  };
-
-  load(0, true);
-  store(0, true);
+  // band tiles: double-buffered, the next tile's loads overlap this tile's math
+  ld.load(0, Kg, Vg);
+  ld.store(0, sK[0], sV[0], sPos[0]);
   __syncthreads();
-  for (int t = 0; t < ntile; ++t) {
+  for (int t = 0; t < nkt; ++t) {
     const int buf = t & 1;
-    if (t + 1 < ntile) load(t + 1, true);
-    if (t < nkt) {
-      const int k0 = kt0 + t * kBK;
-      const uint32_t gw = sBits[2 * t] | (2 * t + 1 < nwords ? sBits[2 * t + 1] : 0u);
-      const bool near = k0 <= qa + 15 + r && k0 + kBK - 1 >= qa - r;
-      if (near || gw != 0u) {
-        const bool interior = k0 + kBK <= kt1 && k0 >= qa + 15 - r && k0 + kBK - 1 <= qa + r;
-        if (interior) {
-          softmax_tile<DT, false>(qf, sK[buf], sV[buf], a.c2, lr, g, m_use, l_run, o, [](int, int) { return true; });
+    if (t + 1 < nkt) ld.load(t + 1, Kg, Vg);
+    const int k0 = kt0 + t * kBK;
+    const uint32_t gw = sBits[2 * t] | (2 * t + 1 < wb.nwords ? sBits[2 * t + 1] : 0u);
+    const bool near = k0 <= qa + 15 + r && k0 + kBK - 1 >= qa - r;
+    if (near || gw != 0u) {
+      const bool interior = k0 + kBK <= kt1 && k0 >= qa + 15 - r && k0 + kBK - 1 <= qa + r;
+      if (interior) {
+        softmax_tile<DT, false>(qf, sK[buf], sV[buf], a.c2, lr, g, m_use, l_run, o, [](int, int) { return true; });
+      } else {
+        // key index inside the tile: 16*st + 4g + i; allowed when it lies in
+        // [lo, hi] (window and sequence end) or is a global key of the band
+        const int lo = qrow - r - k0, hi = min(qrow + r, kt1 - 1) - k0;
+        if (gw == 0u) {
+          softmax_tile<DT, true>(qf, sK[buf], sV[buf], a.c2, lr, g, m_use, l_run, o, [&](int s4, int i) {
+            const int kk = 16 * s4 + 4 * g + i;
+            return kk >= lo && kk <= hi;
+          });
         } else {
           softmax_tile<DT, true>(qf, sK[buf], sV[buf], a.c2, lr, g, m_use, l_run, o, [&](int s4, int i) {
-            const int k = k0 + 16 * s4 + 4 * g + i;
-            return k < kt1 && (abs(qrow - k) <= r || gbit(k));
+            const int kk = 16 * s4 + 4 * g + i;
+            return (kk >= lo && kk <= hi) || (k0 + kk < kt1 && gbit(k0 + kk));
           });
         }
       }
-    } else {
-      const int* sp = sPos[buf];
-      softmax_tile<DT, true>(qf, sK[buf], sV[buf], a.c2, lr, g, m_use, l_run, o,
-                             [&](int s4, int i) { return sp[16 * s4 + 4 * g + i] >= 0; });
     }
-    if (t + 1 < ntile) store(buf ^ 1, true);
+    if (t + 1 < nkt) ld.store(t + 1, sK[buf ^ 1], sV[buf ^ 1], sPos[buf ^ 1]);
+    __syncthreads();
+  }
+  // global keys outside the band (few tiles; not pipelined)
+  for (int t = nkt; t < ntile; ++t) {
+    ld.load(t, Kg, Vg);
+    ld.store(t, sK[0], sV[0], sPos[0]);
+    __syncthreads();
+    const int* sp = sPos[0];
+    softmax_tile<DT, true>(qf, sK[0], sV[0], a.c2, lr, g, m_use, l_run, o,
+                           [&](int s4, int i) { return sp[16 * s4 + 4 * g + i] >= 0; });
     __syncthreads();
   }
 
@@ -403,76 +423,128 @@ __global__ __launch_bounds__(kThreads) void k_window_attn(AttnArgs a) {
     if (g == 0 && lseg) lseg[qrow] = lse2 * kLn2;
   } else if (!qin && qrow < n) {
 #pragma unroll
-    for (int dt = 0; dt < 4; ++dt) store_row4<DT>(Og + (long long)qrow * a.ld_out + 16 * dt + 4 * g, f32x4{0.f, 0.f, 0.f, 0.f});
+    for (int dt = 0; dt < 4; ++dt)
+      store_row4<DT>(Og + (long long)qrow * a.ld_out + 16 * dt + 4 * g, f32x4{0.f, 0.f, 0.f, 0.f});
     if (g == 0 && lseg) lseg[qrow] = -INFINITY;
   }
-  if (g == 0) sL2[16 * w + lr] = qvalid ? lse2 : INFINITY;
-  if (!a.part_band && !a.bp_band) return;  // uniform across the block
+  // excluded rows (global or padding) get +inf: their pass-2 probabilities are 0
+  if (g == 0 && l2g && qrow < n) l2g[qrow] = qvalid ? lse2 : INFINITY;
+}
 
-  // ---- pass 2: exact probabilities, column sums per key
-  load(0, false);
-  store(0, false);
-  __syncthreads();
+// Pass 2: exact probabilities of the block's non-global queries, summed per
+// key into the band and global-key partials (and written to the paper's band
+// layout when requested).  Wave w owns key sub-tile w of each staged tile.
+template <int DT, bool kBandProbs>
+__global__ __launch_bounds__(kThreads) SC_OCC(kBandProbs ? 2 : 4) void k_window_score(AttnArgs a) {
+  using TR = Tr<DT>;
+  using T = typename TR::T;
+  using Frag = typename TR::Frag;
+  constexpr int P = TR::kPitch;
+  __shared__ __attribute__((aligned(16))) T sQ[kBQ * P];
+  __shared__ __attribute__((aligned(16))) T sK[2][kBK * P];
+  __shared__ int sPos[2][kBK];
+  __shared__ int sNx;
+  extern __shared__ uint32_t sDyn[];
+
+  const WinBlock wb = win_block(a);
+  if (wb.q0 >= wb.L) return;  // the score reduction never reads padding blocks
+  const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6, g = lane >> 4, lr = lane & 15;
+  const int n = a.n, r = a.r, G = a.G, L = wb.L, q0 = wb.q0, kt0 = wb.kt0, kt1 = wb.kt1, nkt = wb.nkt;
+  const T* Qg = static_cast<const T*>(a.q) + wb.b * a.bs_in + wb.h * kHeadDim;
+  const T* Kg = static_cast<const T*>(a.k) + wb.b * a.bs_in + wb.h * kHeadDim;
+  const float* l2g = a.win_lse2 + (long long)wb.bh * n;
+  const int* gp = wb.nxc ? a.gpos + (long long)wb.b * G : nullptr;
+  uint32_t* sBits = sDyn;
+  int* sXList = reinterpret_cast<int*>(sDyn + a.rwp / 32 + 2);
+  {
+    Stage<DT> sq;
+    sq.load_range(Qg + (long long)q0 * a.ld_in, a.ld_in, 0, L - q0);
+    sq.store(sQ);
+  }
+  const int ntile = win_tables(a, wb, sBits, sXList, &sNx);
+  auto gbit = [&](int k) -> bool {
+    const int o = k - kt0;
+    return (sBits[o >> 5] >> (o & 31)) & 1u;
+  };
+  WinLoader<DT> ld{a, wb, gp, sXList};
+  ld.load(0, Kg, nullptr);
+  ld.store(0, sK[0], nullptr, sPos[0]);
+  // the block's log2-LSE go through LDS: values a loop consumes must not come
+  // from outstanding global loads (those would be waited for in every tile)
+  __shared__ float sL2[kBQ];
+  if (tid < kBQ) sL2[tid] = q0 + tid < L ? l2g[q0 + tid] : INFINITY;
+
   Frag qf2[4][TR::kChunks];
   float l2[4][4];
+  float* pb = a.part_band ? a.part_band + ((long long)wb.bh * a.nqb + wb.qb) * a.rwp : nullptr;
+  float* pe = a.part_band ? a.part_extra + ((long long)wb.bh * a.nqb + wb.qb) * G : nullptr;
+  float* bpb = kBandProbs ? a.bp_band + (long long)wb.bh * n * a.bw : nullptr;
+  float* bpc = kBandProbs ? a.bp_gcol + (long long)wb.bh * n * G : nullptr;
+  // global-key partials of slots never visited stay zero (written before the
+  // first barrier of the loop below, overwritten after it)
+  if (pe)
+    for (int j = tid; j < G; j += kThreads) pe[j] = 0.f;
+  __syncthreads();
 #pragma unroll
   for (int qst = 0; qst < 4; ++qst) {
     TR::load_frags(sQ + (16 * qst + lr) * P, g, qf2[qst]);
 #pragma unroll
     for (int i = 0; i < 4; ++i) l2[qst][i] = sL2[16 * qst + 4 * g + i];
   }
-  float* pb = a.part_band ? a.part_band + ((long long)bh * a.nqb + qb) * a.rwp : nullptr;
-  float* pe = a.part_band ? a.part_extra + ((long long)bh * a.nqb + qb) * G : nullptr;
-  float* bpb = a.bp_band ? a.bp_band + (long long)bh * n * a.bw : nullptr;
-  float* bpc = a.bp_band ? a.bp_gcol + (long long)bh * n * G : nullptr;
-  // global-key partials of slots never visited stay zero
-  if (pe)
-    for (int j = tid; j < G; j += kThreads) pe[j] = 0.f;
 
-  for (int t = 0; t < ntile; ++t) {
+  for (int t = 0; t < nkt; ++t) {
     const int buf = t & 1;
-    if (t + 1 < ntile) load(t + 1, false);
+    if (t + 1 < nkt) ld.load(t + 1, Kg, nullptr);
+    const int k0 = kt0 + t * kBK;
+    const int key = k0 + 16 * w + lr;
+    const bool kin = key < kt1;
+    const bool kglob = kin && gbit(key);
+    // query index inside the block: 16*qst + 4g + i; allowed within
+    // [key - r - q0, key + r - q0] or when the key is global
+    const int lo = key - r - q0, hi = key + r - q0;
+    auto ok = [&](int qst, int i) {
+      const int qq = 16 * qst + 4 * g + i;
+      return kin && (kglob || (qq >= lo && qq <= hi));
+    };
     float cs;
-    if (t < nkt) {
-      const int k0 = kt0 + t * kBK;
-      const int key = k0 + 16 * w + lr;
-      auto ok = [&](int qst, int i) {
+    if constexpr (kBandProbs) {
+      const int kslot = kglob ? find_slot(gp, G, key) : -1;
+      cs = score_tile<DT, true>(qf2, l2, sK[buf], w, a.c2, lr, g, ok, [&](int qst, int i, float p) {
         const int q = q0 + 16 * qst + 4 * g + i;
-        return key < kt1 && (abs(q - key) <= r || gbit(key));
-      };
-      if (bpb) {
-        const bool kglob = key < kt1 && gbit(key);
-        const int kslot = kglob ? find_slot(gp, G, key) : -1;
-        cs = score_tile<DT, true>(qf2, l2, sK[buf], w, a.c2, lr, g, ok, [&](int qst, int i, float p) {
-          const int q = q0 + 16 * qst + 4 * g + i;
-          if (!(q < L) || key >= kt1 || p == 0.f) return;
-          if (kglob) {
-            if (kslot >= 0) bpc[(long long)q * G + kslot] = p;
-          } else if (abs(q - key) <= a.rb) {
-            bpb[(long long)q * a.bw + (key - q + a.rb)] = p;
-          }
-        });
-      } else {
-        const bool interior = k0 + kBK <= kt1 && k0 >= q0 + kBQ - 1 - r && k0 + kBK - 1 <= q0 + r;
-        cs = interior ? score_tile<DT, false>(qf2, l2, sK[buf], w, a.c2, lr, g, ok, NoEmit{})
-                      : score_tile<DT, true>(qf2, l2, sK[buf], w, a.c2, lr, g, ok, NoEmit{});
-      }
-      if (pb && g == 0 && key < kt1) pb[key - kt0] = cs;
+        if (!(q < L) || !kin || p == 0.f) return;
+        if (kglob) {
+          if (kslot >= 0) bpc[(long long)q * G + kslot] = p;
+        } else if (abs(q - key) <= a.rb) {
+          bpb[(long long)q * a.bw + (key - q + a.rb)] = p;
+        }
+      });
     } else {
-      const int slot = kBK * sXList[t - nkt] + 16 * w + lr;
-      const bool kvalid = sPos[buf][16 * w + lr] >= 0;
-      auto ok = [&](int, int) { return kvalid; };
-      if (bpc) {
-        cs = score_tile<DT, true>(qf2, l2, sK[buf], w, a.c2, lr, g, ok, [&](int qst, int i, float p) {
-          const int q = q0 + 16 * qst + 4 * g + i;
-          if (kvalid && q < L && p != 0.f) bpc[(long long)q * G + slot] = p;
-        });
-      } else {
-        cs = score_tile<DT, true>(qf2, l2, sK[buf], w, a.c2, lr, g, ok, NoEmit{});
-      }
-      if (pe && g == 0 && slot < G) pe[slot] = cs;
+      const bool interior = k0 + kBK <= kt1 && k0 >= q0 + kBQ - 1 - r && k0 + kBK - 1 <= q0 + r;
+      cs = interior ? score_tile<DT, false>(qf2, l2, sK[buf], w, a.c2, lr, g, ok, NoEmit{})
+                    : score_tile<DT, true>(qf2, l2, sK[buf], w, a.c2, lr, g, ok, NoEmit{});
     }
-    if (t + 1 < ntile) store(buf ^ 1, false);
+    if (pb && g == 0 && kin) pb[key - kt0] = cs;
+    if (t + 1 < nkt) ld.store(t + 1, sK[buf ^ 1], nullptr, sPos[buf ^ 1]);
+    __syncthreads();
+  }
+  // global keys outside the band
+  for (int t = nkt; t < ntile; ++t) {
+    ld.load(t, Kg, nullptr);
+    ld.store(t, sK[0], nullptr, sPos[0]);
+    __syncthreads();
+    const int slot = kBK * sXList[t - nkt] + 16 * w + lr;
+    const bool kvalid = sPos[0][16 * w + lr] >= 0;
+    auto ok = [&](int, int) { return kvalid; };
+    float cs;
+    if constexpr (kBandProbs) {
+      cs = score_tile<DT, true>(qf2, l2, sK[0], w, a.c2, lr, g, ok, [&](int qst, int i, float p) {
+        const int q = q0 + 16 * qst + 4 * g + i;
+        if (kvalid && q < L && p != 0.f) bpc[(long long)q * G + slot] = p;
+      });
+    } else {
+      cs = score_tile<DT, true>(qf2, l2, sK[0], w, a.c2, lr, g, ok, NoEmit{});
+    }
+    if (pe && g == 0 && slot < G) pe[slot] = cs;
     __syncthreads();
   }
 }
@@ -524,16 +596,16 @@ __global__ __launch_bounds__(kThreads) void k_global_rows_fwd(AttnArgs a) {
   const T* Kg = static_cast<const T*>(a.k) + blk.b * a.bs_in + blk.h * kHeadDim;
   const T* Vg = static_cast<const T*>(a.v) + blk.b * a.bs_in + blk.h * kHeadDim;
   const int ntile = (kend - kbeg + kBK - 1) / kBK;
-  auto rowf = [&](int t, int row) { const int k = kbeg + t * kBK + row; return k < kend ? k : -1; };
-  Stage<DT> st;
-  auto load = [&](int t) {
-    st.load_k(Kg, a.ld_in, [&](int row) { return rowf(t, row); });
-    st.load_v(Vg, a.ld_in, [&](int row) { return rowf(t, row); });
-  };
-  stage_rows<DT>(sQ, Qg, a.ld_in, [&](int row) { return sPos[row]; });
-  load(0);
-  st.store_k(sK[0]);
-  st.store_v(sV[0]);
+  Stage<DT> stk, stv;
+  {
+    Stage<DT> sq;
+    sq.load_rows(Qg, a.ld_in, [&](int row) { return sPos[row]; });
+    sq.store(sQ);
+  }
+  stk.load_range(Kg, a.ld_in, kbeg, kend);
+  stv.load_range(Vg, a.ld_in, kbeg, kend);
+  stk.store(sK[0]);
+  stv.store(sV[0]);
   __syncthreads();
   typename TR::Frag qf[TR::kChunks];
   TR::load_frags(sQ + (16 * w + lr) * P, g, qf);
@@ -543,15 +615,20 @@ __global__ __launch_bounds__(kThreads) void k_global_rows_fwd(AttnArgs a) {
   for (int dt = 0; dt < 4; ++dt) o[dt] = f32x4{0.f, 0.f, 0.f, 0.f};
   for (int t = 0; t < ntile; ++t) {
     const int buf = t & 1, k0 = kbeg + t * kBK;
-    if (t + 1 < ntile) load(t + 1);
-    if (k0 + kBK <= kend)
-      softmax_tile<DT, false>(qf, sK[buf], sV[buf], a.c2, lr, g, m_use, l_run, o, [](int, int) { return true; });
-    else
-      softmax_tile<DT, true>(qf, sK[buf], sV[buf], a.c2, lr, g, m_use, l_run, o,
-                             [&](int s4, int i) { return k0 + 16 * s4 + 4 * g + i < kend; });
     if (t + 1 < ntile) {
-      st.store_k(sK[buf ^ 1]);
-      st.store_v(sV[buf ^ 1]);
+      stk.load_range(Kg, a.ld_in, k0 + kBK, kend);
+      stv.load_range(Vg, a.ld_in, k0 + kBK, kend);
+    }
+    if (k0 + kBK <= kend) {
+      softmax_tile<DT, false>(qf, sK[buf], sV[buf], a.c2, lr, g, m_use, l_run, o, [](int, int) { return true; });
+    } else {
+      const int hi = kend - 1 - k0;
+      softmax_tile<DT, true>(qf, sK[buf], sV[buf], a.c2, lr, g, m_use, l_run, o,
+                             [&](int s4, int i) { return 16 * s4 + 4 * g + i <= hi; });
+    }
+    if (t + 1 < ntile) {
+      stk.store(sK[buf ^ 1]);
+      stv.store(sV[buf ^ 1]);
     }
     __syncthreads();
   }
@@ -633,13 +710,14 @@ __global__ __launch_bounds__(kThreads) void k_global_rows_score(AttnArgs a) {
   const T* Qg = static_cast<const T*>(a.q) + blk.b * a.bs_in + blk.h * kHeadDim;
   const T* Kg = static_cast<const T*>(a.k) + blk.b * a.bs_in + blk.h * kHeadDim;
   const int ntile = (kend - kbeg + kBK - 1) / kBK;
-  Stage<DT> st;
-  auto load = [&](int t) {
-    st.load_k(Kg, a.ld_in, [&](int row) { const int k = kbeg + t * kBK + row; return k < kend ? k : -1; });
-  };
-  stage_rows<DT>(sQ, Qg, a.ld_in, [&](int row) { return sPos[row]; });
-  load(0);
-  st.store_k(sK[0]);
+  Stage<DT> stk;
+  {
+    Stage<DT> sq;
+    sq.load_rows(Qg, a.ld_in, [&](int row) { return sPos[row]; });
+    sq.store(sQ);
+  }
+  stk.load_range(Kg, a.ld_in, kbeg, kend);
+  stk.store(sK[0]);
   __syncthreads();
   typename TR::Frag qf[4][TR::kChunks];
   float l2[4][4];
@@ -651,21 +729,22 @@ __global__ __launch_bounds__(kThreads) void k_global_rows_score(AttnArgs a) {
       l2[qst][i] = a.gr_lse2[(long long)blk.bh * a.Gp + kGlobalChunk * blk.gc + 16 * qst + 4 * g + i];
   }
   for (int t = 0; t < ntile; ++t) {
-    const int buf = t & 1;
-    if (t + 1 < ntile) load(t + 1);
-    const int key = kbeg + t * kBK + 16 * w + lr;
-    auto ok = [&](int, int) { return key < kend; };
+    const int buf = t & 1, k0 = kbeg + t * kBK;
+    if (t + 1 < ntile) stk.load_range(Kg, a.ld_in, k0 + kBK, kend);
+    const int key = k0 + 16 * w + lr;
+    const bool kin = key < kend;
+    auto ok = [&](int, int) { return kin; };
     float cs;
     if (bpr) {
       cs = score_tile<DT, true>(qf, l2, sK[buf], w, a.c2, lr, g, ok, [&](int qst, int i, float p) {
         const int slot = kGlobalChunk * blk.gc + 16 * qst + 4 * g + i;
-        if (key < kend && slot < a.G && p != 0.f) bpr[(long long)slot * a.n + key] = p;
+        if (kin && slot < a.G && p != 0.f) bpr[(long long)slot * a.n + key] = p;
       });
     } else {
       cs = score_tile<DT, true>(qf, l2, sK[buf], w, a.c2, lr, g, ok, NoEmit{});
     }
-    if (pg && g == 0 && key < kend) pg[key] = cs;
-    if (t + 1 < ntile) st.store_k(sK[buf ^ 1]);
+    if (pg && g == 0 && kin) pg[key] = cs;
+    if (t + 1 < ntile) stk.store(sK[buf ^ 1]);
     __syncthreads();
   }
 }
@@ -793,12 +872,6 @@ size_t band_probs_floats(int B, int H, int n, const AttnGeom& g, int G) {
   return (size_t)B * H * n * ((size_t)g.bw + 2 * (size_t)G);
 }
 
-size_t attn_workspace_bytes(int B, int H, const AttnGeom& g) {
-  if (g.Gp == 0) return 0;
-  const size_t per = (size_t)B * H * g.Gp;
-  return sizeof(float) * (per * g.nkc * (2 + kHeadDim) + per);
-}
-
 // ------------------------------------------------- benchmark kernel timing
 namespace {
 constexpr int kMaxProfiled = 4096;
@@ -854,8 +927,13 @@ static hipError_t launch_window_t(const AttnArgs& a, hipStream_t s) {
   }
   const int nxc = a.G > 0 && a.gpos ? (a.G + kBK - 1) / kBK : 0;
   const size_t dyn = sizeof(uint32_t) * ((size_t)a.rwp / 32 + 2 + nxc + 1);
+  const unsigned blocks = (unsigned)(a.nqb * a.H * a.B);
   profile_begin(s);
-  hipLaunchKernelGGL(k_window_attn<DT>, dim3((unsigned)(a.nqb * a.H * a.B)), dim3(kThreads), dyn, s, a);
+  hipLaunchKernelGGL(k_window_attn<DT>, dim3(blocks), dim3(kThreads), dyn, s, a);
+  if (a.bp_band)
+    hipLaunchKernelGGL((k_window_score<DT, true>), dim3(blocks), dim3(kThreads), dyn, s, a);
+  else if (a.part_band)
+    hipLaunchKernelGGL((k_window_score<DT, false>), dim3(blocks), dim3(kThreads), dyn, s, a);
   profile_end(s);
   if (a.G > 0 && a.gpos && (a.part_grow || a.bp_grow)) {
     const unsigned grid = (unsigned)(a.nkc * a.ngc * a.H * a.B);

@@ -25,20 +25,47 @@ constexpr float kLn2 = 0.6931471805599453f;
 SC_DEV float fast_exp2(float x) { return __builtin_amdgcn_exp2f(x); }
 SC_DEV float fast_log2(float x) { return __builtin_amdgcn_logf(x); }
 
-SC_DEV float shfl_xor(float v, int m) { return __shfl_xor(v, m, 64); }
-SC_DEV float shfl(float v, int src) { return __shfl(v, src, 64); }
-
-// Sum over the four lane groups (lanes lr, lr+16, lr+32, lr+48); every lane
-// gets the same result, added in the same order.
-SC_DEV float group_sum(float v) {
-  v += shfl_xor(v, 16);
-  v += shfl_xor(v, 32);
-  return v;
+// Cross-row exchanges on the VALU (gfx950 v_permlane16/32_swap).  With both
+// operands equal to v, permlane16_swap returns (rows 0,0,2,2 ; rows 1,1,3,3)
+// of v and permlane32_swap returns (low half twice ; high half twice), so the
+// sum of the two results is the all-reduce over lanes l and l^16 (resp. l^32),
+// computed in the same order in every lane.
+SC_DEV float xor16_sum(float v) {
+  const unsigned u = __builtin_bit_cast(unsigned, v);
+  const auto r = __builtin_amdgcn_permlane16_swap(u, u, false, false);
+  return __builtin_bit_cast(float, (unsigned)r[0]) + __builtin_bit_cast(float, (unsigned)r[1]);
 }
-SC_DEV float group_max(float v) {
-  v = fmaxf(v, shfl_xor(v, 16));
-  v = fmaxf(v, shfl_xor(v, 32));
-  return v;
+SC_DEV float xor32_sum(float v) {
+  const unsigned u = __builtin_bit_cast(unsigned, v);
+  const auto r = __builtin_amdgcn_permlane32_swap(u, u, false, false);
+  return __builtin_bit_cast(float, (unsigned)r[0]) + __builtin_bit_cast(float, (unsigned)r[1]);
+}
+SC_DEV float xor16_max(float v) {
+  const unsigned u = __builtin_bit_cast(unsigned, v);
+  const auto r = __builtin_amdgcn_permlane16_swap(u, u, false, false);
+  return fmaxf(__builtin_bit_cast(float, (unsigned)r[0]), __builtin_bit_cast(float, (unsigned)r[1]));
+}
+SC_DEV float xor32_max(float v) {
+  const unsigned u = __builtin_bit_cast(unsigned, v);
+  const auto r = __builtin_amdgcn_permlane32_swap(u, u, false, false);
+  return fmaxf(__builtin_bit_cast(float, (unsigned)r[0]), __builtin_bit_cast(float, (unsigned)r[1]));
+}
+
+// Sum / max over the four lane groups (lanes lr, lr+16, lr+32, lr+48); every
+// lane gets the same result, combined in the same order.
+SC_DEV float group_sum(float v) { return xor32_sum(xor16_sum(v)); }
+SC_DEV float group_max(float v) { return xor32_max(xor16_max(v)); }
+
+typedef __attribute__((ext_vector_type(4))) short i16x4;
+typedef __attribute__((ext_vector_type(8))) short i16x8;
+
+// gfx950 LDS transpose read (ds_read_tr16_b64): every lane supplies the
+// address of 4 consecutive 16-bit elements; within each group of 16 lanes,
+// lane j receives element j % 4 of the blocks read by lanes j/4, 4 + j/4,
+// 8 + j/4 and 12 + j/4 (in that order).
+SC_DEV i16x4 lds_read_tr16(const void* p) {
+  return __builtin_amdgcn_ds_read_tr16_b64_v4i16(
+      (__attribute__((address_space(3))) i16x4*)(const_cast<void*>(p)));
 }
 
 // Workgroups are dispatched round-robin over the 8 XCDs (each with its own L2).

@@ -34,6 +34,7 @@ struct AttnArgs {
   float* gr_ml;           // [B, H, nkc, Gp, 2]
   float* gr_o;            // [B, H, nkc, Gp, 64]
   float* gr_lse2;         // [B, H, Gp]
+  float* win_lse2;        // [B, H, n] log2-LSE of the window rows (+inf: excluded)
   // paper band layout (null unless requested)
   float* bp_band;         // [B, H, n, bw]
   float* bp_gcol;         // [B, H, n, G]
@@ -48,7 +49,6 @@ struct AttnGeom {
 AttnGeom attn_geom(int n, int window, int G);
 size_t partials_floats(int B, int H, int n, const AttnGeom& g, int G);
 size_t band_probs_floats(int B, int H, int n, const AttnGeom& g, int G);
-size_t attn_workspace_bytes(int B, int H, const AttnGeom& g);
 
 hipError_t launch_window_attention(int dtype, const AttnArgs& a, hipStream_t s);
 // benchmark timing of the window-attention kernel (events on the launch stream)

@@ -71,6 +71,7 @@ def test_invalid_descriptors_rejected_before_launch():
     assert call_attn(desc(dtype=7)) == B.SC_EINVAL
     assert call_attn(desc(softmax_scale=float("nan"))) == B.SC_EINVAL
     assert call_attn(desc(softmax_scale=float("inf"))) == B.SC_EINVAL
+    assert call_attn(desc(softmax_scale=-0.125)) == B.SC_EINVAL
     assert call_attn(desc(valid_len=None)) == B.SC_EINVAL
     # G > 0 needs global positions, and G may not exceed n
     assert call_attn(desc(G=3)) == B.SC_EINVAL
@@ -92,7 +93,8 @@ def test_workspace_checked():
     assert need > 0
     assert call_attn(d, ws=None, ws_bytes=0) == B.SC_EWORKSPACE
     assert call_attn(d, ws=0x900000, ws_bytes=need - 1) == B.SC_EWORKSPACE
-    assert sc.sc_window_attention_workspace_size(desc()) == 0  # no global tokens: no split partials
+    # without global tokens only the per-row log2-LSE handed from pass 1 to pass 2 remains
+    assert sc.sc_window_attention_workspace_size(desc()) == 4 * 2 * 4 * 256
 
 
 def test_sizes():
