@@ -7,12 +7,12 @@
  *
  *   sc_window_attention   banded Q.K^T, masked softmax and P.V for the sliding
  *                         window (Sec. 4.2.1, Fig. 4) plus the global tokens'
- *                         dense rows and columns (Sec. 3.1 "Global attention",
+ *                         dense rows and columns (Sec. 3.2.1 "Global attention",
  *                         Fig. 3b-c; Sec. 5.5), and the per-query partial sums
  *                         of the attention probabilities each key receives;
  *   sc_ltp_score          the importance score of every token: probabilities
  *                         accumulated down its column after the row softmax
- *                         (Sec. 1, Fig. 1 caption; Sec. 3.2), i.e. the sum over
+ *                         (Sec. 1, Fig. 1 caption; Sec. 3.3), i.e. the sum over
  *                         the band's sub-diagonal plus the global strips
  *                         (Sec. 5.5), averaged over heads and valid queries;
  *   sc_ltp_prune_compact  the binarised mask (keep iff score > threshold,
@@ -115,7 +115,7 @@ size_t sc_band_probs_size(const sc_attn_desc *desc);
 size_t sc_window_attention_workspace_size(const sc_attn_desc *desc);
 
 /*
- * Sliding-window + global sparse attention of one layer (Sec. 4.2.1, Sec. 3.1,
+ * Sliding-window + global sparse attention of one layer (Sec. 4.2.1, Sec. 3.2.1,
  * Sec. 5.5): for every valid query i of sequence b and head h,
  *   N(i) = { j < L : |i - j| <= r  or  i global  or  j global },  r = floor(w/2)
  *   out[b,i,h,:] = sum_{j in N(i)} softmax_j(alpha * q_i . k_j) * v_j
@@ -138,7 +138,7 @@ sc_status sc_window_attention(const sc_attn_desc *desc, const void *q, const voi
 size_t sc_ltp_score_workspace_size(const sc_attn_desc *desc, int32_t mode);
 
 /*
- * Importance score of every token (Sec. 1 Fig. 1; Sec. 3.2; Sec. 5.5):
+ * Importance score of every token (Sec. 1 Fig. 1; Sec. 3.3; Sec. 5.5):
  *   scores[b,k] = 1/(H * L_b) * sum_h sum_{i < L_b} P_h[i][k]   for k < L_b,
  *   scores[b,k] = 0                                              for k >= L_b,
  * so the scores of one sequence sum to one.  Deterministic: fixed-order sums,

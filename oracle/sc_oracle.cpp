@@ -10,10 +10,10 @@
 // Sources (SparseCoder, arXiv 2310.07109):
 //   * sliding-window local attention: token i attends to its neighbours within
 //     the window (Sec. 4.2.1, Fig. 4); global ("special") tokens attend to every
-//     token and are attended to by every token (Sec. 3.1, Fig. 3b-c; Sec. 5.5);
+//     token and are attended to by every token (Sec. 3.2.1 "Global attention", Fig. 3b-c; Sec. 5.5);
 //   * importance score of a token: attention probabilities accumulated down the
 //     token's column after the row-wise softmax (Sec. 1, Fig. 1 caption;
-//     Sec. 3.2), for sparse attention the band's sub-diagonal plus the global
+//     Sec. 3.3), for sparse attention the band's sub-diagonal plus the global
 //     rows and columns (Sec. 5.5); normalised here to the mean over heads and
 //     valid queries;
 //   * binarised mask: keep iff score > layer threshold, strictly (Sec. 4.2.2,

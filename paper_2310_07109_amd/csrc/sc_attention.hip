@@ -1,6 +1,6 @@
 // Sliding-window + global-token sparse attention with exact importance-score
 // partials, for gfx950 (SparseCoder, arXiv 2310.07109: Sec. 4.2.1 window,
-// Sec. 3.1 global tokens, Sec. 5.5 score extraction).
+// Sec. 3.2.1 global tokens, Sec. 5.5 score extraction).
 //
 // Decomposition of the allowed (query i, key j) pairs of one sequence, both
 // valid, into three disjoint regions:
@@ -246,6 +246,13 @@ SC_DEV WinBlock win_block(const AttnArgs& a) {
   return wb;
 }
 
+// Global keys of band tile t as a 64-bit mask (bit j: key kt0 + 64t + j).
+SC_DEV unsigned long long tile_gmask(const uint32_t* sBits, int t, int nwords) {
+  const unsigned long long lo = sBits[2 * t];
+  const unsigned long long hi = 2 * t + 1 < nwords ? sBits[2 * t + 1] : 0u;
+  return lo | (hi << 32);
+}
+
 // Fills the bitmask and the chunk list; returns the number of tiles (band
 // tiles, then global-slot tiles).  Contains barriers; call with q0 < L.
 SC_DEV int win_tables(const AttnArgs& a, const WinBlock& wb, uint32_t* sBits, int* sXList, int* sNx) {
@@ -375,27 +382,22 @@ __global__ __launch_bounds__(kThreads) SC_OCC(3) void k_window_attn(AttnArgs a) 
     const int buf = t & 1;
     if (t + 1 < nkt) ld.load(t + 1, Kg, Vg);
     const int k0 = kt0 + t * kBK;
-    const uint32_t gw = sBits[2 * t] | (2 * t + 1 < wb.nwords ? sBits[2 * t + 1] : 0u);
     const bool near = k0 <= qa + 15 + r && k0 + kBK - 1 >= qa - r;
-    if (near || gw != 0u) {
+    if (near || tile_gmask(sBits, t, wb.nwords) != 0ull) {
       const bool interior = k0 + kBK <= kt1 && k0 >= qa + 15 - r && k0 + kBK - 1 <= qa + r;
       if (interior) {
         softmax_tile<DT, false>(qf, sK[buf], sV[buf], a.c2, lr, g, m_use, l_run, o, [](int, int) { return true; });
       } else {
         // key index inside the tile: 16*st + 4g + i; allowed when it lies in
-        // [lo, hi] (window and sequence end) or is a global key of the band
+        // [lo, hi] (window and sequence end) or is a global key of the band.
+        // Branch-free: the tile's global keys come as one 64-bit mask (bits
+        // beyond kt1 are never set).
         const int lo = qrow - r - k0, hi = min(qrow + r, kt1 - 1) - k0;
-        if (gw == 0u) {
-          softmax_tile<DT, true>(qf, sK[buf], sV[buf], a.c2, lr, g, m_use, l_run, o, [&](int s4, int i) {
-            const int kk = 16 * s4 + 4 * g + i;
-            return kk >= lo && kk <= hi;
-          });
-        } else {
-          softmax_tile<DT, true>(qf, sK[buf], sV[buf], a.c2, lr, g, m_use, l_run, o, [&](int s4, int i) {
-            const int kk = 16 * s4 + 4 * g + i;
-            return (kk >= lo && kk <= hi) || (k0 + kk < kt1 && gbit(k0 + kk));
-          });
-        }
+        const unsigned long long gm = tile_gmask(sBits, t, wb.nwords) >> (4 * g);
+        softmax_tile<DT, true>(qf, sK[buf], sV[buf], a.c2, lr, g, m_use, l_run, o, [&](int s4, int i) {
+          const int kk = 16 * s4 + 4 * g + i;
+          return ((kk >= lo) & (kk <= hi)) | (bool)((gm >> (16 * s4 + i)) & 1ull);
+        });
       }
     }
     if (t + 1 < nkt) ld.store(t + 1, sK[buf ^ 1], sV[buf ^ 1], sPos[buf ^ 1]);
@@ -504,7 +506,7 @@ __global__ __launch_bounds__(kThreads) SC_OCC(kBandProbs ? 2 : 4) void k_window_
     const int lo = key - r - q0, hi = key + r - q0;
     auto ok = [&](int qst, int i) {
       const int qq = 16 * qst + 4 * g + i;
-      return kin && (kglob || (qq >= lo && qq <= hi));
+      return kin & (kglob | ((qq >= lo) & (qq <= hi)));
     };
     float cs;
     if constexpr (kBandProbs) {
