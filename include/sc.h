@@ -95,9 +95,9 @@ const char *sc_status_str(sc_status s);
 
 /* Bytes of the score partials written by sc_window_attention and read by
  * sc_ltp_score(SC_SCORE_FROM_PARTIALS); 0 on an invalid descriptor.  The layout
- * is private to the library: per (sequence, head, 64-query block) sums of the
- * probabilities that block's queries give each key of its band and each
- * global key, plus per (sequence, head) sums over the global queries. */
+ * is private to the library: per (sequence, head) the band column sums of the
+ * non-global keys, the column sums of the global keys per 512-query range, and
+ * the column sums over the global query rows. */
 size_t sc_score_partials_size(const sc_attn_desc *desc);
 
 /* Bytes of the band-stored probabilities (paper layout, Sec. 5.5 / Fig. 3d),

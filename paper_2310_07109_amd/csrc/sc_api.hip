@@ -74,6 +74,8 @@ AttnArgs make_attn_args(const sc_attn_desc* d, const AttnGeom& geo) {
   a.Gp = geo.Gp;
   a.bw = geo.bw;
   a.rb = geo.rb;
+  a.nkb = geo.nkb;
+  a.nqr = geo.nqr;
   return a;
 }
 
@@ -88,8 +90,8 @@ void carve_attn_ws(AttnArgs& a, Carver& c) {
 
 void set_partials(AttnArgs& a, float* sp) {
   a.part_band = sp;
-  a.part_extra = sp ? sp + (size_t)a.B * a.H * a.nqb * a.rwp : nullptr;
-  a.part_grow = sp ? a.part_extra + (size_t)a.B * a.H * a.nqb * a.G : nullptr;
+  a.part_extra = sp ? sp + (size_t)a.B * a.H * a.n : nullptr;
+  a.part_grow = sp ? a.part_extra + (size_t)a.B * a.H * a.nqr * a.G : nullptr;
 }
 
 size_t attn_ws_size(const sc_attn_desc* d) {

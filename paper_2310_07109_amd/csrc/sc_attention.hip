@@ -161,36 +161,39 @@ SC_DEV void softmax_tile(const typename Tr<DT>::Frag (&qf)[Tr<DT>::kChunks], con
   }
 }
 
-// ------------------------------------------------------------ pass 2 tile ---
-// Column sums of exact probabilities for the 16 keys of sub-tile `w` of the
-// staged tile over the 64 queries of the block.  Result register (qst, i) of
-// the MFMA is (query 16*qst + 4g + i, key lr).  ok(qst, i) masks pairs;
-// emit(qst, i, p) sees every probability (used for the band layout).
+// ------------------------------------------------------------ column tile ---
+// Exact probabilities of the 64 staged queries (rows of sQ, log2-LSE in sL)
+// for the 16 keys held in kf, summed per key into this lane's partial.  MFMA
+// result register (qst, i) is (query 16*qst + 4g + i, key lr), so the sum over
+// queries stays inside the lane; the 4 lane groups are combined once, by the
+// caller, after the last tile.  ok(qst, i) masks pairs; emit(q, p) sees every
+// probability (used for the paper's band layout).
 template <int DT, bool kMasked, typename OkFn, typename EmitFn>
-SC_DEV float score_tile(const typename Tr<DT>::Frag (&qf)[4][Tr<DT>::kChunks], const float (&l2)[4][4],
-                        const typename Tr<DT>::T* sK, int w, float c2, int lr, int g, OkFn ok, EmitFn emit) {
+SC_DEV float col_tile(const typename Tr<DT>::Frag (&kf)[Tr<DT>::kChunks], const typename Tr<DT>::T* sQ,
+                      const float* sL, float c2, int lr, int g, OkFn ok, EmitFn emit) {
   using TR = Tr<DT>;
-  typename TR::Frag kf[TR::kChunks];
-  TR::load_frags(sK + (16 * w + lr) * TR::kPitch, g, kf);
   float cs = 0.f;
 #pragma unroll
   for (int qst = 0; qst < 4; ++qst) {
+    typename TR::Frag qf[TR::kChunks];
+    TR::load_frags(sQ + (16 * qst + lr) * TR::kPitch, g, qf);
+    const f32x4 l2 = *reinterpret_cast<const f32x4*>(sL + 16 * qst + 4 * g);
     f32x4 acc = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
-    for (int c = 0; c < TR::kChunks; ++c) acc = TR::mma(qf[qst][c], kf[c], acc);
+    for (int c = 0; c < TR::kChunks; ++c) acc = TR::mma(qf[c], kf[c], acc);
 #pragma unroll
     for (int i = 0; i < 4; ++i) {
-      float p = fast_exp2(fmaf(acc[i], c2, -l2[qst][i]));
+      float p = fast_exp2(fmaf(acc[i], c2, -l2[i]));
       if (kMasked && !ok(qst, i)) p = 0.f;
-      emit(qst, i, p);
+      emit(16 * qst + 4 * g + i, p);
       cs += p;
     }
   }
-  return group_sum(cs);
+  return cs;
 }
 
 struct NoEmit {
-  SC_DEV void operator()(int, int, float) const {}
+  SC_DEV void operator()(int, float) const {}
 };
 
 template <int DT>
@@ -207,30 +210,35 @@ SC_DEV void store_row4(typename Tr<DT>::T* dst, f32x4 v) {
   }
 }
 
-// Slot of global key `key` of sequence row gp[0..G) (ascending), or -1.
-SC_DEV int find_slot(const int* gp, int G, int key) {
-  int lo = 0, hi = G - 1;
-  while (lo <= hi) {
-    const int mid = (lo + hi) >> 1;
-    const int p = gp[mid];
-    if (p == key) return mid;
-    if (p >= 0 && p < key) lo = mid + 1;
-    else hi = mid - 1;
-  }
-  return -1;
-}
+// LDS shared by all block types of a launch (each block type uses its own
+// subset; pointers are handed to the per-type device functions).
+template <int DT, bool kWithV>
+struct SmemT {
+  using T = typename Tr<DT>::T;
+  static constexpr int P = Tr<DT>::kPitch;
+  __attribute__((aligned(16))) T a[kBQ * P];     // query tile (pass 1, global rows) / key block (columns)
+  __attribute__((aligned(16))) T b[2][kBK * P];  // key tiles (pass 1, global rows) / query tiles (columns)
+  __attribute__((aligned(16))) T c[kWithV ? 2 : 1][kWithV ? kBK * P : 8];  // value tiles (pass 1)
+  __attribute__((aligned(16))) float l[2][kBQ];  // log2-LSE of staged query rows
+  int pos[2][kBK];                                 // positions of gathered rows
+  int misc[4];
+};
+template <int DT>
+using Smem = SmemT<DT, true>;      // launch 1 (softmax and P.V need V tiles)
+template <int DT>
+using SmemCol = SmemT<DT, false>;  // launch 2 (column sums need no V)
 
-// ------------------------------------------------------- window kernels -----
+// -------------------------------------------------------- window pass 1 -----
 // Geometry of one window block (sequence b, head h, queries q0 .. q0+63) and
 // its LDS tables: the global-token bitmask over the key range [kt0, kt1) and
 // the list of 64-slot chunks that hold global keys outside that range.
 struct WinBlock {
-  int qb, bh, h, b, L, q0, kt0, kt1, nkt, nwords, nxc, ntile;
+  int qb, bh, h, b, L, q0, kt0, kt1, nkt, nwords, nxc;
 };
 
-SC_DEV WinBlock win_block(const AttnArgs& a) {
+SC_DEV WinBlock win_block(const AttnArgs& a, int blk) {
   WinBlock wb;
-  const int lin = xcd_remap(blockIdx.x, a.nqb * a.H * a.B);
+  const int lin = xcd_remap(blk, a.nqb * a.H * a.B);
   wb.qb = lin % a.nqb;
   wb.bh = lin / a.nqb;
   wb.h = wb.bh % a.H;
@@ -242,7 +250,6 @@ SC_DEV WinBlock win_block(const AttnArgs& a) {
   wb.nkt = (wb.kt1 - wb.kt0 + kBK - 1) / kBK;
   wb.nwords = (wb.kt1 - wb.kt0 + 31) >> 5;
   wb.nxc = (a.gpos && a.G > 0) ? (a.G + kBK - 1) / kBK : 0;
-  wb.ntile = wb.nkt;
   return wb;
 }
 
@@ -279,8 +286,8 @@ SC_DEV int win_tables(const AttnArgs& a, const WinBlock& wb, uint32_t* sBits, in
   return wb.nkt + *sNx;
 }
 
-// Tile loader shared by both passes: band tiles are contiguous key ranges,
-// global-slot tiles gather the rows of global keys outside the band.
+// Tile loader of pass 1: band tiles are contiguous key ranges, global-slot
+// tiles gather the rows of global keys outside the band.
 template <int DT>
 struct WinLoader {
   using T = typename Tr<DT>::T;
@@ -300,37 +307,30 @@ struct WinLoader {
     if (t < wb.nkt) {
       const int k0 = wb.kt0 + t * kBK;
       stk.load_range(Kg, a.ld_in, k0, wb.kt1);
-      if (Vg) stv.load_range(Vg, a.ld_in, k0, wb.kt1);
+      stv.load_range(Vg, a.ld_in, k0, wb.kt1);
     } else {
       const int c = sXList[t - wb.nkt];
       stk.load_rows(Kg, a.ld_in, [&](int row) { return slot_row(c, row); });
-      if (Vg) stv.load_rows(Vg, a.ld_in, [&](int row) { return slot_row(c, row); });
+      stv.load_rows(Vg, a.ld_in, [&](int row) { return slot_row(c, row); });
       if (threadIdx.x < kBK) pos_reg = slot_row(c, threadIdx.x);
     }
   }
   SC_DEV void store(int t, T* sK, T* sV, int* sPos) const {
     stk.store(sK);
-    if (sV) stv.store(sV);
+    stv.store(sV);
     if (t >= wb.nkt && threadIdx.x < kBK) sPos[threadIdx.x] = pos_reg;
   }
 };
 
-// Pass 1: O, LSE (and the log2 LSE handed to pass 2) for the non-global
-// queries of the block; zero rows for padding queries.
+// Pass 1: O, LSE (and the log2 LSE used by the column sums) for the
+// non-global queries of the block; zero rows for padding queries.
 template <int DT>
-__global__ __launch_bounds__(kThreads) SC_OCC(3) void k_window_attn(AttnArgs a) {
+SC_DEV void window_fwd_block(const AttnArgs& a, int blk, Smem<DT>& sm, uint32_t* sDyn) {
   using TR = Tr<DT>;
   using T = typename TR::T;
   using Frag = typename TR::Frag;
   constexpr int P = TR::kPitch;
-  __shared__ __attribute__((aligned(16))) T sQ[kBQ * P];
-  __shared__ __attribute__((aligned(16))) T sK[2][kBK * P];
-  __shared__ __attribute__((aligned(16))) T sV[2][kBK * P];
-  __shared__ int sPos[2][kBK];
-  __shared__ int sNx;
-  extern __shared__ uint32_t sDyn[];  // [global bitmask over the band range][active global-slot chunks]
-
-  const WinBlock wb = win_block(a);
+  const WinBlock wb = win_block(a, blk);
   const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6, g = lane >> 4, lr = lane & 15;
   const int n = a.n, r = a.r, L = wb.L, q0 = wb.q0, kt0 = wb.kt0, kt1 = wb.kt1, nkt = wb.nkt;
   const T* Qg = static_cast<const T*>(a.q) + wb.b * a.bs_in + wb.h * kHeadDim;
@@ -346,9 +346,11 @@ __global__ __launch_bounds__(kThreads) SC_OCC(3) void k_window_attn(AttnArgs a) 
       const int q = q0 + c / kCpr;
       if (q < n) zero16(Og + (long long)q * a.ld_out + (c % kCpr) * kEpc);
     }
-    if (lseg)
-      for (int i = tid; i < kBQ; i += kThreads)
-        if (q0 + i < n) lseg[q0 + i] = -INFINITY;
+    for (int i = tid; i < kBQ; i += kThreads)
+      if (q0 + i < n) {
+        if (lseg) lseg[q0 + i] = -INFINITY;
+        if (l2g) l2g[q0 + i] = INFINITY;
+      }
     return;
   }
   uint32_t* sBits = sDyn;
@@ -356,9 +358,9 @@ __global__ __launch_bounds__(kThreads) SC_OCC(3) void k_window_attn(AttnArgs a) 
   {  // padding query rows are staged as zeros: their (unused) logits stay finite
     Stage<DT> sq;
     sq.load_range(Qg + (long long)q0 * a.ld_in, a.ld_in, 0, L - q0);
-    sq.store(sQ);
+    sq.store(sm.a);
   }
-  const int ntile = win_tables(a, wb, sBits, sXList, &sNx);
+  const int ntile = win_tables(a, wb, sBits, sXList, &sm.misc[0]);
   auto gbit = [&](int k) -> bool {
     const int o = k - kt0;
     return (sBits[o >> 5] >> (o & 31)) & 1u;
@@ -366,7 +368,7 @@ __global__ __launch_bounds__(kThreads) SC_OCC(3) void k_window_attn(AttnArgs a) 
   WinLoader<DT> ld{a, wb, wb.nxc ? a.gpos + (long long)wb.b * a.G : nullptr, sXList};
 
   Frag qf[TR::kChunks];
-  TR::load_frags(sQ + (16 * w + lr) * P, g, qf);
+  TR::load_frags(sm.a + (16 * w + lr) * P, g, qf);
   const int qa = q0 + 16 * w;
   const int qrow = qa + lr;
   float m_use = kNegBig, l_run = 0.f;
@@ -376,7 +378,7 @@ __global__ __launch_bounds__(kThreads) SC_OCC(3) void k_window_attn(AttnArgs a) 
 
   // band tiles: double-buffered, the next tile's loads overlap this tile's math
   ld.load(0, Kg, Vg);
-  ld.store(0, sK[0], sV[0], sPos[0]);
+  ld.store(0, sm.b[0], sm.c[0], sm.pos[0]);
   __syncthreads();
   for (int t = 0; t < nkt; ++t) {
     const int buf = t & 1;
@@ -386,7 +388,8 @@ __global__ __launch_bounds__(kThreads) SC_OCC(3) void k_window_attn(AttnArgs a) 
     if (near || tile_gmask(sBits, t, wb.nwords) != 0ull) {
       const bool interior = k0 + kBK <= kt1 && k0 >= qa + 15 - r && k0 + kBK - 1 <= qa + r;
       if (interior) {
-        softmax_tile<DT, false>(qf, sK[buf], sV[buf], a.c2, lr, g, m_use, l_run, o, [](int, int) { return true; });
+        softmax_tile<DT, false>(qf, sm.b[buf], sm.c[buf], a.c2, lr, g, m_use, l_run, o,
+                                [](int, int) { return true; });
       } else {
         // key index inside the tile: 16*st + 4g + i; allowed when it lies in
         // [lo, hi] (window and sequence end) or is a global key of the band.
@@ -394,22 +397,22 @@ __global__ __launch_bounds__(kThreads) SC_OCC(3) void k_window_attn(AttnArgs a) 
         // beyond kt1 are never set).
         const int lo = qrow - r - k0, hi = min(qrow + r, kt1 - 1) - k0;
         const unsigned long long gm = tile_gmask(sBits, t, wb.nwords) >> (4 * g);
-        softmax_tile<DT, true>(qf, sK[buf], sV[buf], a.c2, lr, g, m_use, l_run, o, [&](int s4, int i) {
+        softmax_tile<DT, true>(qf, sm.b[buf], sm.c[buf], a.c2, lr, g, m_use, l_run, o, [&](int s4, int i) {
           const int kk = 16 * s4 + 4 * g + i;
           return ((kk >= lo) & (kk <= hi)) | (bool)((gm >> (16 * s4 + i)) & 1ull);
         });
       }
     }
-    if (t + 1 < nkt) ld.store(t + 1, sK[buf ^ 1], sV[buf ^ 1], sPos[buf ^ 1]);
+    if (t + 1 < nkt) ld.store(t + 1, sm.b[buf ^ 1], sm.c[buf ^ 1], sm.pos[buf ^ 1]);
     __syncthreads();
   }
   // global keys outside the band (few tiles; not pipelined)
   for (int t = nkt; t < ntile; ++t) {
     ld.load(t, Kg, Vg);
-    ld.store(t, sK[0], sV[0], sPos[0]);
+    ld.store(t, sm.b[0], sm.c[0], sm.pos[0]);
     __syncthreads();
-    const int* sp = sPos[0];
-    softmax_tile<DT, true>(qf, sK[0], sV[0], a.c2, lr, g, m_use, l_run, o,
+    const int* sp = sm.pos[0];
+    softmax_tile<DT, true>(qf, sm.b[0], sm.c[0], a.c2, lr, g, m_use, l_run, o,
                            [&](int s4, int i) { return sp[16 * s4 + 4 * g + i] >= 0; });
     __syncthreads();
   }
@@ -429,137 +432,18 @@ __global__ __launch_bounds__(kThreads) SC_OCC(3) void k_window_attn(AttnArgs a) 
       store_row4<DT>(Og + (long long)qrow * a.ld_out + 16 * dt + 4 * g, f32x4{0.f, 0.f, 0.f, 0.f});
     if (g == 0 && lseg) lseg[qrow] = -INFINITY;
   }
-  // excluded rows (global or padding) get +inf: their pass-2 probabilities are 0
+  // excluded rows (global or padding) get +inf: their column-sum probabilities are 0
   if (g == 0 && l2g && qrow < n) l2g[qrow] = qvalid ? lse2 : INFINITY;
 }
 
-// Pass 2: exact probabilities of the block's non-global queries, summed per
-// key into the band and global-key partials (and written to the paper's band
-// layout when requested).  Wave w owns key sub-tile w of each staged tile.
-template <int DT, bool kBandProbs>
-__global__ __launch_bounds__(kThreads) SC_OCC(kBandProbs ? 2 : 4) void k_window_score(AttnArgs a) {
-  using TR = Tr<DT>;
-  using T = typename TR::T;
-  using Frag = typename TR::Frag;
-  constexpr int P = TR::kPitch;
-  __shared__ __attribute__((aligned(16))) T sQ[kBQ * P];
-  __shared__ __attribute__((aligned(16))) T sK[2][kBK * P];
-  __shared__ int sPos[2][kBK];
-  __shared__ int sNx;
-  extern __shared__ uint32_t sDyn[];
-
-  const WinBlock wb = win_block(a);
-  if (wb.q0 >= wb.L) return;  // the score reduction never reads padding blocks
-  const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6, g = lane >> 4, lr = lane & 15;
-  const int n = a.n, r = a.r, G = a.G, L = wb.L, q0 = wb.q0, kt0 = wb.kt0, kt1 = wb.kt1, nkt = wb.nkt;
-  const T* Qg = static_cast<const T*>(a.q) + wb.b * a.bs_in + wb.h * kHeadDim;
-  const T* Kg = static_cast<const T*>(a.k) + wb.b * a.bs_in + wb.h * kHeadDim;
-  const float* l2g = a.win_lse2 + (long long)wb.bh * n;
-  const int* gp = wb.nxc ? a.gpos + (long long)wb.b * G : nullptr;
-  uint32_t* sBits = sDyn;
-  int* sXList = reinterpret_cast<int*>(sDyn + a.rwp / 32 + 2);
-  {
-    Stage<DT> sq;
-    sq.load_range(Qg + (long long)q0 * a.ld_in, a.ld_in, 0, L - q0);
-    sq.store(sQ);
-  }
-  const int ntile = win_tables(a, wb, sBits, sXList, &sNx);
-  auto gbit = [&](int k) -> bool {
-    const int o = k - kt0;
-    return (sBits[o >> 5] >> (o & 31)) & 1u;
-  };
-  WinLoader<DT> ld{a, wb, gp, sXList};
-  ld.load(0, Kg, nullptr);
-  ld.store(0, sK[0], nullptr, sPos[0]);
-  // the block's log2-LSE go through LDS: values a loop consumes must not come
-  // from outstanding global loads (those would be waited for in every tile)
-  __shared__ float sL2[kBQ];
-  if (tid < kBQ) sL2[tid] = q0 + tid < L ? l2g[q0 + tid] : INFINITY;
-
-  Frag qf2[4][TR::kChunks];
-  float l2[4][4];
-  float* pb = a.part_band ? a.part_band + ((long long)wb.bh * a.nqb + wb.qb) * a.rwp : nullptr;
-  float* pe = a.part_band ? a.part_extra + ((long long)wb.bh * a.nqb + wb.qb) * G : nullptr;
-  float* bpb = kBandProbs ? a.bp_band + (long long)wb.bh * n * a.bw : nullptr;
-  float* bpc = kBandProbs ? a.bp_gcol + (long long)wb.bh * n * G : nullptr;
-  // global-key partials of slots never visited stay zero (written before the
-  // first barrier of the loop below, overwritten after it)
-  if (pe)
-    for (int j = tid; j < G; j += kThreads) pe[j] = 0.f;
-  __syncthreads();
-#pragma unroll
-  for (int qst = 0; qst < 4; ++qst) {
-    TR::load_frags(sQ + (16 * qst + lr) * P, g, qf2[qst]);
-#pragma unroll
-    for (int i = 0; i < 4; ++i) l2[qst][i] = sL2[16 * qst + 4 * g + i];
-  }
-
-  for (int t = 0; t < nkt; ++t) {
-    const int buf = t & 1;
-    if (t + 1 < nkt) ld.load(t + 1, Kg, nullptr);
-    const int k0 = kt0 + t * kBK;
-    const int key = k0 + 16 * w + lr;
-    const bool kin = key < kt1;
-    const bool kglob = kin && gbit(key);
-    // query index inside the block: 16*qst + 4g + i; allowed within
-    // [key - r - q0, key + r - q0] or when the key is global
-    const int lo = key - r - q0, hi = key + r - q0;
-    auto ok = [&](int qst, int i) {
-      const int qq = 16 * qst + 4 * g + i;
-      return kin & (kglob | ((qq >= lo) & (qq <= hi)));
-    };
-    float cs;
-    if constexpr (kBandProbs) {
-      const int kslot = kglob ? find_slot(gp, G, key) : -1;
-      cs = score_tile<DT, true>(qf2, l2, sK[buf], w, a.c2, lr, g, ok, [&](int qst, int i, float p) {
-        const int q = q0 + 16 * qst + 4 * g + i;
-        if (!(q < L) || !kin || p == 0.f) return;
-        if (kglob) {
-          if (kslot >= 0) bpc[(long long)q * G + kslot] = p;
-        } else if (abs(q - key) <= a.rb) {
-          bpb[(long long)q * a.bw + (key - q + a.rb)] = p;
-        }
-      });
-    } else {
-      const bool interior = k0 + kBK <= kt1 && k0 >= q0 + kBQ - 1 - r && k0 + kBK - 1 <= q0 + r;
-      cs = interior ? score_tile<DT, false>(qf2, l2, sK[buf], w, a.c2, lr, g, ok, NoEmit{})
-                    : score_tile<DT, true>(qf2, l2, sK[buf], w, a.c2, lr, g, ok, NoEmit{});
-    }
-    if (pb && g == 0 && kin) pb[key - kt0] = cs;
-    if (t + 1 < nkt) ld.store(t + 1, sK[buf ^ 1], nullptr, sPos[buf ^ 1]);
-    __syncthreads();
-  }
-  // global keys outside the band
-  for (int t = nkt; t < ntile; ++t) {
-    ld.load(t, Kg, nullptr);
-    ld.store(t, sK[0], nullptr, sPos[0]);
-    __syncthreads();
-    const int slot = kBK * sXList[t - nkt] + 16 * w + lr;
-    const bool kvalid = sPos[0][16 * w + lr] >= 0;
-    auto ok = [&](int, int) { return kvalid; };
-    float cs;
-    if constexpr (kBandProbs) {
-      cs = score_tile<DT, true>(qf2, l2, sK[0], w, a.c2, lr, g, ok, [&](int qst, int i, float p) {
-        const int q = q0 + 16 * qst + 4 * g + i;
-        if (kvalid && q < L && p != 0.f) bpc[(long long)q * G + slot] = p;
-      });
-    } else {
-      cs = score_tile<DT, true>(qf2, l2, sK[0], w, a.c2, lr, g, ok, NoEmit{});
-    }
-    if (pe && g == 0 && slot < G) pe[slot] = cs;
-    __syncthreads();
-  }
-}
-
-// -------------------------------------------------- global-row kernels -----
+// ------------------------------------------------------ global rows -------
 // Global query rows attend to every valid key: a dense strip, split over key
 // ranges of kGlobalKeySpan.  Block = 64 global slots x one key range.
 struct GrBlock {
   int kc, gc, h, b, bh;
 };
-SC_DEV GrBlock gr_block(const AttnArgs& a) {
+SC_DEV GrBlock gr_block(const AttnArgs& a, int lin) {
   GrBlock r;
-  int lin = blockIdx.x;
   r.kc = lin % a.nkc;
   lin /= a.nkc;
   r.gc = lin % a.ngc;
@@ -570,30 +454,33 @@ SC_DEV GrBlock gr_block(const AttnArgs& a) {
   return r;
 }
 
+// Positions of the block's 64 global slots (-1: unused) into pos; returns
+// whether any is used.  Contains a barrier.
+SC_DEV bool gr_slots(const AttnArgs& a, const GrBlock& blk, int L, int* pos) {
+  int valid = 0;
+  if (threadIdx.x < kGlobalChunk) {
+    const int j = kGlobalChunk * blk.gc + threadIdx.x;
+    const int p = j < a.G ? a.gpos[(long long)blk.b * a.G + j] : -1;
+    valid = p >= 0 && p < L;
+    pos[threadIdx.x] = valid ? p : -1;
+  }
+  return __syncthreads_or(valid);
+}
+
+// Forward of the global rows over one key range: running max, sum and
+// unnormalised P.V per row, merged later across ranges.
 template <int DT>
-__global__ __launch_bounds__(kThreads) void k_global_rows_fwd(AttnArgs a) {
+SC_DEV void gr_fwd_block(const AttnArgs& a, int lin, Smem<DT>& sm) {
   using TR = Tr<DT>;
   using T = typename TR::T;
   constexpr int P = TR::kPitch;
-  __shared__ __attribute__((aligned(16))) T sQ[kBQ * P];
-  __shared__ __attribute__((aligned(16))) T sK[2][kBK * P];
-  __shared__ __attribute__((aligned(16))) T sV[2][kBK * P];
-  __shared__ int sPos[kGlobalChunk];
-  const GrBlock blk = gr_block(a);
+  const GrBlock blk = gr_block(a, lin);
   const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6, g = lane >> 4, lr = lane & 15;
   const int L = clampi(a.valid_len[blk.b], 0, a.n);
   const int kbeg = blk.kc * kGlobalKeySpan;
   if (kbeg >= L) return;
   const int kend = min(L, kbeg + kGlobalKeySpan);
-  const int* gp = a.gpos + (long long)blk.b * a.G;
-  int valid = 0;
-  if (tid < kGlobalChunk) {
-    const int j = kGlobalChunk * blk.gc + tid;
-    const int p = j < a.G ? gp[j] : -1;
-    valid = p >= 0 && p < L;
-    sPos[tid] = valid ? p : -1;
-  }
-  if (!__syncthreads_or(valid)) return;
+  if (!gr_slots(a, blk, L, sm.pos[0])) return;
   const T* Qg = static_cast<const T*>(a.q) + blk.b * a.bs_in + blk.h * kHeadDim;
   const T* Kg = static_cast<const T*>(a.k) + blk.b * a.bs_in + blk.h * kHeadDim;
   const T* Vg = static_cast<const T*>(a.v) + blk.b * a.bs_in + blk.h * kHeadDim;
@@ -601,16 +488,17 @@ __global__ __launch_bounds__(kThreads) void k_global_rows_fwd(AttnArgs a) {
   Stage<DT> stk, stv;
   {
     Stage<DT> sq;
-    sq.load_rows(Qg, a.ld_in, [&](int row) { return sPos[row]; });
-    sq.store(sQ);
+    const int* sp = sm.pos[0];
+    sq.load_rows(Qg, a.ld_in, [&](int row) { return sp[row]; });
+    sq.store(sm.a);
   }
   stk.load_range(Kg, a.ld_in, kbeg, kend);
   stv.load_range(Vg, a.ld_in, kbeg, kend);
-  stk.store(sK[0]);
-  stv.store(sV[0]);
+  stk.store(sm.b[0]);
+  stv.store(sm.c[0]);
   __syncthreads();
   typename TR::Frag qf[TR::kChunks];
-  TR::load_frags(sQ + (16 * w + lr) * P, g, qf);
+  TR::load_frags(sm.a + (16 * w + lr) * P, g, qf);
   float m_use = kNegBig, l_run = 0.f;
   f32x4 o[4];
 #pragma unroll
@@ -622,15 +510,15 @@ __global__ __launch_bounds__(kThreads) void k_global_rows_fwd(AttnArgs a) {
       stv.load_range(Vg, a.ld_in, k0 + kBK, kend);
     }
     if (k0 + kBK <= kend) {
-      softmax_tile<DT, false>(qf, sK[buf], sV[buf], a.c2, lr, g, m_use, l_run, o, [](int, int) { return true; });
+      softmax_tile<DT, false>(qf, sm.b[buf], sm.c[buf], a.c2, lr, g, m_use, l_run, o, [](int, int) { return true; });
     } else {
       const int hi = kend - 1 - k0;
-      softmax_tile<DT, true>(qf, sK[buf], sV[buf], a.c2, lr, g, m_use, l_run, o,
+      softmax_tile<DT, true>(qf, sm.b[buf], sm.c[buf], a.c2, lr, g, m_use, l_run, o,
                              [&](int s4, int i) { return 16 * s4 + 4 * g + i <= hi; });
     }
     if (t + 1 < ntile) {
-      stk.store(sK[buf ^ 1]);
-      stv.store(sV[buf ^ 1]);
+      stk.store(sm.b[buf ^ 1]);
+      stv.store(sm.c[buf ^ 1]);
     }
     __syncthreads();
   }
@@ -645,167 +533,330 @@ __global__ __launch_bounds__(kThreads) void k_global_rows_fwd(AttnArgs a) {
   for (int dt = 0; dt < 4; ++dt) *reinterpret_cast<f32x4*>(a.gr_o + idx * kHeadDim + 16 * dt + 4 * g) = o[dt];
 }
 
-// One wave per (sequence, head, global slot): merge the key-range partials.
+// Launch 1: global-row forward blocks first (when there are global tokens),
+// then the window pass-1 blocks.
 template <int DT>
-__global__ __launch_bounds__(kThreads) void k_global_rows_merge(AttnArgs a) {
-  using T = typename Tr<DT>::T;
-  const long long wid = (long long)blockIdx.x * (kThreads / 64) + (threadIdx.x >> 6);
-  const int lane = threadIdx.x & 63;
-  if (wid >= (long long)a.B * a.H * a.Gp) return;
-  const int slot = (int)(wid % a.Gp);
-  const int bh = (int)(wid / a.Gp), b = bh / a.H, h = bh % a.H;
-  const int L = clampi(a.valid_len[b], 0, a.n);
-  const int p = slot < a.G ? a.gpos[(long long)b * a.G + slot] : -1;
-  if (!(p >= 0 && p < L)) {
-    if (lane == 0) a.gr_lse2[wid] = INFINITY;
-    return;
-  }
-  const int nk = (L + kGlobalKeySpan - 1) / kGlobalKeySpan;
-  float m = kNegBig;
-  for (int kc = 0; kc < nk; ++kc) m = fmaxf(m, a.gr_ml[2 * (((long long)bh * a.nkc + kc) * a.Gp + slot)]);
-  float l = 0.f, acc = 0.f;
-  for (int kc = 0; kc < nk; ++kc) {
-    const long long idx = ((long long)bh * a.nkc + kc) * a.Gp + slot;
-    const float f = fast_exp2(a.gr_ml[2 * idx] - m);
-    l += a.gr_ml[2 * idx + 1] * f;
-    acc += a.gr_o[idx * kHeadDim + lane] * f;
-  }
-  const float lse2 = m + fast_log2(l);
-  T* Og = static_cast<T*>(a.out) + b * a.bs_out + (long long)p * a.ld_out + h * kHeadDim;
-  Og[lane] = (T)(acc / l);
-  if (lane == 0) {
-    if (a.lse) a.lse[(long long)bh * a.n + p] = lse2 * kLn2;
-    a.gr_lse2[wid] = lse2;
-  }
+__global__ __launch_bounds__(kThreads) SC_OCC(3) void k_attn_fwd(AttnArgs a) {
+  __shared__ Smem<DT> sm;
+  extern __shared__ uint32_t sDyn[];
+  if ((int)blockIdx.x < a.n_gr)
+    gr_fwd_block<DT>(a, blockIdx.x, sm);
+  else
+    window_fwd_block<DT>(a, blockIdx.x - a.n_gr, sm, sDyn);
 }
 
-// Column sums over the global query rows of one slot chunk, per key.
-template <int DT>
-__global__ __launch_bounds__(kThreads) void k_global_rows_score(AttnArgs a) {
+// -------------------------------------------------------- column sums ------
+// Column sums of the exact probabilities, key-outer: a block owns 64 keys,
+// keeps their K fragments in registers and walks the query tiles that reach
+// them, so every key's sum over queries is finished inside the block.
+//   band columns    keys k0..k0+63 of a sequence; queries of their band;
+//                   global keys are skipped (their columns are dense)
+//   global columns  64 global slots; queries of one 512-query range
+// Query rows come with their log2-LSE from pass 1 (+inf for global and
+// padding rows, whose own probabilities are counted by the global-row blocks).
+template <int DT, bool kBandProbs>
+SC_DEV void band_col_block(const AttnArgs& a, int blk, SmemCol<DT>& sm) {
   using TR = Tr<DT>;
   using T = typename TR::T;
   constexpr int P = TR::kPitch;
-  __shared__ __attribute__((aligned(16))) T sQ[kBQ * P];
-  __shared__ __attribute__((aligned(16))) T sK[2][kBK * P];
-  __shared__ int sPos[kGlobalChunk];
-  const GrBlock blk = gr_block(a);
+  const int lin = xcd_remap(blk, a.nkb * a.H * a.B);
+  const int kb = lin % a.nkb, bh = lin / a.nkb, h = bh % a.H, b = bh / a.H;
+  const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6, g = lane >> 4, lr = lane & 15;
+  const int n = a.n, r = a.r, G = a.G;
+  const int L = clampi(a.valid_len[b], 0, n);
+  const int k0 = kb * kBK;
+  if (k0 >= L) return;  // the score reduction reads keys below L only
+  const int kend = min(L, k0 + kBK);
+  const T* Qg = static_cast<const T*>(a.q) + b * a.bs_in + h * kHeadDim;
+  const T* Kg = static_cast<const T*>(a.k) + b * a.bs_in + h * kHeadDim;
+  const float* l2g = a.win_lse2 + (long long)bh * n;
+  const int* gp = (a.gpos && G > 0) ? a.gpos + (long long)b * G : nullptr;
+  uint32_t* gmask = reinterpret_cast<uint32_t*>(sm.misc);
+  if (tid < 2) gmask[tid] = 0u;
+  {
+    Stage<DT> sk;
+    sk.load_range(Kg + (long long)k0 * a.ld_in, a.ld_in, 0, kend - k0);
+    sk.store(sm.a);
+  }
+  __syncthreads();
+  for (int j = tid; j < (gp ? G : 0); j += kThreads) {
+    const int p = gp[j];
+    if (p >= k0 && p < kend) atomicOr(&gmask[(p - k0) >> 5], 1u << ((p - k0) & 31));
+  }
+  const int qlo = max(0, k0 - r), qhi = min(L, k0 + kBK + r);
+  const int nqt = (qhi - qlo + kBQ - 1) / kBQ;
+  Stage<DT> sq;
+  float lreg = INFINITY;
+  auto load = [&](int t) {
+    const int qs = qlo + t * kBQ;
+    sq.load_range(Qg, a.ld_in, qs, qhi);
+    if (tid < kBQ) lreg = qs + tid < qhi ? l2g[qs + tid] : INFINITY;
+  };
+  auto store = [&](int buf) {
+    sq.store(sm.b[buf]);
+    if (tid < kBQ) sm.l[buf][tid] = lreg;
+  };
+  load(0);
+  store(0);
+  __syncthreads();
+  typename TR::Frag kf[TR::kChunks];
+  TR::load_frags(sm.a + (16 * w + lr) * P, g, kf);
+  const int key = k0 + 16 * w + lr;
+  const bool kuse = key < kend && !((gmask[(key - k0) >> 5] >> ((key - k0) & 31)) & 1u);
+  float* bpb = kBandProbs ? a.bp_band + (long long)bh * n * a.bw : nullptr;
+  float cs = 0.f;
+  for (int t = 0; t < nqt; ++t) {
+    const int buf = t & 1;
+    if (t + 1 < nqt) load(t + 1);
+    const int qs = qlo + t * kBQ;
+    // allowed: |q - key| <= r with q = qs + qq, qq = 16*qst + 4g + i
+    const int lo = key - r - qs, hi = key + r - qs;
+    auto ok = [&](int qst, int i) {
+      const int qq = 16 * qst + 4 * g + i;
+      return (qq >= lo) & (qq <= hi);
+    };
+    if constexpr (kBandProbs) {
+      cs += col_tile<DT, true>(kf, sm.b[buf], sm.l[buf], a.c2, lr, g, ok, [&](int qq, float p) {
+        const int q = qs + qq;
+        if (kuse && q < L && p != 0.f && abs(q - key) <= a.rb) bpb[(long long)q * a.bw + (key - q + a.rb)] = p;
+      });
+    } else {
+      const bool interior = qs >= k0 + kBK - 1 - r && qs + kBQ - 1 <= k0 + r;
+      cs += interior ? col_tile<DT, false>(kf, sm.b[buf], sm.l[buf], a.c2, lr, g, ok, NoEmit{})
+                     : col_tile<DT, true>(kf, sm.b[buf], sm.l[buf], a.c2, lr, g, ok, NoEmit{});
+    }
+    if (t + 1 < nqt) store(buf ^ 1);
+    __syncthreads();
+  }
+  cs = group_sum(cs);
+  if (a.part_band && g == 0 && key < n) a.part_band[(long long)bh * n + key] = kuse ? cs : 0.f;
+}
+
+template <int DT, bool kBandProbs>
+SC_DEV void gcol_block(const AttnArgs& a, int lin, SmemCol<DT>& sm) {
+  using TR = Tr<DT>;
+  using T = typename TR::T;
+  constexpr int P = TR::kPitch;
+  const int qr = lin % a.nqr;
+  lin /= a.nqr;
+  const int gc = lin % a.ngc;
+  lin /= a.ngc;
+  const int h = lin % a.H, b = lin / a.H, bh = b * a.H + h;
+  const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6, g = lane >> 4, lr = lane & 15;
+  const int n = a.n, G = a.G;
+  const int L = clampi(a.valid_len[b], 0, n);
+  const int qbeg = qr * kGlobalKeySpan;
+  if (qbeg >= L) return;  // the score reduction reads ranges below L only
+  const int qend = min(L, qbeg + kGlobalKeySpan);
+  const T* Qg = static_cast<const T*>(a.q) + b * a.bs_in + h * kHeadDim;
+  const T* Kg = static_cast<const T*>(a.k) + b * a.bs_in + h * kHeadDim;
+  const float* l2g = a.win_lse2 + (long long)bh * n;
+  const int* gp = a.gpos + (long long)b * G;
+  int* pos = sm.pos[0];
+  if (tid < kGlobalChunk) {
+    const int j = kGlobalChunk * gc + tid;
+    const int p = j < G ? gp[j] : -1;
+    pos[tid] = (p >= 0 && p < L) ? p : -1;
+  }
+  __syncthreads();
+  {
+    Stage<DT> sk;
+    sk.load_rows(Kg, a.ld_in, [&](int row) { return pos[row]; });
+    sk.store(sm.a);
+  }
+  const int nqt = (qend - qbeg + kBQ - 1) / kBQ;
+  Stage<DT> sq;
+  float lreg = INFINITY;
+  auto load = [&](int t) {
+    const int qs = qbeg + t * kBQ;
+    sq.load_range(Qg, a.ld_in, qs, qend);
+    if (tid < kBQ) lreg = qs + tid < qend ? l2g[qs + tid] : INFINITY;
+  };
+  auto store = [&](int buf) {
+    sq.store(sm.b[buf]);
+    if (tid < kBQ) sm.l[buf][tid] = lreg;
+  };
+  load(0);
+  store(0);
+  __syncthreads();
+  typename TR::Frag kf[TR::kChunks];
+  TR::load_frags(sm.a + (16 * w + lr) * P, g, kf);
+  const int slot = kGlobalChunk * gc + 16 * w + lr;
+  const bool kuse = pos[16 * w + lr] >= 0;
+  float* bpc = kBandProbs ? a.bp_gcol + (long long)bh * n * G : nullptr;
+  float cs = 0.f;
+  for (int t = 0; t < nqt; ++t) {
+    const int buf = t & 1;
+    if (t + 1 < nqt) load(t + 1);
+    const int qs = qbeg + t * kBQ;
+    if constexpr (kBandProbs) {
+      cs += col_tile<DT, false>(kf, sm.b[buf], sm.l[buf], a.c2, lr, g, [](int, int) { return true; },
+                                [&](int qq, float p) {
+                                  const int q = qs + qq;
+                                  if (kuse && q < L && p != 0.f) bpc[(long long)q * G + slot] = p;
+                                });
+    } else {
+      cs += col_tile<DT, false>(kf, sm.b[buf], sm.l[buf], a.c2, lr, g, [](int, int) { return true; }, NoEmit{});
+    }
+    if (t + 1 < nqt) store(buf ^ 1);
+    __syncthreads();
+  }
+  cs = group_sum(cs);
+  if (a.part_extra && g == 0 && slot < G) a.part_extra[((long long)bh * a.nqr + qr) * G + slot] = kuse ? cs : 0.f;
+}
+
+// Global rows, second half: merge the key-range partials of the block's 64
+// rows into their log2-LSE (and, for the first key range, into their output
+// rows and natural LSE), then the rows' probabilities summed per key.
+template <int DT, bool kBandProbs>
+SC_DEV void gr_col_block(const AttnArgs& a, int lin, SmemCol<DT>& sm) {
+  using TR = Tr<DT>;
+  using T = typename TR::T;
+  constexpr int P = TR::kPitch;
+  const GrBlock blk = gr_block(a, lin);
   const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6, g = lane >> 4, lr = lane & 15;
   const int L = clampi(a.valid_len[blk.b], 0, a.n);
   const int kbeg = blk.kc * kGlobalKeySpan;
   if (kbeg >= L) return;
   const int kend = min(L, kbeg + kGlobalKeySpan);
-  const int* gp = a.gpos + (long long)blk.b * a.G;
   float* pg = a.part_grow ? a.part_grow + ((long long)blk.bh * a.ngc + blk.gc) * a.n : nullptr;
-  float* bpr = a.bp_grow ? a.bp_grow + (long long)blk.bh * a.G * a.n : nullptr;
-  int valid = 0;
-  if (tid < kGlobalChunk) {
-    const int j = kGlobalChunk * blk.gc + tid;
-    const int p = j < a.G ? gp[j] : -1;
-    valid = p >= 0 && p < L;
-    sPos[tid] = valid ? p : -1;
-  }
-  if (!__syncthreads_or(valid)) {
+  const bool want_cols = a.part_grow || a.bp_grow;
+  if (!want_cols && blk.kc != 0) return;  // only the merge of the output rows is needed
+  if (!gr_slots(a, blk, L, sm.pos[0])) {
     if (pg)
       for (int k = kbeg + tid; k < kend; k += kThreads) pg[k] = 0.f;
     return;
   }
+  const int* pos = sm.pos[0];
+  const int nk = (L + kGlobalKeySpan - 1) / kGlobalKeySpan;
+  float* sM = sm.l[1];  // per-row running max of the merge
+  if (tid < kGlobalChunk) {
+    const int slot = kGlobalChunk * blk.gc + tid;
+    float lse2 = INFINITY, m = kNegBig;
+    if (pos[tid] >= 0) {
+      for (int kc = 0; kc < nk; ++kc) m = fmaxf(m, a.gr_ml[2 * (((long long)blk.bh * a.nkc + kc) * a.Gp + slot)]);
+      float l = 0.f;
+      for (int kc = 0; kc < nk; ++kc) {
+        const long long idx = ((long long)blk.bh * a.nkc + kc) * a.Gp + slot;
+        l += a.gr_ml[2 * idx + 1] * fast_exp2(a.gr_ml[2 * idx] - m);
+      }
+      lse2 = m + fast_log2(l);
+      if (blk.kc == 0 && a.lse) a.lse[(long long)blk.bh * a.n + pos[tid]] = lse2 * kLn2;
+    }
+    sm.l[0][tid] = lse2;
+    sM[tid] = m;
+  }
+  __syncthreads();
+  if (blk.kc == 0) {  // output rows of the global queries
+    T* Ob = static_cast<T*>(a.out) + blk.b * a.bs_out + blk.h * kHeadDim;
+    for (int e = tid; e < kGlobalChunk * kHeadDim; e += kThreads) {
+      const int row = e / kHeadDim, d = e % kHeadDim;
+      if (pos[row] < 0) continue;
+      const int slot = kGlobalChunk * blk.gc + row;
+      const float m = sM[row], lse2 = sm.l[0][row];
+      float acc = 0.f;
+      for (int kc = 0; kc < nk; ++kc) {
+        const long long idx = ((long long)blk.bh * a.nkc + kc) * a.Gp + slot;
+        acc += a.gr_o[idx * kHeadDim + d] * fast_exp2(a.gr_ml[2 * idx] - m);
+      }
+      Ob[(long long)pos[row] * a.ld_out + d] = (T)(acc * fast_exp2(m - lse2));
+    }
+  }
+  if (!want_cols) return;
   const T* Qg = static_cast<const T*>(a.q) + blk.b * a.bs_in + blk.h * kHeadDim;
   const T* Kg = static_cast<const T*>(a.k) + blk.b * a.bs_in + blk.h * kHeadDim;
   const int ntile = (kend - kbeg + kBK - 1) / kBK;
   Stage<DT> stk;
   {
     Stage<DT> sq;
-    sq.load_rows(Qg, a.ld_in, [&](int row) { return sPos[row]; });
-    sq.store(sQ);
+    sq.load_rows(Qg, a.ld_in, [&](int row) { return pos[row]; });
+    sq.store(sm.a);
   }
   stk.load_range(Kg, a.ld_in, kbeg, kend);
-  stk.store(sK[0]);
+  stk.store(sm.b[0]);
   __syncthreads();
-  typename TR::Frag qf[4][TR::kChunks];
-  float l2[4][4];
-#pragma unroll
-  for (int qst = 0; qst < 4; ++qst) {
-    TR::load_frags(sQ + (16 * qst + lr) * P, g, qf[qst]);
-#pragma unroll
-    for (int i = 0; i < 4; ++i)
-      l2[qst][i] = a.gr_lse2[(long long)blk.bh * a.Gp + kGlobalChunk * blk.gc + 16 * qst + 4 * g + i];
-  }
+  float* bpr = kBandProbs ? a.bp_grow + (long long)blk.bh * a.G * a.n : nullptr;
   for (int t = 0; t < ntile; ++t) {
     const int buf = t & 1, k0 = kbeg + t * kBK;
     if (t + 1 < ntile) stk.load_range(Kg, a.ld_in, k0 + kBK, kend);
+    // this wave's 16 keys as the K operand, the 64 global rows as queries
+    typename TR::Frag kf[TR::kChunks];
+    TR::load_frags(sm.b[buf] + (16 * w + lr) * P, g, kf);
     const int key = k0 + 16 * w + lr;
     const bool kin = key < kend;
-    auto ok = [&](int, int) { return kin; };
     float cs;
-    if (bpr) {
-      cs = score_tile<DT, true>(qf, l2, sK[buf], w, a.c2, lr, g, ok, [&](int qst, int i, float p) {
-        const int slot = kGlobalChunk * blk.gc + 16 * qst + 4 * g + i;
+    if constexpr (kBandProbs) {
+      cs = col_tile<DT, false>(kf, sm.a, sm.l[0], a.c2, lr, g, [](int, int) { return true; }, [&](int qq, float p) {
+        const int slot = kGlobalChunk * blk.gc + qq;
         if (kin && slot < a.G && p != 0.f) bpr[(long long)slot * a.n + key] = p;
       });
     } else {
-      cs = score_tile<DT, true>(qf, l2, sK[buf], w, a.c2, lr, g, ok, NoEmit{});
+      cs = col_tile<DT, false>(kf, sm.a, sm.l[0], a.c2, lr, g, [](int, int) { return true; }, NoEmit{});
     }
+    cs = group_sum(cs);
     if (pg && g == 0 && kin) pg[key] = cs;
-    if (t + 1 < ntile) stk.store(sK[buf ^ 1]);
+    if (t + 1 < ntile) stk.store(sm.b[buf ^ 1]);
     __syncthreads();
   }
 }
 
-// ------------------------------------------------------ score reduction ----
-// scores[b, k] = (sum over heads of: the band partials of every query block
-// whose band holds k, the global-key partials if k is global, and the
-// global-row sums) / (H * L).  Workgroup = 64 keys of one sequence; wave w
-// sums heads w, w + nw, ...; the nw wave sums are then added in wave order.
-// Fixed order everywhere; no atomics.
-constexpr int kScoreKeys = 64;
-constexpr int kScoreMaxWaves = 16;
+// Launch 2: global-row column blocks, band-column blocks, global-column
+// blocks (the last two only when score partials or the band layout are asked
+// for).
+template <int DT, bool kBandProbs>
+__global__ __launch_bounds__(kThreads) SC_OCC(kBandProbs ? 2 : 4) void k_attn_cols(AttnArgs a) {
+  __shared__ SmemCol<DT> sm;
+  int blk = blockIdx.x;
+  if (blk < a.n_gr) {
+    gr_col_block<DT, kBandProbs>(a, blk, sm);
+    return;
+  }
+  blk -= a.n_gr;
+  if (blk < a.n_bcol) {
+    band_col_block<DT, kBandProbs>(a, blk, sm);
+    return;
+  }
+  blk -= a.n_bcol;
+  gcol_block<DT, kBandProbs>(a, blk, sm);
+}
 
-__global__ __launch_bounds__(64 * kScoreMaxWaves) void k_score_from_partials(const float* part, const int* valid_len,
-                                                                             const int* gpos, int B, int n, int H,
-                                                                             int G, AttnGeom geo, float* scores) {
-  __shared__ int smap[kScoreKeys];
-  __shared__ float red[kScoreMaxWaves][kScoreKeys];
-  const int b = blockIdx.y, kb = blockIdx.x * kScoreKeys, tid = threadIdx.x;
-  const int lane = tid & 63, w = tid >> 6, nw = blockDim.x >> 6;
-  const int k = kb + lane;
+// ------------------------------------------------------ score reduction ----
+// scores[b, k] = (sum over heads of: the band column sum of k, its global
+// column (summed over query ranges) if k is global, and the global rows'
+// column sums) / (H * L).  One thread per key; fixed order; no atomics.
+__global__ __launch_bounds__(256) void k_score_from_partials(const float* part, const int* valid_len, const int* gpos,
+                                                             int B, int n, int H, int G, AttnGeom geo,
+                                                             float* scores) {
+  __shared__ int smap[256];
+  const int b = blockIdx.y, kb = blockIdx.x * 256, tid = threadIdx.x, k = kb + tid;
   const int L = clampi(valid_len[b], 0, n);
-  if (tid < kScoreKeys) smap[tid] = -1;
+  smap[tid] = -1;
   __syncthreads();
   if (gpos)
-    for (int j = tid; j < G; j += blockDim.x) {
+    for (int j = tid; j < G; j += 256) {
       const int p = gpos[(long long)b * G + j];
-      if (p >= kb && p < kb + kScoreKeys && p < L) smap[p - kb] = j;
+      if (p >= kb && p < kb + 256 && p < L) smap[p - kb] = j;
     }
   __syncthreads();
+  if (k >= n) return;
+  if (k >= L) {
+    scores[(long long)b * n + k] = 0.f;
+    return;
+  }
+  const float* band = part;
+  const float* gcol = band + (size_t)B * H * n;
+  const float* grow = gcol + (size_t)B * H * geo.nqr * G;
+  const int slot = smap[tid];
+  const int nqrv = (L + kGlobalKeySpan - 1) / kGlobalKeySpan;
   float acc = 0.f;
-  if (k < L) {
-    const float* band = part;
-    const float* extra = band + (size_t)B * H * geo.nqb * geo.rwp;
-    const float* grow = extra + (size_t)B * H * geo.nqb * G;
-    const int r = geo.r;
-    const int nqbv = (L + kBQ - 1) / kBQ;
-    // blocks whose key range [max(0, qb*64 - r), qb*64 + 64 + r) holds k
-    const int qlo = k - r - (kBQ - 1) <= 0 ? 0 : (k - r) / kBQ;
-    const int qhi = min(nqbv - 1, (k + r) / kBQ);
-    const int slot = smap[lane];
-    for (int h = w; h < H; h += nw) {
-      const long long bh = (long long)b * H + h;
-      const float* pb = band + bh * geo.nqb * geo.rwp;
-      for (int qb = qlo; qb <= qhi; ++qb) acc += pb[(long long)qb * geo.rwp + (k - max(0, qb * kBQ - r))];
-      if (slot >= 0) {
-        const float* pe = extra + bh * geo.nqb * G + slot;
-        for (int qb = 0; qb < nqbv; ++qb) acc += pe[(long long)qb * G];
-      }
-      for (int gc = 0; gc < geo.ngc; ++gc) acc += grow[(bh * geo.ngc + gc) * n + k];
-    }
+  for (int h = 0; h < H; ++h) {
+    const long long bh = (long long)b * H + h;
+    acc += band[bh * n + k];
+    if (slot >= 0)
+      for (int qr = 0; qr < nqrv; ++qr) acc += gcol[(bh * geo.nqr + qr) * G + slot];
+    for (int gc = 0; gc < geo.ngc; ++gc) acc += grow[(bh * geo.ngc + gc) * n + k];
   }
-  red[w][lane] = acc;
-  __syncthreads();
-  if (w == 0 && k < n) {
-    float tot = 0.f;
-    for (int i = 0; i < nw; ++i) tot += red[i][lane];
-    scores[(long long)b * n + k] = k < L ? tot / ((float)H * (float)L) : 0.f;
-  }
+  scores[(long long)b * n + k] = acc / ((float)H * (float)L);
 }
 
 // Paper layout: the score of key k is its band sub-diagonal (entries (i, j)
@@ -861,13 +912,15 @@ AttnGeom attn_geom(int n, int window, int G) {
   g.ngc = (G + kGlobalChunk - 1) / kGlobalChunk;
   g.Gp = g.ngc * kGlobalChunk;
   g.nkc = (n + kGlobalKeySpan - 1) / kGlobalKeySpan;
+  g.nkb = (n + kBK - 1) / kBK;
+  g.nqr = (n + kGlobalKeySpan - 1) / kGlobalKeySpan;
   g.rb = window / 2 < n - 1 ? window / 2 : n - 1;
   g.bw = 2 * g.rb + 1;
   return g;
 }
 
 size_t partials_floats(int B, int H, int n, const AttnGeom& g, int G) {
-  return (size_t)B * H * ((size_t)g.nqb * (g.rwp + G) + (size_t)g.ngc * n);
+  return (size_t)B * H * ((size_t)n + (size_t)g.nqr * G + (size_t)g.ngc * n);
 }
 
 size_t band_probs_floats(int B, int H, int n, const AttnGeom& g, int G) {
@@ -920,27 +973,26 @@ int profile_read(double* total_ms, long long* launches) {
 }
 
 template <int DT>
-static hipError_t launch_window_t(const AttnArgs& a, hipStream_t s) {
-  if (a.G > 0 && a.gpos) {
-    const unsigned grid = (unsigned)(a.nkc * a.ngc * a.H * a.B);
-    hipLaunchKernelGGL(k_global_rows_fwd<DT>, dim3(grid), dim3(kThreads), 0, s, a);
-    const long long waves = (long long)a.B * a.H * a.Gp;
-    hipLaunchKernelGGL(k_global_rows_merge<DT>, dim3((unsigned)((waves + 3) / 4)), dim3(kThreads), 0, s, a);
-  }
-  const int nxc = a.G > 0 && a.gpos ? (a.G + kBK - 1) / kBK : 0;
+static hipError_t launch_window_t(const AttnArgs& a0, hipStream_t s) {
+  AttnArgs a = a0;
+  const bool glob = a.G > 0 && a.gpos;
+  const bool cols = a.part_band || a.bp_band;
+  a.n_gr = glob ? a.nkc * a.ngc * a.H * a.B : 0;
+  a.n_bcol = cols ? a.nkb * a.H * a.B : 0;
+  const int n_gcol = (cols && glob) ? a.nqr * a.ngc * a.H * a.B : 0;
+  const int nxc = glob ? (a.G + kBK - 1) / kBK : 0;
   const size_t dyn = sizeof(uint32_t) * ((size_t)a.rwp / 32 + 2 + nxc + 1);
-  const unsigned blocks = (unsigned)(a.nqb * a.H * a.B);
+  const unsigned fwd_blocks = (unsigned)(a.n_gr + a.nqb * a.H * a.B);
+  const unsigned col_blocks = (unsigned)(a.n_gr + a.n_bcol + n_gcol);
   profile_begin(s);
-  hipLaunchKernelGGL(k_window_attn<DT>, dim3(blocks), dim3(kThreads), dyn, s, a);
-  if (a.bp_band)
-    hipLaunchKernelGGL((k_window_score<DT, true>), dim3(blocks), dim3(kThreads), dyn, s, a);
-  else if (a.part_band)
-    hipLaunchKernelGGL((k_window_score<DT, false>), dim3(blocks), dim3(kThreads), dyn, s, a);
-  profile_end(s);
-  if (a.G > 0 && a.gpos && (a.part_grow || a.bp_grow)) {
-    const unsigned grid = (unsigned)(a.nkc * a.ngc * a.H * a.B);
-    hipLaunchKernelGGL(k_global_rows_score<DT>, dim3(grid), dim3(kThreads), 0, s, a);
+  hipLaunchKernelGGL(k_attn_fwd<DT>, dim3(fwd_blocks), dim3(kThreads), dyn, s, a);
+  if (col_blocks > 0) {
+    if (a.bp_band)
+      hipLaunchKernelGGL((k_attn_cols<DT, true>), dim3(col_blocks), dim3(kThreads), 0, s, a);
+    else
+      hipLaunchKernelGGL((k_attn_cols<DT, false>), dim3(col_blocks), dim3(kThreads), 0, s, a);
   }
+  profile_end(s);
   return hipGetLastError();
 }
 
@@ -950,10 +1002,9 @@ hipError_t launch_window_attention(int dtype, const AttnArgs& a, hipStream_t s) 
 
 hipError_t launch_score_from_partials(const float* partials, const int* valid_len, const int* gpos, int B, int n,
                                       int H, int G, const AttnGeom& g, float* scores, hipStream_t s) {
-  dim3 grid((n + kScoreKeys - 1) / kScoreKeys, B);
-  const int nw = H < kScoreMaxWaves ? H : kScoreMaxWaves;
-  hipLaunchKernelGGL(k_score_from_partials, grid, dim3(64 * nw), 0, s, partials, valid_len, G > 0 ? gpos : nullptr, B,
-                     n, H, G, g, scores);
+  dim3 grid((n + 255) / 256, B);
+  hipLaunchKernelGGL(k_score_from_partials, grid, dim3(256), 0, s, partials, valid_len, G > 0 ? gpos : nullptr, B, n,
+                     H, G, g, scores);
   return hipGetLastError();
 }
 

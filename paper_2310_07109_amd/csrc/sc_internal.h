@@ -25,11 +25,12 @@ struct AttnArgs {
   long long ld_out, bs_out; // same for out
   int B, n, H, G, r;      // r = half window, clamped to [0, n]
   float c2;               // softmax scale * log2(e)
-  // score partials (null: skip the exact-probability pass)
-  float* part_band;       // [B, H, nqb, rwp]
-  float* part_extra;      // [B, H, nqb, G]
-  float* part_grow;       // [B, H, ngc, n]
-  int nqb, rwp, ngc, nkc, Gp;
+  // score partials (null: skip the exact-probability column sums)
+  float* part_band;       // [B, H, n]      band column sums of non-global keys
+  float* part_extra;      // [B, H, nqr, G] global-key columns per 512-query range
+  float* part_grow;       // [B, H, ngc, n] column sums over the global rows
+  int nqb, rwp, ngc, nkc, Gp, nkb, nqr;
+  int n_gr, n_bcol;       // block counts of the global-row and band-column parts of a launch
   // global-row split partials (workspace)
   float* gr_ml;           // [B, H, nkc, Gp, 2]
   float* gr_o;            // [B, H, nkc, Gp, 64]
@@ -43,7 +44,7 @@ struct AttnArgs {
 };
 
 struct AttnGeom {
-  int nqb, rwp, ngc, Gp, nkc, r, bw, rb;
+  int nqb, rwp, ngc, Gp, nkc, r, bw, rb, nkb, nqr;
 };
 
 AttnGeom attn_geom(int n, int window, int G);

@@ -99,11 +99,10 @@ def test_workspace_checked():
 
 def test_sizes():
     d = desc()
-    # partials: per (b, h): nqb * (rwp + G) + ngc * n floats; rwp = min(64 + 2r, n)
-    nqb, rwp = 4, min(64 + 64, 256)
-    assert sc.sc_score_partials_size(d) == 4 * 2 * 4 * (nqb * rwp)
+    # partials: per (b, h): n band column sums + ceil(n/512) * G global columns + ceil(G/64) * n global-row sums
+    assert sc.sc_score_partials_size(d) == 4 * 2 * 4 * 256
     dg = desc(global_pos=FakeT(0x50000), G=3)
-    assert sc.sc_score_partials_size(dg) == 4 * 2 * 4 * (nqb * (rwp + 3) + 1 * 256)
+    assert sc.sc_score_partials_size(dg) == 4 * 2 * 4 * (256 + 1 * 3 + 1 * 256)
     # band layout: [B,H,n,2r+1] + [B,H,n,G] + [B,H,G,n]
     assert sc.sc_band_probs_size(dg) == 4 * 2 * 4 * 256 * (65 + 2 * 3)
     # huge window: r clamps to n - 1 for the band layout
