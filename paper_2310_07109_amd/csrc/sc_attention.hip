@@ -212,21 +212,30 @@ SC_DEV void store_row4(typename Tr<DT>::T* dst, f32x4 v) {
 
 // LDS shared by all block types of a launch (each block type uses its own
 // subset; pointers are handed to the per-type device functions).
-template <int DT, bool kWithV>
-struct SmemT {
+// Launch 1 (softmax and P.V): double-buffered K and V tiles.  The query tile
+// is staged in b[1] before the pipeline starts: its fragments move to
+// registers first, and b[1] is only written after a barrier.
+template <int DT>
+struct Smem {
   using T = typename Tr<DT>::T;
   static constexpr int P = Tr<DT>::kPitch;
-  __attribute__((aligned(16))) T a[kBQ * P];     // query tile (pass 1, global rows) / key block (columns)
-  __attribute__((aligned(16))) T b[2][kBK * P];  // key tiles (pass 1, global rows) / query tiles (columns)
-  __attribute__((aligned(16))) T c[kWithV ? 2 : 1][kWithV ? kBK * P : 8];  // value tiles (pass 1)
+  __attribute__((aligned(16))) T b[2][kBK * P];  // key tiles (query tile first in b[1])
+  __attribute__((aligned(16))) T c[2][kBK * P];  // value tiles
+  int pos[2][kBK];                                 // positions of gathered rows
+  int misc[4];
+};
+// Launch 2 (column sums): a resident key block, double-buffered query tiles
+// with their log2-LSE.
+template <int DT>
+struct SmemCol {
+  using T = typename Tr<DT>::T;
+  static constexpr int P = Tr<DT>::kPitch;
+  __attribute__((aligned(16))) T a[kBK * P];     // key block
+  __attribute__((aligned(16))) T b[2][kBQ * P];  // query tiles (key tiles for the global rows)
   __attribute__((aligned(16))) float l[2][kBQ];  // log2-LSE of staged query rows
   int pos[2][kBK];                                 // positions of gathered rows
   int misc[4];
 };
-template <int DT>
-using Smem = SmemT<DT, true>;      // launch 1 (softmax and P.V need V tiles)
-template <int DT>
-using SmemCol = SmemT<DT, false>;  // launch 2 (column sums need no V)
 
 // -------------------------------------------------------- window pass 1 -----
 // Geometry of one window block (sequence b, head h, queries q0 .. q0+63) and
@@ -358,7 +367,7 @@ SC_DEV void window_fwd_block(const AttnArgs& a, int blk, Smem<DT>& sm, uint32_t*
   {  // padding query rows are staged as zeros: their (unused) logits stay finite
     Stage<DT> sq;
     sq.load_range(Qg + (long long)q0 * a.ld_in, a.ld_in, 0, L - q0);
-    sq.store(sm.a);
+    sq.store(sm.b[1]);
   }
   const int ntile = win_tables(a, wb, sBits, sXList, &sm.misc[0]);
   auto gbit = [&](int k) -> bool {
@@ -368,7 +377,7 @@ SC_DEV void window_fwd_block(const AttnArgs& a, int blk, Smem<DT>& sm, uint32_t*
   WinLoader<DT> ld{a, wb, wb.nxc ? a.gpos + (long long)wb.b * a.G : nullptr, sXList};
 
   Frag qf[TR::kChunks];
-  TR::load_frags(sm.a + (16 * w + lr) * P, g, qf);
+  TR::load_frags(sm.b[1] + (16 * w + lr) * P, g, qf);
   const int qa = q0 + 16 * w;
   const int qrow = qa + lr;
   float m_use = kNegBig, l_run = 0.f;
@@ -379,7 +388,7 @@ SC_DEV void window_fwd_block(const AttnArgs& a, int blk, Smem<DT>& sm, uint32_t*
   // band tiles: double-buffered, the next tile's loads overlap this tile's math
   ld.load(0, Kg, Vg);
   ld.store(0, sm.b[0], sm.c[0], sm.pos[0]);
-  __syncthreads();
+  __syncthreads();  // also: every wave holds its query fragments before b[1] is reused
   for (int t = 0; t < nkt; ++t) {
     const int buf = t & 1;
     if (t + 1 < nkt) ld.load(t + 1, Kg, Vg);
@@ -490,7 +499,7 @@ SC_DEV void gr_fwd_block(const AttnArgs& a, int lin, Smem<DT>& sm) {
     Stage<DT> sq;
     const int* sp = sm.pos[0];
     sq.load_rows(Qg, a.ld_in, [&](int row) { return sp[row]; });
-    sq.store(sm.a);
+    sq.store(sm.b[1]);
   }
   stk.load_range(Kg, a.ld_in, kbeg, kend);
   stv.load_range(Vg, a.ld_in, kbeg, kend);
@@ -498,7 +507,8 @@ SC_DEV void gr_fwd_block(const AttnArgs& a, int lin, Smem<DT>& sm) {
   stv.store(sm.c[0]);
   __syncthreads();
   typename TR::Frag qf[TR::kChunks];
-  TR::load_frags(sm.a + (16 * w + lr) * P, g, qf);
+  TR::load_frags(sm.b[1] + (16 * w + lr) * P, g, qf);
+  __syncthreads();  // every wave holds its query fragments before b[1] is reused
   float m_use = kNegBig, l_run = 0.f;
   f32x4 o[4];
 #pragma unroll
@@ -536,7 +546,7 @@ SC_DEV void gr_fwd_block(const AttnArgs& a, int lin, Smem<DT>& sm) {
 // Launch 1: global-row forward blocks first (when there are global tokens),
 // then the window pass-1 blocks.
 template <int DT>
-__global__ __launch_bounds__(kThreads) SC_OCC(3) void k_attn_fwd(AttnArgs a) {
+__global__ __launch_bounds__(kThreads) SC_OCC(4) void k_attn_fwd(AttnArgs a) {
   __shared__ Smem<DT> sm;
   extern __shared__ uint32_t sDyn[];
   if ((int)blockIdx.x < a.n_gr)
@@ -823,40 +833,53 @@ __global__ __launch_bounds__(kThreads) SC_OCC(kBandProbs ? 2 : 4) void k_attn_co
 // ------------------------------------------------------ score reduction ----
 // scores[b, k] = (sum over heads of: the band column sum of k, its global
 // column (summed over query ranges) if k is global, and the global rows'
-// column sums) / (H * L).  One thread per key; fixed order; no atomics.
-__global__ __launch_bounds__(256) void k_score_from_partials(const float* part, const int* valid_len, const int* gpos,
-                                                             int B, int n, int H, int G, AttnGeom geo,
-                                                             float* scores) {
-  __shared__ int smap[256];
-  const int b = blockIdx.y, kb = blockIdx.x * 256, tid = threadIdx.x, k = kb + tid;
+// column sums) / (H * L).  Workgroup = 64 keys x 4 head groups; group j sums
+// heads j, j + 4, ...; the 4 group sums are added in group order.  Fixed
+// order everywhere; no atomics.
+constexpr int kScoreKeys = 64;
+constexpr int kScoreGroups = 4;
+
+__global__ __launch_bounds__(kScoreKeys * kScoreGroups) void k_score_from_partials(
+    const float* part, const int* valid_len, const int* gpos, int B, int n, int H, int G, AttnGeom geo,
+    float* scores) {
+  __shared__ int smap[kScoreKeys];
+  __shared__ float red[kScoreGroups][kScoreKeys];
+  const int b = blockIdx.y, kb = blockIdx.x * kScoreKeys, tid = threadIdx.x;
+  const int lane = tid % kScoreKeys, hg = tid / kScoreKeys, k = kb + lane;
   const int L = clampi(valid_len[b], 0, n);
-  smap[tid] = -1;
+  if (tid < kScoreKeys) smap[tid] = -1;
   __syncthreads();
   if (gpos)
-    for (int j = tid; j < G; j += 256) {
+    for (int j = tid; j < G; j += blockDim.x) {
       const int p = gpos[(long long)b * G + j];
-      if (p >= kb && p < kb + 256 && p < L) smap[p - kb] = j;
+      if (p >= kb && p < kb + kScoreKeys && p < L) smap[p - kb] = j;
     }
   __syncthreads();
-  if (k >= n) return;
-  if (k >= L) {
-    scores[(long long)b * n + k] = 0.f;
-    return;
-  }
-  const float* band = part;
-  const float* gcol = band + (size_t)B * H * n;
-  const float* grow = gcol + (size_t)B * H * geo.nqr * G;
-  const int slot = smap[tid];
-  const int nqrv = (L + kGlobalKeySpan - 1) / kGlobalKeySpan;
   float acc = 0.f;
-  for (int h = 0; h < H; ++h) {
-    const long long bh = (long long)b * H + h;
-    acc += band[bh * n + k];
-    if (slot >= 0)
-      for (int qr = 0; qr < nqrv; ++qr) acc += gcol[(bh * geo.nqr + qr) * G + slot];
-    for (int gc = 0; gc < geo.ngc; ++gc) acc += grow[(bh * geo.ngc + gc) * n + k];
+  if (k < L) {
+    const float* band = part;
+    const float* gcol = band + (size_t)B * H * n;
+    const float* grow = gcol + (size_t)B * H * geo.nqr * G;
+    const int slot = smap[lane];
+    const int nqrv = (L + kGlobalKeySpan - 1) / kGlobalKeySpan;
+#pragma unroll 4
+    for (int h = hg; h < H; h += kScoreGroups) {
+      const long long bh = (long long)b * H + h;
+      float v = band[bh * n + k];
+      for (int gc = 0; gc < geo.ngc; ++gc) v += grow[(bh * geo.ngc + gc) * n + k];
+      if (slot >= 0)
+        for (int qr = 0; qr < nqrv; ++qr) v += gcol[(bh * geo.nqr + qr) * G + slot];
+      acc += v;
+    }
   }
-  scores[(long long)b * n + k] = acc / ((float)H * (float)L);
+  red[hg][lane] = acc;
+  __syncthreads();
+  if (hg == 0 && k < n) {
+    float tot = 0.f;
+#pragma unroll
+    for (int j = 0; j < kScoreGroups; ++j) tot += red[j][lane];
+    scores[(long long)b * n + k] = k < L ? tot / ((float)H * (float)L) : 0.f;
+  }
 }
 
 // Paper layout: the score of key k is its band sub-diagonal (entries (i, j)
@@ -1002,9 +1025,9 @@ hipError_t launch_window_attention(int dtype, const AttnArgs& a, hipStream_t s) 
 
 hipError_t launch_score_from_partials(const float* partials, const int* valid_len, const int* gpos, int B, int n,
                                       int H, int G, const AttnGeom& g, float* scores, hipStream_t s) {
-  dim3 grid((n + 255) / 256, B);
-  hipLaunchKernelGGL(k_score_from_partials, grid, dim3(256), 0, s, partials, valid_len, G > 0 ? gpos : nullptr, B, n,
-                     H, G, g, scores);
+  dim3 grid((n + kScoreKeys - 1) / kScoreKeys, B);
+  hipLaunchKernelGGL(k_score_from_partials, grid, dim3(kScoreKeys * kScoreGroups), 0, s, partials, valid_len,
+                     G > 0 ? gpos : nullptr, B, n, H, G, g, scores);
   return hipGetLastError();
 }
 
