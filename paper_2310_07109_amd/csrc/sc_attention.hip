@@ -75,11 +75,13 @@ struct Stage {
       r[i] = k >= 0 ? *reinterpret_cast<const uint4*>(g + (long long)k * ld + part * kEpc) : make_uint4(0, 0, 0, 0);
     }
   }
+  // into a key / query tile (kValue false) or a value tile (kValue true)
+  template <bool kValue = false>
   SC_DEV void store(T* lds) const {
 #pragma unroll
     for (int i = 0; i < kCpt; ++i) {
       const int c = threadIdx.x + kThreads * i, row = c / kCpr, part = c % kCpr;
-      *reinterpret_cast<uint4*>(lds + row * P + part * kEpc) = r[i];
+      *reinterpret_cast<uint4*>(lds + (kValue ? Tr<DT>::voff(row, part) : Tr<DT>::off(row, part))) = r[i];
     }
   }
 };
@@ -99,7 +101,7 @@ SC_DEV void softmax_tile(const typename Tr<DT>::Frag (&qf)[Tr<DT>::kChunks], con
 #pragma unroll
   for (int st = 0; st < 4; ++st) {
     typename TR::Frag kf[TR::kChunks];
-    TR::load_frags(sK + (16 * st + lr) * P, g, kf);
+    TR::load_frags(sK, 16 * st + lr, g, kf);
     f32x4 acc = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
     for (int c = 0; c < TR::kChunks; ++c) acc = TR::mma(kf[c], qf[c], acc);
@@ -141,8 +143,10 @@ SC_DEV void softmax_tile(const typename Tr<DT>::Frag (&qf)[Tr<DT>::kChunks], con
         pb[i] = (__bf16)p[2 * kc][i];
         pb[4 + i] = (__bf16)p[2 * kc + 1][i];
       }
-      const typename TR::T* v0 = sV + (32 * kc + 4 * g + (lr >> 2)) * P + 4 * (lr & 3);
-      const typename TR::T* v1 = v0 + 16 * P;
+      // lane (g, lr) supplies dims 16dt + 4(lr&3) .. +3 of value rows
+      // 32kc + 4g + lr/4 and 32kc + 16 + 4g + lr/4
+      const typename TR::T* v0 = sV + TR::voff(32 * kc + 4 * g + (lr >> 2), 0) + 4 * (lr & 3);
+      const typename TR::T* v1 = v0 + 16 * TR::kPitchV;
 #pragma unroll
       for (int dt = 0; dt < 4; ++dt) {
         const i16x4 a0 = lds_read_tr16(v0 + 16 * dt);
@@ -157,7 +161,8 @@ SC_DEV void softmax_tile(const typename Tr<DT>::Frag (&qf)[Tr<DT>::kChunks], con
 #pragma unroll
       for (int i = 0; i < 4; ++i)
 #pragma unroll
-        for (int dt = 0; dt < 4; ++dt) o[dt] = TR::mma(sV[(16 * st + 4 * g + i) * P + 16 * dt + lr], p[st][i], o[dt]);
+        for (int dt = 0; dt < 4; ++dt)
+          o[dt] = TR::mma(sV[TR::voff(16 * st + 4 * g + i, 4 * dt + (lr >> 2)) + (lr & 3)], p[st][i], o[dt]);
   }
 }
 
@@ -176,7 +181,7 @@ SC_DEV float col_tile(const typename Tr<DT>::Frag (&kf)[Tr<DT>::kChunks], const 
 #pragma unroll
   for (int qst = 0; qst < 4; ++qst) {
     typename TR::Frag qf[TR::kChunks];
-    TR::load_frags(sQ + (16 * qst + lr) * TR::kPitch, g, qf);
+    TR::load_frags(sQ, 16 * qst + lr, g, qf);
     const f32x4 l2 = *reinterpret_cast<const f32x4*>(sL + 16 * qst + 4 * g);
     f32x4 acc = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
@@ -220,7 +225,7 @@ struct Smem {
   using T = typename Tr<DT>::T;
   static constexpr int P = Tr<DT>::kPitch;
   __attribute__((aligned(16))) T b[2][kBK * P];  // key tiles (query tile first in b[1])
-  __attribute__((aligned(16))) T c[2][kBK * P];  // value tiles
+  __attribute__((aligned(16))) T c[2][kBK * Tr<DT>::kPitchV];  // value tiles
   int pos[2][kBK];                                 // positions of gathered rows
   int misc[4];
 };
@@ -326,7 +331,7 @@ struct WinLoader {
   }
   SC_DEV void store(int t, T* sK, T* sV, int* sPos) const {
     stk.store(sK);
-    stv.store(sV);
+    stv.template store<true>(sV);
     if (t >= wb.nkt && threadIdx.x < kBK) sPos[threadIdx.x] = pos_reg;
   }
 };
@@ -377,7 +382,7 @@ SC_DEV void window_fwd_block(const AttnArgs& a, int blk, Smem<DT>& sm, uint32_t*
   WinLoader<DT> ld{a, wb, wb.nxc ? a.gpos + (long long)wb.b * a.G : nullptr, sXList};
 
   Frag qf[TR::kChunks];
-  TR::load_frags(sm.b[1] + (16 * w + lr) * P, g, qf);
+  TR::load_frags(sm.b[1], 16 * w + lr, g, qf);
   const int qa = q0 + 16 * w;
   const int qrow = qa + lr;
   float m_use = kNegBig, l_run = 0.f;
@@ -504,10 +509,10 @@ SC_DEV void gr_fwd_block(const AttnArgs& a, int lin, Smem<DT>& sm) {
   stk.load_range(Kg, a.ld_in, kbeg, kend);
   stv.load_range(Vg, a.ld_in, kbeg, kend);
   stk.store(sm.b[0]);
-  stv.store(sm.c[0]);
+  stv.template store<true>(sm.c[0]);
   __syncthreads();
   typename TR::Frag qf[TR::kChunks];
-  TR::load_frags(sm.b[1] + (16 * w + lr) * P, g, qf);
+  TR::load_frags(sm.b[1], 16 * w + lr, g, qf);
   __syncthreads();  // every wave holds its query fragments before b[1] is reused
   float m_use = kNegBig, l_run = 0.f;
   f32x4 o[4];
@@ -528,7 +533,7 @@ SC_DEV void gr_fwd_block(const AttnArgs& a, int lin, Smem<DT>& sm) {
     }
     if (t + 1 < ntile) {
       stk.store(sm.b[buf ^ 1]);
-      stv.store(sm.c[buf ^ 1]);
+      stv.template store<true>(sm.c[buf ^ 1]);
     }
     __syncthreads();
   }
@@ -610,7 +615,7 @@ SC_DEV void band_col_block(const AttnArgs& a, int blk, SmemCol<DT>& sm) {
   store(0);
   __syncthreads();
   typename TR::Frag kf[TR::kChunks];
-  TR::load_frags(sm.a + (16 * w + lr) * P, g, kf);
+  TR::load_frags(sm.a, 16 * w + lr, g, kf);
   const int key = k0 + 16 * w + lr;
   const bool kuse = key < kend && !((gmask[(key - k0) >> 5] >> ((key - k0) & 31)) & 1u);
   float* bpb = kBandProbs ? a.bp_band + (long long)bh * n * a.bw : nullptr;
@@ -690,7 +695,7 @@ SC_DEV void gcol_block(const AttnArgs& a, int lin, SmemCol<DT>& sm) {
   store(0);
   __syncthreads();
   typename TR::Frag kf[TR::kChunks];
-  TR::load_frags(sm.a + (16 * w + lr) * P, g, kf);
+  TR::load_frags(sm.a, 16 * w + lr, g, kf);
   const int slot = kGlobalChunk * gc + 16 * w + lr;
   const bool kuse = pos[16 * w + lr] >= 0;
   float* bpc = kBandProbs ? a.bp_gcol + (long long)bh * n * G : nullptr;
@@ -791,7 +796,7 @@ SC_DEV void gr_col_block(const AttnArgs& a, int lin, SmemCol<DT>& sm) {
     if (t + 1 < ntile) stk.load_range(Kg, a.ld_in, k0 + kBK, kend);
     // this wave's 16 keys as the K operand, the 64 global rows as queries
     typename TR::Frag kf[TR::kChunks];
-    TR::load_frags(sm.b[buf] + (16 * w + lr) * P, g, kf);
+    TR::load_frags(sm.b[buf], 16 * w + lr, g, kf);
     const int key = k0 + 16 * w + lr;
     const bool kin = key < kend;
     float cs;
