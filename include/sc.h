@@ -79,6 +79,10 @@ typedef int32_t sc_status;
  *   valid_len   device int32 [B]: 0 <= valid_len[b] <= n.
  *   softmax_scale  alpha >= 0 applied to Q.K^T before the softmax (finite).
  *   dtype       SC_F32 or SC_BF16 for q, k, v and outputs.
+ * Sizes the kernels cannot index return SC_EUNSUPPORTED: one sequence's rows
+ * of q, k or v (n * H * d elements; for sc_encoder_attn_stack its fused q|k|v
+ * rows, 3 * n * H * d) must span less than 4 GiB, and each launch grid must
+ * have fewer than 2^31 workgroups.
  */
 typedef struct sc_attn_desc {
   int32_t B, n, H, d;

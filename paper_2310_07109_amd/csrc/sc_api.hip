@@ -1,6 +1,8 @@
 // C ABI of the library (declared in include/sc.h): argument validation on the
 // host, workspace carving, and launch sequencing on the caller's stream.
 // Nothing here allocates device memory or synchronises.
+#include <algorithm>
+#include <cfloat>
 #include <cmath>
 #include <cstdint>
 #include <cstring>
@@ -33,6 +35,8 @@ sc_status check_desc(const sc_attn_desc* d) {
   const long long blocks = (long long)((d->n + 63) / 64) * d->H * d->B;
   if (blocks >= (1LL << 31)) return SC_EUNSUPPORTED;
   if ((long long)d->B * d->n >= (1LL << 31)) return SC_EUNSUPPORTED;
+  // tile loads address one sequence's rows with 32-bit byte offsets
+  if ((long long)d->n * d->H * d->d * (long long)elem_size(d->dtype) >= (1LL << 32)) return SC_EUNSUPPORTED;
   return SC_OK;
 }
 
@@ -66,7 +70,11 @@ AttnArgs make_attn_args(const sc_attn_desc* d, const AttnGeom& geo) {
   a.H = d->H;
   a.G = d->G;
   a.r = geo.r;
-  a.c2 = d->softmax_scale * 1.4426950408889634f;
+  // Scale in log2 units.  The kernels need c2 > 0 (disallowed logits are set
+  // to -inf and exp2(-inf * c2) must be 0); a zero scale becomes the smallest
+  // normal float, which yields the same fp32 probabilities for logits below
+  // 2^26 in magnitude (every scaled logit then rounds away next to 1 in exp2).
+  a.c2 = std::max(d->softmax_scale * 1.4426950408889634f, FLT_MIN);
   a.nqb = geo.nqb;
   a.rwp = geo.rwp;
   a.ngc = geo.ngc;
@@ -312,6 +320,7 @@ sc_status sc_encoder_attn_stack(const sc_attn_desc* d, int32_t n_layers, const v
   if (st != SC_OK) return st;
   if (d->dtype != SC_BF16) return SC_EUNSUPPORTED;
   if ((long long)d->H * d->d > 2048) return SC_EUNSUPPORTED;
+  if ((long long)d->n * 3 * d->H * d->d * 2 >= (1LL << 32)) return SC_EUNSUPPORTED;  // fused q|k|v rows
   if (n_layers < 1 || !x_in || !Wqkv || !Wo || !thresholds || !x_out || !final_len) return SC_EINVAL;
   if (!(ln_eps > 0.f) || !std::isfinite(ln_eps)) return SC_EINVAL;
   for (int l = 0; l < n_layers; ++l)

@@ -114,7 +114,7 @@ SC_DEV void softmax_tile(const typename Tr<DT>::Frag (&qf)[Tr<DT>::kChunks], con
 #pragma unroll
     for (int i = 0; i < 4; ++i) {
       valid[st][i] = !kMasked || ok(st, i);
-      tmax = fmaxf(tmax, valid[st][i] ? s[st][i] : -INFINITY);
+      tmax = vmax(tmax, valid[st][i] ? s[st][i] : -INFINITY);
     }
   tmax = group_max(tmax) * c2;
   if (tmax > m_use + kTau) {
@@ -145,12 +145,11 @@ SC_DEV void softmax_tile(const typename Tr<DT>::Frag (&qf)[Tr<DT>::kChunks], con
       }
       // lane (g, lr) supplies dims 16dt + 4(lr&3) .. +3 of value rows
       // 32kc + 4g + lr/4 and 32kc + 16 + 4g + lr/4
-      const typename TR::T* v0 = sV + TR::voff(32 * kc + 4 * g + (lr >> 2), 0) + 4 * (lr & 3);
-      const typename TR::T* v1 = v0 + 16 * TR::kPitchV;
+      const int vr = 32 * kc + 4 * g + (lr >> 2), b = (lr >> 1) & 1, e = 4 * (lr & 1);
 #pragma unroll
       for (int dt = 0; dt < 4; ++dt) {
-        const i16x4 a0 = lds_read_tr16(v0 + 16 * dt);
-        const i16x4 a1 = lds_read_tr16(v1 + 16 * dt);
+        const i16x4 a0 = lds_read_tr16(sV + TR::voff(vr, 2 * dt + b) + e);
+        const i16x4 a1 = lds_read_tr16(sV + TR::voff(vr + 16, 2 * dt + b) + e);
         const i16x8 a = __builtin_shufflevector(a0, a1, 0, 1, 2, 3, 4, 5, 6, 7);
         o[dt] = TR::mma(__builtin_bit_cast(bf16x8, a), pb, o[dt]);
       }
@@ -243,24 +242,23 @@ struct SmemCol {
 };
 
 // -------------------------------------------------------- window pass 1 -----
-// Geometry of one window block (sequence b, head h, queries q0 .. q0+63) and
+// Geometry of one window block (sequence b, head h, queries q0 .. q0+QB-1) and
 // its LDS tables: the global-token bitmask over the key range [kt0, kt1) and
 // the list of 64-slot chunks that hold global keys outside that range.
 struct WinBlock {
   int qb, bh, h, b, L, q0, kt0, kt1, nkt, nwords, nxc;
 };
 
+template <int QB = kBQ>
 SC_DEV WinBlock win_block(const AttnArgs& a, int blk) {
   WinBlock wb;
-  const int lin = xcd_remap(blk, a.nqb * a.H * a.B);
-  wb.qb = lin % a.nqb;
-  wb.bh = lin / a.nqb;
+  xcd_pair_map(blk, a.nqb, a.H * a.B, wb.bh, wb.qb);
   wb.h = wb.bh % a.H;
   wb.b = wb.bh / a.H;
   wb.L = clampi(a.valid_len[wb.b], 0, a.n);
-  wb.q0 = wb.qb * kBQ;
+  wb.q0 = wb.qb * QB;
   wb.kt0 = max(0, wb.q0 - a.r);
-  wb.kt1 = min(wb.L, wb.q0 + kBQ + a.r);
+  wb.kt1 = min(wb.L, wb.q0 + QB + a.r);
   wb.nkt = (wb.kt1 - wb.kt0 + kBK - 1) / kBK;
   wb.nwords = (wb.kt1 - wb.kt0 + 31) >> 5;
   wb.nxc = (a.gpos && a.G > 0) ? (a.G + kBK - 1) / kBK : 0;
@@ -488,6 +486,7 @@ SC_DEV void gr_fwd_block(const AttnArgs& a, int lin, Smem<DT>& sm) {
   using TR = Tr<DT>;
   using T = typename TR::T;
   constexpr int P = TR::kPitch;
+  if (lin >= a.nkc * a.ngc * a.H * a.B) return;  // padding of the block count to a multiple of 8
   const GrBlock blk = gr_block(a, lin);
   const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6, g = lane >> 4, lr = lane & 15;
   const int L = clampi(a.valid_len[blk.b], 0, a.n);
@@ -548,14 +547,299 @@ SC_DEV void gr_fwd_block(const AttnArgs& a, int lin, Smem<DT>& sm) {
   for (int dt = 0; dt < 4; ++dt) *reinterpret_cast<f32x4*>(a.gr_o + idx * kHeadDim + 16 * dt + 4 * g) = o[dt];
 }
 
+
+// ------------------------------------------- bf16 pass 1, 32 queries a wave --
+// A wave owns 32 queries as two 16-query sub-blocks that share every K
+// fragment and every V read (two MFMAs per LDS read).  K/V tiles reach LDS
+// through the direct global->LDS loads of gfx950, without staging registers:
+// lane i of a wave load fills the 16 bytes at base + 16 i, so the swizzled
+// layout is produced by choosing which 16-byte unit of its row lane i fetches.
+constexpr int kBQ2 = 128;
+
+// One direct load: lane i's 16 bytes at base + voff land at LDS byte address
+// lds + 16 i (gfx950 global_load_lds_dwordx4, destination base in m0).  Inline
+// assembly on purpose: the compiler cannot tell these writes from later LDS
+// reads of the other tile buffer and would wait for them before every read;
+// here they are completed explicitly by wait_dma() before the barrier that
+// publishes the tile.
+SC_DEV unsigned lds_addr(const void* p) {
+  return (unsigned)(size_t)(const __attribute__((address_space(3))) void*)p;
+}
+SC_DEV void lds_dma16(const void* base, unsigned voff, unsigned lds) {
+  asm volatile("s_mov_b32 m0, %2\n\ts_nop 0\n\tglobal_load_lds_dwordx4 %0, %1"
+               :
+               : "v"(voff), "s"(base), "s"(lds)
+               : "memory", "m0");
+}
+SC_DEV void wait_dma() { asm volatile("s_waitcnt vmcnt(0)" ::: "memory"); }
+
+// Rows 16w .. 16w+15 of a 64-row bf16 tile (two wave loads of 8 rows); tile
+// row R holds global row rowfn(R), which must be a valid row.  Byte offsets
+// from the slice base fit in 32 bits (checked by the host).
+template <typename RowFn>
+SC_DEV void tile_dma(const __bf16* g, unsigned ld_bytes, __bf16* tile, int w, int lane, RowFn rowfn) {
+#pragma unroll
+  for (int j = 0; j < 2; ++j) {
+    const int R0 = 16 * w + 8 * j, R = R0 + (lane >> 3);
+    const unsigned u = (lane & 7) ^ (lane >> 3);  // slot (lane & 7) of row R holds unit slot ^ (R & 7)
+    lds_dma16(g, (unsigned)rowfn(R) * ld_bytes + 16u * u, lds_addr(tile + R0 * Tr<1>::kPitch));
+  }
+}
+
+// One 64-key tile for the two query sub-blocks of a wave.  Bit st of `live`
+// (wave-uniform) says whether 16-key sub-tile st can hold an allowed pair; in
+// masked tiles ok(j, st, i) decides the pair (sub-block j's query, key
+// 16 st + 4g + i).  Disallowed logits become -inf, which exp2 maps to 0
+// (c2 > 0 is guaranteed by the host).
+template <bool kMasked, typename OkFn>
+SC_DEV void softmax_tile2(const bf16x8 (&qf)[2][2], const __bf16* sK, const __bf16* sV, float c2, int lr, int g,
+                          float (&m_use)[2], float (&l_run)[2], f32x4 (&o)[2][4], unsigned live, OkFn ok) {
+  using TR = Tr<1>;
+  auto is_live = [&](int st) { return !kMasked || ((live >> st) & 1u); };
+  f32x4 s[2][4];
+#pragma unroll
+  for (int st = 0; st < 4; ++st) {
+    s[0][st] = f32x4{0.f, 0.f, 0.f, 0.f};
+    s[1][st] = f32x4{0.f, 0.f, 0.f, 0.f};
+    if (is_live(st)) {
+      bf16x8 kf[2];
+      TR::load_frags(sK, 16 * st + lr, g, kf);
+#pragma unroll
+      for (int j = 0; j < 2; ++j) {
+        s[j][st] = TR::mma(kf[0], qf[j][0], s[j][st]);
+        s[j][st] = TR::mma(kf[1], qf[j][1], s[j][st]);
+      }
+    }
+  }
+  if constexpr (kMasked) {
+#pragma unroll
+    for (int j = 0; j < 2; ++j)
+#pragma unroll
+      for (int st = 0; st < 4; ++st)
+#pragma unroll
+        for (int i = 0; i < 4; ++i) s[j][st][i] = (is_live(st) && ok(j, st, i)) ? s[j][st][i] : -INFINITY;
+  }
+  // raise a running max only when the tile max exceeds it by kTau (lanes
+  // that do not need it skip the rescale under the execution mask)
+#pragma unroll
+  for (int j = 0; j < 2; ++j) {
+    float m4[4];
+#pragma unroll
+    for (int st = 0; st < 4; ++st) m4[st] = vmax(vmax(s[j][st][0], s[j][st][1]), vmax(s[j][st][2], s[j][st][3]));
+    const float tmax = group_max(vmax(vmax(m4[0], m4[1]), vmax(m4[2], m4[3]))) * c2;
+    if (tmax > m_use[j] + kTau) {
+      const float f = fast_exp2(m_use[j] - tmax);
+      l_run[j] *= f;
+#pragma unroll
+      for (int dt = 0; dt < 4; ++dt) o[j][dt] *= f;
+      m_use[j] = tmax;
+    }
+  }
+  bf16x8 pb[2][2];
+#pragma unroll
+  for (int j = 0; j < 2; ++j) {
+    float part[4];
+#pragma unroll
+    for (int st = 0; st < 4; ++st) {
+      float p[4];
+#pragma unroll
+      for (int i = 0; i < 4; ++i) p[i] = fast_exp2(fmaf(s[j][st][i], c2, -m_use[j]));
+      part[st] = (p[0] + p[1]) + (p[2] + p[3]);
+#pragma unroll
+      for (int i = 0; i < 4; ++i) pb[j][st >> 1][4 * (st & 1) + i] = (__bf16)p[i];
+    }
+    l_run[j] += (part[0] + part[1]) + (part[2] + part[3]);
+  }
+  // O^T += V^T P^T: the V operand comes from transposed reads of the
+  // row-major tile; lane (g, lr) supplies dims 16dt + 4(lr&3) .. +3 of rows
+  // 32kc + 4g + lr/4 and 32kc + 16 + 4g + lr/4 (keys in MFMA order)
+#pragma unroll
+  for (int kc = 0; kc < 2; ++kc) {
+    if (!is_live(2 * kc) && !is_live(2 * kc + 1)) continue;
+    const int vr = 32 * kc + 4 * g + (lr >> 2), b = (lr >> 1) & 1, e = 4 * (lr & 1);
+#pragma unroll
+    for (int dt = 0; dt < 4; ++dt) {
+      const i16x4 a0 = lds_read_tr16(sV + TR::off(vr, 2 * dt + b) + e);
+      const i16x4 a1 = lds_read_tr16(sV + TR::off(vr + 16, 2 * dt + b) + e);
+      const bf16x8 vf = __builtin_bit_cast(bf16x8, __builtin_shufflevector(a0, a1, 0, 1, 2, 3, 4, 5, 6, 7));
+      o[0][dt] = TR::mma(vf, pb[0][kc], o[0][dt]);
+      o[1][dt] = TR::mma(vf, pb[1][kc], o[1][dt]);
+    }
+  }
+}
+
+// Pass 1 for bf16: O, LSE and the log2 LSE of the block's 128 queries.
+SC_DEV void window_fwd_v2(const AttnArgs& a, int blk, Smem<1>& sm, uint32_t* sDyn) {
+  using T = __bf16;
+  const WinBlock wb = win_block<kBQ2>(a, blk);
+  const int tid = threadIdx.x, lane = tid & 63, w = __builtin_amdgcn_readfirstlane(tid >> 6), g = lane >> 4,
+            lr = lane & 15;
+  const int n = a.n, r = a.r, L = wb.L, q0 = wb.q0, kt0 = wb.kt0, kt1 = wb.kt1, nkt = wb.nkt;
+  const long long ld = a.ld_in;
+  const unsigned ldb = (unsigned)(2 * a.ld_in);
+  const T* Qg = static_cast<const T*>(a.q) + wb.b * a.bs_in + wb.h * kHeadDim;
+  const T* Kg = static_cast<const T*>(a.k) + wb.b * a.bs_in + wb.h * kHeadDim;
+  const T* Vg = static_cast<const T*>(a.v) + wb.b * a.bs_in + wb.h * kHeadDim;
+  T* Og = static_cast<T*>(a.out) + wb.b * a.bs_out + wb.h * kHeadDim;
+  float* lseg = a.lse ? a.lse + (long long)wb.bh * n : nullptr;
+  float* l2g = a.win_lse2 ? a.win_lse2 + (long long)wb.bh * n : nullptr;
+
+  if (q0 >= L) {  // padding block: zero output rows
+    for (int c = tid; c < kBQ2 * 8; c += kThreads) {
+      const int q = q0 + (c >> 3);
+      if (q < n) zero16(Og + (long long)q * a.ld_out + 8 * (c & 7));
+    }
+    for (int i = tid; i < kBQ2; i += kThreads)
+      if (q0 + i < n) {
+        if (lseg) lseg[q0 + i] = -INFINITY;
+        if (l2g) l2g[q0 + i] = INFINITY;
+      }
+    return;
+  }
+  uint32_t* sBits = sDyn;
+  int* sXList = reinterpret_cast<int*>(sDyn + a.rwp / 32 + 2);
+  auto band_rows = [&](int k0) { return [=](int R) { return min(k0 + R, kt1 - 1); }; };
+  tile_dma(Kg, ldb, sm.b[0], w, lane, band_rows(kt0));
+  tile_dma(Vg, ldb, sm.c[0], w, lane, band_rows(kt0));
+  const int ntile = win_tables(a, wb, sBits, sXList, &sm.misc[0]);
+  auto gbit = [&](int k) -> bool {
+    const int o = k - kt0;
+    return (sBits[o >> 5] >> (o & 31)) & 1u;
+  };
+  // query fragments straight from HBM (rows clamped below L; same dims per
+  // lane group as the key fragments)
+  const int qa = q0 + 32 * w;
+  bf16x8 qf[2][2];
+#pragma unroll
+  for (int j = 0; j < 2; ++j) {
+    const T* qrow = Qg + (long long)min(qa + 16 * j + lr, L - 1) * ld;
+    qf[j][0] = *reinterpret_cast<const bf16x8*>(qrow + 8 * g);
+    qf[j][1] = *reinterpret_cast<const bf16x8*>(qrow + 32 + 8 * g);
+  }
+  float m_use[2] = {kNegBig, kNegBig}, l_run[2] = {0.f, 0.f};
+  f32x4 o[2][4];
+#pragma unroll
+  for (int j = 0; j < 2; ++j)
+#pragma unroll
+    for (int dt = 0; dt < 4; ++dt) o[j][dt] = f32x4{0.f, 0.f, 0.f, 0.f};
+  // all vector loads so far (the first tiles, the query fragments) complete
+  // here; the compiler-visible wait keeps it from waiting for the query loads
+  // inside the tile loop, where the prefetch loads are in flight
+  __builtin_amdgcn_s_waitcnt(0x0F70);  // vmcnt(0)
+  wait_dma();
+  __syncthreads();
+
+  // per-lane band bounds of sub-block j relative to a tile start, shifted by
+  // the lane group's key offset 4g: key 16st + i of the lane is allowed when
+  // it lies in [lo - k0, hi - k0]
+  int lo[2], hi[2];
+#pragma unroll
+  for (int j = 0; j < 2; ++j) {
+    const int q = qa + 16 * j + lr;
+    lo[j] = q - r - 4 * g;
+    hi[j] = min(q + r, kt1 - 1) - 4 * g;
+  }
+  for (int t = 0; t < nkt; ++t) {
+    const int buf = t & 1, k0 = kt0 + t * kBK;
+    if (t + 1 < nkt) {
+      tile_dma(Kg, ldb, sm.b[buf ^ 1], w, lane, band_rows(k0 + kBK));
+      tile_dma(Vg, ldb, sm.c[buf ^ 1], w, lane, band_rows(k0 + kBK));
+    }
+    const unsigned long long gall = tile_gmask(sBits, t, wb.nwords);
+    const bool near = k0 <= qa + 31 + r && k0 + kBK - 1 >= qa - r;
+    if (near || gall != 0ull) {
+      if (k0 + kBK <= kt1 && k0 >= qa + 31 - r && k0 + kBK - 1 <= qa + r) {
+        softmax_tile2<false>(qf, sm.b[buf], sm.c[buf], a.c2, lr, g, m_use, l_run, o, 0xFu,
+                             [](int, int, int) { return true; });
+      } else {
+        const int wlo = qa - r - k0, whi = min(qa + 31 + r, kt1 - 1) - k0;
+        unsigned live = 0u;
+#pragma unroll
+        for (int st = 0; st < 4; ++st)
+          live |= (unsigned)((16 * st + 15 >= wlo && 16 * st <= whi) || ((gall >> (16 * st)) & 0xFFFFull) != 0ull)
+                  << st;
+        const int l0 = lo[0] - k0, h0 = hi[0] - k0, l1 = lo[1] - k0, h1 = hi[1] - k0;
+        if (gall == 0ull) {
+          softmax_tile2<true>(qf, sm.b[buf], sm.c[buf], a.c2, lr, g, m_use, l_run, o, live, [&](int j, int st, int i) {
+            const int c = 16 * st + i;
+            return j == 0 ? (c >= l0) & (c <= h0) : (c >= l1) & (c <= h1);
+          });
+        } else {
+          const unsigned long long gm = gall >> (4 * g);
+          softmax_tile2<true>(qf, sm.b[buf], sm.c[buf], a.c2, lr, g, m_use, l_run, o, live, [&](int j, int st, int i) {
+            const int c = 16 * st + i;
+            const bool band = j == 0 ? (c >= l0) & (c <= h0) : (c >= l1) & (c <= h1);
+            return band | (bool)((gm >> c) & 1ull);
+          });
+        }
+      }
+    }
+    if (t + 1 < nkt) wait_dma();
+    __syncthreads();
+  }
+  // global keys outside the block's key range, 64 slots per tile (few tiles;
+  // not pipelined)
+  const int* gp = wb.nxc ? a.gpos + (long long)wb.b * a.G : nullptr;
+  auto slot_row = [&](int c, int row) {
+    const int j = kBK * c + row;
+    const int p = j < a.G ? gp[j] : -1;
+    return (p >= 0 && p < L && (p < kt0 || p >= kt1)) ? p : -1;
+  };
+  for (int t = nkt; t < ntile; ++t) {
+    const int c = sXList[t - nkt];
+    auto rows = [&](int R) {
+      const int p = slot_row(c, R);
+      return p >= 0 ? p : kt0;
+    };
+    tile_dma(Kg, ldb, sm.b[0], w, lane, rows);
+    tile_dma(Vg, ldb, sm.c[0], w, lane, rows);
+    if (tid < kBK) sm.pos[0][tid] = slot_row(c, tid);
+    wait_dma();
+    __syncthreads();
+    const unsigned long long used = __ballot(sm.pos[0][lane] >= 0);
+    unsigned live = 0u;
+#pragma unroll
+    for (int st = 0; st < 4; ++st) live |= (unsigned)(((used >> (16 * st)) & 0xFFFFull) != 0ull) << st;
+    const unsigned long long gm = used >> (4 * g);
+    softmax_tile2<true>(qf, sm.b[0], sm.c[0], a.c2, lr, g, m_use, l_run, o, live,
+                        [&](int, int st, int i) { return (bool)((gm >> (16 * st + i)) & 1ull); });
+    __syncthreads();
+  }
+
+#pragma unroll
+  for (int j = 0; j < 2; ++j) {
+    const float l_row = group_sum(l_run[j]);
+    const int qrow = qa + 16 * j + lr;
+    const bool qin = qrow < L;
+    const bool qvalid = qin && !gbit(qrow);  // qrow in [q0, L) lies inside [kt0, kt1)
+    const float lse2 = m_use[j] + fast_log2(l_row);
+    if (qvalid) {
+      const float inv = 1.0f / l_row;
+#pragma unroll
+      for (int dt = 0; dt < 4; ++dt)
+        store_row4<1>(Og + (long long)qrow * a.ld_out + 16 * dt + 4 * g, o[j][dt] * inv);
+      if (g == 0 && lseg) lseg[qrow] = lse2 * kLn2;
+    } else if (!qin && qrow < n) {
+#pragma unroll
+      for (int dt = 0; dt < 4; ++dt)
+        store_row4<1>(Og + (long long)qrow * a.ld_out + 16 * dt + 4 * g, f32x4{0.f, 0.f, 0.f, 0.f});
+      if (g == 0 && lseg) lseg[qrow] = -INFINITY;
+    }
+    // excluded rows (global or padding) get +inf: their column-sum probabilities are 0
+    if (g == 0 && l2g && qrow < n) l2g[qrow] = qvalid ? lse2 : INFINITY;
+  }
+}
+
 // Launch 1: global-row forward blocks first (when there are global tokens),
 // then the window pass-1 blocks.
 template <int DT>
-__global__ __launch_bounds__(kThreads) SC_OCC(4) void k_attn_fwd(AttnArgs a) {
+__global__ __launch_bounds__(kThreads) SC_OCC(DT == 1 ? 3 : 2) void k_attn_fwd(AttnArgs a) {
   __shared__ Smem<DT> sm;
   extern __shared__ uint32_t sDyn[];
   if ((int)blockIdx.x < a.n_gr)
     gr_fwd_block<DT>(a, blockIdx.x, sm);
+  else if constexpr (DT == 1)
+    window_fwd_v2(a, blockIdx.x - a.n_gr, sm, sDyn);
   else
     window_fwd_block<DT>(a, blockIdx.x - a.n_gr, sm, sDyn);
 }
@@ -574,8 +858,9 @@ SC_DEV void band_col_block(const AttnArgs& a, int blk, SmemCol<DT>& sm) {
   using TR = Tr<DT>;
   using T = typename TR::T;
   constexpr int P = TR::kPitch;
-  const int lin = xcd_remap(blk, a.nkb * a.H * a.B);
-  const int kb = lin % a.nkb, bh = lin / a.nkb, h = bh % a.H, b = bh / a.H;
+  int kb, bh;
+  xcd_pair_map(blk, a.nkb, a.H * a.B, bh, kb);
+  const int h = bh % a.H, b = bh / a.H;
   const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6, g = lane >> 4, lr = lane & 15;
   const int n = a.n, r = a.r, G = a.G;
   const int L = clampi(a.valid_len[b], 0, n);
@@ -728,6 +1013,7 @@ SC_DEV void gr_col_block(const AttnArgs& a, int lin, SmemCol<DT>& sm) {
   using TR = Tr<DT>;
   using T = typename TR::T;
   constexpr int P = TR::kPitch;
+  if (lin >= a.nkc * a.ngc * a.H * a.B) return;  // padding of the block count to a multiple of 8
   const GrBlock blk = gr_block(a, lin);
   const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6, g = lane >> 4, lr = lane & 15;
   const int L = clampi(a.valid_len[blk.b], 0, a.n);
@@ -1005,10 +1291,17 @@ static hipError_t launch_window_t(const AttnArgs& a0, hipStream_t s) {
   AttnArgs a = a0;
   const bool glob = a.G > 0 && a.gpos;
   const bool cols = a.part_band || a.bp_band;
-  a.n_gr = glob ? a.nkc * a.ngc * a.H * a.B : 0;
+  // global-row blocks come first in both launches; their count is padded to a
+  // multiple of 8 so that the next block type starts on XCD 0
+  a.n_gr = glob ? (a.nkc * a.ngc * a.H * a.B + 7) & ~7 : 0;
   a.n_bcol = cols ? a.nkb * a.H * a.B : 0;
   const int n_gcol = (cols && glob) ? a.nqr * a.ngc * a.H * a.B : 0;
   const int nxc = glob ? (a.G + kBK - 1) / kBK : 0;
+  if (DT == 1) {  // bf16 pass 1 runs 128-query blocks
+    a.nqb = (a.n + kBQ2 - 1) / kBQ2;
+    const long long rw = (long long)kBQ2 + 2LL * a.r;
+    a.rwp = (int)(rw < a.n ? rw : a.n);
+  }
   const size_t dyn = sizeof(uint32_t) * ((size_t)a.rwp / 32 + 2 + nxc + 1);
   const unsigned fwd_blocks = (unsigned)(a.n_gr + a.nqb * a.H * a.B);
   const unsigned col_blocks = (unsigned)(a.n_gr + a.n_bcol + n_gcol);

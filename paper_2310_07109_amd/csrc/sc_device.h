@@ -23,6 +23,10 @@ constexpr float kLog2e = 1.4426950408889634f;
 constexpr float kLn2 = 0.6931471805599453f;
 
 SC_DEV float fast_exp2(float x) { return __builtin_amdgcn_exp2f(x); }
+
+// IEEE 754-2019 maximum (NaN-propagating): compiles to v_maximum3_f32 without
+// the NaN-quieting copies that fmaxf needs on MFMA results in IEEE mode.
+SC_DEV float vmax(float a, float b) { return __builtin_elementwise_maximum(a, b); }
 SC_DEV float fast_log2(float x) { return __builtin_amdgcn_logf(x); }
 
 // Cross-row exchanges on the VALU (gfx950 v_permlane16/32_swap).  With both
@@ -43,12 +47,12 @@ SC_DEV float xor32_sum(float v) {
 SC_DEV float xor16_max(float v) {
   const unsigned u = __builtin_bit_cast(unsigned, v);
   const auto r = __builtin_amdgcn_permlane16_swap(u, u, false, false);
-  return fmaxf(__builtin_bit_cast(float, (unsigned)r[0]), __builtin_bit_cast(float, (unsigned)r[1]));
+  return vmax(__builtin_bit_cast(float, (unsigned)r[0]), __builtin_bit_cast(float, (unsigned)r[1]));
 }
 SC_DEV float xor32_max(float v) {
   const unsigned u = __builtin_bit_cast(unsigned, v);
   const auto r = __builtin_amdgcn_permlane32_swap(u, u, false, false);
-  return fmaxf(__builtin_bit_cast(float, (unsigned)r[0]), __builtin_bit_cast(float, (unsigned)r[1]));
+  return vmax(__builtin_bit_cast(float, (unsigned)r[0]), __builtin_bit_cast(float, (unsigned)r[1]));
 }
 
 // Sum / max over the four lane groups (lanes lr, lr+16, lr+32, lr+48); every
@@ -68,13 +72,25 @@ SC_DEV i16x4 lds_read_tr16(const void* p) {
       (__attribute__((address_space(3))) i16x4*)(const_cast<void*>(p)));
 }
 
-// Workgroups are dispatched round-robin over the 8 XCDs (each with its own L2).
-// Renumber them so that consecutive logical blocks run on the same XCD: the
-// query blocks of one (sequence, head) then share K/V tiles in one L2.
-SC_DEV int xcd_remap(int i, int total) {
-  const int full = (total / 8) * 8;
-  if (i >= full) return i;
-  return (i % 8) * (full / 8) + i / 8;
+// Workgroups are dispatched round-robin over the 8 XCDs (each with its own
+// L2): workgroup i runs on XCD i % 8.  For a grid of `pairs` x `inner`
+// blocks (a (sequence, head) pair and its query or key blocks), block i is
+// mapped to (pair, idx) so that the inner blocks of a pair run on one XCD in
+// order (neighbours share K/V tiles in that L2) and the pairs are dealt
+// round-robin over the XCDs, which spreads sequences of different length
+// evenly.  When pairs is not a multiple of 8 the last pairs % 8 pairs keep
+// the plain order.  The caller's block index must start at a multiple of 8.
+SC_DEV void xcd_pair_map(int i, int inner, int pairs, int& pair, int& idx) {
+  const int full = pairs & ~7;
+  if (i < full * inner) {
+    const int x = i & 7, j = i >> 3;
+    pair = 8 * (j / inner) + x;
+    idx = j % inner;
+  } else {
+    const int rest = i - full * inner;
+    pair = full + rest / inner;
+    idx = rest % inner;
+  }
 }
 
 template <int DT>
@@ -87,21 +103,22 @@ struct Tr;
 // free of LDS bank conflicts for those reads.
 
 // bfloat16: one MFMA v_mfma_f32_16x16x32_bf16 covers 32 of the 64 head dims;
-// a lane holds 8 consecutive dims (16 bytes) of its row.  Key / query rows are
-// unpadded (128 B) with the unit index XOR-swizzled by the row's low 3 bits;
-// value rows are padded to 160 B, which keeps the four 16-dim column blocks of
-// a transposed read at fixed offsets from one address.  Both layouts measured
-// conflict-free on gfx950 (the former 144-byte pitch made the fragment reads
-// 1.7x slower).
+// a lane holds 8 consecutive dims (16 bytes) of its row.  Rows are unpadded
+// (128 B) with the unit index XOR-swizzled by the row's low 3 bits, for key,
+// query and value tiles alike: the 16-byte fragment reads (lane -> row lr,
+// unit g) and the transposed 8-byte reads of value tiles then touch distinct
+// LDS banks (measured on gfx950: as fast as linear reads, where a padded
+// 144-byte pitch made the fragment reads 1.7x slower), and whole rows stay
+// 128-byte runs that the direct global->LDS loads can fill.
 template <>
 struct Tr<1> {
   using T = __bf16;
   using Frag = bf16x8;
   static constexpr int kChunks = 2;
-  static constexpr int kPitch = 64;   // elements per key / query row
-  static constexpr int kPitchV = 80;  // elements per value row
+  static constexpr int kPitch = 64;  // elements per row
+  static constexpr int kPitchV = 64;
   SC_DEV static int off(int row, int unit) { return row * kPitch + 8 * (unit ^ (row & 7)); }
-  SC_DEV static int voff(int row, int unit) { return row * kPitchV + 8 * unit; }
+  SC_DEV static int voff(int row, int unit) { return off(row, unit); }
   SC_DEV static f32x4 mma(Frag a, Frag b, f32x4 c) {
     return __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, b, c, 0, 0, 0);
   }
