@@ -277,11 +277,13 @@ SC_DEV unsigned long long tile_gmask(const uint32_t* sBits, int t, int nwords) {
 SC_DEV int win_tables(const AttnArgs& a, const WinBlock& wb, uint32_t* sBits, int* sXList, int* sNx) {
   const int tid = threadIdx.x;
   const int* gp = wb.nxc ? a.gpos + (long long)wb.b * a.G : nullptr;
+  const int G = gp ? a.G : 0;
+  const int p_first = tid < G ? gp[tid] : -1;  // in flight with the caller's loads
   for (int i = tid; i < wb.nwords; i += kThreads) sBits[i] = 0u;
   for (int i = tid; i < wb.nxc; i += kThreads) sXList[i] = 0;
   __syncthreads();
-  for (int j = tid; j < (gp ? a.G : 0); j += kThreads) {
-    const int p = gp[j];
+  for (int j = tid; j < G; j += kThreads) {
+    const int p = j == tid ? p_first : gp[j];
     if (p >= wb.kt0 && p < wb.kt1)
       atomicOr(&sBits[(p - wb.kt0) >> 5], 1u << ((p - wb.kt0) & 31));
     else if (p >= 0 && p < wb.L)
@@ -699,13 +701,10 @@ SC_DEV void window_fwd_v2(const AttnArgs& a, int blk, Smem<1>& sm, uint32_t* sDy
   uint32_t* sBits = sDyn;
   int* sXList = reinterpret_cast<int*>(sDyn + a.rwp / 32 + 2);
   auto band_rows = [&](int k0) { return [=](int R) { return min(k0 + R, kt1 - 1); }; };
+  // the first K/V tile, the query fragments and the global positions (read
+  // by win_tables) are in flight together
   tile_dma(Kg, ldb, sm.b[0], w, lane, band_rows(kt0));
   tile_dma(Vg, ldb, sm.c[0], w, lane, band_rows(kt0));
-  const int ntile = win_tables(a, wb, sBits, sXList, &sm.misc[0]);
-  auto gbit = [&](int k) -> bool {
-    const int o = k - kt0;
-    return (sBits[o >> 5] >> (o & 31)) & 1u;
-  };
   // query fragments straight from HBM (rows clamped below L; same dims per
   // lane group as the key fragments)
   const int qa = q0 + 32 * w;
@@ -716,6 +715,11 @@ SC_DEV void window_fwd_v2(const AttnArgs& a, int blk, Smem<1>& sm, uint32_t* sDy
     qf[j][0] = *reinterpret_cast<const bf16x8*>(qrow + 8 * g);
     qf[j][1] = *reinterpret_cast<const bf16x8*>(qrow + 32 + 8 * g);
   }
+  const int ntile = win_tables(a, wb, sBits, sXList, &sm.misc[0]);
+  auto gbit = [&](int k) -> bool {
+    const int o = k - kt0;
+    return (sBits[o >> 5] >> (o & 31)) & 1u;
+  };
   float m_use[2] = {kNegBig, kNegBig}, l_run[2] = {0.f, 0.f};
   f32x4 o[2][4];
 #pragma unroll

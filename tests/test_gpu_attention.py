@@ -38,6 +38,7 @@ SMALL = [
     ("global at last valid token", "bf16", 2, 160, 2, 32, 2, (160, 160),
      dict(gp_override=[[0, 159], [5, 159]])),
     ("unused slots", "f32", 2, 140, 2, 40, 4, (140, 140), dict(gp_override=[[3, 77, -1, -1], [-1, -1, -1, -1]])),
+    ("600 global tokens", "bf16", 1, 1200, 2, 64, 600, (1100, 1200), {}),
 ]
 
 
