@@ -936,6 +936,137 @@ SC_DEV void band_col_block(const AttnArgs& a, int blk, SmemCol<DT>& sm) {
   if (a.part_band && g == 0 && key < n) a.part_band[(long long)bh * n + key] = kuse ? cs : 0.f;
 }
 
+
+// --------------------------------------- bf16 band columns, 32 keys a wave --
+// A block owns 128 keys (4 waves x 32 as two 16-key sub-blocks that share
+// every query fragment), keeps their K fragments in registers and walks the
+// 64-query tiles that reach them.  Query tiles and their log2-LSE arrive by
+// direct global->LDS loads, double-buffered.
+constexpr int kBK2 = 128;
+
+// Direct load of 4 bytes per lane: lane i's dword lands at lds + 4 i.
+SC_DEV void lds_dma4(const void* base, unsigned voff, unsigned lds) {
+  asm volatile("s_mov_b32 m0, %2\n\ts_nop 0\n\tglobal_load_lds_dword %0, %1"
+               :
+               : "v"(voff), "s"(base), "s"(lds)
+               : "memory", "m0");
+}
+
+// One 64-query tile against the wave's two key sub-blocks.  Lane (g, lr) of
+// sub-block j holds key lr and queries 16 qst + 4g + i; the query is allowed
+// for key j when 16 qst + i lies in [lo[j], hi[j]] (kMasked only).
+template <bool kMasked>
+SC_DEV void col_tile2(const bf16x8 (&kf)[2][2], const __bf16* sQ, const float* sL, float c2, int lr, int g,
+                      f32x4 (&cs)[2], const int (&lo)[2], const int (&hi)[2]) {
+  using TR = Tr<1>;
+#pragma unroll
+  for (int qst = 0; qst < 4; ++qst) {
+    bf16x8 qf[2];
+    TR::load_frags(sQ, 16 * qst + lr, g, qf);
+    const f32x4 l2 = *reinterpret_cast<const f32x4*>(sL + 16 * qst + 4 * g);
+#pragma unroll
+    for (int j = 0; j < 2; ++j) {
+      f32x4 acc = {0.f, 0.f, 0.f, 0.f};
+      acc = TR::mma(qf[0], kf[j][0], acc);
+      acc = TR::mma(qf[1], kf[j][1], acc);
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        float p = fast_exp2(fmaf(acc[i], c2, -l2[i]));
+        if constexpr (kMasked) {
+          const int c = 16 * qst + i;
+          p = (c >= lo[j]) & (c <= hi[j]) ? p : 0.f;
+        }
+        cs[j][i] += p;
+      }
+    }
+  }
+}
+
+SC_DEV void band_col_v2(const AttnArgs& a, int blk, SmemCol<1>& sm) {
+  using TR = Tr<1>;
+  using T = __bf16;
+  int kb, bh;
+  xcd_pair_map(blk, a.nkb, a.H * a.B, bh, kb);
+  const int h = bh % a.H, b = bh / a.H;
+  const int tid = threadIdx.x, lane = tid & 63, w = __builtin_amdgcn_readfirstlane(tid >> 6), g = lane >> 4,
+            lr = lane & 15;
+  const int n = a.n, r = a.r;
+  const int L = clampi(a.valid_len[b], 0, n);
+  const int k0 = kb * kBK2;
+  if (k0 >= L) return;  // the score reduction reads keys below L only
+  const int kend = min(L, k0 + kBK2);
+  const long long ld = a.ld_in;
+  const unsigned ldb = (unsigned)(2 * a.ld_in);
+  const T* Qg = static_cast<const T*>(a.q) + b * a.bs_in + h * kHeadDim;
+  const T* Kg = static_cast<const T*>(a.k) + b * a.bs_in + h * kHeadDim;
+  const float* l2g = a.win_lse2 + (long long)bh * n;
+  const int qlo = max(0, k0 - r), qhi = min(L, k0 + kBK2 + r);
+  const int nqt = (qhi - qlo + kBQ - 1) / kBQ;
+  // query tile t (rows clamped below qhi) and the log2-LSE of its rows
+  // (indices clamped below n; rows at or beyond qhi are masked)
+  auto issue = [&](int t, int bf) {
+    const int qs = qlo + t * kBQ;
+    tile_dma(Qg, ldb, sm.b[bf], w, lane, [=](int R) { return min(qs + R, qhi - 1); });
+    if (w == 0) lds_dma4(l2g, 4u * (unsigned)min(qs + lane, n - 1), lds_addr(sm.l[bf]));
+  };
+  issue(0, 0);
+  // K fragments of the wave's 32 keys straight from HBM (rows clamped below kend)
+  const int kw0 = k0 + 32 * w;
+  bf16x8 kf[2][2];
+#pragma unroll
+  for (int j = 0; j < 2; ++j) {
+    const T* krow = Kg + (long long)min(kw0 + 16 * j + lr, kend - 1) * ld;
+    kf[j][0] = *reinterpret_cast<const bf16x8*>(krow + 8 * g);
+    kf[j][1] = *reinterpret_cast<const bf16x8*>(krow + 32 + 8 * g);
+  }
+  // global keys of the block: their band columns are not used
+  const int* gp = (a.gpos && a.G > 0) ? a.gpos + (long long)b * a.G : nullptr;
+  const int G = gp ? a.G : 0;
+  const int p_first = tid < G ? gp[tid] : -1;
+  uint32_t* gmask = reinterpret_cast<uint32_t*>(sm.misc);
+  if (tid < kBK2 / 32) gmask[tid] = 0u;
+  __syncthreads();
+  for (int j = tid; j < G; j += kThreads) {
+    const int p = j == tid ? p_first : gp[j];
+    if (p >= k0 && p < kend) atomicOr(&gmask[(p - k0) >> 5], 1u << ((p - k0) & 31));
+  }
+  __builtin_amdgcn_s_waitcnt(0x0F70);  // vmcnt(0): K fragments, positions
+  wait_dma();
+  __syncthreads();
+
+  // per-lane bounds: query 16 qst + i of the lane (tile start qs) is allowed
+  // for key sub-block j when it lies in [lo[j] - qs, hi[j] - qs]
+  int lo[2], hi[2];
+#pragma unroll
+  for (int j = 0; j < 2; ++j) {
+    const int key = kw0 + 16 * j + lr;
+    lo[j] = key - r - 4 * g;
+    hi[j] = min(key + r, qhi - 1) - 4 * g;
+  }
+  f32x4 cs[2] = {{0.f, 0.f, 0.f, 0.f}, {0.f, 0.f, 0.f, 0.f}};
+  for (int t = 0; t < nqt; ++t) {
+    const int buf = t & 1, qs = qlo + t * kBQ;
+    if (t + 1 < nqt) issue(t + 1, buf ^ 1);
+    if (qs <= kw0 + 31 + r && qs + kBQ - 1 >= kw0 - r) {
+      if (qs >= kw0 + 31 - r && qs + kBQ - 1 <= kw0 + r && qs + kBQ <= qhi) {
+        col_tile2<false>(kf, sm.b[buf], sm.l[buf], a.c2, lr, g, cs, lo, hi);
+      } else {
+        const int l2[2] = {lo[0] - qs, lo[1] - qs}, h2[2] = {hi[0] - qs, hi[1] - qs};
+        col_tile2<true>(kf, sm.b[buf], sm.l[buf], a.c2, lr, g, cs, l2, h2);
+      }
+    }
+    if (t + 1 < nqt) wait_dma();
+    __syncthreads();
+  }
+#pragma unroll
+  for (int j = 0; j < 2; ++j) {
+    const float c = group_sum((cs[j][0] + cs[j][1]) + (cs[j][2] + cs[j][3]));
+    const int key = kw0 + 16 * j + lr;
+    const bool kuse = key < kend && !((gmask[(key - k0) >> 5] >> ((key - k0) & 31)) & 1u);
+    if (a.part_band && g == 0 && key < n) a.part_band[(long long)bh * n + key] = kuse ? c : 0.f;
+  }
+}
+
 template <int DT, bool kBandProbs>
 SC_DEV void gcol_block(const AttnArgs& a, int lin, SmemCol<DT>& sm) {
   using TR = Tr<DT>;
@@ -1118,7 +1249,10 @@ __global__ __launch_bounds__(kThreads) SC_OCC(kBandProbs ? 2 : 4) void k_attn_co
   }
   blk -= a.n_gr;
   if (blk < a.n_bcol) {
-    band_col_block<DT, kBandProbs>(a, blk, sm);
+    if constexpr (DT == 1 && !kBandProbs)
+      band_col_v2(a, blk, sm);
+    else
+      band_col_block<DT, kBandProbs>(a, blk, sm);
     return;
   }
   blk -= a.n_bcol;
@@ -1298,6 +1432,7 @@ static hipError_t launch_window_t(const AttnArgs& a0, hipStream_t s) {
   // global-row blocks come first in both launches; their count is padded to a
   // multiple of 8 so that the next block type starts on XCD 0
   a.n_gr = glob ? (a.nkc * a.ngc * a.H * a.B + 7) & ~7 : 0;
+  if (DT == 1 && !a.bp_band) a.nkb = (a.n + kBK2 - 1) / kBK2;  // 128-key column blocks
   a.n_bcol = cols ? a.nkb * a.H * a.B : 0;
   const int n_gcol = (cols && glob) ? a.nqr * a.ngc * a.H * a.B : 0;
   const int nxc = glob ? (a.G + kBK - 1) / kBK : 0;
