@@ -171,14 +171,17 @@ SC_DEV void softmax_tile(const typename Tr<DT>::Frag (&qf)[Tr<DT>::kChunks], con
 // result register (qst, i) is (query 16*qst + 4g + i, key lr), so the sum over
 // queries stays inside the lane; the 4 lane groups are combined once, by the
 // caller, after the last tile.  ok(qst, i) masks pairs; emit(q, p) sees every
-// probability (used for the paper's band layout).
+// probability (used for the paper's band layout).  Bit qst of `live` (wave-
+// uniform) says whether query group qst holds a used row; other groups are
+// skipped.
 template <int DT, bool kMasked, typename OkFn, typename EmitFn>
 SC_DEV float col_tile(const typename Tr<DT>::Frag (&kf)[Tr<DT>::kChunks], const typename Tr<DT>::T* sQ,
-                      const float* sL, float c2, int lr, int g, OkFn ok, EmitFn emit) {
+                      const float* sL, float c2, int lr, int g, OkFn ok, EmitFn emit, unsigned live = 0xFu) {
   using TR = Tr<DT>;
   float cs = 0.f;
 #pragma unroll
   for (int qst = 0; qst < 4; ++qst) {
+    if (!((live >> qst) & 1u)) continue;  // wave-uniform: no query of this group is used
     typename TR::Frag qf[TR::kChunks];
     TR::load_frags(sQ, 16 * qst + lr, g, qf);
     const f32x4 l2 = *reinterpret_cast<const f32x4*>(sL + 16 * qst + 4 * g);
@@ -514,6 +517,9 @@ SC_DEV void gr_fwd_block(const AttnArgs& a, int lin, Smem<DT>& sm) {
   __syncthreads();
   typename TR::Frag qf[TR::kChunks];
   TR::load_frags(sm.b[1], 16 * w + lr, g, qf);
+  // waves whose 16 slots are all unused only help with the loads (with G = 32
+  // that is half of each block)
+  const bool wlive = __ballot(sm.pos[0][16 * w + lr] >= 0) != 0ull;
   __syncthreads();  // every wave holds its query fragments before b[1] is reused
   float m_use = kNegBig, l_run = 0.f;
   f32x4 o[4];
@@ -525,7 +531,8 @@ SC_DEV void gr_fwd_block(const AttnArgs& a, int lin, Smem<DT>& sm) {
       stk.load_range(Kg, a.ld_in, k0 + kBK, kend);
       stv.load_range(Vg, a.ld_in, k0 + kBK, kend);
     }
-    if (k0 + kBK <= kend) {
+    if (!wlive) {
+    } else if (k0 + kBK <= kend) {
       softmax_tile<DT, false>(qf, sm.b[buf], sm.c[buf], a.c2, lr, g, m_use, l_run, o, [](int, int) { return true; });
     } else {
       const int hi = kend - 1 - k0;
@@ -1118,13 +1125,15 @@ SC_DEV void gcol_block(const AttnArgs& a, int lin, SmemCol<DT>& sm) {
   TR::load_frags(sm.a, 16 * w + lr, g, kf);
   const int slot = kGlobalChunk * gc + 16 * w + lr;
   const bool kuse = pos[16 * w + lr] >= 0;
+  const bool wlive = __ballot(kuse) != 0ull;  // some of the wave's 16 global keys is used
   float* bpc = kBandProbs ? a.bp_gcol + (long long)bh * n * G : nullptr;
   float cs = 0.f;
   for (int t = 0; t < nqt; ++t) {
     const int buf = t & 1;
     if (t + 1 < nqt) load(t + 1);
     const int qs = qbeg + t * kBQ;
-    if constexpr (kBandProbs) {
+    if (!wlive) {
+    } else if constexpr (kBandProbs) {
       cs += col_tile<DT, false>(kf, sm.b[buf], sm.l[buf], a.c2, lr, g, [](int, int) { return true; },
                                 [&](int qq, float p) {
                                   const int q = qs + qq;
@@ -1212,6 +1221,9 @@ SC_DEV void gr_col_block(const AttnArgs& a, int lin, SmemCol<DT>& sm) {
   stk.store(sm.b[0]);
   __syncthreads();
   float* bpr = kBandProbs ? a.bp_grow + (long long)blk.bh * a.G * a.n : nullptr;
+  unsigned qlive = 0u;  // 16-slot groups that hold a used global row
+#pragma unroll
+  for (int qst = 0; qst < 4; ++qst) qlive |= (unsigned)(__ballot(pos[16 * qst + lr] >= 0) != 0ull) << qst;
   for (int t = 0; t < ntile; ++t) {
     const int buf = t & 1, k0 = kbeg + t * kBK;
     if (t + 1 < ntile) stk.load_range(Kg, a.ld_in, k0 + kBK, kend);
@@ -1225,9 +1237,9 @@ SC_DEV void gr_col_block(const AttnArgs& a, int lin, SmemCol<DT>& sm) {
       cs = col_tile<DT, false>(kf, sm.a, sm.l[0], a.c2, lr, g, [](int, int) { return true; }, [&](int qq, float p) {
         const int slot = kGlobalChunk * blk.gc + qq;
         if (kin && slot < a.G && p != 0.f) bpr[(long long)slot * a.n + key] = p;
-      });
+      }, qlive);
     } else {
-      cs = col_tile<DT, false>(kf, sm.a, sm.l[0], a.c2, lr, g, [](int, int) { return true; }, NoEmit{});
+      cs = col_tile<DT, false>(kf, sm.a, sm.l[0], a.c2, lr, g, [](int, int) { return true; }, NoEmit{}, qlive);
     }
     cs = group_sum(cs);
     if (pg && g == 0 && kin) pg[key] = cs;
