@@ -491,7 +491,6 @@ SC_DEV void gr_fwd_block(const AttnArgs& a, int lin, Smem<DT>& sm) {
   using TR = Tr<DT>;
   using T = typename TR::T;
   constexpr int P = TR::kPitch;
-  if (lin >= a.nkc * a.ngc * a.H * a.B) return;  // padding of the block count to a multiple of 8
   const GrBlock blk = gr_block(a, lin);
   const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6, g = lane >> 4, lr = lane & 15;
   const int L = clampi(a.valid_len[blk.b], 0, a.n);
@@ -841,18 +840,21 @@ SC_DEV void window_fwd_v2(const AttnArgs& a, int blk, Smem<1>& sm, uint32_t* sDy
   }
 }
 
-// Launch 1: global-row forward blocks first (when there are global tokens),
-// then the window pass-1 blocks.
+// Launch 1: the window pass-1 blocks, then the global-row forward blocks
+// (when there are global tokens).
 template <int DT>
 __global__ __launch_bounds__(kThreads) SC_OCC(DT == 1 ? 3 : 2) void k_attn_fwd(AttnArgs a) {
   __shared__ Smem<DT> sm;
   extern __shared__ uint32_t sDyn[];
-  if ((int)blockIdx.x < a.n_gr)
-    gr_fwd_block<DT>(a, blockIdx.x, sm);
+  // window blocks first (their XCD mapping assumes they start at block 0);
+  // the global-row blocks come last and fill the window blocks' uneven tail
+  const int nwin = a.nqb * a.H * a.B;
+  if ((int)blockIdx.x >= nwin)
+    gr_fwd_block<DT>(a, blockIdx.x - nwin, sm);
   else if constexpr (DT == 1)
-    window_fwd_v2(a, blockIdx.x - a.n_gr, sm, sDyn);
+    window_fwd_v2(a, blockIdx.x, sm, sDyn);
   else
-    window_fwd_block<DT>(a, blockIdx.x - a.n_gr, sm, sDyn);
+    window_fwd_block<DT>(a, blockIdx.x, sm, sDyn);
 }
 
 // -------------------------------------------------------- column sums ------
@@ -1157,7 +1159,7 @@ SC_DEV void gr_col_block(const AttnArgs& a, int lin, SmemCol<DT>& sm) {
   using TR = Tr<DT>;
   using T = typename TR::T;
   constexpr int P = TR::kPitch;
-  if (lin >= a.nkc * a.ngc * a.H * a.B) return;  // padding of the block count to a multiple of 8
+  if (lin >= a.n_gr) return;  // padding of the block count to a multiple of 8
   const GrBlock blk = gr_block(a, lin);
   const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6, g = lane >> 4, lr = lane & 15;
   const int L = clampi(a.valid_len[blk.b], 0, a.n);
@@ -1248,18 +1250,21 @@ SC_DEV void gr_col_block(const AttnArgs& a, int lin, SmemCol<DT>& sm) {
   }
 }
 
-// Launch 2: global-row column blocks, band-column blocks, global-column
-// blocks (the last two only when score partials or the band layout are asked
-// for).
+// Launch 2: global-row column blocks, then band-column and global-column
+// blocks (both only when score partials or the band layout are asked for).
 template <int DT, bool kBandProbs>
 __global__ __launch_bounds__(kThreads) SC_OCC(kBandProbs ? 2 : 4) void k_attn_cols(AttnArgs a) {
   __shared__ SmemCol<DT> sm;
+  // global-row column blocks first (long; started early they overlap the
+  // rest), their count padded to a multiple of 8 so that the band-column
+  // blocks start on XCD 0 as their mapping assumes; then band-column and
+  // global-column blocks
   int blk = blockIdx.x;
-  if (blk < a.n_gr) {
+  if (blk < a.n_grc) {
     gr_col_block<DT, kBandProbs>(a, blk, sm);
     return;
   }
-  blk -= a.n_gr;
+  blk -= a.n_grc;
   if (blk < a.n_bcol) {
     if constexpr (DT == 1 && !kBandProbs)
       band_col_v2(a, blk, sm);
@@ -1267,8 +1272,7 @@ __global__ __launch_bounds__(kThreads) SC_OCC(kBandProbs ? 2 : 4) void k_attn_co
       band_col_block<DT, kBandProbs>(a, blk, sm);
     return;
   }
-  blk -= a.n_bcol;
-  gcol_block<DT, kBandProbs>(a, blk, sm);
+  gcol_block<DT, kBandProbs>(a, blk - a.n_bcol, sm);
 }
 
 // ------------------------------------------------------ score reduction ----
@@ -1441,12 +1445,11 @@ static hipError_t launch_window_t(const AttnArgs& a0, hipStream_t s) {
   AttnArgs a = a0;
   const bool glob = a.G > 0 && a.gpos;
   const bool cols = a.part_band || a.bp_band;
-  // global-row blocks come first in both launches; their count is padded to a
-  // multiple of 8 so that the next block type starts on XCD 0
-  a.n_gr = glob ? (a.nkc * a.ngc * a.H * a.B + 7) & ~7 : 0;
+  a.n_gr = glob ? a.nkc * a.ngc * a.H * a.B : 0;
+  a.n_grc = (a.n_gr + 7) & ~7;
   if (DT == 1 && !a.bp_band) a.nkb = (a.n + kBK2 - 1) / kBK2;  // 128-key column blocks
   a.n_bcol = cols ? a.nkb * a.H * a.B : 0;
-  const int n_gcol = (cols && glob) ? a.nqr * a.ngc * a.H * a.B : 0;
+  a.n_gcol = (cols && glob) ? a.nqr * a.ngc * a.H * a.B : 0;
   const int nxc = glob ? (a.G + kBK - 1) / kBK : 0;
   if (DT == 1) {  // bf16 pass 1 runs 128-query blocks
     a.nqb = (a.n + kBQ2 - 1) / kBQ2;
@@ -1455,7 +1458,7 @@ static hipError_t launch_window_t(const AttnArgs& a0, hipStream_t s) {
   }
   const size_t dyn = sizeof(uint32_t) * ((size_t)a.rwp / 32 + 2 + nxc + 1);
   const unsigned fwd_blocks = (unsigned)(a.n_gr + a.nqb * a.H * a.B);
-  const unsigned col_blocks = (unsigned)(a.n_gr + a.n_bcol + n_gcol);
+  const unsigned col_blocks = (unsigned)(a.n_grc + a.n_bcol + a.n_gcol);
   profile_begin(s);
   hipLaunchKernelGGL(k_attn_fwd<DT>, dim3(fwd_blocks), dim3(kThreads), dyn, s, a);
   if (col_blocks > 0) {
