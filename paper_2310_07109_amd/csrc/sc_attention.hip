@@ -769,7 +769,16 @@ SC_DEV void window_fwd_v2(const AttnArgs& a, int blk, Smem<1>& sm, uint32_t* sDy
           live |= (unsigned)((16 * st + 15 >= wlo && 16 * st <= whi) || ((gall >> (16 * st)) & 0xFFFFull) != 0ull)
                   << st;
         const int l0 = lo[0] - k0, h0 = hi[0] - k0, l1 = lo[1] - k0, h1 = hi[1] - k0;
-        if (gall == 0ull) {
+        // a band edge is one-sided in most tiles: the band starts inside the
+        // tile for some query (nlo) or ends inside it (nhi), wave-uniform
+        const bool nlo = qa + 31 - r - k0 > 0, nhi = min(qa + r, kt1 - 1) - k0 < kBK - 1;
+        if (gall == 0ull && !nhi) {
+          softmax_tile2<true>(qf, sm.b[buf], sm.c[buf], a.c2, lr, g, m_use, l_run, o, live,
+                              [&](int j, int st, int i) { return 16 * st + i >= (j == 0 ? l0 : l1); });
+        } else if (gall == 0ull && !nlo) {
+          softmax_tile2<true>(qf, sm.b[buf], sm.c[buf], a.c2, lr, g, m_use, l_run, o, live,
+                              [&](int j, int st, int i) { return 16 * st + i <= (j == 0 ? h0 : h1); });
+        } else if (gall == 0ull) {
           softmax_tile2<true>(qf, sm.b[buf], sm.c[buf], a.c2, lr, g, m_use, l_run, o, live, [&](int j, int st, int i) {
             const int c = 16 * st + i;
             return j == 0 ? (c >= l0) & (c <= h0) : (c >= l1) & (c <= h1);
@@ -963,8 +972,8 @@ SC_DEV void lds_dma4(const void* base, unsigned voff, unsigned lds) {
 
 // One 64-query tile against the wave's two key sub-blocks.  Lane (g, lr) of
 // sub-block j holds key lr and queries 16 qst + 4g + i; the query is allowed
-// for key j when 16 qst + i lies in [lo[j], hi[j]] (kMasked only).
-template <bool kMasked>
+// for key j when 16 qst + i >= lo[j] (tested if kLo) and <= hi[j] (if kHi).
+template <bool kLo, bool kHi>
 SC_DEV void col_tile2(const bf16x8 (&kf)[2][2], const __bf16* sQ, const float* sL, float c2, int lr, int g,
                       f32x4 (&cs)[2], const int (&lo)[2], const int (&hi)[2]) {
   using TR = Tr<1>;
@@ -981,10 +990,13 @@ SC_DEV void col_tile2(const bf16x8 (&kf)[2][2], const __bf16* sQ, const float* s
 #pragma unroll
       for (int i = 0; i < 4; ++i) {
         float p = fast_exp2(fmaf(acc[i], c2, -l2[i]));
-        if constexpr (kMasked) {
-          const int c = 16 * qst + i;
+        const int c = 16 * qst + i;
+        if constexpr (kLo && kHi)
           p = (c >= lo[j]) & (c <= hi[j]) ? p : 0.f;
-        }
+        else if constexpr (kLo)
+          p = c >= lo[j] ? p : 0.f;
+        else if constexpr (kHi)
+          p = c <= hi[j] ? p : 0.f;
         cs[j][i] += p;
       }
     }
@@ -1058,10 +1070,10 @@ SC_DEV void band_col_v2(const AttnArgs& a, int blk, SmemCol<1>& sm) {
     if (t + 1 < nqt) issue(t + 1, buf ^ 1);
     if (qs <= kw0 + 31 + r && qs + kBQ - 1 >= kw0 - r) {
       if (qs >= kw0 + 31 - r && qs + kBQ - 1 <= kw0 + r && qs + kBQ <= qhi) {
-        col_tile2<false>(kf, sm.b[buf], sm.l[buf], a.c2, lr, g, cs, lo, hi);
+        col_tile2<false, false>(kf, sm.b[buf], sm.l[buf], a.c2, lr, g, cs, lo, hi);
       } else {
         const int l2[2] = {lo[0] - qs, lo[1] - qs}, h2[2] = {hi[0] - qs, hi[1] - qs};
-        col_tile2<true>(kf, sm.b[buf], sm.l[buf], a.c2, lr, g, cs, l2, h2);
+        col_tile2<true, true>(kf, sm.b[buf], sm.l[buf], a.c2, lr, g, cs, l2, h2);
       }
     }
     if (t + 1 < nqt) wait_dma();
