@@ -70,6 +70,110 @@ def algorithmic_counts(inp):
     return pairs_window, pairs_global
 
 
+def roofline(flops, bytes_, kern_ms):
+    """Roofline of the two window-attention launches against the larger of the MFMA and HBM floors."""
+    t_mfma = flops / (MFMA_PEAK_TFLOPS["bf16"] * 1e12)
+    t_hbm = bytes_ / (HBM_PEAK_GBS * 1e9)
+    if t_mfma >= t_hbm:
+        achieved = flops / (kern_ms * 1e-3) / 1e12
+        roof = dict(bound="mfma", achieved=round(achieved, 2), peak=MFMA_PEAK_TFLOPS["bf16"], unit="TFLOP/s")
+    else:
+        achieved = bytes_ / (kern_ms * 1e-3) / 1e9
+        roof = dict(bound="hbm", achieved=round(achieved, 1), peak=HBM_PEAK_GBS, unit="GB/s")
+    roof["frac"] = round(roof["achieved"] / roof["peak"], 4)
+    roof["floor_mfma_us"] = round(t_mfma * 1e6, 2)
+    roof["floor_hbm_us"] = round(t_hbm * 1e6, 2)
+    return roof
+
+
+def measure(sc, si, torch, np, inp, theta, steps, warmup, dev="cuda:0"):
+    """Times `steps` steps (window attention with score partials, scores, prune + compaction of O) after
+    `warmup` untimed ones.  theta None picks the median score of the valid non-global tokens (about half
+    pruned), from one untimed step."""
+    B, n, H, dd, G = inp["B"], inp["n"], inp["H"], inp["d"], inp["G"]
+
+    def i32(a):
+        return torch.from_numpy(np.ascontiguousarray(a, dtype=np.int32)).to(dev)
+
+    def bf(a):
+        return torch.from_numpy(np.ascontiguousarray(a).view(np.int16)).to(dev).view(torch.bfloat16)
+
+    d = sc.Desc(B, n, H, inp["window"], i32(inp["valid_len"]), i32(inp["global_pos"]), inp["alpha"], sc.SC_BF16)
+    q, k, v = bf(inp["q"]), bf(inp["k"]), bf(inp["v"])
+    out = torch.empty_like(q)
+    lse = torch.empty((B, H, n), dtype=torch.float32, device=dev)
+    sp = torch.empty(sc.sc_score_partials_size(d) // 4, dtype=torch.float32, device=dev)
+    ws_attn = torch.empty(max(sc.sc_window_attention_workspace_size(d), 1), dtype=torch.uint8, device=dev)
+    scores = torch.empty((B, n), dtype=torch.float32, device=dev)
+    oc = torch.empty_like(out)
+    outs = dict(keep_idx=torch.empty((B, n), dtype=torch.int32, device=dev),
+                new_len=torch.empty((B,), dtype=torch.int32, device=dev),
+                new_global_pos=torch.empty((B, max(G, 1)), dtype=torch.int32, device=dev),
+                orig_idx_out=torch.empty((B, n), dtype=torch.int32, device=dev))
+    ws_prune = torch.empty(sc.sc_ltp_prune_compact_workspace_size(d), dtype=torch.uint8, device=dev)
+    if theta is None:
+        sc.sc_window_attention(d, q, k, v, out=out, lse=lse, score_partials=sp, workspace=ws_attn)
+        sc.sc_ltp_score(d, sp, scores=scores)
+        sv = scores.cpu().numpy()
+        vals = []
+        for b in range(B):
+            L = int(inp["valid_len"][b])
+            glob = {int(x) for x in inp["global_pos"][b] if 0 <= x < L}
+            vals.extend(float(sv[b, t]) for t in range(L) if t not in glob)
+        theta = float(np.median(vals)) if vals else 0.0
+
+    def step():
+        sc.sc_window_attention(d, q, k, v, out=out, lse=lse, score_partials=sp, workspace=ws_attn)
+        sc.sc_ltp_score(d, sp, scores=scores)
+        sc.sc_ltp_prune_compact(d, scores, theta, True, [out], dsts=[oc], outs=outs, workspace=ws_prune)
+
+    for _ in range(warmup):
+        step()
+    torch.cuda.synchronize()
+    sc.sc_profile_window_kernel(True)
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    w0 = time.perf_counter()
+    e0.record()
+    for _ in range(steps):
+        step()
+    e1.record()
+    torch.cuda.synchronize()
+    wall_ms = (time.perf_counter() - w0) * 1e3 / steps
+    ms = e0.elapsed_time(e1) / steps
+    kern_ms, launches = sc.sc_profile_window_kernel_read()
+    sc.sc_profile_window_kernel(False)
+    kern_ms /= max(launches, 1)
+
+    tokens = int(np.sum(inp["valid_len"]))
+    pairs_w, pairs_g = algorithmic_counts(inp)
+    # algorithmic work of the two launches: Q.K^T and P.V once per allowed pair (the window rows and the
+    # global rows); read Q, K, V, write O (bf16), the LSE and the score partials (fp32)
+    flops = 4.0 * dd * H * (pairs_w + pairs_g)
+    bytes_ = tokens * H * (4 * dd * 2 + 4) + sp.numel() * 4
+    roof = roofline(flops, bytes_, kern_ms)
+    return dict(ms=ms, wall_ms=wall_ms, kern_ms=kern_ms, tokens=tokens, kept=outs["new_len"].cpu().tolist(),
+                flops=flops, bytes=bytes_, roof=roof, theta=theta, pairs=H * (pairs_w + pairs_g))
+
+
+def sweep(args, sc, si, torch, np):
+    """Window and length sweeps of the same step (one JSON line per point).  Window sweep: B8 n4096;
+    length sweep: window 512 and B = 32768 / n padded tokens; both H12 bf16, 32 global tokens, valid lengths
+    U[n/2, n], the threshold at the median score (about half pruned)."""
+    base = si.CONFIGS[4]
+    points = [("window", 4096, w) for w in (16, 64, 128, 256, 512, 1024)]
+    points += [("length", n, 512) for n in (1024, 2048, 4096, 8192, 16384)]
+    for kind, n, w in points:
+        B = 8 if kind == "window" else 32768 // n
+        inp = si.make_attention_inputs(base, B=B, n=n, window=w, len_range=(n // 2, n))
+        m = measure(sc, si, torch, np, inp, None, args.steps, args.warmup)
+        print(json.dumps({
+            "sweep": kind, "n": n, "window": w, "batch": B, "valid_tokens": m["tokens"],
+            "allowed_pairs": m["pairs"], "ms_per_step": round(m["ms"], 4),
+            "value": round(m["tokens"] / (m["ms"] * 1e-3), 1), "unit": "kept-token-layers/s",
+            "attention_us": round(m["kern_ms"] * 1e3, 2), "ns_per_pair": round(m["kern_ms"] * 1e6 / m["pairs"], 4),
+            "roofline": m["roof"], "kept_fraction": round(sum(m["kept"]) / m["tokens"], 3)}), flush=True)
+
+
 def main():
     ap = argparse.ArgumentParser(description=__doc__)
     ap.add_argument("--gpus", type=int, default=1)
@@ -79,6 +183,9 @@ def main():
     ap.add_argument("--copy-calibration", type=int, default=0, metavar="MIB",
                     help="after the run, copy MIB MiB once on the GPU (a reference kernel of known traffic for "
                          "hardware counters)")
+    ap.add_argument("--sweep", action="store_true",
+                    help="instead of the single measurement, sweep the window (n 4096) and the length (window "
+                         "512), one JSON line per point")
     args = ap.parse_args()
     if args.gpus != 1:
         print(f"bench.py measures one GPU only: the hot path runs on a single MI355X; --gpus {args.gpus} is not "
@@ -91,80 +198,25 @@ def main():
     import paper_2310_07109_amd as sc
     import sc_inputs as si
 
+    torch.cuda.set_device(0)
+    dev = "cuda:0"
+    if args.sweep:
+        sweep(args, sc, si, torch, np)
+        return
     cfg = si.CONFIGS[4]
     with open(os.path.join(ROOT, "tests", "golden", "thresholds.json")) as f:
         theta = json.load(f)["4"]["theta"]
     t0 = time.time()
     inp = si.make_attention_inputs(cfg)
     gen_s = time.time() - t0
-    dev = "cuda:0"
-    torch.cuda.set_device(0)
-
-    def i32(a):
-        return torch.from_numpy(np.ascontiguousarray(a, dtype=np.int32)).to(dev)
-
-    def bf(a):
-        return torch.from_numpy(np.ascontiguousarray(a).view(np.int16)).to(dev).view(torch.bfloat16)
-
-    d = sc.Desc(cfg.B, cfg.n, cfg.H, cfg.window, i32(inp["valid_len"]), i32(inp["global_pos"]), cfg.alpha,
-                sc.SC_BF16)
-    q, k, v = bf(inp["q"]), bf(inp["k"]), bf(inp["v"])
-    out = torch.empty_like(q)
-    lse = torch.empty((cfg.B, cfg.H, cfg.n), dtype=torch.float32, device=dev)
-    sp = torch.empty(sc.sc_score_partials_size(d) // 4, dtype=torch.float32, device=dev)
-    ws_attn = torch.empty(max(sc.sc_window_attention_workspace_size(d), 1), dtype=torch.uint8, device=dev)
-    scores = torch.empty((cfg.B, cfg.n), dtype=torch.float32, device=dev)
-    oc = torch.empty_like(out)
-    outs = dict(keep_idx=torch.empty((cfg.B, cfg.n), dtype=torch.int32, device=dev),
-                new_len=torch.empty((cfg.B,), dtype=torch.int32, device=dev),
-                new_global_pos=torch.empty((cfg.B, cfg.n_global), dtype=torch.int32, device=dev),
-                orig_idx_out=torch.empty((cfg.B, cfg.n), dtype=torch.int32, device=dev))
-    ws_prune = torch.empty(sc.sc_ltp_prune_compact_workspace_size(d), dtype=torch.uint8, device=dev)
-
-    def step():
-        sc.sc_window_attention(d, q, k, v, out=out, lse=lse, score_partials=sp, workspace=ws_attn)
-        sc.sc_ltp_score(d, sp, scores=scores)
-        sc.sc_ltp_prune_compact(d, scores, theta, True, [out], dsts=[oc], outs=outs, workspace=ws_prune)
-
-    for _ in range(args.warmup):
-        step()
-    torch.cuda.synchronize()
-    sc.sc_profile_window_kernel(True)
-    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-    w0 = time.perf_counter()
-    e0.record()
-    for _ in range(args.steps):
-        step()
-    e1.record()
-    torch.cuda.synchronize()
-    wall_ms = (time.perf_counter() - w0) * 1e3 / args.steps
-    ms = e0.elapsed_time(e1) / args.steps
-    kern_ms, launches = sc.sc_profile_window_kernel_read()
-    sc.sc_profile_window_kernel(False)
-    kern_ms /= max(launches, 1)
-
-    tokens = int(np.sum(inp["valid_len"]))
-    kept = outs["new_len"].cpu().tolist()
-    pairs_w, pairs_g = algorithmic_counts(inp)
-    hd = cfg.d
-    # algorithmic work of the two launches: Q.K^T and P.V once per allowed pair (the window rows and the
-    # global rows); read Q, K, V, write O (bf16), the LSE and the score partials (fp32)
-    flops = 4.0 * hd * cfg.H * (pairs_w + pairs_g)
-    bytes_ = tokens * cfg.H * (4 * hd * 2 + 4) + sp.numel() * 4
-    t_mfma = flops / (MFMA_PEAK_TFLOPS["bf16"] * 1e12)
-    t_hbm = bytes_ / (HBM_PEAK_GBS * 1e9)
-    if t_mfma >= t_hbm:
-        achieved = flops / (kern_ms * 1e-3) / 1e12
-        roof = dict(bound="mfma", achieved=round(achieved, 2), peak=MFMA_PEAK_TFLOPS["bf16"], unit="TFLOP/s")
-    else:
-        achieved = bytes_ / (kern_ms * 1e-3) / 1e9
-        roof = dict(bound="hbm", achieved=round(achieved, 1), peak=HBM_PEAK_GBS, unit="GB/s")
-    roof["frac"] = round(roof["achieved"] / roof["peak"], 4)
+    m = measure(sc, si, torch, np, inp, theta, args.steps, args.warmup, dev)
+    ms, tokens = m["ms"], m["tokens"]
+    roof = m["roof"]
     roof["traffic"] = recorded_traffic()
     roof["kernel"] = "k_attn_fwd<bf16> + k_attn_cols<bf16> (the two launches of the window attention)"
-    roof["kernel_us"] = round(kern_ms * 1e3, 2)
-    roof["algorithmic_flop"] = flops
-    roof["algorithmic_bytes"] = bytes_
+    roof["kernel_us"] = round(m["kern_ms"] * 1e3, 2)
+    roof["algorithmic_flop"] = m["flops"]
+    roof["algorithmic_bytes"] = m["bytes"]
 
     value = tokens / (ms * 1e-3)
     result = {
@@ -177,8 +229,8 @@ def main():
                    "global_tokens": cfg.n_global, "valid_tokens": tokens, "threshold": theta,
                    "parallelism": "none (1 GPU)"},
         "roofline": roof,
-        "kept_per_sequence": kept,
-        "wall_ms_per_step": round(wall_ms, 4),
+        "kept_per_sequence": m["kept"],
+        "wall_ms_per_step": round(m["wall_ms"], 4),
     }
     if not args.no_cpu_baseline:
         import oracle

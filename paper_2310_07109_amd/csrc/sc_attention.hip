@@ -89,32 +89,34 @@ struct Stage {
 // ------------------------------------------------------------ pass 1 tile ---
 // One 64-key tile for the 16 queries of a wave.  s[st][i] is the logit of
 // (key 16*st + 4g + i, query lr).  ok(st, i) masks keys (kMasked only).
-// The running max m_use is in scaled log2 units; softmax_scale >= 0, so the
-// tile max is taken on the raw logits and scaled once.
-template <int DT, bool kMasked, typename OkFn>
+// kHalf >= 0 restricts the tile to its 32 keys 32 kHalf .. 32 kHalf + 31
+// (sub-tiles 2 kHalf and 2 kHalf + 1).  The running max m_use is in scaled
+// log2 units; softmax_scale >= 0, so the tile max is taken on the raw logits
+// and scaled once.
+template <int DT, bool kMasked, int kHalf = -1, typename OkFn>
 SC_DEV void softmax_tile(const typename Tr<DT>::Frag (&qf)[Tr<DT>::kChunks], const typename Tr<DT>::T* sK,
                          const typename Tr<DT>::T* sV, float c2, int lr, int g, float& m_use, float& l_run,
                          f32x4 (&o)[4], OkFn ok) {
   using TR = Tr<DT>;
-  constexpr int P = TR::kPitch;
-  f32x4 s[4];
+  constexpr int kSt0 = kHalf < 0 ? 0 : 2 * kHalf, kNst = kHalf < 0 ? 4 : 2;
+  f32x4 s[kNst];
 #pragma unroll
-  for (int st = 0; st < 4; ++st) {
+  for (int sj = 0; sj < kNst; ++sj) {
     typename TR::Frag kf[TR::kChunks];
-    TR::load_frags(sK, 16 * st + lr, g, kf);
+    TR::load_frags(sK, 16 * (kSt0 + sj) + lr, g, kf);
     f32x4 acc = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
     for (int c = 0; c < TR::kChunks; ++c) acc = TR::mma(kf[c], qf[c], acc);
-    s[st] = acc;
+    s[sj] = acc;
   }
-  bool valid[4][4];
+  bool valid[kNst][4];
   float tmax = -INFINITY;
 #pragma unroll
-  for (int st = 0; st < 4; ++st)
+  for (int sj = 0; sj < kNst; ++sj)
 #pragma unroll
     for (int i = 0; i < 4; ++i) {
-      valid[st][i] = !kMasked || ok(st, i);
-      tmax = vmax(tmax, valid[st][i] ? s[st][i] : -INFINITY);
+      valid[sj][i] = !kMasked || ok(kSt0 + sj, i);
+      tmax = vmax(tmax, valid[sj][i] ? s[sj][i] : -INFINITY);
     }
   tmax = group_max(tmax) * c2;
   if (tmax > m_use + kTau) {
@@ -124,24 +126,25 @@ SC_DEV void softmax_tile(const typename Tr<DT>::Frag (&qf)[Tr<DT>::kChunks], con
     for (int dt = 0; dt < 4; ++dt) o[dt] *= f;
     m_use = tmax;
   }
-  float p[4][4];
+  float p[kNst][4];
 #pragma unroll
-  for (int st = 0; st < 4; ++st)
+  for (int sj = 0; sj < kNst; ++sj)
 #pragma unroll
     for (int i = 0; i < 4; ++i) {
-      const float e = fast_exp2(fmaf(s[st][i], c2, -m_use));
-      p[st][i] = valid[st][i] ? e : 0.f;
-      l_run += p[st][i];
+      const float e = fast_exp2(fmaf(s[sj][i], c2, -m_use));
+      p[sj][i] = valid[sj][i] ? e : 0.f;
+      l_run += p[sj][i];
     }
   if constexpr (DT == 1) {
     // keys of lane group g in MFMA order: 32kc + 4g + (0..3), then 32kc + 16 + 4g + (0..3)
 #pragma unroll
-    for (int kc = 0; kc < 2; ++kc) {
+    for (int kj = 0; kj < kNst / 2; ++kj) {
+      const int kc = kSt0 / 2 + kj;
       bf16x8 pb;
 #pragma unroll
       for (int i = 0; i < 4; ++i) {
-        pb[i] = (__bf16)p[2 * kc][i];
-        pb[4 + i] = (__bf16)p[2 * kc + 1][i];
+        pb[i] = (__bf16)p[2 * kj][i];
+        pb[4 + i] = (__bf16)p[2 * kj + 1][i];
       }
       // lane (g, lr) supplies dims 16dt + 4(lr&3) .. +3 of value rows
       // 32kc + 4g + lr/4 and 32kc + 16 + 4g + lr/4
@@ -156,12 +159,13 @@ SC_DEV void softmax_tile(const typename Tr<DT>::Frag (&qf)[Tr<DT>::kChunks], con
     }
   } else {
 #pragma unroll
-    for (int st = 0; st < 4; ++st)
+    for (int sj = 0; sj < kNst; ++sj)
 #pragma unroll
       for (int i = 0; i < 4; ++i)
 #pragma unroll
         for (int dt = 0; dt < 4; ++dt)
-          o[dt] = TR::mma(sV[TR::voff(16 * st + 4 * g + i, 4 * dt + (lr >> 2)) + (lr & 3)], p[st][i], o[dt]);
+          o[dt] = TR::mma(sV[TR::voff(16 * (kSt0 + sj) + 4 * g + i, 4 * dt + (lr >> 2)) + (lr & 3)], p[sj][i],
+                          o[dt]);
   }
 }
 
@@ -471,13 +475,13 @@ SC_DEV GrBlock gr_block(const AttnArgs& a, int lin) {
   return r;
 }
 
-// Positions of the block's 64 global slots (-1: unused) into pos; returns
+// Positions of the block's global slots (-1: unused) into pos[0..63]; returns
 // whether any is used.  Contains a barrier.
 SC_DEV bool gr_slots(const AttnArgs& a, const GrBlock& blk, int L, int* pos) {
   int valid = 0;
-  if (threadIdx.x < kGlobalChunk) {
+  if (threadIdx.x < kBK) {  // 64 staged rows; those beyond the chunk's slots are unused
     const int j = kGlobalChunk * blk.gc + threadIdx.x;
-    const int p = j < a.G ? a.gpos[(long long)blk.b * a.G + j] : -1;
+    const int p = threadIdx.x < kGlobalChunk && j < a.G ? a.gpos[(long long)blk.b * a.G + j] : -1;
     valid = p >= 0 && p < L;
     pos[threadIdx.x] = valid ? p : -1;
   }
@@ -514,11 +518,12 @@ SC_DEV void gr_fwd_block(const AttnArgs& a, int lin, Smem<DT>& sm) {
   stk.store(sm.b[0]);
   stv.template store<true>(sm.c[0]);
   __syncthreads();
+  // wave w serves the 16 slots of group sg = w & 1 over the key half kh = w >> 1
+  // of every tile; the two halves are merged at the end
+  const int sg = w & 1, kh = w >> 1;
   typename TR::Frag qf[TR::kChunks];
-  TR::load_frags(sm.b[1], 16 * w + lr, g, qf);
-  // waves whose 16 slots are all unused only help with the loads (with G = 32
-  // that is half of each block)
-  const bool wlive = __ballot(sm.pos[0][16 * w + lr] >= 0) != 0ull;
+  TR::load_frags(sm.b[1], 16 * sg + lr, g, qf);
+  const bool wlive = __ballot(sm.pos[0][16 * sg + lr] >= 0) != 0ull;  // some slot of the group is used
   __syncthreads();  // every wave holds its query fragments before b[1] is reused
   float m_use = kNegBig, l_run = 0.f;
   f32x4 o[4];
@@ -530,13 +535,21 @@ SC_DEV void gr_fwd_block(const AttnArgs& a, int lin, Smem<DT>& sm) {
       stk.load_range(Kg, a.ld_in, k0 + kBK, kend);
       stv.load_range(Vg, a.ld_in, k0 + kBK, kend);
     }
-    if (!wlive) {
-    } else if (k0 + kBK <= kend) {
-      softmax_tile<DT, false>(qf, sm.b[buf], sm.c[buf], a.c2, lr, g, m_use, l_run, o, [](int, int) { return true; });
-    } else {
-      const int hi = kend - 1 - k0;
-      softmax_tile<DT, true>(qf, sm.b[buf], sm.c[buf], a.c2, lr, g, m_use, l_run, o,
-                             [&](int s4, int i) { return 16 * s4 + 4 * g + i <= hi; });
+    if (wlive && k0 + 32 * kh < kend) {
+      if (k0 + kBK <= kend) {
+        auto all = [](int, int) { return true; };
+        if (kh == 0)
+          softmax_tile<DT, false, 0>(qf, sm.b[buf], sm.c[buf], a.c2, lr, g, m_use, l_run, o, all);
+        else
+          softmax_tile<DT, false, 1>(qf, sm.b[buf], sm.c[buf], a.c2, lr, g, m_use, l_run, o, all);
+      } else {
+        const int hi = kend - 1 - k0;
+        auto below = [&](int s4, int i) { return 16 * s4 + 4 * g + i <= hi; };
+        if (kh == 0)
+          softmax_tile<DT, true, 0>(qf, sm.b[buf], sm.c[buf], a.c2, lr, g, m_use, l_run, o, below);
+        else
+          softmax_tile<DT, true, 1>(qf, sm.b[buf], sm.c[buf], a.c2, lr, g, m_use, l_run, o, below);
+      }
     }
     if (t + 1 < ntile) {
       stk.store(sm.b[buf ^ 1]);
@@ -544,8 +557,33 @@ SC_DEV void gr_fwd_block(const AttnArgs& a, int lin, Smem<DT>& sm) {
     }
     __syncthreads();
   }
-  const float l_row = group_sum(l_run);
-  const int slot = kGlobalChunk * blk.gc + 16 * w + lr;
+  float l_row = group_sum(l_run);
+  // merge the two key halves of each slot group through LDS (the key tiles
+  // are no longer needed): the kh = 1 wave publishes its row state, the
+  // kh = 0 wave combines, in that fixed order
+  constexpr int kXRow = 68;  // floats per row: 64 dims, max, sum (16-byte aligned rows)
+  float* xch = reinterpret_cast<float*>(&sm.b[0][0]);
+  float* xrow = xch + (16 * sg + lr) * kXRow;
+  if (kh == 1) {
+#pragma unroll
+    for (int dt = 0; dt < 4; ++dt) *reinterpret_cast<f32x4*>(xrow + 16 * dt + 4 * g) = o[dt];
+    if (g == 0) {
+      xrow[64] = m_use;
+      xrow[65] = l_row;
+    }
+  }
+  __syncthreads();
+  if (kh == 1) return;
+  {
+    const float m1 = xrow[64], l1 = xrow[65];
+    const float m = vmax(m_use, m1);
+    const float f0 = fast_exp2(m_use - m), f1 = fast_exp2(m1 - m);
+    l_row = l_row * f0 + l1 * f1;
+#pragma unroll
+    for (int dt = 0; dt < 4; ++dt) o[dt] = o[dt] * f0 + *reinterpret_cast<const f32x4*>(xrow + 16 * dt + 4 * g) * f1;
+    m_use = m;
+  }
+  const int slot = kGlobalChunk * blk.gc + 16 * sg + lr;
   const long long idx = ((long long)blk.bh * a.nkc + blk.kc) * a.Gp + slot;
   if (g == 0) {
     a.gr_ml[2 * idx] = m_use;
@@ -1109,9 +1147,9 @@ SC_DEV void gcol_block(const AttnArgs& a, int lin, SmemCol<DT>& sm) {
   const float* l2g = a.win_lse2 + (long long)bh * n;
   const int* gp = a.gpos + (long long)b * G;
   int* pos = sm.pos[0];
-  if (tid < kGlobalChunk) {
+  if (tid < kBK) {  // 64 staged rows; those beyond the chunk's slots are unused
     const int j = kGlobalChunk * gc + tid;
-    const int p = j < G ? gp[j] : -1;
+    const int p = tid < kGlobalChunk && j < G ? gp[j] : -1;
     pos[tid] = (p >= 0 && p < L) ? p : -1;
   }
   __syncthreads();
@@ -1135,10 +1173,15 @@ SC_DEV void gcol_block(const AttnArgs& a, int lin, SmemCol<DT>& sm) {
   load(0);
   store(0);
   __syncthreads();
+  // wave w serves the 16 global keys of group kg = w & 1 against the query
+  // half qh = w >> 1 (16-query groups 2 qh, 2 qh + 1) of every tile; the two
+  // halves' sums are added at the end
+  const int kg = w & 1, qh = w >> 1;
+  const unsigned qlive = qh ? 0xCu : 0x3u;
   typename TR::Frag kf[TR::kChunks];
-  TR::load_frags(sm.a, 16 * w + lr, g, kf);
-  const int slot = kGlobalChunk * gc + 16 * w + lr;
-  const bool kuse = pos[16 * w + lr] >= 0;
+  TR::load_frags(sm.a, 16 * kg + lr, g, kf);
+  const int slot = kGlobalChunk * gc + 16 * kg + lr;
+  const bool kuse = pos[16 * kg + lr] >= 0;
   const bool wlive = __ballot(kuse) != 0ull;  // some of the wave's 16 global keys is used
   float* bpc = kBandProbs ? a.bp_gcol + (long long)bh * n * G : nullptr;
   float cs = 0.f;
@@ -1152,15 +1195,24 @@ SC_DEV void gcol_block(const AttnArgs& a, int lin, SmemCol<DT>& sm) {
                                 [&](int qq, float p) {
                                   const int q = qs + qq;
                                   if (kuse && q < L && p != 0.f) bpc[(long long)q * G + slot] = p;
-                                });
+                                }, qlive);
     } else {
-      cs += col_tile<DT, false>(kf, sm.b[buf], sm.l[buf], a.c2, lr, g, [](int, int) { return true; }, NoEmit{});
+      cs += col_tile<DT, false>(kf, sm.b[buf], sm.l[buf], a.c2, lr, g, [](int, int) { return true; }, NoEmit{},
+                                qlive);
     }
     if (t + 1 < nqt) store(buf ^ 1);
     __syncthreads();
   }
   cs = group_sum(cs);
-  if (a.part_extra && g == 0 && slot < G) a.part_extra[((long long)bh * a.nqr + qr) * G + slot] = kuse ? cs : 0.f;
+  // the qh = 1 wave hands its sum to the qh = 0 wave of the same keys (the
+  // staged LSE rows are no longer needed)
+  float* xs = sm.l[0];
+  if (qh == 1 && g == 0) xs[16 * kg + lr] = cs;
+  __syncthreads();
+  if (qh == 0) {
+    cs += xs[16 * kg + lr];
+    if (a.part_extra && g == 0 && slot < G) a.part_extra[((long long)bh * a.nqr + qr) * G + slot] = kuse ? cs : 0.f;
+  }
 }
 
 // Global rows, second half: merge the key-range partials of the block's 64

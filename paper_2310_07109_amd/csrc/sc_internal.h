@@ -8,7 +8,7 @@ namespace sc {
 
 constexpr int kQueryBlock = 64;    // queries per window-attention workgroup
 constexpr int kKeyTile = 64;       // keys per LDS tile
-constexpr int kGlobalChunk = 64;   // global slots per workgroup of the global-row kernels
+constexpr int kGlobalChunk = 32;   // global slots per workgroup of the global-row / global-column blocks
 constexpr int kGlobalKeySpan = 512;  // keys per split of the global-row kernels
 
 // Geometry + pointers of one attention launch sequence.  Element strides let
