@@ -602,6 +602,15 @@ SC_DEV void gr_fwd_block(const AttnArgs& a, int lin, Smem<DT>& sm) {
 // layout is produced by choosing which 16-byte unit of its row lane i fetches.
 constexpr int kBQ2 = 128;
 
+// The lane id, opaque to the compiler: values derived from it are
+// recomputed where they are used instead of being hoisted out of the tile
+// loops and held in registers across them.
+SC_DEV int opaque_lane() {
+  int lane;
+  asm volatile("v_mbcnt_lo_u32_b32 %0, -1, 0\n\tv_mbcnt_hi_u32_b32 %0, -1, %0" : "=v"(lane));
+  return lane;
+}
+
 // One direct load: lane i's 16 bytes at base + voff land at LDS byte address
 // lds + 16 i (gfx950 global_load_lds_dwordx4, destination base in m0).  Inline
 // assembly on purpose: the compiler cannot tell these writes from later LDS
@@ -623,7 +632,8 @@ SC_DEV void wait_dma() { asm volatile("s_waitcnt vmcnt(0)" ::: "memory"); }
 // row R holds global row rowfn(R), which must be a valid row.  Byte offsets
 // from the slice base fit in 32 bits (checked by the host).
 template <typename RowFn>
-SC_DEV void tile_dma(const __bf16* g, unsigned ld_bytes, __bf16* tile, int w, int lane, RowFn rowfn) {
+SC_DEV void tile_dma(const __bf16* g, unsigned ld_bytes, __bf16* tile, int w, int, RowFn rowfn) {
+  const int lane = opaque_lane();
 #pragma unroll
   for (int j = 0; j < 2; ++j) {
     const int R0 = 16 * w + 8 * j, R = R0 + (lane >> 3);
@@ -637,12 +647,12 @@ SC_DEV void tile_dma(const __bf16* g, unsigned ld_bytes, __bf16* tile, int w, in
 // masked tiles ok(j, st, i) decides the pair (sub-block j's query, key
 // 16 st + 4g + i).  Disallowed logits become -inf, which exp2 maps to 0
 // (c2 > 0 is guaranteed by the host).
-template <bool kMasked, typename OkFn>
-SC_DEV void softmax_tile2(const bf16x8 (&qf)[2][2], const __bf16* sK, const __bf16* sV, float c2, int lr, int g,
-                          float (&m_use)[2], float (&l_run)[2], f32x4 (&o)[2][4], unsigned live, OkFn ok) {
+// S^T = K Q^T of one 64-key tile for both sub-blocks; dead sub-tiles give 0.
+template <bool kMasked>
+SC_DEV void qk_tile2(const bf16x8 (&qf)[2][2], const __bf16* sK, int lr_in, int g_in, unsigned live, f32x4 (&s)[2][4]) {
   using TR = Tr<1>;
   auto is_live = [&](int st) { return !kMasked || ((live >> st) & 1u); };
-  f32x4 s[2][4];
+  const int lr = lr_in, g = g_in;
 #pragma unroll
   for (int st = 0; st < 4; ++st) {
     s[0][st] = f32x4{0.f, 0.f, 0.f, 0.f};
@@ -657,30 +667,45 @@ SC_DEV void softmax_tile2(const bf16x8 (&qf)[2][2], const __bf16* sK, const __bf
       }
     }
   }
-  if constexpr (kMasked) {
-#pragma unroll
-    for (int j = 0; j < 2; ++j)
-#pragma unroll
-      for (int st = 0; st < 4; ++st)
-#pragma unroll
-        for (int i = 0; i < 4; ++i) s[j][st][i] = (is_live(st) && ok(j, st, i)) ? s[j][st][i] : -INFINITY;
-  }
-  // raise a running max only when the tile max exceeds it by kTau (lanes
-  // that do not need it skip the rescale under the execution mask)
+}
+
+// Row maxima of a tile in log2 units (per sub-block).
+SC_DEV void tile_max2(const f32x4 (&s)[2][4], float c2, float (&tmax)[2]) {
 #pragma unroll
   for (int j = 0; j < 2; ++j) {
     float m4[4];
 #pragma unroll
     for (int st = 0; st < 4; ++st) m4[st] = vmax(vmax(s[j][st][0], s[j][st][1]), vmax(s[j][st][2], s[j][st][3]));
-    const float tmax = group_max(vmax(vmax(m4[0], m4[1]), vmax(m4[2], m4[3]))) * c2;
-    if (tmax > m_use[j] + kTau) {
-      const float f = fast_exp2(m_use[j] - tmax);
-      l_run[j] *= f;
-#pragma unroll
-      for (int dt = 0; dt < 4; ++dt) o[j][dt] *= f;
-      m_use[j] = tmax;
-    }
+    tmax[j] = group_max(vmax(vmax(m4[0], m4[1]), vmax(m4[2], m4[3]))) * c2;
   }
+}
+
+// Whether any lane's running max must be raised (tile max above it by kTau).
+SC_DEV bool need_raise2(const float (&tmax)[2], const float (&m_use)[2]) {
+  return __builtin_amdgcn_ballot_w64((tmax[0] > m_use[0] + kTau) | (tmax[1] > m_use[1] + kTau)) != 0ull;
+}
+
+// Raises the running maxima that need it and rescales their sums and
+// accumulators (lanes that do not need it scale by 1).
+SC_DEV void raise2(const float (&tmax)[2], float (&m_use)[2], float (&l_run)[2], f32x4 (&o)[2][4]) {
+#pragma unroll
+  for (int j = 0; j < 2; ++j) {
+    const bool up = tmax[j] > m_use[j] + kTau;
+    const float f = up ? fast_exp2(m_use[j] - tmax[j]) : 1.0f;
+    m_use[j] = up ? tmax[j] : m_use[j];
+    l_run[j] *= f;
+#pragma unroll
+    for (int dt = 0; dt < 4; ++dt) o[j][dt] *= f;
+  }
+}
+
+// P = exp2(S c2 - m) (summed into l) and O^T += V^T P^T for one tile.
+template <bool kMasked>
+SC_DEV void pv_tile2(const f32x4 (&s)[2][4], const __bf16* sV, float c2, int, int, const float (&m_use)[2],
+                     float (&l_run)[2], f32x4 (&o)[2][4], unsigned live) {
+  using TR = Tr<1>;
+  auto is_live = [&](int st) { return !kMasked || ((live >> st) & 1u); };
+  const int ln = opaque_lane(), lr = ln & 15, g = ln >> 4;
   bf16x8 pb[2][2];
 #pragma unroll
   for (int j = 0; j < 2; ++j) {
@@ -712,6 +737,32 @@ SC_DEV void softmax_tile2(const bf16x8 (&qf)[2][2], const __bf16* sK, const __bf
       o[1][dt] = TR::mma(vf, pb[1][kc], o[1][dt]);
     }
   }
+}
+
+// One 64-key tile for the two query sub-blocks of a wave.  Bit st of `live`
+// (wave-uniform) says whether 16-key sub-tile st can hold an allowed pair; in
+// masked tiles ok(j, st, i) decides the pair (sub-block j's query, key
+// 16 st + 4g + i).  Disallowed logits become -inf, which exp2 maps to 0
+// (c2 > 0 is guaranteed by the host).  The running max is raised only when
+// the tile max exceeds it by kTau (for the whole wave when any lane needs it).
+template <bool kMasked, typename OkFn>
+SC_DEV void softmax_tile2(const bf16x8 (&qf)[2][2], const __bf16* sK, const __bf16* sV, float c2, int lr, int g,
+                          float (&m_use)[2], float (&l_run)[2], f32x4 (&o)[2][4], unsigned live, OkFn ok) {
+  f32x4 s[2][4];
+  qk_tile2<kMasked>(qf, sK, lr, g, live, s);
+  if constexpr (kMasked) {
+#pragma unroll
+    for (int j = 0; j < 2; ++j)
+#pragma unroll
+      for (int st = 0; st < 4; ++st)
+#pragma unroll
+        for (int i = 0; i < 4; ++i)
+          s[j][st][i] = (((live >> st) & 1u) && ok(j, st, i)) ? s[j][st][i] : -INFINITY;
+  }
+  float tmax[2];
+  tile_max2(s, c2, tmax);
+  if (need_raise2(tmax, m_use)) raise2(tmax, m_use, l_run, o);
+  pv_tile2<kMasked>(s, sV, c2, lr, g, m_use, l_run, o, live);
 }
 
 // Pass 1 for bf16: O, LSE and the log2 LSE of the block's 128 queries.
@@ -787,52 +838,76 @@ SC_DEV void window_fwd_v2(const AttnArgs& a, int blk, Smem<1>& sm, uint32_t* sDy
     lo[j] = q - r - 4 * g;
     hi[j] = min(q + r, kt1 - 1) - 4 * g;
   }
-  for (int t = 0; t < nkt; ++t) {
-    const int buf = t & 1, k0 = kt0 + t * kBK;
+  // every tile step: load the next tile into the other buffer, compute,
+  // wait for the load, barrier (the same sequence in all three phases below)
+  auto issue = [&](int t) {
     if (t + 1 < nkt) {
-      tile_dma(Kg, ldb, sm.b[buf ^ 1], w, lane, band_rows(k0 + kBK));
-      tile_dma(Vg, ldb, sm.c[buf ^ 1], w, lane, band_rows(k0 + kBK));
+      const int k1 = kt0 + (t + 1) * kBK;
+      tile_dma(Kg, ldb, sm.b[(t + 1) & 1], w, lane, band_rows(k1));
+      tile_dma(Vg, ldb, sm.c[(t + 1) & 1], w, lane, band_rows(k1));
     }
-    const unsigned long long gall = tile_gmask(sBits, t, wb.nwords);
-    const bool near = k0 <= qa + 31 + r && k0 + kBK - 1 >= qa - r;
-    if (near || gall != 0ull) {
-      if (k0 + kBK <= kt1 && k0 >= qa + 31 - r && k0 + kBK - 1 <= qa + r) {
-        softmax_tile2<false>(qf, sm.b[buf], sm.c[buf], a.c2, lr, g, m_use, l_run, o, 0xFu,
-                             [](int, int, int) { return true; });
-      } else {
-        const int wlo = qa - r - k0, whi = min(qa + 31 + r, kt1 - 1) - k0;
-        unsigned live = 0u;
-#pragma unroll
-        for (int st = 0; st < 4; ++st)
-          live |= (unsigned)((16 * st + 15 >= wlo && 16 * st <= whi) || ((gall >> (16 * st)) & 0xFFFFull) != 0ull)
-                  << st;
-        const int l0 = lo[0] - k0, h0 = hi[0] - k0, l1 = lo[1] - k0, h1 = hi[1] - k0;
-        // a band edge is one-sided in most tiles: the band starts inside the
-        // tile for some query (nlo) or ends inside it (nhi), wave-uniform
-        const bool nlo = qa + 31 - r - k0 > 0, nhi = min(qa + r, kt1 - 1) - k0 < kBK - 1;
-        if (gall == 0ull && !nhi) {
-          softmax_tile2<true>(qf, sm.b[buf], sm.c[buf], a.c2, lr, g, m_use, l_run, o, live,
-                              [&](int j, int st, int i) { return 16 * st + i >= (j == 0 ? l0 : l1); });
-        } else if (gall == 0ull && !nlo) {
-          softmax_tile2<true>(qf, sm.b[buf], sm.c[buf], a.c2, lr, g, m_use, l_run, o, live,
-                              [&](int j, int st, int i) { return 16 * st + i <= (j == 0 ? h0 : h1); });
-        } else if (gall == 0ull) {
-          softmax_tile2<true>(qf, sm.b[buf], sm.c[buf], a.c2, lr, g, m_use, l_run, o, live, [&](int j, int st, int i) {
-            const int c = 16 * st + i;
-            return j == 0 ? (c >= l0) & (c <= h0) : (c >= l1) & (c <= h1);
-          });
-        } else {
-          const unsigned long long gm = gall >> (4 * g);
-          softmax_tile2<true>(qf, sm.b[buf], sm.c[buf], a.c2, lr, g, m_use, l_run, o, live, [&](int j, int st, int i) {
-            const int c = 16 * st + i;
-            const bool band = j == 0 ? (c >= l0) & (c <= h0) : (c >= l1) & (c <= h1);
-            return band | (bool)((gm >> c) & 1ull);
-          });
-        }
-      }
-    }
+  };
+  auto finish = [&](int t) {
     if (t + 1 < nkt) wait_dma();
     __syncthreads();
+  };
+  // tiles that need a mask (band edges, global keys) or are skipped
+  auto edge_tile = [&](int t) {
+    const int buf = t & 1, k0 = kt0 + t * kBK;
+    const unsigned long long gall = tile_gmask(sBits, t, wb.nwords);
+    const bool near = k0 <= qa + 31 + r && k0 + kBK - 1 >= qa - r;
+    if (!near && gall == 0ull) return;
+    const int wlo = qa - r - k0, whi = min(qa + 31 + r, kt1 - 1) - k0;
+    unsigned live = 0u;
+#pragma unroll
+    for (int st = 0; st < 4; ++st)
+      live |= (unsigned)((16 * st + 15 >= wlo && 16 * st <= whi) || ((gall >> (16 * st)) & 0xFFFFull) != 0ull) << st;
+    const int l0 = lo[0] - k0, h0 = hi[0] - k0, l1 = lo[1] - k0, h1 = hi[1] - k0;
+    // a band edge is one-sided in most tiles: the band starts inside the
+    // tile for some query (nlo) or ends inside it (nhi), wave-uniform
+    const bool nlo = qa + 31 - r - k0 > 0, nhi = min(qa + r, kt1 - 1) - k0 < kBK - 1;
+    if (gall == 0ull && !nhi) {
+      softmax_tile2<true>(qf, sm.b[buf], sm.c[buf], a.c2, lr, g, m_use, l_run, o, live,
+                          [&](int j, int st, int i) { return 16 * st + i >= (j == 0 ? l0 : l1); });
+    } else if (gall == 0ull && !nlo) {
+      softmax_tile2<true>(qf, sm.b[buf], sm.c[buf], a.c2, lr, g, m_use, l_run, o, live,
+                          [&](int j, int st, int i) { return 16 * st + i <= (j == 0 ? h0 : h1); });
+    } else if (gall == 0ull) {
+      softmax_tile2<true>(qf, sm.b[buf], sm.c[buf], a.c2, lr, g, m_use, l_run, o, live, [&](int j, int st, int i) {
+        const int c = 16 * st + i;
+        return j == 0 ? (c >= l0) & (c <= h0) : (c >= l1) & (c <= h1);
+      });
+    } else {
+      const unsigned long long gm = gall >> (4 * g);
+      softmax_tile2<true>(qf, sm.b[buf], sm.c[buf], a.c2, lr, g, m_use, l_run, o, live, [&](int j, int st, int i) {
+        const int c = 16 * st + i;
+        const bool band = j == 0 ? (c >= l0) & (c <= h0) : (c >= l1) & (c <= h1);
+        return band | (bool)((gm >> c) & 1ull);
+      });
+    }
+  };
+  // interior tiles [ia, ib) of this wave: every key of the tile lies in the
+  // band of all 32 queries and below kt1 (global keys among them are band
+  // keys), so no mask is needed
+  const int ia = clampi(-((kt0 - (qa + 31 - r)) >> 6), 0, nkt);
+  const int ib = clampi(((min(qa + r, kt1 - 1) - (kBK - 1) - kt0) >> 6) + 1, ia, nkt);
+  int t = 0;
+  for (; t < ia; ++t) {
+    issue(t);
+    edge_tile(t);
+    finish(t);
+  }
+  // interior loop: one variant, no mask
+  for (; t < ib; ++t) {
+    issue(t);
+    softmax_tile2<false>(qf, sm.b[t & 1], sm.c[t & 1], a.c2, lr, g, m_use, l_run, o, 0xFu,
+                         [](int, int, int) { return true; });
+    finish(t);
+  }
+  for (; t < nkt; ++t) {
+    issue(t);
+    edge_tile(t);
+    finish(t);
   }
   // global keys outside the block's key range, 64 slots per tile (few tiles;
   // not pipelined)
