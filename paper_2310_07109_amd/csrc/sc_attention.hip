@@ -1315,17 +1315,36 @@ SC_DEV void gr_col_block(const AttnArgs& a, int lin, SmemCol<DT>& sm) {
   }
   const int* pos = sm.pos[0];
   const int nk = (L + kGlobalKeySpan - 1) / kGlobalKeySpan;
-  float* sM = sm.l[1];  // per-row running max of the merge
-  if (tid < kGlobalChunk) {
-    const int slot = kGlobalChunk * blk.gc + tid;
-    float lse2 = INFINITY, m = kNegBig;
-    if (pos[tid] >= 0) {
-      for (int kc = 0; kc < nk; ++kc) m = fmaxf(m, a.gr_ml[2 * (((long long)blk.bh * a.nkc + kc) * a.Gp + slot)]);
-      float l = 0.f;
-      for (int kc = 0; kc < nk; ++kc) {
+  float* sM = sm.l[1];  // per-row max of the merge
+  // merge of the key-chunk partials (m, l) of the block's global rows: thread
+  // (row, part) combines chunks part, part + 8, ... (a single round of loads
+  // for up to 8 chunks), then 32 threads combine the 8 parts
+  static_assert(kThreads == 8 * kGlobalChunk, "merge layout: 8 parts of kGlobalChunk rows");
+  float* red = reinterpret_cast<float*>(sm.b[1]);  // [2][8][kGlobalChunk]; b[1] is free until the tile loop
+  {
+    const int row = tid % kGlobalChunk, part = tid / kGlobalChunk;
+    const int slot = kGlobalChunk * blk.gc + row;
+    float m = kNegBig, l = 0.f;
+    if (pos[row] >= 0)
+      for (int kc = part; kc < nk; kc += 8) {
         const long long idx = ((long long)blk.bh * a.nkc + kc) * a.Gp + slot;
-        l += a.gr_ml[2 * idx + 1] * fast_exp2(a.gr_ml[2 * idx] - m);
+        const float mk = a.gr_ml[2 * idx], lk = a.gr_ml[2 * idx + 1];
+        const float mn = fmaxf(m, mk);
+        l = l * fast_exp2(m - mn) + lk * fast_exp2(mk - mn);
+        m = mn;
       }
+    red[tid] = m;
+    red[kThreads + tid] = l;
+  }
+  __syncthreads();
+  if (tid < kGlobalChunk) {
+    float m = kNegBig, l = 0.f;
+#pragma unroll
+    for (int p = 0; p < 8; ++p) m = fmaxf(m, red[p * kGlobalChunk + tid]);
+#pragma unroll
+    for (int p = 0; p < 8; ++p) l += red[kThreads + p * kGlobalChunk + tid] * fast_exp2(red[p * kGlobalChunk + tid] - m);
+    float lse2 = INFINITY;
+    if (pos[tid] >= 0) {
       lse2 = m + fast_log2(l);
       if (blk.kc == 0 && a.lse) a.lse[(long long)blk.bh * a.n + pos[tid]] = lse2 * kLn2;
     }
@@ -1333,19 +1352,32 @@ SC_DEV void gr_col_block(const AttnArgs& a, int lin, SmemCol<DT>& sm) {
     sM[tid] = m;
   }
   __syncthreads();
-  if (blk.kc == 0) {  // output rows of the global queries
-    T* Ob = static_cast<T*>(a.out) + blk.b * a.bs_out + blk.h * kHeadDim;
-    for (int e = tid; e < kGlobalChunk * kHeadDim; e += kThreads) {
-      const int row = e / kHeadDim, d = e % kHeadDim;
-      if (pos[row] < 0) continue;
+  if (blk.kc == 0) {  // output rows of the global queries: 8 dims of one row per thread
+    const int row = tid >> 3, d0 = 8 * (tid & 7);
+    if (pos[row] >= 0) {
+      T* Ob = static_cast<T*>(a.out) + blk.b * a.bs_out + blk.h * kHeadDim;
       const int slot = kGlobalChunk * blk.gc + row;
       const float m = sM[row], lse2 = sm.l[0][row];
-      float acc = 0.f;
-      for (int kc = 0; kc < nk; ++kc) {
-        const long long idx = ((long long)blk.bh * a.nkc + kc) * a.Gp + slot;
-        acc += a.gr_o[idx * kHeadDim + d] * fast_exp2(a.gr_ml[2 * idx] - m);
+      float acc[8] = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
+      for (int kc0 = 0; kc0 < nk; kc0 += 4) {  // four chunks' loads in flight together
+        f32x4 v[4][2];
+        float wt[4];
+#pragma unroll
+        for (int u = 0; u < 4; ++u) {
+          const int kc = min(kc0 + u, nk - 1);
+          const long long idx = ((long long)blk.bh * a.nkc + kc) * a.Gp + slot;
+          v[u][0] = *reinterpret_cast<const f32x4*>(a.gr_o + idx * kHeadDim + d0);
+          v[u][1] = *reinterpret_cast<const f32x4*>(a.gr_o + idx * kHeadDim + d0 + 4);
+          wt[u] = kc0 + u < nk ? fast_exp2(a.gr_ml[2 * idx] - m) : 0.f;
+        }
+#pragma unroll
+        for (int u = 0; u < 4; ++u)
+#pragma unroll
+          for (int i = 0; i < 8; ++i) acc[i] += v[u][i >> 2][i & 3] * wt[u];
       }
-      Ob[(long long)pos[row] * a.ld_out + d] = (T)(acc * fast_exp2(m - lse2));
+      const float sc = fast_exp2(m - lse2);
+#pragma unroll
+      for (int i = 0; i < 8; ++i) Ob[(long long)pos[row] * a.ld_out + d0 + i] = (T)(acc[i] * sc);
     }
   }
   if (!want_cols) return;
