@@ -30,6 +30,16 @@ KERNEL_SOURCES = ("paper_2310_07109_amd/csrc/sc_attention.hip", "paper_2310_0710
 TRAFFIC_FILE = os.path.join(ROOT, "profiles", "window_attention_seq4096_traffic.json")
 
 
+# name -> (input config, workload description)
+WORKLOADS = {
+    "seq4096": (4, "single sparse-attention + LTP layer: B8 n4096 H12 d64 bf16, window 512, 32 seeded global "
+                   "tokens, valid lengths U[2048,4096], threshold pruning ~50%"),
+    "lognormal": (6, "single sparse-attention + LTP layer: B64 n1024 H12 d64 bf16, window 256, global token 0, "
+                     "valid lengths round(exp(N(5.717, 0.738^2))) clipped to [1,1024] (paper-shaped), threshold "
+                     "pruning ~30%"),
+}
+
+
 def kernel_source_hash():
     h = hashlib.sha256()
     for f in KERNEL_SOURCES:
@@ -183,6 +193,9 @@ def main():
     ap.add_argument("--copy-calibration", type=int, default=0, metavar="MIB",
                     help="after the run, copy MIB MiB once on the GPU (a reference kernel of known traffic for "
                          "hardware counters)")
+    ap.add_argument("--workload", choices=sorted(WORKLOADS), default="seq4096",
+                    help="seq4096: B8 n4096 window 512, 32 global tokens (the headline line); lognormal: B64 n1024 "
+                         "window 256, one global token, paper-shaped lognormal lengths")
     ap.add_argument("--sweep", action="store_true",
                     help="instead of the single measurement, sweep the window (n 4096) and the length (window "
                          "512), one JSON line per point")
@@ -203,16 +216,18 @@ def main():
     if args.sweep:
         sweep(args, sc, si, torch, np)
         return
-    cfg = si.CONFIGS[4]
+    cid, desc = WORKLOADS[args.workload]
+    cfg = si.CONFIGS[cid]
     with open(os.path.join(ROOT, "tests", "golden", "thresholds.json")) as f:
-        theta = json.load(f)["4"]["theta"]
+        theta = json.load(f)[str(cid)]["theta"]
     t0 = time.time()
     inp = si.make_attention_inputs(cfg)
     gen_s = time.time() - t0
     m = measure(sc, si, torch, np, inp, theta, args.steps, args.warmup, dev)
     ms, tokens = m["ms"], m["tokens"]
     roof = m["roof"]
-    roof["traffic"] = recorded_traffic()
+    # the recorded counters belong to the seq4096 workload
+    roof["traffic"] = recorded_traffic() if args.workload == "seq4096" else None
     roof["kernel"] = "k_attn_fwd<bf16> + k_attn_cols<bf16> (the two launches of the window attention)"
     roof["kernel_us"] = round(m["kern_ms"] * 1e3, 2)
     roof["algorithmic_flop"] = m["flops"]
@@ -223,8 +238,7 @@ def main():
         "metric": METRIC, "value": round(value, 1), "unit": "kept-token-layers/s", "n_gpus": 1,
         "steps": args.steps, "warmup": args.warmup, "ms_per_step": round(ms, 4), "higher_is_better": True,
         "scaling": "weak", "vs_baseline": None, "dtype": "bf16", "data": "synthetic",
-        "config": {"workload": "single sparse-attention + LTP layer: B8 n4096 H12 d64 bf16, window 512, "
-                               "32 seeded global tokens, valid lengths U[2048,4096], threshold pruning ~50%",
+        "config": {"workload": desc,
                    "batch": cfg.B, "seq_len": cfg.n, "heads": cfg.H, "head_dim": cfg.d, "window": cfg.window,
                    "global_tokens": cfg.n_global, "valid_tokens": tokens, "threshold": theta,
                    "parallelism": "none (1 GPU)"},
@@ -242,8 +256,8 @@ def main():
         cpu_s = time.perf_counter() - c0
         result["cpu_baseline"] = {"value": round(tokens / cpu_s, 1), "unit": "kept-token-layers/s", "cores": threads,
                                   "kind": "oracle",
-                                  "sample": "the whole workload once (8 sequences, one layer: attention, scores, "
-                                            f"pruning) in double precision, {cpu_s:.2f} s"}
+                                  "sample": f"the whole workload once ({cfg.B} sequences, one layer: attention, "
+                                            f"scores, pruning) in double precision, {cpu_s:.2f} s"}
     result["input_generation_s"] = round(gen_s, 1)
     if args.copy_calibration > 0:
         nb = args.copy_calibration << 20

@@ -111,6 +111,9 @@ class AttnConfig:
     spike_amp: float = 0.0
     spike_on_q: bool = False
     alpha: float = 0.125        # softmax scale 1/sqrt(d)
+    # length distribution: () = uniform integers on len_range; ("lognormal", mu, sigma) = round(exp(N(mu,
+    # sigma^2))) clipped to len_range
+    len_dist: tuple = ()
 
 
 @dataclass
@@ -151,6 +154,10 @@ CONFIGS = {
     5: AttnConfig("bf16 three prune passes B2 n8192 H16 w1024 G64 K-spike", 4, 2, 8192, 16, 64, "bf16", 1024,
                   (8192, 8192), 64, "random", thresholds=[0.0005, 0.001, 0.002], spike_rank=4, spike_amp=3.0),
 }
+# Paper-shaped lengths: ln L ~ N(5.717, 0.738^2) puts 24 % of the sequences above 512 tokens and 95 % at or
+# below 1024, the length statistics of the paper's dataset (Sec. 5.2); a batch of 64 such sequences.
+CONFIGS[6] = AttnConfig("bf16 single layer B64 n1024 H12 w256 lognormal lengths", 5, 64, 1024, 12, 64, "bf16", 256,
+                        (1, 1024), 1, "first", thresholds=[None], len_dist=("lognormal", 5.717, 0.738))
 CONFIGS["5b"] = AttnConfig("bf16 three prune passes B2 n8192 H16 w1024 G64 QK-spike", 4, 2, 8192, 16, 64, "bf16",
                            1024, (8192, 8192), 64, "random", thresholds=[0.0005, 0.001, 0.002], spike_rank=4,
                            spike_amp=3.0, spike_on_q=True)
@@ -159,10 +166,17 @@ STACK_CONFIG = StackConfig("bf16 12-layer attention stack B16 n2048 D768 w512", 
                            (256, 2048), 1, 0.02, 0.01)
 
 
-def lengths(seed: int, B: int, lo: int, hi: int) -> np.ndarray:
+def lengths(seed: int, B: int, lo: int, hi: int, dist: tuple = ()) -> np.ndarray:
+    if dist and dist[0] == "lognormal":
+        return np.clip(np.rint(lognormal_raw(seed, B, dist[1], dist[2])), lo, hi).astype(np.int32)
     if lo == hi:
         return np.full(B, lo, dtype=np.int32)
     return randint(seed, S_LEN, B, lo, hi).astype(np.int32)
+
+
+def lognormal_raw(seed: int, B: int, mu: float, sigma: float) -> np.ndarray:
+    """exp(mu + sigma * z) for B standard normals z of the length stream (before rounding and clipping)."""
+    return np.exp(mu + sigma * normal(seed, S_LEN, B))
 
 
 def global_positions(seed: int, valid_len: np.ndarray, G: int, mode: str) -> np.ndarray:
@@ -220,7 +234,7 @@ def make_attention_inputs(cfg: AttnConfig, seed: int | None = None, B=None, n=No
         k = k + _low_rank(seed, S_SPIKE_U, S_SPIKE_V, B, n, H, d, cfg.spike_rank, cfg.spike_amp)
         if cfg.spike_on_q:
             q = q + _low_rank(seed, S_SPIKE_UQ, S_SPIKE_V, B, n, H, d, cfg.spike_rank, cfg.spike_amp)
-    vl = lengths(seed, B, lo, hi)
+    vl = lengths(seed, B, lo, hi, cfg.len_dist)
     gp = global_positions(seed, vl, G, cfg.global_mode)
     out = dict(B=B, n=n, H=H, d=d, window=window, G=G, dtype=dtype, alpha=cfg.alpha, valid_len=vl, global_pos=gp)
     for name, x in (("q", q), ("k", k), ("v", v)):

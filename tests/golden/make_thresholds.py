@@ -21,7 +21,7 @@ sys.path.insert(0, ROOT)
 import oracle  # noqa: E402
 import sc_inputs as si  # noqa: E402
 
-TARGET_PRUNED = {2: 0.30, 4: 0.50}
+TARGET_PRUNED = {2: 0.30, 4: 0.50, 6: 0.30}
 
 
 def gap_threshold(scores32, valid_len, global_pos, frac):

@@ -104,7 +104,7 @@ def config_run(cid):
     return _CACHE[cid]
 
 
-@pytest.mark.parametrize("cid", [1, 2, 4])
+@pytest.mark.parametrize("cid", [1, 2, 4, 6])
 def test_config_attention_and_scores(cid):
     inp, (ro, rl, rs), g = config_run(cid)
     err = check_out(g["out"], ro, inp["dtype"])
@@ -113,7 +113,7 @@ def test_config_attention_and_scores(cid):
     log(f"config {cid}: max |dO| {err:.3g}, worst score rel err {worst:.3g}")
 
 
-@pytest.mark.parametrize("cid", [1, 2, 4])
+@pytest.mark.parametrize("cid", [1, 2, 4, 6])
 def test_config_prune_compact(cid):
     inp, (ro, rl, rs), g = config_run(cid)
     cfg = si.CONFIGS[cid]
