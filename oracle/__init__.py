@@ -46,12 +46,13 @@ def lib():
         L.orc_sparse_attention.argtypes = [ci, ci, ci, ci, ci, ci, i32p, i32p, cd, f64p, f64p, f64p, f64p, f64p,
                                            f64p, f64p, ci]
         L.orc_ltp_prune.argtypes = [ci, ci, ci, i32p, i32p, f32p, cf, ci, i32p, i32p, i32p, i32p, i32p]
+        L.orc_topk_prune.argtypes = [ci, ci, ci, i32p, i32p, f32p, cf, ci, i32p, i32p, i32p, i32p, i32p]
         L.orc_gather_rows.argtypes = [ci, ci, cl, vp, vp, i32p, i32p]
         L.orc_encoder_layer.argtypes = [ci, ci, ci, ci, ci, ci, i32p, i32p, cd, f64p, f64p, f64p, cf, ci, cd, f64p,
                                         i32p, i32p, i32p, f32p, ci]
         L.orc_encoder_stack.argtypes = [ci, ci, ci, ci, ci, ci, i32p, i32p, cd, ci, f64p, f64p, f64p, f32p, ci, cd,
                                         f64p, i32p, i32p, i32p, ci]
-        for f in ("orc_sparse_attention", "orc_ltp_prune", "orc_gather_rows", "orc_encoder_layer",
+        for f in ("orc_sparse_attention", "orc_ltp_prune", "orc_topk_prune", "orc_gather_rows", "orc_encoder_layer",
                   "orc_encoder_stack"):
             getattr(L, f).restype = ci
         _lib = L
@@ -106,6 +107,15 @@ def sparse_attention(q, k, v, valid_len, global_pos, window, alpha, want_colsum=
 
 def ltp_prune(scores32, valid_len, global_pos, threshold, keep_global=1, orig_in=None):
     """scores32: [B, n] float32.  Returns (keep_idx, new_len, new_global_pos, orig_out)."""
+    return _prune(lib().orc_ltp_prune, scores32, valid_len, global_pos, threshold, keep_global, orig_in)
+
+
+def topk_prune(scores32, valid_len, global_pos, keep_ratio, keep_global=1, orig_in=None):
+    """Rank rule: keep ceil(keep_ratio * C) of the C candidates per sequence.  Returns as ltp_prune."""
+    return _prune(lib().orc_topk_prune, scores32, valid_len, global_pos, keep_ratio, keep_global, orig_in)
+
+
+def _prune(fn, scores32, valid_len, global_pos, value, keep_global, orig_in):
     s = np.ascontiguousarray(scores32, dtype=np.float32)
     B, n = s.shape
     gp = _i32(global_pos).reshape(B, -1)
@@ -116,10 +126,9 @@ def ltp_prune(scores32, valid_len, global_pos, threshold, keep_global=1, orig_in
     ngp = np.empty((B, G), np.int32)
     orig_out = np.empty((B, n), np.int32)
     oi = None if orig_in is None else _i32(orig_in)
-    rc = lib().orc_ltp_prune(B, n, G, _p(gp, ctypes.c_int32), _p(vl, ctypes.c_int32), _p(s, ctypes.c_float),
-                             np.float32(threshold).item(), int(keep_global), _p(keep_idx, ctypes.c_int32),
-                             _p(new_len, ctypes.c_int32), _p(ngp, ctypes.c_int32), _p(oi, ctypes.c_int32),
-                             _p(orig_out, ctypes.c_int32))
+    rc = fn(B, n, G, _p(gp, ctypes.c_int32), _p(vl, ctypes.c_int32), _p(s, ctypes.c_float), np.float32(value).item(),
+            int(keep_global), _p(keep_idx, ctypes.c_int32), _p(new_len, ctypes.c_int32), _p(ngp, ctypes.c_int32),
+            _p(oi, ctypes.c_int32), _p(orig_out, ctypes.c_int32))
     assert rc == 0
     return keep_idx, new_len, ngp, orig_out
 

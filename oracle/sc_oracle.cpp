@@ -19,6 +19,9 @@
 //   * binarised mask: keep iff score > layer threshold, strictly (Sec. 4.2.2,
 //     the display equation of step 2); hard pruning removes masked tokens
 //     (Sec. 4.2.2 step 3) and later layers see the shorter sequence (Sec. 4.2).
+//   * top-k pruning (a rank rule in place of the threshold; not the paper's
+//     rule, a variant from the token-pruning family of its Sec. 2): the
+//     ceil(keep_ratio * C) best-scored candidates per sequence are kept.
 // Where the paper is silent the readings are: half-width r = floor(w/2) with
 // |i - j| <= r inclusive; the softmax scale is an argument; prefix padding
 // (tokens >= valid length are neither queries nor keys); scores divided by
@@ -161,6 +164,37 @@ int orc_sparse_attention(int B, int n, int H, int d, int window, int G, const in
   return 0;
 }
 
+// Compaction of sequence b from its keep flags: kept tokens in ascending order
+// (keep_idx, new_len), surviving global tokens renumbered (new_global_pos),
+// original positions composed (orig_out).
+static void compact_sequence(int b, int n, int L, int G, const int32_t* global_pos, const std::vector<char>& keep,
+                             int32_t* keep_idx, int32_t* new_len, int32_t* new_global_pos, const int32_t* orig_in,
+                             int32_t* orig_out) {
+  std::vector<int> new_index(n, -1);
+  int cnt = 0;
+  for (int k = 0; k < n; ++k) {
+    if (k < L && keep[k]) {
+      new_index[k] = cnt;
+      keep_idx[(long)b * n + cnt] = k;
+      ++cnt;
+    }
+  }
+  for (int j = cnt; j < n; ++j) keep_idx[(long)b * n + j] = -1;
+  new_len[b] = cnt;
+  int gc = 0;
+  for (int j = 0; j < G; ++j) {
+    int p = global_pos[(long)b * G + j];
+    if (p >= 0 && p < L && new_index[p] >= 0) new_global_pos[(long)b * G + gc++] = new_index[p];
+  }
+  for (int j = gc; j < G; ++j) new_global_pos[(long)b * G + j] = -1;
+  if (orig_out) {
+    for (int j = 0; j < n; ++j) {
+      int src = keep_idx[(long)b * n + j];
+      orig_out[(long)b * n + j] = src < 0 ? -1 : (orig_in ? orig_in[(long)b * n + src] : src);
+    }
+  }
+}
+
 // Binarised mask and hard pruning of one layer.  The decision is taken on the
 // float32 score against the float32 threshold: keep iff k < L and (s > theta
 // or (keep_global and k is global)).  Kept tokens keep their relative order.
@@ -175,30 +209,44 @@ int orc_ltp_prune(int B, int n, int G, const int32_t* global_pos, const int32_t*
   for (int b = 0; b < B; ++b) {
     int L = std::min(std::max(valid_len[b], 0), n);
     std::vector<char> g = global_flags(n, L, G, global_pos + (long)b * G);
-    std::vector<int> new_index(n, -1);
-    int cnt = 0;
-    for (int k = 0; k < n; ++k) {
-      bool keep = k < L && (scores[(long)b * n + k] > threshold || (keep_global && g[k]));
-      if (keep) {
-        new_index[k] = cnt;
-        keep_idx[(long)b * n + cnt] = k;
-        ++cnt;
-      }
+    std::vector<char> keep(n, 0);
+    for (int k = 0; k < L; ++k) keep[k] = scores[(long)b * n + k] > threshold || (keep_global && g[k]);
+    compact_sequence(b, n, L, G, global_pos, keep, keep_idx, new_len, new_global_pos, orig_in, orig_out);
+  }
+  return 0;
+}
+
+// Top-k pruning: the same compaction with a rank rule instead of the
+// threshold (the paper's Sec. 2 places LTP among token-pruning methods, some
+// of which keep a fixed fraction of the tokens by rank).  Per sequence the
+// candidates are the valid tokens, except the global ones when keep_global is
+// set (those are kept anyway); of C candidates the K = ceil(keep_ratio * C)
+// (in double, clamped to [0, C]) with the largest float32 scores are kept,
+// equal scores going to the lower index.
+int orc_topk_prune(int B, int n, int G, const int32_t* global_pos, const int32_t* valid_len, const float* scores,
+                   float keep_ratio, int keep_global, int32_t* keep_idx, int32_t* new_len, int32_t* new_global_pos,
+                   const int32_t* orig_in, int32_t* orig_out) {
+  if (B < 0 || n < 0 || G < 0) return -1;
+  for (int b = 0; b < B; ++b) {
+    int L = std::min(std::max(valid_len[b], 0), n);
+    std::vector<char> g = global_flags(n, L, G, global_pos + (long)b * G);
+    std::vector<char> keep(n, 0);
+    std::vector<int> cand;
+    for (int k = 0; k < L; ++k) {
+      if (keep_global && g[k])
+        keep[k] = 1;
+      else
+        cand.push_back(k);
     }
-    for (int j = cnt; j < n; ++j) keep_idx[(long)b * n + j] = -1;
-    new_len[b] = cnt;
-    int gc = 0;
-    for (int j = 0; j < G; ++j) {
-      int p = global_pos[(long)b * G + j];
-      if (p >= 0 && p < L && new_index[p] >= 0) new_global_pos[(long)b * G + gc++] = new_index[p];
-    }
-    for (int j = gc; j < G; ++j) new_global_pos[(long)b * G + j] = -1;
-    if (orig_out) {
-      for (int j = 0; j < n; ++j) {
-        int src = keep_idx[(long)b * n + j];
-        orig_out[(long)b * n + j] = src < 0 ? -1 : (orig_in ? orig_in[(long)b * n + src] : src);
-      }
-    }
+    const long C = (long)cand.size();
+    const double prod = (double)keep_ratio * (double)C;
+    const long K = prod <= 0.0 ? 0 : (prod >= (double)C ? C : (long)std::ceil(prod));
+    // candidates are in index order; a stable sort by descending score keeps
+    // that order among equal scores
+    const float* s = scores + (long)b * n;
+    std::stable_sort(cand.begin(), cand.end(), [&](int x, int y) { return s[x] > s[y]; });
+    for (long i = 0; i < K; ++i) keep[cand[i]] = 1;
+    compact_sequence(b, n, L, G, global_pos, keep, keep_idx, new_len, new_global_pos, orig_in, orig_out);
   }
   return 0;
 }

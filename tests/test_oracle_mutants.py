@@ -37,6 +37,10 @@ MUTANTS = [
     ("residual dropped", "t[c] = x[src * D + c];", "t[c] = 0.0;"),
     ("unbiased variance", "var /= (double)D;", "var /= (double)(D - 1);"),
     ("value of the query used", "const double* vj = v + (long)nbr[t] * ld;", "const double* vj = v + (long)i * ld;"),
+    ("top-k ties to the higher index", "std::stable_sort(cand.begin()",
+     "std::reverse(cand.begin(), cand.end());\n    std::stable_sort(cand.begin()"),
+    ("top-k count rounded down", "(long)std::ceil(prod)", "(long)std::floor(prod)"),
+    ("top-k counts kept globals as candidates", "      else\n        cand.push_back(k);", "      cand.push_back(k);"),
 ]
 
 

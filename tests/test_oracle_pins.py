@@ -273,6 +273,75 @@ def check_prune_brute_force():
             assert list(oo[b, :nl[b]]) == orig and np.all(oo[b, nl[b]:] == -1)
 
 
+def _topk_inputs(rng, B=4, n=60, G=3, levels=None):
+    """Scores (optionally quantised to a few levels, so that ties are common), lengths, global positions."""
+    s = rng.random((B, n)).astype(np.float32) * 0.05
+    if levels:
+        s = (np.floor(s / 0.05 * levels) / levels * 0.05).astype(np.float32)
+    vl = rng.integers(0, n + 1, B).astype(np.int32)
+    gp = np.full((B, G), -1, np.int32)
+    for b in range(B):
+        g = rng.choice(max(vl[b], 1), size=min(G, vl[b]), replace=False) if vl[b] else []
+        gp[b, :len(g)] = np.sort(g)
+    return s, vl, gp
+
+
+def check_topk_rank_invariants():
+    """Kept candidates: exactly ceil(ratio * C) of them; no dropped candidate scores above a kept one; at the
+    boundary score the kept ones precede the dropped ones; globals kept; survivors in order."""
+    rng = np.random.default_rng(11)
+    for trial in range(40):
+        s, vl, gp = _topk_inputs(rng, levels=(4 if trial % 2 else None))
+        ratio = float(rng.choice([0.0, 0.1, 0.25, 0.5, 0.77, 1.0]))
+        kg = int(trial % 3 != 0)
+        ki, nl, ngp, _ = oracle.topk_prune(s, vl, gp, ratio, kg)
+        for b in range(s.shape[0]):
+            L = int(vl[b])
+            g = set(int(p) for p in gp[b] if 0 <= p < L)
+            kept = ki[b, :nl[b]].tolist()
+            assert kept == sorted(set(kept)) and all(0 <= k < L for k in kept)
+            cand = [k for k in range(L) if not (kg and k in g)]
+            K = math.ceil(np.float64(np.float32(ratio)) * len(cand)) if ratio > 0 else 0
+            kc = [k for k in kept if k in cand]
+            dropped = [k for k in cand if k not in set(kc)]
+            assert len(kc) == min(K, len(cand))
+            if kg:
+                assert g <= set(kept)
+            if kc and dropped:
+                lo = min(s[b, k] for k in kc)
+                assert max(s[b, k] for k in dropped) <= lo
+                tie_kept = [k for k in kc if s[b, k] == lo]
+                tie_dropped = [k for k in dropped if s[b, k] == lo]
+                if tie_dropped:
+                    assert max(tie_kept) < min(tie_dropped)
+
+
+def check_topk_equals_threshold_rule():
+    """When the cut falls in a gap of the scores, top-k keeps exactly what the (separately pinned) threshold
+    rule keeps with a threshold inside that gap; ratio 1 keeps every valid token, ratio 0 only the globals."""
+    rng = np.random.default_rng(12)
+    for trial in range(30):
+        s, vl, gp = _topk_inputs(rng, B=1)
+        L = int(vl[0])
+        g = set(int(p) for p in gp[0] if 0 <= p < L)
+        cand = sorted((float(s[0, k]) for k in range(L) if k not in g), reverse=True)
+        if len(cand) >= 2:
+            K = int(rng.integers(1, len(cand)))
+            if cand[K - 1] > cand[K]:
+                theta = float(np.float32((cand[K - 1] + cand[K]) / 2))
+                ratio = (K - 0.5) / len(cand)
+                a = oracle.topk_prune(s, vl, gp, ratio, 1)
+                t = oracle.ltp_prune(s, vl, gp, theta, 1)
+                for x, y in zip(a, t):
+                    assert np.array_equal(x, y)
+        ki, nl, _, _ = oracle.topk_prune(s, vl, gp, 1.0, 1)
+        assert nl[0] == L and list(ki[0, :L]) == list(range(L))
+        ki, nl, _, _ = oracle.topk_prune(s, vl, gp, 0.0, 1)
+        assert list(ki[0, :nl[0]]) == sorted(g)
+        ki, nl, _, _ = oracle.topk_prune(s, vl, gp, 0.0, 0)
+        assert nl[0] == 0
+
+
 def check_prune_invariants():
     q, k, v, vl, gp, w = rand_case(400, n=64, B=3)
     _, _, s = run(q, k, v, vl, gp, w)
@@ -422,7 +491,8 @@ ATTENTION_CHECKS = [check_brute_force, check_window_covers_sequence_is_dense, ch
                     check_zero_window_no_global, check_constant_values, check_zero_queries_rational_scores,
                     check_score_invariants, check_reflection_symmetry, check_head_permutation,
                     check_sec55_example_structure, check_padding_is_invisible]
-PRUNE_CHECKS = [check_prune_brute_force, check_prune_invariants, check_mask_rule_golden, check_gather_rows]
+PRUNE_CHECKS = [check_prune_brute_force, check_prune_invariants, check_mask_rule_golden, check_gather_rows,
+                check_topk_rank_invariants, check_topk_equals_threshold_rule]
 STACK_CHECKS = [check_bf16_rounding, check_encoder_layer_against_libraries, check_layernorm_statistics,
                 check_stack_composition]
 ALL_CHECKS = ATTENTION_CHECKS + PRUNE_CHECKS + STACK_CHECKS + [check_paper_threshold_schedule]
