@@ -96,10 +96,11 @@ def roofline(flops, bytes_, kern_ms):
     return roof
 
 
-def measure(sc, si, torch, np, inp, theta, steps, warmup, dev="cuda:0"):
+def measure(sc, si, torch, np, inp, theta, steps, warmup, dev="cuda:0", keep_ratio=None):
     """Times `steps` steps (window attention with score partials, scores, prune + compaction of O) after
     `warmup` untimed ones.  theta None picks the median score of the valid non-global tokens (about half
-    pruned), from one untimed step."""
+    pruned), from one untimed step.  keep_ratio: prune by the top-k rule (sc_topk_prune_compact) instead of
+    the threshold."""
     B, n, H, dd, G = inp["B"], inp["n"], inp["H"], inp["d"], inp["G"]
 
     def i32(a):
@@ -121,7 +122,7 @@ def measure(sc, si, torch, np, inp, theta, steps, warmup, dev="cuda:0"):
                 new_global_pos=torch.empty((B, max(G, 1)), dtype=torch.int32, device=dev),
                 orig_idx_out=torch.empty((B, n), dtype=torch.int32, device=dev))
     ws_prune = torch.empty(sc.sc_ltp_prune_compact_workspace_size(d), dtype=torch.uint8, device=dev)
-    if theta is None:
+    if theta is None and keep_ratio is None:
         sc.sc_window_attention(d, q, k, v, out=out, lse=lse, score_partials=sp, workspace=ws_attn)
         sc.sc_ltp_score(d, sp, scores=scores)
         sv = scores.cpu().numpy()
@@ -135,7 +136,10 @@ def measure(sc, si, torch, np, inp, theta, steps, warmup, dev="cuda:0"):
     def step():
         sc.sc_window_attention(d, q, k, v, out=out, lse=lse, score_partials=sp, workspace=ws_attn)
         sc.sc_ltp_score(d, sp, scores=scores)
-        sc.sc_ltp_prune_compact(d, scores, theta, True, [out], dsts=[oc], outs=outs, workspace=ws_prune)
+        if keep_ratio is None:
+            sc.sc_ltp_prune_compact(d, scores, theta, True, [out], dsts=[oc], outs=outs, workspace=ws_prune)
+        else:
+            sc.sc_topk_prune_compact(d, scores, keep_ratio, True, [out], dsts=[oc], outs=outs, workspace=ws_prune)
 
     for _ in range(warmup):
         step()
@@ -196,6 +200,9 @@ def main():
     ap.add_argument("--workload", choices=sorted(WORKLOADS), default="seq4096",
                     help="seq4096: B8 n4096 window 512, 32 global tokens (the headline line); lognormal: B64 n1024 "
                          "window 256, one global token, paper-shaped lognormal lengths")
+    ap.add_argument("--prune", choices=("threshold", "topk"), default="threshold",
+                    help="pruning rule of the step: the layer threshold (the paper's rule) or top-k by keep ratio")
+    ap.add_argument("--keep-ratio", type=float, default=0.5, help="top-k rule: fraction of candidates kept")
     ap.add_argument("--sweep", action="store_true",
                     help="instead of the single measurement, sweep the window (n 4096) and the length (window "
                          "512), one JSON line per point")
@@ -223,7 +230,8 @@ def main():
     t0 = time.time()
     inp = si.make_attention_inputs(cfg)
     gen_s = time.time() - t0
-    m = measure(sc, si, torch, np, inp, theta, args.steps, args.warmup, dev)
+    keep_ratio = args.keep_ratio if args.prune == "topk" else None
+    m = measure(sc, si, torch, np, inp, theta, args.steps, args.warmup, dev, keep_ratio=keep_ratio)
     ms, tokens = m["ms"], m["tokens"]
     roof = m["roof"]
     # the recorded counters belong to the seq4096 workload
@@ -240,7 +248,9 @@ def main():
         "scaling": "weak", "vs_baseline": None, "dtype": "bf16", "data": "synthetic",
         "config": {"workload": desc,
                    "batch": cfg.B, "seq_len": cfg.n, "heads": cfg.H, "head_dim": cfg.d, "window": cfg.window,
-                   "global_tokens": cfg.n_global, "valid_tokens": tokens, "threshold": theta,
+                   "global_tokens": cfg.n_global, "valid_tokens": tokens,
+                   "pruning": (f"top-k, keep ratio {keep_ratio}" if keep_ratio is not None else
+                               f"threshold {theta}"),
                    "parallelism": "none (1 GPU)"},
         "roofline": roof,
         "kept_per_sequence": m["kept"],
@@ -252,7 +262,10 @@ def main():
         c0 = time.perf_counter()
         _, _, rs = oracle.sparse_attention(inp["q64"], inp["k64"], inp["v64"], inp["valid_len"], inp["global_pos"],
                                            cfg.window, cfg.alpha, nthreads=threads)
-        oracle.ltp_prune(rs.astype(np.float32), inp["valid_len"], inp["global_pos"], theta, 1)
+        if keep_ratio is None:
+            oracle.ltp_prune(rs.astype(np.float32), inp["valid_len"], inp["global_pos"], theta, 1)
+        else:
+            oracle.topk_prune(rs.astype(np.float32), inp["valid_len"], inp["global_pos"], keep_ratio, 1)
         cpu_s = time.perf_counter() - c0
         result["cpu_baseline"] = {"value": round(tokens / cpu_s, 1), "unit": "kept-token-layers/s", "cores": threads,
                                   "kind": "oracle",

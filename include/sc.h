@@ -19,6 +19,9 @@
  *                         Sec. 4.2.2 step 2) and hard pruning: surviving tokens
  *                         are compacted into a shorter sequence (Sec. 4.2.2
  *                         step 3) for the next layer;
+ *   sc_topk_prune_compact the same compaction with a top-k rule instead of the
+ *                         threshold (a variant in the family of cascade token
+ *                         pruning the paper cites in Sec. 2);
  *   sc_encoder_attn_stack the attention-only encoder stack (QKV projection,
  *                         the three steps above, output projection, residual
  *                         and LayerNorm) over several layers, each layer on the
@@ -181,6 +184,26 @@ sc_status sc_ltp_prune_compact(const sc_attn_desc *desc, const float *scores, fl
                                int32_t *keep_idx, int32_t *new_len, int32_t *new_global_pos,
                                const int32_t *orig_idx_in, int32_t *orig_idx_out, void *workspace, size_t ws_bytes,
                                void *stream);
+
+/*
+ * Top-k pruning, an alternative selection rule to the threshold above (the
+ * paper's Sec. 2 places LTP among token-pruning methods, some of which keep a
+ * fixed fraction of the tokens by rank).  Per sequence b, the candidates are the
+ * valid tokens k < L_b, except the global ones when keep_global is set (those
+ * are always kept); with C_b candidates,
+ *   K_b = ceil(keep_ratio * C_b)   (computed in double; 0 <= K_b <= C_b)
+ * candidates are kept: those with the K_b largest scores, where equal scores
+ * (compared in float32) go to the lower index.  Survivors keep their order.
+ *   keep_ratio      in [0, 1] (else SC_EINVAL; NaN included).
+ * Every other argument, output, overlap rule, error and the workspace (same
+ * size as sc_ltp_prune_compact_workspace_size) are as for
+ * sc_ltp_prune_compact.
+ */
+sc_status sc_topk_prune_compact(const sc_attn_desc *desc, const float *scores, float keep_ratio, int32_t keep_global,
+                                int32_t n_tensors, const void *const *src, void *const *dst, const int64_t *row_bytes,
+                                int32_t *keep_idx, int32_t *new_len, int32_t *new_global_pos,
+                                const int32_t *orig_idx_in, int32_t *orig_idx_out, void *workspace, size_t ws_bytes,
+                                void *stream);
 
 size_t sc_encoder_attn_stack_workspace_size(const sc_attn_desc *desc, int32_t n_layers);
 

@@ -50,6 +50,7 @@ def load():
         "sc_ltp_score": (i32, [dp, i32, vp, vp, vp, sz, vp]),
         "sc_ltp_prune_compact_workspace_size": (sz, [dp]),
         "sc_ltp_prune_compact": (i32, [dp, vp, f32, i32, i32, vp, vp, vp, vp, vp, vp, vp, vp, vp, sz, vp]),
+        "sc_topk_prune_compact": (i32, [dp, vp, f32, i32, i32, vp, vp, vp, vp, vp, vp, vp, vp, vp, sz, vp]),
         "sc_encoder_attn_stack_workspace_size": (sz, [dp, i32]),
         "sc_encoder_attn_stack": (i32, [dp, i32, vp, vp, vp, vp, i32, f32, vp, vp, vp, vp, vp, sz, vp]),
         "sc_profile_window_kernel": (i32, [i32]),
@@ -177,9 +178,22 @@ def sc_ltp_prune_compact_workspace_size(desc: Desc) -> int:
 
 def sc_ltp_prune_compact(desc: Desc, scores, threshold, keep_global=True, tensors=(), dsts=None, orig_idx_in=None,
                          want_orig=True, outs=None, workspace=None, stream=None):
-    """Returns (keep_idx, new_len, new_global_pos, orig_idx_out, dsts).
+    """Threshold rule.  Returns (keep_idx, new_len, new_global_pos, orig_idx_out, dsts).
 
     outs: optional dict of preallocated keep_idx / new_len / new_global_pos / orig_idx_out."""
+    return _prune_compact("sc_ltp_prune_compact", desc, scores, threshold, keep_global, tensors, dsts, orig_idx_in,
+                          want_orig, outs, workspace, stream)
+
+
+def sc_topk_prune_compact(desc: Desc, scores, keep_ratio, keep_global=True, tensors=(), dsts=None, orig_idx_in=None,
+                          want_orig=True, outs=None, workspace=None, stream=None):
+    """Top-k rule (keep ceil(keep_ratio * candidates) per sequence); same returns as sc_ltp_prune_compact."""
+    return _prune_compact("sc_topk_prune_compact", desc, scores, keep_ratio, keep_global, tensors, dsts, orig_idx_in,
+                          want_orig, outs, workspace, stream)
+
+
+def _prune_compact(fn, desc, scores, value, keep_global, tensors, dsts, orig_idx_in, want_orig, outs, workspace,
+                   stream):
     import torch
     L = load()
     cd = desc.c()
@@ -202,10 +216,9 @@ def sc_ltp_prune_compact(desc: Desc, scores, threshold, keep_global=True, tensor
     wsb = L.sc_ltp_prune_compact_workspace_size(ctypes.byref(cd))
     ws = _ws(wsb, dev) if workspace is None else workspace
     wsb = wsb if workspace is None else workspace.numel() * workspace.element_size()
-    _check(L.sc_ltp_prune_compact(ctypes.byref(cd), _ptr(scores), ctypes.c_float(threshold), int(bool(keep_global)),
-                                  nt, src_arr, dst_arr, rb_arr, _ptr(keep_idx), _ptr(new_len), _ptr(ngp),
-                                  _ptr(orig_idx_in), _ptr(orig_out), _ptr(ws), wsb, _stream(stream)),
-           "sc_ltp_prune_compact")
+    _check(getattr(L, fn)(ctypes.byref(cd), _ptr(scores), ctypes.c_float(value), int(bool(keep_global)), nt, src_arr,
+                          dst_arr, rb_arr, _ptr(keep_idx), _ptr(new_len), _ptr(ngp), _ptr(orig_idx_in),
+                          _ptr(orig_out), _ptr(ws), wsb, _stream(stream)), fn)
     return keep_idx, new_len, ngp, orig_out, dsts
 
 

@@ -213,11 +213,14 @@ size_t sc_ltp_prune_compact_workspace_size(const sc_attn_desc* d) {
   return sizeof(int32_t) * (size_t)d->B * d->n;
 }
 
-sc_status sc_ltp_prune_compact(const sc_attn_desc* d, const float* scores, float threshold, int32_t keep_global,
-                               int32_t n_tensors, const void* const* src, void* const* dst, const int64_t* row_bytes,
-                               int32_t* keep_idx, int32_t* new_len, int32_t* new_global_pos,
-                               const int32_t* orig_idx_in, int32_t* orig_idx_out, void* workspace, size_t ws_bytes,
-                               void* stream) {
+namespace {
+
+// Threshold (topk = 0) or top-k (topk = 1) selection, then the gather.
+sc_status prune_compact(const sc_attn_desc* d, const float* scores, float threshold, int topk, float keep_ratio,
+                        int32_t keep_global, int32_t n_tensors, const void* const* src, void* const* dst,
+                        const int64_t* row_bytes, int32_t* keep_idx, int32_t* new_len, int32_t* new_global_pos,
+                        const int32_t* orig_idx_in, int32_t* orig_idx_out, void* workspace, size_t ws_bytes,
+                        void* stream) {
   sc_status st = check_desc(d);
   if (st != SC_OK) return st;
   if (!scores || !keep_idx || !new_len) return SC_EINVAL;
@@ -253,6 +256,8 @@ sc_status sc_ltp_prune_compact(const sc_attn_desc* d, const float* scores, float
   p.G = d->G;
   p.threshold = threshold;
   p.keep_global = keep_global ? 1 : 0;
+  p.topk = topk;
+  p.keep_ratio = keep_ratio;
   p.keep_idx = keep_idx;
   p.new_len = new_len;
   p.new_gpos = new_global_pos;
@@ -264,6 +269,27 @@ sc_status sc_ltp_prune_compact(const sc_attn_desc* d, const float* scores, float
   ga.keep_idx = keep_idx;
   ga.new_len = new_len;
   return sc::launch_gather(ga, s) == hipSuccess ? SC_OK : SC_EHIP;
+}
+
+}  // namespace
+
+sc_status sc_ltp_prune_compact(const sc_attn_desc* d, const float* scores, float threshold, int32_t keep_global,
+                               int32_t n_tensors, const void* const* src, void* const* dst, const int64_t* row_bytes,
+                               int32_t* keep_idx, int32_t* new_len, int32_t* new_global_pos,
+                               const int32_t* orig_idx_in, int32_t* orig_idx_out, void* workspace, size_t ws_bytes,
+                               void* stream) {
+  return prune_compact(d, scores, threshold, 0, 0.f, keep_global, n_tensors, src, dst, row_bytes, keep_idx, new_len,
+                       new_global_pos, orig_idx_in, orig_idx_out, workspace, ws_bytes, stream);
+}
+
+sc_status sc_topk_prune_compact(const sc_attn_desc* d, const float* scores, float keep_ratio, int32_t keep_global,
+                                int32_t n_tensors, const void* const* src, void* const* dst, const int64_t* row_bytes,
+                                int32_t* keep_idx, int32_t* new_len, int32_t* new_global_pos,
+                                const int32_t* orig_idx_in, int32_t* orig_idx_out, void* workspace, size_t ws_bytes,
+                                void* stream) {
+  if (!(keep_ratio >= 0.f && keep_ratio <= 1.f)) return SC_EINVAL;  // also rejects NaN
+  return prune_compact(d, scores, 0.f, 1, keep_ratio, keep_global, n_tensors, src, dst, row_bytes, keep_idx, new_len,
+                       new_global_pos, orig_idx_in, orig_idx_out, workspace, ws_bytes, stream);
 }
 
 // ------------------------------------------------------------------ stack --
@@ -374,6 +400,8 @@ sc_status sc_encoder_attn_stack(const sc_attn_desc* d, int32_t n_layers, const v
     p.G = G;
     p.threshold = thresholds[l];
     p.keep_global = keep_global ? 1 : 0;
+    p.topk = 0;
+    p.keep_ratio = 0.f;
     p.keep_idx = w.keep_idx;
     p.new_len = len_nxt;
     p.new_gpos = G > 0 ? gp_nxt : nullptr;

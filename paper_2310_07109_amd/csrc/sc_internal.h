@@ -68,6 +68,8 @@ struct PruneArgs {
   int B, n, G;
   float threshold;
   int keep_global;
+  int topk;                // 0: threshold rule; 1: keep the ceil(keep_ratio * C) best candidates per sequence
+  float keep_ratio;
   int* keep_idx;           // [B, n]
   int* new_len;            // [B]
   int* new_gpos;           // [B, G] or null

@@ -8,6 +8,15 @@
 //                token its rank inside its wave, an LDS scan of the 16 wave
 //                totals gives the wave offsets, and a running carry links the
 //                chunks.  Exact and deterministic (integer work only).
+//                Top-k rule (an alternative to the threshold, in the family
+//                of SpAtten's cascade token pruning cited in Sec. 2): each
+//                sequence keeps its ceil(keep_ratio * C) highest-scored
+//                candidates (C = valid tokens, less the global ones when those
+//                are kept anyway); equal scores go to the lower index.  The
+//                K-th largest score is found exactly by a radix select on the
+//                order-preserving 32-bit image of the float (four 8-bit digits,
+//                an LDS histogram and a 256-bin suffix scan per digit); tied
+//                scores are ranked in index order by the same block scan.
 // k_gather_rows  one wavefront per output row copies the kept input row with
 //                16-byte lanes (coalesced), for up to four tensors at once.
 #include "sc_device.h"
@@ -18,6 +27,7 @@ namespace {
 
 constexpr int kScanThreads = 1024;
 constexpr int kScanWaves = kScanThreads / 64;
+
 
 // Exclusive rank of this lane among the lanes of its wave whose flag is set,
 // and the wave's total.
@@ -53,8 +63,37 @@ SC_DEV int block_rank(bool flag, int* s_wave, int& total) {
   return off;
 }
 
+// Order-preserving image of a float score (ascending keys = ascending
+// values; -0 maps to +0 so that equal scores have equal keys).
+SC_DEV uint32_t score_key(float f) {
+  uint32_t u = __float_as_uint(f);
+  if (u == 0x80000000u) u = 0u;
+  return (u & 0x80000000u) ? ~u : (u | 0x80000000u);
+}
+
+// Inclusive prefix sum over threads 0..255 of v (threads 256+ pass 0 and get
+// a meaningless result).  Contains barriers; all threads must call it.
+SC_DEV int scan256(int v, int* s_tmp) {
+  const int w = threadIdx.x >> 6, lane = threadIdx.x & 63;
+  int incl = v;
+#pragma unroll
+  for (int off = 1; off < 64; off <<= 1) {
+    const int u = __shfl_up(incl, off, 64);
+    if (lane >= off) incl += u;
+  }
+  if (lane == 63 && w < 4) s_tmp[w] = incl;
+  __syncthreads();
+  int add = 0;
+  for (int j = 0; j < w && j < 4; ++j) add += s_tmp[j];
+  __syncthreads();  // s_tmp is reused by the next call
+  return incl + add;
+}
+
 __global__ __launch_bounds__(kScanThreads) void k_prune_scan(PruneArgs p) {
   __shared__ int s_wave[2 * kScanWaves + 1];
+  __shared__ int s_hist[256];
+  __shared__ int s_sel[2];
+  __shared__ int s_tmp[4];
   extern __shared__ uint32_t s_gbits[];  // global-token bitmask over [0, n)
   const int b = blockIdx.x, tid = threadIdx.x, n = p.n;
   const int L = clampi(p.valid_len[b], 0, n);
@@ -69,17 +108,73 @@ __global__ __launch_bounds__(kScanThreads) void k_prune_scan(PruneArgs p) {
     }
   __syncthreads();
   const float* s = p.scores + (long long)b * n;
+  auto is_glob = [&](int k) { return (bool)((s_gbits[k >> 5] >> (k & 31)) & 1u); };
+  // top-k: candidates, their count C, K = ceil(keep_ratio * C), the K-th
+  // largest key T and the number `want` of candidates with key T to keep.
+  // Key 0 marks a non-candidate (no float maps to it but a negative NaN).
+  auto cand_key = [&](int k) -> uint32_t {
+    return (k < L && !(p.keep_global && is_glob(k))) ? score_key(s[k]) : 0u;
+  };
+  uint32_t T = 0u;
+  int want = 0;
+  bool none = true;  // no candidate is kept by rank
+  if (p.topk) {
+    if (tid == 0) s_sel[0] = 0;
+    __syncthreads();
+    int cnt = 0;
+    for (int k = tid; k < L; k += kScanThreads) cnt += cand_key(k) != 0u;
+    // candidate count: per-wave sums, one LDS atomic per wave
+#pragma unroll
+    for (int off = 32; off > 0; off >>= 1) cnt += __shfl_xor(cnt, off, 64);
+    if ((tid & 63) == 0) atomicAdd(&s_sel[0], cnt);
+    __syncthreads();
+    const int C = s_sel[0];
+    __syncthreads();
+    const double prod = (double)p.keep_ratio * (double)C;
+    const int K = prod <= 0.0 ? 0 : (prod >= (double)C ? C : (int)ceil(prod));
+    none = K == 0;
+    want = K;
+    for (int shift = 24; shift >= 0 && !none; shift -= 8) {
+      if (tid < 256) s_hist[tid] = 0;
+      __syncthreads();
+      const uint32_t hmask = shift == 24 ? 0u : ~0u << (shift + 8);
+      for (int k = tid; k < L; k += kScanThreads) {
+        const uint32_t key = cand_key(k);
+        if (key != 0u && (key & hmask) == (T & hmask)) atomicAdd(&s_hist[(key >> shift) & 255u], 1);
+      }
+      __syncthreads();
+      // bins from the top: the digit whose bin holds the want-th largest key
+      const int c = tid < 256 ? s_hist[255 - tid] : 0;
+      const int incl = scan256(c, s_tmp);
+      if (tid < 256 && incl >= want && incl - c < want) {
+        s_sel[0] = 255 - tid;
+        s_sel[1] = want - (incl - c);
+      }
+      __syncthreads();
+      T |= (uint32_t)s_sel[0] << shift;
+      want = s_sel[1];
+      __syncthreads();  // s_sel is rewritten by the next digit
+    }
+  }
   int* kidx = p.keep_idx + (long long)b * n;
   int* nidx = p.new_index + (long long)b * n;
   const int* oin = p.orig_in ? p.orig_in + (long long)b * n : nullptr;
   int* oout = p.orig_out ? p.orig_out + (long long)b * n : nullptr;
-  int carry = 0;
+  int carry = 0, tie_carry = 0;
   for (int base = 0; base < n; base += kScanThreads) {
     const int k = base + tid;
     bool keep = false;
-    if (k < L) {
-      const bool glob = (s_gbits[k >> 5] >> (k & 31)) & 1u;
-      keep = s[k] > p.threshold || (p.keep_global && glob);
+    if (!p.topk) {
+      if (k < L) keep = s[k] > p.threshold || (p.keep_global && is_glob(k));
+    } else {
+      const bool gkeep = k < L && p.keep_global && is_glob(k);
+      const uint32_t key = cand_key(k);
+      const bool cand = key != 0u && !none;
+      const bool tie = cand && key == T;
+      int ties;
+      const int tr = tie_carry + block_rank(tie, s_wave, ties);
+      tie_carry += ties;
+      keep = gkeep || (cand && (key > T || (tie && tr < want)));
     }
     int total;
     const int pos = carry + block_rank(keep, s_wave, total);

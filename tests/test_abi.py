@@ -25,7 +25,7 @@ def declared_functions():
 def test_exports_every_declared_symbol():
     L = sc.load()
     names = declared_functions()
-    assert len(names) == 13
+    assert len(names) == 14
     for name in names:
         assert hasattr(L, name), name
 
@@ -135,6 +135,20 @@ def test_prune_validation():
     assert call(nt=1, src=one(0x1000000), dst=one(0x1000000 + 128), rb=rb) == B.SC_EINVAL  # src/dst overlap
     assert call(nt=1, src=one(0x1000000), dst=one(0x2000000), rb=(ctypes.c_int64 * 1)(0)) == B.SC_EINVAL
     assert call(oin=0x3000000, oout=0x3000000 + 8) == B.SC_EINVAL
+
+
+def test_topk_validation():
+    L = sc.load()
+    cd = desc().c()
+    ws_need = sc.sc_ltp_prune_compact_workspace_size(desc())
+
+    def call(ratio, ws=0x800000):
+        return L.sc_topk_prune_compact(ctypes.byref(cd), 0x100000, ctypes.c_float(ratio), 1, 0, None, None, None,
+                                       0x200000, 0x300000, None, None, None, ws, ws_need, None)
+
+    for bad in (-0.01, 1.01, float("nan"), float("inf")):
+        assert call(bad) == B.SC_EINVAL
+    assert call(0.5, ws=None) == B.SC_EWORKSPACE
 
 
 def test_score_and_stack_validation():

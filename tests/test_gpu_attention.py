@@ -207,3 +207,52 @@ def test_orig_index_composition_and_poisoned_tail():
         m = nl[b]
         assert np.array_equal(orig[b, :m], oin[b, keep[b, :m]]) and np.all(orig[b, m:] == -1)
         assert np.all(np.isnan(oc[b, m:])) and not np.isnan(oc[b, :m]).any()
+
+
+def _topk_compare(d, scores_np, vl, gp, ratio, keep_global, rows=None):
+    """GPU top-k compaction of float32 scores against the oracle, bit-exact (indices and gathered rows)."""
+    s32 = torch.from_numpy(np.ascontiguousarray(scores_np, dtype=np.float32)).to("cuda:0")
+    tensors = [rows] if rows is not None else []
+    keep, nl, ngp, orig, dsts = sc.sc_topk_prune_compact(d, s32, ratio, keep_global, tensors)
+    rk, rnl, rngp, rorig = oracle.topk_prune(scores_np, vl, gp, ratio, keep_global)
+    assert np.array_equal(nl.cpu().numpy(), rnl), (ratio, keep_global)
+    assert np.array_equal(keep.cpu().numpy(), rk)
+    assert np.array_equal(orig.cpu().numpy(), rorig)
+    if ngp is not None:
+        assert np.array_equal(ngp.cpu().numpy(), rngp)
+    if rows is not None:
+        src, dst = rows.view(torch.int16).cpu().numpy(), dsts[0].view(torch.int16).cpu().numpy()
+        for b in range(len(rnl)):
+            assert np.array_equal(dst[b, :rnl[b]], src[b, rk[b, :rnl[b]]])
+    return rnl
+
+
+@pytest.mark.parametrize("cid", [2, 4, 6])
+def test_config_topk_prune(cid):
+    """Top-k rule on the oracle's float32 scores of a workload: bit-exact keep lists and compaction."""
+    inp, (ro, rl, rs), g = config_run(cid)
+    d = g["desc"]
+    for ratio in (0.0, 0.3, 0.5, 0.9, 1.0):
+        for kg in (1, 0):
+            nl = _topk_compare(d, rs.astype(np.float32), inp["valid_len"], inp["global_pos"], ratio, kg,
+                               rows=g["out_t"] if (ratio == 0.5 and kg) else None)
+    log(f"config {cid}: top-k ratio 1.0 keeps {nl.tolist()}")
+
+
+def test_topk_ties_signs_and_lengths():
+    """Ties everywhere (scores on 3 levels), negative scores and both zeros, lengths 0 / 1 / n / ragged over
+    several 1024-token chunks."""
+    rng = np.random.default_rng(5)
+    B, n, G = 6, 2600, 5
+    vl = np.array([0, 1, n, 1500, 2047, 999], np.int32)
+    gp = np.full((B, G), -1, np.int32)
+    for b in range(B):
+        if vl[b]:
+            gp[b, :min(G, vl[b])] = np.sort(rng.choice(vl[b], size=min(G, vl[b]), replace=False))
+    levels = np.array([-0.5, -0.0, 0.0, 0.25, 0.25, 1.0], np.float32)
+    s = levels[rng.integers(0, len(levels), (B, n))]
+    d = sc.Desc(B, n, 2, 8, dev_i32(vl), dev_i32(gp), 0.125, sc.SC_BF16)
+    rows = torch.from_numpy(rng.integers(-30000, 30000, (B, n, 16)).astype(np.int16)).to("cuda:0").view(torch.bfloat16)
+    for ratio in (0.0, 1e-4, 0.2, 1.0 / 3.0, 0.5, 0.75, 1.0):
+        for kg in (1, 0):
+            _topk_compare(d, s, vl, gp, ratio, kg, rows=rows if kg else None)
