@@ -52,8 +52,12 @@ def lib():
                                         i32p, i32p, i32p, f32p, ci]
         L.orc_encoder_stack.argtypes = [ci, ci, ci, ci, ci, ci, i32p, i32p, cd, ci, f64p, f64p, f64p, f32p, ci, cd,
                                         f64p, i32p, i32p, i32p, ci]
+        L.orc_encoder_layer_ffn.argtypes = [ci, ci, ci, ci, ci, ci, i32p, i32p, cd, f64p, f64p, f64p, f64p, f64p, ci,
+                                            cf, ci, cd, f64p, i32p, i32p, i32p, f32p, ci]
+        L.orc_encoder_stack_ffn.argtypes = [ci, ci, ci, ci, i32p, ci, i32p, i32p, cd, ci, f64p, f64p, f64p, f64p,
+                                            f64p, ci, f32p, ci, cd, f64p, i32p, i32p, i32p, ci]
         for f in ("orc_sparse_attention", "orc_ltp_prune", "orc_topk_prune", "orc_gather_rows", "orc_encoder_layer",
-                  "orc_encoder_stack"):
+                  "orc_encoder_stack", "orc_encoder_layer_ffn", "orc_encoder_stack_ffn"):
             getattr(L, f).restype = ci
         _lib = L
     return _lib
@@ -145,8 +149,9 @@ def gather_rows(src, keep_idx, new_len, dst=None):
 
 
 def encoder_layer(x, wqkv, wo, valid_len, global_pos, H, window, alpha, threshold, keep_global=1, ln_eps=1e-5,
-                  nthreads=None):
-    """x: [B, n, D] doubles (bf16 values).  Returns (y, keep_idx, new_len, new_global_pos, scores32)."""
+                  nthreads=None, w1=None, w2=None):
+    """x: [B, n, D] doubles (bf16 values).  Returns (y, keep_idx, new_len, new_global_pos, scores32).
+    w1 [D, F], w2 [F, D]: the feed-forward block (None: attention-only layer)."""
     x = _f64(x)
     B, n, D = x.shape
     d = D // H
@@ -158,6 +163,16 @@ def encoder_layer(x, wqkv, wo, valid_len, global_pos, H, window, alpha, threshol
     new_len = np.empty(B, np.int32)
     ngp = np.empty((B, G), np.int32)
     sc = np.empty((B, n), np.float32)
+    if w1 is not None:
+        w1, w2 = _f64(w1), _f64(w2)
+        rc = lib().orc_encoder_layer_ffn(
+            B, n, H, d, int(window), G, _p(gp, ctypes.c_int32), _p(vl, ctypes.c_int32), float(alpha),
+            _p(x, ctypes.c_double), _p(_f64(wqkv), ctypes.c_double), _p(_f64(wo), ctypes.c_double),
+            _p(w1, ctypes.c_double), _p(w2, ctypes.c_double), int(w1.shape[1]), np.float32(threshold).item(),
+            int(keep_global), float(ln_eps), _p(y, ctypes.c_double), _p(keep_idx, ctypes.c_int32),
+            _p(new_len, ctypes.c_int32), _p(ngp, ctypes.c_int32), _p(sc, ctypes.c_float), nthreads or default_threads())
+        assert rc == 0
+        return y, keep_idx, new_len, ngp, sc
     rc = lib().orc_encoder_layer(B, n, H, d, int(window), G, _p(gp, ctypes.c_int32), _p(vl, ctypes.c_int32),
                                  float(alpha), _p(x, ctypes.c_double), _p(_f64(wqkv), ctypes.c_double),
                                  _p(_f64(wo), ctypes.c_double), np.float32(threshold).item(), int(keep_global),
@@ -169,8 +184,9 @@ def encoder_layer(x, wqkv, wo, valid_len, global_pos, H, window, alpha, threshol
 
 
 def encoder_stack(x, wqkv_list, wo_list, valid_len, global_pos, H, window, alpha, thresholds, keep_global=1,
-                  ln_eps=1e-5, nthreads=None):
-    """Returns (y, final_len, orig_idx, kept_per_layer)."""
+                  ln_eps=1e-5, nthreads=None, w1_list=None, w2_list=None):
+    """Returns (y, final_len, orig_idx, kept_per_layer).  window: one int, or one per layer; w1_list / w2_list:
+    the feed-forward blocks of the layers (None: attention-only layers)."""
     x = _f64(x)
     B, n, D = x.shape
     d = D // H
@@ -185,6 +201,19 @@ def encoder_stack(x, wqkv_list, wo_list, valid_len, global_pos, H, window, alpha
     fl = np.empty(B, np.int32)
     oi = np.empty((B, n), np.int32)
     kpl = np.empty((nl, B), np.int32)
+    if w1_list is not None or not np.isscalar(window):
+        win = np.ascontiguousarray(np.broadcast_to(np.asarray(window, dtype=np.int32), (nl,)))
+        assert w1_list is not None, "per-layer windows are part of the full stack"
+        w1 = _f64(np.stack(w1_list))
+        w2 = _f64(np.stack(w2_list))
+        rc = lib().orc_encoder_stack_ffn(
+            B, n, H, d, _p(win, ctypes.c_int32), G, _p(gp, ctypes.c_int32), _p(vl, ctypes.c_int32), float(alpha), nl,
+            _p(x, ctypes.c_double), _p(wq, ctypes.c_double), _p(wo, ctypes.c_double), _p(w1, ctypes.c_double),
+            _p(w2, ctypes.c_double), int(w1.shape[2]), _p(th, ctypes.c_float), int(keep_global), float(ln_eps),
+            _p(y, ctypes.c_double), _p(fl, ctypes.c_int32), _p(oi, ctypes.c_int32), _p(kpl, ctypes.c_int32),
+            nthreads or default_threads())
+        assert rc == 0
+        return y, fl, oi, kpl
     rc = lib().orc_encoder_stack(B, n, H, d, int(window), G, _p(gp, ctypes.c_int32), _p(vl, ctypes.c_int32),
                                  float(alpha), nl, _p(x, ctypes.c_double), _p(wq, ctypes.c_double),
                                  _p(wo, ctypes.c_double), _p(th, ctypes.c_float), int(keep_global), float(ln_eps),

@@ -265,21 +265,41 @@ int orc_gather_rows(int B, int n, long row_bytes, const void* src, void* dst, co
   return 0;
 }
 
-// One layer of the attention-only encoder stack (RoBERTa-shaped, no FFN):
+// LayerNorm of one row (gamma = 1, beta = 0, biased variance, eps inside the
+// square root), rounded to bf16.
+static void layer_norm_bf16(const std::vector<double>& t, long D, double ln_eps, double* yr) {
+  double mean = 0.0;
+  for (long c = 0; c < D; ++c) mean += t[c];
+  mean /= (double)D;
+  double var = 0.0;
+  for (long c = 0; c < D; ++c) var += (t[c] - mean) * (t[c] - mean);
+  var /= (double)D;
+  double inv = 1.0 / std::sqrt(var + ln_eps);
+  for (long c = 0; c < D; ++c) yr[c] = round_bf16((t[c] - mean) * inv);
+}
+
+// GELU in its exact form, x * Phi(x) with the standard normal CDF Phi.
+static double gelu(double v) { return 0.5 * v * (1.0 + std::erf(v / std::sqrt(2.0))); }
+
+// One encoder layer (RoBERTa-shaped, post-LN, no biases; Sec. 4.2, Fig. 5):
 //   qkv = bf16(x . Wqkv)            [columns q | k | v, each head-major]
 //   O   = bf16(sparse attention(q, k, v))
 //   s   = float32(importance scores); keep / compaction as orc_ltp_prune
-//   y   = bf16(LayerNorm(x + O . Wo)) on the kept rows, gamma = 1, beta = 0,
-//         biased variance, eps inside the square root.
-// x: [B, n, D] exact bf16 values; Wqkv: [D, 3D] and Wo: [D, D] row-major.
-// Outputs: y [B, n, D] compacted (rows >= new_len zero), keep_idx [B, n],
-// new_len [B], new_global_pos [B, G], scores (optional) [B, n] float32.
-int orc_encoder_layer(int B, int n, int H, int d, int window, int G, const int32_t* global_pos,
-                      const int32_t* valid_len, double alpha, const double* x, const double* Wqkv,
-                      const double* Wo, float threshold, int keep_global, double ln_eps, double* y,
-                      int32_t* keep_idx, int32_t* new_len, int32_t* new_global_pos, float* scores_out,
-                      int nthreads) {
-  if (B < 0 || n < 0 || H <= 0 || d <= 0) return -1;
+//   x1  = bf16(LayerNorm(x + O . Wo)) on the kept rows
+// and, with a feed-forward block (W1 non-NULL), on the kept rows
+//   h   = bf16(GELU(x1 . W1))       W1 [D, F]
+//   y   = bf16(LayerNorm(x1 + h . W2))   W2 [F, D]
+// else y = x1.  LayerNorm: gamma = 1, beta = 0, biased variance, eps inside
+// the square root.  x: [B, n, D] exact bf16 values; Wqkv: [D, 3D] and Wo:
+// [D, D] row-major.  Outputs: y [B, n, D] compacted (rows >= new_len zero),
+// keep_idx [B, n], new_len [B], new_global_pos [B, G], scores (optional)
+// [B, n] float32.
+static int encoder_layer(int B, int n, int H, int d, int window, int G, const int32_t* global_pos,
+                         const int32_t* valid_len, double alpha, const double* x, const double* Wqkv,
+                         const double* Wo, const double* W1, const double* W2, int F, float threshold,
+                         int keep_global, double ln_eps, double* y, int32_t* keep_idx, int32_t* new_len,
+                         int32_t* new_global_pos, float* scores_out, int nthreads) {
+  if (B < 0 || n < 0 || H <= 0 || d <= 0 || (W1 && F <= 0)) return -1;
   set_threads(nthreads);
   const long D = (long)H * d, D3 = 3 * D;
   std::vector<double> qv((size_t)B * n * D), kv((size_t)B * n * D), vv((size_t)B * n * D);
@@ -310,7 +330,7 @@ int orc_encoder_layer(int B, int n, int H, int d, int window, int G, const int32
   if (scores_out) std::memcpy(scores_out, s32.data(), s32.size() * sizeof(float));
   orc_ltp_prune(B, n, G, global_pos, valid_len, s32.data(), threshold, keep_global, keep_idx, new_len,
                 new_global_pos, nullptr, nullptr);
-  // a9 on the kept rows: residual + output projection + LayerNorm.
+  // a9 (and the feed-forward block) on the kept rows.
 #pragma omp parallel for schedule(dynamic, 4)
   for (long row = 0; row < (long)B * n; ++row) {
     int b = (int)(row / n), j = (int)(row % n);
@@ -327,28 +347,63 @@ int orc_encoder_layer(int B, int n, int H, int d, int window, int G, const int32
       const double* w = Wo + c * D;
       for (long e = 0; e < D; ++e) t[e] += ov * w[e];
     }
-    double mean = 0.0;
-    for (long c = 0; c < D; ++c) mean += t[c];
-    mean /= (double)D;
-    double var = 0.0;
-    for (long c = 0; c < D; ++c) var += (t[c] - mean) * (t[c] - mean);
-    var /= (double)D;
-    double inv = 1.0 / std::sqrt(var + ln_eps);
-    for (long c = 0; c < D; ++c) yr[c] = round_bf16((t[c] - mean) * inv);
+    if (!W1) {
+      layer_norm_bf16(t, D, ln_eps, yr);
+      continue;
+    }
+    std::vector<double> x1(D), h(F, 0.0);
+    layer_norm_bf16(t, D, ln_eps, x1.data());
+    for (long c = 0; c < D; ++c) {
+      const double* w = W1 + c * (long)F;
+      for (long f = 0; f < F; ++f) h[f] += x1[c] * w[f];
+    }
+    for (long f = 0; f < F; ++f) h[f] = round_bf16(gelu(h[f]));
+    for (long c = 0; c < D; ++c) t[c] = x1[c];
+    for (long f = 0; f < F; ++f) {
+      const double* w = W2 + f * D;
+      for (long c = 0; c < D; ++c) t[c] += h[f] * w[c];
+    }
+    layer_norm_bf16(t, D, ln_eps, yr);
   }
   return 0;
 }
 
-// The multi-layer stack: orc_encoder_layer applied n_layers times, each layer
-// on the previous layer's compacted output and renumbered global tokens.
-//   Wqkv: n_layers consecutive [D, 3D] matrices; Wo: n_layers consecutive [D, D].
-//   thresholds [n_layers]; y [B, n, D]; final_len [B]; orig_idx [B, n] (input
-//   position of each surviving row, -1 beyond final_len); kept_per_layer
-//   [n_layers, B] (sequence length after each layer's pruning).
-int orc_encoder_stack(int B, int n, int H, int d, int window, int G, const int32_t* global_pos,
-                      const int32_t* valid_len, double alpha, int n_layers, const double* x, const double* Wqkv,
-                      const double* Wo, const float* thresholds, int keep_global, double ln_eps, double* y,
-                      int32_t* final_len, int32_t* orig_idx, int32_t* kept_per_layer, int nthreads) {
+// One attention-only layer (no feed-forward block): encoder_layer with W1 = NULL.
+int orc_encoder_layer(int B, int n, int H, int d, int window, int G, const int32_t* global_pos,
+                      const int32_t* valid_len, double alpha, const double* x, const double* Wqkv,
+                      const double* Wo, float threshold, int keep_global, double ln_eps, double* y,
+                      int32_t* keep_idx, int32_t* new_len, int32_t* new_global_pos, float* scores_out,
+                      int nthreads) {
+  return encoder_layer(B, n, H, d, window, G, global_pos, valid_len, alpha, x, Wqkv, Wo, nullptr, nullptr, 0,
+                       threshold, keep_global, ln_eps, y, keep_idx, new_len, new_global_pos, scores_out, nthreads);
+}
+
+// One full layer with the feed-forward block (W1 [D, F], W2 [F, D]).
+int orc_encoder_layer_ffn(int B, int n, int H, int d, int window, int G, const int32_t* global_pos,
+                          const int32_t* valid_len, double alpha, const double* x, const double* Wqkv,
+                          const double* Wo, const double* W1, const double* W2, int F, float threshold,
+                          int keep_global, double ln_eps, double* y, int32_t* keep_idx, int32_t* new_len,
+                          int32_t* new_global_pos, float* scores_out, int nthreads) {
+  if (!W1 || !W2) return -1;
+  return encoder_layer(B, n, H, d, window, G, global_pos, valid_len, alpha, x, Wqkv, Wo, W1, W2, F, threshold,
+                       keep_global, ln_eps, y, keep_idx, new_len, new_global_pos, scores_out, nthreads);
+}
+
+// The multi-layer stack: the layer applied n_layers times, each layer on the
+// previous layer's compacted output and renumbered global tokens.
+//   windows [n_layers]: the window of each layer (Sec. 7.1 names the scheme
+//   of small windows in lower layers and large ones in higher layers); Wqkv:
+//   n_layers consecutive [D, 3D] matrices; Wo: n_layers
+//   consecutive [D, D]; W1 / W2 (NULL: attention-only layers): n_layers
+//   consecutive [D, F] / [F, D].  thresholds [n_layers]; y [B, n, D];
+//   final_len [B]; orig_idx [B, n] (input position of each surviving row, -1
+//   beyond final_len); kept_per_layer [n_layers, B] (sequence length after
+//   each layer's pruning).
+static int encoder_stack(int B, int n, int H, int d, const int32_t* windows, int G, const int32_t* global_pos,
+                         const int32_t* valid_len, double alpha, int n_layers, const double* x, const double* Wqkv,
+                         const double* Wo, const double* W1, const double* W2, int F, const float* thresholds,
+                         int keep_global, double ln_eps, double* y, int32_t* final_len, int32_t* orig_idx,
+                         int32_t* kept_per_layer, int nthreads) {
   const long D = (long)H * d;
   std::vector<double> cur(x, x + (size_t)B * n * D), nxt((size_t)B * n * D);
   std::vector<int32_t> len(valid_len, valid_len + B), gp(global_pos, global_pos + (size_t)B * G);
@@ -356,9 +411,11 @@ int orc_encoder_stack(int B, int n, int H, int d, int window, int G, const int32
   for (int b = 0; b < B; ++b)
     for (int j = 0; j < n; ++j) orig[(size_t)b * n + j] = j < len[b] ? j : -1;
   for (int l = 0; l < n_layers; ++l) {
-    int rc = orc_encoder_layer(B, n, H, d, window, G, gp.data(), len.data(), alpha, cur.data(),
-                               Wqkv + (size_t)l * D * 3 * D, Wo + (size_t)l * D * D, thresholds[l], keep_global,
-                               ln_eps, nxt.data(), kidx.data(), nl.data(), ngp.data(), nullptr, nthreads);
+    int rc = encoder_layer(B, n, H, d, windows[l], G, gp.data(), len.data(), alpha, cur.data(),
+                           Wqkv + (size_t)l * D * 3 * D, Wo + (size_t)l * D * D,
+                           W1 ? W1 + (size_t)l * D * F : nullptr, W2 ? W2 + (size_t)l * F * D : nullptr, F,
+                           thresholds[l], keep_global, ln_eps, nxt.data(), kidx.data(), nl.data(), ngp.data(),
+                           nullptr, nthreads);
     if (rc) return rc;
     for (int b = 0; b < B; ++b)
       for (int j = 0; j < n; ++j) {
@@ -375,6 +432,27 @@ int orc_encoder_stack(int B, int n, int H, int d, int window, int G, const int32
   std::memcpy(final_len, len.data(), (size_t)B * sizeof(int32_t));
   std::memcpy(orig_idx, orig.data(), orig.size() * sizeof(int32_t));
   return 0;
+}
+
+// Attention-only stack with one window for every layer.
+int orc_encoder_stack(int B, int n, int H, int d, int window, int G, const int32_t* global_pos,
+                      const int32_t* valid_len, double alpha, int n_layers, const double* x, const double* Wqkv,
+                      const double* Wo, const float* thresholds, int keep_global, double ln_eps, double* y,
+                      int32_t* final_len, int32_t* orig_idx, int32_t* kept_per_layer, int nthreads) {
+  std::vector<int32_t> windows(n_layers > 0 ? n_layers : 1, window);
+  return encoder_stack(B, n, H, d, windows.data(), G, global_pos, valid_len, alpha, n_layers, x, Wqkv, Wo, nullptr,
+                       nullptr, 0, thresholds, keep_global, ln_eps, y, final_len, orig_idx, kept_per_layer, nthreads);
+}
+
+// Full stack: per-layer windows and the feed-forward block in every layer.
+int orc_encoder_stack_ffn(int B, int n, int H, int d, const int32_t* windows, int G, const int32_t* global_pos,
+                          const int32_t* valid_len, double alpha, int n_layers, const double* x, const double* Wqkv,
+                          const double* Wo, const double* W1, const double* W2, int F, const float* thresholds,
+                          int keep_global, double ln_eps, double* y, int32_t* final_len, int32_t* orig_idx,
+                          int32_t* kept_per_layer, int nthreads) {
+  if (!windows || !W1 || !W2) return -1;
+  return encoder_stack(B, n, H, d, windows, G, global_pos, valid_len, alpha, n_layers, x, Wqkv, Wo, W1, W2, F,
+                       thresholds, keep_global, ln_eps, y, final_len, orig_idx, kept_per_layer, nthreads);
 }
 
 }  // extern "C"

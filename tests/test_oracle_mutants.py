@@ -41,6 +41,10 @@ MUTANTS = [
      "std::reverse(cand.begin(), cand.end());\n    std::stable_sort(cand.begin()"),
     ("top-k count rounded down", "(long)std::ceil(prod)", "(long)std::floor(prod)"),
     ("top-k counts kept globals as candidates", "      else\n        cand.push_back(k);", "      cand.push_back(k);"),
+    ("GELU replaced by ReLU", "return 0.5 * v * (1.0 + std::erf(v / std::sqrt(2.0)));", "return v > 0.0 ? v : 0.0;"),
+    ("feed-forward residual dropped", "for (long c = 0; c < D; ++c) t[c] = x1[c];", "for (long c = 0; c < D; ++c) t[c] = 0.0;"),
+    ("feed-forward hidden not stored as bf16", "h[f] = round_bf16(gelu(h[f]));", "h[f] = gelu(h[f]);"),
+    ("per-layer window ignored", "int rc = encoder_layer(B, n, H, d, windows[l],", "int rc = encoder_layer(B, n, H, d, windows[0],"),
 ]
 
 

@@ -397,8 +397,9 @@ def check_bf16_rounding():
     assert oracle.round_bf16(-(1 + 2 ** -8)) == -1.0
 
 
-def _ref_layer(x, wqkv, wo, vl, gp, H, alpha, theta, eps):
-    """Library composition for dense windows: numpy matmul, torch SDPA, torch layer_norm, torch bf16."""
+def _ref_layer(x, wqkv, wo, vl, gp, H, alpha, theta, eps, w1=None, w2=None):
+    """Library composition for dense windows: numpy matmul, torch SDPA, torch layer_norm, torch bf16, and for
+    the feed-forward block torch's exact GELU."""
     B, n, D = x.shape
     d = D // H
     qkv = _torch_bf16(x @ wqkv)
@@ -416,6 +417,9 @@ def _ref_layer(x, wqkv, wo, vl, gp, H, alpha, theta, eps):
         O = _torch_bf16(O.permute(0, 2, 1, 3).reshape(L, D).numpy())
         t = torch.from_numpy(x[b, :L] + O @ wo)
         yy = _torch_bf16(torch.nn.functional.layer_norm(t, (D,), eps=eps).numpy())
+        if w1 is not None:
+            h = _torch_bf16(torch.nn.functional.gelu(torch.from_numpy(yy @ w1), approximate="none").numpy())
+            yy = _torch_bf16(torch.nn.functional.layer_norm(torch.from_numpy(yy + h @ w2), (D,), eps=eps).numpy())
         y[b, :len(kept)] = yy[kept]
         kept_all.append(kept)
         nl.append(len(kept))
@@ -448,6 +452,61 @@ def check_encoder_layer_against_libraries():
         ulp = np.maximum(np.abs(ry), 1e-30) * 2.0 ** -7
         assert np.all(diff <= ulp)                    # at most one bf16 step apart ...
         assert np.mean(diff == 0) > 0.995             # ... and nearly all identical
+
+
+def _ffn_weights(seed, D, F=None):
+    rng = np.random.default_rng(seed)
+    F = F or 4 * D
+    return _torch_bf16(rng.standard_normal((D, F)) * 0.3), _torch_bf16(rng.standard_normal((F, D)) * 0.3)
+
+
+def check_ffn_layer_against_libraries():
+    """Full layer (attention, prune, Wo + LN, GELU feed-forward + LN) against the library composition."""
+    x, wqkv, wo, vl, gp, H = stack_case(503)
+    n, D = x.shape[1], x.shape[2]
+    w1, w2 = _ffn_weights(7, D)
+    for theta in (-1.0, 0.045):
+        y, ki, nl, ngp, sc = oracle.encoder_layer(x, wqkv, wo, vl, gp, H, 2 * n, 0.6, theta, w1=w1, w2=w2)
+        ry, rkept, rnl = _ref_layer(x, wqkv, wo, vl, gp, H, 0.6, theta, 1e-5, w1, w2)
+        assert list(nl) == rnl
+        diff = np.abs(y - ry)
+        ulp = np.maximum(np.abs(ry), 1e-30) * 2.0 ** -7
+        assert np.mean(diff <= ulp) > 0.998           # one bf16 step, except where a step upstream moved it
+        assert np.mean(diff == 0) > 0.98
+
+
+def check_ffn_zero_output_weights():
+    """W2 = 0: the feed-forward block adds nothing, so the layer is LayerNorm of the attention-only output."""
+    x, wqkv, wo, vl, gp, H = stack_case(504)
+    D = x.shape[2]
+    w1, _ = _ffn_weights(8, D)
+    y, ki, nl, _, _ = oracle.encoder_layer(x, wqkv, wo, vl, gp, H, 6, 0.6, 0.04, w1=w1, w2=np.zeros((4 * D, D)))
+    y0, ki0, nl0, _, _ = oracle.encoder_layer(x, wqkv, wo, vl, gp, H, 6, 0.6, 0.04)
+    assert np.array_equal(ki, ki0) and np.array_equal(nl, nl0)
+    ref = _torch_bf16(torch.nn.functional.layer_norm(torch.from_numpy(y0), (D,), eps=1e-5).numpy())
+    for b in range(x.shape[0]):
+        assert np.array_equal(y[b, :nl[b]], ref[b, :nl[b]])
+        assert np.all(y[b, nl[b]:] == 0)
+
+
+def check_full_stack_composition():
+    """Full stack with per-layer windows = its layers applied in turn."""
+    x, wqkv, wo, vl, gp, H = stack_case(505)
+    n, D = x.shape[1], x.shape[2]
+    th = [0.0, 0.05, 0.06]
+    wins = [2, 6, 2 * n]
+    wq = [wqkv, wqkv[:, ::-1].copy(), wqkv * 0.5]
+    wo_ = [wo, wo.T.copy(), wo]
+    f1, f2 = zip(*[_ffn_weights(20 + l, D, 3 * D) for l in range(3)])
+    y, fl, oi, kpl = oracle.encoder_stack(x, wq, wo_, vl, gp, H, wins, 0.6, th, w1_list=f1, w2_list=f2)
+    cur, cl, cg = x, vl, gp
+    orig = np.where(np.arange(n)[None, :] < vl[:, None], np.arange(n)[None, :], -1)
+    for l in range(3):
+        cur, ki, cl, cg, _ = oracle.encoder_layer(cur, wq[l], wo_[l], cl, cg, H, wins[l], 0.6, th[l], w1=f1[l],
+                                                  w2=f2[l])
+        orig = np.where(ki >= 0, np.take_along_axis(orig, np.maximum(ki, 0), 1), -1)
+        assert list(kpl[l]) == list(cl)
+    assert np.array_equal(y, cur) and list(fl) == list(cl) and np.array_equal(oi, orig)
 
 
 def check_layernorm_statistics():
@@ -494,7 +553,8 @@ ATTENTION_CHECKS = [check_brute_force, check_window_covers_sequence_is_dense, ch
 PRUNE_CHECKS = [check_prune_brute_force, check_prune_invariants, check_mask_rule_golden, check_gather_rows,
                 check_topk_rank_invariants, check_topk_equals_threshold_rule]
 STACK_CHECKS = [check_bf16_rounding, check_encoder_layer_against_libraries, check_layernorm_statistics,
-                check_stack_composition]
+                check_stack_composition, check_ffn_layer_against_libraries, check_ffn_zero_output_weights,
+                check_full_stack_composition]
 ALL_CHECKS = ATTENTION_CHECKS + PRUNE_CHECKS + STACK_CHECKS + [check_paper_threshold_schedule]
 
 
