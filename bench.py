@@ -37,7 +37,84 @@ WORKLOADS = {
     "lognormal": (6, "single sparse-attention + LTP layer: B64 n1024 H12 d64 bf16, window 256, global token 0, "
                      "valid lengths round(exp(N(5.717, 0.738^2))) clipped to [1,1024] (paper-shaped), threshold "
                      "pruning ~30%"),
+    "encoder": (None, "12-layer RoBERTa-base-shaped SparseCoder encoder: B16 n2048 D768 (12 heads x 64), GELU "
+                      "feed-forward 3072, windows 64,64,128,128,256,256,512x6, global token 0, valid lengths "
+                      "U[256,2048], thresholds 0.01*l/11, pruning after every layer"),
 }
+
+
+def pairs_of(valid_len, global_pos, window):
+    """Allowed (query, key) pairs of one layer: the window rows and the global rows."""
+    pw, pg = algorithmic_counts(dict(B=len(valid_len), valid_len=valid_len, global_pos=global_pos, window=window))
+    return pw + pg
+
+
+def model_flops(lens_in, lens_kept, pairs, D, H, d, F):
+    """FLOPs of one encoder layer broken down as the paper does (Sec. 5.1, after Electra): projections (Q, K, V
+    on the layer's input tokens, the output projection on the surviving ones), sparse attention (Q.K^T and P.V
+    per allowed pair and head), the feed-forward block on the surviving tokens, and other operations (softmax:
+    5 per pair and head for max, subtract, exp, sum, divide; importance scores: 1 add per pair and head; two
+    LayerNorms: 5 per element; GELU: 8 per hidden element).  A multiply-add counts 2."""
+    t_in, t_kept = float(sum(lens_in)), float(sum(lens_kept))
+    proj = 2 * t_in * D * 3 * D + 2 * t_kept * D * D
+    attn = 2 * 2 * d * H * pairs
+    ffn = 2 * 2 * t_kept * D * F
+    other = 6 * H * pairs + 2 * 5 * t_kept * D + 8 * t_kept * F
+    return dict(projection=proj, attention=attn, ffn=ffn, other=other)
+
+
+def measure_encoder(args, sc, si, torch, np, dev="cuda:0"):
+    """Times the full encoder stack (sc_encoder_stack over 12 layers)."""
+    cfg = si.STACK_FULL_CONFIG
+    t0 = time.time()
+    inp = si.make_stack_inputs(cfg)
+    gen_s = time.time() - t0
+
+    def bf(a):
+        return torch.from_numpy(np.ascontiguousarray(a).view(np.int16)).to(dev).view(torch.bfloat16)
+
+    def i32(a):
+        return torch.from_numpy(np.ascontiguousarray(a, dtype=np.int32)).to(dev)
+
+    d = sc.Desc(cfg.B, cfg.n, cfg.H, cfg.window, i32(inp["valid_len"]), i32(inp["global_pos"]), cfg.alpha, sc.SC_BF16)
+    x = bf(inp["x"])
+    wq, wo, w1, w2 = ([bf(w) for w in inp[k]] for k in ("wqkv", "wo", "w1", "w2"))
+    th = cfg.thresholds()
+    ws = torch.empty(sc.sc_encoder_stack_workspace_size(d, cfg.n_layers, cfg.ffn_dim), dtype=torch.uint8, device=dev)
+    x_out = torch.empty_like(x)
+
+    def step():
+        return sc.sc_encoder_stack(d, x, wq, wo, w1, w2, th, windows=inp["windows"], x_out=x_out, workspace=ws)
+
+    for _ in range(args.warmup):
+        step()
+    torch.cuda.synchronize()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record()
+    for _ in range(args.steps):
+        res = step()
+    e1.record()
+    torch.cuda.synchronize()
+    ms = e0.elapsed_time(e1) / args.steps
+    kpl = res[3].cpu().numpy()
+    # per-layer input lengths and global positions (token 0 is global and always kept, so it stays at 0)
+    lens_in = [inp["valid_len"].astype(np.int64)] + [kpl[l].astype(np.int64) for l in range(cfg.n_layers - 1)]
+    tokens = int(sum(int(np.sum(li)) for li in lens_in))
+    D, F = cfg.H * cfg.d, cfg.ffn_dim
+    parts = dict(projection=0.0, attention=0.0, ffn=0.0, other=0.0)
+    for l in range(cfg.n_layers):
+        li = lens_in[l]
+        gp = np.where(li[:, None] > 0, 0, -1).astype(np.int32)
+        f = model_flops(li, kpl[l], pairs_of(li, gp, inp["windows"][l]), D, cfg.H, cfg.d, F)
+        for k in parts:
+            parts[k] += f[k]
+    total = sum(parts.values())
+    achieved = total / (ms * 1e-3) / 1e12
+    return dict(ms=ms, tokens=tokens, kept_per_layer=[int(np.sum(k)) for k in kpl], gen_s=gen_s,
+                gflops={k: round(v / 1e9, 2) for k, v in parts.items()}, total_gflops=round(total / 1e9, 2),
+                roof=dict(bound="mfma", achieved=round(achieved, 2), peak=MFMA_PEAK_TFLOPS["bf16"], unit="TFLOP/s",
+                          frac=round(achieved / MFMA_PEAK_TFLOPS["bf16"], 4), traffic=None,
+                          kernel="whole encoder step (model FLOPs as counted by model_flops)"))
 
 
 def kernel_source_hash():
@@ -224,6 +301,17 @@ def main():
         sweep(args, sc, si, torch, np)
         return
     cid, desc = WORKLOADS[args.workload]
+    if cid is None:
+        m = measure_encoder(args, sc, si, torch, np, dev)
+        print(json.dumps({
+            "metric": METRIC, "value": round(m["tokens"] / (m["ms"] * 1e-3), 1), "unit": "kept-token-layers/s",
+            "n_gpus": 1, "steps": args.steps, "warmup": args.warmup, "ms_per_step": round(m["ms"], 4),
+            "higher_is_better": True, "scaling": "weak", "vs_baseline": None, "dtype": "bf16", "data": "synthetic",
+            "config": {"workload": desc, "layer_input_tokens": m["tokens"], "kept_per_layer": m["kept_per_layer"],
+                       "parallelism": "none (1 GPU)"},
+            "model_gflops": m["gflops"], "model_gflops_total": m["total_gflops"], "roofline": m["roof"],
+            "input_generation_s": round(m["gen_s"], 1)}), flush=True)
+        return
     cfg = si.CONFIGS[cid]
     with open(os.path.join(ROOT, "tests", "golden", "thresholds.json")) as f:
         theta = json.load(f)[str(cid)]["theta"]

@@ -22,6 +22,8 @@
  *   sc_topk_prune_compact the same compaction with a top-k rule instead of the
  *                         threshold (a variant in the family of cascade token
  *                         pruning the paper cites in Sec. 2);
+ *   sc_encoder_stack      the full encoder stack: the layers above with a GELU
+ *                         feed-forward block and a window per layer;
  *   sc_encoder_attn_stack the attention-only encoder stack (QKV projection,
  *                         the three steps above, output projection, residual
  *                         and LayerNorm) over several layers, each layer on the
@@ -231,6 +233,31 @@ sc_status sc_encoder_attn_stack(const sc_attn_desc *desc, int32_t n_layers, cons
                                 int32_t keep_global, float ln_eps, void *x_out, int32_t *final_len,
                                 int32_t *orig_idx, int32_t *kept_per_layer, void *workspace, size_t ws_bytes,
                                 void *stream);
+
+size_t sc_encoder_stack_workspace_size(const sc_attn_desc *desc, int32_t n_layers, int32_t ffn_dim);
+
+/*
+ * Full encoder stack: every layer as in sc_encoder_attn_stack, followed by the
+ * feed-forward block of a RoBERTa-shaped post-LN layer (Sec. 4.2, Fig. 5), with
+ * a window per layer (Sec. 7.1 names small windows in lower layers and large
+ * ones in higher layers):
+ *   x1  = bf16(LayerNorm(x + O . Wo[l]))          on the survivors
+ *   h   = bf16(GELU(x1 . W1[l]))                   W1 [D, ffn_dim]; GELU exact,
+ *                                                   v * Phi(v)
+ *   x   = bf16(LayerNorm(x1 + h . W2[l]))          W2 [ffn_dim, D]
+ * No biases; LayerNorm gamma 1, beta 0, eps ln_eps.
+ *   windows         HOST int32 [n_layers], each >= 0, or NULL (desc->window in
+ *                   every layer).
+ *   W1, W2          HOST arrays of n_layers device pointers (bf16), non-NULL.
+ *   ffn_dim         > 0 and a multiple of 8 (3072 for RoBERTa-base).
+ * Everything else (arguments, outputs, errors) as for sc_encoder_attn_stack;
+ * the workspace is sc_encoder_stack_workspace_size(desc, n_layers, ffn_dim).
+ */
+sc_status sc_encoder_stack(const sc_attn_desc *desc, int32_t n_layers, const int32_t *windows, const void *x_in,
+                           const void *const *Wqkv, const void *const *Wo, const void *const *W1,
+                           const void *const *W2, int32_t ffn_dim, const float *thresholds, int32_t keep_global,
+                           float ln_eps, void *x_out, int32_t *final_len, int32_t *orig_idx, int32_t *kept_per_layer,
+                           void *workspace, size_t ws_bytes, void *stream);
 
 /*
  * Kernel timing for benchmarks.  While enabled, the window-attention kernels

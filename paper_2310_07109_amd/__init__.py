@@ -9,15 +9,17 @@ There is no fallback: without the built library every call raises.
 """
 from ._binding import (SC_BF16, SC_F32, SC_SCORE_FROM_BAND_PROBS, SC_SCORE_FROM_PARTIALS, Desc, ScError,  # noqa
                        lib_path, load, sc_band_probs_size, sc_encoder_attn_stack,
-                       sc_encoder_attn_stack_workspace_size, sc_ltp_prune_compact, sc_topk_prune_compact,
-                       sc_ltp_prune_compact_workspace_size, sc_ltp_score, sc_ltp_score_workspace_size, sc_profile_window_kernel,
-                       sc_profile_window_kernel_read,
-                       sc_score_partials_size, sc_status_str, sc_window_attention, sc_window_attention_workspace_size)
+                       sc_encoder_attn_stack_workspace_size, sc_encoder_stack, sc_encoder_stack_workspace_size,
+                       sc_ltp_prune_compact, sc_ltp_prune_compact_workspace_size, sc_ltp_score,
+                       sc_ltp_score_workspace_size, sc_profile_window_kernel, sc_profile_window_kernel_read,
+                       sc_score_partials_size, sc_status_str, sc_topk_prune_compact, sc_window_attention,
+                       sc_window_attention_workspace_size)
 
 __all__ = [
     "SC_BF16", "SC_F32", "SC_SCORE_FROM_PARTIALS", "SC_SCORE_FROM_BAND_PROBS", "Desc", "ScError", "load",
     "lib_path", "sc_status_str", "sc_score_partials_size", "sc_band_probs_size",
     "sc_window_attention_workspace_size", "sc_window_attention", "sc_ltp_score_workspace_size", "sc_ltp_score",
-    "sc_ltp_prune_compact_workspace_size", "sc_ltp_prune_compact", "sc_topk_prune_compact", "sc_encoder_attn_stack_workspace_size",
-    "sc_encoder_attn_stack", "sc_profile_window_kernel", "sc_profile_window_kernel_read",
+    "sc_ltp_prune_compact_workspace_size", "sc_ltp_prune_compact", "sc_topk_prune_compact",
+    "sc_encoder_attn_stack_workspace_size", "sc_encoder_attn_stack", "sc_encoder_stack_workspace_size",
+    "sc_encoder_stack", "sc_profile_window_kernel", "sc_profile_window_kernel_read",
 ]

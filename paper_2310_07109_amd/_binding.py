@@ -53,6 +53,8 @@ def load():
         "sc_topk_prune_compact": (i32, [dp, vp, f32, i32, i32, vp, vp, vp, vp, vp, vp, vp, vp, vp, sz, vp]),
         "sc_encoder_attn_stack_workspace_size": (sz, [dp, i32]),
         "sc_encoder_attn_stack": (i32, [dp, i32, vp, vp, vp, vp, i32, f32, vp, vp, vp, vp, vp, sz, vp]),
+        "sc_encoder_stack_workspace_size": (sz, [dp, i32, i32]),
+        "sc_encoder_stack": (i32, [dp, i32, vp, vp, vp, vp, vp, vp, i32, vp, i32, f32, vp, vp, vp, vp, vp, sz, vp]),
         "sc_profile_window_kernel": (i32, [i32]),
         "sc_profile_window_kernel_read": (i32, [ctypes.POINTER(ctypes.c_double), ctypes.POINTER(ctypes.c_int64)]),
     }
@@ -247,6 +249,35 @@ def sc_encoder_attn_stack(desc: Desc, x_in, wqkv, wo, thresholds, keep_global=Tr
     _check(L.sc_encoder_attn_stack(ctypes.byref(cd), nl, _ptr(x_in), wq, wo_, th, int(bool(keep_global)),
                                    ctypes.c_float(ln_eps), _ptr(x_out), _ptr(final_len), _ptr(orig), _ptr(kpl),
                                    _ptr(ws), wsb, _stream(stream)), "sc_encoder_attn_stack")
+    return x_out, final_len, orig, kpl
+
+
+def sc_encoder_stack_workspace_size(desc: Desc, n_layers: int, ffn_dim: int) -> int:
+    return load().sc_encoder_stack_workspace_size(ctypes.byref(desc.c()), int(n_layers), int(ffn_dim))
+
+
+def sc_encoder_stack(desc: Desc, x_in, wqkv, wo, w1, w2, thresholds, windows=None, keep_global=True, ln_eps=1e-5,
+                     x_out=None, workspace=None, stream=None):
+    """Full stack (feed-forward block, per-layer windows).  Returns (x_out, final_len, orig_idx, kept_per_layer)."""
+    import torch
+    L = load()
+    cd = desc.c()
+    dev = x_in.device
+    nl = len(wqkv)
+    B, n = desc.B, desc.n
+    F = int(w1[0].shape[1])
+    x_out = torch.empty_like(x_in) if x_out is None else x_out
+    final_len = torch.empty((B,), dtype=torch.int32, device=dev)
+    orig = torch.empty((B, n), dtype=torch.int32, device=dev)
+    kpl = torch.empty((nl, B), dtype=torch.int32, device=dev)
+    arr = lambda ts: (ctypes.c_void_p * nl)(*[t.data_ptr() for t in ts])  # noqa: E731
+    th = (ctypes.c_float * nl)(*[float(t) for t in thresholds])
+    win = None if windows is None else (ctypes.c_int32 * nl)(*[int(w) for w in windows])
+    wsb = L.sc_encoder_stack_workspace_size(ctypes.byref(cd), nl, F)
+    ws = _ws(wsb, dev) if workspace is None else workspace
+    _check(L.sc_encoder_stack(ctypes.byref(cd), nl, win, _ptr(x_in), arr(wqkv), arr(wo), arr(w1), arr(w2), F, th,
+                              int(bool(keep_global)), ctypes.c_float(ln_eps), _ptr(x_out), _ptr(final_len),
+                              _ptr(orig), _ptr(kpl), _ptr(ws), wsb, _stream(stream)), "sc_encoder_stack")
     return x_out, final_len, orig, kpl
 
 

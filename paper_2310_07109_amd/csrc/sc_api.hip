@@ -297,12 +297,14 @@ namespace {
 
 struct StackWs {
   __bf16 *qkv, *o, *oc, *xc, *xa, *xb;
+  __bf16 *x1, *h;  // feed-forward block: attention sub-layer output, hidden activations
   float *t, *scores, *partials;
   int *len_a, *len_b, *gp_a, *gp_b, *orig_a, *orig_b, *keep_idx, *new_index;
   AttnArgs attn;
 };
 
-size_t carve_stack(const sc_attn_desc* d, void* base, StackWs* ws) {
+// Workspace of the stack; F = feed-forward width (0: attention-only layers).
+size_t carve_stack(const sc_attn_desc* d, int F, void* base, StackWs* ws) {
   const AttnGeom geo = sc::attn_geom(d->n, d->window, d->G);
   const size_t D = (size_t)d->H * d->d, bn = (size_t)d->B * d->n, G = (size_t)d->G;
   Carver c(base);
@@ -313,6 +315,8 @@ size_t carve_stack(const sc_attn_desc* d, void* base, StackWs* ws) {
   w.xc = c.take<__bf16>(bn * D);
   w.xa = c.take<__bf16>(bn * D);
   w.xb = c.take<__bf16>(bn * D);
+  w.x1 = F > 0 ? c.take<__bf16>(bn * D) : nullptr;
+  w.h = F > 0 ? c.take<__bf16>(bn * (size_t)F) : nullptr;
   w.t = c.take<float>(bn * D);
   w.scores = c.take<float>(bn);
   w.partials = c.take<float>(sc::partials_floats(d->B, d->H, d->n, geo, d->G));
@@ -324,24 +328,31 @@ size_t carve_stack(const sc_attn_desc* d, void* base, StackWs* ws) {
   w.orig_b = c.take<int>(bn);
   w.keep_idx = c.take<int>(bn);
   w.new_index = c.take<int>(bn);
+  // the attention workspace and the partials do not depend on the window
   w.attn = make_attn_args(d, geo);
   carve_attn_ws(w.attn, c);
   if (ws) *ws = w;
   return c.off;
 }
 
-}  // namespace
-
-size_t sc_encoder_attn_stack_workspace_size(const sc_attn_desc* d, int32_t n_layers) {
-  if (check_desc(d) != SC_OK || n_layers < 1) return 0;
-  return carve_stack(d, nullptr, nullptr);
+// The window-dependent geometry of the attention arguments.
+void set_window(AttnArgs& a, int n, int window, int G) {
+  const AttnGeom geo = sc::attn_geom(n, window, G);
+  a.r = geo.r;
+  a.nqb = geo.nqb;
+  a.rwp = geo.rwp;
+  a.rb = geo.rb;
+  a.bw = geo.bw;
+  a.nkb = geo.nkb;
 }
 
-sc_status sc_encoder_attn_stack(const sc_attn_desc* d, int32_t n_layers, const void* x_in,
-                                const void* const* Wqkv, const void* const* Wo, const float* thresholds,
-                                int32_t keep_global, float ln_eps, void* x_out, int32_t* final_len,
-                                int32_t* orig_idx, int32_t* kept_per_layer, void* workspace, size_t ws_bytes,
-                                void* stream) {
+// Layers of the stack: windows (host, NULL = desc->window for every layer);
+// W1 / W2 NULL = attention-only layers, else feed-forward width F.
+sc_status run_stack(const sc_attn_desc* d, int32_t n_layers, const int32_t* windows, const void* x_in,
+                    const void* const* Wqkv, const void* const* Wo, const void* const* W1, const void* const* W2,
+                    int32_t F, const float* thresholds, int32_t keep_global, float ln_eps, void* x_out,
+                    int32_t* final_len, int32_t* orig_idx, int32_t* kept_per_layer, void* workspace, size_t ws_bytes,
+                    void* stream) {
   sc_status st = check_desc(d);
   if (st != SC_OK) return st;
   if (d->dtype != SC_BF16) return SC_EUNSUPPORTED;
@@ -349,15 +360,20 @@ sc_status sc_encoder_attn_stack(const sc_attn_desc* d, int32_t n_layers, const v
   if ((long long)d->n * 3 * d->H * d->d * 2 >= (1LL << 32)) return SC_EUNSUPPORTED;  // fused q|k|v rows
   if (n_layers < 1 || !x_in || !Wqkv || !Wo || !thresholds || !x_out || !final_len) return SC_EINVAL;
   if (!(ln_eps > 0.f) || !std::isfinite(ln_eps)) return SC_EINVAL;
-  for (int l = 0; l < n_layers; ++l)
+  const bool ffn = W1 != nullptr;
+  if (ffn && (!W2 || F <= 0 || F % 8 != 0)) return SC_EINVAL;
+  for (int l = 0; l < n_layers; ++l) {
     if (!Wqkv[l] || !Wo[l]) return SC_EINVAL;
-  const size_t need = sc_encoder_attn_stack_workspace_size(d, n_layers);
+    if (ffn && (!W1[l] || !W2[l])) return SC_EINVAL;
+    if (windows && windows[l] < 0) return SC_EINVAL;
+  }
+  const size_t need = carve_stack(d, ffn ? F : 0, nullptr, nullptr);
   if (!workspace || ws_bytes < need) return SC_EWORKSPACE;
   const size_t D = (size_t)d->H * d->d, bn = (size_t)d->B * d->n, xb = bn * D * 2;
   if (overlaps(x_out, xb, x_in, xb) || overlaps(x_out, xb, workspace, need) || overlaps(x_in, xb, workspace, need))
     return SC_EINVAL;
   StackWs w;
-  carve_stack(d, workspace, &w);
+  carve_stack(d, ffn ? F : 0, workspace, &w);
   hipStream_t s = static_cast<hipStream_t>(stream);
   const int B = d->B, n = d->n, H = d->H, G = d->G, Di = (int)D;
   bool ok = true;
@@ -369,11 +385,13 @@ sc_status sc_encoder_attn_stack(const sc_attn_desc* d, int32_t n_layers, const v
   chk(sc::launch_iota_orig(d->valid_len, orig_cur, B, n, s));
   const __bf16* cur = static_cast<const __bf16*>(x_in);
   for (int l = 0; l < n_layers && ok; ++l) {
+    const int window = windows ? windows[l] : d->window;
     __bf16* nxt = (l == n_layers - 1) ? static_cast<__bf16*>(x_out) : ((l & 1) ? w.xb : w.xa);
     // a1: qkv projection of the surviving rows
-    chk(sc::launch_gemm_bf16(cur, Wqkv[l], w.qkv, 0, B, n, Di, 3 * Di, len_cur, s));
+    chk(sc::launch_gemm_bf16(cur, Wqkv[l], w.qkv, sc::kGemmBf16, B, n, Di, 3 * Di, len_cur, s));
     // a2-a5: sparse attention reading q|k|v out of the fused projection
     AttnArgs a = w.attn;
+    set_window(a, n, window, G);
     a.q = w.qkv;
     a.k = w.qkv + D;
     a.v = w.qkv + 2 * D;
@@ -388,7 +406,7 @@ sc_status sc_encoder_attn_stack(const sc_attn_desc* d, int32_t n_layers, const v
     set_partials(a, w.partials);
     chk(sc::launch_window_attention(SC_BF16, a, s));
     // a6: importance scores
-    const AttnGeom geo = sc::attn_geom(n, d->window, G);
+    const AttnGeom geo = sc::attn_geom(n, window, G);
     chk(sc::launch_score_from_partials(w.partials, len_cur, G > 0 ? gp_cur : nullptr, B, n, H, G, geo, w.scores, s));
     // a7-a8: threshold, scan, gather of O and of the residual input
     sc::PruneArgs p;
@@ -423,8 +441,16 @@ sc_status sc_encoder_attn_stack(const sc_attn_desc* d, int32_t n_layers, const v
     ga.new_len = len_nxt;
     chk(sc::launch_gather(ga, s));
     // a9: output projection, residual, LayerNorm on the survivors
-    chk(sc::launch_gemm_bf16(w.oc, Wo[l], w.t, 1, B, n, Di, Di, len_nxt, s));
-    chk(sc::launch_residual_layernorm(w.xc, w.t, nxt, B, n, Di, ln_eps, len_nxt, s));
+    chk(sc::launch_gemm_bf16(w.oc, Wo[l], w.t, sc::kGemmF32, B, n, Di, Di, len_nxt, s));
+    if (!ffn) {
+      chk(sc::launch_residual_layernorm(w.xc, w.t, nxt, B, n, Di, ln_eps, len_nxt, s));
+    } else {
+      // feed-forward block: h = GELU(x1 . W1), then LayerNorm(x1 + h . W2)
+      chk(sc::launch_residual_layernorm(w.xc, w.t, w.x1, B, n, Di, ln_eps, len_nxt, s));
+      chk(sc::launch_gemm_bf16(w.x1, W1[l], w.h, sc::kGemmGeluBf16, B, n, Di, F, len_nxt, s));
+      chk(sc::launch_gemm_bf16(w.h, W2[l], w.t, sc::kGemmF32, B, n, F, Di, len_nxt, s));
+      chk(sc::launch_residual_layernorm(w.x1, w.t, nxt, B, n, Di, ln_eps, len_nxt, s));
+    }
     if (kept_per_layer) chk(sc::launch_record_len(len_nxt, kept_per_layer + (size_t)l * B, B, s));
     cur = nxt;
     int* tmp;
@@ -435,6 +461,37 @@ sc_status sc_encoder_attn_stack(const sc_attn_desc* d, int32_t n_layers, const v
   chk(sc::launch_copy_i32(len_cur, final_len, B, s));
   if (orig_idx) chk(sc::launch_copy_i32(orig_cur, orig_idx, (long long)bn, s));
   return ok ? SC_OK : SC_EHIP;
+}
+
+}  // namespace
+
+size_t sc_encoder_attn_stack_workspace_size(const sc_attn_desc* d, int32_t n_layers) {
+  if (check_desc(d) != SC_OK || n_layers < 1) return 0;
+  return carve_stack(d, 0, nullptr, nullptr);
+}
+
+sc_status sc_encoder_attn_stack(const sc_attn_desc* d, int32_t n_layers, const void* x_in,
+                                const void* const* Wqkv, const void* const* Wo, const float* thresholds,
+                                int32_t keep_global, float ln_eps, void* x_out, int32_t* final_len,
+                                int32_t* orig_idx, int32_t* kept_per_layer, void* workspace, size_t ws_bytes,
+                                void* stream) {
+  return run_stack(d, n_layers, nullptr, x_in, Wqkv, Wo, nullptr, nullptr, 0, thresholds, keep_global, ln_eps, x_out,
+                   final_len, orig_idx, kept_per_layer, workspace, ws_bytes, stream);
+}
+
+size_t sc_encoder_stack_workspace_size(const sc_attn_desc* d, int32_t n_layers, int32_t ffn_dim) {
+  if (check_desc(d) != SC_OK || n_layers < 1 || ffn_dim <= 0) return 0;
+  return carve_stack(d, ffn_dim, nullptr, nullptr);
+}
+
+sc_status sc_encoder_stack(const sc_attn_desc* d, int32_t n_layers, const int32_t* windows, const void* x_in,
+                           const void* const* Wqkv, const void* const* Wo, const void* const* W1,
+                           const void* const* W2, int32_t ffn_dim, const float* thresholds, int32_t keep_global,
+                           float ln_eps, void* x_out, int32_t* final_len, int32_t* orig_idx, int32_t* kept_per_layer,
+                           void* workspace, size_t ws_bytes, void* stream) {
+  if (!W1 || !W2) return SC_EINVAL;
+  return run_stack(d, n_layers, windows, x_in, Wqkv, Wo, W1, W2, ffn_dim, thresholds, keep_global, ln_eps, x_out,
+                   final_len, orig_idx, kept_per_layer, workspace, ws_bytes, stream);
 }
 
 sc_status sc_profile_window_kernel(int32_t enable) {

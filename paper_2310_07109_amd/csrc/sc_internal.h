@@ -92,7 +92,9 @@ hipError_t launch_gather(const GatherArgs& g, hipStream_t s);
 // Stack pieces.
 // y[rows, N] = x[rows, K] . W[K, N] (bf16 in, fp32 accumulate), rows of
 // sequence b limited to len[b] (others untouched); output bf16 or fp32.
-hipError_t launch_gemm_bf16(const void* x, const void* w, void* y, int out_f32, int B, int n, int K, int N,
+// GEMM epilogues: bf16 store, fp32 store, GELU then bf16 store.
+constexpr int kGemmBf16 = 0, kGemmF32 = 1, kGemmGeluBf16 = 2;
+hipError_t launch_gemm_bf16(const void* x, const void* w, void* y, int mode, int B, int n, int K, int N,
                             const int* len, hipStream_t s);
 // y = bf16(LayerNorm(x_res + t)) per row, rows of sequence b < len[b].
 hipError_t launch_residual_layernorm(const void* x_res, const float* t, void* y, int B, int n, int D, float eps,

@@ -8,7 +8,9 @@
 //               [K, N] (as stored by the caller), so its tile is transposed
 //               while it is written to LDS to give each lane 8 consecutive k.
 //               Rows of sequence b at or beyond len[b] are skipped: the GEMM
-//               runs on the surviving tokens only.
+//               runs on the surviving tokens only.  Epilogue: bf16 store,
+//               fp32 store, or GELU (exact form, x * Phi(x)) then bf16 store
+//               for the first feed-forward product.
 // k_residual_ln y = bf16(LayerNorm(x + t)), one wavefront per row, fp32
 //               statistics (biased variance), gamma = 1, beta = 0.
 #include "sc_device.h"
@@ -20,8 +22,10 @@ namespace {
 constexpr int kBM = 128, kBN = 128, kBKg = 32;
 constexpr int kGPitch = kBKg + 8;  // 80-byte rows: 16 consecutive rows hit distinct banks
 
+SC_DEV float gelu_exact(float v) { return 0.5f * v * (1.0f + erff(v * 0.70710678118654752f)); }
+
 __global__ __launch_bounds__(256) void k_gemm_bf16(const __bf16* __restrict__ X, const __bf16* __restrict__ W,
-                                                   void* __restrict__ Y, int out_f32, int n, int K, int N,
+                                                   void* __restrict__ Y, int mode, int n, int K, int N,
                                                    const int* __restrict__ len) {
   __shared__ __attribute__((aligned(16))) __bf16 sX[kBM * kGPitch];
   __shared__ __attribute__((aligned(16))) __bf16 sW[kBN * kGPitch];  // transposed: [col][k]
@@ -93,8 +97,10 @@ __global__ __launch_bounds__(256) void k_gemm_bf16(const __bf16* __restrict__ X,
         const int col = n0 + wn + 16 * j + lr;
         if (col >= N) continue;
         const long long off = ((long long)b * n + m) * N + col;
-        if (out_f32)
+        if (mode == kGemmF32)
           static_cast<float*>(Y)[off] = acc[i][j][e];
+        else if (mode == kGemmGeluBf16)
+          static_cast<__bf16*>(Y)[off] = (__bf16)gelu_exact(acc[i][j][e]);
         else
           static_cast<__bf16*>(Y)[off] = (__bf16)acc[i][j][e];
       }
@@ -146,11 +152,11 @@ __global__ void k_record_len(const int* len, int* dst, int B) {
 
 }  // namespace
 
-hipError_t launch_gemm_bf16(const void* x, const void* w, void* y, int out_f32, int B, int n, int K, int N,
+hipError_t launch_gemm_bf16(const void* x, const void* w, void* y, int mode, int B, int n, int K, int N,
                             const int* len, hipStream_t s) {
   dim3 grid((N + kBN - 1) / kBN, (n + kBM - 1) / kBM, B);
   hipLaunchKernelGGL(k_gemm_bf16, grid, dim3(256), 0, s, static_cast<const __bf16*>(x),
-                     static_cast<const __bf16*>(w), y, out_f32, n, K, N, len);
+                     static_cast<const __bf16*>(w), y, mode, n, K, N, len);
   return hipGetLastError();
 }
 

@@ -25,6 +25,7 @@ _M2 = np.uint64(0x94D049BB133111EB)
 S_Q, S_K, S_V, S_LEN, S_GLOB, S_SPIKE_U, S_SPIKE_V, S_X = 1, 2, 3, 4, 5, 6, 7, 8
 S_SPIKE_UQ = 9
 S_WQKV0, S_WO0 = 100, 101  # + 2 * layer
+S_W10, S_W20 = 300, 301      # + 2 * layer (feed-forward block)
 
 
 def _mix(z: np.ndarray) -> np.ndarray:
@@ -131,6 +132,8 @@ class StackConfig:
     w_std: float
     theta_max: float
     alpha: float = 0.125
+    ffn_dim: int = 0            # feed-forward width (0: attention-only layers)
+    windows: tuple = ()         # per-layer windows (empty: `window` in every layer)
     ln_eps: float = 1e-5
 
     @property
@@ -164,6 +167,11 @@ CONFIGS["5b"] = AttnConfig("bf16 three prune passes B2 n8192 H16 w1024 G64 QK-sp
 
 STACK_CONFIG = StackConfig("bf16 12-layer attention stack B16 n2048 D768 w512", 2, 16, 2048, 12, 64, 12, 512,
                            (256, 2048), 1, 0.02, 0.01)
+# Full RoBERTa-base-shaped encoder: the attention stack's inputs and weights (same seed) plus a 3072-wide GELU
+# feed-forward block per layer, and windows growing with depth (small in lower layers, large in higher ones).
+STACK_FULL_CONFIG = StackConfig("bf16 12-layer encoder B16 n2048 D768 FFN3072 windows 64-512", 2, 16, 2048, 12, 64,
+                                12, 512, (256, 2048), 1, 0.02, 0.01, ffn_dim=3072,
+                                windows=(64, 64, 128, 128, 256, 256, 512, 512, 512, 512, 512, 512))
 
 
 def lengths(seed: int, B: int, lo: int, hi: int, dist: tuple = ()) -> np.ndarray:
@@ -267,11 +275,23 @@ def make_stack_inputs(cfg: StackConfig, seed: int | None = None, B=None, n=None,
         s, e = quantise(b, "bf16")
         wo.append(s)
         wo64.append(e)
+    w1, w1_64, w2, w2_64 = [], [], [], []
+    for l in range(nl if cfg.ffn_dim > 0 else 0):
+        F = cfg.ffn_dim
+        a = normal(seed, S_W10 + 2 * l, D * F).reshape(D, F) * cfg.w_std
+        b = normal(seed, S_W20 + 2 * l, F * D).reshape(F, D) * cfg.w_std
+        s, e = quantise(a, "bf16")
+        w1.append(s)
+        w1_64.append(e)
+        s, e = quantise(b, "bf16")
+        w2.append(s)
+        w2_64.append(e)
     vl = lengths(seed, B, lo, hi)
     gp = global_positions(seed, vl, cfg.n_global, "first")
+    windows = list(cfg.windows[:nl]) if cfg.windows else [cfg.window] * nl
     return dict(B=B, n=n, H=H, d=cfg.d, D=D, n_layers=nl, window=cfg.window, G=cfg.n_global, alpha=cfg.alpha,
                 ln_eps=cfg.ln_eps, x=xs, x64=x64, wqkv=wqkv, wqkv64=wqkv64, wo=wo, wo64=wo64, valid_len=vl,
-                global_pos=gp)
+                global_pos=gp, w1=w1, w1_64=w1_64, w2=w2, w2_64=w2_64, windows=windows)
 
 
 def paper_threshold_schedule(final_threshold: float, n_layers: int):

@@ -25,7 +25,7 @@ def declared_functions():
 def test_exports_every_declared_symbol():
     L = sc.load()
     names = declared_functions()
-    assert len(names) == 14
+    assert len(names) == 16
     for name in names:
         assert hasattr(L, name), name
 
@@ -149,6 +149,27 @@ def test_topk_validation():
     for bad in (-0.01, 1.01, float("nan"), float("inf")):
         assert call(bad) == B.SC_EINVAL
     assert call(0.5, ws=None) == B.SC_EWORKSPACE
+
+
+def test_full_stack_validation():
+    L = sc.load()
+    cd = desc().c()
+    w = (ctypes.c_void_p * 1)(0x5000000)
+    th = (ctypes.c_float * 1)(0.0)
+
+    def call(W1=w, W2=w, F=64, windows=None, ws=0x900000):
+        return L.sc_encoder_stack(ctypes.byref(cd), 1, windows, 0x100000, w, w, W1, W2, F, th, 1,
+                                  ctypes.c_float(1e-5), 0x200000, 0x300000, None, None, ws, 1 << 30, None)
+
+    assert call(W1=None) == B.SC_EINVAL
+    assert call(W2=None) == B.SC_EINVAL
+    assert call(F=0) == B.SC_EINVAL
+    assert call(F=12) == B.SC_EINVAL                       # not a multiple of 8
+    assert call(windows=(ctypes.c_int32 * 1)(-1)) == B.SC_EINVAL
+    assert call(ws=None) == B.SC_EWORKSPACE
+    d = desc()
+    assert sc.sc_encoder_stack_workspace_size(d, 2, 3072) > sc.sc_encoder_attn_stack_workspace_size(d, 2)
+    assert sc.sc_encoder_stack_workspace_size(d, 2, 0) == 0
 
 
 def test_score_and_stack_validation():

@@ -24,10 +24,13 @@ def to_f64(t):
     return t.float().cpu().numpy().astype(np.float64)
 
 
-def run_layer(x_t, wq_t, wo_t, vl, gp, H, window, alpha, theta):
+def run_layer(x_t, wq_t, wo_t, vl, gp, H, window, alpha, theta, w1_t=None, w2_t=None):
     B, n, D = x_t.shape
     d = sc.Desc(B, n, H, window, dev_i32(vl), dev_i32(gp), alpha, sc.SC_BF16)
-    y, fl, orig, kpl = sc.sc_encoder_attn_stack(d, x_t, [wq_t], [wo_t], [theta])
+    if w1_t is None:
+        y, fl, orig, kpl = sc.sc_encoder_attn_stack(d, x_t, [wq_t], [wo_t], [theta])
+    else:
+        y, fl, orig, kpl = sc.sc_encoder_stack(d, x_t, [wq_t], [wo_t], [w1_t], [w2_t], [theta], windows=[window])
     torch.cuda.synchronize()
     return y, fl.cpu().numpy(), orig.cpu().numpy()
 
@@ -42,18 +45,27 @@ def remap_globals(gp, orig, new_len):
     return out
 
 
-def layerwise(x_bits, wq_bits, wo_bits, vl, gp, H, window, alpha, thetas, seqs=None, tag=""):
-    """Run the stack one layer at a time on the GPU; check each layer against the oracle on `seqs`."""
+def layerwise(x_bits, wq_bits, wo_bits, vl, gp, H, window, alpha, thetas, seqs=None, tag="", w1_bits=None,
+              w2_bits=None, windows=None):
+    """Run the stack one layer at a time on the GPU; check each layer against the oracle on `seqs`.
+    w1_bits / w2_bits: feed-forward weights per layer (full layers); windows: one per layer."""
     x_t = bf16_dev(x_bits)
     seqs = list(range(x_bits.shape[0])) if seqs is None else seqs
     excluded_total = 0
     for l, theta in enumerate(thetas):
         wq_t, wo_t = bf16_dev(wq_bits[l]), bf16_dev(wo_bits[l])
-        y_t, nl, orig = run_layer(x_t, wq_t, wo_t, vl, gp, H, window, alpha, theta)
+        win = windows[l] if windows is not None else window
+        ffn = {}
+        if w1_bits is not None:
+            ffn = dict(w1=si.bf16_bits_to_f64(w1_bits[l]), w2=si.bf16_bits_to_f64(w2_bits[l]))
+            y_t, nl, orig = run_layer(x_t, wq_t, wo_t, vl, gp, H, win, alpha, theta, bf16_dev(w1_bits[l]),
+                                      bf16_dev(w2_bits[l]))
+        else:
+            y_t, nl, orig = run_layer(x_t, wq_t, wo_t, vl, gp, H, win, alpha, theta)
         x64 = to_f64(x_t)[seqs]
         ry, rk, rnl, rngp, rs = oracle.encoder_layer(x64, si.bf16_bits_to_f64(wq_bits[l]),
-                                                     si.bf16_bits_to_f64(wo_bits[l]), vl[seqs], gp[seqs], H, window,
-                                                     alpha, theta)
+                                                     si.bf16_bits_to_f64(wo_bits[l]), vl[seqs], gp[seqs], H, win,
+                                                     alpha, theta, **ffn)
         y = to_f64(y_t)
         for i, b in enumerate(seqs):
             L = int(vl[b])
@@ -64,7 +76,8 @@ def layerwise(x_bits, wq_bits, wo_bits, vl, gp, H, window, alpha, thetas, seqs=N
             excluded_total += len(near - g)
             assert set(kept_gpu) - near == set(kept_ref) - near, f"layer {l} seq {b}: kept sets differ"
             if set(kept_gpu) == set(kept_ref):
-                check_out(y[b, :nl[b]], ry[i, :rnl[i]], "bf16", what=f"layer {l} seq {b} hidden")
+                check_out(y[b, :nl[b]], ry[i, :rnl[i]], "bf16", what=f"layer {l} seq {b} hidden",
+                          bf16_step=w1_bits is not None)
         log(f"{tag} layer {l}: theta {theta:.5f} kept {nl.tolist()} (near-theta excluded so far {excluded_total})")
         gp = remap_globals(gp, orig, nl)
         vl = nl.astype(np.int32)
@@ -122,3 +135,59 @@ def test_config3_stack_sampled_sequences():
     log(f"config 3: lengths {vl.tolist()}, oracle on sequences {seqs}")
     layerwise(inp["x"], inp["wqkv"], inp["wo"], vl, inp["global_pos"], cfg.H, cfg.window, cfg.alpha,
               cfg.thresholds(), seqs=seqs, tag="config 3")
+
+
+def test_small_full_stack_layerwise_and_chained():
+    """Full layers (GELU feed-forward block) with a window per layer, layer by layer against the oracle; the
+    multi-layer call equals the chain of single-layer calls bit for bit."""
+    cfg = si.StackConfig("small full", 23, 3, 300, 2, 64, 4, 64, (120, 300), 1, 0.05, 0.012, ffn_dim=512,
+                         windows=(8, 32, 64, 600))
+    inp = si.make_stack_inputs(cfg)
+    inp["valid_len"][2] = 1
+    inp["global_pos"] = si.global_positions(cfg.seed, inp["valid_len"], 1, "first")
+    thetas = [0.0, 0.004, 0.008, 0.012]
+    xl, vl_final = layerwise(inp["x"], inp["wqkv"], inp["wo"], inp["valid_len"], inp["global_pos"], cfg.H,
+                             cfg.window, cfg.alpha, thetas, tag="small full", w1_bits=inp["w1"], w2_bits=inp["w2"],
+                             windows=inp["windows"])
+    d = sc.Desc(cfg.B, cfg.n, cfg.H, cfg.window, dev_i32(inp["valid_len"]), dev_i32(inp["global_pos"]), cfg.alpha,
+                sc.SC_BF16)
+    dv = lambda ws: [bf16_dev(w) for w in ws]  # noqa: E731
+    y, fl, orig, kpl = sc.sc_encoder_stack(d, bf16_dev(inp["x"]), dv(inp["wqkv"]), dv(inp["wo"]), dv(inp["w1"]),
+                                           dv(inp["w2"]), thetas, windows=inp["windows"])
+    fl = fl.cpu().numpy()
+    assert np.array_equal(fl, vl_final)
+    for b in range(cfg.B):
+        assert torch.equal(y[b, :fl[b]].view(torch.int16), xl[b, :fl[b]].view(torch.int16))
+
+
+def test_full_stack_unpruned_against_oracle_stack():
+    cfg = si.StackConfig("nop full", 24, 2, 130, 2, 64, 3, 32, (100, 130), 1, 0.05, 0.0, ffn_dim=256,
+                         windows=(16, 48, 32))
+    inp = si.make_stack_inputs(cfg)
+    d = sc.Desc(cfg.B, cfg.n, cfg.H, cfg.window, dev_i32(inp["valid_len"]), dev_i32(inp["global_pos"]), cfg.alpha,
+                sc.SC_BF16)
+    dv = lambda ws: [bf16_dev(w) for w in ws]  # noqa: E731
+    y, fl, orig, kpl = sc.sc_encoder_stack(d, bf16_dev(inp["x"]), dv(inp["wqkv"]), dv(inp["wo"]), dv(inp["w1"]),
+                                           dv(inp["w2"]), [-1.0] * 3, windows=inp["windows"])
+    assert np.array_equal(fl.cpu().numpy(), inp["valid_len"])
+    ry, rfl, roi, rkpl = oracle.encoder_stack(inp["x64"], inp["wqkv64"], inp["wo64"], inp["valid_len"],
+                                              inp["global_pos"], cfg.H, inp["windows"], cfg.alpha, [-1.0] * 3,
+                                              w1_list=inp["w1_64"], w2_list=inp["w2_64"])
+    yy = to_f64(y)
+    for b in range(cfg.B):
+        L = int(inp["valid_len"][b])
+        check_out(yy[b, :L], ry[b, :L], "bf16", what="unpruned full stack", bf16_step=True)
+
+
+def test_full_encoder_config_sampled_sequences():
+    """RoBERTa-base-shaped full encoder (FFN 3072, windows 64..512), B16 n2048: all sequences on the GPU, the
+    oracle on a sample of sequences, layer by layer."""
+    cfg = si.STACK_FULL_CONFIG
+    log("full encoder: generating inputs")
+    inp = si.make_stack_inputs(cfg)
+    vl = inp["valid_len"]
+    seqs = [int(np.argmin(vl)), int(np.argmax(vl))]
+    log(f"full encoder: lengths {vl.tolist()}, oracle on sequences {seqs}")
+    layerwise(inp["x"], inp["wqkv"], inp["wo"], vl, inp["global_pos"], cfg.H, cfg.window, cfg.alpha,
+              cfg.thresholds(), seqs=seqs, tag="full encoder", w1_bits=inp["w1"], w2_bits=inp["w2"],
+              windows=inp["windows"])
