@@ -72,6 +72,32 @@ SC_DEV i16x4 lds_read_tr16(const void* p) {
       (__attribute__((address_space(3))) i16x4*)(const_cast<void*>(p)));
 }
 
+// The lane id, opaque to the compiler: values derived from it are
+// recomputed where they are used instead of being hoisted out of the tile
+// loops and held in registers across them.
+SC_DEV int opaque_lane() {
+  int lane;
+  asm volatile("v_mbcnt_lo_u32_b32 %0, -1, 0\n\tv_mbcnt_hi_u32_b32 %0, -1, %0" : "=v"(lane));
+  return lane;
+}
+
+// One direct load: lane i's 16 bytes at base + voff land at LDS byte address
+// lds + 16 i (gfx950 global_load_lds_dwordx4, destination base in m0).  Inline
+// assembly on purpose: the compiler cannot tell these writes from later LDS
+// reads of the other tile buffer and would wait for them before every read;
+// here they are completed explicitly by wait_dma() before the barrier that
+// publishes the tile.
+SC_DEV unsigned lds_addr(const void* p) {
+  return (unsigned)(size_t)(const __attribute__((address_space(3))) void*)p;
+}
+SC_DEV void lds_dma16(const void* base, unsigned voff, unsigned lds) {
+  asm volatile("s_mov_b32 m0, %2\n\ts_nop 0\n\tglobal_load_lds_dwordx4 %0, %1"
+               :
+               : "v"(voff), "s"(base), "s"(lds)
+               : "memory", "m0");
+}
+SC_DEV void wait_dma() { asm volatile("s_waitcnt vmcnt(0)" ::: "memory"); }
+
 // Workgroups are dispatched round-robin over the 8 XCDs (each with its own
 // L2): workgroup i runs on XCD i % 8.  For a grid of `pairs` x `inner`
 // blocks (a (sequence, head) pair and its query or key blocks), block i is

@@ -11,6 +11,21 @@
 //               runs on the surviving tokens only.  Epilogue: bf16 store,
 //               fp32 store, or GELU (exact form, x * Phi(x)) then bf16 store
 //               for the first feed-forward product.
+// k_gemm_v2     the same product when K % 64 == 0 and N % 128 == 0 (the
+//               encoder's shapes): 128 x 128 workgroup tile, K stages of 64
+//               brought into LDS by gfx950's direct global->LDS loads, double
+//               buffered.  X rows are stored as 128-byte rows whose 16-byte
+//               units are XOR-swizzled by the row's low 3 bits and read as
+//               16-byte A fragments; W stays row-major ([k][n], 256-byte rows,
+//               units swizzled by twice the row's low 3 bits) and the B
+//               fragments (8 consecutive k of one column) come from transposing
+//               LDS reads (ds_read_b64_tr_b16).  Those reads hand each lane the
+//               rows 4g..4g+3 and 16+4g..16+4g+3 of a 32-row chunk, so W's rows
+//               are loaded into that order and the lane receives k = 8g..8g+7.
+//               All N tiles of one M tile run on one XCD (X is fetched once);
+//               M tile t of sequence b goes to XCD (t + b) mod 8, so that the
+//               first tiles of the sequences (often the only live ones after
+//               pruning) spread over the XCDs.
 // k_residual_ln y = bf16(LayerNorm(x + t)), one wavefront per row, fp32
 //               statistics (biased variance), gamma = 1, beta = 0.
 #include "sc_device.h"
@@ -107,6 +122,123 @@ __global__ __launch_bounds__(256) void k_gemm_bf16(const __bf16* __restrict__ X,
     }
 }
 
+constexpr int kGK = 64;  // k per stage of k_gemm_v2
+
+struct GemmSmem {
+  __attribute__((aligned(16))) __bf16 x[2][kBM * kGK];  // [row][k], 128-byte rows
+  __attribute__((aligned(16))) __bf16 w[2][kGK * kBN];  // [k][n], 256-byte rows
+};
+
+SC_DEV int gx_off(int row, int unit) { return row * kGK + 8 * (unit ^ (row & 7)); }
+SC_DEV int gw_off(int row, int unit) { return row * kBN + 8 * (unit ^ (2 * (row & 7))); }
+// W row held by LDS row r of a stage: within each 32-row chunk, LDS row
+// 4g + t holds k = 8g + t and LDS row 16 + 4g + t holds k = 8g + 4 + t.
+SC_DEV int gw_krow(int r) { return (r & ~31) + 8 * ((r & 15) >> 2) + 4 * ((r >> 4) & 1) + (r & 3); }
+
+SC_DEV void gemm_store(void* Y, int mode, long long off, float v) {
+  if (mode == kGemmF32)
+    static_cast<float*>(Y)[off] = v;
+  else if (mode == kGemmGeluBf16)
+    static_cast<__bf16*>(Y)[off] = (__bf16)gelu_exact(v);
+  else
+    static_cast<__bf16*>(Y)[off] = (__bf16)v;
+}
+
+__global__ __launch_bounds__(256) void k_gemm_v2(const __bf16* __restrict__ X, const __bf16* __restrict__ W,
+                                                 void* __restrict__ Y, int mode, int B, int n, int K, int N,
+                                                 const int* __restrict__ len) {
+  __shared__ GemmSmem sm;
+  // block i runs on XCD i % 8 and takes the (i / 8 / Nt)-th M tile of that
+  // XCD (tiles t = (x - b) mod 8, +8, ... of sequences b = 0, 1, ...) with
+  // N tile (i / 8) % Nt
+  const int Nt = N / kBN, Mt = (n + kBM - 1) / kBM;
+  const int xcd = blockIdx.x & 7, j = blockIdx.x >> 3;
+  const int jm = j / Nt, nt = j % Nt;
+  int b = -1, t = 0;
+  for (int bb = 0, acc = 0; bb < B; ++bb) {
+    const int t0 = (xcd - bb) & 7;
+    const int cnt = t0 < Mt ? (Mt - t0 + 7) / 8 : 0;
+    if (jm < acc + cnt) {
+      b = bb;
+      t = t0 + 8 * (jm - acc);
+      break;
+    }
+    acc += cnt;
+  }
+  if (b < 0) return;
+  const int m0 = t * kBM, n0 = nt * kBN;
+  const int rows = len ? clampi(len[b], 0, n) : n;
+  if (m0 >= rows) return;
+  const int tid = threadIdx.x, lane = tid & 63, w = __builtin_amdgcn_readfirstlane(tid >> 6), g = lane >> 4,
+            lr = lane & 15;
+  const int wm = (w >> 1) * 64, wn = (w & 1) * 64;
+  const __bf16* Xb = X + (long long)b * n * K;
+  const unsigned xrow_b = 2u * (unsigned)K, wrow_b = 2u * (unsigned)N;  // byte offsets fit in 32 bits (host)
+  auto issue = [&](int k0, int bf) {
+    const int ln = opaque_lane();
+#pragma unroll
+    for (int t = 0; t < 4; ++t) {  // X: wave w fills rows 32w .. 32w+31, 8 rows per load
+      const int R0 = 32 * w + 8 * t, R = R0 + (ln >> 3);
+      const int u = (ln & 7) ^ (R & 7);
+      const int gr = min(m0 + R, rows - 1);
+      lds_dma16(Xb, (unsigned)gr * xrow_b + 2u * (unsigned)(k0 + 8 * u), lds_addr(sm.x[bf] + R0 * kGK));
+    }
+#pragma unroll
+    for (int t = 0; t < 4; ++t) {  // W: wave w fills rows 16w .. 16w+15, 4 rows per load
+      const int R0 = 16 * w + 4 * t, R = R0 + (ln >> 4);
+      const int u = (ln & 15) ^ (2 * (R & 7));
+      lds_dma16(W, (unsigned)(k0 + gw_krow(R)) * wrow_b + 2u * (unsigned)(n0 + 8 * u), lds_addr(sm.w[bf] + R0 * kBN));
+    }
+  };
+  f32x4 acc[4][4];
+#pragma unroll
+  for (int i = 0; i < 4; ++i)
+#pragma unroll
+    for (int jn = 0; jn < 4; ++jn) acc[i][jn] = f32x4{0.f, 0.f, 0.f, 0.f};
+  const int nk = K / kGK;
+  issue(0, 0);
+  wait_dma();
+  __syncthreads();
+  for (int s = 0; s < nk; ++s) {
+    const int bf = s & 1;
+    if (s + 1 < nk) issue((s + 1) * kGK, bf ^ 1);
+    const __bf16* sx = sm.x[bf];
+    const __bf16* sw = sm.w[bf];
+#pragma unroll
+    for (int kc = 0; kc < 2; ++kc) {
+      bf16x8 af[4], bfr[4];
+#pragma unroll
+      for (int i = 0; i < 4; ++i) af[i] = *reinterpret_cast<const bf16x8*>(sx + gx_off(wm + 16 * i + lr, 4 * kc + g));
+      const int vr = 32 * kc + 4 * g + (lr >> 2), bsel = (lr >> 1) & 1, e = 4 * (lr & 1);
+#pragma unroll
+      for (int jn = 0; jn < 4; ++jn) {
+        const int U = 2 * ((wn >> 4) + jn) + bsel;
+        const i16x4 a0 = lds_read_tr16(sw + gw_off(vr, U) + e);
+        const i16x4 a1 = lds_read_tr16(sw + gw_off(vr + 16, U) + e);
+        bfr[jn] = __builtin_bit_cast(bf16x8, __builtin_shufflevector(a0, a1, 0, 1, 2, 3, 4, 5, 6, 7));
+      }
+#pragma unroll
+      for (int i = 0; i < 4; ++i)
+#pragma unroll
+        for (int jn = 0; jn < 4; ++jn)
+          acc[i][jn] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(af[i], bfr[jn], acc[i][jn], 0, 0, 0);
+    }
+    if (s + 1 < nk) wait_dma();
+    __syncthreads();
+  }
+  // result (row wm + 16i + 4g + e, col wn + 16jn + lr)
+#pragma unroll
+  for (int i = 0; i < 4; ++i)
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+      const int m = m0 + wm + 16 * i + 4 * g + e;
+      if (m >= rows) continue;
+#pragma unroll
+      for (int jn = 0; jn < 4; ++jn)
+        gemm_store(Y, mode, ((long long)b * n + m) * N + n0 + wn + 16 * jn + lr, acc[i][jn][e]);
+    }
+}
+
 __global__ __launch_bounds__(256) void k_residual_ln(const __bf16* __restrict__ xr, const float* __restrict__ t,
                                                      __bf16* __restrict__ y, int B, int n, int D, float eps,
                                                      const int* __restrict__ len) {
@@ -154,6 +286,15 @@ __global__ void k_record_len(const int* len, int* dst, int B) {
 
 hipError_t launch_gemm_bf16(const void* x, const void* w, void* y, int mode, int B, int n, int K, int N,
                             const int* len, hipStream_t s) {
+  if (K % kGK == 0 && N % kBN == 0 && K > 0 && N > 0 && (long long)n * K * 2 < (1LL << 32) &&
+      (long long)K * N * 2 < (1LL << 32)) {
+    // per XCD at most B * ceil(Mt / 8) M tiles
+    const long long per_xcd = (long long)B * (((n + kBM - 1) / kBM + 7) / 8);
+    const long long blocks = 8 * (long long)(N / kBN) * per_xcd;
+    hipLaunchKernelGGL(k_gemm_v2, dim3((unsigned)blocks), dim3(256), 0, s, static_cast<const __bf16*>(x),
+                       static_cast<const __bf16*>(w), y, mode, B, n, K, N, len);
+    return hipGetLastError();
+  }
   dim3 grid((N + kBN - 1) / kBN, (n + kBM - 1) / kBM, B);
   hipLaunchKernelGGL(k_gemm_bf16, grid, dim3(256), 0, s, static_cast<const __bf16*>(x),
                      static_cast<const __bf16*>(w), y, mode, n, K, N, len);
