@@ -45,6 +45,7 @@ def lib():
         L.orc_round_bf16.restype = cd
         L.orc_sparse_attention.argtypes = [ci, ci, ci, ci, ci, ci, i32p, i32p, cd, f64p, f64p, f64p, f64p, f64p,
                                            f64p, f64p, ci]
+        L.orc_sparse_attention_causal.argtypes = L.orc_sparse_attention.argtypes
         L.orc_ltp_prune.argtypes = [ci, ci, ci, i32p, i32p, f32p, cf, ci, i32p, i32p, i32p, i32p, i32p]
         L.orc_topk_prune.argtypes = [ci, ci, ci, i32p, i32p, f32p, cf, ci, i32p, i32p, i32p, i32p, i32p]
         L.orc_gather_rows.argtypes = [ci, ci, cl, vp, vp, i32p, i32p]
@@ -56,7 +57,7 @@ def lib():
                                             cf, ci, cd, f64p, i32p, i32p, i32p, f32p, ci]
         L.orc_encoder_stack_ffn.argtypes = [ci, ci, ci, ci, i32p, ci, i32p, i32p, cd, ci, f64p, f64p, f64p, f64p,
                                             f64p, ci, f32p, ci, cd, f64p, i32p, i32p, i32p, ci]
-        for f in ("orc_sparse_attention", "orc_ltp_prune", "orc_topk_prune", "orc_gather_rows", "orc_encoder_layer",
+        for f in ("orc_sparse_attention", "orc_sparse_attention_causal", "orc_ltp_prune", "orc_topk_prune", "orc_gather_rows", "orc_encoder_layer",
                   "orc_encoder_stack", "orc_encoder_layer_ffn", "orc_encoder_stack_ffn"):
             getattr(L, f).restype = ci
         _lib = L
@@ -89,8 +90,9 @@ def round_bf16(x: float) -> float:
     return lib().orc_round_bf16(float(x))
 
 
-def sparse_attention(q, k, v, valid_len, global_pos, window, alpha, want_colsum=False, nthreads=None):
-    """q, k, v: [B, n, H, d] doubles.  Returns (out, lse, scores[, colsum])."""
+def sparse_attention(q, k, v, valid_len, global_pos, window, alpha, want_colsum=False, nthreads=None, causal=False):
+    """q, k, v: [B, n, H, d] doubles.  Returns (out, lse, scores[, colsum]).  causal: keys after the query are
+    not attended."""
     q, k, v = _f64(q), _f64(k), _f64(v)
     B, n, H, d = q.shape
     gp = _i32(global_pos).reshape(B, -1)
@@ -100,7 +102,8 @@ def sparse_attention(q, k, v, valid_len, global_pos, window, alpha, want_colsum=
     lse = np.empty((B, H, n))
     scores = np.empty((B, n))
     colsum = np.empty((B, H, n)) if want_colsum else None
-    rc = lib().orc_sparse_attention(B, n, H, d, int(window), G, _p(gp, ctypes.c_int32), _p(vl, ctypes.c_int32),
+    fn = lib().orc_sparse_attention_causal if causal else lib().orc_sparse_attention
+    rc = fn(B, n, H, d, int(window), G, _p(gp, ctypes.c_int32), _p(vl, ctypes.c_int32),
                                     float(alpha), _p(q, ctypes.c_double), _p(k, ctypes.c_double),
                                     _p(v, ctypes.c_double), _p(out, ctypes.c_double), _p(lse, ctypes.c_double),
                                     _p(scores, ctypes.c_double), _p(colsum, ctypes.c_double),

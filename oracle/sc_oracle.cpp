@@ -70,9 +70,11 @@ double round_bf16(double x) {
 // The attention of one (sequence, head).  Rows are tokens; row stride is `ld`
 // doubles between consecutive tokens.  Writes out rows (stride ld_out), the
 // per-query log-sum-exp, and adds every probability P[q][k] into colsum[k].
+// causal: keys after the query are never attended (the decoder variant the
+// paper's Sec. 7.2 names as future work).
 void attend_one_head(int n, int d, int L, int r, const std::vector<char>& is_global, double alpha,
                      const double* q, const double* k, const double* v, long ld, double* out, long ld_out,
-                     double* lse, double* colsum) {
+                     double* lse, double* colsum, bool causal) {
   std::vector<int> nbr;
   std::vector<double> s;
   nbr.reserve(n);
@@ -84,9 +86,11 @@ void attend_one_head(int n, int d, int L, int r, const std::vector<char>& is_glo
       lse[i] = -std::numeric_limits<double>::infinity();
       continue;
     }
-    // Allowed(i, j): both valid, and inside the window or either one global.
+    // Allowed(i, j): both valid, and inside the window or either one global;
+    // causal: and j <= i.
     nbr.clear();
-    for (int j = 0; j < L; ++j)
+    const int jend = causal ? std::min(i + 1, L) : L;
+    for (int j = 0; j < jend; ++j)
       if (std::abs(i - j) <= r || is_global[i] || is_global[j]) nbr.push_back(j);
     s.assign(nbr.size(), 0.0);
     double m = -std::numeric_limits<double>::infinity();
@@ -133,10 +137,10 @@ double orc_round_bf16(double x) { return round_bf16(x); }
 //   out [B, n, H, d]; lse [B, H, n] (-inf for padding rows); scores [B, n]:
 //   s_k = (1 / (H * L)) * sum_h sum_{q < L} P_h[q][k] for k < L, 0 otherwise.
 //   colsum (optional) [B, H, n]: the per-head column sums before averaging.
-int orc_sparse_attention(int B, int n, int H, int d, int window, int G, const int32_t* global_pos,
-                         const int32_t* valid_len, double alpha, const double* q, const double* k,
-                         const double* v, double* out, double* lse, double* scores, double* colsum,
-                         int nthreads) {
+static int sparse_attention(int B, int n, int H, int d, int window, int G, const int32_t* global_pos,
+                            const int32_t* valid_len, double alpha, const double* q, const double* k,
+                            const double* v, double* out, double* lse, double* scores, double* colsum, bool causal,
+                            int nthreads) {
   if (B < 0 || n < 0 || H <= 0 || d <= 0 || window < 0 || G < 0) return -1;
   set_threads(nthreads);
   const int r = window / 2;
@@ -149,7 +153,7 @@ int orc_sparse_attention(int B, int n, int H, int d, int window, int G, const in
     std::vector<char> g = global_flags(n, L, G, global_pos + (long)b * G);
     long base = (long)b * n * ld + (long)h * d;
     attend_one_head(n, d, L, r, g, alpha, q + base, k + base, v + base, ld, out + base, ld,
-                    lse + ((long)b * H + h) * n, cs.data() + ((size_t)b * H + h) * n);
+                    lse + ((long)b * H + h) * n, cs.data() + ((size_t)b * H + h) * n, causal);
   }
   for (int b = 0; b < B; ++b) {
     int L = std::min(std::max(valid_len[b], 0), n);
@@ -162,6 +166,24 @@ int orc_sparse_attention(int B, int n, int H, int d, int window, int G, const in
   }
   if (colsum) std::memcpy(colsum, cs.data(), cs.size() * sizeof(double));
   return 0;
+}
+
+int orc_sparse_attention(int B, int n, int H, int d, int window, int G, const int32_t* global_pos,
+                         const int32_t* valid_len, double alpha, const double* q, const double* k,
+                         const double* v, double* out, double* lse, double* scores, double* colsum,
+                         int nthreads) {
+  return sparse_attention(B, n, H, d, window, G, global_pos, valid_len, alpha, q, k, v, out, lse, scores, colsum,
+                          false, nthreads);
+}
+
+// The causal variant: as orc_sparse_attention with Allowed(i, j) also requiring
+// j <= i (band, global rows and global columns alike).
+int orc_sparse_attention_causal(int B, int n, int H, int d, int window, int G, const int32_t* global_pos,
+                                const int32_t* valid_len, double alpha, const double* q, const double* k,
+                                const double* v, double* out, double* lse, double* scores, double* colsum,
+                                int nthreads) {
+  return sparse_attention(B, n, H, d, window, G, global_pos, valid_len, alpha, q, k, v, out, lse, scores, colsum,
+                          true, nthreads);
 }
 
 // Compaction of sequence b from its keep flags: kept tokens in ascending order

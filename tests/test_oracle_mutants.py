@@ -44,6 +44,9 @@ MUTANTS = [
     ("GELU replaced by ReLU", "return 0.5 * v * (1.0 + std::erf(v / std::sqrt(2.0)));", "return v > 0.0 ? v : 0.0;"),
     ("feed-forward residual dropped", "for (long c = 0; c < D; ++c) t[c] = x1[c];", "for (long c = 0; c < D; ++c) t[c] = 0.0;"),
     ("feed-forward hidden not stored as bf16", "h[f] = round_bf16(gelu(h[f]));", "h[f] = gelu(h[f]);"),
+    ("causal query sees the future", "const int jend = causal ? std::min(i + 1, L) : L;", "const int jend = L;"),
+    ("causal global rows see the future", "const int jend = causal ? std::min(i + 1, L) : L;",
+     "const int jend = causal && !is_global[i] ? std::min(i + 1, L) : L;"),
     ("per-layer window ignored", "int rc = encoder_layer(B, n, H, d, windows[l],", "int rc = encoder_layer(B, n, H, d, windows[0],"),
 ]
 

@@ -37,14 +37,16 @@ def rand_case(seed, B=2, n=24, H=3, d=8, window=None, G=None, full=False, scale=
     return q, k, v, vl, gp, window
 
 
-def allowed_matrix(n, L, r, gflags):
+def allowed_matrix(n, L, r, gflags, causal=False):
     i = np.arange(n)[:, None]
     j = np.arange(n)[None, :]
     m = (np.abs(i - j) <= r) | gflags[:, None] | gflags[None, :]
+    if causal:
+        m = m & (j <= i)
     return m & (i < L) & (j < L)
 
 
-def brute_force(q, k, v, vl, gp, window, alpha):
+def brute_force(q, k, v, vl, gp, window, alpha, causal=False):
     """Explicit n x n masked softmax attention in numpy (tiny inputs only)."""
     B, n, H, d = q.shape
     r = window // 2
@@ -57,7 +59,7 @@ def brute_force(q, k, v, vl, gp, window, alpha):
         for p in gp[b]:
             if 0 <= p < L:
                 gf[p] = True
-        M = allowed_matrix(n, L, r, gf)
+        M = allowed_matrix(n, L, r, gf, causal)
         for h in range(H):
             S = alpha * q[b, :, h, :] @ k[b, :, h, :].T
             S = np.where(M, S, -np.inf)
@@ -92,6 +94,33 @@ def check_brute_force():
         assert np.array_equal(fin, np.isfinite(l))
         np.testing.assert_allclose(l[fin], bl[fin], rtol=0, atol=1e-12)
         np.testing.assert_allclose(s, bs, rtol=0, atol=1e-13)
+
+
+def check_causal_brute_force():
+    """Causal variant (keys after the query never attended, band and global strips alike) against the explicit
+    n x n mask."""
+    for seed in range(12):
+        q, k, v, vl, gp, w = rand_case(300 + seed)
+        o, l, s = run(q, k, v, vl, gp, w, causal=True)
+        bo, bl, bs = brute_force(q, k, v, vl, gp, w, 0.35, causal=True)
+        np.testing.assert_allclose(o, bo, rtol=0, atol=1e-12)
+        fin = np.isfinite(bl)
+        assert np.array_equal(fin, np.isfinite(l))
+        np.testing.assert_allclose(l[fin], bl[fin], rtol=0, atol=1e-12)
+        np.testing.assert_allclose(s, bs, rtol=0, atol=1e-13)
+
+
+def check_causal_dense_is_library_causal_attention():
+    """A window covering the sequence, no global token, causal: torch's causal SDPA (float64); the first token
+    attends only to itself; the scores still sum to one."""
+    q, k, v, vl, gp, _ = rand_case(310, n=20, full=True, G=0)
+    o, l, s = run(q, k, v, vl, gp, 1000, causal=True)
+    Q, K, V = (torch.from_numpy(x).permute(0, 2, 1, 3) for x in (q, k, v))
+    O = torch.nn.functional.scaled_dot_product_attention(Q, K, V, scale=0.35, is_causal=True)
+    np.testing.assert_allclose(o, O.permute(0, 2, 1, 3).numpy(), atol=1e-12)
+    assert np.array_equal(o[:, 0], v[:, 0])
+    np.testing.assert_allclose(l[:, :, 0], 0.35 * np.einsum("bhd,bhd->bh", q[:, 0], k[:, 0]), atol=1e-12)
+    np.testing.assert_allclose(s.sum(1), 1.0, atol=1e-12)
 
 
 def _sdpa(q, k, v, alpha):
@@ -546,7 +575,8 @@ def check_paper_threshold_schedule():
         assert abs(sched[int(layer) - 1] - val) < 1e-15
 
 
-ATTENTION_CHECKS = [check_brute_force, check_window_covers_sequence_is_dense, check_all_global_is_dense,
+ATTENTION_CHECKS = [check_brute_force, check_causal_brute_force, check_causal_dense_is_library_causal_attention,
+                    check_window_covers_sequence_is_dense, check_all_global_is_dense,
                     check_zero_window_no_global, check_constant_values, check_zero_queries_rational_scores,
                     check_score_invariants, check_reflection_symmetry, check_head_permutation,
                     check_sec55_example_structure, check_padding_is_invisible]
