@@ -138,8 +138,9 @@ def recorded_traffic():
     return rec.get("bytes_per_call")
 
 
-def algorithmic_counts(inp):
-    """Allowed (query, key) pairs of the non-global valid queries and of the global rows."""
+def algorithmic_counts(inp, causal=False):
+    """Allowed (query, key) pairs of the non-global valid queries and of the global rows (causal: keys at or
+    before the query only)."""
     import numpy as np
     r = inp["window"] // 2
     pairs_window = pairs_global = 0
@@ -147,13 +148,14 @@ def algorithmic_counts(inp):
         L = int(inp["valid_len"][b])
         g = np.array(sorted(int(p) for p in inp["global_pos"][b] if 0 <= p < L), dtype=np.int64)
         q = np.arange(L, dtype=np.int64)
-        lo, hi = np.maximum(0, q - r), np.minimum(L - 1, q + r)
+        lo, hi = np.maximum(0, q - r), np.minimum(L - 1, q if causal else q + r)
         band = hi - lo + 1
         g_in = np.searchsorted(g, hi, side="right") - np.searchsorted(g, lo, side="left")
+        g_reach = np.searchsorted(g, q, side="right") if causal else len(g)  # global keys the query may see
         nonglob = np.ones(L, bool)
         nonglob[g] = False
-        pairs_window += int(np.sum((band + len(g) - g_in)[nonglob]))
-        pairs_global += len(g) * L
+        pairs_window += int(np.sum((band + g_reach - g_in)[nonglob]))
+        pairs_global += int(np.sum(g + 1)) if causal else len(g) * L
     return pairs_window, pairs_global
 
 
@@ -173,11 +175,11 @@ def roofline(flops, bytes_, kern_ms):
     return roof
 
 
-def measure(sc, si, torch, np, inp, theta, steps, warmup, dev="cuda:0", keep_ratio=None):
+def measure(sc, si, torch, np, inp, theta, steps, warmup, dev="cuda:0", keep_ratio=None, causal=False):
     """Times `steps` steps (window attention with score partials, scores, prune + compaction of O) after
     `warmup` untimed ones.  theta None picks the median score of the valid non-global tokens (about half
     pruned), from one untimed step.  keep_ratio: prune by the top-k rule (sc_topk_prune_compact) instead of
-    the threshold."""
+    the threshold.  causal: the causal variant of the attention."""
     B, n, H, dd, G = inp["B"], inp["n"], inp["H"], inp["d"], inp["G"]
 
     def i32(a):
@@ -186,7 +188,8 @@ def measure(sc, si, torch, np, inp, theta, steps, warmup, dev="cuda:0", keep_rat
     def bf(a):
         return torch.from_numpy(np.ascontiguousarray(a).view(np.int16)).to(dev).view(torch.bfloat16)
 
-    d = sc.Desc(B, n, H, inp["window"], i32(inp["valid_len"]), i32(inp["global_pos"]), inp["alpha"], sc.SC_BF16)
+    d = sc.Desc(B, n, H, inp["window"], i32(inp["valid_len"]), i32(inp["global_pos"]), inp["alpha"], sc.SC_BF16,
+                causal=causal)
     q, k, v = bf(inp["q"]), bf(inp["k"]), bf(inp["v"])
     out = torch.empty_like(q)
     lse = torch.empty((B, H, n), dtype=torch.float32, device=dev)
@@ -236,7 +239,7 @@ def measure(sc, si, torch, np, inp, theta, steps, warmup, dev="cuda:0", keep_rat
     kern_ms /= max(launches, 1)
 
     tokens = int(np.sum(inp["valid_len"]))
-    pairs_w, pairs_g = algorithmic_counts(inp)
+    pairs_w, pairs_g = algorithmic_counts(inp, causal)
     # algorithmic work of the two launches: Q.K^T and P.V once per allowed pair (the window rows and the
     # global rows); read Q, K, V, write O (bf16), the LSE and the score partials (fp32)
     flops = 4.0 * dd * H * (pairs_w + pairs_g)
@@ -280,6 +283,9 @@ def main():
     ap.add_argument("--prune", choices=("threshold", "topk"), default="threshold",
                     help="pruning rule of the step: the layer threshold (the paper's rule) or top-k by keep ratio")
     ap.add_argument("--keep-ratio", type=float, default=0.5, help="top-k rule: fraction of candidates kept")
+    ap.add_argument("--causal", action="store_true",
+                    help="the causal variant of the attention (keys after the query never attended); the "
+                         "threshold is then the median score (the stored one belongs to the bidirectional scores)")
     ap.add_argument("--sweep", action="store_true",
                     help="instead of the single measurement, sweep the window (n 4096) and the length (window "
                          "512), one JSON line per point")
@@ -319,11 +325,15 @@ def main():
     inp = si.make_attention_inputs(cfg)
     gen_s = time.time() - t0
     keep_ratio = args.keep_ratio if args.prune == "topk" else None
-    m = measure(sc, si, torch, np, inp, theta, args.steps, args.warmup, dev, keep_ratio=keep_ratio)
+    if args.causal:
+        theta = None
+    m = measure(sc, si, torch, np, inp, theta, args.steps, args.warmup, dev, keep_ratio=keep_ratio,
+                causal=args.causal)
+    theta = m["theta"]
     ms, tokens = m["ms"], m["tokens"]
     roof = m["roof"]
-    # the recorded counters belong to the seq4096 workload
-    roof["traffic"] = recorded_traffic() if args.workload == "seq4096" else None
+    # the recorded counters belong to the (bidirectional, threshold-pruned) seq4096 workload
+    roof["traffic"] = recorded_traffic() if (args.workload == "seq4096" and not args.causal) else None
     roof["kernel"] = "k_attn_fwd<bf16> + k_attn_cols<bf16> (the two launches of the window attention)"
     roof["kernel_us"] = round(m["kern_ms"] * 1e3, 2)
     roof["algorithmic_flop"] = m["flops"]
@@ -338,7 +348,7 @@ def main():
                    "batch": cfg.B, "seq_len": cfg.n, "heads": cfg.H, "head_dim": cfg.d, "window": cfg.window,
                    "global_tokens": cfg.n_global, "valid_tokens": tokens,
                    "pruning": (f"top-k, keep ratio {keep_ratio}" if keep_ratio is not None else
-                               f"threshold {theta}"),
+                               f"threshold {theta}"), "attention": "causal" if args.causal else "bidirectional",
                    "parallelism": "none (1 GPU)"},
         "roofline": roof,
         "kept_per_sequence": m["kept"],
@@ -349,7 +359,7 @@ def main():
         threads = oracle.default_threads()
         c0 = time.perf_counter()
         _, _, rs = oracle.sparse_attention(inp["q64"], inp["k64"], inp["v64"], inp["valid_len"], inp["global_pos"],
-                                           cfg.window, cfg.alpha, nthreads=threads)
+                                           cfg.window, cfg.alpha, nthreads=threads, causal=args.causal)
         if keep_ratio is None:
             oracle.ltp_prune(rs.astype(np.float32), inp["valid_len"], inp["global_pos"], theta, 1)
         else:

@@ -97,6 +97,12 @@ typedef struct sc_attn_desc {
   const int32_t *valid_len;
   float softmax_scale;
   int32_t dtype;
+  /* 0: the bidirectional attention above; 1: causal variant (the decoder
+   * direction the paper's Sec. 7.2 names as future work): N(i) also requires
+   * j <= i, for the band and the global rows and columns alike.  Causal needs
+   * SC_BF16 and no band_probs output (else SC_EUNSUPPORTED); other values are
+   * SC_EINVAL. */
+  int32_t causal;
 } sc_attn_desc;
 
 /* Human-readable text for a status code (static storage). */
@@ -218,7 +224,7 @@ size_t sc_encoder_attn_stack_workspace_size(const sc_attn_desc *desc, int32_t n_
  *   keep, compaction as sc_ltp_prune_compact with thresholds[l]
  *   x   = bf16(LayerNorm(x + O . Wo[l]))     on the survivors; Wo [D, D];
  *                                            LayerNorm gamma 1, beta 0, eps ln_eps
- * desc gives the layer-0 geometry (dtype must be SC_BF16, D = H*d); lengths and
+ * desc gives the layer-0 geometry (dtype must be SC_BF16, causal 0, D = H*d); lengths and
  * global positions shrink on the device from layer to layer, with no host
  * synchronisation.
  *   x_in            bf16 [B, n, D]; x_out bf16 [B, n, D] (survivors first).

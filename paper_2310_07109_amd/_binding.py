@@ -23,7 +23,8 @@ class ScError(RuntimeError):
 class _Desc(ctypes.Structure):
     _fields_ = [("B", ctypes.c_int32), ("n", ctypes.c_int32), ("H", ctypes.c_int32), ("d", ctypes.c_int32),
                 ("window", ctypes.c_int32), ("G", ctypes.c_int32), ("global_pos", ctypes.c_void_p),
-                ("valid_len", ctypes.c_void_p), ("softmax_scale", ctypes.c_float), ("dtype", ctypes.c_int32)]
+                ("valid_len", ctypes.c_void_p), ("softmax_scale", ctypes.c_float), ("dtype", ctypes.c_int32),
+                ("causal", ctypes.c_int32)]
 
 
 def lib_path() -> str:
@@ -91,18 +92,21 @@ class Desc:
     valid_len: int32 device tensor [B]; global_pos: int32 device tensor [B, G] or None.
     """
 
-    def __init__(self, B, n, H, window, valid_len, global_pos=None, softmax_scale=0.125, dtype=SC_BF16, d=64):
+    def __init__(self, B, n, H, window, valid_len, global_pos=None, softmax_scale=0.125, dtype=SC_BF16, d=64,
+                 causal=False):
         self.B, self.n, self.H, self.d, self.window = int(B), int(n), int(H), int(d), int(window)
         self.valid_len = valid_len
         self.global_pos = global_pos
         self.G = 0 if global_pos is None else int(global_pos.shape[1])
         self.softmax_scale = float(softmax_scale)
         self.dtype = int(dtype)
+        self.causal = int(bool(causal))
 
     def c(self) -> _Desc:
         return _Desc(self.B, self.n, self.H, self.d, self.window, self.G,
                      None if self.global_pos is None else self.global_pos.data_ptr(),
-                     None if self.valid_len is None else self.valid_len.data_ptr(), self.softmax_scale, self.dtype)
+                     None if self.valid_len is None else self.valid_len.data_ptr(), self.softmax_scale, self.dtype,
+                     self.causal)
 
     def torch_dtype(self):
         import torch

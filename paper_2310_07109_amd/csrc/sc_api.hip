@@ -30,7 +30,9 @@ sc_status check_desc(const sc_attn_desc* d) {
   if (d->G > 0 && !d->global_pos) return SC_EINVAL;
   if (!std::isfinite(d->softmax_scale) || d->softmax_scale < 0.f) return SC_EINVAL;
   if (d->dtype != SC_F32 && d->dtype != SC_BF16) return SC_EINVAL;
+  if (d->causal != 0 && d->causal != 1) return SC_EINVAL;
   if (d->d != 64) return SC_EUNSUPPORTED;
+  if (d->causal && d->dtype != SC_BF16) return SC_EUNSUPPORTED;
   // grid sizes must fit the launch limits
   const long long blocks = (long long)((d->n + 63) / 64) * d->H * d->B;
   if (blocks >= (1LL << 31)) return SC_EUNSUPPORTED;
@@ -70,6 +72,7 @@ AttnArgs make_attn_args(const sc_attn_desc* d, const AttnGeom& geo) {
   a.H = d->H;
   a.G = d->G;
   a.r = geo.r;
+  a.causal = d->causal;
   // Scale in log2 units.  The kernels need c2 > 0 (disallowed logits are set
   // to -inf and exp2(-inf * c2) must be 0); a zero scale becomes the smallest
   // normal float, which yields the same fp32 probabilities for logits below
@@ -148,6 +151,7 @@ sc_status sc_window_attention(const sc_attn_desc* d, const void* q, const void* 
   sc_status st = check_desc(d);
   if (st != SC_OK) return st;
   if (!q || !k || !v || !out) return SC_EINVAL;
+  if (d->causal && band_probs) return SC_EUNSUPPORTED;
   const size_t tb = tensor_bytes(d);
   if (overlaps(out, tb, q, tb) || overlaps(out, tb, k, tb) || overlaps(out, tb, v, tb)) return SC_EINVAL;
   const size_t lse_b = sizeof(float) * d->B * d->H * d->n;
@@ -355,7 +359,7 @@ sc_status run_stack(const sc_attn_desc* d, int32_t n_layers, const int32_t* wind
                     void* stream) {
   sc_status st = check_desc(d);
   if (st != SC_OK) return st;
-  if (d->dtype != SC_BF16) return SC_EUNSUPPORTED;
+  if (d->dtype != SC_BF16 || d->causal) return SC_EUNSUPPORTED;
   if ((long long)d->H * d->d > 2048) return SC_EUNSUPPORTED;
   if ((long long)d->n * 3 * d->H * d->d * 2 >= (1LL << 32)) return SC_EUNSUPPORTED;  // fused q|k|v rows
   if (n_layers < 1 || !x_in || !Wqkv || !Wo || !thresholds || !x_out || !final_len) return SC_EINVAL;

@@ -265,7 +265,7 @@ SC_DEV WinBlock win_block(const AttnArgs& a, int blk) {
   wb.L = clampi(a.valid_len[wb.b], 0, a.n);
   wb.q0 = wb.qb * QB;
   wb.kt0 = max(0, wb.q0 - a.r);
-  wb.kt1 = min(wb.L, wb.q0 + QB + a.r);
+  wb.kt1 = min(wb.L, wb.q0 + QB + (a.causal ? 0 : a.r));  // causal: no key after the block's last query
   wb.nkt = (wb.kt1 - wb.kt0 + kBK - 1) / kBK;
   wb.nwords = (wb.kt1 - wb.kt0 + 31) >> 5;
   wb.nxc = (a.gpos && a.G > 0) ? (a.G + kBK - 1) / kBK : 0;
@@ -293,7 +293,7 @@ SC_DEV int win_tables(const AttnArgs& a, const WinBlock& wb, uint32_t* sBits, in
     const int p = j == tid ? p_first : gp[j];
     if (p >= wb.kt0 && p < wb.kt1)
       atomicOr(&sBits[(p - wb.kt0) >> 5], 1u << ((p - wb.kt0) & 31));
-    else if (p >= 0 && p < wb.L)
+    else if (p >= 0 && p < wb.L && !(a.causal && p >= wb.kt1))  // causal: later keys are never attended
       sXList[j / kBK] = 1;
   }
   __syncthreads();
@@ -524,6 +524,7 @@ SC_DEV void gr_fwd_block(const AttnArgs& a, int lin, Smem<DT>& sm) {
   typename TR::Frag qf[TR::kChunks];
   TR::load_frags(sm.b[1], 16 * sg + lr, g, qf);
   const bool wlive = __ballot(sm.pos[0][16 * sg + lr] >= 0) != 0ull;  // some slot of the group is used
+  const int rowpos = sm.pos[0][16 * sg + lr];                           // the lane's global row (-1: unused)
   __syncthreads();  // every wave holds its query fragments before b[1] is reused
   float m_use = kNegBig, l_run = 0.f;
   f32x4 o[4];
@@ -536,7 +537,14 @@ SC_DEV void gr_fwd_block(const AttnArgs& a, int lin, Smem<DT>& sm) {
       stv.load_range(Vg, a.ld_in, k0 + kBK, kend);
     }
     if (wlive && k0 + 32 * kh < kend) {
-      if (k0 + kBK <= kend) {
+      if (a.causal) {  // the lane's global row attends keys up to its own position
+        const int hi = min(kend - 1, rowpos) - k0;
+        auto upto = [&](int s4, int i) { return 16 * s4 + 4 * g + i <= hi; };
+        if (kh == 0)
+          softmax_tile<DT, true, 0>(qf, sm.b[buf], sm.c[buf], a.c2, lr, g, m_use, l_run, o, upto);
+        else
+          softmax_tile<DT, true, 1>(qf, sm.b[buf], sm.c[buf], a.c2, lr, g, m_use, l_run, o, upto);
+      } else if (k0 + kBK <= kend) {
         auto all = [](int, int) { return true; };
         if (kh == 0)
           softmax_tile<DT, false, 0>(qf, sm.b[buf], sm.c[buf], a.c2, lr, g, m_use, l_run, o, all);
@@ -746,6 +754,10 @@ SC_DEV void window_fwd_v2(const AttnArgs& a, int blk, Smem<1>& sm, uint32_t* sDy
   const int tid = threadIdx.x, lane = tid & 63, w = __builtin_amdgcn_readfirstlane(tid >> 6), g = lane >> 4,
             lr = lane & 15;
   const int n = a.n, r = a.r, L = wb.L, q0 = wb.q0, kt0 = wb.kt0, kt1 = wb.kt1, nkt = wb.nkt;
+  // reach of the band after the query: r, or 0 in the causal variant (where a
+  // global key after the query is not attended either)
+  const bool causal = a.causal != 0;
+  const int rh = causal ? 0 : r;
   const long long ld = a.ld_in;
   const unsigned ldb = (unsigned)(2 * a.ld_in);
   const T* Qg = static_cast<const T*>(a.q) + wb.b * a.bs_in + wb.h * kHeadDim;
@@ -810,7 +822,7 @@ SC_DEV void window_fwd_v2(const AttnArgs& a, int blk, Smem<1>& sm, uint32_t* sDy
   for (int j = 0; j < 2; ++j) {
     const int q = qa + 16 * j + lr;
     lo[j] = q - r - 4 * g;
-    hi[j] = min(q + r, kt1 - 1) - 4 * g;
+    hi[j] = min(q + rh, kt1 - 1) - 4 * g;
   }
   // every tile step: load the next tile into the other buffer, compute,
   // wait for the load, barrier (the same sequence in all three phases below)
@@ -829,9 +841,9 @@ SC_DEV void window_fwd_v2(const AttnArgs& a, int blk, Smem<1>& sm, uint32_t* sDy
   auto edge_tile = [&](int t) {
     const int buf = t & 1, k0 = kt0 + t * kBK;
     const unsigned long long gall = tile_gmask(sBits, t, wb.nwords);
-    const bool near = k0 <= qa + 31 + r && k0 + kBK - 1 >= qa - r;
+    const bool near = k0 <= qa + 31 + rh && k0 + kBK - 1 >= qa - r;
     if (!near && gall == 0ull) return;
-    const int wlo = qa - r - k0, whi = min(qa + 31 + r, kt1 - 1) - k0;
+    const int wlo = qa - r - k0, whi = min(qa + 31 + rh, kt1 - 1) - k0;
     unsigned live = 0u;
 #pragma unroll
     for (int st = 0; st < 4; ++st)
@@ -839,7 +851,7 @@ SC_DEV void window_fwd_v2(const AttnArgs& a, int blk, Smem<1>& sm, uint32_t* sDy
     const int l0 = lo[0] - k0, h0 = hi[0] - k0, l1 = lo[1] - k0, h1 = hi[1] - k0;
     // a band edge is one-sided in most tiles: the band starts inside the
     // tile for some query (nlo) or ends inside it (nhi), wave-uniform
-    const bool nlo = qa + 31 - r - k0 > 0, nhi = min(qa + r, kt1 - 1) - k0 < kBK - 1;
+    const bool nlo = qa + 31 - r - k0 > 0, nhi = min(qa + rh, kt1 - 1) - k0 < kBK - 1;
     if (gall == 0ull && !nhi) {
       softmax_tile2<true>(qf, sm.b[buf], sm.c[buf], a.c2, lr, g, m_use, l_run, o, live,
                           [&](int j, int st, int i) { return 16 * st + i >= (j == 0 ? l0 : l1); });
@@ -853,10 +865,13 @@ SC_DEV void window_fwd_v2(const AttnArgs& a, int blk, Smem<1>& sm, uint32_t* sDy
       });
     } else {
       const unsigned long long gm = gall >> (4 * g);
+      // a global key is attended by every query, or (causal) by the queries
+      // at or after it
+      const int g0 = causal ? h0 : 1 << 30, g1 = causal ? h1 : 1 << 30;
       softmax_tile2<true>(qf, sm.b[buf], sm.c[buf], a.c2, lr, g, m_use, l_run, o, live, [&](int j, int st, int i) {
         const int c = 16 * st + i;
         const bool band = j == 0 ? (c >= l0) & (c <= h0) : (c >= l1) & (c <= h1);
-        return band | (bool)((gm >> c) & 1ull);
+        return band | (((gm >> c) & 1ull) != 0ull && c <= (j == 0 ? g0 : g1));
       });
     }
   };
@@ -864,7 +879,7 @@ SC_DEV void window_fwd_v2(const AttnArgs& a, int blk, Smem<1>& sm, uint32_t* sDy
   // band of all 32 queries and below kt1 (global keys among them are band
   // keys), so no mask is needed
   const int ia = clampi(-((kt0 - (qa + 31 - r)) >> 6), 0, nkt);
-  const int ib = clampi(((min(qa + r, kt1 - 1) - (kBK - 1) - kt0) >> 6) + 1, ia, nkt);
+  const int ib = clampi(((min(qa + rh, kt1 - 1) - (kBK - 1) - kt0) >> 6) + 1, ia, nkt);
   int t = 0;
   for (; t < ia; ++t) {
     issue(t);
@@ -889,7 +904,7 @@ SC_DEV void window_fwd_v2(const AttnArgs& a, int blk, Smem<1>& sm, uint32_t* sDy
   auto slot_row = [&](int c, int row) {
     const int j = kBK * c + row;
     const int p = j < a.G ? gp[j] : -1;
-    return (p >= 0 && p < L && (p < kt0 || p >= kt1)) ? p : -1;
+    return (p >= 0 && p < L && (p < kt0 || (!causal && p >= kt1))) ? p : -1;
   };
   for (int t = nkt; t < ntile; ++t) {
     const int c = sXList[t - nkt];
@@ -1108,7 +1123,10 @@ SC_DEV void band_col_v2(const AttnArgs& a, int blk, SmemCol<1>& sm) {
   const T* Qg = static_cast<const T*>(a.q) + b * a.bs_in + h * kHeadDim;
   const T* Kg = static_cast<const T*>(a.k) + b * a.bs_in + h * kHeadDim;
   const float* l2g = a.win_lse2 + (long long)bh * n;
-  const int qlo = max(0, k0 - r), qhi = min(L, k0 + kBK2 + r);
+  // queries before a key reach it through the band by r, or not at all in the
+  // causal variant
+  const int rl = a.causal ? 0 : r;
+  const int qlo = max(0, k0 - rl), qhi = min(L, k0 + kBK2 + r);
   const int nqt = (qhi - qlo + kBQ - 1) / kBQ;
   // query tile t (rows clamped below qhi) and the log2-LSE of its rows
   // (indices clamped below n; rows at or beyond qhi are masked)
@@ -1148,15 +1166,15 @@ SC_DEV void band_col_v2(const AttnArgs& a, int blk, SmemCol<1>& sm) {
 #pragma unroll
   for (int j = 0; j < 2; ++j) {
     const int key = kw0 + 16 * j + lr;
-    lo[j] = key - r - 4 * g;
+    lo[j] = key - rl - 4 * g;
     hi[j] = min(key + r, qhi - 1) - 4 * g;
   }
   f32x4 cs[2] = {{0.f, 0.f, 0.f, 0.f}, {0.f, 0.f, 0.f, 0.f}};
   for (int t = 0; t < nqt; ++t) {
     const int buf = t & 1, qs = qlo + t * kBQ;
     if (t + 1 < nqt) issue(t + 1, buf ^ 1);
-    if (qs <= kw0 + 31 + r && qs + kBQ - 1 >= kw0 - r) {
-      if (qs >= kw0 + 31 - r && qs + kBQ - 1 <= kw0 + r && qs + kBQ <= qhi) {
+    if (qs <= kw0 + 31 + r && qs + kBQ - 1 >= kw0 - rl) {
+      if (qs >= kw0 + 31 - rl && qs + kBQ - 1 <= kw0 + r && qs + kBQ <= qhi) {
         col_tile2<false, false>(kf, sm.b[buf], sm.l[buf], a.c2, lr, g, cs, lo, hi);
       } else {
         const int l2[2] = {lo[0] - qs, lo[1] - qs}, h2[2] = {hi[0] - qs, hi[1] - qs};
@@ -1245,6 +1263,10 @@ SC_DEV void gcol_block(const AttnArgs& a, int lin, SmemCol<DT>& sm) {
                                   const int q = qs + qq;
                                   if (kuse && q < L && p != 0.f) bpc[(long long)q * G + slot] = p;
                                 }, qlive);
+    } else if (a.causal) {  // a global key is attended by the queries at or after it
+      const int kp = pos[16 * kg + lr];
+      cs += col_tile<DT, true>(kf, sm.b[buf], sm.l[buf], a.c2, lr, g,
+                               [&](int qst, int i) { return qs + 16 * qst + 4 * g + i >= kp; }, NoEmit{}, qlive);
     } else {
       cs += col_tile<DT, false>(kf, sm.b[buf], sm.l[buf], a.c2, lr, g, [](int, int) { return true; }, NoEmit{},
                                 qlive);
@@ -1385,6 +1407,9 @@ SC_DEV void gr_col_block(const AttnArgs& a, int lin, SmemCol<DT>& sm) {
         const int slot = kGlobalChunk * blk.gc + qq;
         if (kin && slot < a.G && p != 0.f) bpr[(long long)slot * a.n + key] = p;
       }, qlive);
+    } else if (a.causal) {  // a global row's probabilities reach the keys up to its position
+      cs = col_tile<DT, true>(kf, sm.a, sm.l[0], a.c2, lr, g,
+                              [&](int qst, int i) { return key <= pos[16 * qst + 4 * g + i]; }, NoEmit{}, qlive);
     } else {
       cs = col_tile<DT, false>(kf, sm.a, sm.l[0], a.c2, lr, g, [](int, int) { return true; }, NoEmit{}, qlive);
     }

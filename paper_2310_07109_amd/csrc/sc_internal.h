@@ -24,6 +24,7 @@ struct AttnArgs {
   long long ld_in, bs_in;   // elements between tokens / sequences of q, k, v
   long long ld_out, bs_out; // same for out
   int B, n, H, G, r;      // r = half window, clamped to [0, n]
+  int causal;             // 1: keys after the query are never attended
   float c2;               // softmax scale * log2(e)
   // score partials (null: skip the exact-probability column sums)
   float* part_band;       // [B, H, n]      band column sums of non-global keys

@@ -78,6 +78,19 @@ def test_invalid_descriptors_rejected_before_launch():
     assert call_attn(desc(global_pos=FakeT(0x50000), G=257)) == B.SC_EINVAL
 
 
+def test_causal_flag_checked():
+    assert call_attn(desc(causal=True, dtype=B.SC_F32)) == B.SC_EUNSUPPORTED
+    L = sc.load()
+    bad = desc()
+    c = bad.c()
+    c.causal = 2
+    assert L.sc_window_attention(ctypes.byref(c), 0x100000, 0x200000, 0x300000, 0x400000, None, None, None,
+                                 0x900000, 1 << 30, None) == B.SC_EINVAL
+    c = desc(causal=True).c()
+    assert L.sc_window_attention(ctypes.byref(c), 0x100000, 0x200000, 0x300000, 0x400000, None, None, 0x800000,
+                                 0x900000, 1 << 30, None) == B.SC_EUNSUPPORTED   # band layout not with causal
+
+
 def test_null_and_aliasing_rejected():
     d = desc()
     assert call_attn(d, q=None) == B.SC_EINVAL

@@ -256,3 +256,61 @@ def test_topk_ties_signs_and_lengths():
     for ratio in (0.0, 1e-4, 0.2, 1.0 / 3.0, 0.5, 0.75, 1.0):
         for kg in (1, 0):
             _topk_compare(d, s, vl, gp, ratio, kg, rows=rows if kg else None)
+
+
+CAUSAL = [
+    # name, B, n, H, window, G, len range, extra (bf16)
+    ("causal single token", 2, 1, 2, 4, 1, (1, 1), {}),
+    ("causal ragged no global", 2, 300, 3, 64, 0, (200, 300), {}),
+    ("causal w0", 1, 70, 2, 0, 0, (70, 70), {}),
+    ("causal ragged with empty seq", 3, 260, 2, 40, 2, (0, 260), dict(lens=[0, 137, 260])),
+    ("causal dense window", 2, 300, 2, 1000, 1, (250, 300), {}),
+    ("causal two slot chunks", 1, 700, 2, 256, 70, (650, 700), {}),
+    ("causal all tokens global", 1, 96, 2, 8, 96, (96, 96), {}),
+    ("causal global at last valid token", 2, 160, 2, 32, 2, (160, 160), dict(gp_override=[[0, 159], [5, 159]])),
+    ("causal 600 global tokens", 1, 1200, 2, 64, 600, (1100, 1200), {}),
+    ("causal long window ragged", 2, 2000, 2, 700, 5, (1500, 2000), {}),
+]
+
+
+@pytest.mark.parametrize("case", CAUSAL, ids=[c[0] for c in CAUSAL])
+def test_causal_small_cases(case):
+    """Causal variant: keys after the query are never attended (band and global strips alike)."""
+    name, B, n, H, window, G, lr, extra = case
+    log(f"case {name}")
+    inp = small_case(name, "bf16", B, n, H, window, G, lr, **extra)
+    ro, rl, rs = oracle.sparse_attention(inp["q64"], inp["k64"], inp["v64"], inp["valid_len"], inp["global_pos"],
+                                         window, inp["alpha"], causal=True)
+    d = make_desc(inp)
+    d.causal = 1
+    q, k, v = (to_dev_storage(inp[x], "bf16") for x in ("q", "k", "v"))
+    out, lse, sp, _ = sc.sc_window_attention(d, q, k, v, lse=True, score_partials=True)
+    scores = sc.sc_ltp_score(d, sp)
+    torch.cuda.synchronize()
+    check_out(out.float().cpu().numpy(), ro, "bf16")
+    check_lse(lse.cpu().numpy(), rl, inp["valid_len"])
+    check_scores(scores.cpu().numpy(), rs, inp["valid_len"])
+
+
+def test_causal_config4_attention_scores_and_pruning():
+    """Causal variant of the seq-4096 workload at full size: O, LSE, scores, and the compaction on the oracle's
+    scores (bit-exact) and on the GPU's own scores (kept lists, near-threshold tokens excluded)."""
+    cfg = si.CONFIGS[4]
+    inp = si.make_attention_inputs(cfg)
+    log("causal config 4: oracle")
+    ro, rl, rs = oracle.sparse_attention(inp["q64"], inp["k64"], inp["v64"], inp["valid_len"], inp["global_pos"],
+                                         inp["window"], inp["alpha"], causal=True)
+    d = make_desc(inp)
+    d.causal = 1
+    q, k, v = (to_dev_storage(inp[x], "bf16") for x in ("q", "k", "v"))
+    out, lse, sp, _ = sc.sc_window_attention(d, q, k, v, lse=True, score_partials=True)
+    scores = sc.sc_ltp_score(d, sp)
+    torch.cuda.synchronize()
+    err = check_out(out.float().cpu().numpy(), ro, "bf16")
+    check_lse(lse.cpu().numpy(), rl, inp["valid_len"])
+    worst = check_scores(scores.cpu().numpy(), rs, inp["valid_len"])
+    theta = float(np.median(rs[0, :int(inp["valid_len"][0])]))
+    keep, nl, ngp, orig, _ = sc.sc_ltp_prune_compact(d, scores, theta, True)
+    excl, dis = compare_keep(keep.cpu().numpy(), nl.cpu().numpy(), rs, theta, inp["valid_len"], inp["global_pos"])
+    log(f"causal config 4: max |dO| {err:.3g}, worst score rel err {worst:.3g}, kept {nl.cpu().tolist()}, "
+        f"near-theta excluded {excl}, disagreements {dis}")
