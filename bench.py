@@ -24,6 +24,14 @@ sys.path.insert(0, ROOT)
 
 METRIC = "kept-token-layers/sec per GPU; % MFMA (window attn) & % HBM peak (score/prune)"
 HBM_PEAK_GBS = 8000.0
+# VALU issue rate: 256 CUs x 4 SIMDs x 16 lanes x 2.4 GHz, one non-packed op per lane per cycle (packed fp32 forms
+# are not used); in Tera lane-ops per second
+VALU_PEAK_TOPS = 256 * 4 * 16 * 2.4e9 / 1e12
+# algorithmic VALU work per allowed (query, key) pair and head, in VALU issue slots: pass 1 (softmax and P.V):
+# one FMA (scale, subtract the max), one exp, one add (row sum), half a max3, half a pack-convert to bf16; pass 2
+# (exact probabilities for the scores): one FMA (scale, subtract the LSE), one exp, one add (column sum).  The
+# exp issues at half the FMA rate (measured on gfx950: 8.2 against 4.2 cycles per wave64), so it counts twice.
+VALU_SLOTS_PER_PAIR = (1 + 1 + 0.5 + 0.5) + 1 + 1 + 2 * 2
 MFMA_PEAK_TFLOPS = {"bf16": 2500.0, "f32": 157.3}
 KERNEL_SOURCES = ("paper_2310_07109_amd/csrc/sc_attention.hip", "paper_2310_07109_amd/csrc/sc_device.h",
                   "paper_2310_07109_amd/csrc/sc_internal.h")
@@ -159,11 +167,18 @@ def algorithmic_counts(inp, causal=False):
     return pairs_window, pairs_global
 
 
-def roofline(flops, bytes_, kern_ms):
-    """Roofline of the two window-attention launches against the larger of the MFMA and HBM floors."""
+def roofline(flops, bytes_, kern_ms, pairs=None):
+    """Roofline of the two window-attention launches against the largest of the MFMA, HBM and VALU floors
+    (VALU: VALU_SLOTS_PER_PAIR issue slots per allowed pair and head, at VALU_PEAK_TOPS)."""
     t_mfma = flops / (MFMA_PEAK_TFLOPS["bf16"] * 1e12)
     t_hbm = bytes_ / (HBM_PEAK_GBS * 1e9)
-    if t_mfma >= t_hbm:
+    alu_ops = VALU_SLOTS_PER_PAIR * pairs if pairs is not None else 0.0
+    t_alu = alu_ops / (VALU_PEAK_TOPS * 1e12)
+    if t_alu >= max(t_mfma, t_hbm):
+        achieved = alu_ops / (kern_ms * 1e-3) / 1e12
+        roof = dict(bound="alu", achieved=round(achieved, 3), peak=round(VALU_PEAK_TOPS, 2),
+                    unit="T VALU lane-op/s")
+    elif t_mfma >= t_hbm:
         achieved = flops / (kern_ms * 1e-3) / 1e12
         roof = dict(bound="mfma", achieved=round(achieved, 2), peak=MFMA_PEAK_TFLOPS["bf16"], unit="TFLOP/s")
     else:
@@ -172,6 +187,8 @@ def roofline(flops, bytes_, kern_ms):
     roof["frac"] = round(roof["achieved"] / roof["peak"], 4)
     roof["floor_mfma_us"] = round(t_mfma * 1e6, 2)
     roof["floor_hbm_us"] = round(t_hbm * 1e6, 2)
+    roof["floor_alu_us"] = round(t_alu * 1e6, 2)
+    roof["hbm_achieved_gbs"] = round(bytes_ / (kern_ms * 1e-3) / 1e9, 1)
     return roof
 
 
@@ -244,7 +261,7 @@ def measure(sc, si, torch, np, inp, theta, steps, warmup, dev="cuda:0", keep_rat
     # global rows); read Q, K, V, write O (bf16), the LSE and the score partials (fp32)
     flops = 4.0 * dd * H * (pairs_w + pairs_g)
     bytes_ = tokens * H * (4 * dd * 2 + 4) + sp.numel() * 4
-    roof = roofline(flops, bytes_, kern_ms)
+    roof = roofline(flops, bytes_, kern_ms, pairs=H * (pairs_w + pairs_g))
     return dict(ms=ms, wall_ms=wall_ms, kern_ms=kern_ms, tokens=tokens, kept=outs["new_len"].cpu().tolist(),
                 flops=flops, bytes=bytes_, roof=roof, theta=theta, pairs=H * (pairs_w + pairs_g))
 
