@@ -1448,19 +1448,66 @@ __global__ __launch_bounds__(kThreads) SC_OCC(kBandProbs ? 2 : 4) void k_attn_co
 // ------------------------------------------------------ score reduction ----
 // scores[b, k] = (sum over heads of: the band column sum of k, its global
 // column (summed over query ranges) if k is global, and the global rows'
-// column sums) / (H * L).  Workgroup = 64 keys x 4 head groups; group j sums
-// heads j, j + 4, ...; the 4 group sums are added in group order.  Fixed
-// order everywhere; no atomics.
+// column sums) / (H * L).  Workgroup = 64 keys x 4 head groups.  Fixed order
+// everywhere; no atomics.
+// Score partials of one layer, as the attention kernels write them.
+struct ScorePartials {
+  const float* band;  // [B, H, n]      band column sums
+  const float* gcol;  // [B, H, nqr, G] global-key columns per 512-query range
+  const float* grow;  // [B, H, ngc, n] column sums over the global rows
+  int n, H, G, ngc, nqr;
+};
+
+// Attention that key k receives from head bh = b * H + h, in two steps
+// applied in this order: score_head_local gives the band column sum plus the
+// global-row sums (chunk by chunk), score_head_global then adds, for a global
+// key in slot `slot` (-1: not global), its global-column sums over the nqrv
+// query ranges in use.  kNgc >= 0 fixes the number of global-row chunks at
+// compile time (it must equal sp.ngc).
+template <int kNgc>
+SC_DEV float score_head_local(const ScorePartials& sp, long long bh, int k) {
+  float v = sp.band[bh * sp.n + k];
+  if constexpr (kNgc >= 0) {
+#pragma unroll
+    for (int gc = 0; gc < kNgc; ++gc) v += sp.grow[(bh * sp.ngc + gc) * sp.n + k];
+  } else {
+    for (int gc = 0; gc < sp.ngc; ++gc) v += sp.grow[(bh * sp.ngc + gc) * sp.n + k];
+  }
+  return v;
+}
+
+SC_DEV float score_head_global(const ScorePartials& sp, long long bh, int slot, int nqrv, float v) {
+  if (slot >= 0)
+    for (int qr = 0; qr < nqrv; ++qr) v += sp.gcol[(bh * sp.nqr + qr) * sp.G + slot];
+  return v;
+}
+
 constexpr int kScoreKeys = 64;
 constexpr int kScoreGroups = 4;
+constexpr int kScorePre = 4;  // heads per group whose band / global-row terms are loaded up front
 
-__global__ __launch_bounds__(kScoreKeys * kScoreGroups) void k_score_from_partials(
-    const float* part, const int* valid_len, const int* gpos, int B, int n, int H, int G, AttnGeom geo,
-    float* scores) {
+// Thread = key x head group (group j sums heads j, j + 4, ... from 0 up; the
+// groups are added in order and the total divided by H * L).  The band and
+// global-row terms of the group's first kScorePre heads are loaded before the
+// length and the global positions arrive (they need neither), so the
+// workgroup waits on memory about once.  kNgc: the number of global-row
+// chunks when fixed at compile time (0 or 1), else -1.
+template <int kNgc>
+__global__ __launch_bounds__(kScoreKeys * kScoreGroups) void k_score_from_partials(ScorePartials sp,
+                                                                                    const int* valid_len,
+                                                                                    const int* gpos, float* scores) {
   __shared__ int smap[kScoreKeys];
   __shared__ float red[kScoreGroups][kScoreKeys];
+  const int n = sp.n, H = sp.H, G = sp.G;
   const int b = blockIdx.y, kb = blockIdx.x * kScoreKeys, tid = threadIdx.x;
   const int lane = tid % kScoreKeys, hg = tid / kScoreKeys, k = kb + lane;
+  float pre[kScorePre];
+  {
+    const int kk = k < n ? k : n - 1;  // clamped key and head: in bounds, unused values are discarded
+#pragma unroll
+    for (int i = 0; i < kScorePre; ++i)
+      pre[i] = score_head_local<kNgc>(sp, (long long)b * H + min(hg + kScoreGroups * i, H - 1), kk);
+  }
   const int L = clampi(valid_len[b], 0, n);
   if (tid < kScoreKeys) smap[tid] = -1;
   __syncthreads();
@@ -1472,19 +1519,16 @@ __global__ __launch_bounds__(kScoreKeys * kScoreGroups) void k_score_from_partia
   __syncthreads();
   float acc = 0.f;
   if (k < L) {
-    const float* band = part;
-    const float* gcol = band + (size_t)B * H * n;
-    const float* grow = gcol + (size_t)B * H * geo.nqr * G;
     const int slot = smap[lane];
     const int nqrv = (L + kGlobalKeySpan - 1) / kGlobalKeySpan;
-#pragma unroll 4
-    for (int h = hg; h < H; h += kScoreGroups) {
+#pragma unroll
+    for (int i = 0; i < kScorePre; ++i) {
+      const int h = hg + kScoreGroups * i;
+      if (h < H) acc += score_head_global(sp, (long long)b * H + h, slot, nqrv, pre[i]);
+    }
+    for (int h = hg + kScoreGroups * kScorePre; h < H; h += kScoreGroups) {
       const long long bh = (long long)b * H + h;
-      float v = band[bh * n + k];
-      for (int gc = 0; gc < geo.ngc; ++gc) v += grow[(bh * geo.ngc + gc) * n + k];
-      if (slot >= 0)
-        for (int qr = 0; qr < nqrv; ++qr) v += gcol[(bh * geo.nqr + qr) * G + slot];
-      acc += v;
+      acc += score_head_global(sp, bh, slot, nqrv, score_head_local<kNgc>(sp, bh, k));
     }
   }
   red[hg][lane] = acc;
@@ -1645,11 +1689,33 @@ hipError_t launch_window_attention(int dtype, const AttnArgs& a, hipStream_t s) 
   return dtype == 1 ? launch_window_t<1>(a, s) : launch_window_t<0>(a, s);
 }
 
+static ScorePartials score_partials(const float* part, int B, int n, int H, int G, const AttnGeom& g) {
+  ScorePartials sp;
+  sp.band = part;
+  sp.gcol = sp.band + (size_t)B * H * n;
+  sp.grow = sp.gcol + (size_t)B * H * g.nqr * G;
+  sp.n = n;
+  sp.H = H;
+  sp.G = G;
+  sp.ngc = g.ngc;
+  sp.nqr = g.nqr;
+  return sp;
+}
+
 hipError_t launch_score_from_partials(const float* partials, const int* valid_len, const int* gpos, int B, int n,
                                       int H, int G, const AttnGeom& g, float* scores, hipStream_t s) {
   dim3 grid((n + kScoreKeys - 1) / kScoreKeys, B);
-  hipLaunchKernelGGL(k_score_from_partials, grid, dim3(kScoreKeys * kScoreGroups), 0, s, partials, valid_len,
-                     G > 0 ? gpos : nullptr, B, n, H, G, g, scores);
+  const ScorePartials sp = score_partials(partials, B, n, H, G, g);
+  const int* gp = G > 0 ? gpos : nullptr;
+  if (g.ngc == 0)
+    hipLaunchKernelGGL(k_score_from_partials<0>, grid, dim3(kScoreKeys * kScoreGroups), 0, s, sp, valid_len, gp,
+                       scores);
+  else if (g.ngc == 1)
+    hipLaunchKernelGGL(k_score_from_partials<1>, grid, dim3(kScoreKeys * kScoreGroups), 0, s, sp, valid_len, gp,
+                       scores);
+  else
+    hipLaunchKernelGGL(k_score_from_partials<-1>, grid, dim3(kScoreKeys * kScoreGroups), 0, s, sp, valid_len, gp,
+                       scores);
   return hipGetLastError();
 }
 
