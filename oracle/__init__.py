@@ -57,8 +57,13 @@ def lib():
                                             cf, ci, cd, f64p, i32p, i32p, i32p, f32p, ci]
         L.orc_encoder_stack_ffn.argtypes = [ci, ci, ci, ci, i32p, ci, i32p, i32p, cd, ci, f64p, f64p, f64p, f64p,
                                             f64p, ci, f32p, ci, cd, f64p, i32p, i32p, i32p, ci]
-        for f in ("orc_sparse_attention", "orc_sparse_attention_causal", "orc_ltp_prune", "orc_topk_prune", "orc_gather_rows", "orc_encoder_layer",
-                  "orc_encoder_stack", "orc_encoder_layer_ffn", "orc_encoder_stack_ffn"):
+        L.orc_soft_prune_forward.argtypes = [ci, ci, ci, ci, ci, ci, i32p, i32p, cd, f64p, f64p, f64p, cd, cd, ci,
+                                             f64p, f64p, f64p, f64p, f64p, ci]
+        L.orc_soft_prune_backward.argtypes = [ci, ci, ci, ci, ci, ci, i32p, i32p, cd, f64p, f64p, f64p, cd, cd, ci,
+                                              f64p, f64p, f64p, f64p, f64p, f64p, ci]
+        for f in ("orc_sparse_attention", "orc_sparse_attention_causal", "orc_ltp_prune", "orc_topk_prune",
+                  "orc_gather_rows", "orc_encoder_layer", "orc_encoder_stack", "orc_encoder_layer_ffn",
+                  "orc_encoder_stack_ffn", "orc_soft_prune_forward", "orc_soft_prune_backward"):
             getattr(L, f).restype = ci
         _lib = L
     return _lib
@@ -110,6 +115,44 @@ def sparse_attention(q, k, v, valid_len, global_pos, window, alpha, want_colsum=
                                     nthreads or default_threads())
     assert rc == 0, rc
     return (out, lse, scores, colsum) if want_colsum else (out, lse, scores)
+
+
+def soft_prune_forward(q, k, v, valid_len, global_pos, window, alpha, theta, temperature, keep_global=1,
+                       nthreads=None):
+    """LTP soft pruning, training form.  Returns (out, lse, scores, mask [B, n], y [B, n, H, d] = mask * out)."""
+    q, k, v = _f64(q), _f64(k), _f64(v)
+    B, n, H, d = q.shape
+    gp = _i32(global_pos).reshape(B, -1)
+    vl = _i32(valid_len)
+    out, y = np.empty_like(q), np.empty_like(q)
+    lse, scores, mask = np.empty((B, H, n)), np.empty((B, n)), np.empty((B, n))
+    c = ctypes.c_double
+    rc = lib().orc_soft_prune_forward(B, n, H, d, int(window), gp.shape[1], _p(gp, ctypes.c_int32),
+                                      _p(vl, ctypes.c_int32), float(alpha), _p(q, c), _p(k, c), _p(v, c),
+                                      float(theta), float(temperature), int(keep_global), _p(out, c), _p(lse, c),
+                                      _p(scores, c), _p(mask, c), _p(y, c), nthreads or default_threads())
+    assert rc == 0, rc
+    return out, lse, scores, mask, y
+
+
+def soft_prune_backward(q, k, v, valid_len, global_pos, window, alpha, theta, temperature, dy, dmask=None,
+                        keep_global=1, nthreads=None):
+    """Backward of soft_prune_forward for dL/dy = dy [B, n, H, d] and dL/dmask = dmask [B, n] (or None).
+    Returns (dq, dk, dv, dtheta)."""
+    q, k, v, dy = _f64(q), _f64(k), _f64(v), _f64(dy)
+    B, n, H, d = q.shape
+    gp = _i32(global_pos).reshape(B, -1)
+    vl = _i32(valid_len)
+    dm = _f64(dmask) if dmask is not None else None
+    dq, dk, dv = np.empty_like(q), np.empty_like(q), np.empty_like(q)
+    dth = np.zeros(1)
+    c = ctypes.c_double
+    rc = lib().orc_soft_prune_backward(B, n, H, d, int(window), gp.shape[1], _p(gp, ctypes.c_int32),
+                                       _p(vl, ctypes.c_int32), float(alpha), _p(q, c), _p(k, c), _p(v, c),
+                                       float(theta), float(temperature), int(keep_global), _p(dy, c), _p(dm, c),
+                                       _p(dq, c), _p(dk, c), _p(dv, c), _p(dth, c), nthreads or default_threads())
+    assert rc == 0, rc
+    return dq, dk, dv, float(dth[0])
 
 
 def ltp_prune(scores32, valid_len, global_pos, threshold, keep_global=1, orig_in=None):

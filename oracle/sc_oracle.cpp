@@ -21,7 +21,10 @@
 //     (Sec. 4.2.2 step 3) and later layers see the shorter sequence (Sec. 4.2).
 //   * top-k pruning (a rank rule in place of the threshold; not the paper's
 //     rule, a variant from the token-pruning family of its Sec. 2): the
-//     ceil(keep_ratio * C) best-scored candidates per sequence are kept.
+//     ceil(keep_ratio * C) best-scored candidates per sequence are kept;
+//   * soft pruning, the training form (Sec. 4.2.2 step 1): a sigmoid soft mask
+//     of the score against the threshold scales the layer output, and its
+//     backward gives the gradients of Q, K, V and the threshold.
 // Where the paper is silent the readings are: half-width r = floor(w/2) with
 // |i - j| <= r inclusive; the softmax scale is an argument; prefix padding
 // (tokens >= valid length are neither queries nor keys); scores divided by
@@ -475,6 +478,156 @@ int orc_encoder_stack_ffn(int B, int n, int H, int d, const int32_t* windows, in
   if (!windows || !W1 || !W2) return -1;
   return encoder_stack(B, n, H, d, windows, G, global_pos, valid_len, alpha, n_layers, x, Wqkv, Wo, W1, W2, F,
                        thresholds, keep_global, ln_eps, y, final_len, orig_idx, kept_per_layer, nthreads);
+}
+
+// ---------------------------------------------------------------------------
+// LTP soft pruning, the training form of the pruning (Sec. 4.2.2 step 1: the
+// model and the per-layer thresholds are trained through a soft mask before
+// the mask is binarised).  The paper states the mask only in words; the form
+// here is the one of the Learned Token Pruning method it adopts (a reading):
+//   m_k = sigmoid((s_k - theta) / T)  for valid tokens that are not kept
+//                                     global tokens,
+//   m_k = 1 for valid global tokens when keep_global is set, 0 for padding,
+//   y[k] = m_k * out[k]               (every head and dimension of the row),
+// with s the importance score of orc_sparse_attention and T a temperature.
+// The backward takes the gradient of a loss with respect to y (dy) and,
+// optionally, an extra gradient with respect to the mask (dmask, e.g. from a
+// regulariser on the kept fraction), and applies the chain rule in the order
+// of the forward: through y = m * out to m and out; through the sigmoid to s
+// and theta; through s = (column sums of P) / (H * L) and through out = P V to
+// P; through the row softmax to the logits; through S = alpha Q K^T to Q, K.
+
+static double sigmoid(double x) { return 1.0 / (1.0 + std::exp(-x)); }
+
+// Neighbours and probabilities of valid query i of one (sequence, head), as
+// attend_one_head defines them (bidirectional).
+static void row_probs(int d, int L, int r, const std::vector<char>& is_global, double alpha, const double* q,
+                      const double* k, long ld, int i, std::vector<int>& nbr, std::vector<double>& p) {
+  nbr.clear();
+  for (int j = 0; j < L; ++j)
+    if (std::abs(i - j) <= r || is_global[i] || is_global[j]) nbr.push_back(j);
+  p.assign(nbr.size(), 0.0);
+  double m = -std::numeric_limits<double>::infinity();
+  for (size_t t = 0; t < nbr.size(); ++t) {
+    double acc = 0.0;
+    for (int c = 0; c < d; ++c) acc += q[(long)i * ld + c] * k[(long)nbr[t] * ld + c];
+    p[t] = alpha * acc;
+    m = std::max(m, p[t]);
+  }
+  double z = 0.0;
+  for (size_t t = 0; t < nbr.size(); ++t) z += std::exp(p[t] - m);
+  for (size_t t = 0; t < nbr.size(); ++t) p[t] = std::exp(p[t] - m) / z;
+}
+
+// Soft mask of every token from the scores.
+static void soft_mask(int B, int n, int G, const int32_t* global_pos, const int32_t* valid_len, const double* scores,
+                      double theta, double T, int keep_global, double* mask) {
+  for (int b = 0; b < B; ++b) {
+    int L = std::min(std::max(valid_len[b], 0), n);
+    std::vector<char> g = global_flags(n, L, G, global_pos + (long)b * G);
+    for (int k = 0; k < n; ++k) {
+      double m = 0.0;
+      if (k < L) m = (keep_global && g[k]) ? 1.0 : sigmoid((scores[(long)b * n + k] - theta) / T);
+      mask[(long)b * n + k] = m;
+    }
+  }
+}
+
+// Forward: out, lse and scores as orc_sparse_attention, then mask [B, n] and
+// y [B, n, H, d] = mask * out.
+int orc_soft_prune_forward(int B, int n, int H, int d, int window, int G, const int32_t* global_pos,
+                           const int32_t* valid_len, double alpha, const double* q, const double* k, const double* v,
+                           double theta, double T, int keep_global, double* out, double* lse, double* scores,
+                           double* mask, double* y, int nthreads) {
+  if (!(T > 0.0)) return -1;
+  int rc = sparse_attention(B, n, H, d, window, G, global_pos, valid_len, alpha, q, k, v, out, lse, scores, nullptr,
+                            false, nthreads);
+  if (rc) return rc;
+  soft_mask(B, n, G, global_pos, valid_len, scores, theta, T, keep_global, mask);
+  const long D = (long)H * d;
+  for (long t = 0; t < (long)B * n; ++t)
+    for (long c = 0; c < D; ++c) y[t * D + c] = mask[t] * out[t * D + c];
+  return 0;
+}
+
+// Backward of orc_soft_prune_forward for the loss gradient dy [B, n, H, d]
+// (with respect to y) and dmask [B, n] (with respect to the mask, or NULL).
+// Writes dq, dk, dv [B, n, H, d] and dtheta (a scalar).
+int orc_soft_prune_backward(int B, int n, int H, int d, int window, int G, const int32_t* global_pos,
+                            const int32_t* valid_len, double alpha, const double* q, const double* k, const double* v,
+                            double theta, double T, int keep_global, const double* dy, const double* dmask,
+                            double* dq, double* dk, double* dv, double* dtheta, int nthreads) {
+  if (B < 0 || n < 0 || H <= 0 || d <= 0 || window < 0 || G < 0 || !(T > 0.0)) return -1;
+  const long D = (long)H * d;
+  const size_t bnD = (size_t)B * n * D;
+  std::vector<double> out(bnD), lse((size_t)B * H * n), scores((size_t)B * n), mask((size_t)B * n);
+  int rc = sparse_attention(B, n, H, d, window, G, global_pos, valid_len, alpha, q, k, v, out.data(), lse.data(),
+                            scores.data(), nullptr, false, nthreads);
+  if (rc) return rc;
+  soft_mask(B, n, G, global_pos, valid_len, scores.data(), theta, T, keep_global, mask.data());
+  // y = m * out: dL/dm_k = sum over the row of dy * out (+ dmask), dL/dout = m * dy.
+  // m = sigmoid(z), z = (s - theta) / T: dL/ds = dL/dm * m (1 - m) / T and
+  // dL/dtheta = - sum of the same over the masked tokens.
+  std::vector<double> gs((size_t)B * n, 0.0), dout(bnD, 0.0);
+  double dth = 0.0;
+  for (int b = 0; b < B; ++b) {
+    int L = std::min(std::max(valid_len[b], 0), n);
+    std::vector<char> g = global_flags(n, L, G, global_pos + (long)b * G);
+    for (int kk = 0; kk < L; ++kk) {
+      const long t = (long)b * n + kk;
+      double dm = dmask ? dmask[t] : 0.0;
+      for (long c = 0; c < D; ++c) {
+        dm += dy[t * D + c] * out[t * D + c];
+        dout[t * D + c] = mask[t] * dy[t * D + c];
+      }
+      if (keep_global && g[kk]) continue;  // a constant mask of 1
+      const double ds = dm * mask[t] * (1.0 - mask[t]) / T;
+      // s_k = (1 / (H L)) sum_h sum_q P_h[q][k]: each P_h[q][k] receives ds / (H L)
+      gs[t] = ds / ((double)H * L);
+      dth -= ds;
+    }
+  }
+  *dtheta = dth;
+  std::fill(dq, dq + bnD, 0.0);
+  std::fill(dk, dk + bnD, 0.0);
+  std::fill(dv, dv + bnD, 0.0);
+  set_threads(nthreads);
+  const int r = window / 2;
+#pragma omp parallel for schedule(dynamic, 1)
+  for (long bh = 0; bh < (long)B * H; ++bh) {
+    int b = (int)(bh / H), h = (int)(bh % H);
+    int L = std::min(std::max(valid_len[b], 0), n);
+    std::vector<char> g = global_flags(n, L, G, global_pos + (long)b * G);
+    const long base = (long)b * n * D + (long)h * d;
+    const double *qh = q + base, *kh = k + base, *vh = v + base, *doh = dout.data() + base;
+    double *dqh = dq + base, *dkh = dk + base, *dvh = dv + base;
+    std::vector<int> nbr;
+    std::vector<double> p, dp;
+    for (int i = 0; i < L; ++i) {
+      row_probs(d, L, r, g, alpha, qh, kh, D, i, nbr, p);
+      // out_i = sum_j P[i][j] v_j and the score term: dL/dP[i][j] = dout_i . v_j + gs_j
+      dp.assign(nbr.size(), 0.0);
+      double rowdot = 0.0;  // sum_j P[i][j] dL/dP[i][j]
+      for (size_t t = 0; t < nbr.size(); ++t) {
+        const int j = nbr[t];
+        double acc = 0.0;
+        for (int c = 0; c < d; ++c) acc += doh[(long)i * D + c] * vh[(long)j * D + c];
+        dp[t] = acc + gs[(long)b * n + j];
+        rowdot += p[t] * dp[t];
+      }
+      for (size_t t = 0; t < nbr.size(); ++t) {
+        const int j = nbr[t];
+        // row softmax: dL/dS[i][j] = P[i][j] (dL/dP[i][j] - sum_l P[i][l] dL/dP[i][l]); S = alpha q_i . k_j
+        const double dsij = p[t] * (dp[t] - rowdot);
+        for (int c = 0; c < d; ++c) {
+          dqh[(long)i * D + c] += alpha * dsij * kh[(long)j * D + c];
+          dkh[(long)j * D + c] += alpha * dsij * qh[(long)i * D + c];
+          dvh[(long)j * D + c] += p[t] * doh[(long)i * D + c];
+        }
+      }
+    }
+  }
+  return 0;
 }
 
 }  // extern "C"

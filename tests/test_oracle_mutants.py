@@ -48,6 +48,24 @@ MUTANTS = [
     ("causal global rows see the future", "const int jend = causal ? std::min(i + 1, L) : L;",
      "const int jend = causal && !is_global[i] ? std::min(i + 1, L) : L;"),
     ("per-layer window ignored", "int rc = encoder_layer(B, n, H, d, windows[l],", "int rc = encoder_layer(B, n, H, d, windows[0],"),
+    ("soft mask: score gradient dropped", "gs[t] = ds / ((double)H * L);", "gs[t] = 0.0;"),
+    ("soft mask: score gradient over the padded length", "gs[t] = ds / ((double)H * L);",
+     "gs[t] = ds / ((double)H * n);"),
+    ("soft mask: sigmoid derivative missing a factor", "const double ds = dm * mask[t] * (1.0 - mask[t]) / T;",
+     "const double ds = dm * mask[t] / T;"),
+    ("soft mask: temperature ignored in the backward", "const double ds = dm * mask[t] * (1.0 - mask[t]) / T;",
+     "const double ds = dm * mask[t] * (1.0 - mask[t]);"),
+    ("soft mask: threshold gradient sign", "dth -= ds;", "dth += ds;"),
+    ("soft mask: output gradient not masked", "dout[t * D + c] = mask[t] * dy[t * D + c];",
+     "dout[t * D + c] = dy[t * D + c];"),
+    ("soft mask: softmax backward without the row term", "const double dsij = p[t] * (dp[t] - rowdot);",
+     "const double dsij = p[t] * dp[t];"),
+    ("soft mask: key gradient from the key", "dkh[(long)j * D + c] += alpha * dsij * qh[(long)i * D + c];",
+     "dkh[(long)j * D + c] += alpha * dsij * kh[(long)i * D + c];"),
+    ("soft mask: value gradient transposed", "dvh[(long)j * D + c] += p[t] * doh[(long)i * D + c];",
+     "dvh[(long)i * D + c] += p[t] * doh[(long)j * D + c];"),
+    ("soft mask: global tokens masked softly", "if (k < L) m = (keep_global && g[k]) ? 1.0 :",
+     "if (k < L) m = false ? 1.0 :"),
 ]
 
 

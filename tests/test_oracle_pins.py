@@ -575,6 +575,117 @@ def check_paper_threshold_schedule():
         assert abs(sched[int(layer) - 1] - val) < 1e-15
 
 
+# ------------------------------------------------- soft pruning (training) --
+def _soft_case(seed, T=0.02):
+    """A small case whose threshold sits at the median score, so that most masks are on the sigmoid's slope."""
+    q, k, v, vl, gp, window = rand_case(seed, B=2, n=20, H=2, d=6, G=2)
+    alpha = 0.35
+    _, _, s, _, _ = oracle.soft_prune_forward(q, k, v, vl, gp, window, alpha, 0.0, 1.0)
+    theta = float(np.median(s[s > 0]))
+    rng = np.random.default_rng(seed + 1)
+    dy = rng.standard_normal(q.shape)
+    dm = rng.standard_normal(s.shape)
+    return q, k, v, vl, gp, window, alpha, theta, T, dy, dm, rng
+
+
+def check_soft_backward_finite_differences():
+    """Central differences of the forward's loss sum(y * dy) + sum(mask * dmask) against the backward."""
+    for seed, use_dm in ((700, True), (701, False)):
+        q, k, v, vl, gp, window, alpha, theta, T, dy, dm, rng = _soft_case(seed)
+        dm = dm if use_dm else None
+
+        def loss(x, th):
+            _, _, _, m, y = oracle.soft_prune_forward(x[0], x[1], x[2], vl, gp, window, alpha, th, T)
+            return float((y * dy).sum() + ((m * dm).sum() if dm is not None else 0.0))
+
+        grads = oracle.soft_prune_backward(q, k, v, vl, gp, window, alpha, theta, T, dy, dm)
+        h = 1e-6
+        B, n, H, d = q.shape
+        for which in range(3):
+            for _ in range(8):
+                b = int(rng.integers(B))
+                idx = (b, int(rng.integers(vl[b])), int(rng.integers(H)), int(rng.integers(d)))
+                xp = [q.copy(), k.copy(), v.copy()]
+                xm = [q.copy(), k.copy(), v.copy()]
+                xp[which][idx] += h
+                xm[which][idx] -= h
+                fd = (loss(xp, theta) - loss(xm, theta)) / (2 * h)
+                an = grads[which][idx]
+                assert abs(fd - an) <= 1e-5 * abs(an) + 1e-7, (seed, which, idx, fd, an)
+        fd = (loss([q, k, v], theta + h) - loss([q, k, v], theta - h)) / (2 * h)
+        assert abs(fd - grads[3]) <= 1e-5 * abs(grads[3]) + 1e-6, (seed, fd, grads[3])
+        for b in range(B):  # padding tokens are neither queries nor keys
+            for g in grads[:3]:
+                assert np.all(g[b, vl[b]:] == 0.0)
+
+
+def _torch_soft_loss(q, k, v, vl, gp, window, alpha, theta, T, dy, dm, keep_global=1):
+    """The soft-pruned layer as dense masked attention in torch (float64); autograd gives its backward."""
+    B, n, H, d = q.shape
+    r = window // 2
+    loss = q.new_zeros(())
+    for b in range(B):
+        L = int(vl[b])
+        gf = np.zeros(n, bool)
+        for p in gp[b]:
+            if 0 <= p < L:
+                gf[p] = True
+        A = torch.from_numpy(allowed_matrix(n, L, r, gf)[:L, :L])
+        cols, outs = [], []
+        for h in range(H):
+            S = alpha * q[b, :L, h] @ k[b, :L, h].T
+            P = torch.softmax(S.masked_fill(~A, float("-inf")), dim=1)
+            cols.append(P.sum(0))
+            outs.append(P @ v[b, :L, h])
+        s = torch.stack(cols).sum(0) / (H * L)
+        gt = torch.from_numpy(gf[:L])
+        m = torch.sigmoid((s - theta) / T)
+        if keep_global:
+            m = torch.where(gt, torch.ones_like(m), m)
+        out = torch.stack(outs, 1)  # [L, H, d]
+        loss = loss + (m[:, None, None] * out * dy[b, :L]).sum() + (m * dm[b, :L]).sum()
+    return loss
+
+
+def check_soft_backward_against_autograd():
+    for seed, kg in ((710, 1), (711, 0), (712, 1)):
+        q, k, v, vl, gp, window, alpha, theta, T, dy, dm, _ = _soft_case(seed)
+        dq, dk, dv, dth = oracle.soft_prune_backward(q, k, v, vl, gp, window, alpha, theta, T, dy, dm,
+                                                     keep_global=kg)
+        tq, tk, tv = (torch.tensor(x, dtype=torch.float64, requires_grad=True) for x in (q, k, v))
+        tth = torch.tensor(theta, dtype=torch.float64, requires_grad=True)
+        loss = _torch_soft_loss(tq, tk, tv, vl, gp, window, alpha, tth, T, torch.from_numpy(dy),
+                                torch.from_numpy(dm), kg)
+        loss.backward()
+        for ours, ref in ((dq, tq.grad), (dk, tk.grad), (dv, tv.grad)):
+            ref = ref.numpy()
+            assert np.allclose(ours, ref, rtol=1e-9, atol=1e-11), float(np.abs(ours - ref).max())
+        assert abs(dth - float(tth.grad)) <= 1e-9 * abs(dth) + 1e-11, (dth, float(tth.grad))
+
+
+def check_soft_mask_limits():
+    """Temperature to 0: the soft mask becomes the binarised mask of the hard rule (Sec. 4.2.2 step 2); the
+    threshold far below every score: the mask is 1 and y is the attention output."""
+    q, k, v, vl, gp, window, alpha, theta, _, _, _, _ = _soft_case(720)
+    out, _, s, m, y = oracle.soft_prune_forward(q, k, v, vl, gp, window, alpha, theta, 1e-12)
+    B, n = s.shape
+    for b in range(B):
+        g = {int(p) for p in gp[b] if 0 <= p < vl[b]}
+        for t in range(n):
+            hard = t < vl[b] and (s[b, t] > theta or t in g)
+            if t < vl[b] and t not in g and abs(s[b, t] - theta) < 1e-9:
+                continue
+            assert m[b, t] == (1.0 if hard else 0.0), (b, t, m[b, t], s[b, t], theta)
+    assert np.array_equal(y, out * m[:, :, None, None])
+    out2, _, _, m2, y2 = oracle.soft_prune_forward(q, k, v, vl, gp, window, alpha, -1e6, 0.01)
+    valid = np.arange(n)[None, :] < vl[:, None]
+    assert np.all(m2[valid] == 1.0) and np.all(m2[~valid] == 0.0)
+    assert np.array_equal(y2, out2)
+
+
+SOFT_CHECKS = [check_soft_backward_finite_differences, check_soft_backward_against_autograd,
+               check_soft_mask_limits]
+
 ATTENTION_CHECKS = [check_brute_force, check_causal_brute_force, check_causal_dense_is_library_causal_attention,
                     check_window_covers_sequence_is_dense, check_all_global_is_dense,
                     check_zero_window_no_global, check_constant_values, check_zero_queries_rational_scores,
@@ -585,7 +696,7 @@ PRUNE_CHECKS = [check_prune_brute_force, check_prune_invariants, check_mask_rule
 STACK_CHECKS = [check_bf16_rounding, check_encoder_layer_against_libraries, check_layernorm_statistics,
                 check_stack_composition, check_ffn_layer_against_libraries, check_ffn_zero_output_weights,
                 check_full_stack_composition]
-ALL_CHECKS = ATTENTION_CHECKS + PRUNE_CHECKS + STACK_CHECKS + [check_paper_threshold_schedule]
+ALL_CHECKS = ATTENTION_CHECKS + PRUNE_CHECKS + STACK_CHECKS + SOFT_CHECKS + [check_paper_threshold_schedule]
 
 
 @pytest.mark.parametrize("check", ALL_CHECKS, ids=lambda f: f.__name__[6:])
