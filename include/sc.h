@@ -22,6 +22,9 @@
  *   sc_topk_prune_compact the same compaction with a top-k rule instead of the
  *                         threshold (a variant in the family of cascade token
  *                         pruning the paper cites in Sec. 2);
+ *   sc_ltp_soft_mask      the soft mask of LTP's training phase (Sec. 4.2.2
+ *                         step 1) and sc_ltp_soft_backward, the gradients of
+ *                         q, k, v and the threshold through it;
  *   sc_encoder_stack      the full encoder stack: the layers above with a GELU
  *                         feed-forward block and a window per layer;
  *   sc_encoder_attn_stack the attention-only encoder stack (QKV projection,
@@ -212,6 +215,51 @@ sc_status sc_topk_prune_compact(const sc_attn_desc *desc, const float *scores, f
                                 int32_t *keep_idx, int32_t *new_len, int32_t *new_global_pos,
                                 const int32_t *orig_idx_in, int32_t *orig_idx_out, void *workspace, size_t ws_bytes,
                                 void *stream);
+
+/*
+ * LTP soft pruning, the training form of the pruning (Sec. 4.2.2 step 1: the
+ * model and the per-layer thresholds are trained through a soft mask, which
+ * is binarised afterwards).  The paper describes the mask in words only; the
+ * form here is the one of the Learned Token Pruning method it adopts:
+ *   mask[b,k] = sigmoid((scores[b,k] - theta) / temperature)  for k < L_b,
+ *               except 1 for global tokens when keep_global is set,
+ *   mask[b,k] = 0 for k >= L_b,
+ *   y[b,k,:,:] = bf16(mask[b,k] * out[b,k,:,:]).
+ * As temperature goes to 0 the mask becomes the binarised mask of
+ * sc_ltp_prune_compact.
+ *   scores      float32 [B, n] (sc_ltp_score).
+ *   out         bf16 [B, n, H, d] (sc_window_attention's output).
+ *   mask        float32 [B, n], written.   y  bf16 [B, n, H, d], written.
+ * desc->dtype must be SC_BF16 and causal 0 (else SC_EUNSUPPORTED); theta
+ * finite and temperature > 0 (else SC_EINVAL).  y must not overlap out.
+ */
+sc_status sc_ltp_soft_mask(const sc_attn_desc *desc, const float *scores, float theta, float temperature,
+                           int32_t keep_global, const void *out, float *mask, void *y, void *stream);
+
+size_t sc_ltp_soft_backward_workspace_size(const sc_attn_desc *desc);
+
+/*
+ * Backward of the soft-pruned layer y = mask * attention(q, k, v), with the
+ * mask computed from the layer's own importance scores (the sigmoid above of
+ * s_k = (1 / (H L)) sum_h sum_q P_h[q][k]).  Given dy = dL/dy and optionally
+ * dmask = dL/dmask (e.g. a regulariser on the kept fraction), it writes
+ *   dq, dk, dv  bf16 [B, n, H, d]: dL/dq, dL/dk, dL/dv through the attention
+ *               output and through the scores (0 on padding rows);
+ *   dtheta      one float32 (device): dL/dtheta.
+ * Inputs: q, k, v, out bf16 [B, n, H, d] and lse float32 [B, H, n] of the
+ * forward sc_window_attention (same desc), mask float32 [B, n] of
+ * sc_ltp_soft_mask, dy bf16 [B, n, H, d], dmask float32 [B, n] or NULL, and
+ * the temperature and keep_global of the forward.  Probabilities are
+ * recomputed from q, k and lse in float32; products run on bf16 MFMA with
+ * float32 accumulation; dL/dmask is accumulated in float32.  Deterministic
+ * (fixed-order sums, no atomics).  desc->dtype must be SC_BF16 and causal 0
+ * (else SC_EUNSUPPORTED).  Outputs must not overlap each other, the inputs
+ * or the workspace.
+ */
+sc_status sc_ltp_soft_backward(const sc_attn_desc *desc, const void *q, const void *k, const void *v,
+                               const void *out, const float *lse, const float *mask, float temperature,
+                               int32_t keep_global, const void *dy, const float *dmask, void *dq, void *dk,
+                               void *dv, float *dtheta, void *workspace, size_t ws_bytes, void *stream);
 
 size_t sc_encoder_attn_stack_workspace_size(const sc_attn_desc *desc, int32_t n_layers);
 

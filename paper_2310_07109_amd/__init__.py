@@ -11,7 +11,8 @@ from ._binding import (SC_BF16, SC_F32, SC_SCORE_FROM_BAND_PROBS, SC_SCORE_FROM_
                        lib_path, load, sc_band_probs_size, sc_encoder_attn_stack,
                        sc_encoder_attn_stack_workspace_size, sc_encoder_stack, sc_encoder_stack_workspace_size,
                        sc_ltp_prune_compact, sc_ltp_prune_compact_workspace_size, sc_ltp_score,
-                       sc_ltp_score_workspace_size, sc_profile_window_kernel, sc_profile_window_kernel_read,
+                       sc_ltp_score_workspace_size, sc_ltp_soft_backward,
+                       sc_ltp_soft_backward_workspace_size, sc_ltp_soft_mask, sc_profile_window_kernel, sc_profile_window_kernel_read,
                        sc_score_partials_size, sc_status_str, sc_topk_prune_compact, sc_window_attention,
                        sc_window_attention_workspace_size)
 
@@ -20,6 +21,7 @@ __all__ = [
     "lib_path", "sc_status_str", "sc_score_partials_size", "sc_band_probs_size",
     "sc_window_attention_workspace_size", "sc_window_attention", "sc_ltp_score_workspace_size", "sc_ltp_score",
     "sc_ltp_prune_compact_workspace_size", "sc_ltp_prune_compact", "sc_topk_prune_compact",
+    "sc_ltp_soft_mask", "sc_ltp_soft_backward_workspace_size", "sc_ltp_soft_backward",
     "sc_encoder_attn_stack_workspace_size", "sc_encoder_attn_stack", "sc_encoder_stack_workspace_size",
     "sc_encoder_stack", "sc_profile_window_kernel", "sc_profile_window_kernel_read",
 ]

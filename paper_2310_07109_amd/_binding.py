@@ -52,6 +52,9 @@ def load():
         "sc_ltp_prune_compact_workspace_size": (sz, [dp]),
         "sc_ltp_prune_compact": (i32, [dp, vp, f32, i32, i32, vp, vp, vp, vp, vp, vp, vp, vp, vp, sz, vp]),
         "sc_topk_prune_compact": (i32, [dp, vp, f32, i32, i32, vp, vp, vp, vp, vp, vp, vp, vp, vp, sz, vp]),
+        "sc_ltp_soft_mask": (i32, [dp, vp, f32, f32, i32, vp, vp, vp, vp]),
+        "sc_ltp_soft_backward_workspace_size": (sz, [dp]),
+        "sc_ltp_soft_backward": (i32, [dp, vp, vp, vp, vp, vp, vp, f32, i32, vp, vp, vp, vp, vp, vp, vp, sz, vp]),
         "sc_encoder_attn_stack_workspace_size": (sz, [dp, i32]),
         "sc_encoder_attn_stack": (i32, [dp, i32, vp, vp, vp, vp, i32, f32, vp, vp, vp, vp, vp, sz, vp]),
         "sc_encoder_stack_workspace_size": (sz, [dp, i32, i32]),
@@ -226,6 +229,44 @@ def _prune_compact(fn, desc, scores, value, keep_global, tensors, dsts, orig_idx
                           dst_arr, rb_arr, _ptr(keep_idx), _ptr(new_len), _ptr(ngp), _ptr(orig_idx_in),
                           _ptr(orig_out), _ptr(ws), wsb, _stream(stream)), fn)
     return keep_idx, new_len, ngp, orig_out, dsts
+
+
+def sc_ltp_soft_mask(desc: Desc, scores, theta, temperature, out, keep_global=True, mask=None, y=None,
+                     stream=None):
+    """Soft mask of LTP's training phase.  Returns (mask [B, n] float32, y = mask * out)."""
+    import torch
+    L = load()
+    mask = torch.empty((desc.B, desc.n), dtype=torch.float32, device=out.device) if mask is None else mask
+    y = torch.empty_like(out) if y is None else y
+    _check(L.sc_ltp_soft_mask(ctypes.byref(desc.c()), _ptr(scores), ctypes.c_float(theta),
+                              ctypes.c_float(temperature), int(bool(keep_global)), _ptr(out), _ptr(mask), _ptr(y),
+                              _stream(stream)), "sc_ltp_soft_mask")
+    return mask, y
+
+
+def sc_ltp_soft_backward_workspace_size(desc: Desc) -> int:
+    return load().sc_ltp_soft_backward_workspace_size(ctypes.byref(desc.c()))
+
+
+def sc_ltp_soft_backward(desc: Desc, q, k, v, out, lse, mask, temperature, dy, dmask=None, keep_global=True,
+                         grads=None, workspace=None, stream=None):
+    """Gradients of the soft-pruned layer.  Returns (dq, dk, dv, dtheta [1] float32 on the device).
+    grads: optional (dq, dk, dv, dtheta) output tensors."""
+    import torch
+    L = load()
+    cd = desc.c()
+    if grads is None:
+        grads = (torch.empty_like(q), torch.empty_like(k), torch.empty_like(v),
+                 torch.empty(1, dtype=torch.float32, device=q.device))
+    dq, dk, dv, dth = grads
+    wsb = L.sc_ltp_soft_backward_workspace_size(ctypes.byref(cd))
+    ws = _ws(wsb, q.device) if workspace is None else workspace
+    wsb = wsb if workspace is None else workspace.numel() * workspace.element_size()
+    _check(L.sc_ltp_soft_backward(ctypes.byref(cd), _ptr(q), _ptr(k), _ptr(v), _ptr(out), _ptr(lse), _ptr(mask),
+                                  ctypes.c_float(temperature), int(bool(keep_global)), _ptr(dy), _ptr(dmask),
+                                  _ptr(dq), _ptr(dk), _ptr(dv), _ptr(dth), _ptr(ws), wsb, _stream(stream)),
+           "sc_ltp_soft_backward")
+    return dq, dk, dv, dth
 
 
 def sc_encoder_attn_stack_workspace_size(desc: Desc, n_layers: int) -> int:

@@ -13,7 +13,7 @@ HERE = os.path.dirname(os.path.abspath(__file__))
 CSRC = os.path.join(HERE, "csrc")
 OUT = os.path.join(HERE, "libsc.so")
 BUILD_DIR = os.path.join(HERE, "_build")
-SOURCES = ["sc_attention.hip", "sc_prune.hip", "sc_stack.hip", "sc_api.hip"]
+SOURCES = ["sc_attention.hip", "sc_prune.hip", "sc_stack.hip", "sc_backward.hip", "sc_api.hip"]
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 ARCH = "gfx950"
 FLAGS = [

@@ -296,6 +296,129 @@ sc_status sc_topk_prune_compact(const sc_attn_desc* d, const float* scores, floa
                        new_global_pos, orig_idx_in, orig_idx_out, workspace, ws_bytes, stream);
 }
 
+// ------------------------------------------------------------ soft pruning --
+namespace {
+
+bool soft_desc_ok(const sc_attn_desc* d, sc_status* st) {
+  *st = check_desc(d);
+  if (*st != SC_OK) return false;
+  if (d->dtype != SC_BF16 || d->causal) {
+    *st = SC_EUNSUPPORTED;
+    return false;
+  }
+  return true;
+}
+
+// Workspace pieces of the backward (pointers null when base is null).
+size_t carve_soft(const sc_attn_desc* d, void* base, sc::SoftArgs* a) {
+  Carver c(base);
+  const size_t bn = (size_t)d->B * d->n, bhn = bn * d->H;
+  const int nsp = (d->n + sc::kBwdSpan - 1) / sc::kBwdSpan, Gp = ((d->G + 63) / 64) * 64;
+  const size_t part = (size_t)d->B * d->H * nsp * Gp;
+  a->dO = c.take<__bf16>(bhn * 64);
+  a->Dq = c.take<float>(bhn);
+  a->gk = c.take<float>(bn);
+  a->dsv = c.take<float>(bn);
+  a->gpg = c.take<float>(part > 0 ? part : 1);
+  a->gdq = c.take<float>(part > 0 ? part * 64 : 1);
+  a->gdk = c.take<float>(part > 0 ? part * 64 : 1);
+  a->gdv = c.take<float>(part > 0 ? part * 64 : 1);
+  a->nsp = nsp;
+  a->Gp = Gp;
+  return c.off;
+}
+
+sc::SoftArgs soft_args(const sc_attn_desc* d) {
+  sc::SoftArgs a;
+  std::memset(&a, 0, sizeof(a));
+  a.B = d->B;
+  a.n = d->n;
+  a.H = d->H;
+  a.G = d->G;
+  a.r = d->window / 2 < d->n ? d->window / 2 : d->n;
+  a.valid_len = d->valid_len;
+  a.gpos = d->G > 0 ? d->global_pos : nullptr;
+  a.alpha = d->softmax_scale;
+  a.c2 = d->softmax_scale * 1.4426950408889634f;
+  return a;
+}
+
+}  // namespace
+
+sc_status sc_ltp_soft_mask(const sc_attn_desc* d, const float* scores, float theta, float temperature,
+                           int32_t keep_global, const void* out, float* mask, void* y, void* stream) {
+  sc_status st;
+  if (!soft_desc_ok(d, &st)) return st;
+  if (!scores || !out || !mask || !y) return SC_EINVAL;
+  if (!std::isfinite(theta) || !(temperature > 0.f) || !std::isfinite(temperature)) return SC_EINVAL;
+  const size_t tb = tensor_bytes(d), sb = sizeof(float) * (size_t)d->B * d->n;
+  if (overlaps(y, tb, out, tb) || overlaps(y, tb, scores, sb) || overlaps(y, tb, mask, sb) ||
+      overlaps(mask, sb, scores, sb) || overlaps(mask, sb, out, tb))
+    return SC_EINVAL;
+  sc::SoftArgs a = soft_args(d);
+  a.scores = scores;
+  a.o = static_cast<const __bf16*>(out);
+  a.mask_out = mask;
+  a.y = static_cast<__bf16*>(y);
+  a.theta = theta;
+  a.inv_t = 1.f / temperature;
+  a.keep_global = keep_global ? 1 : 0;
+  return sc::launch_soft_mask(a, static_cast<hipStream_t>(stream)) == hipSuccess ? SC_OK : SC_EHIP;
+}
+
+size_t sc_ltp_soft_backward_workspace_size(const sc_attn_desc* d) {
+  sc_status st;
+  if (!soft_desc_ok(d, &st)) return 0;
+  sc::SoftArgs a;
+  return carve_soft(d, nullptr, &a);
+}
+
+sc_status sc_ltp_soft_backward(const sc_attn_desc* d, const void* q, const void* k, const void* v, const void* out,
+                               const float* lse, const float* mask, float temperature, int32_t keep_global,
+                               const void* dy, const float* dmask, void* dq, void* dk, void* dv, float* dtheta,
+                               void* workspace, size_t ws_bytes, void* stream) {
+  sc_status st;
+  if (!soft_desc_ok(d, &st)) return st;
+  if (!q || !k || !v || !out || !lse || !mask || !dy || !dq || !dk || !dv || !dtheta) return SC_EINVAL;
+  if (!(temperature > 0.f) || !std::isfinite(temperature)) return SC_EINVAL;
+  const size_t need = sc_ltp_soft_backward_workspace_size(d);
+  if (!workspace || ws_bytes < need) return SC_EWORKSPACE;
+  const size_t tb = tensor_bytes(d), sb = sizeof(float) * (size_t)d->B * d->n;
+  const size_t lb = sizeof(float) * (size_t)d->B * d->H * d->n;
+  const void* ins[] = {q, k, v, out, dy};
+  const void* outs[] = {dq, dk, dv};
+  for (const void* o : outs) {
+    for (const void* i : ins)
+      if (overlaps(o, tb, i, tb)) return SC_EINVAL;
+    if (overlaps(o, tb, lse, lb) || overlaps(o, tb, mask, sb) || overlaps(o, tb, workspace, need) ||
+        overlaps(o, tb, dtheta, sizeof(float)) || (dmask && overlaps(o, tb, dmask, sb)))
+      return SC_EINVAL;
+  }
+  if (overlaps(dq, tb, dk, tb) || overlaps(dq, tb, dv, tb) || overlaps(dk, tb, dv, tb)) return SC_EINVAL;
+  for (const void* i : ins)
+    if (overlaps(workspace, need, i, tb)) return SC_EINVAL;
+  if (overlaps(workspace, need, lse, lb) || overlaps(workspace, need, mask, sb) ||
+      overlaps(workspace, need, dtheta, sizeof(float)) || (dmask && overlaps(workspace, need, dmask, sb)))
+    return SC_EINVAL;
+  sc::SoftArgs a = soft_args(d);
+  carve_soft(d, workspace, &a);
+  a.q = static_cast<const __bf16*>(q);
+  a.k = static_cast<const __bf16*>(k);
+  a.v = static_cast<const __bf16*>(v);
+  a.o = static_cast<const __bf16*>(out);
+  a.dy = static_cast<const __bf16*>(dy);
+  a.lse = lse;
+  a.mask = mask;
+  a.dmask = dmask;
+  a.dq = static_cast<__bf16*>(dq);
+  a.dk = static_cast<__bf16*>(dk);
+  a.dv = static_cast<__bf16*>(dv);
+  a.dtheta = dtheta;
+  a.inv_t = 1.f / temperature;
+  a.keep_global = keep_global ? 1 : 0;
+  return sc::launch_soft_backward(a, static_cast<hipStream_t>(stream)) == hipSuccess ? SC_OK : SC_EHIP;
+}
+
 // ------------------------------------------------------------------ stack --
 namespace {
 

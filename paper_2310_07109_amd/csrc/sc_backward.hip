@@ -1,0 +1,604 @@
+// LTP soft pruning on gfx950: the training form of the pruning (SparseCoder,
+// arXiv 2310.07109, Sec. 4.2.2 step 1: the model and the per-layer
+// thresholds are trained through a soft mask before the mask is binarised)
+// and its backward through the sparse attention and the importance scores.
+//
+// Forward (k_soft_mask, one wave per token):
+//   m_k = sigmoid((s_k - theta) / T) for valid tokens that are not kept
+//   global tokens, 1 for those, 0 for padding;  y[k] = m_k * out[k].
+//
+// Backward, given dL/dy and optionally dL/dm (e.g. from a regulariser):
+//   k_soft_rows     one wave per token: dO = bf16(m * dy); dm = sum dy * out
+//                   (+ dL/dm); ds = dm m (1 - m) / T (0 for kept global
+//                   tokens and padding); g = ds / (H L); D = dO . out per head.
+//   k_bwd_rows<0>   D_q += sum_j P[q][j] g_j (the score's share of the row
+//                   term of the softmax backward).
+//   k_bwd_dfin      D of the global query rows from their span partials.
+//   k_bwd_rows<1>   dQ_q = alpha sum_j dS[q][j] K_j, with
+//                   dS = P (dO_q . V_j + g_j - D_q) and P = exp2(S c2 - LSE2)
+//                   recomputed from the forward's LSE.
+//   k_bwd_cols      dK_j = alpha sum_q dS[q][j] Q_q, dV_j = sum_q P[q][j] dO_q.
+//   k_bwd_finish    the global rows' dQ and the global keys' dK, dV from their
+//                   span partials; dtheta = -sum ds.
+// Row-side work (D, dQ) is done per 64-query block over the block's band key
+// tiles plus tiles of gathered global keys, and per (64 global query rows,
+// 512-key span) for the global rows.  Column-side work (dK, dV) is done per
+// 64-key block over its band query tiles plus tiles of gathered global query
+// rows, and per (64 global keys, 512-query span) for the global keys.  Each
+// allowed pair is counted once on each side: (q, k) with k global lives in the
+// global-key tiles and the global-column blocks, q global in the global-row
+// blocks and the global-query tiles, the rest in the band.  Every sum has a
+// fixed order; no atomics.
+//
+// MFMA layouts are the forward's: S^T = K Q^T puts a query in each lane and
+// 4 keys per register (row side), S = Q K^T a key in each lane and 4 queries
+// per register (column side); the second product of each side reads its
+// row-major LDS tile with transposed reads, rows in MFMA k order.
+#include "sc_device.h"
+#include "sc_internal.h"
+
+namespace sc {
+namespace {
+
+using TRb = Tr<1>;
+
+SC_DEV float wave_sum(float v) {
+#pragma unroll
+  for (int off = 32; off > 0; off >>= 1) v += __shfl_xor(v, off, 64);
+  return v;
+}
+
+// Whether token k of the sequence is a used global slot (G small: one pass of
+// the wave over the slots).
+SC_DEV bool wave_is_global(const int* gp, int G, int k) {
+  bool hit = false;
+  for (int j = threadIdx.x & 63; j < G; j += 64) hit |= gp[j] == k;
+  return __builtin_amdgcn_ballot_w64(hit) != 0ull;
+}
+
+// ------------------------------------------------------------ forward mask --
+__global__ __launch_bounds__(256) void k_soft_mask(SoftArgs a) {
+  const int w = threadIdx.x >> 6, lane = threadIdx.x & 63;
+  const long long t = (long long)blockIdx.x * 4 + w;
+  if (t >= (long long)a.B * a.n) return;
+  const int b = (int)(t / a.n), k = (int)(t % a.n);
+  const int L = clampi(a.valid_len[b], 0, a.n);
+  const long long ld = (long long)a.H * kHeadDim;
+  float m = 0.f;
+  if (k < L) {
+    const bool g = a.keep_global && a.gpos && wave_is_global(a.gpos + (long long)b * a.G, a.G, k);
+    m = g ? 1.f : 1.f / (1.f + __expf(-(a.scores[t] - a.theta) * a.inv_t));
+  }
+  if (lane == 0) a.mask_out[t] = m;
+  const __bf16* o = a.o + t * ld;
+  __bf16* y = a.y + t * ld;
+  for (int u = lane; u < a.H * 8; u += 64) {
+    bf16x8 x = *reinterpret_cast<const bf16x8*>(o + 8 * u);
+#pragma unroll
+    for (int e = 0; e < 8; ++e) x[e] = (__bf16)(m * (float)x[e]);
+    *reinterpret_cast<bf16x8*>(y + 8 * u) = x;
+  }
+}
+
+// ------------------------------------------------------------- row terms --
+__global__ __launch_bounds__(256) void k_soft_rows(SoftArgs a) {
+  const int w = threadIdx.x >> 6, lane = threadIdx.x & 63;
+  const long long t = (long long)blockIdx.x * 4 + w;
+  if (t >= (long long)a.B * a.n) return;
+  const int b = (int)(t / a.n), k = (int)(t % a.n), H = a.H;
+  const int L = clampi(a.valid_len[b], 0, a.n);
+  const long long ld = (long long)H * kHeadDim;
+  const __bf16* dy = a.dy + t * ld;
+  const __bf16* o = a.o + t * ld;
+  __bf16* dO = a.dO + t * ld;
+  float* Dq = a.Dq + (long long)b * H * a.n + k;  // head h at Dq[h * n]
+  if (k >= L) {
+    for (int u = lane; u < H * 8; u += 64) *reinterpret_cast<uint4*>(dO + 8 * u) = make_uint4(0, 0, 0, 0);
+    for (int h = lane; h < H; h += 64) Dq[(long long)h * a.n] = 0.f;
+    if (lane == 0) {
+      a.gk[t] = 0.f;
+      a.dsv[t] = 0.f;
+    }
+    return;
+  }
+  const float m = a.mask[t];
+  float dm = 0.f;
+  // 16-byte units: unit u holds dims 8(u % 8) .. of head u / 8; in each pass
+  // of the wave, lanes 8j .. 8j + 7 hold the whole of one head
+  for (int base = 0; base < H * 8; base += 64) {
+    const int u = base + lane;
+    float hd = 0.f;
+    if (u < H * 8) {
+      const bf16x8 yv = *reinterpret_cast<const bf16x8*>(dy + 8 * u);
+      const bf16x8 ov = *reinterpret_cast<const bf16x8*>(o + 8 * u);
+      bf16x8 dv;
+#pragma unroll
+      for (int e = 0; e < 8; ++e) {
+        const float yf = (float)yv[e], of = (float)ov[e];
+        dm = fmaf(yf, of, dm);
+        dv[e] = (__bf16)(m * yf);
+        hd = fmaf((float)dv[e], of, hd);
+      }
+      *reinterpret_cast<bf16x8*>(dO + 8 * u) = dv;
+    }
+    hd += __shfl_xor(hd, 1, 64);
+    hd += __shfl_xor(hd, 2, 64);
+    hd += __shfl_xor(hd, 4, 64);
+    if ((lane & 7) == 0 && u < H * 8) Dq[(long long)(u >> 3) * a.n] = hd;
+  }
+  dm = wave_sum(dm);
+  if (a.dmask) dm += a.dmask[t];
+  const bool g = a.keep_global && a.gpos && wave_is_global(a.gpos + (long long)b * a.G, a.G, k);
+  const float ds = g ? 0.f : dm * m * (1.f - m) * a.inv_t;
+  if (lane == 0) {
+    a.gk[t] = ds / ((float)H * (float)L);
+    a.dsv[t] = ds;
+  }
+}
+
+// ---------------------------------------------------------- tile helpers --
+// Rows 16w .. 16w + 15 of a 64-row tile of a [*, ld] bf16 tensor; tile row R
+// holds tensor row rows[R] (or row 0, unused, where rows[R] < 0).
+SC_DEV void load_rows(const __bf16* base, unsigned ld_bytes, __bf16* tile, int w, const int* rows) {
+  const int lane = opaque_lane();
+#pragma unroll
+  for (int j = 0; j < 2; ++j) {
+    const int R0 = 16 * w + 8 * j, R = R0 + (lane >> 3);
+    const unsigned u = (lane & 7) ^ (lane >> 3);
+    const int row = rows[R];
+    lds_dma16(base, (unsigned)(row >= 0 ? row : 0) * ld_bytes + 16u * u, lds_addr(tile + R0 * TRb::kPitch));
+  }
+}
+
+// acc[dt] += A^T B where A is a 64-row bf16 tile (rows in MFMA k order:
+// lane (g, lr) supplies dims 16 dt + 4 (lr & 3) .. of rows 32 kc + 4g + lr / 4
+// and 32 kc + 16 + 4g + lr / 4) and B the packed bf16 operand of chunk kc.
+SC_DEV void mma_tr(const __bf16* tile, const bf16x8 (&pb)[2], f32x4 (&acc)[4]) {
+  const int ln = opaque_lane(), lr = ln & 15, g = ln >> 4;
+#pragma unroll
+  for (int kc = 0; kc < 2; ++kc) {
+    const int vr = 32 * kc + 4 * g + (lr >> 2), bsel = (lr >> 1) & 1, e = 4 * (lr & 1);
+#pragma unroll
+    for (int dt = 0; dt < 4; ++dt) {
+      const i16x4 a0 = lds_read_tr16(tile + TRb::off(vr, 2 * dt + bsel) + e);
+      const i16x4 a1 = lds_read_tr16(tile + TRb::off(vr + 16, 2 * dt + bsel) + e);
+      const bf16x8 af = __builtin_bit_cast(bf16x8, __builtin_shufflevector(a0, a1, 0, 1, 2, 3, 4, 5, 6, 7));
+      acc[dt] = TRb::mma(af, pb[kc], acc[dt]);
+    }
+  }
+}
+
+// s[st] = A_st B^T for the four 16-row sub-tiles of an LDS tile A (rows
+// 16 st + lr) and a register operand B of the wave's 16 rows.
+SC_DEV void mma_rows(const __bf16* tile, const bf16x8 (&bf)[2], f32x4 (&s)[4], int lr, int g) {
+#pragma unroll
+  for (int st = 0; st < 4; ++st) {
+    bf16x8 af[2];
+    TRb::load_frags(tile, 16 * st + lr, g, af);
+    f32x4 c = f32x4{0.f, 0.f, 0.f, 0.f};
+    c = TRb::mma(af[0], bf[0], c);
+    c = TRb::mma(af[1], bf[1], c);
+    s[st] = c;
+  }
+}
+
+// The global-token bitmask of a sequence in LDS (band blocks).
+SC_DEV void build_bits(uint32_t* bits, const int* gp, int G, int L, int n) {
+  const int nw = (n + 31) >> 5;
+  for (int i = threadIdx.x; i < nw; i += blockDim.x) bits[i] = 0u;
+  __syncthreads();
+  if (gp)
+    for (int j = threadIdx.x; j < G; j += blockDim.x) {
+      const int p = gp[j];
+      if (p >= 0 && p < L) atomicOr(&bits[p >> 5], 1u << (p & 31));
+    }
+  __syncthreads();
+}
+
+SC_DEV bool bit_of(const uint32_t* bits, int t) { return (bits[t >> 5] >> (t & 31)) & 1u; }
+
+SC_DEV void store4_bf16(__bf16* p, f32x4 v, float scale) {
+  bf16x4 x;
+#pragma unroll
+  for (int i = 0; i < 4; ++i) x[i] = (__bf16)(v[i] * scale);
+  *reinterpret_cast<bf16x4*>(p) = x;
+}
+
+// ------------------------------------------------------------- row side --
+// kMode 0: D += P g;  kMode 1: dQ.  kGRows: global-row blocks (64 gathered
+// global queries x one 512-key span) instead of band blocks (64 queries).
+template <int kMode, bool kGRows>
+__global__ __launch_bounds__(256) void k_bwd_rows(SoftArgs a) {
+  __shared__ __align__(16) __bf16 sK[64 * 64];
+  __shared__ __align__(16) __bf16 sV[kMode == 1 ? 64 * 64 : 8];
+  __shared__ __align__(16) int sRow[64];
+  __shared__ __align__(16) float sG[64];
+  extern __shared__ uint32_t sBits[];
+  const int tid = threadIdx.x, lane = tid & 63, w = __builtin_amdgcn_readfirstlane(tid >> 6), lr = lane & 15,
+            g = lane >> 4;
+  const int H = a.H, n = a.n, G = a.G, r = a.r;
+  int blk = blockIdx.x, bh, q0 = 0, span = 0, gc = 0;
+  if constexpr (!kGRows) {
+    const int nqb = (n + 63) / 64;
+    q0 = 64 * (blk % nqb);
+    bh = blk / nqb;
+  } else {
+    span = blk % a.nsp;
+    blk /= a.nsp;
+    const int ngc = a.Gp / 64;
+    gc = blk % ngc;
+    bh = blk / ngc;
+  }
+  const int b = bh / H, h = bh % H;
+  const int L = clampi(a.valid_len[b], 0, n);
+  const int* gp = a.gpos ? a.gpos + (long long)b * G : nullptr;
+  const long long ld = (long long)H * kHeadDim;
+  const unsigned ldb = (unsigned)(2 * ld);
+  const long long seq = (long long)b * n * ld + (long long)h * kHeadDim;
+  if constexpr (!kGRows) {
+    if (q0 >= L) {
+      if (kMode == 1)  // padding queries: zero gradient rows
+        for (int i = tid; i < 64 * 8; i += 256) {
+          const int q = q0 + i / 8;
+          if (q < n) *reinterpret_cast<uint4*>(a.dq + seq + q * ld + 8 * (i % 8)) = make_uint4(0, 0, 0, 0);
+        }
+      return;
+    }
+    build_bits(sBits, gp, G, L, n);
+  } else {
+    if (span * kBwdSpan >= L) return;
+  }
+  // this lane's query
+  int q, slot = 0;
+  bool qok;
+  if constexpr (!kGRows) {
+    q = q0 + 16 * w + lr;
+    qok = q < L && !bit_of(sBits, q);
+  } else {
+    slot = 64 * gc + 16 * w + lr;
+    q = (gp && slot < G) ? gp[slot] : -1;
+    qok = q >= 0 && q < L;
+  }
+  const int qs = qok ? q : 0;
+  bf16x8 qf[2], df[2];
+  qf[0] = *reinterpret_cast<const bf16x8*>(a.q + seq + qs * ld + 8 * g);
+  qf[1] = *reinterpret_cast<const bf16x8*>(a.q + seq + qs * ld + 32 + 8 * g);
+  if constexpr (kMode == 1) {
+    df[0] = *reinterpret_cast<const bf16x8*>(a.dO + seq + qs * ld + 8 * g);
+    df[1] = *reinterpret_cast<const bf16x8*>(a.dO + seq + qs * ld + 32 + 8 * g);
+  }
+  const long long dqi = (long long)bh * n + qs;
+  const float lse2 = qok ? a.lse[dqi] * kLog2e : 0.f;
+  const float Dv = (kMode == 1 && qok) ? a.Dq[dqi] : 0.f;
+  const float c2 = a.c2;
+  // key tiles: the band, then the gathered global keys (band blocks); or the span
+  int kt0, kt1, ngt = 0;
+  if constexpr (!kGRows) {
+    kt0 = max(0, q0 - r);
+    kt1 = min(L, q0 + 64 + r);
+    ngt = gp ? (G + 63) / 64 : 0;
+  } else {
+    kt0 = span * kBwdSpan;
+    kt1 = min(L, kt0 + kBwdSpan);
+  }
+  const int nband = (kt1 - kt0 + 63) / 64;
+  float pg = 0.f;
+  f32x4 acc[4];
+#pragma unroll
+  for (int dt = 0; dt < 4; ++dt) acc[dt] = f32x4{0.f, 0.f, 0.f, 0.f};
+  for (int t = 0; t < nband + ngt; ++t) {
+    const bool gtile = t >= nband;
+    const int kbase = gtile ? 64 * (t - nband) : kt0 + 64 * t;
+    if (tid < 64) {
+      int key;
+      if (!gtile) {
+        key = kbase + tid;
+        if (key >= kt1 || (!kGRows && bit_of(sBits, key))) key = -1;
+      } else {
+        key = kbase + tid < G ? gp[kbase + tid] : -1;
+        if (key >= L) key = -1;
+      }
+      sRow[tid] = key;
+      sG[tid] = key >= 0 ? a.gk[(long long)b * n + key] : 0.f;
+    }
+    __syncthreads();
+    load_rows(a.k + seq, ldb, sK, w, sRow);
+    if constexpr (kMode == 1) load_rows(a.v + seq, ldb, sV, w, sRow);
+    wait_dma();
+    __syncthreads();
+    f32x4 s[4];
+    mma_rows(sK, qf, s, lr, g);
+    float p[4][4];
+#pragma unroll
+    for (int st = 0; st < 4; ++st) {
+      const int4 rows = *reinterpret_cast<const int4*>(sRow + 16 * st + 4 * g);
+      const int rr[4] = {rows.x, rows.y, rows.z, rows.w};
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        const int key = rr[i];
+        const bool ok = qok && key >= 0 && (gtile || kGRows || abs(q - key) <= r);
+        p[st][i] = ok ? fast_exp2(fmaf(s[st][i], c2, -lse2)) : 0.f;
+      }
+    }
+    if constexpr (kMode == 0) {
+#pragma unroll
+      for (int st = 0; st < 4; ++st) {
+        const f32x4 gg = *reinterpret_cast<const f32x4*>(sG + 16 * st + 4 * g);
+#pragma unroll
+        for (int i = 0; i < 4; ++i) pg = fmaf(p[st][i], gg[i], pg);
+      }
+    } else {
+      f32x4 dp[4];
+      mma_rows(sV, df, dp, lr, g);
+      bf16x8 pb[2];
+#pragma unroll
+      for (int st = 0; st < 4; ++st) {
+        const f32x4 gg = *reinterpret_cast<const f32x4*>(sG + 16 * st + 4 * g);
+#pragma unroll
+        for (int i = 0; i < 4; ++i) pb[st >> 1][4 * (st & 1) + i] = (__bf16)(p[st][i] * (dp[st][i] + gg[i] - Dv));
+      }
+      mma_tr(sK, pb, acc);
+    }
+    __syncthreads();  // the next tile overwrites sK, sV, sRow, sG
+  }
+  if constexpr (kMode == 0) {
+    const float tot = group_sum(pg);
+    if (g == 0 && qok) {
+      if constexpr (!kGRows)
+        a.Dq[dqi] += tot;
+      else
+        a.gpg[((long long)bh * a.nsp + span) * a.Gp + slot] = tot;
+    }
+  } else {
+    if constexpr (!kGRows) {
+      if (q < n && (q >= L || qok)) {
+        __bf16* dst = a.dq + seq + q * ld;
+#pragma unroll
+        for (int dt = 0; dt < 4; ++dt) store4_bf16(dst + 16 * dt + 4 * g, acc[dt], q < L ? a.alpha : 0.f);
+      }
+    } else if (qok) {
+      float* dst = a.gdq + (((long long)bh * a.nsp + span) * a.Gp + slot) * kHeadDim;
+#pragma unroll
+      for (int dt = 0; dt < 4; ++dt) {
+        f32x4 v = acc[dt];
+#pragma unroll
+        for (int i = 0; i < 4; ++i) v[i] *= a.alpha;
+        *reinterpret_cast<f32x4*>(dst + 16 * dt + 4 * g) = v;
+      }
+    }
+  }
+}
+
+// D of the global query rows: + their span partials, in span order.
+__global__ __launch_bounds__(64) void k_bwd_dfin(SoftArgs a) {
+  const int bh = blockIdx.x, b = bh / a.H, n = a.n;
+  const int L = clampi(a.valid_len[b], 0, n);
+  const int nspv = (L + kBwdSpan - 1) / kBwdSpan;
+  for (int j = threadIdx.x; j < a.G; j += 64) {
+    const int q = a.gpos[(long long)b * a.G + j];
+    if (q < 0 || q >= L) continue;
+    float tot = a.Dq[(long long)bh * n + q];
+    for (int sp = 0; sp < nspv; ++sp) tot += a.gpg[((long long)bh * a.nsp + sp) * a.Gp + j];
+    a.Dq[(long long)bh * n + q] = tot;
+  }
+}
+
+// ---------------------------------------------------------- column side --
+// dK, dV.  kGCols: global-column blocks (64 gathered global keys x one
+// 512-query span) instead of band blocks (64 keys).
+template <bool kGCols>
+__global__ __launch_bounds__(256) void k_bwd_cols(SoftArgs a) {
+  __shared__ __align__(16) __bf16 sQ[64 * 64];
+  __shared__ __align__(16) __bf16 sO[64 * 64];  // dO rows
+  __shared__ __align__(16) int sRow[64];
+  __shared__ __align__(16) float sL2[64];
+  __shared__ __align__(16) float sD[64];
+  extern __shared__ uint32_t sBits[];
+  const int tid = threadIdx.x, lane = tid & 63, w = __builtin_amdgcn_readfirstlane(tid >> 6), lr = lane & 15,
+            g = lane >> 4;
+  const int H = a.H, n = a.n, G = a.G, r = a.r;
+  int blk = blockIdx.x, bh, k0 = 0, span = 0, gc = 0;
+  if constexpr (!kGCols) {
+    const int nkb = (n + 63) / 64;
+    k0 = 64 * (blk % nkb);
+    bh = blk / nkb;
+  } else {
+    span = blk % a.nsp;
+    blk /= a.nsp;
+    const int ngc = a.Gp / 64;
+    gc = blk % ngc;
+    bh = blk / ngc;
+  }
+  const int b = bh / H, h = bh % H;
+  const int L = clampi(a.valid_len[b], 0, n);
+  const int* gp = a.gpos ? a.gpos + (long long)b * G : nullptr;
+  const long long ld = (long long)H * kHeadDim;
+  const unsigned ldb = (unsigned)(2 * ld);
+  const long long seq = (long long)b * n * ld + (long long)h * kHeadDim;
+  if constexpr (!kGCols) {
+    if (k0 >= L) {  // padding keys: zero gradient rows
+      for (int i = tid; i < 64 * 8; i += 256) {
+        const int k = k0 + i / 8;
+        if (k < n) {
+          *reinterpret_cast<uint4*>(a.dk + seq + k * ld + 8 * (i % 8)) = make_uint4(0, 0, 0, 0);
+          *reinterpret_cast<uint4*>(a.dv + seq + k * ld + 8 * (i % 8)) = make_uint4(0, 0, 0, 0);
+        }
+      }
+      return;
+    }
+    build_bits(sBits, gp, G, L, n);
+  } else {
+    if (span * kBwdSpan >= L) return;
+  }
+  int k, slot = 0;
+  bool kok;
+  if constexpr (!kGCols) {
+    k = k0 + 16 * w + lr;
+    kok = k < L && !bit_of(sBits, k);
+  } else {
+    slot = 64 * gc + 16 * w + lr;
+    k = (gp && slot < G) ? gp[slot] : -1;
+    kok = k >= 0 && k < L;
+  }
+  const int ks = kok ? k : 0;
+  bf16x8 kf[2], vf[2];
+  kf[0] = *reinterpret_cast<const bf16x8*>(a.k + seq + ks * ld + 8 * g);
+  kf[1] = *reinterpret_cast<const bf16x8*>(a.k + seq + ks * ld + 32 + 8 * g);
+  vf[0] = *reinterpret_cast<const bf16x8*>(a.v + seq + ks * ld + 8 * g);
+  vf[1] = *reinterpret_cast<const bf16x8*>(a.v + seq + ks * ld + 32 + 8 * g);
+  const float gkv = kok ? a.gk[(long long)b * n + k] : 0.f;
+  const float c2 = a.c2;
+  int qt0, qt1, ngt = 0;
+  if constexpr (!kGCols) {
+    qt0 = max(0, k0 - r);
+    qt1 = min(L, k0 + 64 + r);
+    ngt = gp ? (G + 63) / 64 : 0;
+  } else {
+    qt0 = span * kBwdSpan;
+    qt1 = min(L, qt0 + kBwdSpan);
+  }
+  const int nband = (qt1 - qt0 + 63) / 64;
+  f32x4 accK[4], accV[4];
+#pragma unroll
+  for (int dt = 0; dt < 4; ++dt) {
+    accK[dt] = f32x4{0.f, 0.f, 0.f, 0.f};
+    accV[dt] = f32x4{0.f, 0.f, 0.f, 0.f};
+  }
+  for (int t = 0; t < nband + ngt; ++t) {
+    const bool gtile = t >= nband;
+    const int qbase = gtile ? 64 * (t - nband) : qt0 + 64 * t;
+    if (tid < 64) {
+      int qq;
+      if (!gtile) {
+        qq = qbase + tid;
+        if (qq >= qt1 || (!kGCols && bit_of(sBits, qq))) qq = -1;
+      } else {
+        qq = qbase + tid < G ? gp[qbase + tid] : -1;
+        if (qq >= L) qq = -1;
+      }
+      sRow[tid] = qq;
+      sL2[tid] = qq >= 0 ? a.lse[(long long)bh * n + qq] * kLog2e : 0.f;
+      sD[tid] = qq >= 0 ? a.Dq[(long long)bh * n + qq] : 0.f;
+    }
+    __syncthreads();
+    load_rows(a.q + seq, ldb, sQ, w, sRow);
+    load_rows(a.dO + seq, ldb, sO, w, sRow);
+    wait_dma();
+    __syncthreads();
+    f32x4 s[4], dp[4];
+    mma_rows(sQ, kf, s, lr, g);
+    mma_rows(sO, vf, dp, lr, g);
+    bf16x8 pP[2], pS[2];
+#pragma unroll
+    for (int st = 0; st < 4; ++st) {
+      const int4 rows = *reinterpret_cast<const int4*>(sRow + 16 * st + 4 * g);
+      const int rr[4] = {rows.x, rows.y, rows.z, rows.w};
+      const f32x4 l2 = *reinterpret_cast<const f32x4*>(sL2 + 16 * st + 4 * g);
+      const f32x4 dd = *reinterpret_cast<const f32x4*>(sD + 16 * st + 4 * g);
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        const int qq = rr[i];
+        const bool ok = kok && qq >= 0 && (gtile || kGCols || abs(qq - k) <= r);
+        const float p = ok ? fast_exp2(fmaf(s[st][i], c2, -l2[i])) : 0.f;
+        pP[st >> 1][4 * (st & 1) + i] = (__bf16)p;
+        pS[st >> 1][4 * (st & 1) + i] = (__bf16)(p * (dp[st][i] + gkv - dd[i]));
+      }
+    }
+    mma_tr(sO, pP, accV);
+    mma_tr(sQ, pS, accK);
+    __syncthreads();
+  }
+  if constexpr (!kGCols) {
+    if (k < n && (k >= L || kok)) {
+      const float sk = k < L ? a.alpha : 0.f, sv = k < L ? 1.f : 0.f;
+#pragma unroll
+      for (int dt = 0; dt < 4; ++dt) {
+        store4_bf16(a.dk + seq + k * ld + 16 * dt + 4 * g, accK[dt], sk);
+        store4_bf16(a.dv + seq + k * ld + 16 * dt + 4 * g, accV[dt], sv);
+      }
+    }
+  } else if (kok) {
+    const long long o = (((long long)bh * a.nsp + span) * a.Gp + slot) * kHeadDim;
+#pragma unroll
+    for (int dt = 0; dt < 4; ++dt) {
+      f32x4 v = accK[dt];
+#pragma unroll
+      for (int i = 0; i < 4; ++i) v[i] *= a.alpha;
+      *reinterpret_cast<f32x4*>(a.gdk + o + 16 * dt + 4 * g) = v;
+      *reinterpret_cast<f32x4*>(a.gdv + o + 16 * dt + 4 * g) = accV[dt];
+    }
+  }
+}
+
+// Global rows' dQ and global keys' dK, dV: sums of the span partials in span
+// order (blocks 0 .. B H - 1); dtheta = -sum ds in a fixed order (last block).
+__global__ __launch_bounds__(256) void k_bwd_finish(SoftArgs a) {
+  __shared__ float red[256];
+  const int tid = threadIdx.x, n = a.n, H = a.H;
+  if ((int)blockIdx.x == a.B * H) {
+    float acc = 0.f;
+    const long long tot = (long long)a.B * n;
+    for (long long i = tid; i < tot; i += 256) acc += a.dsv[i];
+    red[tid] = acc;
+    __syncthreads();
+    for (int off = 128; off > 0; off >>= 1) {
+      if (tid < off) red[tid] += red[tid + off];
+      __syncthreads();
+    }
+    if (tid == 0) *a.dtheta = -red[0];
+    return;
+  }
+  if (a.G == 0 || !a.gpos) return;
+  const int bh = blockIdx.x, b = bh / H, h = bh % H;
+  const int L = clampi(a.valid_len[b], 0, n);
+  const int nspv = (L + kBwdSpan - 1) / kBwdSpan;
+  const long long ld = (long long)H * kHeadDim;
+  const long long seq = (long long)b * n * ld + (long long)h * kHeadDim;
+  for (int i = tid; i < a.G * kHeadDim; i += 256) {
+    const int j = i / kHeadDim, c = i % kHeadDim;
+    const int p = a.gpos[(long long)b * a.G + j];
+    if (p < 0 || p >= L) continue;
+    float sq = 0.f, sk = 0.f, sv = 0.f;
+    for (int sp = 0; sp < nspv; ++sp) {
+      const long long o = (((long long)bh * a.nsp + sp) * a.Gp + j) * kHeadDim + c;
+      sq += a.gdq[o];
+      sk += a.gdk[o];
+      sv += a.gdv[o];
+    }
+    a.dq[seq + p * ld + c] = (__bf16)sq;
+    a.dk[seq + p * ld + c] = (__bf16)sk;
+    a.dv[seq + p * ld + c] = (__bf16)sv;
+  }
+}
+
+}  // namespace
+
+hipError_t launch_soft_mask(const SoftArgs& a, hipStream_t s) {
+  const long long rows = (long long)a.B * a.n;
+  hipLaunchKernelGGL(k_soft_mask, dim3((unsigned)((rows + 3) / 4)), dim3(256), 0, s, a);
+  return hipGetLastError();
+}
+
+hipError_t launch_soft_backward(const SoftArgs& a, hipStream_t s) {
+  const long long rows = (long long)a.B * a.n;
+  const unsigned bh = (unsigned)(a.B * a.H);
+  const unsigned nb = (unsigned)((a.n + 63) / 64);
+  const size_t bits = sizeof(uint32_t) * (((size_t)a.n + 31) / 32);
+  const unsigned ngr = bh * (unsigned)(a.Gp / 64) * (unsigned)a.nsp;
+  hipLaunchKernelGGL(k_soft_rows, dim3((unsigned)((rows + 3) / 4)), dim3(256), 0, s, a);
+  hipLaunchKernelGGL((k_bwd_rows<0, false>), dim3(bh * nb), dim3(256), bits, s, a);
+  if (a.G > 0) {
+    hipLaunchKernelGGL((k_bwd_rows<0, true>), dim3(ngr), dim3(256), 0, s, a);
+    hipLaunchKernelGGL(k_bwd_dfin, dim3(bh), dim3(64), 0, s, a);
+  }
+  hipLaunchKernelGGL((k_bwd_rows<1, false>), dim3(bh * nb), dim3(256), bits, s, a);
+  hipLaunchKernelGGL((k_bwd_cols<false>), dim3(bh * nb), dim3(256), bits, s, a);
+  if (a.G > 0) {
+    hipLaunchKernelGGL((k_bwd_rows<1, true>), dim3(ngr), dim3(256), 0, s, a);
+    hipLaunchKernelGGL((k_bwd_cols<true>), dim3(ngr), dim3(256), 0, s, a);
+  }
+  hipLaunchKernelGGL(k_bwd_finish, dim3(bh + 1), dim3(256), 0, s, a);
+  return hipGetLastError();
+}
+
+}  // namespace sc

@@ -80,6 +80,41 @@ struct PruneArgs {
 };
 hipError_t launch_prune(const PruneArgs& p, hipStream_t s);
 
+// LTP soft pruning, training form: forward mask and the backward of
+// y = mask * attention(q, k, v) through the attention and the scores.  All
+// token tensors are contiguous [B, n, H, 64] bf16.
+constexpr int kBwdSpan = 512;  // keys (queries) per global-row (global-column) block of the backward
+
+struct SoftArgs {
+  const __bf16 *q, *k, *v, *o, *dy;
+  const float* lse;     // [B, H, n] natural log (forward output)
+  const float* mask;    // [B, n]
+  const float* dmask;   // [B, n] or null
+  const float* scores;  // [B, n] (forward mask only)
+  __bf16* y;            // [B, n, H, 64] (forward mask only)
+  float* mask_out;      // [B, n] (forward mask only)
+  __bf16 *dq, *dk, *dv;
+  float* dtheta;        // one float
+  const int* valid_len;
+  const int* gpos;      // [B, G] or null
+  int B, n, H, G, r;
+  int keep_global;
+  float alpha, c2;      // softmax scale, and scale * log2(e)
+  float theta, inv_t;   // threshold (forward) and 1 / temperature
+  int nsp, Gp;          // spans of kBwdSpan tokens; G padded to a multiple of 64
+  // workspace
+  __bf16* dO;           // [B, n, H, 64]  mask * dy
+  float* Dq;            // [B, H, n]      sum_j P dL/dP of each query row
+  float* gk;            // [B, n]         score gradient of each key over H * L
+  float* dsv;           // [B, n]         score gradient (for the threshold's)
+  float* gpg;           // [B, H, nsp, Gp]      global rows: sum_j P g per key span
+  float* gdq;           // [B, H, nsp, Gp, 64]  global rows: dQ per key span
+  float* gdk;           // [B, H, nsp, Gp, 64]  global keys: dK per query span
+  float* gdv;           // [B, H, nsp, Gp, 64]  global keys: dV per query span
+};
+hipError_t launch_soft_mask(const SoftArgs& a, hipStream_t s);
+hipError_t launch_soft_backward(const SoftArgs& a, hipStream_t s);
+
 struct GatherArgs {
   int B, n, nt;
   const char* src[4];

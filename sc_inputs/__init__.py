@@ -24,6 +24,7 @@ _M2 = np.uint64(0x94D049BB133111EB)
 # Stream ids (one per drawn tensor / quantity).
 S_Q, S_K, S_V, S_LEN, S_GLOB, S_SPIKE_U, S_SPIKE_V, S_X = 1, 2, 3, 4, 5, 6, 7, 8
 S_SPIKE_UQ = 9
+S_DY, S_DMASK = 10, 11        # upstream gradients of the soft-pruning backward
 S_WQKV0, S_WO0 = 100, 101  # + 2 * layer
 S_W10, S_W20 = 300, 301      # + 2 * layer (feed-forward block)
 
@@ -250,6 +251,15 @@ def make_attention_inputs(cfg: AttnConfig, seed: int | None = None, B=None, n=No
         out[name] = s
         out[name + "64"] = e
     return out
+
+
+def make_soft_gradients(seed: int, B: int, n: int, H: int, d: int, dmask: bool = True):
+    """Upstream gradients of a soft-pruned layer: dy [B, n, H, d] ~ N(0, 1) in bf16 (storage bits and exact
+    doubles) and dmask [B, n] ~ N(0, 1) rounded to float32 (or None)."""
+    cnt = B * n * H * d
+    dy_s, dy64 = quantise(normal(seed, S_DY, cnt).reshape(B, n, H, d), "bf16")
+    dm = normal(seed, S_DMASK, B * n).reshape(B, n).astype(np.float32) if dmask else None
+    return dy_s, dy64, dm
 
 
 def make_stack_inputs(cfg: StackConfig, seed: int | None = None, B=None, n=None, n_layers=None, len_range=None,

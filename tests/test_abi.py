@@ -25,7 +25,7 @@ def declared_functions():
 def test_exports_every_declared_symbol():
     L = sc.load()
     names = declared_functions()
-    assert len(names) == 16
+    assert len(names) == 19
     for name in names:
         assert hasattr(L, name), name
 
@@ -162,6 +162,43 @@ def test_topk_validation():
     for bad in (-0.01, 1.01, float("nan"), float("inf")):
         assert call(bad) == B.SC_EINVAL
     assert call(0.5, ws=None) == B.SC_EWORKSPACE
+
+
+def test_soft_pruning_validation():
+    """Every call here is rejected on the host (nothing is launched on the fake addresses)."""
+    L = sc.load()
+    d = desc()
+    cd = d.c()
+    A = [0x1000000 * (i + 1) for i in range(12)]  # disjoint fake device buffers
+
+    def fwd(scores=A[0], theta=0.01, t=0.01, out=A[1], mask=A[2], y=A[3], dd=cd):
+        return L.sc_ltp_soft_mask(ctypes.byref(dd), scores, ctypes.c_float(theta), ctypes.c_float(t), 1, out, mask,
+                                  y, None)
+
+    assert fwd(scores=None) == B.SC_EINVAL
+    assert fwd(t=0.0) == B.SC_EINVAL
+    assert fwd(t=-1.0) == B.SC_EINVAL
+    assert fwd(theta=float("nan")) == B.SC_EINVAL
+    assert fwd(y=A[1] + 64) == B.SC_EINVAL  # y overlaps out
+    f32 = desc(dtype=B.SC_F32)
+    assert fwd(dd=f32.c()) == B.SC_EUNSUPPORTED
+    causal = desc(causal=True)
+    assert fwd(dd=causal.c()) == B.SC_EUNSUPPORTED
+    ws_need = sc.sc_ltp_soft_backward_workspace_size(d)
+    assert ws_need > 0 and sc.sc_ltp_soft_backward_workspace_size(f32) == 0
+
+    def bwd(dq=A[7], dk=A[8], dv=A[9], dth=A[10], ws=A[11], wsb=ws_need, t=0.01, q=A[0]):
+        return L.sc_ltp_soft_backward(ctypes.byref(cd), q, A[1], A[2], A[3], A[4], A[5], ctypes.c_float(t), 1,
+                                      A[6], None, dq, dk, dv, dth, ws, wsb, None)
+
+    assert bwd(q=None) == B.SC_EINVAL
+    assert bwd(dth=None) == B.SC_EINVAL
+    assert bwd(t=0.0) == B.SC_EINVAL
+    assert bwd(ws=None) == B.SC_EWORKSPACE
+    assert bwd(wsb=ws_need - 1) == B.SC_EWORKSPACE
+    assert bwd(dq=A[0] + 128) == B.SC_EINVAL  # dq overlaps q
+    assert bwd(dk=A[7] + 128) == B.SC_EINVAL  # dk overlaps dq
+    assert bwd(dth=A[11] + 4) == B.SC_EINVAL  # dtheta inside the workspace
 
 
 def test_full_stack_validation():
