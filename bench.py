@@ -45,6 +45,9 @@ WORKLOADS = {
     "lognormal": (6, "single sparse-attention + LTP layer: B64 n1024 H12 d64 bf16, window 256, global token 0, "
                      "valid lengths round(exp(N(5.717, 0.738^2))) clipped to [1,1024] (paper-shaped), threshold "
                      "pruning ~30%"),
+    "soft": ("soft", "training step of one LTP soft-pruned layer (Sec. 4.2.2 step 1): B8 n4096 H12 d64 bf16, "
+                     "window 512, 32 seeded global tokens, valid lengths U[2048,4096]; forward (attention, scores, "
+                     "soft mask) and backward to Q, K, V and the threshold, upstream gradients N(0,1)"),
     "encoder": (None, "12-layer RoBERTa-base-shaped SparseCoder encoder: B16 n2048 D768 (12 heads x 64), GELU "
                       "feed-forward 3072, windows 64,64,128,128,256,256,512x6, global token 0, valid lengths "
                       "U[256,2048], thresholds 0.01*l/11, pruning after every layer"),
@@ -69,6 +72,118 @@ def model_flops(lens_in, lens_kept, pairs, D, H, d, F):
     ffn = 2 * 2 * t_kept * D * F
     other = 6 * H * pairs + 2 * 5 * t_kept * D + 8 * t_kept * F
     return dict(projection=proj, attention=attn, ffn=ffn, other=other)
+
+
+# the soft-pruning backward, per allowed pair and head: five bf16 products (S = Q.K^T recomputed, dP = dO.V^T,
+# dQ = dS.K, dK = dS^T.Q, dV = P^T.dO) and, in VALU issue slots, one exp (2 slots), the logit FMA, the two
+# operations forming dS = P (dP + g - D) and two halves of bf16 packs (P and dS)
+BWD_PRODUCTS = 5
+BWD_VALU_SLOTS_PER_PAIR = 2 + 1 + 2 + 1
+
+
+def measure_soft(args, sc, si, torch, np, dev="cuda:0"):
+    """Times the training step of one soft-pruned layer (LTP's soft pruning): window attention with the LSE and
+    score partials, scores, soft mask, and the backward to Q, K, V and the threshold."""
+    cfg = si.CONFIGS[4]
+    t0 = time.time()
+    inp = si.make_attention_inputs(cfg)
+    dy_s, dy64, dm = si.make_soft_gradients(21, cfg.B, cfg.n, cfg.H, cfg.d)
+    gen_s = time.time() - t0
+    B, n, H, dd = cfg.B, cfg.n, cfg.H, cfg.d
+
+    def bf(a):
+        return torch.from_numpy(np.ascontiguousarray(a).view(np.int16)).to(dev).view(torch.bfloat16)
+
+    def i32(a):
+        return torch.from_numpy(np.ascontiguousarray(a, dtype=np.int32)).to(dev)
+
+    d = sc.Desc(B, n, H, cfg.window, i32(inp["valid_len"]), i32(inp["global_pos"]), cfg.alpha, sc.SC_BF16)
+    q, k, v, dy = bf(inp["q"]), bf(inp["k"]), bf(inp["v"]), bf(dy_s)
+    dmask = torch.from_numpy(dm).to(dev)
+    out = torch.empty_like(q)
+    lse = torch.empty((B, H, n), dtype=torch.float32, device=dev)
+    sp = torch.empty(sc.sc_score_partials_size(d) // 4, dtype=torch.float32, device=dev)
+    ws_attn = torch.empty(max(sc.sc_window_attention_workspace_size(d), 1), dtype=torch.uint8, device=dev)
+    scores = torch.empty((B, n), dtype=torch.float32, device=dev)
+    mask = torch.empty((B, n), dtype=torch.float32, device=dev)
+    y = torch.empty_like(out)
+    grads = (torch.empty_like(q), torch.empty_like(k), torch.empty_like(v),
+             torch.empty(1, dtype=torch.float32, device=dev))
+    ws_b = torch.empty(sc.sc_ltp_soft_backward_workspace_size(d), dtype=torch.uint8, device=dev)
+    # threshold at the median score of the valid non-global tokens, temperature their spread
+    sc.sc_window_attention(d, q, k, v, out=out, lse=lse, score_partials=sp, workspace=ws_attn)
+    sc.sc_ltp_score(d, sp, scores=scores)
+    sv = scores.cpu().numpy()
+    vals = []
+    for b in range(B):
+        L = int(inp["valid_len"][b])
+        glob = {int(x) for x in inp["global_pos"][b] if 0 <= x < L}
+        vals.extend(float(sv[b, t]) for t in range(L) if t not in glob)
+    theta, temp = float(np.median(vals)), max(float(np.std(vals)), 1e-6)
+    ev = [torch.cuda.Event(enable_timing=True) for _ in range(2 * args.steps)]
+
+    def step(i=None):
+        sc.sc_window_attention(d, q, k, v, out=out, lse=lse, score_partials=sp, workspace=ws_attn)
+        sc.sc_ltp_score(d, sp, scores=scores)
+        sc.sc_ltp_soft_mask(d, scores, theta, temp, out, mask=mask, y=y)
+        if i is not None:
+            ev[2 * i].record()
+        sc.sc_ltp_soft_backward(d, q, k, v, out, lse, mask, temp, dy, dmask, grads=grads, workspace=ws_b)
+        if i is not None:
+            ev[2 * i + 1].record()
+
+    for _ in range(args.warmup):
+        step()
+    torch.cuda.synchronize()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record()
+    for i in range(args.steps):
+        step(i)
+    e1.record()
+    torch.cuda.synchronize()
+    ms = e0.elapsed_time(e1) / args.steps
+    bwd_ms = sum(ev[2 * i].elapsed_time(ev[2 * i + 1]) for i in range(args.steps)) / args.steps
+    tokens = int(np.sum(inp["valid_len"]))
+    pw, pg = algorithmic_counts(inp)
+    pairs = H * (pw + pg)
+    flops = 2.0 * dd * BWD_PRODUCTS * pairs
+    # read Q, K, V, O, dY (bf16) and the LSE per valid token and head, the mask and its gradient per token; write
+    # dQ, dK, dV (bf16)
+    bytes_ = tokens * H * (8 * 2 * dd + 4) + tokens * 8
+    t_mfma = flops / (MFMA_PEAK_TFLOPS["bf16"] * 1e12)
+    t_hbm = bytes_ / (HBM_PEAK_GBS * 1e9)
+    alu = BWD_VALU_SLOTS_PER_PAIR * pairs
+    t_alu = alu / (VALU_PEAK_TOPS * 1e12)
+    if t_mfma >= max(t_hbm, t_alu):
+        roof = dict(bound="mfma", achieved=round(flops / (bwd_ms * 1e-3) / 1e12, 2), peak=MFMA_PEAK_TFLOPS["bf16"],
+                    unit="TFLOP/s")
+    elif t_hbm >= t_alu:
+        roof = dict(bound="hbm", achieved=round(bytes_ / (bwd_ms * 1e-3) / 1e9, 1), peak=HBM_PEAK_GBS, unit="GB/s")
+    else:
+        roof = dict(bound="alu", achieved=round(alu / (bwd_ms * 1e-3) / 1e12, 3), peak=round(VALU_PEAK_TOPS, 2),
+                    unit="T VALU lane-op/s")
+    roof["frac"] = round(roof["achieved"] / roof["peak"], 4)
+    roof.update(floor_mfma_us=round(t_mfma * 1e6, 2), floor_hbm_us=round(t_hbm * 1e6, 2),
+                floor_alu_us=round(t_alu * 1e6, 2), traffic=None, kernel="sc_ltp_soft_backward (all its launches)",
+                kernel_us=round(bwd_ms * 1e3, 2), algorithmic_flop=flops, algorithmic_bytes=bytes_)
+    res = dict(ms=ms, bwd_ms=bwd_ms, tokens=tokens, theta=theta, temp=temp, roof=roof, gen_s=gen_s,
+               dtheta=float(grads[3].item()))
+    if not args.no_cpu_baseline:
+        import oracle
+        threads = oracle.default_threads()
+        c0 = time.perf_counter()
+        rows = [0]
+        sel = [inp[x][rows] for x in ("q64", "k64", "v64")]
+        vl, gp = inp["valid_len"][rows], inp["global_pos"][rows]
+        oracle.soft_prune_forward(*sel, vl, gp, cfg.window, cfg.alpha, theta, temp, 1, nthreads=threads)
+        oracle.soft_prune_backward(*sel, vl, gp, cfg.window, cfg.alpha, theta, temp, dy64[rows],
+                                   dm[rows].astype(np.float64), 1, nthreads=threads)
+        cpu_s = time.perf_counter() - c0
+        res["cpu_baseline"] = {"value": round(int(vl.sum()) / cpu_s, 1), "unit": "token-layers/s (training step)",
+                               "cores": threads, "kind": "oracle",
+                               "sample": f"sequence 0 of the workload ({int(vl.sum())} tokens): soft-pruned "
+                                         f"forward and backward in double precision, {cpu_s:.2f} s"}
+    return res
 
 
 def measure_encoder(args, sc, si, torch, np, dev="cuda:0"):
@@ -296,7 +411,8 @@ def main():
                          "hardware counters)")
     ap.add_argument("--workload", choices=sorted(WORKLOADS), default="seq4096",
                     help="seq4096: B8 n4096 window 512, 32 global tokens (the headline line); lognormal: B64 n1024 "
-                         "window 256, one global token, paper-shaped lognormal lengths")
+                         "window 256, one global token, paper-shaped lognormal lengths; encoder: the 12-layer "
+                         "stack; soft: training step (forward and backward) of one soft-pruned layer at seq4096")
     ap.add_argument("--prune", choices=("threshold", "topk"), default="threshold",
                     help="pruning rule of the step: the layer threshold (the paper's rule) or top-k by keep ratio")
     ap.add_argument("--keep-ratio", type=float, default=0.5, help="top-k rule: fraction of candidates kept")
@@ -324,6 +440,21 @@ def main():
         sweep(args, sc, si, torch, np)
         return
     cid, desc = WORKLOADS[args.workload]
+    if cid == "soft":
+        m = measure_soft(args, sc, si, torch, np, dev)
+        line = {
+            "metric": METRIC, "value": round(m["tokens"] / (m["ms"] * 1e-3), 1),
+            "unit": "token-layers/s (training step)", "n_gpus": 1, "steps": args.steps, "warmup": args.warmup,
+            "ms_per_step": round(m["ms"], 4), "higher_is_better": True, "scaling": "weak", "vs_baseline": None,
+            "dtype": "bf16", "data": "synthetic",
+            "config": {"workload": desc, "valid_tokens": m["tokens"], "threshold": m["theta"],
+                       "temperature": m["temp"], "parallelism": "none (1 GPU)"},
+            "roofline": m["roof"], "backward_ms": round(m["bwd_ms"], 4), "dtheta": m["dtheta"],
+            "input_generation_s": round(m["gen_s"], 1)}
+        if "cpu_baseline" in m:
+            line["cpu_baseline"] = m["cpu_baseline"]
+        print(json.dumps(line), flush=True)
+        return
     if cid is None:
         m = measure_encoder(args, sc, si, torch, np, dev)
         print(json.dumps({

@@ -20,6 +20,11 @@ FLAGS = [
     f"--offload-arch={ARCH}", "-O3", "-std=c++17", "-fPIC", "-Wall", "-Wno-unused-function",
     # Packed fp32 VALU forms are kept out of the code object.
     "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",
+    # MFMA accumulators in the unified VGPR file rather than in AGPRs: the
+    # AGPR form copied every zero-initialised tile result in and out each tile
+    # (v_accvgpr_write / read) and cost occupancy (the GEMM: 140 VGPRs + 64
+    # AGPRs against 120 VGPRs).
+    "-mllvm", "-amdgpu-mfma-vgpr-form",
 ]
 
 

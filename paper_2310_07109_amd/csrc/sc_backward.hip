@@ -34,6 +34,8 @@
 // 4 keys per register (row side), S = Q K^T a key in each lane and 4 queries
 // per register (column side); the second product of each side reads its
 // row-major LDS tile with transposed reads, rows in MFMA k order.
+#include <type_traits>
+
 #include "sc_device.h"
 #include "sc_internal.h"
 
@@ -137,19 +139,6 @@ __global__ __launch_bounds__(256) void k_soft_rows(SoftArgs a) {
 }
 
 // ---------------------------------------------------------- tile helpers --
-// Rows 16w .. 16w + 15 of a 64-row tile of a [*, ld] bf16 tensor; tile row R
-// holds tensor row rows[R] (or row 0, unused, where rows[R] < 0).
-SC_DEV void load_rows(const __bf16* base, unsigned ld_bytes, __bf16* tile, int w, const int* rows) {
-  const int lane = opaque_lane();
-#pragma unroll
-  for (int j = 0; j < 2; ++j) {
-    const int R0 = 16 * w + 8 * j, R = R0 + (lane >> 3);
-    const unsigned u = (lane & 7) ^ (lane >> 3);
-    const int row = rows[R];
-    lds_dma16(base, (unsigned)(row >= 0 ? row : 0) * ld_bytes + 16u * u, lds_addr(tile + R0 * TRb::kPitch));
-  }
-}
-
 // acc[dt] += A^T B where A is a 64-row bf16 tile (rows in MFMA k order:
 // lane (g, lr) supplies dims 16 dt + 4 (lr & 3) .. of rows 32 kc + 4g + lr / 4
 // and 32 kc + 16 + 4g + lr / 4) and B the packed bf16 operand of chunk kc.
@@ -209,10 +198,10 @@ SC_DEV void store4_bf16(__bf16* p, f32x4 v, float scale) {
 // global queries x one 512-key span) instead of band blocks (64 queries).
 template <int kMode, bool kGRows>
 __global__ __launch_bounds__(256) void k_bwd_rows(SoftArgs a) {
-  __shared__ __align__(16) __bf16 sK[64 * 64];
-  __shared__ __align__(16) __bf16 sV[kMode == 1 ? 64 * 64 : 8];
-  __shared__ __align__(16) int sRow[64];
-  __shared__ __align__(16) float sG[64];
+  __shared__ __align__(16) __bf16 sK[2][64 * 64];
+  __shared__ __align__(16) __bf16 sV[kMode == 1 ? 2 : 1][kMode == 1 ? 64 * 64 : 8];
+  __shared__ __align__(16) float sBias[2][64];  // 0 for a key counted in this tile, -inf otherwise
+  __shared__ __align__(16) float sG[2][64];
   extern __shared__ uint32_t sBits[];
   const int tid = threadIdx.x, lane = tid & 63, w = __builtin_amdgcn_readfirstlane(tid >> 6), lr = lane & 15,
             g = lane >> 4;
@@ -281,65 +270,110 @@ __global__ __launch_bounds__(256) void k_bwd_rows(SoftArgs a) {
     kt0 = span * kBwdSpan;
     kt1 = min(L, kt0 + kBwdSpan);
   }
-  const int nband = (kt1 - kt0 + 63) / 64;
+  const int nband = (kt1 - kt0 + 63) / 64, nt = nband + ngt;
+  // key of tile row R of tile tt, or -1 where no pair of this block's side is
+  // counted in that tile; dma_row: a valid row to load in its place
+  auto key_of = [&](int tt, int R) {
+    if (tt < nband) {
+      const int key = kt0 + 64 * tt + R;
+      return (key < kt1 && (kGRows || !bit_of(sBits, key))) ? key : -1;
+    }
+    const int sl = 64 * (tt - nband) + R;
+    const int key = sl < G ? gp[sl] : -1;
+    return (key >= 0 && key < L) ? key : -1;
+  };
+  auto issue = [&](int tt, int buf) {
+    const int lane2 = opaque_lane();
+#pragma unroll
+    for (int j = 0; j < 2; ++j) {
+      const int R0 = 16 * w + 8 * j, R = R0 + (lane2 >> 3);
+      int row;
+      if (tt < nband) {
+        row = min(kt0 + 64 * tt + R, L - 1);
+      } else {
+        const int sl = 64 * (tt - nband) + R;
+        row = sl < G ? gp[sl] : 0;
+        row = (row >= 0 && row < L) ? row : 0;
+      }
+      const unsigned u = (lane2 & 7) ^ (lane2 >> 3), voff = (unsigned)row * ldb + 16u * u;
+      lds_dma16(a.k + seq, voff, lds_addr(&sK[buf][R0 * TRb::kPitch]));
+      if constexpr (kMode == 1) lds_dma16(a.v + seq, voff, lds_addr(&sV[buf][R0 * TRb::kPitch]));
+    }
+  };
   float pg = 0.f;
   f32x4 acc[4];
 #pragma unroll
   for (int dt = 0; dt < 4; ++dt) acc[dt] = f32x4{0.f, 0.f, 0.f, 0.f};
-  for (int t = 0; t < nband + ngt; ++t) {
-    const bool gtile = t >= nband;
-    const int kbase = gtile ? 64 * (t - nband) : kt0 + 64 * t;
-    if (tid < 64) {
-      int key;
-      if (!gtile) {
-        key = kbase + tid;
-        if (key >= kt1 || (!kGRows && bit_of(sBits, key))) key = -1;
-      } else {
-        key = kbase + tid < G ? gp[kbase + tid] : -1;
-        if (key >= L) key = -1;
-      }
-      sRow[tid] = key;
-      sG[tid] = key >= 0 ? a.gk[(long long)b * n + key] : 0.f;
-    }
-    __syncthreads();
-    load_rows(a.k + seq, ldb, sK, w, sRow);
-    if constexpr (kMode == 1) load_rows(a.v + seq, ldb, sV, w, sRow);
-    wait_dma();
-    __syncthreads();
+  // one tile; kEdge: the band condition is checked per pair (edge tiles of a
+  // band block), else every counted key of the tile is in the band of every
+  // query of the block.  Lanes of queries not counted here compute values
+  // that are never stored.
+  auto tile = [&](auto edge_c, int t, int cur) {
+    constexpr bool kEdge = decltype(edge_c)::value;
+    const int kbase = kt0 + 64 * t;
     f32x4 s[4];
-    mma_rows(sK, qf, s, lr, g);
+    mma_rows(sK[cur], qf, s, lr, g);
     float p[4][4];
 #pragma unroll
     for (int st = 0; st < 4; ++st) {
-      const int4 rows = *reinterpret_cast<const int4*>(sRow + 16 * st + 4 * g);
-      const int rr[4] = {rows.x, rows.y, rows.z, rows.w};
+      const f32x4 bias = *reinterpret_cast<const f32x4*>(&sBias[cur][16 * st + 4 * g]);
 #pragma unroll
       for (int i = 0; i < 4; ++i) {
-        const int key = rr[i];
-        const bool ok = qok && key >= 0 && (gtile || kGRows || abs(q - key) <= r);
-        p[st][i] = ok ? fast_exp2(fmaf(s[st][i], c2, -lse2)) : 0.f;
+        float x = fmaf(s[st][i], c2, -lse2) + bias[i];
+        if constexpr (kEdge) x = (unsigned)(kbase + 16 * st + 4 * g + i - q + r) <= (unsigned)(2 * r) ? x : -INFINITY;
+        p[st][i] = fast_exp2(x);
       }
     }
     if constexpr (kMode == 0) {
 #pragma unroll
       for (int st = 0; st < 4; ++st) {
-        const f32x4 gg = *reinterpret_cast<const f32x4*>(sG + 16 * st + 4 * g);
+        const f32x4 gg = *reinterpret_cast<const f32x4*>(&sG[cur][16 * st + 4 * g]);
 #pragma unroll
         for (int i = 0; i < 4; ++i) pg = fmaf(p[st][i], gg[i], pg);
       }
     } else {
       f32x4 dp[4];
-      mma_rows(sV, df, dp, lr, g);
+      mma_rows(sV[cur], df, dp, lr, g);
       bf16x8 pb[2];
 #pragma unroll
       for (int st = 0; st < 4; ++st) {
-        const f32x4 gg = *reinterpret_cast<const f32x4*>(sG + 16 * st + 4 * g);
+        const f32x4 gg = *reinterpret_cast<const f32x4*>(&sG[cur][16 * st + 4 * g]);
 #pragma unroll
         for (int i = 0; i < 4; ++i) pb[st >> 1][4 * (st & 1) + i] = (__bf16)(p[st][i] * (dp[st][i] + gg[i] - Dv));
       }
-      mma_tr(sK, pb, acc);
+      mma_tr(sK[cur], pb, acc);
     }
-    __syncthreads();  // the next tile overwrites sK, sV, sRow, sG
+  };
+  if (nt > 0) {
+    issue(0, 0);
+    if (tid < 64) {
+      const int key = key_of(0, tid);
+      sBias[0][tid] = key >= 0 ? 0.f : -INFINITY;
+      sG[0][tid] = key >= 0 ? a.gk[(long long)b * n + key] : 0.f;
+    }
+  }
+  for (int t = 0; t < nt; ++t) {
+    const int cur = t & 1;
+    wait_dma();
+    __syncthreads();  // tile t and its metadata are in LDS; buffers of tile t - 1 are free
+    const bool more = t + 1 < nt;
+    if (more) issue(t + 1, cur ^ 1);
+    float nbias = 0.f, ng = 0.f;
+    if (tid < 64 && more) {
+      const int nkey = key_of(t + 1, tid);
+      nbias = nkey >= 0 ? 0.f : -INFINITY;
+      ng = nkey >= 0 ? a.gk[(long long)b * n + nkey] : 0.f;
+    }
+    const int kbase = kt0 + 64 * t;
+    const bool edge = !kGRows && t < nband && !(kbase >= q0 + 63 - r && kbase + 63 <= q0 + r);
+    if (edge)
+      tile(std::true_type{}, t, cur);
+    else
+      tile(std::false_type{}, t, cur);
+    if (tid < 64 && more) {  // the metadata buffer of tile t + 1 was last read by tile t - 1
+      sBias[cur ^ 1][tid] = nbias;
+      sG[cur ^ 1][tid] = ng;
+    }
   }
   if constexpr (kMode == 0) {
     const float tot = group_sum(pg);
@@ -351,10 +385,13 @@ __global__ __launch_bounds__(256) void k_bwd_rows(SoftArgs a) {
     }
   } else {
     if constexpr (!kGRows) {
-      if (q < n && (q >= L || qok)) {
-        __bf16* dst = a.dq + seq + q * ld;
+      __bf16* dst = a.dq + seq + q * ld;
+      if (qok) {
 #pragma unroll
-        for (int dt = 0; dt < 4; ++dt) store4_bf16(dst + 16 * dt + 4 * g, acc[dt], q < L ? a.alpha : 0.f);
+        for (int dt = 0; dt < 4; ++dt) store4_bf16(dst + 16 * dt + 4 * g, acc[dt], a.alpha);
+      } else if (q >= L && q < n) {
+#pragma unroll
+        for (int dt = 0; dt < 4; ++dt) *reinterpret_cast<uint2*>(dst + 16 * dt + 4 * g) = make_uint2(0, 0);
       }
     } else if (qok) {
       float* dst = a.gdq + (((long long)bh * a.nsp + span) * a.Gp + slot) * kHeadDim;
@@ -388,11 +425,10 @@ __global__ __launch_bounds__(64) void k_bwd_dfin(SoftArgs a) {
 // 512-query span) instead of band blocks (64 keys).
 template <bool kGCols>
 __global__ __launch_bounds__(256) void k_bwd_cols(SoftArgs a) {
-  __shared__ __align__(16) __bf16 sQ[64 * 64];
-  __shared__ __align__(16) __bf16 sO[64 * 64];  // dO rows
-  __shared__ __align__(16) int sRow[64];
-  __shared__ __align__(16) float sL2[64];
-  __shared__ __align__(16) float sD[64];
+  __shared__ __align__(16) __bf16 sQ[2][64 * 64];
+  __shared__ __align__(16) __bf16 sO[2][64 * 64];  // dO rows
+  __shared__ __align__(16) float sL2[2][64];  // LSE2 of a query counted in this tile, +inf otherwise
+  __shared__ __align__(16) float sD[2][64];
   extern __shared__ uint32_t sBits[];
   const int tid = threadIdx.x, lane = tid & 63, w = __builtin_amdgcn_readfirstlane(tid >> 6), lr = lane & 15,
             g = lane >> 4;
@@ -457,64 +493,110 @@ __global__ __launch_bounds__(256) void k_bwd_cols(SoftArgs a) {
     qt0 = span * kBwdSpan;
     qt1 = min(L, qt0 + kBwdSpan);
   }
-  const int nband = (qt1 - qt0 + 63) / 64;
+  const int nband = (qt1 - qt0 + 63) / 64, nt = nband + ngt;
+  auto query_of = [&](int tt, int R) {
+    if (tt < nband) {
+      const int qq = qt0 + 64 * tt + R;
+      return (qq < qt1 && (kGCols || !bit_of(sBits, qq))) ? qq : -1;
+    }
+    const int sl = 64 * (tt - nband) + R;
+    const int qq = sl < G ? gp[sl] : -1;
+    return (qq >= 0 && qq < L) ? qq : -1;
+  };
+  auto issue = [&](int tt, int buf) {
+    const int lane2 = opaque_lane();
+#pragma unroll
+    for (int j = 0; j < 2; ++j) {
+      const int R0 = 16 * w + 8 * j, R = R0 + (lane2 >> 3);
+      int row;
+      if (tt < nband) {
+        row = min(qt0 + 64 * tt + R, L - 1);
+      } else {
+        const int sl = 64 * (tt - nband) + R;
+        row = sl < G ? gp[sl] : 0;
+        row = (row >= 0 && row < L) ? row : 0;
+      }
+      const unsigned u = (lane2 & 7) ^ (lane2 >> 3), voff = (unsigned)row * ldb + 16u * u;
+      lds_dma16(a.q + seq, voff, lds_addr(&sQ[buf][R0 * TRb::kPitch]));
+      lds_dma16(a.dO + seq, voff, lds_addr(&sO[buf][R0 * TRb::kPitch]));
+    }
+  };
   f32x4 accK[4], accV[4];
 #pragma unroll
   for (int dt = 0; dt < 4; ++dt) {
     accK[dt] = f32x4{0.f, 0.f, 0.f, 0.f};
     accV[dt] = f32x4{0.f, 0.f, 0.f, 0.f};
   }
-  for (int t = 0; t < nband + ngt; ++t) {
-    const bool gtile = t >= nband;
-    const int qbase = gtile ? 64 * (t - nband) : qt0 + 64 * t;
-    if (tid < 64) {
-      int qq;
-      if (!gtile) {
-        qq = qbase + tid;
-        if (qq >= qt1 || (!kGCols && bit_of(sBits, qq))) qq = -1;
-      } else {
-        qq = qbase + tid < G ? gp[qbase + tid] : -1;
-        if (qq >= L) qq = -1;
-      }
-      sRow[tid] = qq;
-      sL2[tid] = qq >= 0 ? a.lse[(long long)bh * n + qq] * kLog2e : 0.f;
-      sD[tid] = qq >= 0 ? a.Dq[(long long)bh * n + qq] : 0.f;
-    }
-    __syncthreads();
-    load_rows(a.q + seq, ldb, sQ, w, sRow);
-    load_rows(a.dO + seq, ldb, sO, w, sRow);
-    wait_dma();
-    __syncthreads();
+  // one tile; kEdge: the band condition is checked per pair.  Lanes of keys
+  // not counted here compute values that are never stored.
+  auto tile = [&](auto edge_c, int t, int cur) {
+    constexpr bool kEdge = decltype(edge_c)::value;
+    const int qbase = qt0 + 64 * t;
     f32x4 s[4], dp[4];
-    mma_rows(sQ, kf, s, lr, g);
-    mma_rows(sO, vf, dp, lr, g);
+    mma_rows(sQ[cur], kf, s, lr, g);
+    mma_rows(sO[cur], vf, dp, lr, g);
     bf16x8 pP[2], pS[2];
 #pragma unroll
     for (int st = 0; st < 4; ++st) {
-      const int4 rows = *reinterpret_cast<const int4*>(sRow + 16 * st + 4 * g);
-      const int rr[4] = {rows.x, rows.y, rows.z, rows.w};
-      const f32x4 l2 = *reinterpret_cast<const f32x4*>(sL2 + 16 * st + 4 * g);
-      const f32x4 dd = *reinterpret_cast<const f32x4*>(sD + 16 * st + 4 * g);
+      const f32x4 l2 = *reinterpret_cast<const f32x4*>(&sL2[cur][16 * st + 4 * g]);
+      const f32x4 dd = *reinterpret_cast<const f32x4*>(&sD[cur][16 * st + 4 * g]);
 #pragma unroll
       for (int i = 0; i < 4; ++i) {
-        const int qq = rr[i];
-        const bool ok = kok && qq >= 0 && (gtile || kGCols || abs(qq - k) <= r);
-        const float p = ok ? fast_exp2(fmaf(s[st][i], c2, -l2[i])) : 0.f;
+        float x = fmaf(s[st][i], c2, -l2[i]);
+        if constexpr (kEdge) x = (unsigned)(qbase + 16 * st + 4 * g + i - k + r) <= (unsigned)(2 * r) ? x : -INFINITY;
+        const float p = fast_exp2(x);
         pP[st >> 1][4 * (st & 1) + i] = (__bf16)p;
         pS[st >> 1][4 * (st & 1) + i] = (__bf16)(p * (dp[st][i] + gkv - dd[i]));
       }
     }
-    mma_tr(sO, pP, accV);
-    mma_tr(sQ, pS, accK);
-    __syncthreads();
+    mma_tr(sO[cur], pP, accV);
+    mma_tr(sQ[cur], pS, accK);
+  };
+  if (nt > 0) {
+    issue(0, 0);
+    if (tid < 64) {
+      const int qq = query_of(0, tid);
+      sL2[0][tid] = qq >= 0 ? a.lse[(long long)bh * n + qq] * kLog2e : INFINITY;
+      sD[0][tid] = qq >= 0 ? a.Dq[(long long)bh * n + qq] : 0.f;
+    }
+  }
+  for (int t = 0; t < nt; ++t) {
+    const int cur = t & 1;
+    wait_dma();
+    __syncthreads();  // tile t and its metadata are in LDS; buffers of tile t - 1 are free
+    const bool more = t + 1 < nt;
+    if (more) issue(t + 1, cur ^ 1);
+    float nl2 = INFINITY, nd = 0.f;
+    if (tid < 64 && more) {
+      const int nq = query_of(t + 1, tid);
+      if (nq >= 0) {
+        nl2 = a.lse[(long long)bh * n + nq] * kLog2e;
+        nd = a.Dq[(long long)bh * n + nq];
+      }
+    }
+    const int qbase = qt0 + 64 * t;
+    const bool edge = !kGCols && t < nband && !(qbase >= k0 + 63 - r && qbase + 63 <= k0 + r);
+    if (edge)
+      tile(std::true_type{}, t, cur);
+    else
+      tile(std::false_type{}, t, cur);
+    if (tid < 64 && more) {  // the metadata buffer of tile t + 1 was last read by tile t - 1
+      sL2[cur ^ 1][tid] = nl2;
+      sD[cur ^ 1][tid] = nd;
+    }
   }
   if constexpr (!kGCols) {
-    if (k < n && (k >= L || kok)) {
-      const float sk = k < L ? a.alpha : 0.f, sv = k < L ? 1.f : 0.f;
+    if (kok) {
 #pragma unroll
       for (int dt = 0; dt < 4; ++dt) {
-        store4_bf16(a.dk + seq + k * ld + 16 * dt + 4 * g, accK[dt], sk);
-        store4_bf16(a.dv + seq + k * ld + 16 * dt + 4 * g, accV[dt], sv);
+        store4_bf16(a.dk + seq + k * ld + 16 * dt + 4 * g, accK[dt], a.alpha);
+        store4_bf16(a.dv + seq + k * ld + 16 * dt + 4 * g, accV[dt], 1.f);
+      }
+    } else if (k >= L && k < n) {
+#pragma unroll
+      for (int dt = 0; dt < 4; ++dt) {
+        *reinterpret_cast<uint2*>(a.dk + seq + k * ld + 16 * dt + 4 * g) = make_uint2(0, 0);
+        *reinterpret_cast<uint2*>(a.dv + seq + k * ld + 16 * dt + 4 * g) = make_uint2(0, 0);
       }
     }
   } else if (kok) {
@@ -536,9 +618,23 @@ __global__ __launch_bounds__(256) void k_bwd_finish(SoftArgs a) {
   __shared__ float red[256];
   const int tid = threadIdx.x, n = a.n, H = a.H;
   if ((int)blockIdx.x == a.B * H) {
-    float acc = 0.f;
-    const long long tot = (long long)a.B * n;
-    for (long long i = tid; i < tot; i += 256) acc += a.dsv[i];
+    // thread t adds the 4-float groups t, t + 256, ... with eight groups in
+    // flight, then the scalar tail; the threads' sums meet in a fixed tree
+    const long long tot = (long long)a.B * n, nv = tot / 4;
+    const f32x4* v4 = reinterpret_cast<const f32x4*>(a.dsv);
+    float part[8] = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
+    for (long long base = tid; base < nv; base += 256 * 8) {
+#pragma unroll
+      for (int u = 0; u < 8; ++u) {
+        const long long i = base + 256LL * u;
+        if (i < nv) {
+          const f32x4 x = v4[i];
+          part[u] += (x[0] + x[1]) + (x[2] + x[3]);
+        }
+      }
+    }
+    float acc = ((part[0] + part[1]) + (part[2] + part[3])) + ((part[4] + part[5]) + (part[6] + part[7]));
+    for (long long i = 4 * nv + tid; i < tot; i += 256) acc += a.dsv[i];
     red[tid] = acc;
     __syncthreads();
     for (int off = 128; off > 0; off >>= 1) {
