@@ -318,7 +318,7 @@ size_t carve_soft(const sc_attn_desc* d, void* base, sc::SoftArgs* a) {
   a->dO = c.take<__bf16>(bhn * 64);
   a->Dq = c.take<float>(bhn);
   a->gk = c.take<float>(bn);
-  a->dsv = c.take<float>(bn);
+  a->dsv = c.take<float>((bn + 3) / 4);
   a->gpg = c.take<float>(part > 0 ? part : 1);
   a->gdq = c.take<float>(part > 0 ? part * 64 : 1);
   a->gdk = c.take<float>(part > 0 ? part * 64 : 1);

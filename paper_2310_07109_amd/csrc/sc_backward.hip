@@ -10,7 +10,8 @@
 // Backward, given dL/dy and optionally dL/dm (e.g. from a regulariser):
 //   k_soft_rows     one wave per token: dO = bf16(m * dy); dm = sum dy * out
 //                   (+ dL/dm); ds = dm m (1 - m) / T (0 for kept global
-//                   tokens and padding); g = ds / (H L); D = dO . out per head.
+//                   tokens and padding); g = ds / (H L); D = dO . out per head;
+//                   ds summed per 4 tokens for the threshold's gradient.
 //   k_bwd_rows<0>   D_q += sum_j P[q][j] g_j (the score's share of the row
 //                   term of the softmax backward).
 //   k_bwd_dfin      D of the global query rows from their span partials.
@@ -74,19 +75,29 @@ __global__ __launch_bounds__(256) void k_soft_mask(SoftArgs a) {
   if (lane == 0) a.mask_out[t] = m;
   const __bf16* o = a.o + t * ld;
   __bf16* y = a.y + t * ld;
-  for (int u = lane; u < a.H * 8; u += 64) {
-    bf16x8 x = *reinterpret_cast<const bf16x8*>(o + 8 * u);
+  if (k >= L) {  // padding: y = 0 without reading out
+    for (int u = lane; u < a.H * 8; u += 64) *reinterpret_cast<uint4*>(y + 8 * u) = make_uint4(0, 0, 0, 0);
+    return;
+  }
+  for (int base = 0; base < a.H * 8; base += 128) {  // two passes' loads in flight
+    bf16x8 x[2];
 #pragma unroll
-    for (int e = 0; e < 8; ++e) x[e] = (__bf16)(m * (float)x[e]);
-    *reinterpret_cast<bf16x8*>(y + 8 * u) = x;
+    for (int ps = 0; ps < 2; ++ps) x[ps] = *reinterpret_cast<const bf16x8*>(o + 8 * min(base + 64 * ps + lane, a.H * 8 - 1));
+#pragma unroll
+    for (int ps = 0; ps < 2; ++ps) {
+      const int u = base + 64 * ps + lane;
+      if (u < a.H * 8) {
+#pragma unroll
+        for (int e = 0; e < 8; ++e) x[ps][e] = (__bf16)(m * (float)x[ps][e]);
+        *reinterpret_cast<bf16x8*>(y + 8 * u) = x[ps];
+      }
+    }
   }
 }
 
 // ------------------------------------------------------------- row terms --
-__global__ __launch_bounds__(256) void k_soft_rows(SoftArgs a) {
-  const int w = threadIdx.x >> 6, lane = threadIdx.x & 63;
-  const long long t = (long long)blockIdx.x * 4 + w;
-  if (t >= (long long)a.B * a.n) return;
+// One wave per token; returns the token's score gradient ds (0 for padding).
+SC_DEV float soft_row(const SoftArgs& a, long long t, int lane) {
   const int b = (int)(t / a.n), k = (int)(t % a.n), H = a.H;
   const int L = clampi(a.valid_len[b], 0, a.n);
   const long long ld = (long long)H * kHeadDim;
@@ -97,45 +108,61 @@ __global__ __launch_bounds__(256) void k_soft_rows(SoftArgs a) {
   if (k >= L) {
     for (int u = lane; u < H * 8; u += 64) *reinterpret_cast<uint4*>(dO + 8 * u) = make_uint4(0, 0, 0, 0);
     for (int h = lane; h < H; h += 64) Dq[(long long)h * a.n] = 0.f;
-    if (lane == 0) {
-      a.gk[t] = 0.f;
-      a.dsv[t] = 0.f;
-    }
-    return;
+    if (lane == 0) a.gk[t] = 0.f;
+    return 0.f;
   }
   const float m = a.mask[t];
   float dm = 0.f;
   // 16-byte units: unit u holds dims 8(u % 8) .. of head u / 8; in each pass
-  // of the wave, lanes 8j .. 8j + 7 hold the whole of one head
-  for (int base = 0; base < H * 8; base += 64) {
-    const int u = base + lane;
-    float hd = 0.f;
-    if (u < H * 8) {
-      const bf16x8 yv = *reinterpret_cast<const bf16x8*>(dy + 8 * u);
-      const bf16x8 ov = *reinterpret_cast<const bf16x8*>(o + 8 * u);
-      bf16x8 dv;
+  // of the wave, lanes 8j .. 8j + 7 hold the whole of one head.  Two passes'
+  // loads are issued before any of them is used.
+  for (int base = 0; base < H * 8; base += 128) {
+    bf16x8 yv[2], ov[2];
 #pragma unroll
-      for (int e = 0; e < 8; ++e) {
-        const float yf = (float)yv[e], of = (float)ov[e];
-        dm = fmaf(yf, of, dm);
-        dv[e] = (__bf16)(m * yf);
-        hd = fmaf((float)dv[e], of, hd);
-      }
-      *reinterpret_cast<bf16x8*>(dO + 8 * u) = dv;
+    for (int ps = 0; ps < 2; ++ps) {
+      const int u = min(base + 64 * ps + lane, H * 8 - 1);  // clamped: loads stay in the row
+      yv[ps] = *reinterpret_cast<const bf16x8*>(dy + 8 * u);
+      ov[ps] = *reinterpret_cast<const bf16x8*>(o + 8 * u);
     }
-    hd += __shfl_xor(hd, 1, 64);
-    hd += __shfl_xor(hd, 2, 64);
-    hd += __shfl_xor(hd, 4, 64);
-    if ((lane & 7) == 0 && u < H * 8) Dq[(long long)(u >> 3) * a.n] = hd;
+#pragma unroll
+    for (int ps = 0; ps < 2; ++ps) {
+      const int u = base + 64 * ps + lane;
+      float hd = 0.f;
+      if (u < H * 8) {
+        bf16x8 dv;
+#pragma unroll
+        for (int e = 0; e < 8; ++e) {
+          const float yf = (float)yv[ps][e], of = (float)ov[ps][e];
+          dm = fmaf(yf, of, dm);
+          dv[e] = (__bf16)(m * yf);
+          hd = fmaf((float)dv[e], of, hd);
+        }
+        *reinterpret_cast<bf16x8*>(dO + 8 * u) = dv;
+      }
+      hd += __shfl_xor(hd, 1, 64);
+      hd += __shfl_xor(hd, 2, 64);
+      hd += __shfl_xor(hd, 4, 64);
+      if ((lane & 7) == 0 && u < H * 8) Dq[(long long)(u >> 3) * a.n] = hd;
+    }
   }
   dm = wave_sum(dm);
   if (a.dmask) dm += a.dmask[t];
   const bool g = a.keep_global && a.gpos && wave_is_global(a.gpos + (long long)b * a.G, a.G, k);
   const float ds = g ? 0.f : dm * m * (1.f - m) * a.inv_t;
-  if (lane == 0) {
-    a.gk[t] = ds / ((float)H * (float)L);
-    a.dsv[t] = ds;
-  }
+  if (lane == 0) a.gk[t] = ds / ((float)H * (float)L);
+  return ds;
+}
+
+// Workgroup = 4 tokens; their ds are added in wave order into dsv[workgroup]
+// (the threshold's gradient sums these partials).
+__global__ __launch_bounds__(256) void k_soft_rows(SoftArgs a) {
+  __shared__ float red[4];
+  const int w = threadIdx.x >> 6, lane = threadIdx.x & 63;
+  const long long t = (long long)blockIdx.x * 4 + w;
+  const float ds = t < (long long)a.B * a.n ? soft_row(a, t, lane) : 0.f;
+  if (lane == 0) red[w] = ds;
+  __syncthreads();
+  if (threadIdx.x == 0) a.dsv[blockIdx.x] = ((red[0] + red[1]) + red[2]) + red[3];
 }
 
 // ---------------------------------------------------------- tile helpers --
@@ -143,7 +170,7 @@ __global__ __launch_bounds__(256) void k_soft_rows(SoftArgs a) {
 // lane (g, lr) supplies dims 16 dt + 4 (lr & 3) .. of rows 32 kc + 4g + lr / 4
 // and 32 kc + 16 + 4g + lr / 4) and B the packed bf16 operand of chunk kc.
 SC_DEV void mma_tr(const __bf16* tile, const bf16x8 (&pb)[2], f32x4 (&acc)[4]) {
-  const int ln = opaque_lane(), lr = ln & 15, g = ln >> 4;
+  const int ln = threadIdx.x & 63, lr = ln & 15, g = ln >> 4;
 #pragma unroll
   for (int kc = 0; kc < 2; ++kc) {
     const int vr = 32 * kc + 4 * g + (lr >> 2), bsel = (lr >> 1) & 1, e = 4 * (lr & 1);
@@ -157,18 +184,23 @@ SC_DEV void mma_tr(const __bf16* tile, const bf16x8 (&pb)[2], f32x4 (&acc)[4]) {
   }
 }
 
-// s[st] = A_st B^T for the four 16-row sub-tiles of an LDS tile A (rows
-// 16 st + lr) and a register operand B of the wave's 16 rows.
-SC_DEV void mma_rows(const __bf16* tile, const bf16x8 (&bf)[2], f32x4 (&s)[4], int lr, int g) {
+// s[st] = init[st] + A_st B^T for the four 16-row sub-tiles of an LDS tile A
+// (rows 16 st + lr) and a register operand B of the wave's 16 rows.
+SC_DEV void mma_rows(const __bf16* tile, const bf16x8 (&bf)[2], f32x4 (&s)[4], int lr, int g,
+                     const f32x4 (&init)[4]) {
 #pragma unroll
   for (int st = 0; st < 4; ++st) {
     bf16x8 af[2];
     TRb::load_frags(tile, 16 * st + lr, g, af);
-    f32x4 c = f32x4{0.f, 0.f, 0.f, 0.f};
+    f32x4 c = init[st];
     c = TRb::mma(af[0], bf[0], c);
     c = TRb::mma(af[1], bf[1], c);
     s[st] = c;
   }
+}
+SC_DEV void mma_rows(const __bf16* tile, const bf16x8 (&bf)[2], f32x4 (&s)[4], int lr, int g) {
+  const f32x4 z[4] = {};
+  mma_rows(tile, bf, s, lr, g, z);
 }
 
 // The global-token bitmask of a sequence in LDS (band blocks).
@@ -196,21 +228,44 @@ SC_DEV void store4_bf16(__bf16* p, f32x4 v, float scale) {
 // ------------------------------------------------------------- row side --
 // kMode 0: D += P g;  kMode 1: dQ.  kGRows: global-row blocks (64 gathered
 // global queries x one 512-key span) instead of band blocks (64 queries).
-template <int kMode, bool kGRows>
-__global__ __launch_bounds__(256) void k_bwd_rows(SoftArgs a) {
-  __shared__ __align__(16) __bf16 sK[2][64 * 64];
-  __shared__ __align__(16) __bf16 sV[kMode == 1 ? 2 : 1][kMode == 1 ? 64 * 64 : 8];
-  __shared__ __align__(16) float sBias[2][64];  // 0 for a key counted in this tile, -inf otherwise
-  __shared__ __align__(16) float sG[2][64];
-  extern __shared__ uint32_t sBits[];
+// LDS of the row side (K and V tiles, double-buffered, and their metadata)
+// and of the column side (Q and dO tiles); one launch may hold both kinds.
+struct RowSmemK {  // the D pass reads K only
+  __bf16 sK[2][64 * 64];
+  float sBias[2][64];  // 0 for a key counted in this tile, -inf otherwise
+  float sG[2][64];
+};
+struct RowSmem {
+  __bf16 sK[2][64 * 64];
+  float sBias[2][64];
+  float sG[2][64];
+  __bf16 sV[2][64 * 64];
+};
+struct ColSmem {
+  __bf16 sQ[2][64 * 64];
+  __bf16 sO[2][64 * 64];  // dO rows
+  float sL2[2][64];       // LSE2 of a query counted in this tile, +inf otherwise
+  float sD[2][64];
+};
+union BwdSmem {
+  RowSmem row;
+  ColSmem col;
+};
+
+template <int kMode, bool kGRows, typename Smem>
+SC_DEV void bwd_rows(const SoftArgs& a, int blk, Smem& sm, uint32_t* sBits) {
+  auto& sK = sm.sK;
+  auto& sBias = sm.sBias;
+  auto& sG = sm.sG;
   const int tid = threadIdx.x, lane = tid & 63, w = __builtin_amdgcn_readfirstlane(tid >> 6), lr = lane & 15,
             g = lane >> 4;
   const int H = a.H, n = a.n, G = a.G, r = a.r;
-  int blk = blockIdx.x, bh, q0 = 0, span = 0, gc = 0;
-  if constexpr (!kGRows) {
+  int bh, q0 = 0, span = 0, gc = 0;
+  if constexpr (!kGRows) {  // a (sequence, head)'s query blocks in order on one XCD
     const int nqb = (n + 63) / 64;
-    q0 = 64 * (blk % nqb);
-    bh = blk / nqb;
+    int qb;
+    xcd_pair_map(blk, nqb, a.B * H, bh, qb);
+    q0 = 64 * qb;
   } else {
     span = blk % a.nsp;
     blk /= a.nsp;
@@ -297,7 +352,7 @@ __global__ __launch_bounds__(256) void k_bwd_rows(SoftArgs a) {
       }
       const unsigned u = (lane2 & 7) ^ (lane2 >> 3), voff = (unsigned)row * ldb + 16u * u;
       lds_dma16(a.k + seq, voff, lds_addr(&sK[buf][R0 * TRb::kPitch]));
-      if constexpr (kMode == 1) lds_dma16(a.v + seq, voff, lds_addr(&sV[buf][R0 * TRb::kPitch]));
+      if constexpr (kMode == 1) lds_dma16(a.v + seq, voff, lds_addr(&sm.sV[buf][R0 * TRb::kPitch]));
     }
   };
   float pg = 0.f;
@@ -332,15 +387,16 @@ __global__ __launch_bounds__(256) void k_bwd_rows(SoftArgs a) {
         for (int i = 0; i < 4; ++i) pg = fmaf(p[st][i], gg[i], pg);
       }
     } else {
-      f32x4 dp[4];
-      mma_rows(sV[cur], df, dp, lr, g);
+      // dP^T + g: the MFMA accumulates onto the keys' score gradients
+      f32x4 gg[4], dp[4];
+#pragma unroll
+      for (int st = 0; st < 4; ++st) gg[st] = *reinterpret_cast<const f32x4*>(&sG[cur][16 * st + 4 * g]);
+      mma_rows(sm.sV[cur], df, dp, lr, g, gg);
       bf16x8 pb[2];
 #pragma unroll
-      for (int st = 0; st < 4; ++st) {
-        const f32x4 gg = *reinterpret_cast<const f32x4*>(&sG[cur][16 * st + 4 * g]);
+      for (int st = 0; st < 4; ++st)
 #pragma unroll
-        for (int i = 0; i < 4; ++i) pb[st >> 1][4 * (st & 1) + i] = (__bf16)(p[st][i] * (dp[st][i] + gg[i] - Dv));
-      }
+        for (int i = 0; i < 4; ++i) pb[st >> 1][4 * (st & 1) + i] = (__bf16)(p[st][i] * (dp[st][i] - Dv));
       mma_tr(sK[cur], pb, acc);
     }
   };
@@ -424,20 +480,20 @@ __global__ __launch_bounds__(64) void k_bwd_dfin(SoftArgs a) {
 // dK, dV.  kGCols: global-column blocks (64 gathered global keys x one
 // 512-query span) instead of band blocks (64 keys).
 template <bool kGCols>
-__global__ __launch_bounds__(256) void k_bwd_cols(SoftArgs a) {
-  __shared__ __align__(16) __bf16 sQ[2][64 * 64];
-  __shared__ __align__(16) __bf16 sO[2][64 * 64];  // dO rows
-  __shared__ __align__(16) float sL2[2][64];  // LSE2 of a query counted in this tile, +inf otherwise
-  __shared__ __align__(16) float sD[2][64];
-  extern __shared__ uint32_t sBits[];
+SC_DEV void bwd_cols(const SoftArgs& a, int blk, ColSmem& sm, uint32_t* sBits) {
+  auto& sQ = sm.sQ;
+  auto& sO = sm.sO;
+  auto& sL2 = sm.sL2;
+  auto& sD = sm.sD;
   const int tid = threadIdx.x, lane = tid & 63, w = __builtin_amdgcn_readfirstlane(tid >> 6), lr = lane & 15,
             g = lane >> 4;
   const int H = a.H, n = a.n, G = a.G, r = a.r;
-  int blk = blockIdx.x, bh, k0 = 0, span = 0, gc = 0;
-  if constexpr (!kGCols) {
+  int bh, k0 = 0, span = 0, gc = 0;
+  if constexpr (!kGCols) {  // a (sequence, head)'s key blocks in order on one XCD
     const int nkb = (n + 63) / 64;
-    k0 = 64 * (blk % nkb);
-    bh = blk / nkb;
+    int kb;
+    xcd_pair_map(blk, nkb, a.B * H, bh, kb);
+    k0 = 64 * kb;
   } else {
     span = blk % a.nsp;
     blk /= a.nsp;
@@ -533,8 +589,10 @@ __global__ __launch_bounds__(256) void k_bwd_cols(SoftArgs a) {
     constexpr bool kEdge = decltype(edge_c)::value;
     const int qbase = qt0 + 64 * t;
     f32x4 s[4], dp[4];
+    const f32x4 gk4[4] = {f32x4{gkv, gkv, gkv, gkv}, f32x4{gkv, gkv, gkv, gkv}, f32x4{gkv, gkv, gkv, gkv},
+                          f32x4{gkv, gkv, gkv, gkv}};
     mma_rows(sQ[cur], kf, s, lr, g);
-    mma_rows(sO[cur], vf, dp, lr, g);
+    mma_rows(sO[cur], vf, dp, lr, g, gk4);  // dP + g of the lane's key
     bf16x8 pP[2], pS[2];
 #pragma unroll
     for (int st = 0; st < 4; ++st) {
@@ -546,7 +604,7 @@ __global__ __launch_bounds__(256) void k_bwd_cols(SoftArgs a) {
         if constexpr (kEdge) x = (unsigned)(qbase + 16 * st + 4 * g + i - k + r) <= (unsigned)(2 * r) ? x : -INFINITY;
         const float p = fast_exp2(x);
         pP[st >> 1][4 * (st & 1) + i] = (__bf16)p;
-        pS[st >> 1][4 * (st & 1) + i] = (__bf16)(p * (dp[st][i] + gkv - dd[i]));
+        pS[st >> 1][4 * (st & 1) + i] = (__bf16)(p * (dp[st][i] - dd[i]));
       }
     }
     mma_tr(sO[cur], pP, accV);
@@ -612,15 +670,61 @@ __global__ __launch_bounds__(256) void k_bwd_cols(SoftArgs a) {
   }
 }
 
+// Block ranges of the two main launches, each starting at a multiple of 8 so
+// that the band blocks' XCD mapping holds: the global-span blocks first (few,
+// long), then the band blocks.
+struct BwdGrid {
+  int gr, gc, band;  // padded block counts of global-row, global-column and band segments
+};
+
+// D pass: [global rows][band rows].
+__global__ __launch_bounds__(256) void k_bwd_dpass(SoftArgs a, BwdGrid gd) {
+  __shared__ __align__(16) RowSmemK sm;
+  extern __shared__ uint32_t sBits[];
+  const int blk = blockIdx.x;
+  if (blk < gd.gr) {
+    if (blk < a.B * a.H * (a.Gp / 64) * a.nsp) bwd_rows<0, true>(a, blk, sm, sBits);
+    return;
+  }
+  bwd_rows<0, false>(a, blk - gd.gr, sm, sBits);
+}
+
+// Gradients: [global columns][global rows][band rows (dQ)][band columns (dK, dV)].
+__global__ __launch_bounds__(256) void k_bwd_grad(SoftArgs a, BwdGrid gd) {
+  __shared__ __align__(16) BwdSmem sm;
+  extern __shared__ uint32_t sBits[];
+  const int nglob = a.B * a.H * (a.Gp / 64) * a.nsp;
+  int blk = blockIdx.x;
+  if (blk < gd.gc) {
+    if (blk < nglob) bwd_cols<true>(a, blk, sm.col, sBits);
+    return;
+  }
+  blk -= gd.gc;
+  if (blk < gd.gr) {
+    if (blk < nglob) bwd_rows<1, true>(a, blk, sm.row, sBits);
+    return;
+  }
+  blk -= gd.gr;
+  if (blk < gd.band) {
+    if (blk < a.B * a.H * ((a.n + 63) / 64)) bwd_rows<1, false>(a, blk, sm.row, sBits);
+    return;
+  }
+  bwd_cols<false>(a, blk - gd.band, sm.col, sBits);
+}
+
 // Global rows' dQ and global keys' dK, dV: sums of the span partials in span
-// order (blocks 0 .. B H - 1); dtheta = -sum ds in a fixed order (last block).
-__global__ __launch_bounds__(256) void k_bwd_finish(SoftArgs a) {
+// order, one thread per (sequence, head, slot, dim) with all its loads in
+// flight (blocks 0 .. nfin - 1); dtheta = -sum ds in a fixed order (the last
+// block).
+constexpr int kFinSpans = 16;  // spans summed with every load issued first (longer sequences loop)
+
+__global__ __launch_bounds__(256) void k_bwd_finish(SoftArgs a, int nfin) {
   __shared__ float red[256];
   const int tid = threadIdx.x, n = a.n, H = a.H;
-  if ((int)blockIdx.x == a.B * H) {
+  if ((int)blockIdx.x == nfin) {
     // thread t adds the 4-float groups t, t + 256, ... with eight groups in
     // flight, then the scalar tail; the threads' sums meet in a fixed tree
-    const long long tot = (long long)a.B * n, nv = tot / 4;
+    const long long tot = ((long long)a.B * n + 3) / 4, nv = tot / 4;  // one partial per 4 tokens
     const f32x4* v4 = reinterpret_cast<const f32x4*>(a.dsv);
     float part[8] = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
     for (long long base = tid; base < nv; base += 256 * 8) {
@@ -644,27 +748,40 @@ __global__ __launch_bounds__(256) void k_bwd_finish(SoftArgs a) {
     if (tid == 0) *a.dtheta = -red[0];
     return;
   }
-  if (a.G == 0 || !a.gpos) return;
-  const int bh = blockIdx.x, b = bh / H, h = bh % H;
+  const long long e = (long long)blockIdx.x * 256 + tid;  // (bh, slot, dim)
+  const int c = (int)(e % kHeadDim), j = (int)((e / kHeadDim) % a.G), bh = (int)(e / ((long long)kHeadDim * a.G));
+  if (bh >= a.B * H) return;
+  const int b = bh / H, h = bh % H;
   const int L = clampi(a.valid_len[b], 0, n);
+  const int p = a.gpos[(long long)b * a.G + j];
+  if (p < 0 || p >= L) return;
   const int nspv = (L + kBwdSpan - 1) / kBwdSpan;
-  const long long ld = (long long)H * kHeadDim;
-  const long long seq = (long long)b * n * ld + (long long)h * kHeadDim;
-  for (int i = tid; i < a.G * kHeadDim; i += 256) {
-    const int j = i / kHeadDim, c = i % kHeadDim;
-    const int p = a.gpos[(long long)b * a.G + j];
-    if (p < 0 || p >= L) continue;
-    float sq = 0.f, sk = 0.f, sv = 0.f;
-    for (int sp = 0; sp < nspv; ++sp) {
-      const long long o = (((long long)bh * a.nsp + sp) * a.Gp + j) * kHeadDim + c;
-      sq += a.gdq[o];
-      sk += a.gdk[o];
-      sv += a.gdv[o];
+  const long long o0 = ((long long)bh * a.nsp * a.Gp + j) * kHeadDim + c, so = (long long)a.Gp * kHeadDim;
+  float sq = 0.f, sk = 0.f, sv = 0.f;
+  for (int base = 0; base < nspv; base += kFinSpans) {
+    float xq[kFinSpans], xk[kFinSpans], xv[kFinSpans];
+#pragma unroll
+    for (int u = 0; u < kFinSpans; ++u) {
+      const bool in = base + u < nspv;
+      const long long o = o0 + (long long)(in ? base + u : 0) * so;
+      xq[u] = in ? a.gdq[o] : 0.f;
+      xk[u] = in ? a.gdk[o] : 0.f;
+      xv[u] = in ? a.gdv[o] : 0.f;
     }
-    a.dq[seq + p * ld + c] = (__bf16)sq;
-    a.dk[seq + p * ld + c] = (__bf16)sk;
-    a.dv[seq + p * ld + c] = (__bf16)sv;
+#pragma unroll
+    for (int u = 0; u < kFinSpans; ++u) {
+      if (base + u < nspv) {
+        sq += xq[u];
+        sk += xk[u];
+        sv += xv[u];
+      }
+    }
   }
+  const long long ld = (long long)H * kHeadDim;
+  const long long at = (long long)b * n * ld + (long long)p * ld + (long long)h * kHeadDim + c;
+  a.dq[at] = (__bf16)sq;
+  a.dk[at] = (__bf16)sk;
+  a.dv[at] = (__bf16)sv;
 }
 
 }  // namespace
@@ -677,23 +794,20 @@ hipError_t launch_soft_mask(const SoftArgs& a, hipStream_t s) {
 
 hipError_t launch_soft_backward(const SoftArgs& a, hipStream_t s) {
   const long long rows = (long long)a.B * a.n;
-  const unsigned bh = (unsigned)(a.B * a.H);
-  const unsigned nb = (unsigned)((a.n + 63) / 64);
+  const int bh = a.B * a.H, nb = (a.n + 63) / 64;
   const size_t bits = sizeof(uint32_t) * (((size_t)a.n + 31) / 32);
-  const unsigned ngr = bh * (unsigned)(a.Gp / 64) * (unsigned)a.nsp;
+  const int nglob = bh * (a.Gp / 64) * a.nsp;  // 0 without global tokens
+  BwdGrid gd;
+  gd.gr = (nglob + 7) & ~7;
+  gd.gc = gd.gr;
+  gd.band = ((bh * nb) + 7) & ~7;
   hipLaunchKernelGGL(k_soft_rows, dim3((unsigned)((rows + 3) / 4)), dim3(256), 0, s, a);
-  hipLaunchKernelGGL((k_bwd_rows<0, false>), dim3(bh * nb), dim3(256), bits, s, a);
-  if (a.G > 0) {
-    hipLaunchKernelGGL((k_bwd_rows<0, true>), dim3(ngr), dim3(256), 0, s, a);
-    hipLaunchKernelGGL(k_bwd_dfin, dim3(bh), dim3(64), 0, s, a);
-  }
-  hipLaunchKernelGGL((k_bwd_rows<1, false>), dim3(bh * nb), dim3(256), bits, s, a);
-  hipLaunchKernelGGL((k_bwd_cols<false>), dim3(bh * nb), dim3(256), bits, s, a);
-  if (a.G > 0) {
-    hipLaunchKernelGGL((k_bwd_rows<1, true>), dim3(ngr), dim3(256), 0, s, a);
-    hipLaunchKernelGGL((k_bwd_cols<true>), dim3(ngr), dim3(256), 0, s, a);
-  }
-  hipLaunchKernelGGL(k_bwd_finish, dim3(bh + 1), dim3(256), 0, s, a);
+  hipLaunchKernelGGL(k_bwd_dpass, dim3((unsigned)(gd.gr + bh * nb)), dim3(256), bits, s, a, gd);
+  if (a.G > 0) hipLaunchKernelGGL(k_bwd_dfin, dim3((unsigned)bh), dim3(64), 0, s, a);
+  hipLaunchKernelGGL(k_bwd_grad, dim3((unsigned)(gd.gc + gd.gr + gd.band + bh * nb)), dim3(256), bits, s, a, gd);
+  const long long nel = (a.G > 0 && a.gpos) ? (long long)bh * a.G * kHeadDim : 0;
+  const int nfin = (int)((nel + 255) / 256);
+  hipLaunchKernelGGL(k_bwd_finish, dim3((unsigned)(nfin + 1)), dim3(256), 0, s, a, nfin);
   return hipGetLastError();
 }
 

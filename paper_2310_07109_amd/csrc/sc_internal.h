@@ -106,7 +106,7 @@ struct SoftArgs {
   __bf16* dO;           // [B, n, H, 64]  mask * dy
   float* Dq;            // [B, H, n]      sum_j P dL/dP of each query row
   float* gk;            // [B, n]         score gradient of each key over H * L
-  float* dsv;           // [B, n]         score gradient (for the threshold's)
+  float* dsv;           // [B n / 4]      score gradients summed per 4 tokens (for the threshold's)
   float* gpg;           // [B, H, nsp, Gp]      global rows: sum_j P g per key span
   float* gdq;           // [B, H, nsp, Gp, 64]  global rows: dQ per key span
   float* gdk;           // [B, H, nsp, Gp, 64]  global keys: dK per query span
