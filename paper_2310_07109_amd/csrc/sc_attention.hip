@@ -602,13 +602,17 @@ SC_DEV void gr_fwd_block(const AttnArgs& a, int lin, Smem<DT>& sm) {
 }
 
 
-// ------------------------------------------- bf16 pass 1, 32 queries a wave --
-// A wave owns 32 queries as two 16-query sub-blocks that share every K
-// fragment and every V read (two MFMAs per LDS read).  K/V tiles reach LDS
+// ----------------------------------------------------------- bf16 pass 1 --
+// A wave owns kSub1 16-query sub-blocks that share every K fragment and every
+// V read.  K/V tiles reach LDS
 // through the direct global->LDS loads of gfx950, without staging registers:
 // lane i of a wave load fills the 16 bytes at base + 16 i, so the swizzled
 // layout is produced by choosing which 16-byte unit of its row lane i fetches.
-constexpr int kBQ2 = 128;
+// 16-query sub-blocks per wave.  Two share every K fragment and V read
+// (two MFMAs per LDS read) but need 168 VGPRs (3 waves per SIMD); one needs
+// 118 (4 waves per SIMD), which measured 3-5 % faster.
+constexpr int kSub1 = 1;
+constexpr int kBQ2 = 64 * kSub1;  // queries per block
 
 // Rows 16w .. 16w+15 of a 64-row bf16 tile (two wave loads of 8 rows); tile
 // row R holds global row rowfn(R), which must be a valid row.  Byte offsets
@@ -624,26 +628,27 @@ SC_DEV void tile_dma(const __bf16* g, unsigned ld_bytes, __bf16* tile, int w, in
   }
 }
 
-// One 64-key tile for the two query sub-blocks of a wave.  Bit st of `live`
+// One 64-key tile for the query sub-blocks of a wave.  Bit st of `live`
 // (wave-uniform) says whether 16-key sub-tile st can hold an allowed pair; in
 // masked tiles ok(j, st, i) decides the pair (sub-block j's query, key
 // 16 st + 4g + i).  Disallowed logits become -inf, which exp2 maps to 0
 // (c2 > 0 is guaranteed by the host).
 // S^T = K Q^T of one 64-key tile for both sub-blocks; dead sub-tiles give 0.
 template <bool kMasked>
-SC_DEV void qk_tile2(const bf16x8 (&qf)[2][2], const __bf16* sK, int lr_in, int g_in, unsigned live, f32x4 (&s)[2][4]) {
+SC_DEV void qk_tile2(const bf16x8 (&qf)[kSub1][2], const __bf16* sK, int lr_in, int g_in, unsigned live,
+                     f32x4 (&s)[kSub1][4]) {
   using TR = Tr<1>;
   auto is_live = [&](int st) { return !kMasked || ((live >> st) & 1u); };
   const int lr = lr_in, g = g_in;
 #pragma unroll
   for (int st = 0; st < 4; ++st) {
-    s[0][st] = f32x4{0.f, 0.f, 0.f, 0.f};
-    s[1][st] = f32x4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+    for (int j = 0; j < kSub1; ++j) s[j][st] = f32x4{0.f, 0.f, 0.f, 0.f};
     if (is_live(st)) {
       bf16x8 kf[2];
       TR::load_frags(sK, 16 * st + lr, g, kf);
 #pragma unroll
-      for (int j = 0; j < 2; ++j) {
+      for (int j = 0; j < kSub1; ++j) {
         s[j][st] = TR::mma(kf[0], qf[j][0], s[j][st]);
         s[j][st] = TR::mma(kf[1], qf[j][1], s[j][st]);
       }
@@ -652,9 +657,9 @@ SC_DEV void qk_tile2(const bf16x8 (&qf)[2][2], const __bf16* sK, int lr_in, int 
 }
 
 // Row maxima of a tile in log2 units (per sub-block).
-SC_DEV void tile_max2(const f32x4 (&s)[2][4], float c2, float (&tmax)[2]) {
+SC_DEV void tile_max2(const f32x4 (&s)[kSub1][4], float c2, float (&tmax)[kSub1]) {
 #pragma unroll
-  for (int j = 0; j < 2; ++j) {
+  for (int j = 0; j < kSub1; ++j) {
     float m4[4];
 #pragma unroll
     for (int st = 0; st < 4; ++st) m4[st] = vmax(vmax(s[j][st][0], s[j][st][1]), vmax(s[j][st][2], s[j][st][3]));
@@ -663,15 +668,19 @@ SC_DEV void tile_max2(const f32x4 (&s)[2][4], float c2, float (&tmax)[2]) {
 }
 
 // Whether any lane's running max must be raised (tile max above it by kTau).
-SC_DEV bool need_raise2(const float (&tmax)[2], const float (&m_use)[2]) {
-  return __builtin_amdgcn_ballot_w64((tmax[0] > m_use[0] + kTau) | (tmax[1] > m_use[1] + kTau)) != 0ull;
+SC_DEV bool need_raise2(const float (&tmax)[kSub1], const float (&m_use)[kSub1]) {
+  bool up = false;
+#pragma unroll
+  for (int j = 0; j < kSub1; ++j) up |= tmax[j] > m_use[j] + kTau;
+  return __builtin_amdgcn_ballot_w64(up) != 0ull;
 }
 
 // Raises the running maxima that need it and rescales their sums and
 // accumulators (lanes that do not need it scale by 1).
-SC_DEV void raise2(const float (&tmax)[2], float (&m_use)[2], float (&l_run)[2], f32x4 (&o)[2][4]) {
+SC_DEV void raise2(const float (&tmax)[kSub1], float (&m_use)[kSub1], float (&l_run)[kSub1],
+                   f32x4 (&o)[kSub1][4]) {
 #pragma unroll
-  for (int j = 0; j < 2; ++j) {
+  for (int j = 0; j < kSub1; ++j) {
     const bool up = tmax[j] > m_use[j] + kTau;
     const float f = up ? fast_exp2(m_use[j] - tmax[j]) : 1.0f;
     m_use[j] = up ? tmax[j] : m_use[j];
@@ -683,14 +692,14 @@ SC_DEV void raise2(const float (&tmax)[2], float (&m_use)[2], float (&l_run)[2],
 
 // P = exp2(S c2 - m) (summed into l) and O^T += V^T P^T for one tile.
 template <bool kMasked>
-SC_DEV void pv_tile2(const f32x4 (&s)[2][4], const __bf16* sV, float c2, int, int, const float (&m_use)[2],
-                     float (&l_run)[2], f32x4 (&o)[2][4], unsigned live) {
+SC_DEV void pv_tile2(const f32x4 (&s)[kSub1][4], const __bf16* sV, float c2, int, int, const float (&m_use)[kSub1],
+                     float (&l_run)[kSub1], f32x4 (&o)[kSub1][4], unsigned live) {
   using TR = Tr<1>;
   auto is_live = [&](int st) { return !kMasked || ((live >> st) & 1u); };
   const int ln = opaque_lane(), lr = ln & 15, g = ln >> 4;
-  bf16x8 pb[2][2];
+  bf16x8 pb[kSub1][2];
 #pragma unroll
-  for (int j = 0; j < 2; ++j) {
+  for (int j = 0; j < kSub1; ++j) {
     float part[4];
 #pragma unroll
     for (int st = 0; st < 4; ++st) {
@@ -715,39 +724,40 @@ SC_DEV void pv_tile2(const f32x4 (&s)[2][4], const __bf16* sV, float c2, int, in
       const i16x4 a0 = lds_read_tr16(sV + TR::off(vr, 2 * dt + b) + e);
       const i16x4 a1 = lds_read_tr16(sV + TR::off(vr + 16, 2 * dt + b) + e);
       const bf16x8 vf = __builtin_bit_cast(bf16x8, __builtin_shufflevector(a0, a1, 0, 1, 2, 3, 4, 5, 6, 7));
-      o[0][dt] = TR::mma(vf, pb[0][kc], o[0][dt]);
-      o[1][dt] = TR::mma(vf, pb[1][kc], o[1][dt]);
+#pragma unroll
+      for (int j = 0; j < kSub1; ++j) o[j][dt] = TR::mma(vf, pb[j][kc], o[j][dt]);
     }
   }
 }
 
-// One 64-key tile for the two query sub-blocks of a wave.  Bit st of `live`
+// One 64-key tile for the query sub-blocks of a wave.  Bit st of `live`
 // (wave-uniform) says whether 16-key sub-tile st can hold an allowed pair; in
 // masked tiles ok(j, st, i) decides the pair (sub-block j's query, key
 // 16 st + 4g + i).  Disallowed logits become -inf, which exp2 maps to 0
 // (c2 > 0 is guaranteed by the host).  The running max is raised only when
 // the tile max exceeds it by kTau (for the whole wave when any lane needs it).
 template <bool kMasked, typename OkFn>
-SC_DEV void softmax_tile2(const bf16x8 (&qf)[2][2], const __bf16* sK, const __bf16* sV, float c2, int lr, int g,
-                          float (&m_use)[2], float (&l_run)[2], f32x4 (&o)[2][4], unsigned live, OkFn ok) {
-  f32x4 s[2][4];
+SC_DEV void softmax_tile2(const bf16x8 (&qf)[kSub1][2], const __bf16* sK, const __bf16* sV, float c2, int lr,
+                          int g, float (&m_use)[kSub1], float (&l_run)[kSub1], f32x4 (&o)[kSub1][4], unsigned live,
+                          OkFn ok) {
+  f32x4 s[kSub1][4];
   qk_tile2<kMasked>(qf, sK, lr, g, live, s);
   if constexpr (kMasked) {
 #pragma unroll
-    for (int j = 0; j < 2; ++j)
+    for (int j = 0; j < kSub1; ++j)
 #pragma unroll
       for (int st = 0; st < 4; ++st)
 #pragma unroll
         for (int i = 0; i < 4; ++i)
           s[j][st][i] = (((live >> st) & 1u) && ok(j, st, i)) ? s[j][st][i] : -INFINITY;
   }
-  float tmax[2];
+  float tmax[kSub1];
   tile_max2(s, c2, tmax);
   if (need_raise2(tmax, m_use)) raise2(tmax, m_use, l_run, o);
   pv_tile2<kMasked>(s, sV, c2, lr, g, m_use, l_run, o, live);
 }
 
-// Pass 1 for bf16: O, LSE and the log2 LSE of the block's 128 queries.
+// Pass 1 for bf16: O, LSE and the log2 LSE of the block's kBQ2 queries.
 SC_DEV void window_fwd_v2(const AttnArgs& a, int blk, Smem<1>& sm, uint32_t* sDyn) {
   using T = __bf16;
   const WinBlock wb = win_block<kBQ2>(a, blk);
@@ -788,10 +798,11 @@ SC_DEV void window_fwd_v2(const AttnArgs& a, int blk, Smem<1>& sm, uint32_t* sDy
   tile_dma(Vg, ldb, sm.c[0], w, lane, band_rows(kt0));
   // query fragments straight from HBM (rows clamped below L; same dims per
   // lane group as the key fragments)
-  const int qa = q0 + 32 * w;
-  bf16x8 qf[2][2];
+  constexpr int kWQ = 16 * kSub1;  // queries per wave
+  const int qa = q0 + kWQ * w;
+  bf16x8 qf[kSub1][2];
 #pragma unroll
-  for (int j = 0; j < 2; ++j) {
+  for (int j = 0; j < kSub1; ++j) {
     const T* qrow = Qg + (long long)min(qa + 16 * j + lr, L - 1) * ld;
     qf[j][0] = *reinterpret_cast<const bf16x8*>(qrow + 8 * g);
     qf[j][1] = *reinterpret_cast<const bf16x8*>(qrow + 32 + 8 * g);
@@ -801,12 +812,15 @@ SC_DEV void window_fwd_v2(const AttnArgs& a, int blk, Smem<1>& sm, uint32_t* sDy
     const int o = k - kt0;
     return (sBits[o >> 5] >> (o & 31)) & 1u;
   };
-  float m_use[2] = {kNegBig, kNegBig}, l_run[2] = {0.f, 0.f};
-  f32x4 o[2][4];
+  float m_use[kSub1], l_run[kSub1];
+  f32x4 o[kSub1][4];
 #pragma unroll
-  for (int j = 0; j < 2; ++j)
+  for (int j = 0; j < kSub1; ++j) {
+    m_use[j] = kNegBig;
+    l_run[j] = 0.f;
 #pragma unroll
     for (int dt = 0; dt < 4; ++dt) o[j][dt] = f32x4{0.f, 0.f, 0.f, 0.f};
+  }
   // all vector loads so far (the first tiles, the query fragments) complete
   // here; the compiler-visible wait keeps it from waiting for the query loads
   // inside the tile loop, where the prefetch loads are in flight
@@ -817,9 +831,9 @@ SC_DEV void window_fwd_v2(const AttnArgs& a, int blk, Smem<1>& sm, uint32_t* sDy
   // per-lane band bounds of sub-block j relative to a tile start, shifted by
   // the lane group's key offset 4g: key 16st + i of the lane is allowed when
   // it lies in [lo - k0, hi - k0]
-  int lo[2], hi[2];
+  int lo[kSub1], hi[kSub1];
 #pragma unroll
-  for (int j = 0; j < 2; ++j) {
+  for (int j = 0; j < kSub1; ++j) {
     const int q = qa + 16 * j + lr;
     lo[j] = q - r - 4 * g;
     hi[j] = min(q + rh, kt1 - 1) - 4 * g;
@@ -841,44 +855,48 @@ SC_DEV void window_fwd_v2(const AttnArgs& a, int blk, Smem<1>& sm, uint32_t* sDy
   auto edge_tile = [&](int t) {
     const int buf = t & 1, k0 = kt0 + t * kBK;
     const unsigned long long gall = tile_gmask(sBits, t, wb.nwords);
-    const bool near = k0 <= qa + 31 + rh && k0 + kBK - 1 >= qa - r;
+    const bool near = k0 <= qa + kWQ - 1 + rh && k0 + kBK - 1 >= qa - r;
     if (!near && gall == 0ull) return;
-    const int wlo = qa - r - k0, whi = min(qa + 31 + rh, kt1 - 1) - k0;
+    const int wlo = qa - r - k0, whi = min(qa + kWQ - 1 + rh, kt1 - 1) - k0;
     unsigned live = 0u;
 #pragma unroll
     for (int st = 0; st < 4; ++st)
       live |= (unsigned)((16 * st + 15 >= wlo && 16 * st <= whi) || ((gall >> (16 * st)) & 0xFFFFull) != 0ull) << st;
-    const int l0 = lo[0] - k0, h0 = hi[0] - k0, l1 = lo[1] - k0, h1 = hi[1] - k0;
+    int lt[kSub1], ht[kSub1];
+#pragma unroll
+    for (int j = 0; j < kSub1; ++j) {
+      lt[j] = lo[j] - k0;
+      ht[j] = hi[j] - k0;
+    }
     // a band edge is one-sided in most tiles: the band starts inside the
     // tile for some query (nlo) or ends inside it (nhi), wave-uniform
-    const bool nlo = qa + 31 - r - k0 > 0, nhi = min(qa + rh, kt1 - 1) - k0 < kBK - 1;
+    const bool nlo = qa + kWQ - 1 - r - k0 > 0, nhi = min(qa + rh, kt1 - 1) - k0 < kBK - 1;
     if (gall == 0ull && !nhi) {
       softmax_tile2<true>(qf, sm.b[buf], sm.c[buf], a.c2, lr, g, m_use, l_run, o, live,
-                          [&](int j, int st, int i) { return 16 * st + i >= (j == 0 ? l0 : l1); });
+                          [&](int j, int st, int i) { return 16 * st + i >= lt[j]; });
     } else if (gall == 0ull && !nlo) {
       softmax_tile2<true>(qf, sm.b[buf], sm.c[buf], a.c2, lr, g, m_use, l_run, o, live,
-                          [&](int j, int st, int i) { return 16 * st + i <= (j == 0 ? h0 : h1); });
+                          [&](int j, int st, int i) { return 16 * st + i <= ht[j]; });
     } else if (gall == 0ull) {
       softmax_tile2<true>(qf, sm.b[buf], sm.c[buf], a.c2, lr, g, m_use, l_run, o, live, [&](int j, int st, int i) {
         const int c = 16 * st + i;
-        return j == 0 ? (c >= l0) & (c <= h0) : (c >= l1) & (c <= h1);
+        return (c >= lt[j]) & (c <= ht[j]);
       });
     } else {
       const unsigned long long gm = gall >> (4 * g);
       // a global key is attended by every query, or (causal) by the queries
       // at or after it
-      const int g0 = causal ? h0 : 1 << 30, g1 = causal ? h1 : 1 << 30;
       softmax_tile2<true>(qf, sm.b[buf], sm.c[buf], a.c2, lr, g, m_use, l_run, o, live, [&](int j, int st, int i) {
         const int c = 16 * st + i;
-        const bool band = j == 0 ? (c >= l0) & (c <= h0) : (c >= l1) & (c <= h1);
-        return band | (((gm >> c) & 1ull) != 0ull && c <= (j == 0 ? g0 : g1));
+        const bool band = (c >= lt[j]) & (c <= ht[j]);
+        return band | (((gm >> c) & 1ull) != 0ull && c <= (causal ? ht[j] : 1 << 30));
       });
     }
   };
   // interior tiles [ia, ib) of this wave: every key of the tile lies in the
-  // band of all 32 queries and below kt1 (global keys among them are band
+  // band of all the wave's queries and below kt1 (global keys among them are band
   // keys), so no mask is needed
-  const int ia = clampi(-((kt0 - (qa + 31 - r)) >> 6), 0, nkt);
+  const int ia = clampi(-((kt0 - (qa + kWQ - 1 - r)) >> 6), 0, nkt);
   const int ib = clampi(((min(qa + rh, kt1 - 1) - (kBK - 1) - kt0) >> 6) + 1, ia, nkt);
   int t = 0;
   for (; t < ia; ++t) {
@@ -928,7 +946,7 @@ SC_DEV void window_fwd_v2(const AttnArgs& a, int blk, Smem<1>& sm, uint32_t* sDy
   }
 
 #pragma unroll
-  for (int j = 0; j < 2; ++j) {
+  for (int j = 0; j < kSub1; ++j) {
     const float l_row = group_sum(l_run[j]);
     const int qrow = qa + 16 * j + lr;
     const bool qin = qrow < L;
@@ -1665,7 +1683,7 @@ static hipError_t launch_window_t(const AttnArgs& a0, hipStream_t s) {
   a.n_bcol = cols ? a.nkb * a.H * a.B : 0;
   a.n_gcol = (cols && glob) ? a.nqr * a.ngc * a.H * a.B : 0;
   const int nxc = glob ? (a.G + kBK - 1) / kBK : 0;
-  if (DT == 1) {  // bf16 pass 1 runs 128-query blocks
+  if (DT == 1) {  // bf16 pass 1 runs kBQ2-query blocks
     a.nqb = (a.n + kBQ2 - 1) / kBQ2;
     const long long rw = (long long)kBQ2 + 2LL * a.r;
     a.rwp = (int)(rw < a.n ? rw : a.n);
