@@ -619,7 +619,7 @@ constexpr int kBQ2 = 64 * kSub1;  // queries per block
 // from the slice base fit in 32 bits (checked by the host).
 template <typename RowFn>
 SC_DEV void tile_dma(const __bf16* g, unsigned ld_bytes, __bf16* tile, int w, int, RowFn rowfn) {
-  const int lane = opaque_lane();
+  const int lane = threadIdx.x & 63;
 #pragma unroll
   for (int j = 0; j < 2; ++j) {
     const int R0 = 16 * w + 8 * j, R = R0 + (lane >> 3);
@@ -696,7 +696,7 @@ SC_DEV void pv_tile2(const f32x4 (&s)[kSub1][4], const __bf16* sV, float c2, int
                      float (&l_run)[kSub1], f32x4 (&o)[kSub1][4], unsigned live) {
   using TR = Tr<1>;
   auto is_live = [&](int st) { return !kMasked || ((live >> st) & 1u); };
-  const int ln = opaque_lane(), lr = ln & 15, g = ln >> 4;
+  const int ln = threadIdx.x & 63, lr = ln & 15, g = ln >> 4;
   bf16x8 pb[kSub1][2];
 #pragma unroll
   for (int j = 0; j < kSub1; ++j) {
