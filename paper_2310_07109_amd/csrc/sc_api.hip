@@ -426,6 +426,7 @@ struct StackWs {
   __bf16 *qkv, *o, *oc, *xc, *xa, *xb;
   __bf16 *x1, *h;  // feed-forward block: attention sub-layer output, hidden activations
   float *t, *scores, *partials;
+  float* split;  // slabs of the split reductions of the output and second feed-forward products
   int *len_a, *len_b, *gp_a, *gp_b, *orig_a, *orig_b, *keep_idx, *new_index;
   AttnArgs attn;
 };
@@ -445,6 +446,7 @@ size_t carve_stack(const sc_attn_desc* d, int F, void* base, StackWs* ws) {
   w.x1 = F > 0 ? c.take<__bf16>(bn * D) : nullptr;
   w.h = F > 0 ? c.take<__bf16>(bn * (size_t)F) : nullptr;
   w.t = c.take<float>(bn * D);
+  w.split = c.take<float>((size_t)sc::kGemmSplitRows * D);
   w.scores = c.take<float>(bn);
   w.partials = c.take<float>(sc::partials_floats(d->B, d->H, d->n, geo, d->G));
   w.len_a = c.take<int>(d->B);
@@ -515,7 +517,7 @@ sc_status run_stack(const sc_attn_desc* d, int32_t n_layers, const int32_t* wind
     const int window = windows ? windows[l] : d->window;
     __bf16* nxt = (l == n_layers - 1) ? static_cast<__bf16*>(x_out) : ((l & 1) ? w.xb : w.xa);
     // a1: qkv projection of the surviving rows
-    chk(sc::launch_gemm_bf16(cur, Wqkv[l], w.qkv, sc::kGemmBf16, B, n, Di, 3 * Di, len_cur, s));
+    chk(sc::launch_gemm_bf16(cur, Wqkv[l], w.qkv, sc::kGemmBf16, B, n, Di, 3 * Di, len_cur, nullptr, s));
     // a2-a5: sparse attention reading q|k|v out of the fused projection
     AttnArgs a = w.attn;
     set_window(a, n, window, G);
@@ -568,15 +570,15 @@ sc_status run_stack(const sc_attn_desc* d, int32_t n_layers, const int32_t* wind
     ga.new_len = len_nxt;
     chk(sc::launch_gather(ga, s));
     // a9: output projection, residual, LayerNorm on the survivors
-    chk(sc::launch_gemm_bf16(w.oc, Wo[l], w.t, sc::kGemmF32, B, n, Di, Di, len_nxt, s));
+    chk(sc::launch_gemm_bf16(w.oc, Wo[l], w.t, sc::kGemmF32, B, n, Di, Di, len_nxt, w.split, s));
     if (!ffn) {
-      chk(sc::launch_residual_layernorm(w.xc, w.t, nxt, B, n, Di, ln_eps, len_nxt, s));
+      chk(sc::launch_residual_layernorm(w.xc, w.t, nxt, B, n, Di, ln_eps, len_nxt, w.split, Di, s));
     } else {
       // feed-forward block: h = GELU(x1 . W1), then LayerNorm(x1 + h . W2)
-      chk(sc::launch_residual_layernorm(w.xc, w.t, w.x1, B, n, Di, ln_eps, len_nxt, s));
-      chk(sc::launch_gemm_bf16(w.x1, W1[l], w.h, sc::kGemmGeluBf16, B, n, Di, F, len_nxt, s));
-      chk(sc::launch_gemm_bf16(w.h, W2[l], w.t, sc::kGemmF32, B, n, F, Di, len_nxt, s));
-      chk(sc::launch_residual_layernorm(w.x1, w.t, nxt, B, n, Di, ln_eps, len_nxt, s));
+      chk(sc::launch_residual_layernorm(w.xc, w.t, w.x1, B, n, Di, ln_eps, len_nxt, w.split, Di, s));
+      chk(sc::launch_gemm_bf16(w.x1, W1[l], w.h, sc::kGemmGeluBf16, B, n, Di, F, len_nxt, nullptr, s));
+      chk(sc::launch_gemm_bf16(w.h, W2[l], w.t, sc::kGemmF32, B, n, F, Di, len_nxt, w.split, s));
+      chk(sc::launch_residual_layernorm(w.x1, w.t, nxt, B, n, Di, ln_eps, len_nxt, w.split, F, s));
     }
     if (kept_per_layer) chk(sc::launch_record_len(len_nxt, kept_per_layer + (size_t)l * B, B, s));
     cur = nxt;

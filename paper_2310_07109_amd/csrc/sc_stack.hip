@@ -26,8 +26,17 @@
 //               M tile t of sequence b goes to XCD (t + b) mod 8, so that the
 //               first tiles of the sequences (often the only live ones after
 //               pruning) spread over the XCDs.
+//               Split reduction for small float32 products: when the
+//               surviving rows fill few tiles (after pruning, often one per
+//               sequence), S blocks per output tile each take K / S of the
+//               reduction and write float32 partial sums into slabs; the
+//               residual LayerNorm adds the slabs in the fixed order
+//               s = 0 .. S-1.  Both kernels derive S from the lengths, so the
+//               host needs no synchronisation.
 // k_residual_ln y = bf16(LayerNorm(x + t)), one wavefront per row, fp32
 //               statistics (biased variance), gamma = 1, beta = 0.
+#include <algorithm>
+
 #include "sc_device.h"
 #include "sc_internal.h"
 
@@ -135,6 +144,36 @@ SC_DEV int gw_off(int row, int unit) { return row * kBN + 8 * (unit ^ (2 * (row 
 // 4g + t holds k = 8g + t and LDS row 16 + 4g + t holds k = 8g + 4 + t.
 SC_DEV int gw_krow(int r) { return (r & ~31) + 8 * ((r & 15) >> 2) + 4 * ((r >> 4) & 1) + (r & 3); }
 
+// Split of the reduction (see the header): tiles = 128-row tiles of the
+// surviving rows (per sequence), S = number of K ranges.  S doubles while
+// the partial sums stay within kGemmSplitRows rows, the launch within
+// kSplitBlocks workgroups, and every range keeps at least 3 stages.  One
+// wave computes it with lane b reading len[b] (B <= kSplitMaxB, else no
+// split); excl = live tiles of the sequences before the lane's, incl = excl
+// plus the lane's own.
+constexpr int kSplitMaxB = 64, kSplitMax = 8, kSplitBlocks = 1024;
+struct SplitPlan {
+  int tiles, S;
+};
+SC_DEV SplitPlan split_plan(const int* len, int B, int n, int Nt, int nk, int& excl, int& incl) {
+  const int lane = threadIdx.x & 63;
+  const bool ok = len && B <= kSplitMaxB;
+  const int c = ok && lane < B ? (clampi(len[lane], 0, n) + kBM - 1) / kBM : 0;
+  incl = c;
+#pragma unroll
+  for (int d = 1; d < 64; d <<= 1) {
+    const int y = __shfl_up(incl, d, 64);
+    if (lane >= d) incl += y;
+  }
+  excl = incl - c;
+  SplitPlan p{__builtin_amdgcn_readlane(incl, 63), 1};
+  if (!ok) return p;
+  while (2 * p.S <= kSplitMax && p.tiles * 2 * p.S * kBM <= kGemmSplitRows &&
+         p.tiles * Nt * 2 * p.S <= kSplitBlocks && nk % (2 * p.S) == 0 && nk / (2 * p.S) >= 3)
+    p.S *= 2;
+  return p;
+}
+
 SC_DEV void gemm_store(void* Y, int mode, long long off, float v) {
   if (mode == kGemmF32)
     static_cast<float*>(Y)[off] = v;
@@ -144,26 +183,44 @@ SC_DEV void gemm_store(void* Y, int mode, long long off, float v) {
     static_cast<__bf16*>(Y)[off] = (__bf16)v;
 }
 
+// part: float32 slabs of the split reduction (NULL: no split; mode must be
+// kGemmF32 otherwise).
 __global__ __launch_bounds__(256) void k_gemm_v2(const __bf16* __restrict__ X, const __bf16* __restrict__ W,
                                                  void* __restrict__ Y, int mode, int B, int n, int K, int N,
-                                                 const int* __restrict__ len) {
+                                                 const int* __restrict__ len, float* __restrict__ part) {
   __shared__ GemmSmem sm;
-  // block i runs on XCD i % 8 and takes the (i / 8 / Nt)-th M tile of that
-  // XCD (tiles t = (x - b) mod 8, +8, ... of sequences b = 0, 1, ...) with
-  // N tile (i / 8) % Nt
-  const int Nt = N / kBN, Mt = (n + kBM - 1) / kBM;
-  const int xcd = blockIdx.x & 7, j = blockIdx.x >> 3;
-  const int jm = j / Nt, nt = j % Nt;
-  int b = -1, t = 0;
-  for (int bb = 0, acc = 0; bb < B; ++bb) {
-    const int t0 = (xcd - bb) & 7;
-    const int cnt = t0 < Mt ? (Mt - t0 + 7) / 8 : 0;
-    if (jm < acc + cnt) {
-      b = bb;
-      t = t0 + 8 * (jm - acc);
-      break;
+  const int Nt = N / kBN, Mt = (n + kBM - 1) / kBM, nk = K / kGK;
+  int excl = 0, incl = 0;
+  const SplitPlan sp = part ? split_plan(len, B, n, Nt, nk, excl, incl) : SplitPlan{0, 1};
+  int b = -1, t = 0, nt = 0, ks = 0, tile = 0;
+  if (sp.S > 1) {
+    // block i: K range i % S of output tile (i / S) % Nt of the (i / S / Nt)-th live M tile
+    int item = blockIdx.x;
+    if (item >= sp.tiles * Nt * sp.S) return;
+    ks = item % sp.S;
+    item /= sp.S;
+    nt = item % Nt;
+    tile = item / Nt;
+    const unsigned long long owner = __ballot(incl > tile);  // lanes of the sequence holding the tile and after
+    b = __builtin_ctzll(owner);
+    t = tile - __shfl(excl, b, 64);
+  } else {
+    // block i runs on XCD i % 8 and takes the (i / 8 / Nt)-th M tile of that
+    // XCD (tiles t = (x - b) mod 8, +8, ... of sequences b = 0, 1, ...) with
+    // N tile (i / 8) % Nt
+    const int xcd = blockIdx.x & 7, j = blockIdx.x >> 3;
+    const int jm = j / Nt;
+    nt = j % Nt;
+    for (int bb = 0, acc = 0; bb < B; ++bb) {
+      const int t0 = (xcd - bb) & 7;
+      const int cnt = t0 < Mt ? (Mt - t0 + 7) / 8 : 0;
+      if (jm < acc + cnt) {
+        b = bb;
+        t = t0 + 8 * (jm - acc);
+        break;
+      }
+      acc += cnt;
     }
-    acc += cnt;
   }
   if (b < 0) return;
   const int m0 = t * kBM, n0 = nt * kBN;
@@ -195,13 +252,13 @@ __global__ __launch_bounds__(256) void k_gemm_v2(const __bf16* __restrict__ X, c
   for (int i = 0; i < 4; ++i)
 #pragma unroll
     for (int jn = 0; jn < 4; ++jn) acc[i][jn] = f32x4{0.f, 0.f, 0.f, 0.f};
-  const int nk = K / kGK;
-  issue(0, 0);
+  const int per = nk / sp.S, s0 = ks * per, s1 = s0 + per;  // this block's stages
+  issue(s0 * kGK, 0);
   wait_dma();
   __syncthreads();
-  for (int s = 0; s < nk; ++s) {
-    const int bf = s & 1;
-    if (s + 1 < nk) issue((s + 1) * kGK, bf ^ 1);
+  for (int s = s0; s < s1; ++s) {
+    const int bf = (s - s0) & 1;
+    if (s + 1 < s1) issue((s + 1) * kGK, bf ^ 1);
     const __bf16* sx = sm.x[bf];
     const __bf16* sw = sm.w[bf];
 #pragma unroll
@@ -223,10 +280,24 @@ __global__ __launch_bounds__(256) void k_gemm_v2(const __bf16* __restrict__ X, c
         for (int jn = 0; jn < 4; ++jn)
           acc[i][jn] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(af[i], bfr[jn], acc[i][jn], 0, 0, 0);
     }
-    if (s + 1 < nk) wait_dma();
+    if (s + 1 < s1) wait_dma();
     __syncthreads();
   }
-  // result (row wm + 16i + 4g + e, col wn + 16jn + lr)
+  // result (row wm + 16i + 4g + e, col wn + 16jn + lr); split: partial ks of
+  // element (128 tile + m - m0, col) at part[((128 tile + m - m0) N + col) S + ks]
+  if (sp.S > 1) {
+    float* slab = part + ((long long)(tile * kBM - m0) * N) * sp.S + ks;
+#pragma unroll
+    for (int i = 0; i < 4; ++i)
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        const int m = m0 + wm + 16 * i + 4 * g + e;
+        if (m >= rows) continue;
+#pragma unroll
+        for (int jn = 0; jn < 4; ++jn) slab[((long long)m * N + n0 + wn + 16 * jn + lr) * sp.S] = acc[i][jn][e];
+      }
+    return;
+  }
 #pragma unroll
   for (int i = 0; i < 4; ++i)
 #pragma unroll
@@ -239,26 +310,71 @@ __global__ __launch_bounds__(256) void k_gemm_v2(const __bf16* __restrict__ X, c
     }
 }
 
-__global__ __launch_bounds__(256) void k_residual_ln(const __bf16* __restrict__ xr, const float* __restrict__ t,
+// Element c of a row's S partial sums (consecutive floats), added in order.
+template <int S>
+SC_DEV float slab_sum(const float* p) {
+  if constexpr (S == 1) {
+    return *p;
+  } else if constexpr (S == 2) {
+    const float2 a = *reinterpret_cast<const float2*>(p);
+    return a.x + a.y;
+  } else {
+    const float4 a = *reinterpret_cast<const float4*>(p);
+    float r = ((a.x + a.y) + a.z) + a.w;
+    if constexpr (S == 8) {
+      const float4 c = *reinterpret_cast<const float4*>(p + 4);
+      r = (((r + c.x) + c.y) + c.z) + c.w;
+    }
+    return r;
+  }
+}
+
+// v[u] = x[c] + t[c] for c = lane + 64 u, t from the row's partial sums.
+template <int S, int kPer>
+SC_DEV void ln_load(float (&v)[kPer], const __bf16* xp, const float* tp, int D, int lane) {
+#pragma unroll
+  for (int u = 0; u < kPer; ++u) {
+    const int c = lane + 64 * u;
+    v[u] = c < D ? slab_sum<S>(tp + (long long)c * S) + (float)xp[c] : 0.f;
+  }
+}
+
+// part, K: the partial sums and reduction length of the product that wrote
+// t, when it may have split its reduction (t itself is then unused).
+// kMaxPer = elements per lane (D <= 64 kMaxPer).  Occupancy bound: 6 waves
+// per SIMD at 16 elements per lane (80 VGPRs, which the unsplit rows need
+// for latency hiding; the split path's wide loads are then issued in a few
+// rounds), 4 at 32.
+template <int kMaxPer>
+__global__ __launch_bounds__(256, kMaxPer <= 16 ? 6 : 4) void k_residual_ln(const __bf16* __restrict__ xr, const float* __restrict__ t,
                                                      __bf16* __restrict__ y, int B, int n, int D, float eps,
-                                                     const int* __restrict__ len) {
+                                                     const int* __restrict__ len, const float* __restrict__ part,
+                                                     int K) {
   const long long row = (long long)blockIdx.x * 4 + (threadIdx.x >> 6);
   const int lane = threadIdx.x & 63;
   if (row >= (long long)B * n) return;
   const int b = (int)(row / n), j = (int)(row % n);
   if (j >= clampi(len[b], 0, n)) return;
   const __bf16* xp = xr + row * D;
-  const float* tp = t + row * D;
   __bf16* yp = y + row * D;
-  constexpr int kMaxPer = 32;  // D <= 2048
   float v[kMaxPer];
+  // loaded as written by an unsplit product before the plan is known (replaced after a split)
+  ln_load<1, kMaxPer>(v, xp, t + row * D, D, lane);
+  int excl = 0, incl = 0;
+  const SplitPlan sp = part ? split_plan(len, B, n, D / kBN, K / kGK, excl, incl) : SplitPlan{0, 1};
+  if (sp.S > 1) {  // the row's place: its tile among the live tiles, then its row in the tile
+    const int tile = j / kBM + __shfl(excl, b, 64);
+    const float* tp = part + ((long long)tile * kBM + j % kBM) * D * sp.S;
+    if (sp.S == 2)
+      ln_load<2, kMaxPer>(v, xp, tp, D, lane);
+    else if (sp.S == 4)
+      ln_load<4, kMaxPer>(v, xp, tp, D, lane);
+    else
+      ln_load<8, kMaxPer>(v, xp, tp, D, lane);
+  }
   float s = 0.f;
 #pragma unroll
-  for (int u = 0; u < kMaxPer; ++u) {
-    const int c = lane + 64 * u;
-    v[u] = c < D ? (float)xp[c] + tp[c] : 0.f;
-    s += v[u];
-  }
+  for (int u = 0; u < kMaxPer; ++u) s += v[u];
   for (int m = 1; m < 64; m <<= 1) s += __shfl_xor(s, m, 64);
   const float mean = s / (float)D;
   float q = 0.f;
@@ -284,15 +400,23 @@ __global__ void k_record_len(const int* len, int* dst, int B) {
 
 }  // namespace
 
+namespace {
+bool gemm_v2_ok(int n, int K, int N) {
+  return K % kGK == 0 && N % kBN == 0 && K > 0 && N > 0 && (long long)n * K * 2 < (1LL << 32) &&
+         (long long)K * N * 2 < (1LL << 32);
+}
+}  // namespace
+
 hipError_t launch_gemm_bf16(const void* x, const void* w, void* y, int mode, int B, int n, int K, int N,
-                            const int* len, hipStream_t s) {
-  if (K % kGK == 0 && N % kBN == 0 && K > 0 && N > 0 && (long long)n * K * 2 < (1LL << 32) &&
-      (long long)K * N * 2 < (1LL << 32)) {
-    // per XCD at most B * ceil(Mt / 8) M tiles
+                            const int* len, float* part, hipStream_t s) {
+  if (gemm_v2_ok(n, K, N)) {
+    // per XCD at most B * ceil(Mt / 8) M tiles; a split launch needs at most kSplitBlocks
     const long long per_xcd = (long long)B * (((n + kBM - 1) / kBM + 7) / 8);
-    const long long blocks = 8 * (long long)(N / kBN) * per_xcd;
+    long long blocks = 8 * (long long)(N / kBN) * per_xcd;
+    if (part && mode == kGemmF32 && len) blocks = std::max<long long>(blocks, kSplitBlocks);
+    else part = nullptr;
     hipLaunchKernelGGL(k_gemm_v2, dim3((unsigned)blocks), dim3(256), 0, s, static_cast<const __bf16*>(x),
-                       static_cast<const __bf16*>(w), y, mode, B, n, K, N, len);
+                       static_cast<const __bf16*>(w), y, mode, B, n, K, N, len, part);
     return hipGetLastError();
   }
   dim3 grid((N + kBN - 1) / kBN, (n + kBM - 1) / kBM, B);
@@ -302,10 +426,12 @@ hipError_t launch_gemm_bf16(const void* x, const void* w, void* y, int mode, int
 }
 
 hipError_t launch_residual_layernorm(const void* x_res, const float* t, void* y, int B, int n, int D, float eps,
-                                     const int* len, hipStream_t s) {
+                                     const int* len, const float* part, int K, hipStream_t s) {
   const long long rows = (long long)B * n;
-  hipLaunchKernelGGL(k_residual_ln, dim3((unsigned)((rows + 3) / 4)), dim3(256), 0, s,
-                     static_cast<const __bf16*>(x_res), t, static_cast<__bf16*>(y), B, n, D, eps, len);
+  if (!gemm_v2_ok(n, K, D)) part = nullptr;  // the product took the path without a split
+  auto* kern = D <= 1024 ? k_residual_ln<16> : k_residual_ln<32>;  // D <= 2048 (checked by the caller)
+  hipLaunchKernelGGL(kern, dim3((unsigned)((rows + 3) / 4)), dim3(256), 0, s, static_cast<const __bf16*>(x_res), t,
+                     static_cast<__bf16*>(y), B, n, D, eps, len, part, K);
   return hipGetLastError();
 }
 

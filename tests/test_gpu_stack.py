@@ -191,3 +191,28 @@ def test_full_encoder_config_sampled_sequences():
     layerwise(inp["x"], inp["wqkv"], inp["wo"], vl, inp["global_pos"], cfg.H, cfg.window, cfg.alpha,
               cfg.thresholds(), seqs=seqs, tag="full encoder", w1_bits=inp["w1"], w2_bits=inp["w2"],
               windows=inp["windows"])
+
+
+def test_split_reduction_full_layers():
+    """RoBERTa-base widths (D 768, FFN 3072) on few short sequences: the surviving rows fill at most nine
+    128-row tiles, so the output and second feed-forward products split their 768- and 3072-long reductions
+    into float32 slabs that the residual LayerNorm adds in a fixed order.  Layer by layer against the oracle,
+    and the two-layer call equals the chain of single-layer calls bit for bit (the split is deterministic)."""
+    cfg = si.StackConfig("split full", 25, 3, 300, 12, 64, 2, 64, (120, 300), 1, 0.02, 0.004, ffn_dim=3072,
+                         windows=(32, 96))
+    inp = si.make_stack_inputs(cfg)
+    inp["valid_len"][1] = 7
+    inp["global_pos"] = si.global_positions(cfg.seed, inp["valid_len"], 1, "first")
+    thetas = [0.0, 0.004]
+    xl, vl_final = layerwise(inp["x"], inp["wqkv"], inp["wo"], inp["valid_len"], inp["global_pos"], cfg.H,
+                             cfg.window, cfg.alpha, thetas, tag="split full", w1_bits=inp["w1"], w2_bits=inp["w2"],
+                             windows=inp["windows"])
+    d = sc.Desc(cfg.B, cfg.n, cfg.H, cfg.window, dev_i32(inp["valid_len"]), dev_i32(inp["global_pos"]), cfg.alpha,
+                sc.SC_BF16)
+    dv = lambda ws: [bf16_dev(w) for w in ws]  # noqa: E731
+    y, fl, orig, kpl = sc.sc_encoder_stack(d, bf16_dev(inp["x"]), dv(inp["wqkv"]), dv(inp["wo"]), dv(inp["w1"]),
+                                           dv(inp["w2"]), thetas, windows=inp["windows"])
+    fl = fl.cpu().numpy()
+    assert np.array_equal(fl, vl_final)
+    for b in range(cfg.B):
+        assert torch.equal(y[b, :fl[b]].view(torch.int16), xl[b, :fl[b]].view(torch.int16))
