@@ -11,12 +11,13 @@
 //               runs on the surviving tokens only.  Epilogue: bf16 store,
 //               fp32 store, or GELU (exact form, x * Phi(x)) then bf16 store
 //               for the first feed-forward product.
-// k_gemm_v2     the same product when K % 64 == 0 and N % 128 == 0 (the
-//               encoder's shapes): 128 x 128 workgroup tile, K stages of 64
-//               brought into LDS by gfx950's direct global->LDS loads, double
-//               buffered.  X rows are stored as 128-byte rows whose 16-byte
-//               units are XOR-swizzled by the row's low 3 bits and read as
-//               16-byte A fragments; W stays row-major ([k][n], 256-byte rows,
+// k_gemm_v2     the same product when K % 32 == 0 and N % 128 == 0 (the
+//               encoder's shapes): 128 x 128 workgroup tile, K stages of 32
+//               brought into LDS by gfx950's direct global->LDS loads, three
+//               stage buffers with two stages in flight (48 KB, so three
+//               workgroups share a CU).  X rows are stored as 64-byte rows
+//               whose 16-byte units are XOR-swizzled by bits 2-3 of the row
+//               and read as 16-byte A fragments; W stays row-major ([k][n], 256-byte rows,
 //               units swizzled by twice the row's low 3 bits) and the B
 //               fragments (8 consecutive k of one column) come from transposing
 //               LDS reads (ds_read_b64_tr_b16).  Those reads hand each lane the
@@ -131,14 +132,32 @@ __global__ __launch_bounds__(256) void k_gemm_bf16(const __bf16* __restrict__ X,
     }
 }
 
-constexpr int kGK = 64;  // k per stage of k_gemm_v2
+// k per stage of k_gemm_v2 and stage buffers (kNBuf - 1 stages in flight).
+// 32 x 3 (48 KB of LDS, three workgroups per CU) measured faster than 64 x 2
+// (64 KB, two per CU), 32 x 4 (two per CU, three stages in flight) and
+// 64 x 3 (one per CU): workgroups per CU matter more than prefetch depth.
+constexpr int kGK = 32;
+constexpr int kNBuf = 3;
+constexpr int kXUnits = kGK / 8;     // 16-byte units per X row
+constexpr int kDmaPerStage = kGK / 8;  // direct loads per thread and stage (X and W)
 
 struct GemmSmem {
-  __attribute__((aligned(16))) __bf16 x[2][kBM * kGK];  // [row][k], 128-byte rows
-  __attribute__((aligned(16))) __bf16 w[2][kGK * kBN];  // [k][n], 256-byte rows
+  __attribute__((aligned(16))) __bf16 x[kNBuf][kBM * kGK];  // [row][k], 2 kGK-byte rows
+  __attribute__((aligned(16))) __bf16 w[kNBuf][kGK * kBN];  // [k][n], 256-byte rows
 };
 
-SC_DEV int gx_off(int row, int unit) { return row * kGK + 8 * (unit ^ (row & 7)); }
+// X rows of 8 units (64 k) swizzle by the row's low 3 bits; rows of 4 units
+// (32 k) by bits 2-3, so that 16 consecutive rows read at one unit hit 16
+// distinct 16-byte bank groups
+SC_DEV int gx_off(int row, int unit) {
+  return row * kGK + 8 * (unit ^ (kXUnits == 8 ? (row & 7) : ((row >> 2) & 3)));
+}
+// s_waitcnt vmcnt(n) alone (expcnt and lgkmcnt at their no-wait maxima)
+template <int N>
+SC_DEV void wait_vm() {
+  static_assert(N >= 0 && N < 64, "vmcnt range");
+  __builtin_amdgcn_s_waitcnt((N & 15) | ((N >> 4) << 14) | (7 << 4) | (15 << 8));
+}
 SC_DEV int gw_off(int row, int unit) { return row * kBN + 8 * (unit ^ (2 * (row & 7))); }
 // W row held by LDS row r of a stage: within each 32-row chunk, LDS row
 // 4g + t holds k = 8g + t and LDS row 16 + 4g + t holds k = 8g + 4 + t.
@@ -233,16 +252,17 @@ __global__ __launch_bounds__(256) void k_gemm_v2(const __bf16* __restrict__ X, c
   const unsigned xrow_b = 2u * (unsigned)K, wrow_b = 2u * (unsigned)N;  // byte offsets fit in 32 bits (host)
   auto issue = [&](int k0, int bf) {
     const int ln = opaque_lane();
+    constexpr int kXRows = 64 / kXUnits;  // X rows per load (1 KB)
 #pragma unroll
-    for (int t = 0; t < 4; ++t) {  // X: wave w fills rows 32w .. 32w+31, 8 rows per load
-      const int R0 = 32 * w + 8 * t, R = R0 + (ln >> 3);
-      const int u = (ln & 7) ^ (R & 7);
+    for (int t = 0; t < 32 / kXRows; ++t) {  // X: wave w fills rows 32w .. 32w+31
+      const int R0 = 32 * w + kXRows * t, R = R0 + ln / kXUnits;
+      const int u = (ln % kXUnits) ^ (kXUnits == 8 ? (R & 7) : ((R >> 2) & 3));
       const int gr = min(m0 + R, rows - 1);
       lds_dma16(Xb, (unsigned)gr * xrow_b + 2u * (unsigned)(k0 + 8 * u), lds_addr(sm.x[bf] + R0 * kGK));
     }
 #pragma unroll
-    for (int t = 0; t < 4; ++t) {  // W: wave w fills rows 16w .. 16w+15, 4 rows per load
-      const int R0 = 16 * w + 4 * t, R = R0 + (ln >> 4);
+    for (int t = 0; t < kGK / 16; ++t) {  // W: wave w fills rows kGK/4 w .., 4 rows per load
+      const int R0 = (kGK / 4) * w + 4 * t, R = R0 + (ln >> 4);
       const int u = (ln & 15) ^ (2 * (R & 7));
       lds_dma16(W, (unsigned)(k0 + gw_krow(R)) * wrow_b + 2u * (unsigned)(n0 + 8 * u), lds_addr(sm.w[bf] + R0 * kBN));
     }
@@ -253,16 +273,30 @@ __global__ __launch_bounds__(256) void k_gemm_v2(const __bf16* __restrict__ X, c
 #pragma unroll
     for (int jn = 0; jn < 4; ++jn) acc[i][jn] = f32x4{0.f, 0.f, 0.f, 0.f};
   const int per = nk / sp.S, s0 = ks * per, s1 = s0 + per;  // this block's stages
-  issue(s0 * kGK, 0);
-  wait_dma();
-  __syncthreads();
+  // stages s0 .. s0 + kNBuf - 2 in flight; stage s + kNBuf - 1 is issued into
+  // the buffer read in stage s - 1 once the barrier of stage s has passed
+#pragma unroll
+  for (int p = 0; p < kNBuf - 1; ++p)
+    if (s0 + p < s1) issue((s0 + p) * kGK, p);
   for (int s = s0; s < s1; ++s) {
-    const int bf = (s - s0) & 1;
-    if (s + 1 < s1) issue((s + 1) * kGK, bf ^ 1);
+    const int later = min(s1 - 1 - s, kNBuf - 2);  // stages issued after s, still in flight
+    if constexpr (kNBuf >= 4) {
+      if (later >= 2) wait_vm<2 * kDmaPerStage>();
+      else if (later == 1) wait_vm<kDmaPerStage>();
+      else wait_vm<0>();
+    } else if constexpr (kNBuf == 3) {
+      if (later >= 1) wait_vm<kDmaPerStage>();
+      else wait_vm<0>();
+    } else {
+      wait_vm<0>();
+    }
+    __syncthreads();
+    if (s + kNBuf - 1 < s1) issue((s + kNBuf - 1) * kGK, (s - s0 + kNBuf - 1) % kNBuf);
+    const int bf = (s - s0) % kNBuf;
     const __bf16* sx = sm.x[bf];
     const __bf16* sw = sm.w[bf];
 #pragma unroll
-    for (int kc = 0; kc < 2; ++kc) {
+    for (int kc = 0; kc < kGK / 32; ++kc) {
       bf16x8 af[4], bfr[4];
 #pragma unroll
       for (int i = 0; i < 4; ++i) af[i] = *reinterpret_cast<const bf16x8*>(sx + gx_off(wm + 16 * i + lr, 4 * kc + g));
@@ -280,8 +314,6 @@ __global__ __launch_bounds__(256) void k_gemm_v2(const __bf16* __restrict__ X, c
         for (int jn = 0; jn < 4; ++jn)
           acc[i][jn] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(af[i], bfr[jn], acc[i][jn], 0, 0, 0);
     }
-    if (s + 1 < s1) wait_dma();
-    __syncthreads();
   }
   // result (row wm + 16i + 4g + e, col wn + 16jn + lr); split: partial ks of
   // element (128 tile + m - m0, col) at part[((128 tile + m - m0) N + col) S + ks]
