@@ -268,6 +268,7 @@ sc_status prune_compact(const sc_attn_desc* d, const float* scores, float thresh
   p.orig_in = orig_idx_in;
   p.orig_out = orig_idx_out;
   p.new_index = static_cast<int*>(workspace);
+  p.len_copy = nullptr;
   hipStream_t s = static_cast<hipStream_t>(stream);
   if (sc::launch_prune(p, s) != hipSuccess) return SC_EHIP;
   ga.keep_idx = keep_idx;
@@ -555,6 +556,7 @@ sc_status run_stack(const sc_attn_desc* d, int32_t n_layers, const int32_t* wind
     p.orig_in = orig_cur;
     p.orig_out = orig_nxt;
     p.new_index = w.new_index;
+    p.len_copy = kept_per_layer ? kept_per_layer + (size_t)l * B : nullptr;
     chk(sc::launch_prune(p, s));
     sc::GatherArgs ga;
     std::memset(&ga, 0, sizeof(ga));
@@ -580,7 +582,6 @@ sc_status run_stack(const sc_attn_desc* d, int32_t n_layers, const int32_t* wind
       chk(sc::launch_gemm_bf16(w.h, W2[l], w.t, sc::kGemmF32, B, n, F, Di, len_nxt, w.split, s));
       chk(sc::launch_residual_layernorm(w.x1, w.t, nxt, B, n, Di, ln_eps, len_nxt, w.split, F, s));
     }
-    if (kept_per_layer) chk(sc::launch_record_len(len_nxt, kept_per_layer + (size_t)l * B, B, s));
     cur = nxt;
     int* tmp;
     tmp = len_cur; len_cur = len_nxt; len_nxt = tmp;

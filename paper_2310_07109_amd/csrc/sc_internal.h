@@ -77,6 +77,7 @@ struct PruneArgs {
   const int* orig_in;      // [B, n] or null
   int* orig_out;           // [B, n] or null
   int* new_index;          // workspace [B, n]
+  int* len_copy;           // [B] or null: a second copy of new_len (e.g. a per-layer record)
 };
 hipError_t launch_prune(const PruneArgs& p, hipStream_t s);
 
@@ -145,6 +146,5 @@ hipError_t launch_residual_layernorm(const void* x_res, const float* t, void* y,
 hipError_t launch_fill_zero(void* p, size_t bytes, hipStream_t s);
 hipError_t launch_copy_i32(const int* src, int* dst, long long count, hipStream_t s);
 hipError_t launch_iota_orig(const int* valid_len, int* orig, int B, int n, hipStream_t s);
-hipError_t launch_record_len(const int* len, int* dst, int B, hipStream_t s);
 
 }  // namespace sc

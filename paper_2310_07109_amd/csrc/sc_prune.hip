@@ -185,7 +185,10 @@ __global__ __launch_bounds__(kScanThreads) void k_prune_scan(PruneArgs p) {
     if (k < n) nidx[k] = keep ? pos : -1;
     carry += total;
   }
-  if (tid == 0) p.new_len[b] = carry;
+  if (tid == 0) {
+    p.new_len[b] = carry;
+    if (p.len_copy) p.len_copy[b] = carry;
+  }
   for (int j = carry + tid; j < n; j += kScanThreads) {
     kidx[j] = -1;
     if (oout) oout[j] = -1;

@@ -425,11 +425,6 @@ __global__ __launch_bounds__(256, kMaxPer <= 16 ? 6 : 4) void k_residual_ln(cons
   }
 }
 
-__global__ void k_record_len(const int* len, int* dst, int B) {
-  const int i = blockIdx.x * blockDim.x + threadIdx.x;
-  if (i < B) dst[i] = len[i];
-}
-
 }  // namespace
 
 namespace {
@@ -464,11 +459,6 @@ hipError_t launch_residual_layernorm(const void* x_res, const float* t, void* y,
   auto* kern = D <= 1024 ? k_residual_ln<16> : k_residual_ln<32>;  // D <= 2048 (checked by the caller)
   hipLaunchKernelGGL(kern, dim3((unsigned)((rows + 3) / 4)), dim3(256), 0, s, static_cast<const __bf16*>(x_res), t,
                      static_cast<__bf16*>(y), B, n, D, eps, len, part, K);
-  return hipGetLastError();
-}
-
-hipError_t launch_record_len(const int* len, int* dst, int B, hipStream_t s) {
-  hipLaunchKernelGGL(k_record_len, dim3((B + 255) / 256), dim3(256), 0, s, len, dst, B);
   return hipGetLastError();
 }
 
