@@ -194,14 +194,15 @@ def test_full_encoder_config_sampled_sequences():
 
 
 def test_split_reduction_full_layers():
-    """RoBERTa-base widths (D 768, FFN 3072) on few short sequences: the surviving rows fill at most nine
+    """RoBERTa-base widths (D 768, FFN 3072) on few short sequences: the surviving rows fill at most seven
     128-row tiles, so the output and second feed-forward products split their 768- and 3072-long reductions
     into float32 slabs that the residual LayerNorm adds in a fixed order.  Layer by layer against the oracle,
     and the two-layer call equals the chain of single-layer calls bit for bit (the split is deterministic)."""
-    cfg = si.StackConfig("split full", 25, 3, 300, 12, 64, 2, 64, (120, 300), 1, 0.02, 0.004, ffn_dim=3072,
+    cfg = si.StackConfig("split full", 25, 4, 300, 12, 64, 2, 64, (120, 300), 1, 0.02, 0.004, ffn_dim=3072,
                          windows=(32, 96))
     inp = si.make_stack_inputs(cfg)
     inp["valid_len"][1] = 7
+    inp["valid_len"][2] = 0  # an empty sequence between live ones: no tiles, the plan's offsets skip it
     inp["global_pos"] = si.global_positions(cfg.seed, inp["valid_len"], 1, "first")
     thetas = [0.0, 0.004]
     xl, vl_final = layerwise(inp["x"], inp["wqkv"], inp["wo"], inp["valid_len"], inp["global_pos"], cfg.H,
