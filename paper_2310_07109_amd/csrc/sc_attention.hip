@@ -361,12 +361,13 @@ SC_DEV void window_fwd_block(const AttnArgs& a, int blk, Smem<DT>& sm, uint32_t*
   float* lseg = a.lse ? a.lse + (long long)wb.bh * n : nullptr;
   float* l2g = a.win_lse2 ? a.win_lse2 + (long long)wb.bh * n : nullptr;
 
-  if (q0 >= L) {  // padding block: zero output rows
+  if (q0 >= L) {  // padding block: zero output rows (unless the caller never reads them)
     constexpr int kEpc = 16 / sizeof(T), kCpr = kHeadDim / kEpc;
-    for (int c = tid; c < kBQ * kCpr; c += kThreads) {
-      const int q = q0 + c / kCpr;
-      if (q < n) zero16(Og + (long long)q * a.ld_out + (c % kCpr) * kEpc);
-    }
+    if (!a.skip_pad_out)
+      for (int c = tid; c < kBQ * kCpr; c += kThreads) {
+        const int q = q0 + c / kCpr;
+        if (q < n) zero16(Og + (long long)q * a.ld_out + (c % kCpr) * kEpc);
+      }
     for (int i = tid; i < kBQ; i += kThreads)
       if (q0 + i < n) {
         if (lseg) lseg[q0 + i] = -INFINITY;
@@ -777,11 +778,12 @@ SC_DEV void window_fwd_v2(const AttnArgs& a, int blk, Smem<1>& sm, uint32_t* sDy
   float* lseg = a.lse ? a.lse + (long long)wb.bh * n : nullptr;
   float* l2g = a.win_lse2 ? a.win_lse2 + (long long)wb.bh * n : nullptr;
 
-  if (q0 >= L) {  // padding block: zero output rows
-    for (int c = tid; c < kBQ2 * 8; c += kThreads) {
-      const int q = q0 + (c >> 3);
-      if (q < n) zero16(Og + (long long)q * a.ld_out + 8 * (c & 7));
-    }
+  if (q0 >= L) {  // padding block: zero output rows (unless the caller never reads them)
+    if (!a.skip_pad_out)
+      for (int c = tid; c < kBQ2 * 8; c += kThreads) {
+        const int q = q0 + (c >> 3);
+        if (q < n) zero16(Og + (long long)q * a.ld_out + 8 * (c & 7));
+      }
     for (int i = tid; i < kBQ2; i += kThreads)
       if (q0 + i < n) {
         if (lseg) lseg[q0 + i] = -INFINITY;
