@@ -217,3 +217,9 @@ def test_split_reduction_full_layers():
     assert np.array_equal(fl, vl_final)
     for b in range(cfg.B):
         assert torch.equal(y[b, :fl[b]].view(torch.int16), xl[b, :fl[b]].view(torch.int16))
+    # run to run: the partial sums are added in a fixed order
+    y2, fl2, orig2, kpl2 = sc.sc_encoder_stack(d, bf16_dev(inp["x"]), dv(inp["wqkv"]), dv(inp["wo"]),
+                                               dv(inp["w1"]), dv(inp["w2"]), thetas, windows=inp["windows"])
+    assert np.array_equal(fl2.cpu().numpy(), fl) and torch.equal(orig2, orig) and torch.equal(kpl2, kpl)
+    for b in range(cfg.B):
+        assert torch.equal(y2[b, :fl[b]].view(torch.int16), y[b, :fl[b]].view(torch.int16))
