@@ -316,9 +316,9 @@ __global__ __launch_bounds__(256) void k_gemm_v2(const __bf16* __restrict__ X, c
     }
   }
   // result (row wm + 16i + 4g + e, col wn + 16jn + lr); split: partial ks of
-  // element (128 tile + m - m0, col) at part[((128 tile + m - m0) N + col) S + ks]
+  // element (128 tile + m - m0, col) at part[(128 (ks tiles + tile) + m - m0) N + col]
   if (sp.S > 1) {
-    float* slab = part + ((long long)(tile * kBM - m0) * N) * sp.S + ks;
+    float* slab = part + ((long long)(ks * sp.tiles + tile) * kBM - m0) * N;
 #pragma unroll
     for (int i = 0; i < 4; ++i)
 #pragma unroll
@@ -326,7 +326,7 @@ __global__ __launch_bounds__(256) void k_gemm_v2(const __bf16* __restrict__ X, c
         const int m = m0 + wm + 16 * i + 4 * g + e;
         if (m >= rows) continue;
 #pragma unroll
-        for (int jn = 0; jn < 4; ++jn) slab[((long long)m * N + n0 + wn + 16 * jn + lr) * sp.S] = acc[i][jn][e];
+        for (int jn = 0; jn < 4; ++jn) slab[(long long)m * N + n0 + wn + 16 * jn + lr] = acc[i][jn][e];
       }
     return;
   }
@@ -342,32 +342,33 @@ __global__ __launch_bounds__(256) void k_gemm_v2(const __bf16* __restrict__ X, c
     }
 }
 
-// Element c of a row's S partial sums (consecutive floats), added in order.
-template <int S>
-SC_DEV float slab_sum(const float* p) {
-  if constexpr (S == 1) {
-    return *p;
-  } else if constexpr (S == 2) {
-    const float2 a = *reinterpret_cast<const float2*>(p);
-    return a.x + a.y;
-  } else {
-    const float4 a = *reinterpret_cast<const float4*>(p);
-    float r = ((a.x + a.y) + a.z) + a.w;
-    if constexpr (S == 8) {
-      const float4 c = *reinterpret_cast<const float4*>(p + 4);
-      r = (((r + c.x) + c.y) + c.z) + c.w;
-    }
-    return r;
-  }
-}
-
-// v[u] = x[c] + t[c] for c = lane + 64 u, t from the row's partial sums.
+// v[4u + q] = x[c + q] + t[c + q] for the columns c = 4 lane + 256 u .. +3
+// (D a multiple of 64), t being the sum of S partial sums that lie `stride`
+// floats apart, added in the order s = 0 .. S-1; 16-byte loads of t.
 template <int S, int kPer>
-SC_DEV void ln_load(float (&v)[kPer], const __bf16* xp, const float* tp, int D, int lane) {
+SC_DEV void ln_load(float (&v)[kPer], const __bf16* xp, const float* tp, long long stride, int D, int lane) {
 #pragma unroll
-  for (int u = 0; u < kPer; ++u) {
-    const int c = lane + 64 * u;
-    v[u] = c < D ? slab_sum<S>(tp + (long long)c * S) + (float)xp[c] : 0.f;
+  for (int u = 0; u < kPer / 4; ++u) {
+    const int c = 4 * lane + 256 * u;
+    if (c < D) {
+      float4 a = *reinterpret_cast<const float4*>(tp + c);
+#pragma unroll
+      for (int k = 1; k < S; ++k) {
+        const float4 e = *reinterpret_cast<const float4*>(tp + k * stride + c);
+        a.x += e.x;
+        a.y += e.y;
+        a.z += e.z;
+        a.w += e.w;
+      }
+      const bf16x4 xv = *reinterpret_cast<const bf16x4*>(xp + c);
+      v[4 * u] = a.x + (float)xv[0];
+      v[4 * u + 1] = a.y + (float)xv[1];
+      v[4 * u + 2] = a.z + (float)xv[2];
+      v[4 * u + 3] = a.w + (float)xv[3];
+    } else {
+#pragma unroll
+      for (int q = 0; q < 4; ++q) v[4 * u + q] = 0.f;
+    }
   }
 }
 
@@ -391,18 +392,19 @@ __global__ __launch_bounds__(256, kMaxPer <= 16 ? 6 : 4) void k_residual_ln(cons
   __bf16* yp = y + row * D;
   float v[kMaxPer];
   // loaded as written by an unsplit product before the plan is known (replaced after a split)
-  ln_load<1, kMaxPer>(v, xp, t + row * D, D, lane);
+  ln_load<1, kMaxPer>(v, xp, t + row * D, 0, D, lane);
   int excl = 0, incl = 0;
   const SplitPlan sp = part ? split_plan(len, B, n, D / kBN, K / kGK, excl, incl) : SplitPlan{0, 1};
   if (sp.S > 1) {  // the row's place: its tile among the live tiles, then its row in the tile
     const int tile = j / kBM + __shfl(excl, b, 64);
-    const float* tp = part + ((long long)tile * kBM + j % kBM) * D * sp.S;
+    const float* tp = part + ((long long)tile * kBM + j % kBM) * D;
+    const long long stride = (long long)sp.tiles * kBM * D;  // between the partial sums
     if (sp.S == 2)
-      ln_load<2, kMaxPer>(v, xp, tp, D, lane);
+      ln_load<2, kMaxPer>(v, xp, tp, stride, D, lane);
     else if (sp.S == 4)
-      ln_load<4, kMaxPer>(v, xp, tp, D, lane);
+      ln_load<4, kMaxPer>(v, xp, tp, stride, D, lane);
     else
-      ln_load<8, kMaxPer>(v, xp, tp, D, lane);
+      ln_load<8, kMaxPer>(v, xp, tp, stride, D, lane);
   }
   float s = 0.f;
 #pragma unroll
@@ -412,16 +414,21 @@ __global__ __launch_bounds__(256, kMaxPer <= 16 ? 6 : 4) void k_residual_ln(cons
   float q = 0.f;
 #pragma unroll
   for (int u = 0; u < kMaxPer; ++u) {
-    const int c = lane + 64 * u;
+    const int c = 4 * lane + 256 * (u / 4);
     const float dv = c < D ? v[u] - mean : 0.f;
     q += dv * dv;
   }
   for (int m = 1; m < 64; m <<= 1) q += __shfl_xor(q, m, 64);
   const float inv = 1.0f / sqrtf(q / (float)D + eps);
 #pragma unroll
-  for (int u = 0; u < kMaxPer; ++u) {
-    const int c = lane + 64 * u;
-    if (c < D) yp[c] = (__bf16)((v[u] - mean) * inv);
+  for (int u = 0; u < kMaxPer / 4; ++u) {
+    const int c = 4 * lane + 256 * u;
+    if (c < D) {
+      bf16x4 o;
+#pragma unroll
+      for (int q4 = 0; q4 < 4; ++q4) o[q4] = (__bf16)((v[4 * u + q4] - mean) * inv);
+      *reinterpret_cast<bf16x4*>(yp + c) = o;
+    }
   }
 }
 
