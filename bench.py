@@ -10,7 +10,17 @@ global tokens at seeded positions, valid lengths uniform in [2048, 4096],
 threshold pruning about half of the valid tokens.
 
 Prints one JSON line.  `value` is kept-token-layers per second (valid tokens
-entering the layer, per second of wall time on the GPU stream).
+entering the layer, per second of GPU-stream time), from the median of the
+per-step event pairs of the timed steps.
+
+Roofline (the workload's dominant kernel, k_attn_fwd: softmax and P.V of the
+window attention): its algorithmic flops (Q.K^T and P.V once per allowed
+(query, key) pair and head, 4 x 64 flop) over its average launch time, measured
+live with hipEvents on the launch stream, against the bf16 MFMA peak; the HBM
+fraction of its algorithmic bytes alongside.  The same figures for both
+window-attention launches, the HBM fractions of the score reduction and of the
+prune + compaction kernels, and the VALU fraction (issue slots per pair) are
+extra fields.
 """
 import argparse
 import hashlib
@@ -36,6 +46,7 @@ MFMA_PEAK_TFLOPS = {"bf16": 2500.0, "f32": 157.3}
 KERNEL_SOURCES = ("paper_2310_07109_amd/csrc/sc_attention.hip", "paper_2310_07109_amd/csrc/sc_device.h",
                   "paper_2310_07109_amd/csrc/sc_internal.h")
 TRAFFIC_FILE = os.path.join(ROOT, "profiles", "window_attention_seq4096_traffic.json")
+DOMINANT = "k_attn_fwd<1>"
 
 
 # name -> (input config, workload description)
@@ -48,9 +59,18 @@ WORKLOADS = {
     "soft": ("soft", "training step of one LTP soft-pruned layer (Sec. 4.2.2 step 1): B8 n4096 H12 d64 bf16, "
                      "window 512, 32 seeded global tokens, valid lengths U[2048,4096]; forward (attention, scores, "
                      "soft mask) and backward to Q, K, V and the threshold, upstream gradients N(0,1)"),
-    "encoder": (None, "12-layer RoBERTa-base-shaped SparseCoder encoder: B16 n2048 D768 (12 heads x 64), GELU "
-                      "feed-forward 3072, windows 64,64,128,128,256,256,512x6, global token 0, valid lengths "
-                      "U[256,2048], thresholds 0.01*l/11, pruning after every layer"),
+    "encoder": ("encoder", "12-layer RoBERTa-base-shaped SparseCoder encoder: B16 n2048 D768 (12 heads x 64), "
+                           "GELU feed-forward 3072, windows 64,64,128,128,256,256,512x6, global token 0, valid "
+                           "lengths U[256,2048], thresholds 0.01*l/11, pruning after every layer"),
+    "stack": ("stack", "12-layer attention-only encoder stack with RoBERTa-base shapes: B16 n2048 D768 (12 heads x "
+                       "64), Wqkv 768x2304 and Wo 768x768 ~ N(0,0.02^2), residual + LayerNorm, no feed-forward, "
+                       "window 512, global token 0, valid lengths U[256,2048], thresholds 0.01*l/11 (l = 0..11), "
+                       "pruning after every layer"),
+    "passes": (5, "three successive prune passes: B2 n8192 H16 d64 bf16, window 1024, 64 seeded global tokens, "
+                  "full length, rank-4 amplitude-3 spike on K, thresholds 0.0005 / 0.001 / 0.002, each pass on the "
+                  "previous pass's compacted Q, K, V"),
+    "passes5b": ("5b", "three successive prune passes as 'passes', with the rank-4 spike on Q as well as K "
+                       "(heavy-tailed scores)"),
 }
 
 
@@ -122,7 +142,7 @@ def measure_soft(args, sc, si, torch, np, dev="cuda:0"):
     theta, temp = float(np.median(vals)), max(float(np.std(vals)), 1e-6)
     ev = [torch.cuda.Event(enable_timing=True) for _ in range(2 * args.steps)]
 
-    def step(i=None):
+    def step(i):
         sc.sc_window_attention(d, q, k, v, out=out, lse=lse, score_partials=sp, workspace=ws_attn)
         sc.sc_ltp_score(d, sp, scores=scores)
         sc.sc_ltp_soft_mask(d, scores, theta, temp, out, mask=mask, y=y)
@@ -132,17 +152,9 @@ def measure_soft(args, sc, si, torch, np, dev="cuda:0"):
         if i is not None:
             ev[2 * i + 1].record()
 
-    for _ in range(args.warmup):
-        step()
-    torch.cuda.synchronize()
-    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-    e0.record()
-    for i in range(args.steps):
-        step(i)
-    e1.record()
-    torch.cuda.synchronize()
-    ms = e0.elapsed_time(e1) / args.steps
-    bwd_ms = sum(ev[2 * i].elapsed_time(ev[2 * i + 1]) for i in range(args.steps)) / args.steps
+    per, mean_ms, wall_ms = timed(step, args.steps, args.warmup, torch)
+    ms = median(per)
+    bwd_ms = median([ev[2 * i].elapsed_time(ev[2 * i + 1]) for i in range(args.steps)])
     tokens = int(np.sum(inp["valid_len"]))
     pw, pg = algorithmic_counts(inp)
     pairs = H * (pw + pg)
@@ -166,29 +178,31 @@ def measure_soft(args, sc, si, torch, np, dev="cuda:0"):
     roof.update(floor_mfma_us=round(t_mfma * 1e6, 2), floor_hbm_us=round(t_hbm * 1e6, 2),
                 floor_alu_us=round(t_alu * 1e6, 2), traffic=None, kernel="sc_ltp_soft_backward (all its launches)",
                 kernel_us=round(bwd_ms * 1e3, 2), algorithmic_flop=flops, algorithmic_bytes=bytes_)
-    res = dict(ms=ms, bwd_ms=bwd_ms, tokens=tokens, theta=theta, temp=temp, roof=roof, gen_s=gen_s,
-               dtheta=float(grads[3].item()))
+    res = dict(ms=ms, mean_ms=mean_ms, wall_ms=wall_ms, bwd_ms=bwd_ms, tokens=tokens, theta=theta, temp=temp,
+               roof=roof, gen_s=gen_s, dtheta=float(grads[3].item()))
     if not args.no_cpu_baseline:
         import oracle
-        threads = oracle.default_threads()
-        c0 = time.perf_counter()
-        rows = [0]
-        sel = [inp[x][rows] for x in ("q64", "k64", "v64")]
-        vl, gp = inp["valid_len"][rows], inp["global_pos"][rows]
-        oracle.soft_prune_forward(*sel, vl, gp, cfg.window, cfg.alpha, theta, temp, 1, nthreads=threads)
-        oracle.soft_prune_backward(*sel, vl, gp, cfg.window, cfg.alpha, theta, temp, dy64[rows],
-                                   dm[rows].astype(np.float64), 1, nthreads=threads)
-        cpu_s = time.perf_counter() - c0
-        res["cpu_baseline"] = {"value": round(int(vl.sum()) / cpu_s, 1), "unit": "token-layers/s (training step)",
-                               "cores": threads, "kind": "oracle",
-                               "sample": f"sequence 0 of the workload ({int(vl.sum())} tokens): soft-pruned "
-                                         f"forward and backward in double precision, {cpu_s:.2f} s"}
+
+        def run(rows, threads):
+            sel = [inp[x][rows] for x in ("q64", "k64", "v64")]
+            vl, gp = inp["valid_len"][rows], inp["global_pos"][rows]
+            oracle.soft_prune_forward(*sel, vl, gp, cfg.window, cfg.alpha, theta, temp, 1, nthreads=threads)
+            oracle.soft_prune_backward(*sel, vl, gp, cfg.window, cfg.alpha, theta, temp, dy64[rows],
+                                       dm[rows].astype(np.float64), 1, nthreads=threads)
+
+        n0 = int(inp["valid_len"][0])
+        res["cpu_baseline"] = cpu_baseline(lambda t: run([0], t), n0, lambda t: run([0], t), n0,
+                                           "token-layers/s (training step)",
+                                           f"sequence 0 of the workload ({n0} tokens): soft-pruned forward and "
+                                           "backward in double precision",
+                                           f"the same sequence")
     return res
 
 
-def measure_encoder(args, sc, si, torch, np, dev="cuda:0"):
-    """Times the full encoder stack (sc_encoder_stack over 12 layers)."""
-    cfg = si.STACK_FULL_CONFIG
+def measure_stack(args, sc, si, torch, np, full, dev="cuda:0"):
+    """Times the 12-layer stack: sc_encoder_stack (full layers with the feed-forward block) or
+    sc_encoder_attn_stack (attention-only layers)."""
+    cfg = si.STACK_FULL_CONFIG if full else si.STACK_CONFIG
     t0 = time.time()
     inp = si.make_stack_inputs(cfg)
     gen_s = time.time() - t0
@@ -201,43 +215,94 @@ def measure_encoder(args, sc, si, torch, np, dev="cuda:0"):
 
     d = sc.Desc(cfg.B, cfg.n, cfg.H, cfg.window, i32(inp["valid_len"]), i32(inp["global_pos"]), cfg.alpha, sc.SC_BF16)
     x = bf(inp["x"])
-    wq, wo, w1, w2 = ([bf(w) for w in inp[k]] for k in ("wqkv", "wo", "w1", "w2"))
+    wq, wo = ([bf(w) for w in inp[k]] for k in ("wqkv", "wo"))
     th = cfg.thresholds()
-    ws = torch.empty(sc.sc_encoder_stack_workspace_size(d, cfg.n_layers, cfg.ffn_dim), dtype=torch.uint8, device=dev)
     x_out = torch.empty_like(x)
+    if full:
+        w1, w2 = ([bf(w) for w in inp[k]] for k in ("w1", "w2"))
+        ws = torch.empty(sc.sc_encoder_stack_workspace_size(d, cfg.n_layers, cfg.ffn_dim), dtype=torch.uint8,
+                         device=dev)
+        windows = list(inp["windows"])
+    else:
+        ws = torch.empty(sc.sc_encoder_attn_stack_workspace_size(d, cfg.n_layers), dtype=torch.uint8, device=dev)
+        windows = [cfg.window] * cfg.n_layers
+    res = {}
 
-    def step():
-        return sc.sc_encoder_stack(d, x, wq, wo, w1, w2, th, windows=inp["windows"], x_out=x_out, workspace=ws)
+    def step(i):
+        if full:
+            res["r"] = sc.sc_encoder_stack(d, x, wq, wo, w1, w2, th, windows=windows, x_out=x_out, workspace=ws)
+        else:
+            res["r"] = sc.sc_encoder_attn_stack(d, x, wq, wo, th, x_out=x_out, workspace=ws)
 
-    for _ in range(args.warmup):
-        step()
-    torch.cuda.synchronize()
-    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-    e0.record()
-    for _ in range(args.steps):
-        res = step()
-    e1.record()
-    torch.cuda.synchronize()
-    ms = e0.elapsed_time(e1) / args.steps
-    kpl = res[3].cpu().numpy()
+    per, mean_ms, wall_ms = timed(step, args.steps, args.warmup, torch)
+    # the per-layer attention times, in a second run of the same steps
+    sc.sc_profile_window_kernel(True)
+    timed(step, args.steps, 0, torch)
+    fwd, cols = sc.sc_profile_window_kernel_read()
+    sc.sc_profile_window_kernel(False)
+    L = cfg.n_layers
+    ms = median(per)
+    kpl = res["r"][3].cpu().numpy()
     # per-layer input lengths and global positions (token 0 is global and always kept, so it stays at 0)
-    lens_in = [inp["valid_len"].astype(np.int64)] + [kpl[l].astype(np.int64) for l in range(cfg.n_layers - 1)]
+    lens_in = [inp["valid_len"].astype(np.int64)] + [kpl[l].astype(np.int64) for l in range(L - 1)]
     tokens = int(sum(int(np.sum(li)) for li in lens_in))
     D, F = cfg.H * cfg.d, cfg.ffn_dim
     parts = dict(projection=0.0, attention=0.0, ffn=0.0, other=0.0)
-    for l in range(cfg.n_layers):
+    layers = []
+    for l in range(L):
         li = lens_in[l]
         gp = np.where(li[:, None] > 0, 0, -1).astype(np.int32)
-        f = model_flops(li, kpl[l], pairs_of(li, gp, inp["windows"][l]), D, cfg.H, cfg.d, F)
+        pairs = pairs_of(li, gp, windows[l])
+        f = model_flops(li, kpl[l], pairs, D, cfg.H, cfg.d, F)
         for k in parts:
             parts[k] += f[k]
+        layers.append(dict(tokens_in=int(np.sum(li)), kept=int(np.sum(kpl[l])), window=windows[l],
+                           attn_fwd_us=round(median(fwd[l::L]) * 1e3, 2), attn_cols_us=round(median(cols[l::L]) * 1e3, 2)))
     total = sum(parts.values())
     achieved = total / (ms * 1e-3) / 1e12
-    return dict(ms=ms, tokens=tokens, kept_per_layer=[int(np.sum(k)) for k in kpl], gen_s=gen_s,
-                gflops={k: round(v / 1e9, 2) for k, v in parts.items()}, total_gflops=round(total / 1e9, 2),
-                roof=dict(bound="mfma", achieved=round(achieved, 2), peak=MFMA_PEAK_TFLOPS["bf16"], unit="TFLOP/s",
-                          frac=round(achieved / MFMA_PEAK_TFLOPS["bf16"], 4), traffic=None,
-                          kernel="whole encoder step (model FLOPs as counted by model_flops)"))
+    # layer 0's window attention against its own floors
+    f0, b0 = attention_work(int(np.sum(lens_in[0])), cfg.H, cfg.d,
+                            cfg.H * pairs_of(lens_in[0], np.where(lens_in[0][:, None] > 0, 0, -1).astype(np.int32),
+                                             windows[0]))
+    t0_fwd = median(fwd[0::L])
+    roof = dict(bound="mfma", achieved=round(achieved, 2), peak=MFMA_PEAK_TFLOPS["bf16"], unit="TFLOP/s",
+                frac=round(achieved / MFMA_PEAK_TFLOPS["bf16"], 4), traffic=None,
+                kernel="whole stack step (model FLOPs as counted by model_flops)",
+                layer0_attention=dict(kernel="k_attn_fwd<bf16> of layer 0", us=round(t0_fwd * 1e3, 2),
+                                      mfma_frac=round(f0 / (t0_fwd * 1e-3) / 1e12 / MFMA_PEAK_TFLOPS["bf16"], 4),
+                                      hbm_frac=round(b0 / (t0_fwd * 1e-3) / 1e9 / HBM_PEAK_GBS, 4),
+                                      floor_mfma_us=round(f0 / (MFMA_PEAK_TFLOPS["bf16"] * 1e12) * 1e6, 2),
+                                      floor_hbm_us=round(b0 / (HBM_PEAK_GBS * 1e9) * 1e6, 2)))
+    t_in0 = float(np.sum(lens_in[0]))
+    gemm0 = 2 * t_in0 * D * 3 * D + 2 * float(np.sum(kpl[0])) * D * D
+    roof["layer0_gemm_floor_us"] = round(gemm0 / (MFMA_PEAK_TFLOPS["bf16"] * 1e12) * 1e6, 2)
+    out = dict(ms=ms, mean_ms=mean_ms, wall_ms=wall_ms, tokens=tokens, kept_per_layer=[int(np.sum(k)) for k in kpl],
+               gen_s=gen_s, gflops={k: round(v / 1e9, 2) for k, v in parts.items()},
+               total_gflops=round(total / 1e9, 2), roof=roof, layers=layers)
+    if not args.no_cpu_baseline:
+        import oracle
+        ffn = dict(w1_list=inp["w1_64"], w2_list=inp["w2_64"]) if full else {}
+        win_arg = list(inp["windows"]) if full else cfg.window
+
+        def run_all(threads):
+            oracle.encoder_stack(inp["x64"], inp["wqkv64"], inp["wo64"], inp["valid_len"], inp["global_pos"], cfg.H,
+                                 win_arg, cfg.alpha, th, nthreads=threads, **ffn)
+
+        one = [int(np.argmin(inp["valid_len"]))]
+
+        def run_one(threads):
+            oracle.encoder_stack(inp["x64"][one], inp["wqkv64"], inp["wo64"], inp["valid_len"][one],
+                                 inp["global_pos"][one], cfg.H, win_arg, cfg.alpha, th, nthreads=threads, **ffn)
+
+        units_one = None
+        _, _, _, k1 = oracle.encoder_stack(inp["x64"][one], inp["wqkv64"], inp["wo64"], inp["valid_len"][one],
+                                           inp["global_pos"][one], cfg.H, win_arg, cfg.alpha, th, **ffn)
+        units_one = int(inp["valid_len"][one].sum()) + int(np.sum(k1[:-1]))
+        out["cpu_baseline"] = cpu_baseline(run_all, tokens, run_one, units_one, "kept-token-layers/s",
+                                           f"the whole workload ({cfg.B} sequences, {L} layers) in double precision",
+                                           f"the shortest sequence ({int(inp['valid_len'][one].sum())} tokens), "
+                                           f"{L} layers")
+    return out
 
 
 def kernel_source_hash():
@@ -248,8 +313,8 @@ def kernel_source_hash():
     return h.hexdigest()[:16]
 
 
-def recorded_traffic():
-    """HBM bytes per call of the two window-attention launches, from the committed counter
+def recorded_traffic(kernel=DOMINANT):
+    """Calibrated HBM bytes (FETCH_SIZE + WRITE_SIZE) per launch of `kernel`, from the committed counter
     measurement, if it was taken on the current kernel sources (else None)."""
     try:
         with open(TRAFFIC_FILE) as f:
@@ -258,7 +323,12 @@ def recorded_traffic():
         return None
     if rec.get("source_hash") != kernel_source_hash():
         return None
-    return rec.get("bytes_per_call")
+    c, cal = rec["counters_kib_per_dispatch"], rec["calibration"]
+    try:
+        return int(round(1024 * (c["FETCH_SIZE"][kernel] * cal["fetch_scale"] +
+                                 c["WRITE_SIZE"][kernel] * cal["write_scale"])))
+    except KeyError:
+        return None
 
 
 def algorithmic_counts(inp, causal=False):
@@ -282,36 +352,110 @@ def algorithmic_counts(inp, causal=False):
     return pairs_window, pairs_global
 
 
-def roofline(flops, bytes_, kern_ms, pairs=None):
-    """Roofline of the two window-attention launches against the largest of the MFMA, HBM and VALU floors
-    (VALU: VALU_SLOTS_PER_PAIR issue slots per allowed pair and head, at VALU_PEAK_TOPS)."""
+def median(xs):
+    xs = sorted(xs)
+    k = len(xs)
+    return 0.0 if k == 0 else (xs[k // 2] if k % 2 else 0.5 * (xs[k // 2 - 1] + xs[k // 2]))
+
+
+def attention_work(tokens, H, d, pairs):
+    """Algorithmic work of one window-attention call (pairs: allowed (query, key) pairs summed over the heads):
+    flops of Q.K^T and P.V once per pair; bytes of reading Q, K, V and writing O (bf16) and the LSE (fp32) per
+    valid token and head."""
+    return 4.0 * d * pairs, tokens * H * (4 * d * 2 + 4)
+
+
+def roofline(flops, bytes_, fwd_ms, cols_ms, pairs, score=None, prune=None, traffic=None):
+    """Roofline of the dominant kernel (launch 1 of the window attention) against the bf16 MFMA peak, with its
+    HBM fraction; both launches against the MFMA, HBM and VALU floors; the score and prune + compaction kernels
+    against HBM.  score / prune: (kernel names, microseconds, algorithmic bytes)."""
     t_mfma = flops / (MFMA_PEAK_TFLOPS["bf16"] * 1e12)
     t_hbm = bytes_ / (HBM_PEAK_GBS * 1e9)
-    alu_ops = VALU_SLOTS_PER_PAIR * pairs if pairs is not None else 0.0
+    alu_ops = VALU_SLOTS_PER_PAIR * pairs
     t_alu = alu_ops / (VALU_PEAK_TOPS * 1e12)
-    if t_alu >= max(t_mfma, t_hbm):
-        achieved = alu_ops / (kern_ms * 1e-3) / 1e12
-        roof = dict(bound="alu", achieved=round(achieved, 3), peak=round(VALU_PEAK_TOPS, 2),
-                    unit="T VALU lane-op/s")
-    elif t_mfma >= t_hbm:
-        achieved = flops / (kern_ms * 1e-3) / 1e12
-        roof = dict(bound="mfma", achieved=round(achieved, 2), peak=MFMA_PEAK_TFLOPS["bf16"], unit="TFLOP/s")
-    else:
-        achieved = bytes_ / (kern_ms * 1e-3) / 1e9
-        roof = dict(bound="hbm", achieved=round(achieved, 1), peak=HBM_PEAK_GBS, unit="GB/s")
-    roof["frac"] = round(roof["achieved"] / roof["peak"], 4)
-    roof["floor_mfma_us"] = round(t_mfma * 1e6, 2)
-    roof["floor_hbm_us"] = round(t_hbm * 1e6, 2)
-    roof["floor_alu_us"] = round(t_alu * 1e6, 2)
-    roof["hbm_achieved_gbs"] = round(bytes_ / (kern_ms * 1e-3) / 1e9, 1)
+    achieved = flops / (fwd_ms * 1e-3) / 1e12
+    both = fwd_ms + cols_ms
+    roof = dict(bound="mfma", achieved=round(achieved, 2), peak=MFMA_PEAK_TFLOPS["bf16"], unit="TFLOP/s",
+                frac=round(achieved / MFMA_PEAK_TFLOPS["bf16"], 4), traffic=traffic,
+                kernel="k_attn_fwd<bf16> (launch 1 of the window attention: softmax and P.V)",
+                kernel_us=round(fwd_ms * 1e3, 2), algorithmic_flop=flops, algorithmic_bytes=bytes_,
+                hbm_achieved_gbs=round(bytes_ / (fwd_ms * 1e-3) / 1e9, 1),
+                hbm_frac=round(bytes_ / (fwd_ms * 1e-3) / 1e9 / HBM_PEAK_GBS, 4),
+                floors_us=dict(mfma=round(t_mfma * 1e6, 2), hbm=round(t_hbm * 1e6, 2), valu=round(t_alu * 1e6, 2)))
+    roof["window_attention_both_launches"] = dict(
+        kernels="k_attn_fwd<bf16> + k_attn_cols<bf16>", us=round(both * 1e3, 2), cols_us=round(cols_ms * 1e3, 2),
+        mfma_frac=round(t_mfma / (both * 1e-3), 4), hbm_frac=round(t_hbm / (both * 1e-3), 4),
+        valu_frac=round(t_alu / (both * 1e-3), 4), valu_achieved_tops=round(alu_ops / (both * 1e-3) / 1e12, 3),
+        valu_peak_tops=round(VALU_PEAK_TOPS, 2), valu_slots_per_pair=VALU_SLOTS_PER_PAIR)
+    for key, part in (("score", score), ("prune_compact", prune)):
+        if part is None:
+            continue
+        names, us, nbytes = part
+        gbs = nbytes / (us * 1e-6) / 1e9 if us > 0 else 0.0
+        roof[key] = dict(kernels=names, us=round(us, 2), algorithmic_bytes=int(nbytes), achieved_gbs=round(gbs, 1),
+                         hbm_frac=round(gbs / HBM_PEAK_GBS, 4))
     return roof
 
 
-def measure(sc, si, torch, np, inp, theta, steps, warmup, dev="cuda:0", keep_ratio=None, causal=False):
+def cpu_model():
+    try:
+        with open("/proc/cpuinfo") as f:
+            for line in f:
+                if line.startswith("model name"):
+                    return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return "unknown"
+
+
+def cpu_baseline(run_all, units_all, run_one, units_one, unit, sample_all, sample_one):
+    """The oracle on the host: the median of 3 runs of run_all() on every thread, then one run of run_one() on a
+    single thread.  units_*: the metric's units each run processes (token-layers)."""
+    import oracle
+    threads = oracle.default_threads()
+    times = []
+    for _ in range(3):
+        c0 = time.perf_counter()
+        run_all(threads)
+        times.append(time.perf_counter() - c0)
+    t_all = median(times)
+    c0 = time.perf_counter()
+    run_one(1)
+    t_one = time.perf_counter() - c0
+    return {"value": round(units_all / t_all, 1), "unit": unit, "cores": threads, "kind": "oracle",
+            "sample": f"{sample_all}; median of 3 runs on {threads} threads ({', '.join(f'{t:.2f}' for t in times)} "
+                      f"s)",
+            "single_thread": {"value": round(units_one / t_one, 1), "unit": unit, "cores": 1,
+                              "sample": f"{sample_one}, {t_one:.2f} s"},
+            "cpu_model": cpu_model(), "host_threads": os.cpu_count()}
+
+
+def timed(step, steps, warmup, torch):
+    """Runs `warmup` untimed steps, then `steps` timed ones bracketed by synchronisations, with an event on the
+    launch stream before every step and after the last.  step(i) gets the step index (None when untimed).
+    Returns (per-step milliseconds, mean milliseconds over the bracket, wall milliseconds per step)."""
+    for _ in range(warmup):
+        step(None)
+    torch.cuda.synchronize()
+    ev = [torch.cuda.Event(enable_timing=True) for _ in range(steps + 1)]
+    w0 = time.perf_counter()
+    for i in range(steps):
+        ev[i].record()
+        step(i)
+    ev[steps].record()
+    torch.cuda.synchronize()
+    wall = (time.perf_counter() - w0) * 1e3 / max(steps, 1)
+    per = [ev[i].elapsed_time(ev[i + 1]) for i in range(steps)]
+    return per, ev[0].elapsed_time(ev[steps]) / max(steps, 1), wall
+
+
+def measure(sc, si, torch, np, inp, theta, steps, warmup, dev="cuda:0", keep_ratio=None, causal=False,
+            band=False):
     """Times `steps` steps (window attention with score partials, scores, prune + compaction of O) after
     `warmup` untimed ones.  theta None picks the median score of the valid non-global tokens (about half
     pruned), from one untimed step.  keep_ratio: prune by the top-k rule (sc_topk_prune_compact) instead of
-    the threshold.  causal: the causal variant of the attention."""
+    the threshold.  causal: the causal variant of the attention.  band: the paper's score path (Sec. 5.5):
+    the window attention stores every probability in the band layout and the scores are summed from it."""
     B, n, H, dd, G = inp["B"], inp["n"], inp["H"], inp["d"], inp["G"]
 
     def i32(a):
@@ -326,6 +470,7 @@ def measure(sc, si, torch, np, inp, theta, steps, warmup, dev="cuda:0", keep_rat
     out = torch.empty_like(q)
     lse = torch.empty((B, H, n), dtype=torch.float32, device=dev)
     sp = torch.empty(sc.sc_score_partials_size(d) // 4, dtype=torch.float32, device=dev)
+    bp = torch.empty(sc.sc_band_probs_size(d) // 4, dtype=torch.float32, device=dev) if band else None
     ws_attn = torch.empty(max(sc.sc_window_attention_workspace_size(d), 1), dtype=torch.uint8, device=dev)
     scores = torch.empty((B, n), dtype=torch.float32, device=dev)
     oc = torch.empty_like(out)
@@ -344,41 +489,124 @@ def measure(sc, si, torch, np, inp, theta, steps, warmup, dev="cuda:0", keep_rat
             glob = {int(x) for x in inp["global_pos"][b] if 0 <= x < L}
             vals.extend(float(sv[b, t]) for t in range(L) if t not in glob)
         theta = float(np.median(vals)) if vals else 0.0
+    sev = [[torch.cuda.Event(enable_timing=True) for _ in range(3)] for _ in range(steps)]
+    marks = [False]
 
-    def step():
-        sc.sc_window_attention(d, q, k, v, out=out, lse=lse, score_partials=sp, workspace=ws_attn)
-        sc.sc_ltp_score(d, sp, scores=scores)
+    def step(i):
+        mark = marks[0] and i is not None
+        if band:
+            sc.sc_window_attention(d, q, k, v, out=out, lse=lse, score_partials=None, band_probs=bp,
+                                   workspace=ws_attn)
+        else:
+            sc.sc_window_attention(d, q, k, v, out=out, lse=lse, score_partials=sp, workspace=ws_attn)
+        if mark:
+            sev[i][0].record()
+        if band:
+            sc.sc_ltp_score(d, bp, mode=sc.SC_SCORE_FROM_BAND_PROBS, scores=scores)
+        else:
+            sc.sc_ltp_score(d, sp, scores=scores)
+        if mark:
+            sev[i][1].record()
         if keep_ratio is None:
             sc.sc_ltp_prune_compact(d, scores, theta, True, [out], dsts=[oc], outs=outs, workspace=ws_prune)
         else:
             sc.sc_topk_prune_compact(d, scores, keep_ratio, True, [out], dsts=[oc], outs=outs, workspace=ws_prune)
+        if mark:
+            sev[i][2].record()
 
-    for _ in range(warmup):
-        step()
-    torch.cuda.synchronize()
+    # the headline: steps bracketed by one event each
+    per, mean_ms, wall_ms = timed(step, steps, warmup, torch)
+    # the breakdown, in a second run of the same steps: the window attention's two launches (the library's
+    # events) and the score and prune + compaction calls (events between the calls)
     sc.sc_profile_window_kernel(True)
-    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-    w0 = time.perf_counter()
-    e0.record()
-    for _ in range(steps):
-        step()
-    e1.record()
-    torch.cuda.synchronize()
-    wall_ms = (time.perf_counter() - w0) * 1e3 / steps
-    ms = e0.elapsed_time(e1) / steps
-    kern_ms, launches = sc.sc_profile_window_kernel_read()
+    marks[0] = True
+    timed(step, steps, 0, torch)
+    fwd, cols = sc.sc_profile_window_kernel_read()
     sc.sc_profile_window_kernel(False)
-    kern_ms /= max(launches, 1)
+    score_us = median([sev[i][0].elapsed_time(sev[i][1]) for i in range(steps)]) * 1e3
+    prune_us = median([sev[i][1].elapsed_time(sev[i][2]) for i in range(steps)]) * 1e3
 
     tokens = int(np.sum(inp["valid_len"]))
+    kept = outs["new_len"].cpu().tolist()
     pairs_w, pairs_g = algorithmic_counts(inp, causal)
-    # algorithmic work of the two launches: Q.K^T and P.V once per allowed pair (the window rows and the
-    # global rows); read Q, K, V, write O (bf16), the LSE and the score partials (fp32)
-    flops = 4.0 * dd * H * (pairs_w + pairs_g)
-    bytes_ = tokens * H * (4 * dd * 2 + 4) + sp.numel() * 4
-    roof = roofline(flops, bytes_, kern_ms, pairs=H * (pairs_w + pairs_g))
-    return dict(ms=ms, wall_ms=wall_ms, kern_ms=kern_ms, tokens=tokens, kept=outs["new_len"].cpu().tolist(),
-                flops=flops, bytes=bytes_, roof=roof, theta=theta, pairs=H * (pairs_w + pairs_g))
+    pairs = H * (pairs_w + pairs_g)
+    flops, bytes_ = attention_work(tokens, H, dd, pairs)
+    # score reduction: read the partials, write the scores; prune + compaction: read the scores, write the kept
+    # indices, composed indices and lengths, read and write each kept row of O
+    score_bytes = sp.numel() * 4 + 4 * B * n
+    if band:  # the paper's layout: read each valid token's band and global-column entries and the global rows
+        r = inp["window"] // 2
+        g_used = sum(len([p for p in inp["global_pos"][b] if 0 <= p < inp["valid_len"][b]]) for b in range(B))
+        score_bytes = 4 * H * (tokens * (min(2 * r + 1, n)) + 2 * g_used * n) + 4 * B * n
+    prune_bytes = 4 * B * n * 3 + 2 * sum(kept) * H * dd * 2
+    roof = roofline(flops, bytes_, median(fwd), median(cols), pairs,
+                    score=("k_score_from_band" if band else "k_score_from_partials", score_us, score_bytes),
+                    prune=("k_prune_scan + k_gather_rows", prune_us, prune_bytes))
+    return dict(ms=median(per), mean_ms=mean_ms, wall_ms=wall_ms, fwd_ms=median(fwd), cols_ms=median(cols),
+                tokens=tokens, kept=kept, flops=flops, bytes=bytes_, roof=roof, theta=theta, pairs=pairs)
+
+
+def measure_passes(sc, si, torch, np, cfg, steps, warmup, dev="cuda:0"):
+    """Times `steps` steps of three successive prune passes: each pass runs the window attention with score
+    partials, the scores, and the threshold prune + compaction of Q, K and V into the next pass's buffers, with
+    the lengths and global positions staying on the device."""
+    inp = si.make_attention_inputs(cfg)
+    B, n, H, dd, G = cfg.B, cfg.n, cfg.H, cfg.d, cfg.n_global
+
+    def i32(a):
+        return torch.from_numpy(np.ascontiguousarray(a, dtype=np.int32)).to(dev)
+
+    def bf(a):
+        return torch.from_numpy(np.ascontiguousarray(a).view(np.int16)).to(dev).view(torch.bfloat16)
+
+    P = len(cfg.thresholds)
+    qkv = [[bf(inp["q"]), bf(inp["k"]), bf(inp["v"])]] + [[torch.empty((B, n, H, dd), dtype=torch.bfloat16,
+                                                                       device=dev) for _ in range(3)]
+                                                          for _ in range(P)]
+    lens = [i32(inp["valid_len"])] + [torch.empty((B,), dtype=torch.int32, device=dev) for _ in range(P)]
+    gps = [i32(inp["global_pos"])] + [torch.empty((B, G), dtype=torch.int32, device=dev) for _ in range(P)]
+    descs = [sc.Desc(B, n, H, cfg.window, lens[p], gps[p], cfg.alpha, sc.SC_BF16) for p in range(P)]
+    d0 = descs[0]
+    out = torch.empty_like(qkv[0][0])
+    lse = torch.empty((B, H, n), dtype=torch.float32, device=dev)
+    sp = torch.empty(sc.sc_score_partials_size(d0) // 4, dtype=torch.float32, device=dev)
+    ws_attn = torch.empty(max(sc.sc_window_attention_workspace_size(d0), 1), dtype=torch.uint8, device=dev)
+    scores = torch.empty((B, n), dtype=torch.float32, device=dev)
+    ws_prune = torch.empty(sc.sc_ltp_prune_compact_workspace_size(d0), dtype=torch.uint8, device=dev)
+    keep = torch.empty((B, n), dtype=torch.int32, device=dev)
+
+    def step(i):
+        for p in range(P):
+            d = descs[p]
+            sc.sc_window_attention(d, *qkv[p], out=out, lse=lse, score_partials=sp, workspace=ws_attn)
+            sc.sc_ltp_score(d, sp, scores=scores)
+            sc.sc_ltp_prune_compact(d, scores, cfg.thresholds[p], True, qkv[p], dsts=qkv[p + 1], want_orig=False,
+                                    outs=dict(keep_idx=keep, new_len=lens[p + 1], new_global_pos=gps[p + 1]),
+                                    workspace=ws_prune)
+
+    per, mean_ms, wall_ms = timed(step, steps, warmup, torch)
+    # the per-pass attention times, in a second run of the same steps
+    sc.sc_profile_window_kernel(True)
+    timed(step, steps, 0, torch)
+    fwd, cols = sc.sc_profile_window_kernel_read()
+    sc.sc_profile_window_kernel(False)
+    lens_h = [inp["valid_len"].astype(np.int64)] + [lens[p + 1].cpu().numpy().astype(np.int64) for p in range(P)]
+    gps_h = [inp["global_pos"]] + [gps[p + 1].cpu().numpy() for p in range(P)]
+    tokens = int(sum(int(np.sum(lens_h[p])) for p in range(P)))
+    # the dominant kernel is pass 1's launch 1
+    pw, pg = algorithmic_counts(dict(B=B, valid_len=lens_h[0], global_pos=gps_h[0], window=cfg.window))
+    flops, bytes_ = attention_work(int(np.sum(lens_h[0])), H, dd, H * (pw + pg))
+    roof = roofline(flops, bytes_, median(fwd[0::P]), median(cols[0::P]), H * (pw + pg))
+    roof["kernel"] = "k_attn_fwd<bf16> of pass 1 (launch 1 of the window attention: softmax and P.V)"
+    roof["traffic"] = None
+    passes = []
+    for p in range(P):
+        pw_, pg_ = algorithmic_counts(dict(B=B, valid_len=lens_h[p], global_pos=gps_h[p], window=cfg.window))
+        passes.append(dict(tokens_in=lens_h[p].tolist(), kept=lens_h[p + 1].tolist(), allowed_pairs=H * (pw_ + pg_),
+                           attn_fwd_us=round(median(fwd[p::P]) * 1e3, 2),
+                           attn_cols_us=round(median(cols[p::P]) * 1e3, 2)))
+    return dict(ms=median(per), mean_ms=mean_ms, wall_ms=wall_ms, tokens=tokens, roof=roof, passes=passes, inp=inp,
+                lens=lens_h, gps=gps_h)
 
 
 def sweep(args, sc, si, torch, np):
@@ -396,7 +624,8 @@ def sweep(args, sc, si, torch, np):
             "sweep": kind, "n": n, "window": w, "batch": B, "valid_tokens": m["tokens"],
             "allowed_pairs": m["pairs"], "ms_per_step": round(m["ms"], 4),
             "value": round(m["tokens"] / (m["ms"] * 1e-3), 1), "unit": "kept-token-layers/s",
-            "attention_us": round(m["kern_ms"] * 1e3, 2), "ns_per_pair": round(m["kern_ms"] * 1e6 / m["pairs"], 4),
+            "attention_us": round((m["fwd_ms"] + m["cols_ms"]) * 1e3, 2),
+            "ns_per_pair": round((m["fwd_ms"] + m["cols_ms"]) * 1e6 / m["pairs"], 4),
             "roofline": m["roof"], "kept_fraction": round(sum(m["kept"]) / m["tokens"], 3)}), flush=True)
 
 
@@ -411,14 +640,19 @@ def main():
                          "hardware counters)")
     ap.add_argument("--workload", choices=sorted(WORKLOADS), default="seq4096",
                     help="seq4096: B8 n4096 window 512, 32 global tokens (the headline line); lognormal: B64 n1024 "
-                         "window 256, one global token, paper-shaped lognormal lengths; encoder: the 12-layer "
-                         "stack; soft: training step (forward and backward) of one soft-pruned layer at seq4096")
+                         "window 256, one global token, paper-shaped lognormal lengths; stack: the 12-layer "
+                         "attention-only stack, B16 n2048; encoder: the 12-layer stack with feed-forward blocks; "
+                         "passes / passes5b: three successive prune passes at B2 n8192 window 1024; soft: training "
+                         "step (forward and backward) of one soft-pruned layer at seq4096")
     ap.add_argument("--prune", choices=("threshold", "topk"), default="threshold",
                     help="pruning rule of the step: the layer threshold (the paper's rule) or top-k by keep ratio")
     ap.add_argument("--keep-ratio", type=float, default=0.5, help="top-k rule: fraction of candidates kept")
     ap.add_argument("--causal", action="store_true",
                     help="the causal variant of the attention (keys after the query never attended); the "
                          "threshold is then the median score (the stored one belongs to the bidirectional scores)")
+    ap.add_argument("--score", choices=("partials", "band"), default="partials",
+                    help="partials: the fused column-sum partials (default); band: the paper's score path, every "
+                         "probability stored in the band layout and summed from it (Sec. 5.5)")
     ap.add_argument("--sweep", action="store_true",
                     help="instead of the single measurement, sweep the window (n 4096) and the length (window "
                          "512), one JSON line per point")
@@ -440,13 +674,14 @@ def main():
         sweep(args, sc, si, torch, np)
         return
     cid, desc = WORKLOADS[args.workload]
+    common = {"n_gpus": 1, "steps": args.steps, "warmup": args.warmup, "higher_is_better": True, "scaling": "weak",
+              "vs_baseline": None, "dtype": "bf16", "data": "synthetic"}
     if cid == "soft":
         m = measure_soft(args, sc, si, torch, np, dev)
         line = {
             "metric": METRIC, "value": round(m["tokens"] / (m["ms"] * 1e-3), 1),
-            "unit": "token-layers/s (training step)", "n_gpus": 1, "steps": args.steps, "warmup": args.warmup,
-            "ms_per_step": round(m["ms"], 4), "higher_is_better": True, "scaling": "weak", "vs_baseline": None,
-            "dtype": "bf16", "data": "synthetic",
+            "unit": "token-layers/s (training step)", **common, "ms_per_step": round(m["ms"], 4),
+            "mean_ms_per_step": round(m["mean_ms"], 4),
             "config": {"workload": desc, "valid_tokens": m["tokens"], "threshold": m["theta"],
                        "temperature": m["temp"], "parallelism": "none (1 GPU)"},
             "roofline": m["roof"], "backward_ms": round(m["bwd_ms"], 4), "dtheta": m["dtheta"],
@@ -455,16 +690,53 @@ def main():
             line["cpu_baseline"] = m["cpu_baseline"]
         print(json.dumps(line), flush=True)
         return
-    if cid is None:
-        m = measure_encoder(args, sc, si, torch, np, dev)
-        print(json.dumps({
+    if cid in ("encoder", "stack"):
+        m = measure_stack(args, sc, si, torch, np, full=cid == "encoder", dev=dev)
+        line = {
             "metric": METRIC, "value": round(m["tokens"] / (m["ms"] * 1e-3), 1), "unit": "kept-token-layers/s",
-            "n_gpus": 1, "steps": args.steps, "warmup": args.warmup, "ms_per_step": round(m["ms"], 4),
-            "higher_is_better": True, "scaling": "weak", "vs_baseline": None, "dtype": "bf16", "data": "synthetic",
+            **common, "ms_per_step": round(m["ms"], 4), "mean_ms_per_step": round(m["mean_ms"], 4),
             "config": {"workload": desc, "layer_input_tokens": m["tokens"], "kept_per_layer": m["kept_per_layer"],
                        "parallelism": "none (1 GPU)"},
             "model_gflops": m["gflops"], "model_gflops_total": m["total_gflops"], "roofline": m["roof"],
-            "input_generation_s": round(m["gen_s"], 1)}), flush=True)
+            "layers": m["layers"], "input_generation_s": round(m["gen_s"], 1)}
+        if "cpu_baseline" in m:
+            line["cpu_baseline"] = m["cpu_baseline"]
+        print(json.dumps(line), flush=True)
+        return
+    if args.workload.startswith("passes"):
+        cfg = si.CONFIGS[cid]
+        t0 = time.time()
+        m = measure_passes(sc, si, torch, np, cfg, args.steps, args.warmup, dev)
+        gen_s = time.time() - t0
+        line = {
+            "metric": METRIC, "value": round(m["tokens"] / (m["ms"] * 1e-3), 1), "unit": "kept-token-layers/s",
+            **common, "ms_per_step": round(m["ms"], 4), "mean_ms_per_step": round(m["mean_ms"], 4),
+            "config": {"workload": desc, "batch": cfg.B, "seq_len": cfg.n, "heads": cfg.H, "head_dim": cfg.d,
+                       "window": cfg.window, "global_tokens": cfg.n_global, "thresholds": cfg.thresholds,
+                       "pass_input_tokens": m["tokens"], "parallelism": "none (1 GPU)"},
+            "roofline": m["roof"], "passes": m["passes"], "setup_s": round(gen_s, 1)}
+        if not args.no_cpu_baseline:
+            import oracle
+            inp = m["inp"]
+
+            def run(rows, threads):
+                q64, k64, v64 = (inp[x][rows] for x in ("q64", "k64", "v64"))
+                vl, gp = inp["valid_len"][rows].copy(), inp["global_pos"][rows].copy()
+                for theta in cfg.thresholds:
+                    _, _, rs = oracle.sparse_attention(q64, k64, v64, vl, gp, cfg.window, cfg.alpha, nthreads=threads)
+                    rk, rnl, rngp, _ = oracle.ltp_prune(rs.astype(np.float32), vl, gp, theta, 1)
+                    q2, k2, v2 = (np.zeros_like(x) for x in (q64, k64, v64))
+                    for b in range(len(rows)):
+                        idx = rk[b, :rnl[b]]
+                        q2[b, :len(idx)], k2[b, :len(idx)], v2[b, :len(idx)] = q64[b, idx], k64[b, idx], v64[b, idx]
+                    q64, k64, v64, vl, gp = q2, k2, v2, rnl.astype(np.int32), rngp
+
+            one = int(m["lens"][0][0]) + sum(int(m["lens"][p][0]) for p in range(1, len(cfg.thresholds)))
+            line["cpu_baseline"] = cpu_baseline(lambda t: run(list(range(cfg.B)), t), m["tokens"],
+                                                lambda t: run([0], t), one, "kept-token-layers/s",
+                                                f"the whole workload ({cfg.B} sequences, three passes) in double "
+                                                "precision", "sequence 0, three passes")
+        print(json.dumps(line), flush=True)
         return
     cfg = si.CONFIGS[cid]
     with open(os.path.join(ROOT, "tests", "golden", "thresholds.json")) as f:
@@ -476,27 +748,23 @@ def main():
     if args.causal:
         theta = None
     m = measure(sc, si, torch, np, inp, theta, args.steps, args.warmup, dev, keep_ratio=keep_ratio,
-                causal=args.causal)
+                causal=args.causal, band=args.score == "band")
     theta = m["theta"]
     ms, tokens = m["ms"], m["tokens"]
     roof = m["roof"]
     # the recorded counters belong to the (bidirectional, threshold-pruned) seq4096 workload
-    roof["traffic"] = recorded_traffic() if (args.workload == "seq4096" and not args.causal) else None
-    roof["kernel"] = "k_attn_fwd<bf16> + k_attn_cols<bf16> (the two launches of the window attention)"
-    roof["kernel_us"] = round(m["kern_ms"] * 1e3, 2)
-    roof["algorithmic_flop"] = m["flops"]
-    roof["algorithmic_bytes"] = m["bytes"]
-
+    roof["traffic"] = recorded_traffic() if (args.workload == "seq4096" and not args.causal and
+                                             keep_ratio is None and args.score == "partials") else None
     value = tokens / (ms * 1e-3)
     result = {
-        "metric": METRIC, "value": round(value, 1), "unit": "kept-token-layers/s", "n_gpus": 1,
-        "steps": args.steps, "warmup": args.warmup, "ms_per_step": round(ms, 4), "higher_is_better": True,
-        "scaling": "weak", "vs_baseline": None, "dtype": "bf16", "data": "synthetic",
+        "metric": METRIC, "value": round(value, 1), "unit": "kept-token-layers/s", **common,
+        "ms_per_step": round(ms, 4), "mean_ms_per_step": round(m["mean_ms"], 4),
         "config": {"workload": desc,
                    "batch": cfg.B, "seq_len": cfg.n, "heads": cfg.H, "head_dim": cfg.d, "window": cfg.window,
                    "global_tokens": cfg.n_global, "valid_tokens": tokens,
                    "pruning": (f"top-k, keep ratio {keep_ratio}" if keep_ratio is not None else
                                f"threshold {theta}"), "attention": "causal" if args.causal else "bidirectional",
+                   "scores": "band layout (paper)" if args.score == "band" else "fused column-sum partials",
                    "parallelism": "none (1 GPU)"},
         "roofline": roof,
         "kept_per_sequence": m["kept"],
@@ -504,19 +772,23 @@ def main():
     }
     if not args.no_cpu_baseline:
         import oracle
-        threads = oracle.default_threads()
-        c0 = time.perf_counter()
-        _, _, rs = oracle.sparse_attention(inp["q64"], inp["k64"], inp["v64"], inp["valid_len"], inp["global_pos"],
-                                           cfg.window, cfg.alpha, nthreads=threads, causal=args.causal)
-        if keep_ratio is None:
-            oracle.ltp_prune(rs.astype(np.float32), inp["valid_len"], inp["global_pos"], theta, 1)
-        else:
-            oracle.topk_prune(rs.astype(np.float32), inp["valid_len"], inp["global_pos"], keep_ratio, 1)
-        cpu_s = time.perf_counter() - c0
-        result["cpu_baseline"] = {"value": round(tokens / cpu_s, 1), "unit": "kept-token-layers/s", "cores": threads,
-                                  "kind": "oracle",
-                                  "sample": f"the whole workload once ({cfg.B} sequences, one layer: attention, "
-                                            f"scores, pruning) in double precision, {cpu_s:.2f} s"}
+
+        def run(rows, threads):
+            _, _, rs = oracle.sparse_attention(inp["q64"][rows], inp["k64"][rows], inp["v64"][rows],
+                                               inp["valid_len"][rows], inp["global_pos"][rows], cfg.window, cfg.alpha,
+                                               nthreads=threads, causal=args.causal)
+            if keep_ratio is None:
+                oracle.ltp_prune(rs.astype(np.float32), inp["valid_len"][rows], inp["global_pos"][rows], theta, 1)
+            else:
+                oracle.topk_prune(rs.astype(np.float32), inp["valid_len"][rows], inp["global_pos"][rows], keep_ratio,
+                                  1)
+
+        allrows = list(range(cfg.B))
+        result["cpu_baseline"] = cpu_baseline(lambda t: run(allrows, t), tokens, lambda t: run([0], t),
+                                              int(inp["valid_len"][0]), "kept-token-layers/s",
+                                              f"the whole workload ({cfg.B} sequences, one layer: attention, scores, "
+                                              "pruning) in double precision",
+                                              f"sequence 0 ({int(inp['valid_len'][0])} tokens), one layer")
     result["input_generation_s"] = round(gen_s, 1)
     if args.copy_calibration > 0:
         nb = args.copy_calibration << 20
@@ -527,7 +799,6 @@ def main():
         torch.cuda.synchronize()
         result["copy_calibration_bytes"] = nb
     print(json.dumps(result), flush=True)
-
 
 if __name__ == "__main__":
     main()

@@ -21,7 +21,7 @@
  *                         step 3) for the next layer;
  *   sc_topk_prune_compact the same compaction with a top-k rule instead of the
  *                         threshold (a variant in the family of cascade token
- *                         pruning the paper cites in Sec. 2);
+ *                         pruning the paper cites in Sec. 3.3);
  *   sc_ltp_soft_mask      the soft mask of LTP's training phase (Sec. 4.2.2
  *                         step 1) and sc_ltp_soft_backward, the gradients of
  *                         q, k, v and the threshold through it;
@@ -198,7 +198,7 @@ sc_status sc_ltp_prune_compact(const sc_attn_desc *desc, const float *scores, fl
 
 /*
  * Top-k pruning, an alternative selection rule to the threshold above (the
- * paper's Sec. 2 places LTP among token-pruning methods, some of which keep a
+ * paper's Sec. 3.3 places LTP among token-pruning methods, some of which keep a
  * fixed fraction of the tokens by rank).  Per sequence b, the candidates are the
  * valid tokens k < L_b, except the global ones when keep_global is set (those
  * are always kept); with C_b candidates,
@@ -314,16 +314,21 @@ sc_status sc_encoder_stack(const sc_attn_desc *desc, int32_t n_layers, const int
                            void *workspace, size_t ws_bytes, void *stream);
 
 /*
- * Kernel timing for benchmarks.  While enabled, the window-attention kernels
- * (its two passes: softmax/P.V, then the exact-probability column sums; the
- * dominant work of sc_window_attention and of each stack layer) are bracketed
- * by a pair of hipEvents recorded on the caller's stream.  sc_profile_window_kernel_read() waits for the recorded
- * events, returns the summed kernel time in milliseconds and the number of
- * launches, and clears the record.  Enabling with a non-zero argument also
- * clears it.  Not thread-safe; at most 4096 launches are recorded.
+ * Kernel timing for benchmarks.  While enabled, every window-attention call
+ * (sc_window_attention, and each layer of the stacks) records three hipEvents
+ * on the caller's stream: before its first launch (softmax and P.V), between
+ * the launches, and after its second launch (the exact-probability column
+ * sums).  sc_profile_window_kernel_read() waits for the recorded events and
+ * writes, for the first min(capacity, *calls) calls in call order, the time of
+ * launch 1 to fwd_ms[i] and of launch 2 to cols_ms[i], in milliseconds (host
+ * arrays owned by the caller); *calls receives the number of calls recorded.
+ * It then clears the record; enabling with a non-zero argument clears it too.
+ * Errors: SC_EINVAL for a null `calls`, a negative capacity or null arrays
+ * with a positive capacity; SC_EHIP if an event failed.  Not thread-safe; at
+ * most 4096 calls are recorded.
  */
 sc_status sc_profile_window_kernel(int32_t enable);
-sc_status sc_profile_window_kernel_read(double *total_ms, int64_t *launches);
+sc_status sc_profile_window_kernel_read(double *fwd_ms, double *cols_ms, int64_t capacity, int64_t *calls);
 
 #ifdef __cplusplus
 }

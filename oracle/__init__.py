@@ -60,7 +60,7 @@ def lib():
         L.orc_soft_prune_forward.argtypes = [ci, ci, ci, ci, ci, ci, i32p, i32p, cd, f64p, f64p, f64p, cd, cd, ci,
                                              f64p, f64p, f64p, f64p, f64p, ci]
         L.orc_soft_prune_backward.argtypes = [ci, ci, ci, ci, ci, ci, i32p, i32p, cd, f64p, f64p, f64p, cd, cd, ci,
-                                              f64p, f64p, f64p, f64p, f64p, f64p, ci]
+                                              f64p, f64p, f64p, f64p, f64p, f64p, f64p, f64p, f64p, f64p, ci]
         for f in ("orc_sparse_attention", "orc_sparse_attention_causal", "orc_ltp_prune", "orc_topk_prune",
                   "orc_gather_rows", "orc_encoder_layer", "orc_encoder_stack", "orc_encoder_layer_ffn",
                   "orc_encoder_stack_ffn", "orc_soft_prune_forward", "orc_soft_prune_backward"):
@@ -136,9 +136,10 @@ def soft_prune_forward(q, k, v, valid_len, global_pos, window, alpha, theta, tem
 
 
 def soft_prune_backward(q, k, v, valid_len, global_pos, window, alpha, theta, temperature, dy, dmask=None,
-                        keep_global=1, nthreads=None):
+                        keep_global=1, nthreads=None, scales=False):
     """Backward of soft_prune_forward for dL/dy = dy [B, n, H, d] and dL/dmask = dmask [B, n] (or None).
-    Returns (dq, dk, dv, dtheta)."""
+    Returns (dq, dk, dv, dtheta); with scales, also (mq, mk, mv, mtheta): the same chain on magnitudes, the
+    error scale of each gradient element."""
     q, k, v, dy = _f64(q), _f64(k), _f64(v), _f64(dy)
     B, n, H, d = q.shape
     gp = _i32(global_pos).reshape(B, -1)
@@ -146,12 +147,17 @@ def soft_prune_backward(q, k, v, valid_len, global_pos, window, alpha, theta, te
     dm = _f64(dmask) if dmask is not None else None
     dq, dk, dv = np.empty_like(q), np.empty_like(q), np.empty_like(q)
     dth = np.zeros(1)
+    mq, mk, mv, mth = (np.empty_like(q), np.empty_like(q), np.empty_like(q), np.zeros(1)) if scales else \
+        (None, None, None, None)
     c = ctypes.c_double
     rc = lib().orc_soft_prune_backward(B, n, H, d, int(window), gp.shape[1], _p(gp, ctypes.c_int32),
                                        _p(vl, ctypes.c_int32), float(alpha), _p(q, c), _p(k, c), _p(v, c),
                                        float(theta), float(temperature), int(keep_global), _p(dy, c), _p(dm, c),
-                                       _p(dq, c), _p(dk, c), _p(dv, c), _p(dth, c), nthreads or default_threads())
+                                       _p(dq, c), _p(dk, c), _p(dv, c), _p(dth, c), _p(mq, c), _p(mk, c), _p(mv, c),
+                                       _p(mth, c), nthreads or default_threads())
     assert rc == 0, rc
+    if scales:
+        return dq, dk, dv, float(dth[0]), mq, mk, mv, float(mth[0])
     return dq, dk, dv, float(dth[0])
 
 

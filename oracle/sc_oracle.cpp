@@ -20,7 +20,7 @@
 //     the display equation of step 2); hard pruning removes masked tokens
 //     (Sec. 4.2.2 step 3) and later layers see the shorter sequence (Sec. 4.2).
 //   * top-k pruning (a rank rule in place of the threshold; not the paper's
-//     rule, a variant from the token-pruning family of its Sec. 2): the
+//     rule, a variant from the token-pruning families of its Sec. 3.3): the
 //     ceil(keep_ratio * C) best-scored candidates per sequence are kept;
 //   * soft pruning, the training form (Sec. 4.2.2 step 1): a sigmoid soft mask
 //     of the score against the threshold scales the layer output, and its
@@ -242,7 +242,7 @@ int orc_ltp_prune(int B, int n, int G, const int32_t* global_pos, const int32_t*
 }
 
 // Top-k pruning: the same compaction with a rank rule instead of the
-// threshold (the paper's Sec. 2 places LTP among token-pruning methods, some
+// threshold (the paper's Sec. 3.3 places LTP among token-pruning methods, some
 // of which keep a fixed fraction of the tokens by rank).  Per sequence the
 // candidates are the valid tokens, except the global ones when keep_global is
 // set (those are kept anyway); of C candidates the K = ceil(keep_ratio * C)
@@ -329,9 +329,13 @@ static int encoder_layer(int B, int n, int H, int d, int window, int G, const in
   const long D = (long)H * d, D3 = 3 * D;
   std::vector<double> qv((size_t)B * n * D), kv((size_t)B * n * D), vv((size_t)B * n * D);
   // a1: projection, double accumulation, bf16 storage.  Padding rows are
-  // projected too; the attention never reads them.
-#pragma omp parallel for schedule(static)
+  // left zero: the attention never reads them.
+#pragma omp parallel for schedule(dynamic, 16)
   for (long row = 0; row < (long)B * n; ++row) {
+    if (row % n >= std::min(std::max(valid_len[row / n], 0), n)) {
+      for (long j = 0; j < D; ++j) qv[row * D + j] = kv[row * D + j] = vv[row * D + j] = 0.0;
+      continue;
+    }
     const double* xr = x + row * D;
     std::vector<double> acc(D3, 0.0);
     for (long c = 0; c < D; ++c) {
@@ -553,10 +557,16 @@ int orc_soft_prune_forward(int B, int n, int H, int d, int window, int G, const 
 // Backward of orc_soft_prune_forward for the loss gradient dy [B, n, H, d]
 // (with respect to y) and dmask [B, n] (with respect to the mask, or NULL).
 // Writes dq, dk, dv [B, n, H, d] and dtheta (a scalar).
+// Optional error scales (each may be NULL): mq, mk, mv [B, n, H, d] and
+// mtheta hold the same chain evaluated on magnitudes (every factor replaced by
+// its absolute value, every difference by a sum), so that a perturbation of
+// relative size u in every rounded factor moves each gradient element by at
+// most about u times its scale (the running error bound of a sum of products).
 int orc_soft_prune_backward(int B, int n, int H, int d, int window, int G, const int32_t* global_pos,
                             const int32_t* valid_len, double alpha, const double* q, const double* k, const double* v,
                             double theta, double T, int keep_global, const double* dy, const double* dmask,
-                            double* dq, double* dk, double* dv, double* dtheta, int nthreads) {
+                            double* dq, double* dk, double* dv, double* dtheta, double* mq, double* mk, double* mv,
+                            double* mtheta, int nthreads) {
   if (B < 0 || n < 0 || H <= 0 || d <= 0 || window < 0 || G < 0 || !(T > 0.0)) return -1;
   const long D = (long)H * d;
   const size_t bnD = (size_t)B * n * D;
@@ -568,29 +578,41 @@ int orc_soft_prune_backward(int B, int n, int H, int d, int window, int G, const
   // y = m * out: dL/dm_k = sum over the row of dy * out (+ dmask), dL/dout = m * dy.
   // m = sigmoid(z), z = (s - theta) / T: dL/ds = dL/dm * m (1 - m) / T and
   // dL/dtheta = - sum of the same over the masked tokens.
-  std::vector<double> gs((size_t)B * n, 0.0), dout(bnD, 0.0);
-  double dth = 0.0;
+  std::vector<double> gs((size_t)B * n, 0.0), dout(bnD, 0.0), gsm((size_t)B * n, 0.0);
+  double dth = 0.0, dthm = 0.0;
   for (int b = 0; b < B; ++b) {
     int L = std::min(std::max(valid_len[b], 0), n);
     std::vector<char> g = global_flags(n, L, G, global_pos + (long)b * G);
     for (int kk = 0; kk < L; ++kk) {
       const long t = (long)b * n + kk;
       double dm = dmask ? dmask[t] : 0.0;
+      double dmm = std::fabs(dm);
       for (long c = 0; c < D; ++c) {
         dm += dy[t * D + c] * out[t * D + c];
+        dmm += std::fabs(dy[t * D + c] * out[t * D + c]);
         dout[t * D + c] = mask[t] * dy[t * D + c];
       }
       if (keep_global && g[kk]) continue;  // a constant mask of 1
       const double ds = dm * mask[t] * (1.0 - mask[t]) / T;
+      const double dsm = dmm * mask[t] * (1.0 - mask[t]) / T;
       // s_k = (1 / (H L)) sum_h sum_q P_h[q][k]: each P_h[q][k] receives ds / (H L)
       gs[t] = ds / ((double)H * L);
+      gsm[t] = dsm / ((double)H * L);
       dth -= ds;
+      dthm += dsm;
     }
   }
   *dtheta = dth;
+  if (mtheta) *mtheta = dthm;
   std::fill(dq, dq + bnD, 0.0);
   std::fill(dk, dk + bnD, 0.0);
   std::fill(dv, dv + bnD, 0.0);
+  const bool scales = mq && mk && mv;
+  if (scales) {
+    std::fill(mq, mq + bnD, 0.0);
+    std::fill(mk, mk + bnD, 0.0);
+    std::fill(mv, mv + bnD, 0.0);
+  }
   set_threads(nthreads);
   const int r = window / 2;
 #pragma omp parallel for schedule(dynamic, 1)
@@ -602,18 +624,24 @@ int orc_soft_prune_backward(int B, int n, int H, int d, int window, int G, const
     const double *qh = q + base, *kh = k + base, *vh = v + base, *doh = dout.data() + base;
     double *dqh = dq + base, *dkh = dk + base, *dvh = dv + base;
     std::vector<int> nbr;
-    std::vector<double> p, dp;
+    std::vector<double> p, dp, dpm;
     for (int i = 0; i < L; ++i) {
       row_probs(d, L, r, g, alpha, qh, kh, D, i, nbr, p);
       // out_i = sum_j P[i][j] v_j and the score term: dL/dP[i][j] = dout_i . v_j + gs_j
       dp.assign(nbr.size(), 0.0);
-      double rowdot = 0.0;  // sum_j P[i][j] dL/dP[i][j]
+      dpm.assign(nbr.size(), 0.0);
+      double rowdot = 0.0, rowdotm = 0.0;  // sum_j P[i][j] dL/dP[i][j]
       for (size_t t = 0; t < nbr.size(); ++t) {
         const int j = nbr[t];
-        double acc = 0.0;
-        for (int c = 0; c < d; ++c) acc += doh[(long)i * D + c] * vh[(long)j * D + c];
+        double acc = 0.0, accm = 0.0;
+        for (int c = 0; c < d; ++c) {
+          acc += doh[(long)i * D + c] * vh[(long)j * D + c];
+          accm += std::fabs(doh[(long)i * D + c] * vh[(long)j * D + c]);
+        }
         dp[t] = acc + gs[(long)b * n + j];
+        dpm[t] = accm + gsm[(long)b * n + j];
         rowdot += p[t] * dp[t];
+        rowdotm += p[t] * dpm[t];
       }
       for (size_t t = 0; t < nbr.size(); ++t) {
         const int j = nbr[t];
@@ -623,6 +651,15 @@ int orc_soft_prune_backward(int B, int n, int H, int d, int window, int G, const
           dqh[(long)i * D + c] += alpha * dsij * kh[(long)j * D + c];
           dkh[(long)j * D + c] += alpha * dsij * qh[(long)i * D + c];
           dvh[(long)j * D + c] += p[t] * doh[(long)i * D + c];
+        }
+        if (scales) {
+          const double dsm = p[t] * (dpm[t] + rowdotm);
+          double *mqh = mq + base, *mkh = mk + base, *mvh = mv + base;
+          for (int c = 0; c < d; ++c) {
+            mqh[(long)i * D + c] += alpha * dsm * std::fabs(kh[(long)j * D + c]);
+            mkh[(long)j * D + c] += alpha * dsm * std::fabs(qh[(long)i * D + c]);
+            mvh[(long)j * D + c] += p[t] * std::fabs(doh[(long)i * D + c]);
+          }
         }
       }
     }

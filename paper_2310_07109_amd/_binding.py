@@ -2,6 +2,7 @@
 from __future__ import annotations
 
 import ctypes
+import functools
 import os
 
 _HERE = os.path.dirname(os.path.abspath(__file__))
@@ -60,7 +61,8 @@ def load():
         "sc_encoder_stack_workspace_size": (sz, [dp, i32, i32]),
         "sc_encoder_stack": (i32, [dp, i32, vp, vp, vp, vp, vp, vp, i32, vp, i32, f32, vp, vp, vp, vp, vp, sz, vp]),
         "sc_profile_window_kernel": (i32, [i32]),
-        "sc_profile_window_kernel_read": (i32, [ctypes.POINTER(ctypes.c_double), ctypes.POINTER(ctypes.c_int64)]),
+        "sc_profile_window_kernel_read": (i32, [ctypes.POINTER(ctypes.c_double), ctypes.POINTER(ctypes.c_double),
+                                                 ctypes.c_int64, ctypes.POINTER(ctypes.c_int64)]),
     }
     for name, (res, args) in sig.items():
         f = getattr(L, name)
@@ -81,6 +83,46 @@ def _check(status: int, where: str):
 
 def _ptr(t):
     return None if t is None else ctypes.c_void_p(t.data_ptr())
+
+
+def _tensor(t, name, dtype=None, shape=None, leading=None):
+    """Checks a tensor argument before its pointer is marshalled: a contiguous CUDA tensor, of `dtype`, of
+    exactly `shape` or with leading dimensions `leading`.  Returns it."""
+    import torch
+    if not isinstance(t, torch.Tensor):
+        raise TypeError(f"{name}: expected a torch.Tensor, got {type(t).__name__}")
+    if not t.is_cuda:
+        raise ValueError(f"{name}: expected a GPU tensor, got one on {t.device}")
+    if not t.is_contiguous():
+        raise ValueError(f"{name}: expected a contiguous tensor")
+    if dtype is not None and t.dtype != dtype:
+        raise TypeError(f"{name}: expected {dtype}, got {t.dtype}")
+    if shape is not None and tuple(t.shape) != tuple(shape):
+        raise ValueError(f"{name}: expected shape {tuple(shape)}, got {tuple(t.shape)}")
+    if leading is not None and tuple(t.shape[:len(leading)]) != tuple(leading):
+        raise ValueError(f"{name}: expected leading dimensions {tuple(leading)}, got {tuple(t.shape)}")
+    return t
+
+
+def _min_bytes(t, name, nbytes):
+    if t.numel() * t.element_size() < nbytes:
+        raise ValueError(f"{name}: {t.numel() * t.element_size()} bytes, {nbytes} needed")
+    return t
+
+
+def _on_stream(fn):
+    """Runs a wrapper with `stream` (when given) as torch's current stream, so that the outputs and workspaces
+    it allocates belong to the stream its kernels are enqueued on: the caching allocator then never hands that
+    memory to work on another stream while the kernels still use it."""
+    @functools.wraps(fn)
+    def run(*args, **kwargs):
+        stream = kwargs.get("stream")
+        if stream is None:
+            return fn(*args, **kwargs)
+        import torch
+        with torch.cuda.stream(stream):
+            return fn(*args, **kwargs)
+    return run
 
 
 def _stream(stream):
@@ -142,6 +184,7 @@ def _opt(spec, make):
     return spec
 
 
+@_on_stream
 def sc_window_attention(desc: Desc, q, k, v, out=None, lse=True, score_partials=True, band_probs=False,
                         workspace=None, stream=None):
     """Returns (out, lse, score_partials, band_probs); absent outputs are None.
@@ -150,15 +193,26 @@ def sc_window_attention(desc: Desc, q, k, v, out=None, lse=True, score_partials=
     import torch
     L = load()
     cd = desc.c()
+    shape = (desc.B, desc.n, desc.H, desc.d)
+    for t, nm in ((q, "q"), (k, "k"), (v, "v")):
+        _tensor(t, nm, desc.torch_dtype(), shape)
     dev = q.device
-    out = torch.empty_like(q) if out is None else out
+    out = torch.empty_like(q) if out is None else _tensor(out, "out", desc.torch_dtype(), shape)
+    if isinstance(lse, torch.Tensor):
+        _tensor(lse, "lse", torch.float32, (desc.B, desc.H, desc.n))
+    if isinstance(score_partials, torch.Tensor):
+        _min_bytes(_tensor(score_partials, "score_partials", torch.float32), "score_partials",
+                   L.sc_score_partials_size(ctypes.byref(cd)))
+    if isinstance(band_probs, torch.Tensor):
+        _min_bytes(_tensor(band_probs, "band_probs", torch.float32), "band_probs",
+                   L.sc_band_probs_size(ctypes.byref(cd)))
     lse_t = _opt(lse, lambda: torch.empty((desc.B, desc.H, desc.n), dtype=torch.float32, device=dev))
     sp = _opt(score_partials, lambda: torch.empty(L.sc_score_partials_size(ctypes.byref(cd)) // 4,
                                                   dtype=torch.float32, device=dev))
     bp = _opt(band_probs, lambda: torch.empty(L.sc_band_probs_size(ctypes.byref(cd)) // 4, dtype=torch.float32,
                                               device=dev))
     wsb = L.sc_window_attention_workspace_size(ctypes.byref(cd))
-    ws = _ws(wsb, dev) if workspace is None else workspace
+    ws = _ws(wsb, dev) if workspace is None else _tensor(workspace, "workspace")
     wsb = wsb if workspace is None else workspace.numel() * workspace.element_size()
     _check(L.sc_window_attention(ctypes.byref(cd), _ptr(q), _ptr(k), _ptr(v), _ptr(out), _ptr(lse_t), _ptr(sp),
                                  _ptr(bp), _ptr(ws), wsb, _stream(stream)), "sc_window_attention")
@@ -169,11 +223,16 @@ def sc_ltp_score_workspace_size(desc: Desc, mode: int = SC_SCORE_FROM_PARTIALS) 
     return load().sc_ltp_score_workspace_size(ctypes.byref(desc.c()), mode)
 
 
+@_on_stream
 def sc_ltp_score(desc: Desc, src, mode: int = SC_SCORE_FROM_PARTIALS, scores=None, stream=None):
     import torch
     L = load()
     cd = desc.c()
-    scores = torch.empty((desc.B, desc.n), dtype=torch.float32, device=src.device) if scores is None else scores
+    need = L.sc_score_partials_size(ctypes.byref(cd)) if mode == SC_SCORE_FROM_PARTIALS else \
+        L.sc_band_probs_size(ctypes.byref(cd))
+    _min_bytes(_tensor(src, "src", torch.float32), "src", need)
+    scores = torch.empty((desc.B, desc.n), dtype=torch.float32, device=src.device) if scores is None else \
+        _tensor(scores, "scores", torch.float32, (desc.B, desc.n))
     wsb = L.sc_ltp_score_workspace_size(ctypes.byref(cd), mode)
     ws = _ws(wsb, src.device)
     _check(L.sc_ltp_score(ctypes.byref(cd), mode, _ptr(src), _ptr(scores), _ptr(ws), wsb, _stream(stream)),
@@ -185,6 +244,7 @@ def sc_ltp_prune_compact_workspace_size(desc: Desc) -> int:
     return load().sc_ltp_prune_compact_workspace_size(ctypes.byref(desc.c()))
 
 
+@_on_stream
 def sc_ltp_prune_compact(desc: Desc, scores, threshold, keep_global=True, tensors=(), dsts=None, orig_idx_in=None,
                          want_orig=True, outs=None, workspace=None, stream=None):
     """Threshold rule.  Returns (keep_idx, new_len, new_global_pos, orig_idx_out, dsts).
@@ -194,6 +254,7 @@ def sc_ltp_prune_compact(desc: Desc, scores, threshold, keep_global=True, tensor
                           want_orig, outs, workspace, stream)
 
 
+@_on_stream
 def sc_topk_prune_compact(desc: Desc, scores, keep_ratio, keep_global=True, tensors=(), dsts=None, orig_idx_in=None,
                           want_orig=True, outs=None, workspace=None, stream=None):
     """Top-k rule (keep ceil(keep_ratio * candidates) per sequence); same returns as sc_ltp_prune_compact."""
@@ -206,24 +267,35 @@ def _prune_compact(fn, desc, scores, value, keep_global, tensors, dsts, orig_idx
     import torch
     L = load()
     cd = desc.c()
-    dev = scores.device
     B, n, G = desc.B, desc.n, desc.G
+    _tensor(scores, "scores", torch.float32, (B, n))
+    dev = scores.device
     outs = outs or {}
+    for key, shape in (("keep_idx", (B, n)), ("new_len", (B,)), ("new_global_pos", (B, G)),
+                       ("orig_idx_out", (B, n))):
+        if outs.get(key) is not None:
+            _tensor(outs[key], key, torch.int32, shape)
+    if orig_idx_in is not None:
+        _tensor(orig_idx_in, "orig_idx_in", torch.int32, (B, n))
     keep_idx = outs.get("keep_idx") if "keep_idx" in outs else torch.empty((B, n), dtype=torch.int32, device=dev)
     new_len = outs.get("new_len") if "new_len" in outs else torch.empty((B,), dtype=torch.int32, device=dev)
     ngp = outs.get("new_global_pos") if "new_global_pos" in outs else (
         torch.empty((B, G), dtype=torch.int32, device=dev) if G > 0 else None)
     orig_out = outs.get("orig_idx_out") if "orig_idx_out" in outs else (
         torch.empty((B, n), dtype=torch.int32, device=dev) if want_orig else None)
-    tensors = list(tensors)
+    tensors = [_tensor(t, f"tensors[{i}]", leading=(B, n)) for i, t in enumerate(tensors)]
     if dsts is None:
         dsts = [torch.empty_like(t) for t in tensors]
+    if len(dsts) != len(tensors):
+        raise ValueError("dsts: one destination per source tensor")
+    for i, (t, o) in enumerate(zip(tensors, dsts)):
+        _tensor(o, f"dsts[{i}]", t.dtype, tuple(t.shape))
     nt = len(tensors)
     src_arr = (ctypes.c_void_p * max(nt, 1))(*[t.data_ptr() for t in tensors])
     dst_arr = (ctypes.c_void_p * max(nt, 1))(*[t.data_ptr() for t in dsts])
     rb_arr = (ctypes.c_int64 * max(nt, 1))(*[t.numel() * t.element_size() // (B * n) for t in tensors])
     wsb = L.sc_ltp_prune_compact_workspace_size(ctypes.byref(cd))
-    ws = _ws(wsb, dev) if workspace is None else workspace
+    ws = _ws(wsb, dev) if workspace is None else _tensor(workspace, "workspace")
     wsb = wsb if workspace is None else workspace.numel() * workspace.element_size()
     _check(getattr(L, fn)(ctypes.byref(cd), _ptr(scores), ctypes.c_float(value), int(bool(keep_global)), nt, src_arr,
                           dst_arr, rb_arr, _ptr(keep_idx), _ptr(new_len), _ptr(ngp), _ptr(orig_idx_in),
@@ -231,13 +303,18 @@ def _prune_compact(fn, desc, scores, value, keep_global, tensors, dsts, orig_idx
     return keep_idx, new_len, ngp, orig_out, dsts
 
 
+@_on_stream
 def sc_ltp_soft_mask(desc: Desc, scores, theta, temperature, out, keep_global=True, mask=None, y=None,
                      stream=None):
     """Soft mask of LTP's training phase.  Returns (mask [B, n] float32, y = mask * out)."""
     import torch
     L = load()
-    mask = torch.empty((desc.B, desc.n), dtype=torch.float32, device=out.device) if mask is None else mask
-    y = torch.empty_like(out) if y is None else y
+    shape = (desc.B, desc.n, desc.H, desc.d)
+    _tensor(scores, "scores", torch.float32, (desc.B, desc.n))
+    _tensor(out, "out", desc.torch_dtype(), shape)
+    mask = torch.empty((desc.B, desc.n), dtype=torch.float32, device=out.device) if mask is None else \
+        _tensor(mask, "mask", torch.float32, (desc.B, desc.n))
+    y = torch.empty_like(out) if y is None else _tensor(y, "y", desc.torch_dtype(), shape)
     _check(L.sc_ltp_soft_mask(ctypes.byref(desc.c()), _ptr(scores), ctypes.c_float(theta),
                               ctypes.c_float(temperature), int(bool(keep_global)), _ptr(out), _ptr(mask), _ptr(y),
                               _stream(stream)), "sc_ltp_soft_mask")
@@ -248,6 +325,7 @@ def sc_ltp_soft_backward_workspace_size(desc: Desc) -> int:
     return load().sc_ltp_soft_backward_workspace_size(ctypes.byref(desc.c()))
 
 
+@_on_stream
 def sc_ltp_soft_backward(desc: Desc, q, k, v, out, lse, mask, temperature, dy, dmask=None, keep_global=True,
                          grads=None, workspace=None, stream=None):
     """Gradients of the soft-pruned layer.  Returns (dq, dk, dv, dtheta [1] float32 on the device).
@@ -255,12 +333,23 @@ def sc_ltp_soft_backward(desc: Desc, q, k, v, out, lse, mask, temperature, dy, d
     import torch
     L = load()
     cd = desc.c()
+    shape = (desc.B, desc.n, desc.H, desc.d)
+    for t, nm in ((q, "q"), (k, "k"), (v, "v"), (out, "out"), (dy, "dy")):
+        _tensor(t, nm, desc.torch_dtype(), shape)
+    _tensor(lse, "lse", torch.float32, (desc.B, desc.H, desc.n))
+    _tensor(mask, "mask", torch.float32, (desc.B, desc.n))
+    if dmask is not None:
+        _tensor(dmask, "dmask", torch.float32, (desc.B, desc.n))
+    if grads is not None:
+        for t, nm in zip(grads[:3], ("dq", "dk", "dv")):
+            _tensor(t, nm, desc.torch_dtype(), shape)
+        _tensor(grads[3], "dtheta", torch.float32, (1,))
     if grads is None:
         grads = (torch.empty_like(q), torch.empty_like(k), torch.empty_like(v),
                  torch.empty(1, dtype=torch.float32, device=q.device))
     dq, dk, dv, dth = grads
     wsb = L.sc_ltp_soft_backward_workspace_size(ctypes.byref(cd))
-    ws = _ws(wsb, q.device) if workspace is None else workspace
+    ws = _ws(wsb, q.device) if workspace is None else _tensor(workspace, "workspace")
     wsb = wsb if workspace is None else workspace.numel() * workspace.element_size()
     _check(L.sc_ltp_soft_backward(ctypes.byref(cd), _ptr(q), _ptr(k), _ptr(v), _ptr(out), _ptr(lse), _ptr(mask),
                                   ctypes.c_float(temperature), int(bool(keep_global)), _ptr(dy), _ptr(dmask),
@@ -269,19 +358,34 @@ def sc_ltp_soft_backward(desc: Desc, q, k, v, out, lse, mask, temperature, dy, d
     return dq, dk, dv, dth
 
 
+def _stack_args(desc, x_in, x_out, wqkv, wo, thresholds):
+    import torch
+    D = desc.H * desc.d
+    _tensor(x_in, "x_in", torch.bfloat16, (desc.B, desc.n, D))
+    if x_out is not None:
+        _tensor(x_out, "x_out", torch.bfloat16, (desc.B, desc.n, D))
+    if len(wo) != len(wqkv) or len(thresholds) != len(wqkv):
+        raise ValueError("wqkv, wo and thresholds: one per layer")
+    for i in range(len(wqkv)):
+        _tensor(wqkv[i], f"wqkv[{i}]", torch.bfloat16, (D, 3 * D))
+        _tensor(wo[i], f"wo[{i}]", torch.bfloat16, (D, D))
+
+
 def sc_encoder_attn_stack_workspace_size(desc: Desc, n_layers: int) -> int:
     return load().sc_encoder_attn_stack_workspace_size(ctypes.byref(desc.c()), int(n_layers))
 
 
+@_on_stream
 def sc_encoder_attn_stack(desc: Desc, x_in, wqkv, wo, thresholds, keep_global=True, ln_eps=1e-5, x_out=None,
                           workspace=None, stream=None):
     """Returns (x_out, final_len, orig_idx, kept_per_layer)."""
     import torch
     L = load()
     cd = desc.c()
-    dev = x_in.device
     nl = len(wqkv)
     B, n = desc.B, desc.n
+    _stack_args(desc, x_in, x_out, wqkv, wo, thresholds)
+    dev = x_in.device
     x_out = torch.empty_like(x_in) if x_out is None else x_out
     final_len = torch.empty((B,), dtype=torch.int32, device=dev)
     orig = torch.empty((B, n), dtype=torch.int32, device=dev)
@@ -290,7 +394,7 @@ def sc_encoder_attn_stack(desc: Desc, x_in, wqkv, wo, thresholds, keep_global=Tr
     wo_ = (ctypes.c_void_p * nl)(*[w.data_ptr() for w in wo])
     th = (ctypes.c_float * nl)(*[float(t) for t in thresholds])
     wsb = L.sc_encoder_attn_stack_workspace_size(ctypes.byref(cd), nl)
-    ws = _ws(wsb, dev) if workspace is None else workspace
+    ws = _ws(wsb, dev) if workspace is None else _min_bytes(_tensor(workspace, "workspace"), "workspace", wsb)
     _check(L.sc_encoder_attn_stack(ctypes.byref(cd), nl, _ptr(x_in), wq, wo_, th, int(bool(keep_global)),
                                    ctypes.c_float(ln_eps), _ptr(x_out), _ptr(final_len), _ptr(orig), _ptr(kpl),
                                    _ptr(ws), wsb, _stream(stream)), "sc_encoder_attn_stack")
@@ -301,16 +405,24 @@ def sc_encoder_stack_workspace_size(desc: Desc, n_layers: int, ffn_dim: int) -> 
     return load().sc_encoder_stack_workspace_size(ctypes.byref(desc.c()), int(n_layers), int(ffn_dim))
 
 
+@_on_stream
 def sc_encoder_stack(desc: Desc, x_in, wqkv, wo, w1, w2, thresholds, windows=None, keep_global=True, ln_eps=1e-5,
                      x_out=None, workspace=None, stream=None):
     """Full stack (feed-forward block, per-layer windows).  Returns (x_out, final_len, orig_idx, kept_per_layer)."""
     import torch
     L = load()
     cd = desc.c()
-    dev = x_in.device
     nl = len(wqkv)
     B, n = desc.B, desc.n
+    _stack_args(desc, x_in, x_out, wqkv, wo, thresholds)
     F = int(w1[0].shape[1])
+    D = desc.H * desc.d
+    if len(w1) != nl or len(w2) != nl or (windows is not None and len(windows) != nl):
+        raise ValueError("w1, w2 and windows: one per layer")
+    for i in range(nl):
+        _tensor(w1[i], f"w1[{i}]", torch.bfloat16, (D, F))
+        _tensor(w2[i], f"w2[{i}]", torch.bfloat16, (F, D))
+    dev = x_in.device
     x_out = torch.empty_like(x_in) if x_out is None else x_out
     final_len = torch.empty((B,), dtype=torch.int32, device=dev)
     orig = torch.empty((B, n), dtype=torch.int32, device=dev)
@@ -319,7 +431,7 @@ def sc_encoder_stack(desc: Desc, x_in, wqkv, wo, w1, w2, thresholds, windows=Non
     th = (ctypes.c_float * nl)(*[float(t) for t in thresholds])
     win = None if windows is None else (ctypes.c_int32 * nl)(*[int(w) for w in windows])
     wsb = L.sc_encoder_stack_workspace_size(ctypes.byref(cd), nl, F)
-    ws = _ws(wsb, dev) if workspace is None else workspace
+    ws = _ws(wsb, dev) if workspace is None else _min_bytes(_tensor(workspace, "workspace"), "workspace", wsb)
     _check(L.sc_encoder_stack(ctypes.byref(cd), nl, win, _ptr(x_in), arr(wqkv), arr(wo), arr(w1), arr(w2), F, th,
                               int(bool(keep_global)), ctypes.c_float(ln_eps), _ptr(x_out), _ptr(final_len),
                               _ptr(orig), _ptr(kpl), _ptr(ws), wsb, _stream(stream)), "sc_encoder_stack")
@@ -330,9 +442,13 @@ def sc_profile_window_kernel(enable: bool):
     _check(load().sc_profile_window_kernel(int(bool(enable))), "sc_profile_window_kernel")
 
 
-def sc_profile_window_kernel_read():
-    """(total kernel milliseconds, launches) since the last enable/read."""
-    ms = ctypes.c_double(0.0)
+def sc_profile_window_kernel_read(capacity: int = 4096):
+    """Per window-attention call since the last enable/read, in call order: (launch-1 milliseconds, launch-2
+    milliseconds), as two lists."""
+    fwd = (ctypes.c_double * capacity)()
+    cols = (ctypes.c_double * capacity)()
     cnt = ctypes.c_int64(0)
-    _check(load().sc_profile_window_kernel_read(ctypes.byref(ms), ctypes.byref(cnt)), "sc_profile_window_kernel_read")
-    return ms.value, cnt.value
+    _check(load().sc_profile_window_kernel_read(fwd, cols, capacity, ctypes.byref(cnt)),
+           "sc_profile_window_kernel_read")
+    k = min(cnt.value, capacity)
+    return list(fwd[:k]), list(cols[:k])

@@ -630,11 +630,11 @@ sc_status sc_profile_window_kernel(int32_t enable) {
   return SC_OK;
 }
 
-sc_status sc_profile_window_kernel_read(double* total_ms, int64_t* launches) {
-  if (!total_ms || !launches) return SC_EINVAL;
+sc_status sc_profile_window_kernel_read(double* fwd_ms, double* cols_ms, int64_t capacity, int64_t* calls) {
+  if (!calls || capacity < 0 || (capacity > 0 && (!fwd_ms || !cols_ms))) return SC_EINVAL;
   long long cnt = 0;
-  if (sc::profile_read(total_ms, &cnt) != 0) return SC_EHIP;
-  *launches = cnt;
+  if (sc::profile_read(fwd_ms, cols_ms, capacity, &cnt) != 0) return SC_EHIP;
+  *calls = cnt;
   return SC_OK;
 }
 

@@ -1630,26 +1630,21 @@ size_t band_probs_floats(int B, int H, int n, const AttnGeom& g, int G) {
 }
 
 // ------------------------------------------------- benchmark kernel timing
+// While enabled, every window-attention call records three events on its
+// stream: before launch 1, between the launches, after launch 2.
 namespace {
 constexpr int kMaxProfiled = 4096;
 bool g_prof_on = false;
 int g_prof_count = 0;
-hipEvent_t g_prof_ev[2 * kMaxProfiled];
-bool g_prof_created[2 * kMaxProfiled] = {};
+hipEvent_t g_prof_ev[3 * kMaxProfiled];
+bool g_prof_created[3 * kMaxProfiled] = {};
 
-void profile_begin(hipStream_t s) {
+void profile_mark(hipStream_t s, int which) {
   if (!g_prof_on || g_prof_count >= kMaxProfiled) return;
-  const int i = 2 * g_prof_count;
-  for (int j = i; j < i + 2; ++j)
-    if (!g_prof_created[j]) g_prof_created[j] = hipEventCreate(&g_prof_ev[j]) == hipSuccess;
+  const int i = 3 * g_prof_count + which;
+  if (!g_prof_created[i]) g_prof_created[i] = hipEventCreate(&g_prof_ev[i]) == hipSuccess;
   if (g_prof_created[i]) (void)hipEventRecord(g_prof_ev[i], s);
-}
-
-void profile_end(hipStream_t s) {
-  if (!g_prof_on || g_prof_count >= kMaxProfiled) return;
-  const int i = 2 * g_prof_count + 1;
-  if (g_prof_created[i]) (void)hipEventRecord(g_prof_ev[i], s);
-  ++g_prof_count;
+  if (which == 2) ++g_prof_count;
 }
 }  // namespace
 
@@ -1659,17 +1654,19 @@ int profile_set(int enable) {
   return 0;
 }
 
-int profile_read(double* total_ms, long long* launches) {
-  double tot = 0.0;
-  for (int i = 0; i < g_prof_count; ++i) {
-    if (!g_prof_created[2 * i] || !g_prof_created[2 * i + 1]) return -1;
-    if (hipEventSynchronize(g_prof_ev[2 * i + 1]) != hipSuccess) return -1;
-    float ms = 0.f;
-    if (hipEventElapsedTime(&ms, g_prof_ev[2 * i], g_prof_ev[2 * i + 1]) != hipSuccess) return -1;
-    tot += ms;
+int profile_read(double* fwd_ms, double* cols_ms, long long cap, long long* calls) {
+  const int cnt = g_prof_count;
+  for (int i = 0; i < cnt && i < cap; ++i) {
+    for (int j = 0; j < 3; ++j)
+      if (!g_prof_created[3 * i + j]) return -1;
+    if (hipEventSynchronize(g_prof_ev[3 * i + 2]) != hipSuccess) return -1;
+    float a = 0.f, b = 0.f;
+    if (hipEventElapsedTime(&a, g_prof_ev[3 * i], g_prof_ev[3 * i + 1]) != hipSuccess) return -1;
+    if (hipEventElapsedTime(&b, g_prof_ev[3 * i + 1], g_prof_ev[3 * i + 2]) != hipSuccess) return -1;
+    fwd_ms[i] = a;
+    cols_ms[i] = b;
   }
-  *total_ms = tot;
-  *launches = g_prof_count;
+  *calls = cnt;
   g_prof_count = 0;
   return 0;
 }
@@ -1693,15 +1690,16 @@ static hipError_t launch_window_t(const AttnArgs& a0, hipStream_t s) {
   const size_t dyn = sizeof(uint32_t) * ((size_t)a.rwp / 32 + 2 + nxc + 1);
   const unsigned fwd_blocks = (unsigned)(a.n_gr + a.nqb * a.H * a.B);
   const unsigned col_blocks = (unsigned)(a.n_grc + a.n_bcol + a.n_gcol);
-  profile_begin(s);
+  profile_mark(s, 0);
   hipLaunchKernelGGL(k_attn_fwd<DT>, dim3(fwd_blocks), dim3(kThreads), dyn, s, a);
+  profile_mark(s, 1);
   if (col_blocks > 0) {
     if (a.bp_band)
       hipLaunchKernelGGL((k_attn_cols<DT, true>), dim3(col_blocks), dim3(kThreads), 0, s, a);
     else
       hipLaunchKernelGGL((k_attn_cols<DT, false>), dim3(col_blocks), dim3(kThreads), 0, s, a);
   }
-  profile_end(s);
+  profile_mark(s, 2);
   return hipGetLastError();
 }
 

@@ -57,7 +57,7 @@ size_t band_probs_floats(int B, int H, int n, const AttnGeom& g, int G);
 hipError_t launch_window_attention(int dtype, const AttnArgs& a, hipStream_t s);
 // benchmark timing of the window-attention kernel (events on the launch stream)
 int profile_set(int enable);
-int profile_read(double* total_ms, long long* launches);
+int profile_read(double* fwd_ms, double* cols_ms, long long cap, long long* calls);
 hipError_t launch_score_from_partials(const float* partials, const int* valid_len, const int* gpos, int B, int n,
                                       int H, int G, const AttnGeom& g, float* scores, hipStream_t s);
 hipError_t launch_score_from_band(const float* bp, const int* valid_len, const int* gpos, int B, int n, int H, int G,

@@ -9,7 +9,7 @@
 //                totals gives the wave offsets, and a running carry links the
 //                chunks.  Exact and deterministic (integer work only).
 //                Top-k rule (an alternative to the threshold, in the family
-//                of SpAtten's cascade token pruning cited in Sec. 2): each
+//                of SpAtten's cascade token pruning cited in Sec. 3.3): each
 //                sequence keeps its ceil(keep_ratio * C) highest-scored
 //                candidates (C = valid tokens, less the global ones when those
 //                are kept anyway); equal scores go to the lower index.  The

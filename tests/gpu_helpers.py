@@ -4,15 +4,20 @@ running the HIP path through the C ABI, and the comparison rules.
 Tolerances (fixed by the workload specification):
   * float32 outputs (O, LSE): |gpu - oracle| <= 1e-4 * |oracle| + 1e-6 * rms(oracle)
   * bfloat16 outputs (O, hidden states): |gpu - oracle| <= 2e-2
-  * hidden states of full layers (with the feed-forward block): 2e-2 + 2^-7 |oracle|.  The block adds two
-    bf16 storage points (the attention sub-layer output and the GELU activations), so the stored output can
-    land one bf16 step away, and a bf16 step exceeds 2e-2 for values beyond 4 (LayerNorm outputs reach them);
-    2^-7 |v| bounds one step at v
+  * hidden states of the stacks (stored as bf16 after LayerNorm): 2e-2 plus one bf16 step at the oracle's
+    value (the spacing 2^(floor(log2 |v|) - 7)).  The two sides accumulate in different orders, so a value
+    near a rounding midpoint can be stored one bf16 step away, and a bf16 step exceeds 2e-2 for values beyond
+    4 (LayerNorm outputs reach them).  Full layers add two more bf16 storage points (the attention sub-layer output and the GELU
+    activations).  The number of elements beyond 2e-2 is returned for the run's record
   * LSE is computed in float32 in both modes and follows the float32 rule
   * scores (float32 reductions of float32 probabilities from the same inputs):
     |gpu - oracle| <= 1e-5 * |oracle|, exactly 0 beyond the valid length
   * kept-token lists: bit-exact, except tokens whose oracle score lies within
-    1e-6 of the threshold, which are excluded and counted
+    1e-6 of the threshold, which are excluded and counted.  When both sides score
+    the same inputs (single-layer calls), a disagreement is further allowed only
+    where the GPU score, within the score tolerance of the oracle's, can lie on the
+    other side of the threshold: |s_oracle - theta| <= 1e-5 |s_oracle|.  Counts of
+    exclusions and disagreements are asserted and recorded for the run's summary.
 """
 import json
 import os
@@ -29,10 +34,18 @@ import paper_2310_07109_amd as sc  # noqa: E402
 
 DEV = "cuda:0"
 NEAR_THETA = 1e-6
+SCORE_REL = 1e-5
 
 
 def log(msg):
     print(msg, flush=True)
+
+
+def record(msg):
+    """A line for the terminal summary of the run (shown even with -q)."""
+    from conftest import RECORDS
+    RECORDS.append(msg)
+    log(msg)
 
 
 def stored_threshold(cfg_id):
@@ -73,16 +86,23 @@ def run_attention(inp, band=False):
     return res
 
 
-def check_out(gpu, ref, dtype, what="out", bf16_step=False):
-    """bf16_step: allow one bf16 step of the stored value on top (full-layer hidden states)."""
+def check_out(gpu, ref, dtype, what="out", bf16_step=False, count_beyond=None):
+    """bf16_step: allow one bf16 step of the stored value on top (stack hidden states).  count_beyond: a
+    one-element list that receives the number of elements above 2e-2 (within the step)."""
     if dtype == "f32":
         rms = float(np.sqrt(np.mean(ref ** 2))) if ref.size else 0.0
         tol = 1e-4 * np.abs(ref) + 1e-6 * rms
     else:
-        tol = np.full(ref.shape, 2e-2) + (2.0 ** -7 * np.abs(ref) if bf16_step else 0.0)
+        tol = np.full(ref.shape, 2e-2)
+        if bf16_step:
+            a = np.abs(ref)
+            step = np.where(a > 0, np.exp2(np.floor(np.log2(np.where(a > 0, a, 1.0))) - 7), 0.0)
+            tol = tol + step
     err = np.abs(gpu - ref)
     bad = err > tol
     assert not bad.any(), f"{what}: {bad.sum()} elements out of tolerance, max err {err.max():.3g}"
+    if count_beyond is not None:
+        count_beyond[0] += int(np.sum(err > 2e-2))
     return float(err.max()) if err.size else 0.0
 
 
@@ -116,10 +136,12 @@ def keep_sets(keep_idx, new_len):
     return [set(keep_idx[b, :new_len[b]].tolist()) for b in range(len(new_len))]
 
 
-def compare_keep(gpu_keep, gpu_len, ref_scores, theta, valid_len, global_pos, keep_global=True):
-    """Kept lists agree on every token whose oracle score is more than 1e-6 from theta.
-
-    Returns (excluded, disagreements among excluded)."""
+def compare_keep(gpu_keep, gpu_len, ref_scores, theta, valid_len, global_pos, keep_global=True, tag=None,
+                 same_inputs=True):
+    """Kept lists agree on every token whose oracle score is more than 1e-6 from theta; with
+    same_inputs, a disagreement also needs |s_oracle - theta| <= 1e-5 |s_oracle| (the GPU score
+    can then lie across theta).  Returns (excluded, disagreements among excluded); with a tag,
+    the counts go to the run's summary."""
     excluded = disagree = 0
     s32 = ref_scores.astype(np.float32)
     for b in range(len(valid_len)):
@@ -132,8 +154,15 @@ def compare_keep(gpu_keep, gpu_len, ref_scores, theta, valid_len, global_pos, ke
             ref = bool(s32[b, k] > np.float32(theta)) or (keep_global and k in g)
             if abs(ref_scores[b, k] - theta) <= NEAR_THETA and not (keep_global and k in g):
                 excluded += 1
-                disagree += int(ref != (k in kept))
+                if ref != (k in kept):
+                    disagree += 1
+                    assert not same_inputs or abs(ref_scores[b, k] - theta) <= SCORE_REL * abs(ref_scores[b, k]), (
+                        f"seq {b} token {k}: kept lists differ {abs(ref_scores[b, k] - theta):.3g} from theta, "
+                        "beyond what the score tolerance allows")
                 continue
             assert ref == (k in kept), f"seq {b} token {k}: oracle keep={ref}"
         assert all(k < L for k in kept)
+    assert disagree <= excluded
+    if tag is not None:
+        record(f"{tag}: near-theta excluded {excluded} of {int(np.sum(valid_len))} tokens, disagreements {disagree}")
     return excluded, disagree

@@ -6,13 +6,17 @@ whole chain in double precision from the same bf16 inputs and gradients.  Tolera
   * mask: |gpu - oracle| <= 1e-4 (float32 sigmoid of float32 scores that agree to 1e-5 relative, divided
     by a temperature of the order of the score spread);
   * y (bf16): as the attention output, 2e-2;
-  * dq, dk, dv (bf16): every product runs on bf16 operands (dO = bf16(m dy), P and dS rounded to bf16 for
-    the MFMAs, the forward's O stored as bf16), each a relative perturbation of 2^-9 of its terms, and the
-    result is stored as bf16 (2^-9); a handful of such roundings, with the cancellation of dP - D in dS
-    amplifying them a few times, stays within 2^-6 in the norm of each tensor and 2^-5 of its largest
-    element per element;
-  * dtheta: a float32 sum of the score gradients of every token, each perturbed by the bf16 output it
-    is taken against; the terms have both signs, so the bound is 2^-6 of the sum of their magnitudes.
+  * dq, dk, dv (bf16), per element: |gpu - oracle| <= 4 u scale, u = 2^-8 the unit roundoff of bf16 and scale
+    the oracle's error scale of that element (the backward's chain evaluated on magnitudes: every factor by
+    its absolute value, every difference by a sum).  A running error bound: every product of the backward
+    takes bf16 operands, so each term of a gradient element carries at most two rounded factors (dV: P packed
+    and dO = bf16(m dy); dQ, dK: dS packed, whose own inputs dP and D carry the rounding of dO and of the
+    forward's stored O, at most u of their magnitude each), the element is stored as bf16 (u of its value,
+    itself at most its scale), the mask's relative error reaches the score gradient (below 2^-10 here) and
+    float32 accumulation adds n 2^-24 (2^-12 for n = 4096): at most about 3.3 u of the scale in all;
+  * dtheta: |gpu - oracle| <= 2u mtheta, mtheta the oracle's scale of dtheta (the sum over tokens of
+    (sum |dy out| + |dmask|) m (1 - m) / T): each term carries the rounding of the stored O (u), the mask's
+    relative error and float32 accumulation over the tokens.
 """
 import numpy as np
 import pytest
@@ -20,14 +24,15 @@ import torch
 
 import oracle
 import sc_inputs as si
-from gpu_helpers import check_out, dev_i32, log, make_desc, to_dev_storage
+from gpu_helpers import check_out, dev_i32, log, make_desc, record, to_dev_storage
 
 pytestmark = pytest.mark.gpu
 
 import paper_2310_07109_amd as sc  # noqa: E402
 
-NORM_TOL = 2.0 ** -6
-ELEM_TOL = 2.0 ** -5
+U_BF16 = 2.0 ** -8
+GRAD_K = 4.0
+DTH_K = 2.0
 
 CASES = [
     # name, B, n, H, window, G, lengths (None: uniform over range), range, input scale, keep_global
@@ -50,14 +55,15 @@ def _np(t):
     return t.float().cpu().numpy().astype(np.float64)
 
 
-def check_grad(name, gpu, ref):
+def check_grad(name, gpu, ref, scale, tag):
+    """Per element: |gpu - ref| <= GRAD_K * U_BF16 * scale (the oracle's error scale of the element)."""
+    err = np.abs(gpu - ref)
+    bound = GRAD_K * U_BF16 * scale
+    worst = float((err / np.maximum(bound, 1e-300)).max()) if err.size else 0.0
     nr = float(np.linalg.norm(ref))
-    err = float(np.linalg.norm(gpu - ref))
-    emax = float(np.abs(gpu - ref).max()) if ref.size else 0.0
-    amax = float(np.abs(ref).max()) if ref.size else 0.0
-    log(f"  {name}: norm rel err {err / max(nr, 1e-30):.3g}, max err / max {emax / max(amax, 1e-30):.3g}")
-    assert err <= NORM_TOL * nr + 1e-30, (name, err, nr)
-    assert emax <= ELEM_TOL * amax + 1e-30, (name, emax, amax)
+    record(f"{tag} {name}: norm rel err {float(np.linalg.norm(gpu - ref)) / max(nr, 1e-30):.3g}, worst err / "
+           f"(4u scale) {worst:.3g}")
+    assert worst <= 1.0, (name, worst)
 
 
 def run_soft(inp, kg, seed=21, theta_at_globals=False, oracle_rows=None):
@@ -87,35 +93,29 @@ def run_soft(inp, kg, seed=21, theta_at_globals=False, oracle_rows=None):
     sel = [inp[x][rows] for x in ("q64", "k64", "v64")]
     ro, rl, rs, rm, ry = oracle.soft_prune_forward(*sel, vl[rows], gp[rows], inp["window"], inp["alpha"], theta,
                                                    temp, kg)
-    rdq, rdk, rdv, rdth = oracle.soft_prune_backward(*sel, vl[rows], gp[rows], inp["window"], inp["alpha"], theta,
-                                                     temp, dy64[rows], dm[rows].astype(np.float64), kg)
+    rdq, rdk, rdv, rdth, mq, mk, mv, mth = oracle.soft_prune_backward(
+        *sel, vl[rows], gp[rows], inp["window"], inp["alpha"], theta, temp, dy64[rows], dm[rows].astype(np.float64),
+        kg, scales=True)
     gpu = dict(mask=mask.cpu().numpy()[rows], y=_np(y)[rows], dq=_np(dq)[rows], dk=_np(dk)[rows],
                dv=_np(dv)[rows], dth=float(dth.item()))
     if oracle_rows is not None:  # dtheta sums every sequence: compare the sampled sequences' share instead
         gpu["dth"] = None
-    # scale of dtheta's error: the sum of the magnitudes of the terms it adds (it cancels)
-    dmk = (dy64[rows] * ro).sum(axis=(2, 3)) + dm[rows].astype(np.float64)
-    terms = np.abs(dmk * rm * (1.0 - rm)) / temp
-    for i, b in enumerate(rows):
-        terms[i, vl[b]:] = 0.0
-        if kg:
-            for p in gp[b]:
-                if 0 <= p < vl[b]:
-                    terms[i, p] = 0.0
-    ref = dict(mask=rm, y=ry, dq=rdq, dk=rdk, dv=rdv, dth=rdth, dth_abs=float(terms.sum()))
+    ref = dict(mask=rm, y=ry, dq=rdq, dk=rdk, dv=rdv, dth=rdth, mq=mq, mk=mk, mv=mv, mth=mth)
     return gpu, ref
 
 
-def compare(gpu, ref, valid_len):
+def compare(gpu, ref, valid_len, tag):
     assert np.all(np.abs(gpu["mask"] - ref["mask"]) <= 1e-4), float(np.abs(gpu["mask"] - ref["mask"]).max())
     check_out(gpu["y"], ref["y"], "bf16", what="y")
-    for key in ("dq", "dk", "dv"):
-        check_grad(key, gpu[key], ref[key])
+    for key, mkey in (("dq", "mq"), ("dk", "mk"), ("dv", "mv")):
+        check_grad(key, gpu[key], ref[key], ref[mkey], tag)
         for b in range(len(valid_len)):
             assert np.all(gpu[key][b, valid_len[b]:] == 0.0), key
     if gpu["dth"] is not None:
-        log(f"  dtheta gpu {gpu['dth']:.6g} oracle {ref['dth']:.6g} (sum of |terms| {ref['dth_abs']:.6g})")
-        assert abs(gpu["dth"] - ref["dth"]) <= NORM_TOL * ref["dth_abs"] + 1e-6
+        e = abs(gpu["dth"] - ref["dth"])
+        record(f"{tag} dtheta: gpu {gpu['dth']:.7g} oracle {ref['dth']:.7g}, rel err "
+               f"{e / max(abs(ref['dth']), 1e-30):.3g}, err / (2u scale) {e / max(DTH_K * U_BF16 * ref['mth'], 1e-300):.3g}")
+        assert e <= DTH_K * U_BF16 * ref["mth"] + 1e-9
 
 
 @pytest.mark.parametrize("case", CASES, ids=[c[0] for c in CASES])
@@ -128,7 +128,7 @@ def test_soft_small_cases(case):
         inp["valid_len"] = np.array(lens, np.int32)
         inp["global_pos"] = si.global_positions(17, inp["valid_len"], G, "random")
     gpu, ref = run_soft(inp, kg)
-    compare(gpu, ref, inp["valid_len"])
+    compare(gpu, ref, inp["valid_len"], f"soft {name}")
 
 
 def test_soft_global_tokens_on_the_slope():
@@ -142,16 +142,15 @@ def test_soft_global_tokens_on_the_slope():
                    if 0 <= p < inp["valid_len"][b] and 0.05 < m[b, p] < 0.95)
     log(f"  global tokens with 0.05 < mask < 0.95: {on_slope}")
     assert on_slope >= 3
-    compare(gpu, ref, inp["valid_len"])
+    compare(gpu, ref, inp["valid_len"], "soft globals on the slope")
 
 
-def test_soft_config4_sampled_sequences():
-    """The B8 n4096 H12 window-512 32-global workload on the GPU (the launch configuration of the benchmark);
-    three of its sequences (among them the longest) through the oracle."""
+def test_soft_config4_all_sequences():
+    """The B8 n4096 H12 window-512 32-global workload on the GPU (the launch configuration of the benchmark),
+    every sequence through the oracle, dtheta over the whole batch."""
     inp = si.make_attention_inputs(si.CONFIGS[4])
-    rows = [0, 2, 5]
-    gpu, ref = run_soft(inp, 1, oracle_rows=rows)
-    compare(gpu, ref, inp["valid_len"][rows])
+    gpu, ref = run_soft(inp, 1)
+    compare(gpu, ref, inp["valid_len"], "soft config 4")
 
 
 def test_soft_backward_deterministic():

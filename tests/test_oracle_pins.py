@@ -683,8 +683,39 @@ def check_soft_mask_limits():
     assert np.array_equal(y2, out2)
 
 
+def check_soft_backward_error_scales():
+    """The error scales of the backward (the chain on magnitudes) dominate the gradients, and bound the first-order
+    change of every gradient element when every element of dy is perturbed by a relative delta of random sign:
+    dy enters the chain linearly (through m * dy and through the mask gradient sum(dy * out)), so that change is at
+    most delta times the scale."""
+    for seed, kg in ((730, 1), (731, 0)):
+        q, k, v, vl, gp, window, alpha, theta, T, dy, dm, rng = _soft_case(seed)
+        dq, dk, dv, dth, mq, mk, mv, mth = oracle.soft_prune_backward(q, k, v, vl, gp, window, alpha, theta, T, dy,
+                                                                      dm, keep_global=kg, scales=True)
+        for g, m in ((dq, mq), (dk, mk), (dv, mv)):
+            assert np.all(np.abs(g) <= m * (1 + 1e-12) + 1e-300)
+        assert abs(dth) <= mth * (1 + 1e-12)
+        delta = 1e-7
+        sign = rng.choice([-1.0, 1.0], size=dy.shape)
+        sgn_m = rng.choice([-1.0, 1.0], size=dm.shape)
+        # dmask perturbed too: its magnitude is part of the scales
+        g2 = oracle.soft_prune_backward(q, k, v, vl, gp, window, alpha, theta, T, dy * (1 + delta * sign),
+                                        dm * (1 + delta * sgn_m), keep_global=kg)
+        for g, gp2, m in ((dq, g2[0], mq), (dk, g2[1], mk), (dv, g2[2], mv)):
+            assert np.all(np.abs(gp2 - g) <= delta * m * (1 + 1e-6) + 1e-15 * np.abs(g).max()), \
+                float((np.abs(gp2 - g) / np.maximum(delta * m, 1e-300)).max())
+        assert abs(g2[3] - dth) <= delta * mth * (1 + 1e-6) + 1e-12 * abs(dth)
+        # a tighter scale would fail: for dv (a plain sum of P * m * dy) the scale is reached when all signs agree
+        g3 = oracle.soft_prune_backward(q, k, v, vl, gp, window, alpha, theta, T, dy * (1 + delta * np.sign(dy)),
+                                        dm, keep_global=kg)
+        b = 0
+        L = int(vl[b])
+        ratio = np.abs(g3[2][b, :L] - dv[b, :L]) / np.maximum(delta * mv[b, :L], 1e-300)
+        assert ratio.max() > 0.5, float(ratio.max())
+
+
 SOFT_CHECKS = [check_soft_backward_finite_differences, check_soft_backward_against_autograd,
-               check_soft_mask_limits]
+               check_soft_mask_limits, check_soft_backward_error_scales]
 
 ATTENTION_CHECKS = [check_brute_force, check_causal_brute_force, check_causal_dense_is_library_causal_attention,
                     check_window_covers_sequence_is_dense, check_all_global_is_dense,
