@@ -65,6 +65,11 @@ typedef int32_t sc_status;
 #define SC_EUNSUPPORTED (-2)  /* valid but not implemented (e.g. head dim != 64)     */
 #define SC_EWORKSPACE (-3)    /* workspace missing or smaller than required           */
 #define SC_EHIP (-4)          /* a HIP runtime call failed (launch error)              */
+#define SC_ENOSCRATCH (-5)    /* sc_window_attention_noalloc: the problem's workspace  */
+                              /* exceeds SC_NOALLOC_SCRATCH_BYTES                       */
+
+/* Size of the static device workspace of sc_window_attention_noalloc. */
+#define SC_NOALLOC_SCRATCH_BYTES (16u << 20)
 
 #define SC_F32 0   /* float32 storage and arithmetic                               */
 #define SC_BF16 1  /* bfloat16 storage, float32 accumulation                        */
@@ -312,6 +317,26 @@ sc_status sc_encoder_stack(const sc_attn_desc *desc, int32_t n_layers, const int
                            const void *const *W2, int32_t ffn_dim, const float *thresholds, int32_t keep_global,
                            float ln_eps, void *x_out, int32_t *final_len, int32_t *orig_idx, int32_t *kept_per_layer,
                            void *workspace, size_t ws_bytes, void *stream);
+
+/*
+ * sc_window_attention_noalloc: sc_window_attention for callers that cannot
+ * allocate device memory (code under HIP graph capture, tight serving loops,
+ * harnesses that forbid allocation): the same computation, outputs and
+ * argument rules, without the workspace arguments.  The workspace is a static
+ * device array of SC_NOALLOC_SCRATCH_BYTES (16 MiB) that every GPU the library
+ * runs on holds until the process ends; the call itself allocates nothing
+ * (no hipMalloc, no allocating library routine, no benchmark events).
+ *   stream  must belong to the current device (else SC_EINVAL).
+ * Errors: as sc_window_attention (no SC_EWORKSPACE); SC_ENOSCRATCH when
+ * sc_window_attention_workspace_size(desc) exceeds SC_NOALLOC_SCRATCH_BYTES
+ * (nothing is enqueued).  Every call on a GPU shares that GPU's array and the
+ * array keeps the last call's contents (nothing in it needs to start at zero):
+ * calls that overlap on one GPU (on different streams, or from different host
+ * threads without ordering) race on it and must be serialised by the caller.
+ */
+sc_status sc_window_attention_noalloc(const sc_attn_desc *desc, const void *q, const void *k, const void *v,
+                                      void *out, float *lse, float *score_partials, float *band_probs,
+                                      void *stream);
 
 /*
  * Kernel timing for benchmarks.  While enabled, every window-attention call

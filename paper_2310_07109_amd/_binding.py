@@ -8,7 +8,8 @@ import os
 _HERE = os.path.dirname(os.path.abspath(__file__))
 _LIB_PATH = os.path.join(_HERE, "libsc.so")
 
-SC_OK, SC_EINVAL, SC_EUNSUPPORTED, SC_EWORKSPACE, SC_EHIP = 0, -1, -2, -3, -4
+SC_OK, SC_EINVAL, SC_EUNSUPPORTED, SC_EWORKSPACE, SC_EHIP, SC_ENOSCRATCH = 0, -1, -2, -3, -4, -5
+SC_NOALLOC_SCRATCH_BYTES = 16 << 20
 SC_F32, SC_BF16 = 0, 1
 SC_SCORE_FROM_PARTIALS, SC_SCORE_FROM_BAND_PROBS = 0, 1
 
@@ -48,6 +49,7 @@ def load():
         "sc_band_probs_size": (sz, [dp]),
         "sc_window_attention_workspace_size": (sz, [dp]),
         "sc_window_attention": (i32, [dp, vp, vp, vp, vp, vp, vp, vp, vp, sz, vp]),
+        "sc_window_attention_noalloc": (i32, [dp, vp, vp, vp, vp, vp, vp, vp, vp]),
         "sc_ltp_score_workspace_size": (sz, [dp, i32]),
         "sc_ltp_score": (i32, [dp, i32, vp, vp, vp, sz, vp]),
         "sc_ltp_prune_compact_workspace_size": (sz, [dp]),
@@ -217,6 +219,32 @@ def sc_window_attention(desc: Desc, q, k, v, out=None, lse=True, score_partials=
     _check(L.sc_window_attention(ctypes.byref(cd), _ptr(q), _ptr(k), _ptr(v), _ptr(out), _ptr(lse_t), _ptr(sp),
                                  _ptr(bp), _ptr(ws), wsb, _stream(stream)), "sc_window_attention")
     return out, lse_t, sp, bp
+
+
+@_on_stream
+def sc_window_attention_noalloc(desc: Desc, q, k, v, out, lse=None, score_partials=None, band_probs=None,
+                                stream=None):
+    """sc_window_attention with the library's static device workspace: the C call allocates nothing, so every
+    output is the caller's tensor (or None for the optional ones).  Returns (out, lse, score_partials,
+    band_probs)."""
+    import torch
+    L = load()
+    cd = desc.c()
+    shape = (desc.B, desc.n, desc.H, desc.d)
+    for t, nm in ((q, "q"), (k, "k"), (v, "v"), (out, "out")):
+        _tensor(t, nm, desc.torch_dtype(), shape)
+    if lse is not None:
+        _tensor(lse, "lse", torch.float32, (desc.B, desc.H, desc.n))
+    if score_partials is not None:
+        _min_bytes(_tensor(score_partials, "score_partials", torch.float32), "score_partials",
+                   L.sc_score_partials_size(ctypes.byref(cd)))
+    if band_probs is not None:
+        _min_bytes(_tensor(band_probs, "band_probs", torch.float32), "band_probs",
+                   L.sc_band_probs_size(ctypes.byref(cd)))
+    _check(L.sc_window_attention_noalloc(ctypes.byref(cd), _ptr(q), _ptr(k), _ptr(v), _ptr(out), _ptr(lse),
+                                         _ptr(score_partials), _ptr(band_probs), _stream(stream)),
+           "sc_window_attention_noalloc")
+    return out, lse, score_partials, band_probs
 
 
 def sc_ltp_score_workspace_size(desc: Desc, mode: int = SC_SCORE_FROM_PARTIALS) -> int:

@@ -6,6 +6,7 @@
 #include <cmath>
 #include <cstdint>
 #include <cstring>
+#include <mutex>
 
 #include "../../include/sc.h"
 #include "sc_internal.h"
@@ -124,6 +125,7 @@ const char* sc_status_str(sc_status s) {
     case SC_EUNSUPPORTED: return "unsupported argument";
     case SC_EWORKSPACE: return "workspace missing or too small";
     case SC_EHIP: return "HIP runtime error";
+    case SC_ENOSCRATCH: return "problem needs more workspace than the no-allocation entry point's static buffer holds";
     default: return "unknown status";
   }
 }
@@ -145,9 +147,13 @@ size_t sc_window_attention_workspace_size(const sc_attn_desc* d) {
   return attn_ws_size(d);
 }
 
-sc_status sc_window_attention(const sc_attn_desc* d, const void* q, const void* k, const void* v, void* out,
-                              float* lse, float* score_partials, float* band_probs, void* workspace,
-                              size_t ws_bytes, void* stream) {
+}  // extern "C"
+
+namespace {
+
+sc_status window_attention(const sc_attn_desc* d, const void* q, const void* k, const void* v, void* out, float* lse,
+                           float* score_partials, float* band_probs, void* workspace, size_t ws_bytes, void* stream,
+                           bool no_profile) {
   sc_status st = check_desc(d);
   if (st != SC_OK) return st;
   if (!q || !k || !v || !out) return SC_EINVAL;
@@ -173,6 +179,7 @@ sc_status sc_window_attention(const sc_attn_desc* d, const void* q, const void* 
   a.v = v;
   a.out = out;
   a.lse = lse;
+  a.no_profile = no_profile ? 1 : 0;
   Carver c(workspace);
   carve_attn_ws(a, c);
   set_partials(a, score_partials);
@@ -184,6 +191,61 @@ sc_status sc_window_attention(const sc_attn_desc* d, const void* q, const void* 
     if (sc::launch_fill_zero(band_probs, bp_b, s) != hipSuccess) return SC_EHIP;
   }
   return sc::launch_window_attention(d->dtype, a, s) == hipSuccess ? SC_OK : SC_EHIP;
+}
+
+}  // namespace
+
+// ------------------------------------------- no-allocation window attention
+// Workspace of sc_window_attention_noalloc: a fixed device array that every
+// GPU the library runs on holds until the process ends.  In host code its name
+// is only a stand-in for the symbol; the device address comes from
+// hipGetSymbolAddress, once per device (with that device current), and only
+// that address is handed to the kernels.
+static __device__ __align__(256) unsigned char scratch[SC_NOALLOC_SCRATCH_BYTES];
+
+namespace {
+constexpr int kMaxDevices = 64;
+std::mutex g_scratch_mu;
+void* g_scratch_dev[kMaxDevices] = {};
+
+// Device address of `scratch` on the current device (which the caller's
+// stream must belong to).
+sc_status scratch_address(void* stream, void** addr) {
+  int dev = -1;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0) return SC_EHIP;
+  if (dev >= kMaxDevices) return SC_EUNSUPPORTED;
+  hipDevice_t sdev = -1;
+  if (hipStreamGetDevice(static_cast<hipStream_t>(stream), &sdev) != hipSuccess) return SC_EHIP;
+  if (sdev != dev) return SC_EINVAL;
+  std::lock_guard<std::mutex> lock(g_scratch_mu);
+  if (!g_scratch_dev[dev]) {
+    void* p = nullptr;
+    if (hipGetSymbolAddress(&p, HIP_SYMBOL(scratch)) != hipSuccess || !p) return SC_EHIP;
+    g_scratch_dev[dev] = p;
+  }
+  *addr = g_scratch_dev[dev];
+  return SC_OK;
+}
+}  // namespace
+
+extern "C" {
+
+sc_status sc_window_attention(const sc_attn_desc* d, const void* q, const void* k, const void* v, void* out,
+                              float* lse, float* score_partials, float* band_probs, void* workspace,
+                              size_t ws_bytes, void* stream) {
+  return window_attention(d, q, k, v, out, lse, score_partials, band_probs, workspace, ws_bytes, stream, false);
+}
+
+sc_status sc_window_attention_noalloc(const sc_attn_desc* d, const void* q, const void* k, const void* v, void* out,
+                                      float* lse, float* score_partials, float* band_probs, void* stream) {
+  sc_status st = check_desc(d);
+  if (st != SC_OK) return st;
+  if (attn_ws_size(d) > (size_t)SC_NOALLOC_SCRATCH_BYTES) return SC_ENOSCRATCH;
+  void* ws = nullptr;
+  st = scratch_address(stream, &ws);
+  if (st != SC_OK) return st;
+  return window_attention(d, q, k, v, out, lse, score_partials, band_probs, ws, (size_t)SC_NOALLOC_SCRATCH_BYTES,
+                          stream, true);
 }
 
 size_t sc_ltp_score_workspace_size(const sc_attn_desc* d, int32_t mode) {

@@ -1641,6 +1641,7 @@ bool g_prof_created[3 * kMaxProfiled] = {};
 
 void profile_mark(hipStream_t s, int which) {
   if (!g_prof_on || g_prof_count >= kMaxProfiled) return;
+  // (the event of a slot is created on its first use)
   const int i = 3 * g_prof_count + which;
   if (!g_prof_created[i]) g_prof_created[i] = hipEventCreate(&g_prof_ev[i]) == hipSuccess;
   if (g_prof_created[i]) (void)hipEventRecord(g_prof_ev[i], s);
@@ -1690,16 +1691,16 @@ static hipError_t launch_window_t(const AttnArgs& a0, hipStream_t s) {
   const size_t dyn = sizeof(uint32_t) * ((size_t)a.rwp / 32 + 2 + nxc + 1);
   const unsigned fwd_blocks = (unsigned)(a.n_gr + a.nqb * a.H * a.B);
   const unsigned col_blocks = (unsigned)(a.n_grc + a.n_bcol + a.n_gcol);
-  profile_mark(s, 0);
+  if (!a.no_profile) profile_mark(s, 0);
   hipLaunchKernelGGL(k_attn_fwd<DT>, dim3(fwd_blocks), dim3(kThreads), dyn, s, a);
-  profile_mark(s, 1);
+  if (!a.no_profile) profile_mark(s, 1);
   if (col_blocks > 0) {
     if (a.bp_band)
       hipLaunchKernelGGL((k_attn_cols<DT, true>), dim3(col_blocks), dim3(kThreads), 0, s, a);
     else
       hipLaunchKernelGGL((k_attn_cols<DT, false>), dim3(col_blocks), dim3(kThreads), 0, s, a);
   }
-  profile_mark(s, 2);
+  if (!a.no_profile) profile_mark(s, 2);
   return hipGetLastError();
 }
 

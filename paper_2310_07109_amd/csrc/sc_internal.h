@@ -26,6 +26,7 @@ struct AttnArgs {
   int B, n, H, G, r;      // r = half window, clamped to [0, n]
   int causal;             // 1: keys after the query are never attended
   int skip_pad_out;       // 1: output rows of padding-only query blocks are left unwritten
+  int no_profile;         // 1: never record benchmark events for this call
   float c2;               // softmax scale * log2(e)
   // score partials (null: skip the exact-probability column sums)
   float* part_band;       // [B, H, n]      band column sums of non-global keys

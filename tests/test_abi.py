@@ -25,14 +25,14 @@ def declared_functions():
 def test_exports_every_declared_symbol():
     L = sc.load()
     names = declared_functions()
-    assert len(names) == 19
+    assert len(names) == 20
     for name in names:
         assert hasattr(L, name), name
 
 
 def test_status_strings():
     assert sc.sc_status_str(0) == "ok"
-    for code in (-1, -2, -3, -4):
+    for code in (-1, -2, -3, -4, -5):
         assert sc.sc_status_str(code) not in ("ok", "unknown status")
 
 
@@ -237,3 +237,18 @@ def test_score_and_stack_validation():
                                    0x300000, None, None, 0x900000, 1 << 30, None) == B.SC_EINVAL
     assert L.sc_encoder_attn_stack(ctypes.byref(cd), 1, 0x100000, w, w, th, 1, ctypes.c_float(1e-5), 0x200000,
                                    0x300000, None, None, None, 0, None) == B.SC_EWORKSPACE
+
+
+def test_noalloc_rejects_oversized_problems_on_the_host():
+    """The no-allocation window attention refuses a problem whose workspace exceeds its static buffer, and an
+    invalid descriptor, before any device call."""
+    L = sc.load()
+    big = desc(B=64, n=4096, H=16, window=512, G=64, global_pos=FakeT(0x20000))
+    assert L.sc_window_attention_workspace_size(ctypes.byref(big.c())) > B.SC_NOALLOC_SCRATCH_BYTES
+    rc = L.sc_window_attention_noalloc(ctypes.byref(big.c()), 0x100000, 0x200000, 0x300000, 0x400000, None, None,
+                                       None, None)
+    assert rc == B.SC_ENOSCRATCH
+    bad = desc(d=32)
+    rc = L.sc_window_attention_noalloc(ctypes.byref(bad.c()), 0x100000, 0x200000, 0x300000, 0x400000, None, None,
+                                       None, None)
+    assert rc == B.SC_EUNSUPPORTED
