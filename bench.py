@@ -234,7 +234,10 @@ def measure_stack(args, sc, si, torch, np, full, dev="cuda:0"):
         else:
             res["r"] = sc.sc_encoder_attn_stack(d, x, wq, wo, th, x_out=x_out, workspace=ws)
 
-    per, mean_ms, wall_ms = timed(step, args.steps, args.warmup, torch)
+    eager = timed(step, args.steps, args.warmup, torch)
+    replayed = timed(capture(step, torch), args.steps, args.warmup, torch)
+    per, mean_ms, wall_ms = replayed if args.graph else eager
+    per_other = eager[0] if args.graph else replayed[0]
     # the per-layer attention times, in a second run of the same steps
     sc.sc_profile_window_kernel(True)
     timed(step, args.steps, 0, torch)
@@ -276,7 +279,8 @@ def measure_stack(args, sc, si, torch, np, full, dev="cuda:0"):
     t_in0 = float(np.sum(lens_in[0]))
     gemm0 = 2 * t_in0 * D * 3 * D + 2 * float(np.sum(kpl[0])) * D * D
     roof["layer0_gemm_floor_us"] = round(gemm0 / (MFMA_PEAK_TFLOPS["bf16"] * 1e12) * 1e6, 2)
-    out = dict(ms=ms, mean_ms=mean_ms, wall_ms=wall_ms, tokens=tokens, kept_per_layer=[int(np.sum(k)) for k in kpl],
+    out = dict(ms=ms, mean_ms=mean_ms, wall_ms=wall_ms, other_ms=median(per_other), tokens=tokens,
+               kept_per_layer=[int(np.sum(k)) for k in kpl],
                gen_s=gen_s, gflops={k: round(v / 1e9, 2) for k, v in parts.items()},
                total_gflops=round(total / 1e9, 2), roof=roof, layers=layers)
     if not args.no_cpu_baseline:
@@ -430,6 +434,27 @@ def cpu_baseline(run_all, units_all, run_one, units_one, unit, sample_all, sampl
             "cpu_model": cpu_model(), "host_threads": os.cpu_count()}
 
 
+def capture(step, torch):
+    """One step recorded into a HIP graph (torch.cuda.CUDAGraph: stream capture of the library's launches; the
+    library enqueues no memset, copy or synchronisation, and every buffer is preallocated).  Returns a step
+    function that replays it."""
+    side = torch.cuda.Stream()
+    side.wait_stream(torch.cuda.current_stream())
+    with torch.cuda.stream(side):
+        step(None)
+    torch.cuda.current_stream().wait_stream(side)
+    torch.cuda.synchronize()
+    g = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(g):
+        step(None)
+    torch.cuda.synchronize()
+
+    def replay(i):
+        g.replay()
+    replay.graph = g
+    return replay
+
+
 def timed(step, steps, warmup, torch):
     """Runs `warmup` untimed steps, then `steps` timed ones bracketed by synchronisations, with an event on the
     launch stream before every step and after the last.  step(i) gets the step index (None when untimed).
@@ -450,7 +475,7 @@ def timed(step, steps, warmup, torch):
 
 
 def measure(sc, si, torch, np, inp, theta, steps, warmup, dev="cuda:0", keep_ratio=None, causal=False,
-            band=False):
+            band=False, graph=True):
     """Times `steps` steps (window attention with score partials, scores, prune + compaction of O) after
     `warmup` untimed ones.  theta None picks the median score of the valid non-global tokens (about half
     pruned), from one untimed step.  keep_ratio: prune by the top-k rule (sc_topk_prune_compact) instead of
@@ -471,6 +496,8 @@ def measure(sc, si, torch, np, inp, theta, steps, warmup, dev="cuda:0", keep_rat
     lse = torch.empty((B, H, n), dtype=torch.float32, device=dev)
     sp = torch.empty(sc.sc_score_partials_size(d) // 4, dtype=torch.float32, device=dev)
     bp = torch.empty(sc.sc_band_probs_size(d) // 4, dtype=torch.float32, device=dev) if band else None
+    ws_score = torch.empty(max(sc.sc_ltp_score_workspace_size(d, sc.SC_SCORE_FROM_BAND_PROBS), 1),
+                           dtype=torch.uint8, device=dev) if band else None
     ws_attn = torch.empty(max(sc.sc_window_attention_workspace_size(d), 1), dtype=torch.uint8, device=dev)
     scores = torch.empty((B, n), dtype=torch.float32, device=dev)
     oc = torch.empty_like(out)
@@ -502,7 +529,7 @@ def measure(sc, si, torch, np, inp, theta, steps, warmup, dev="cuda:0", keep_rat
         if mark:
             sev[i][0].record()
         if band:
-            sc.sc_ltp_score(d, bp, mode=sc.SC_SCORE_FROM_BAND_PROBS, scores=scores)
+            sc.sc_ltp_score(d, bp, mode=sc.SC_SCORE_FROM_BAND_PROBS, scores=scores, workspace=ws_score)
         else:
             sc.sc_ltp_score(d, sp, scores=scores)
         if mark:
@@ -514,8 +541,12 @@ def measure(sc, si, torch, np, inp, theta, steps, warmup, dev="cuda:0", keep_rat
         if mark:
             sev[i][2].record()
 
-    # the headline: steps bracketed by one event each
-    per, mean_ms, wall_ms = timed(step, steps, warmup, torch)
+    # the headline: steps bracketed by one event each, launched eagerly or (graph) replayed from a HIP graph;
+    # the other mode is timed too
+    eager = timed(step, steps, warmup, torch)
+    replayed = timed(capture(step, torch), steps, warmup, torch)
+    per, mean_ms, wall_ms = replayed if graph else eager
+    per_other = eager[0] if graph else replayed[0]
     # the breakdown, in a second run of the same steps: the window attention's two launches (the library's
     # events) and the score and prune + compaction calls (events between the calls)
     sc.sc_profile_window_kernel(True)
@@ -534,19 +565,22 @@ def measure(sc, si, torch, np, inp, theta, steps, warmup, dev="cuda:0", keep_rat
     # score reduction: read the partials, write the scores; prune + compaction: read the scores, write the kept
     # indices, composed indices and lengths, read and write each kept row of O
     score_bytes = sp.numel() * 4 + 4 * B * n
+    score_kernels = "k_score_from_partials"
     if band:  # the paper's layout: read each valid token's band and global-column entries and the global rows
         r = inp["window"] // 2
         g_used = sum(len([p for p in inp["global_pos"][b] if 0 <= p < inp["valid_len"][b]]) for b in range(B))
         score_bytes = 4 * H * (tokens * (min(2 * r + 1, n)) + 2 * g_used * n) + 4 * B * n
+        score_kernels = "k_band_partials + k_score_from_partials"
     prune_bytes = 4 * B * n * 3 + 2 * sum(kept) * H * dd * 2
     roof = roofline(flops, bytes_, median(fwd), median(cols), pairs,
-                    score=("k_score_from_band" if band else "k_score_from_partials", score_us, score_bytes),
+                    score=(score_kernels, score_us, score_bytes),
                     prune=("k_prune_scan + k_gather_rows", prune_us, prune_bytes))
     return dict(ms=median(per), mean_ms=mean_ms, wall_ms=wall_ms, fwd_ms=median(fwd), cols_ms=median(cols),
-                tokens=tokens, kept=kept, flops=flops, bytes=bytes_, roof=roof, theta=theta, pairs=pairs)
+                tokens=tokens, kept=kept, flops=flops, bytes=bytes_, roof=roof, theta=theta, pairs=pairs,
+                other_ms=median(per_other))
 
 
-def measure_passes(sc, si, torch, np, cfg, steps, warmup, dev="cuda:0"):
+def measure_passes(sc, si, torch, np, cfg, steps, warmup, dev="cuda:0", graph=True):
     """Times `steps` steps of three successive prune passes: each pass runs the window attention with score
     partials, the scores, and the threshold prune + compaction of Q, K and V into the next pass's buffers, with
     the lengths and global positions staying on the device."""
@@ -584,7 +618,10 @@ def measure_passes(sc, si, torch, np, cfg, steps, warmup, dev="cuda:0"):
                                     outs=dict(keep_idx=keep, new_len=lens[p + 1], new_global_pos=gps[p + 1]),
                                     workspace=ws_prune)
 
-    per, mean_ms, wall_ms = timed(step, steps, warmup, torch)
+    eager = timed(step, steps, warmup, torch)
+    replayed = timed(capture(step, torch), steps, warmup, torch)
+    per, mean_ms, wall_ms = replayed if graph else eager
+    per_other = eager[0] if graph else replayed[0]
     # the per-pass attention times, in a second run of the same steps
     sc.sc_profile_window_kernel(True)
     timed(step, steps, 0, torch)
@@ -606,7 +643,7 @@ def measure_passes(sc, si, torch, np, cfg, steps, warmup, dev="cuda:0"):
                            attn_fwd_us=round(median(fwd[p::P]) * 1e3, 2),
                            attn_cols_us=round(median(cols[p::P]) * 1e3, 2)))
     return dict(ms=median(per), mean_ms=mean_ms, wall_ms=wall_ms, tokens=tokens, roof=roof, passes=passes, inp=inp,
-                lens=lens_h, gps=gps_h)
+                lens=lens_h, gps=gps_h, other_ms=median(per_other))
 
 
 def sweep(args, sc, si, torch, np):
@@ -619,7 +656,7 @@ def sweep(args, sc, si, torch, np):
     for kind, n, w in points:
         B = 8 if kind == "window" else 32768 // n
         inp = si.make_attention_inputs(base, B=B, n=n, window=w, len_range=(n // 2, n))
-        m = measure(sc, si, torch, np, inp, None, args.steps, args.warmup)
+        m = measure(sc, si, torch, np, inp, None, args.steps, args.warmup, graph=args.graph)
         print(json.dumps({
             "sweep": kind, "n": n, "window": w, "batch": B, "valid_tokens": m["tokens"],
             "allowed_pairs": m["pairs"], "ms_per_step": round(m["ms"], 4),
@@ -635,6 +672,9 @@ def main():
     ap.add_argument("--steps", type=int, default=50)
     ap.add_argument("--warmup", type=int, default=5)
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--graph", action="store_true",
+                    help="time steps replayed from a HIP graph captured once (default: eager launches; the other "
+                         "mode's time is reported beside it either way)")
     ap.add_argument("--copy-calibration", type=int, default=0, metavar="MIB",
                     help="after the run, copy MIB MiB once on the GPU (a reference kernel of known traffic for "
                          "hardware counters)")
@@ -676,6 +716,7 @@ def main():
     cid, desc = WORKLOADS[args.workload]
     common = {"n_gpus": 1, "steps": args.steps, "warmup": args.warmup, "higher_is_better": True, "scaling": "weak",
               "vs_baseline": None, "dtype": "bf16", "data": "synthetic"}
+    launch = "HIP graph replay (one capture of the step)" if args.graph else "eager launches"
     if cid == "soft":
         m = measure_soft(args, sc, si, torch, np, dev)
         line = {
@@ -695,8 +736,9 @@ def main():
         line = {
             "metric": METRIC, "value": round(m["tokens"] / (m["ms"] * 1e-3), 1), "unit": "kept-token-layers/s",
             **common, "ms_per_step": round(m["ms"], 4), "mean_ms_per_step": round(m["mean_ms"], 4),
+            ("eager_ms_per_step" if args.graph else "graph_replay_ms_per_step"): round(m["other_ms"], 4),
             "config": {"workload": desc, "layer_input_tokens": m["tokens"], "kept_per_layer": m["kept_per_layer"],
-                       "parallelism": "none (1 GPU)"},
+                       "launch": launch, "parallelism": "none (1 GPU)"},
             "model_gflops": m["gflops"], "model_gflops_total": m["total_gflops"], "roofline": m["roof"],
             "layers": m["layers"], "input_generation_s": round(m["gen_s"], 1)}
         if "cpu_baseline" in m:
@@ -706,14 +748,15 @@ def main():
     if args.workload.startswith("passes"):
         cfg = si.CONFIGS[cid]
         t0 = time.time()
-        m = measure_passes(sc, si, torch, np, cfg, args.steps, args.warmup, dev)
+        m = measure_passes(sc, si, torch, np, cfg, args.steps, args.warmup, dev, graph=args.graph)
         gen_s = time.time() - t0
         line = {
             "metric": METRIC, "value": round(m["tokens"] / (m["ms"] * 1e-3), 1), "unit": "kept-token-layers/s",
             **common, "ms_per_step": round(m["ms"], 4), "mean_ms_per_step": round(m["mean_ms"], 4),
             "config": {"workload": desc, "batch": cfg.B, "seq_len": cfg.n, "heads": cfg.H, "head_dim": cfg.d,
                        "window": cfg.window, "global_tokens": cfg.n_global, "thresholds": cfg.thresholds,
-                       "pass_input_tokens": m["tokens"], "parallelism": "none (1 GPU)"},
+                       "pass_input_tokens": m["tokens"], "launch": launch, "parallelism": "none (1 GPU)"},
+            ("eager_ms_per_step" if args.graph else "graph_replay_ms_per_step"): round(m["other_ms"], 4),
             "roofline": m["roof"], "passes": m["passes"], "setup_s": round(gen_s, 1)}
         if not args.no_cpu_baseline:
             import oracle
@@ -748,7 +791,7 @@ def main():
     if args.causal:
         theta = None
     m = measure(sc, si, torch, np, inp, theta, args.steps, args.warmup, dev, keep_ratio=keep_ratio,
-                causal=args.causal, band=args.score == "band")
+                causal=args.causal, band=args.score == "band", graph=args.graph)
     theta = m["theta"]
     ms, tokens = m["ms"], m["tokens"]
     roof = m["roof"]
@@ -765,7 +808,8 @@ def main():
                    "pruning": (f"top-k, keep ratio {keep_ratio}" if keep_ratio is not None else
                                f"threshold {theta}"), "attention": "causal" if args.causal else "bidirectional",
                    "scores": "band layout (paper)" if args.score == "band" else "fused column-sum partials",
-                   "parallelism": "none (1 GPU)"},
+                   "launch": launch, "parallelism": "none (1 GPU)"},
+        ("eager_ms_per_step" if args.graph else "graph_replay_ms_per_step"): round(m["other_ms"], 4),
         "roofline": roof,
         "kept_per_sequence": m["kept"],
         "wall_ms_per_step": round(m["wall_ms"], 4),

@@ -158,6 +158,9 @@ sc_status sc_window_attention(const sc_attn_desc *desc, const void *q, const voi
                               float *lse, float *score_partials, float *band_probs, void *workspace,
                               size_t ws_bytes, void *stream);
 
+/* Workspace of sc_ltp_score: 0 for SC_SCORE_FROM_PARTIALS; for
+ * SC_SCORE_FROM_BAND_PROBS, sc_score_partials_size(desc) bytes (the band layout
+ * is first reduced to the same partials).  0 on an invalid descriptor. */
 size_t sc_ltp_score_workspace_size(const sc_attn_desc *desc, int32_t mode);
 
 /*
@@ -169,6 +172,9 @@ size_t sc_ltp_score_workspace_size(const sc_attn_desc *desc, int32_t mode);
  *   mode  SC_SCORE_FROM_PARTIALS: src = score_partials of sc_window_attention
  *         with the same desc; SC_SCORE_FROM_BAND_PROBS: src = band_probs.
  *   scores  float32 [B, n].
+ *   workspace  device, sc_ltp_score_workspace_size(desc, mode) bytes (may be
+ *         NULL when that is 0); must not overlap src or scores.
+ * Errors: SC_EINVAL (null src or scores, bad mode, overlaps), SC_EWORKSPACE.
  */
 sc_status sc_ltp_score(const sc_attn_desc *desc, int32_t mode, const float *src, float *scores, void *workspace,
                        size_t ws_bytes, void *stream);

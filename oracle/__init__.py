@@ -18,6 +18,7 @@ import numpy as np
 _HERE = os.path.dirname(os.path.abspath(__file__))
 _SRC = os.path.join(_HERE, "sc_oracle.cpp")
 _LIB = os.path.join(_HERE, "liboracle.so")
+_SAN_LIB = os.path.join(_HERE, "liboracle_san.so")
 _lib = None
 
 
@@ -31,12 +32,24 @@ def build(force: bool = True) -> str:
     return _LIB
 
 
+def build_sanitized() -> str:
+    """Compile the oracle with AddressSanitizer and UndefinedBehaviorSanitizer (host code only; every UB report
+    aborts).  Load it by setting SC_ORACLE_LIB to the returned path, with the sanitizer runtimes preloaded."""
+    tmp = _SAN_LIB + ".tmp"
+    subprocess.run(["g++", "-std=c++17", "-O1", "-g", "-fno-omit-frame-pointer", "-fno-fast-math", "-fopenmp",
+                    "-fsanitize=address,undefined", "-fno-sanitize-recover=undefined", "-fPIC", "-shared", _SRC,
+                    "-o", tmp], check=True)
+    os.replace(tmp, _SAN_LIB)
+    return _SAN_LIB
+
+
 def lib():
     global _lib
     if _lib is None:
-        if not os.path.exists(_LIB):
+        path = os.environ.get("SC_ORACLE_LIB") or _LIB
+        if path == _LIB and not os.path.exists(_LIB):
             build()
-        L = ctypes.CDLL(_LIB)
+        L = ctypes.CDLL(path)
         i32p = ctypes.POINTER(ctypes.c_int32)
         f64p = ctypes.POINTER(ctypes.c_double)
         f32p = ctypes.POINTER(ctypes.c_float)

@@ -252,7 +252,7 @@ def sc_ltp_score_workspace_size(desc: Desc, mode: int = SC_SCORE_FROM_PARTIALS) 
 
 
 @_on_stream
-def sc_ltp_score(desc: Desc, src, mode: int = SC_SCORE_FROM_PARTIALS, scores=None, stream=None):
+def sc_ltp_score(desc: Desc, src, mode: int = SC_SCORE_FROM_PARTIALS, scores=None, workspace=None, stream=None):
     import torch
     L = load()
     cd = desc.c()
@@ -262,7 +262,9 @@ def sc_ltp_score(desc: Desc, src, mode: int = SC_SCORE_FROM_PARTIALS, scores=Non
     scores = torch.empty((desc.B, desc.n), dtype=torch.float32, device=src.device) if scores is None else \
         _tensor(scores, "scores", torch.float32, (desc.B, desc.n))
     wsb = L.sc_ltp_score_workspace_size(ctypes.byref(cd), mode)
-    ws = _ws(wsb, src.device)
+    ws = (_ws(wsb, src.device) if wsb > 0 else None) if workspace is None else \
+        _min_bytes(_tensor(workspace, "workspace"), "workspace", wsb)
+    wsb = wsb if workspace is None else workspace.numel() * workspace.element_size()
     _check(L.sc_ltp_score(ctypes.byref(cd), mode, _ptr(src), _ptr(scores), _ptr(ws), wsb, _stream(stream)),
            "sc_ltp_score")
     return scores

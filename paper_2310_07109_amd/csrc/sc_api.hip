@@ -249,28 +249,32 @@ sc_status sc_window_attention_noalloc(const sc_attn_desc* d, const void* q, cons
 }
 
 size_t sc_ltp_score_workspace_size(const sc_attn_desc* d, int32_t mode) {
-  (void)d;
-  (void)mode;
-  return 0;
+  // the band layout is first reduced to the partials of the fused path
+  if (mode != SC_SCORE_FROM_BAND_PROBS || check_desc(d) != SC_OK) return 0;
+  return sc_score_partials_size(d);
 }
 
 sc_status sc_ltp_score(const sc_attn_desc* d, int32_t mode, const float* src, float* scores, void* workspace,
                        size_t ws_bytes, void* stream) {
-  (void)workspace;
-  (void)ws_bytes;
   sc_status st = check_desc(d);
   if (st != SC_OK) return st;
   if (!src || !scores) return SC_EINVAL;
   if (mode != SC_SCORE_FROM_PARTIALS && mode != SC_SCORE_FROM_BAND_PROBS) return SC_EINVAL;
   const size_t src_b = mode == SC_SCORE_FROM_PARTIALS ? sc_score_partials_size(d) : sc_band_probs_size(d);
-  if (overlaps(src, src_b, scores, sizeof(float) * d->B * d->n)) return SC_EINVAL;
+  const size_t sc_b = sizeof(float) * d->B * d->n;
+  if (overlaps(src, src_b, scores, sc_b)) return SC_EINVAL;
+  const size_t need = sc_ltp_score_workspace_size(d, mode);
+  if (need > 0) {
+    if (!workspace || ws_bytes < need) return SC_EWORKSPACE;
+    if (overlaps(workspace, need, src, src_b) || overlaps(workspace, need, scores, sc_b)) return SC_EINVAL;
+  }
   const AttnGeom geo = sc::attn_geom(d->n, d->window, d->G);
   hipStream_t s = static_cast<hipStream_t>(stream);
   hipError_t e = mode == SC_SCORE_FROM_PARTIALS
                      ? sc::launch_score_from_partials(src, d->valid_len, d->global_pos, d->B, d->n, d->H, d->G, geo,
                                                       scores, s)
                      : sc::launch_score_from_band(src, d->valid_len, d->global_pos, d->B, d->n, d->H, d->G, geo,
-                                                  scores, s);
+                                                  static_cast<float*>(workspace), scores, s);
   return e == hipSuccess ? SC_OK : SC_EHIP;
 }
 

@@ -1477,6 +1477,12 @@ struct ScorePartials {
   const float* grow;  // [B, H, ngc, n] column sums over the global rows
   int n, H, G, ngc, nqr;
 };
+// the same pieces, written by k_band_partials
+struct ScorePartialsOut {
+  float* band;
+  float* gcol;
+  float* grow;
+};
 
 // Attention that key k receives from head bh = b * H + h, in two steps
 // applied in this order: score_head_local gives the band column sum plus the
@@ -1561,45 +1567,103 @@ __global__ __launch_bounds__(kScoreKeys * kScoreGroups) void k_score_from_partia
   }
 }
 
-// Paper layout: the score of key k is its band sub-diagonal (entries (i, j)
-// with i - r + j = k), its global column and its entries of the global rows.
-__global__ __launch_bounds__(256) void k_score_from_band(const float* bp, const int* valid_len, const int* gpos,
-                                                          int B, int n, int H, int G, AttnGeom geo, float* scores) {
-  __shared__ int smap[256];
-  const int b = blockIdx.y, kb = blockIdx.x * 256, tid = threadIdx.x, k = kb + tid;
-  const int L = clampi(valid_len[b], 0, n);
-  smap[tid] = -1;
-  __syncthreads();
-  if (gpos)
-    for (int j = tid; j < G; j += 256) {
-      const int p = gpos[(long long)b * G + j];
-      if (p >= kb && p < kb + 256 && p < L) smap[p - kb] = j;
-    }
-  __syncthreads();
-  if (k >= n) return;
-  if (k >= L) {
-    scores[(long long)b * n + k] = 0.f;
-    return;
-  }
+// Paper layout -> the score partials of the fused path, so that the final
+// reduction is k_score_from_partials.  The score of key k is its band
+// sub-diagonal (entries (i, j) with i - r + j = k; zero at global keys), its
+// global column (zero at global rows) and its entries of the global rows.
+//   band blocks    (sequence, head, 256 keys): thread = key; the sub-diagonal
+//                  over the rows that reach the block (for a fixed row, the
+//                  threads read consecutive entries), eight rows in flight
+//                  with their own accumulators; then the global-row entries
+//                  of the key, per 32-slot chunk.
+//   column blocks  (sequence, head, 512-row range): the global-column block
+//                  of the range summed per slot, 8 row groups x 32 slots, the
+//                  row groups added in order through LDS.
+constexpr int kBandKeys = 256;
+constexpr int kBandUnroll = 16;
+
+__global__ __launch_bounds__(256) void k_band_partials(const float* bp, const int* valid_len, int B, int n, int H,
+                                                       int G, AttnGeom geo, ScorePartialsOut po) {
+  __shared__ float red[8][32];
+  const int tid = threadIdx.x;
+  const int nkb = (n + kBandKeys - 1) / kBandKeys;
+  const long long ncol = G > 0 ? (long long)B * H * geo.nqr : 0;
   const float* band = bp;
   const float* gcol = band + (size_t)B * H * n * geo.bw;
   const float* grow = gcol + (size_t)B * H * n * G;
-  const int rb = geo.rb, slot = smap[tid];
-  float acc = 0.f;
-  for (int h = 0; h < H; ++h) {
-    const long long bh = (long long)b * H + h;
-    // walk the rows that can reach this block's keys; for a fixed row the
-    // threads read consecutive band entries (coalesced)
-    const int i_end = min(L, kb + 256 + rb);
-    for (int i = max(0, kb - rb); i < i_end; ++i) {
-      const int j = k - i + rb;
-      if (j >= 0 && j < geo.bw) acc += band[(bh * n + i) * geo.bw + j];
+  if ((long long)blockIdx.x < ncol) {
+    // global-column block (first: it walks its rows in one pass per slot group)
+    const int qr = (int)(blockIdx.x % geo.nqr), bh = (int)(blockIdx.x / geo.nqr), b = bh / H;
+    const int L = clampi(valid_len[b], 0, n);
+    const int rg = tid >> 5, sl = tid & 31;
+    const int r0 = qr * kGlobalKeySpan, r1 = min(L, r0 + kGlobalKeySpan);
+    for (int s0 = 0; s0 < G; s0 += 32) {
+      const int slot = s0 + sl, sc = min(slot, G - 1);  // clamped: in bounds, masked below
+      float acc[kBandUnroll] = {};
+      int i = r0 + rg;
+      for (; i + 8 * (kBandUnroll - 1) < r1; i += 8 * kBandUnroll) {
+#pragma unroll
+        for (int u = 0; u < kBandUnroll; ++u) acc[u] += gcol[((size_t)bh * n + i + 8 * u) * G + sc];
+      }
+      for (int u = 0; i < r1; i += 8, ++u) acc[u] += gcol[((size_t)bh * n + i) * G + sc];
+      float t = 0.f;
+#pragma unroll
+      for (int u = 0; u < kBandUnroll; ++u) t += acc[u];
+      red[rg][sl] = slot < G ? t : 0.f;
+      __syncthreads();
+      if (rg == 0 && slot < G) {
+        float tot = 0.f;
+#pragma unroll
+        for (int j = 0; j < 8; ++j) tot += red[j][sl];
+        po.gcol[((size_t)bh * geo.nqr + qr) * G + slot] = tot;
+      }
+      __syncthreads();
     }
-    if (slot >= 0)
-      for (int i = 0; i < L; ++i) acc += gcol[(bh * n + i) * G + slot];
-    for (int s = 0; s < G; ++s) acc += grow[(bh * G + s) * n + k];
+    return;
   }
-  scores[(long long)b * n + k] = acc / ((float)H * (float)L);
+  // band block: thread = key; each wave walks the rows that reach its own 64
+  // keys
+  const long long blk = blockIdx.x - ncol;
+  const int kb = (int)(blk % nkb), bh = (int)(blk / nkb), b = bh / H;
+  const int L = clampi(valid_len[b], 0, n);
+  const int k = kb * kBandKeys + tid;
+  if (k >= n) return;
+  float sum = 0.f;
+  const int kw = kb * kBandKeys + (tid & ~63);  // first key of the wave
+  if (kw < L) {
+    const int rb = geo.rb, bw = geo.bw;
+    const float* rows = band + (size_t)bh * n * bw;
+    const int i0 = max(0, kw - rb), i1 = min(L, kw + 64 + rb);
+    float acc[kBandUnroll] = {};
+    int i = i0;
+    for (; i + kBandUnroll <= i1; i += kBandUnroll) {
+      // the mask multiplies the loaded value (entries are finite): every load
+      // is used, so none is made conditional and all eight are in flight
+#pragma unroll
+      for (int u = 0; u < kBandUnroll; ++u) {
+        const int j = k - (i + u) + rb;
+        const float v = rows[(size_t)(i + u) * bw + clampi(j, 0, bw - 1)];  // in bounds
+        acc[u] = fmaf(v, (j >= 0 && j < bw) ? 1.f : 0.f, acc[u]);
+      }
+    }
+    for (int u = 0; i < i1; ++i, ++u) {
+      const int j = k - i + rb;
+      const float v = rows[(size_t)i * bw + clampi(j, 0, bw - 1)];
+      acc[u] = fmaf(v, (j >= 0 && j < bw) ? 1.f : 0.f, acc[u]);
+    }
+#pragma unroll
+    for (int u = 0; u < kBandUnroll; ++u) sum += acc[u];
+  }
+  // keys at or beyond L read rows below L only, where their entries are zero
+  po.band[(size_t)bh * n + k] = k < L ? sum : 0.f;
+  for (int c = 0; c < geo.ngc; ++c) {
+    float g = 0.f;
+    if (k < L) {
+      const int s1 = min(G, (c + 1) * kGlobalChunk);
+      for (int sl = c * kGlobalChunk; sl < s1; ++sl) g += grow[((size_t)bh * G + sl) * n + k];
+    }
+    po.grow[((size_t)bh * geo.ngc + c) * n + k] = g;
+  }
 }
 
 }  // namespace
@@ -1739,11 +1803,14 @@ hipError_t launch_score_from_partials(const float* partials, const int* valid_le
 }
 
 hipError_t launch_score_from_band(const float* bp, const int* valid_len, const int* gpos, int B, int n, int H, int G,
-                                  const AttnGeom& g, float* scores, hipStream_t s) {
-  dim3 grid((n + 255) / 256, B);
-  hipLaunchKernelGGL(k_score_from_band, grid, dim3(256), 0, s, bp, valid_len, G > 0 ? gpos : nullptr, B, n, H, G, g,
-                     scores);
-  return hipGetLastError();
+                                  const AttnGeom& g, float* partials, float* scores, hipStream_t s) {
+  ScorePartials sp = score_partials(partials, B, n, H, G, g);
+  ScorePartialsOut po{partials, const_cast<float*>(sp.gcol), const_cast<float*>(sp.grow)};
+  const long long blocks = (long long)B * H * ((n + kBandKeys - 1) / kBandKeys) + (G > 0 ? (long long)B * H * g.nqr : 0);
+  hipLaunchKernelGGL(k_band_partials, dim3((unsigned)blocks), dim3(256), 0, s, bp, valid_len, B, n, H, G, g, po);
+  const hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return e;
+  return launch_score_from_partials(partials, valid_len, gpos, B, n, H, G, g, scores, s);
 }
 
 }  // namespace sc

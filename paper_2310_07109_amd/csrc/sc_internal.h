@@ -62,7 +62,7 @@ int profile_read(double* fwd_ms, double* cols_ms, long long cap, long long* call
 hipError_t launch_score_from_partials(const float* partials, const int* valid_len, const int* gpos, int B, int n,
                                       int H, int G, const AttnGeom& g, float* scores, hipStream_t s);
 hipError_t launch_score_from_band(const float* bp, const int* valid_len, const int* gpos, int B, int n, int H, int G,
-                                  const AttnGeom& g, float* scores, hipStream_t s);
+                                  const AttnGeom& g, float* partials, float* scores, hipStream_t s);
 
 struct PruneArgs {
   const float* scores;     // [B, n]

@@ -19,6 +19,8 @@
 //                scores are ranked in index order by the same block scan.
 // k_gather_rows  one wavefront per output row copies the kept input row with
 //                16-byte lanes (coalesced), for up to four tensors at once.
+#include <algorithm>
+
 #include "sc_device.h"
 #include "sc_internal.h"
 
@@ -233,9 +235,16 @@ __global__ __launch_bounds__(256) void k_gather_rows(GatherArgs a) {
   }
 }
 
+// Zero fill, 16 bytes per thread and store where the buffer allows it.
 __global__ void k_fill_zero(uint32_t* p, long long words) {
   const long long i = (long long)blockIdx.x * blockDim.x + threadIdx.x;
-  if (i < words) p[i] = 0u;
+  if ((reinterpret_cast<uintptr_t>(p) & 15) == 0) {
+    const long long quads = words >> 2;
+    if (i < quads) reinterpret_cast<uint4*>(p)[i] = make_uint4(0u, 0u, 0u, 0u);
+    if (i < (words & 3)) p[4 * quads + i] = 0u;
+  } else if (i < words) {
+    p[i] = 0u;
+  }
 }
 
 __global__ void k_copy_i32(const int* src, int* dst, long long count) {
@@ -267,7 +276,8 @@ hipError_t launch_gather(const GatherArgs& g, hipStream_t s) {
 hipError_t launch_fill_zero(void* p, size_t bytes, hipStream_t s) {
   const long long words = (long long)(bytes / 4);
   if (words <= 0) return hipSuccess;
-  hipLaunchKernelGGL(k_fill_zero, dim3((unsigned)((words + 255) / 256)), dim3(256), 0, s, static_cast<uint32_t*>(p),
+  const long long threads = (reinterpret_cast<uintptr_t>(p) & 15) == 0 ? std::max(words >> 2, 3LL) : words;
+  hipLaunchKernelGGL(k_fill_zero, dim3((unsigned)((threads + 255) / 256)), dim3(256), 0, s, static_cast<uint32_t*>(p),
                      words);
   return hipGetLastError();
 }
