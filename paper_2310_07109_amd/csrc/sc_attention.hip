@@ -307,6 +307,79 @@ SC_DEV int win_tables(const AttnArgs& a, const WinBlock& wb, uint32_t* sBits, in
   return wb.nkt + *sNx;
 }
 
+// The same tables when the block has at most 64 global slots, built by wave 0
+// alone from one position per lane (p, loaded by the caller): the in-band
+// bitmask (zeroed, then or-ed: the LDS operations of one wave take effect in
+// program order) and the out-of-band positions compacted in slot order into
+// sPos[0 .. *sCnt), with *sNx = 1 when there are any (chunk 0).  One barrier.
+SC_DEV int win_tables_small(const AttnArgs& a, const WinBlock& wb, int p, int w, int lane, uint32_t* sBits,
+                            int* sXList, int* sNx, int* sPos, int* sCnt) {
+  if (w == 0) {
+    for (int i = lane; i < wb.nwords; i += 64) sBits[i] = 0u;
+    if (p >= wb.kt0 && p < wb.kt1) atomicOr(&sBits[(p - wb.kt0) >> 5], 1u << ((p - wb.kt0) & 31));
+    const bool oob = p >= 0 && p < wb.L && (p < wb.kt0 || (!a.causal && p >= wb.kt1));
+    const unsigned long long m = __ballot(oob);
+    const int rank = __builtin_amdgcn_mbcnt_hi((uint32_t)(m >> 32), __builtin_amdgcn_mbcnt_lo((uint32_t)m, 0u));
+    if (oob) sPos[rank] = p;
+    if (lane == 0) {
+      *sNx = m != 0ull ? 1 : 0;
+      *sCnt = __popcll(m);
+      sXList[0] = 0;
+    }
+  }
+  __syncthreads();
+  return wb.nkt + *sNx;
+}
+
+// win_tables for the bf16 window blocks, which also compacts the first
+// listed chunk: its out-of-band global positions, in slot order, go to
+// sPos[0 .. *sCnt).  The wave whose threads loaded that chunk's slots does it
+// from registers (no second load of the positions); a first chunk beyond the
+// workgroup's first kThreads slots is loaded again by wave 0.  Contains
+// barriers; call with q0 < L.
+SC_DEV int win_tables2(const AttnArgs& a, const WinBlock& wb, uint32_t* sBits, int* sXList, int* sNx, int* sPos,
+                       int* sCnt) {
+  const int tid = threadIdx.x;
+  const int* gp = wb.nxc ? a.gpos + (long long)wb.b * a.G : nullptr;
+  const int G = gp ? a.G : 0;
+  const int p_first = tid < G ? gp[tid] : -1;  // in flight with the caller's loads
+  auto out_of_band = [&](int p) { return p >= 0 && p < wb.L && (p < wb.kt0 || (!a.causal && p >= wb.kt1)); };
+  for (int i = tid; i < wb.nwords; i += kThreads) sBits[i] = 0u;
+  for (int i = tid; i < wb.nxc; i += kThreads) sXList[i] = 0;
+  __syncthreads();
+  for (int j = tid; j < G; j += kThreads) {
+    const int p = j == tid ? p_first : gp[j];
+    if (p >= wb.kt0 && p < wb.kt1)
+      atomicOr(&sBits[(p - wb.kt0) >> 5], 1u << ((p - wb.kt0) & 31));
+    else if (out_of_band(p))  // causal: later keys are never attended
+      sXList[j / kBK] = 1;
+  }
+  __syncthreads();
+  if (tid == 0) {
+    int m = 0;
+    for (int c = 0; c < wb.nxc; ++c)
+      if (sXList[c]) sXList[m++] = c;
+    *sNx = m;
+  }
+  __syncthreads();
+  const int nx = *sNx;
+  if (nx > 0) {
+    const int c0 = sXList[0];
+    constexpr int kRegChunks = kThreads / kBK;  // chunks whose slots the workgroup's threads loaded
+    if ((tid >> 6) == (c0 < kRegChunks ? c0 : 0)) {
+      const int j = kBK * c0 + (tid & 63);
+      const int p = c0 < kRegChunks ? p_first : (j < G ? gp[j] : -1);  // p_first is gp[j] when c0 < kRegChunks
+      const bool use = out_of_band(p);
+      const unsigned long long m = __ballot(use);
+      const int rank = __builtin_amdgcn_mbcnt_hi((uint32_t)(m >> 32), __builtin_amdgcn_mbcnt_lo((uint32_t)m, 0u));
+      if (use) sPos[rank] = p;
+      if ((tid & 63) == 0) *sCnt = __popcll(m);
+    }
+    __syncthreads();
+  }
+  return wb.nkt + nx;
+}
+
 // Tile loader of pass 1: band tiles are contiguous key ranges, global-slot
 // tiles gather the rows of global keys outside the band.
 template <int DT>
@@ -625,7 +698,10 @@ SC_DEV void tile_dma(const __bf16* g, unsigned ld_bytes, __bf16* tile, int w, in
   for (int j = 0; j < 2; ++j) {
     const int R0 = 16 * w + 8 * j, R = R0 + (lane >> 3);
     const unsigned u = (lane & 7) ^ (lane >> 3);  // slot (lane & 7) of row R holds unit slot ^ (R & 7)
-    lds_dma16(g, (unsigned)rowfn(R) * ld_bytes + 16u * u, lds_addr(tile + R0 * Tr<1>::kPitch));
+    // the LDS base is the same for the whole wave; readfirstlane lets the
+    // compiler keep it in a scalar register when it derives from a loaded value
+    lds_dma16(g, (unsigned)rowfn(R) * ld_bytes + 16u * u,
+              __builtin_amdgcn_readfirstlane(lds_addr(tile + R0 * Tr<1>::kPitch)));
   }
 }
 
@@ -635,14 +711,16 @@ SC_DEV void tile_dma(const __bf16* g, unsigned ld_bytes, __bf16* tile, int w, in
 // 16 st + 4g + i).  Disallowed logits become -inf, which exp2 maps to 0
 // (c2 > 0 is guaranteed by the host).
 // S^T = K Q^T of one 64-key tile for both sub-blocks; dead sub-tiles give 0.
-template <bool kMasked>
+// kNst: the tile's first kNst 16-key sub-tiles are computed (4: the whole
+// tile; 2: keys 0..31, for gathered global keys that fill half a tile).
+template <bool kMasked, int kNst = 4>
 SC_DEV void qk_tile2(const bf16x8 (&qf)[kSub1][2], const __bf16* sK, int lr_in, int g_in, unsigned live,
                      f32x4 (&s)[kSub1][4]) {
   using TR = Tr<1>;
   auto is_live = [&](int st) { return !kMasked || ((live >> st) & 1u); };
   const int lr = lr_in, g = g_in;
 #pragma unroll
-  for (int st = 0; st < 4; ++st) {
+  for (int st = 0; st < kNst; ++st) {
 #pragma unroll
     for (int j = 0; j < kSub1; ++j) s[j][st] = f32x4{0.f, 0.f, 0.f, 0.f};
     if (is_live(st)) {
@@ -658,28 +736,47 @@ SC_DEV void qk_tile2(const bf16x8 (&qf)[kSub1][2], const __bf16* sK, int lr_in, 
 }
 
 // Row maxima of a tile in log2 units (per sub-block).
-SC_DEV void tile_max2(const f32x4 (&s)[kSub1][4], float c2, float (&tmax)[kSub1]) {
+// Maxima of the lane's own logits of a tile (raw, unscaled), per sub-block.
+// (a tree of three-input maxima: 8 for 16 values, 4 for 8)
+template <int kNst = 4>
+SC_DEV void lane_max2(const f32x4 (&s)[kSub1][4], float (&lmax)[kSub1]) {
+  auto max3 = [](float a, float b, float c) { return vmax(vmax(a, b), c); };
 #pragma unroll
   for (int j = 0; j < kSub1; ++j) {
-    float m4[4];
+    float v[16];
 #pragma unroll
-    for (int st = 0; st < 4; ++st) m4[st] = vmax(vmax(s[j][st][0], s[j][st][1]), vmax(s[j][st][2], s[j][st][3]));
-    tmax[j] = group_max(vmax(vmax(m4[0], m4[1]), vmax(m4[2], m4[3]))) * c2;
+    for (int st = 0; st < kNst; ++st)
+#pragma unroll
+      for (int i = 0; i < 4; ++i) v[4 * st + i] = s[j][st][i];
+    if constexpr (kNst == 4) {
+      const float r0 = max3(v[0], v[1], v[2]), r1 = max3(v[3], v[4], v[5]), r2 = max3(v[6], v[7], v[8]);
+      const float r3 = max3(v[9], v[10], v[11]), r4 = max3(v[12], v[13], v[14]);
+      lmax[j] = vmax(max3(r0, r1, r2), max3(r3, r4, v[15]));
+    } else {
+      lmax[j] = max3(max3(v[0], v[1], v[2]), max3(v[3], v[4], v[5]), vmax(v[6], v[7]));
+    }
   }
 }
 
-// Whether any lane's running max must be raised (tile max above it by kTau).
-SC_DEV bool need_raise2(const float (&tmax)[kSub1], const float (&m_use)[kSub1]) {
+// Whether any lane's running max must be raised: some logit of the lane's
+// own keys above the running max by kTau.  The running max of a query is the
+// same in the 4 lane groups that hold its keys, so the lane's own maximum
+// decides; only a raise needs the maximum over the groups (raise2).
+SC_DEV bool need_raise2(const float (&lmax)[kSub1], const float (&m_use)[kSub1], float c2) {
   bool up = false;
 #pragma unroll
-  for (int j = 0; j < kSub1; ++j) up |= tmax[j] > m_use[j] + kTau;
+  for (int j = 0; j < kSub1; ++j) up |= lmax[j] * c2 > m_use[j] + kTau;
   return __builtin_amdgcn_ballot_w64(up) != 0ull;
 }
 
 // Raises the running maxima that need it and rescales their sums and
-// accumulators (lanes that do not need it scale by 1).
-SC_DEV void raise2(const float (&tmax)[kSub1], float (&m_use)[kSub1], float (&l_run)[kSub1],
+// accumulators (lanes that do not need it scale by 1).  lmax: the lanes' own
+// maxima; the tile maximum of a query is taken over its 4 lane groups here.
+SC_DEV void raise2(const float (&lmax)[kSub1], float c2, float (&m_use)[kSub1], float (&l_run)[kSub1],
                    f32x4 (&o)[kSub1][4]) {
+  float tmax[kSub1];
+#pragma unroll
+  for (int j = 0; j < kSub1; ++j) tmax[j] = group_max(lmax[j]) * c2;
 #pragma unroll
   for (int j = 0; j < kSub1; ++j) {
     const bool up = tmax[j] > m_use[j] + kTau;
@@ -692,7 +789,7 @@ SC_DEV void raise2(const float (&tmax)[kSub1], float (&m_use)[kSub1], float (&l_
 }
 
 // P = exp2(S c2 - m) (summed into l) and O^T += V^T P^T for one tile.
-template <bool kMasked>
+template <bool kMasked, int kNst = 4>
 SC_DEV void pv_tile2(const f32x4 (&s)[kSub1][4], const __bf16* sV, float c2, int, int, const float (&m_use)[kSub1],
                      float (&l_run)[kSub1], f32x4 (&o)[kSub1][4], unsigned live) {
   using TR = Tr<1>;
@@ -703,7 +800,7 @@ SC_DEV void pv_tile2(const f32x4 (&s)[kSub1][4], const __bf16* sV, float c2, int
   for (int j = 0; j < kSub1; ++j) {
     float part[4];
 #pragma unroll
-    for (int st = 0; st < 4; ++st) {
+    for (int st = 0; st < kNst; ++st) {
       float p[4];
 #pragma unroll
       for (int i = 0; i < 4; ++i) p[i] = fast_exp2(fmaf(s[j][st][i], c2, -m_use[j]));
@@ -711,13 +808,13 @@ SC_DEV void pv_tile2(const f32x4 (&s)[kSub1][4], const __bf16* sV, float c2, int
 #pragma unroll
       for (int i = 0; i < 4; ++i) pb[j][st >> 1][4 * (st & 1) + i] = (__bf16)p[i];
     }
-    l_run[j] += (part[0] + part[1]) + (part[2] + part[3]);
+    l_run[j] += kNst == 4 ? (part[0] + part[1]) + (part[2] + part[3]) : part[0] + part[1];
   }
   // O^T += V^T P^T: the V operand comes from transposed reads of the
   // row-major tile; lane (g, lr) supplies dims 16dt + 4(lr&3) .. +3 of rows
   // 32kc + 4g + lr/4 and 32kc + 16 + 4g + lr/4 (keys in MFMA order)
 #pragma unroll
-  for (int kc = 0; kc < 2; ++kc) {
+  for (int kc = 0; kc < kNst / 2; ++kc) {
     if (!is_live(2 * kc) && !is_live(2 * kc + 1)) continue;
     const int vr = 32 * kc + 4 * g + (lr >> 2), b = (lr >> 1) & 1, e = 4 * (lr & 1);
 #pragma unroll
@@ -737,25 +834,25 @@ SC_DEV void pv_tile2(const f32x4 (&s)[kSub1][4], const __bf16* sV, float c2, int
 // 16 st + 4g + i).  Disallowed logits become -inf, which exp2 maps to 0
 // (c2 > 0 is guaranteed by the host).  The running max is raised only when
 // the tile max exceeds it by kTau (for the whole wave when any lane needs it).
-template <bool kMasked, typename OkFn>
+template <bool kMasked, typename OkFn, int kNst = 4>
 SC_DEV void softmax_tile2(const bf16x8 (&qf)[kSub1][2], const __bf16* sK, const __bf16* sV, float c2, int lr,
                           int g, float (&m_use)[kSub1], float (&l_run)[kSub1], f32x4 (&o)[kSub1][4], unsigned live,
                           OkFn ok) {
   f32x4 s[kSub1][4];
-  qk_tile2<kMasked>(qf, sK, lr, g, live, s);
+  qk_tile2<kMasked, kNst>(qf, sK, lr, g, live, s);
   if constexpr (kMasked) {
 #pragma unroll
     for (int j = 0; j < kSub1; ++j)
 #pragma unroll
-      for (int st = 0; st < 4; ++st)
+      for (int st = 0; st < kNst; ++st)
 #pragma unroll
         for (int i = 0; i < 4; ++i)
           s[j][st][i] = (((live >> st) & 1u) && ok(j, st, i)) ? s[j][st][i] : -INFINITY;
   }
-  float tmax[kSub1];
-  tile_max2(s, c2, tmax);
-  if (need_raise2(tmax, m_use)) raise2(tmax, m_use, l_run, o);
-  pv_tile2<kMasked>(s, sV, c2, lr, g, m_use, l_run, o, live);
+  float lmax[kSub1];
+  lane_max2<kNst>(s, lmax);
+  if (need_raise2(lmax, m_use, c2)) raise2(lmax, c2, m_use, l_run, o);
+  pv_tile2<kMasked, kNst>(s, sV, c2, lr, g, m_use, l_run, o, live);
 }
 
 // Pass 1 for bf16: O, LSE and the log2 LSE of the block's kBQ2 queries.
@@ -794,8 +891,11 @@ SC_DEV void window_fwd_v2(const AttnArgs& a, int blk, Smem<1>& sm, uint32_t* sDy
   uint32_t* sBits = sDyn;
   int* sXList = reinterpret_cast<int*>(sDyn + a.rwp / 32 + 2);
   auto band_rows = [&](int k0) { return [=](int R) { return min(k0 + R, kt1 - 1); }; };
-  // the first K/V tile, the query fragments and the global positions (read
-  // by win_tables) are in flight together
+  // the global positions (up to 64 slots: one per lane of wave 0), the first
+  // K/V tile and the query fragments are in flight together
+  const bool small_g = a.G <= kBK;
+  const int* gpb = wb.nxc ? a.gpos + (long long)wb.b * a.G : nullptr;
+  const int p_lane = (small_g && gpb && w == 0 && lane < a.G) ? gpb[lane] : -1;
   tile_dma(Kg, ldb, sm.b[0], w, lane, band_rows(kt0));
   tile_dma(Vg, ldb, sm.c[0], w, lane, band_rows(kt0));
   // query fragments straight from HBM (rows clamped below L; same dims per
@@ -809,11 +909,46 @@ SC_DEV void window_fwd_v2(const AttnArgs& a, int blk, Smem<1>& sm, uint32_t* sDy
     qf[j][0] = *reinterpret_cast<const bf16x8*>(qrow + 8 * g);
     qf[j][1] = *reinterpret_cast<const bf16x8*>(qrow + 32 + 8 * g);
   }
-  const int ntile = win_tables(a, wb, sBits, sXList, &sm.misc[0]);
+  // bitmask of in-band global keys, the list of 64-slot chunks with keys
+  // outside [kt0, kt1), and the first listed chunk compacted into sm.pos[1]
+  const int ntile = small_g ? win_tables_small(a, wb, p_lane, w, lane, sBits, sXList, &sm.misc[0], sm.pos[1],
+                                               &sm.misc[2])
+                            : win_tables2(a, wb, sBits, sXList, &sm.misc[0], sm.pos[1], &sm.misc[2]);
+  const int nx = __builtin_amdgcn_readfirstlane(ntile - nkt);  // block-uniform (read from LDS)
+  const bool hasg = nx > 0;
   auto gbit = [&](int k) -> bool {
     const int o = k - kt0;
     return (sBits[o >> 5] >> (o & 31)) & 1u;
   };
+  // Global keys outside the block's key range, one 64-slot chunk of the
+  // global list per tile, compacted (used slots first, in slot order) so that
+  // they fill the first rows of the tile.  gather_chunk (further chunks, G >
+  // 64) compacts chunk c into sm.pos[buf] (a barrier) and gathers its rows.
+  const int* gp = wb.nxc ? a.gpos + (long long)wb.b * a.G : nullptr;
+  auto slot_row = [&](int c, int row) {
+    const int j = kBK * c + row;
+    const int p = j < a.G ? gp[j] : -1;
+    return (p >= 0 && p < L && (p < kt0 || (!causal && p >= kt1))) ? p : -1;
+  };
+  auto gather_rows = [&](int buf, int cnt) {
+    auto rows = [&](int R) { return R < cnt ? sm.pos[buf][R] : kt0; };
+    tile_dma(Kg, ldb, sm.b[buf], w, lane, rows);
+    tile_dma(Vg, ldb, sm.c[buf], w, lane, rows);
+  };
+  auto gather_chunk = [&](int c, int buf) -> int {
+    if (tid < kBK) {  // wave 0: one slot per lane
+      const int p = slot_row(c, tid);
+      const unsigned long long m = __ballot(p >= 0);
+      const int rank = __builtin_amdgcn_mbcnt_hi((uint32_t)(m >> 32), __builtin_amdgcn_mbcnt_lo((uint32_t)m, 0u));
+      if (p >= 0) sm.pos[buf][rank] = p;
+      if (tid == 0) sm.misc[1 + buf] = __popcll(m);
+    }
+    __syncthreads();
+    const int cnt = sm.misc[1 + buf];
+    gather_rows(buf, cnt);
+    return cnt;
+  };
+  const int gcnt0 = hasg ? sm.misc[2] : 0;
   float m_use[kSub1], l_run[kSub1];
   f32x4 o[kSub1][4];
 #pragma unroll
@@ -829,6 +964,17 @@ SC_DEV void window_fwd_v2(const AttnArgs& a, int blk, Smem<1>& sm, uint32_t* sDy
   __builtin_amdgcn_s_waitcnt(0x0F70);  // vmcnt(0)
   wait_dma();
   __syncthreads();
+  // a gathered chunk: every query of the block attends its first cnt keys
+  // (out-of-band global keys; in the causal variant only those before the
+  // block are listed); half a tile when they fit in 32 rows
+  auto glob_tile = [&](int buf, int cnt) {
+    const unsigned live = (cnt > 0 ? 1u : 0u) | (cnt > 16 ? 2u : 0u) | (cnt > 32 ? 4u : 0u) | (cnt > 48 ? 8u : 0u);
+    auto ok = [&](int, int st, int i) { return 16 * st + 4 * g + i < cnt; };
+    if (cnt <= 32)
+      softmax_tile2<true, decltype(ok), 2>(qf, sm.b[buf], sm.c[buf], a.c2, lr, g, m_use, l_run, o, live, ok);
+    else
+      softmax_tile2<true, decltype(ok), 4>(qf, sm.b[buf], sm.c[buf], a.c2, lr, g, m_use, l_run, o, live, ok);
+  };
 
   // per-lane band bounds of sub-block j relative to a tile start, shifted by
   // the lane group's key offset 4g: key 16st + i of the lane is allowed when
@@ -840,14 +986,22 @@ SC_DEV void window_fwd_v2(const AttnArgs& a, int blk, Smem<1>& sm, uint32_t* sDy
     lo[j] = q - r - 4 * g;
     hi[j] = min(q + rh, kt1 - 1) - 4 * g;
   }
-  // every tile step: load the next tile into the other buffer, compute,
-  // wait for the load, barrier (the same sequence in all three phases below)
+  // Pipeline steps: band tile 0, then (hasg) the first gathered global chunk,
+  // then band tiles 1 .. nkt-1; step s computes from buffer s & 1 while the
+  // next step's data arrive in the other.  Band tile t therefore lives in
+  // buffer t & 1, or (t + 1) & 1 after the global chunk.
+  const int par = hasg ? 1 : 0;
+  auto bufof = [&](int t) { return (t + (t > 0 ? par : 0)) & 1; };
+  auto load_band = [&](int t) {
+    const int k1 = kt0 + t * kBK;
+    tile_dma(Kg, ldb, sm.b[bufof(t)], w, lane, band_rows(k1));
+    tile_dma(Vg, ldb, sm.c[bufof(t)], w, lane, band_rows(k1));
+  };
+  // every tile step: load the next step's data into the other buffer,
+  // compute, wait for the load, barrier (the same sequence in all three
+  // phases below; band tile 0 and the global chunk are peeled off)
   auto issue = [&](int t) {
-    if (t + 1 < nkt) {
-      const int k1 = kt0 + (t + 1) * kBK;
-      tile_dma(Kg, ldb, sm.b[(t + 1) & 1], w, lane, band_rows(k1));
-      tile_dma(Vg, ldb, sm.c[(t + 1) & 1], w, lane, band_rows(k1));
-    }
+    if (t + 1 < nkt) load_band(t + 1);
   };
   auto finish = [&](int t) {
     if (t + 1 < nkt) wait_dma();
@@ -855,7 +1009,7 @@ SC_DEV void window_fwd_v2(const AttnArgs& a, int blk, Smem<1>& sm, uint32_t* sDy
   };
   // tiles that need a mask (band edges, global keys) or are skipped
   auto edge_tile = [&](int t) {
-    const int buf = t & 1, k0 = kt0 + t * kBK;
+    const int buf = bufof(t), k0 = kt0 + t * kBK;
     const unsigned long long gall = tile_gmask(sBits, t, wb.nwords);
     const bool near = k0 <= qa + kWQ - 1 + rh && k0 + kBK - 1 >= qa - r;
     if (!near && gall == 0ull) return;
@@ -900,17 +1054,40 @@ SC_DEV void window_fwd_v2(const AttnArgs& a, int blk, Smem<1>& sm, uint32_t* sDy
   // keys), so no mask is needed
   const int ia = clampi(-((kt0 - (qa + kWQ - 1 - r)) >> 6), 0, nkt);
   const int ib = clampi(((min(qa + rh, kt1 - 1) - (kBK - 1) - kt0) >> 6) + 1, ia, nkt);
-  int t = 0;
+  auto interior_tile = [&](int t) {
+    const int buf = bufof(t);
+    softmax_tile2<false>(qf, sm.b[buf], sm.c[buf], a.c2, lr, g, m_use, l_run, o, 0xFu,
+                         [](int, int, int) { return true; });
+  };
+  // step 0: band tile 0 (interior for this wave only when ia == 0 < ib)
+  // while the global chunk's gather (or band tile 1) arrives
+  if (hasg)
+    gather_rows(1, gcnt0);
+  else
+    issue(0);
+  if (ia == 0 && ib > 0)
+    interior_tile(0);
+  else
+    edge_tile(0);
+  if (hasg || nkt > 1) wait_dma();
+  __syncthreads();
+  // step 1 (hasg): the gathered global chunk while band tile 1 arrives
+  if (hasg) {
+    if (nkt > 1) load_band(1);
+    glob_tile(1, gcnt0);
+    if (nkt > 1) wait_dma();
+    __syncthreads();
+  }
+  int t = 1;
   for (; t < ia; ++t) {
     issue(t);
     edge_tile(t);
     finish(t);
   }
   // interior loop: one variant, no mask
-  for (; t < ib; ++t) {
+  for (t = max(t, ia); t < ib; ++t) {
     issue(t);
-    softmax_tile2<false>(qf, sm.b[t & 1], sm.c[t & 1], a.c2, lr, g, m_use, l_run, o, 0xFu,
-                         [](int, int, int) { return true; });
+    interior_tile(t);
     finish(t);
   }
   for (; t < nkt; ++t) {
@@ -918,32 +1095,13 @@ SC_DEV void window_fwd_v2(const AttnArgs& a, int blk, Smem<1>& sm, uint32_t* sDy
     edge_tile(t);
     finish(t);
   }
-  // global keys outside the block's key range, 64 slots per tile (few tiles;
+  // further chunks of out-of-band global keys (more than 64 global slots;
   // not pipelined)
-  const int* gp = wb.nxc ? a.gpos + (long long)wb.b * a.G : nullptr;
-  auto slot_row = [&](int c, int row) {
-    const int j = kBK * c + row;
-    const int p = j < a.G ? gp[j] : -1;
-    return (p >= 0 && p < L && (p < kt0 || (!causal && p >= kt1))) ? p : -1;
-  };
-  for (int t = nkt; t < ntile; ++t) {
-    const int c = sXList[t - nkt];
-    auto rows = [&](int R) {
-      const int p = slot_row(c, R);
-      return p >= 0 ? p : kt0;
-    };
-    tile_dma(Kg, ldb, sm.b[0], w, lane, rows);
-    tile_dma(Vg, ldb, sm.c[0], w, lane, rows);
-    if (tid < kBK) sm.pos[0][tid] = slot_row(c, tid);
+  for (int x = 1; x < nx; ++x) {
+    const int cnt = gather_chunk(sXList[x], 0);
     wait_dma();
     __syncthreads();
-    const unsigned long long used = __ballot(sm.pos[0][lane] >= 0);
-    unsigned live = 0u;
-#pragma unroll
-    for (int st = 0; st < 4; ++st) live |= (unsigned)(((used >> (16 * st)) & 0xFFFFull) != 0ull) << st;
-    const unsigned long long gm = used >> (4 * g);
-    softmax_tile2<true>(qf, sm.b[0], sm.c[0], a.c2, lr, g, m_use, l_run, o, live,
-                        [&](int, int st, int i) { return (bool)((gm >> (16 * st + i)) & 1ull); });
+    glob_tile(0, cnt);
     __syncthreads();
   }
 
