@@ -554,6 +554,7 @@ sc_status run_stack(const sc_attn_desc* d, int32_t n_layers, const int32_t* wind
   if (d->dtype != SC_BF16 || d->causal) return SC_EUNSUPPORTED;
   if ((long long)d->H * d->d > 2048) return SC_EUNSUPPORTED;
   if ((long long)d->n * 3 * d->H * d->d * 2 >= (1LL << 32)) return SC_EUNSUPPORTED;  // fused q|k|v rows
+  if (d->B > sc::kPackMaxB) return SC_EUNSUPPORTED;  // row packing of the products and LayerNorms
   if (n_layers < 1 || !x_in || !Wqkv || !Wo || !thresholds || !x_out || !final_len) return SC_EINVAL;
   if (!(ln_eps > 0.f) || !std::isfinite(ln_eps)) return SC_EINVAL;
   const bool ffn = W1 != nullptr;

@@ -131,18 +131,21 @@ hipError_t launch_gather(const GatherArgs& g, hipStream_t s);
 // Stack pieces.
 // y[rows, N] = x[rows, K] . W[K, N] (bf16 in, fp32 accumulate), rows of
 // sequence b limited to len[b] (others untouched); output bf16 or fp32.
-// GEMM epilogues: bf16 store, fp32 store, GELU then bf16 store.
-// part (float32, kGemmSplitRows * N, or NULL): with kGemmF32 and lengths,
-// a product whose surviving rows fill few tiles splits its reduction into
-// slabs there instead of writing y; the residual LayerNorm given the same
-// part, lengths and K adds them.
+// GEMM epilogues: bf16 store, fp32 store, GELU then bf16 store.  The
+// surviving rows of all sequences are packed into shared row tiles on the
+// device (B <= kPackMaxB).
+// part (float32, kGemmSplitRows * N, or NULL): with kGemmF32, a product
+// whose packed rows fill few tiles splits its reduction into slabs there
+// instead of writing y; the residual LayerNorm given the same part,
+// lengths and K adds them.
 constexpr int kGemmBf16 = 0, kGemmF32 = 1, kGemmGeluBf16 = 2;
 constexpr int kGemmSplitRows = 128 * 128;
+constexpr int kPackMaxB = 8192;
 hipError_t launch_gemm_bf16(const void* x, const void* w, void* y, int mode, int B, int n, int K, int N,
                             const int* len, float* part, hipStream_t s);
 // y = bf16(LayerNorm(x_res + t)) per row, rows of sequence b < len[b]; t or,
 // when part is not NULL, the slabs of the product of reduction length K that
-// wrote it.
+// wrote it.  B <= kPackMaxB.
 hipError_t launch_residual_layernorm(const void* x_res, const float* t, void* y, int B, int n, int D, float eps,
                                      const int* len, const float* part, int K, hipStream_t s);
 hipError_t launch_fill_zero(void* p, size_t bytes, hipStream_t s);
