@@ -336,10 +336,9 @@ sc_status prune_compact(const sc_attn_desc* d, const float* scores, float thresh
   p.new_index = static_cast<int*>(workspace);
   p.len_copy = nullptr;
   hipStream_t s = static_cast<hipStream_t>(stream);
-  if (sc::launch_prune(p, s) != hipSuccess) return SC_EHIP;
   ga.keep_idx = keep_idx;
   ga.new_len = new_len;
-  return sc::launch_gather(ga, s) == hipSuccess ? SC_OK : SC_EHIP;
+  return sc::launch_prune_gather(p, ga, s) == hipSuccess ? SC_OK : SC_EHIP;
 }
 
 }  // namespace
@@ -625,7 +624,6 @@ sc_status run_stack(const sc_attn_desc* d, int32_t n_layers, const int32_t* wind
     p.orig_out = orig_nxt;
     p.new_index = w.new_index;
     p.len_copy = kept_per_layer ? kept_per_layer + (size_t)l * B : nullptr;
-    chk(sc::launch_prune(p, s));
     sc::GatherArgs ga;
     std::memset(&ga, 0, sizeof(ga));
     ga.B = B;
@@ -638,7 +636,7 @@ sc_status run_stack(const sc_attn_desc* d, int32_t n_layers, const int32_t* wind
     ga.row_bytes[0] = ga.row_bytes[1] = (long long)D * 2;
     ga.keep_idx = w.keep_idx;
     ga.new_len = len_nxt;
-    chk(sc::launch_gather(ga, s));
+    chk(sc::launch_prune_gather(p, ga, s));
     // a9: output projection, residual, LayerNorm on the survivors
     chk(sc::launch_gemm_bf16(w.oc, Wo[l], w.t, sc::kGemmF32, B, n, Di, Di, len_nxt, w.split, s));
     if (!ffn) {

@@ -127,6 +127,10 @@ struct GatherArgs {
   const int* new_len;
 };
 hipError_t launch_gather(const GatherArgs& g, hipStream_t s);
+// The prune of p followed by the gather of g (keep_idx and new_len of g are
+// p's): one launch for the threshold rule on 16-byte aligned rows, else the
+// two above.
+hipError_t launch_prune_gather(const PruneArgs& p, const GatherArgs& g, hipStream_t s);
 
 // Stack pieces.
 // y[rows, N] = x[rows, K] . W[K, N] (bf16 in, fp32 accumulate), rows of

@@ -19,6 +19,14 @@
 //                scores are ranked in index order by the same block scan.
 // k_gather_rows  one wavefront per output row copies the kept input row with
 //                16-byte lanes (coalesced), for up to four tensors at once.
+// k_prune_compact the threshold rule and the compaction in one launch, for
+//                16-byte aligned rows: workgroup (c, b) owns tokens
+//                [64c, 64c + 64) of sequence b.  It counts the kept tokens
+//                before its chunk itself (every score before it, read from
+//                L2), ranks its own tokens with a ballot, writes their
+//                survivor slots and copies their rows; the last chunk's
+//                workgroup, whose count spans the whole sequence, writes the
+//                new length and the -1 tails.  No workgroup waits on another.
 #include <algorithm>
 
 #include "sc_device.h"
@@ -214,6 +222,162 @@ __global__ __launch_bounds__(kScanThreads) void k_prune_scan(PruneArgs p) {
   for (int j = gcarry + tid; j < p.G; j += kScanThreads) ngp[j] = -1;
 }
 
+constexpr int kChunk = 64;   // tokens per workgroup of k_prune_compact
+constexpr int kPcThreads = 256;
+
+// Threshold rule: keep(k) = k < L and (score > threshold or (keep_global and
+// k global)), compared in float32 as in k_prune_scan.
+__global__ __launch_bounds__(kPcThreads) void k_prune_compact(PruneArgs p, GatherArgs g) {
+  extern __shared__ uint32_t s_gbits[];  // global-token bitmask over [0, c1)
+  __shared__ int s_red[2][kPcThreads / 64];
+  __shared__ int s_k[kChunk], s_pos[kChunk];
+  __shared__ int s_nk, s_gchunk;
+  constexpr int kPre = 16;  // scores per thread loaded before the length and the bitmap are known
+  const int b = blockIdx.y, tid = threadIdx.x, lane = tid & 63, w = tid >> 6, n = p.n;
+  const int c0 = blockIdx.x * kChunk, c1 = min(c0 + kChunk, n);
+  const bool last = c1 == n;
+  const float* s = p.scores + (long long)b * n;
+  // issued together: the length, this thread's global slot, the first
+  // kPre * 256 scores before the chunk (clamped into it) and the chunk's own
+  // score (wave 0)
+  const int Lraw = p.valid_len[b];
+  const int* gp = (p.gpos && p.G > 0) ? p.gpos + (long long)b * p.G : nullptr;
+  const int q0 = gp && tid < p.G ? gp[tid] : -1;
+  float v[kPre];
+#pragma unroll
+  for (int i = 0; i < kPre; ++i) v[i] = c0 > 0 ? s[min(tid + kPcThreads * i, c0 - 1)] : 0.f;
+  const float own = s[min(c0 + lane, c1 - 1)];
+  const int L = clampi(Lraw, 0, n);
+  const int nwords = (c1 + 31) >> 5;
+  for (int i = tid; i < nwords; i += kPcThreads) s_gbits[i] = 0u;
+  __syncthreads();
+  if (q0 >= 0 && q0 < L && q0 < c1) atomicOr(&s_gbits[q0 >> 5], 1u << (q0 & 31));
+  for (int j = tid + kPcThreads; gp && j < p.G; j += kPcThreads) {
+    const int q = gp[j];
+    if (q >= 0 && q < L && q < c1) atomicOr(&s_gbits[q >> 5], 1u << (q & 31));
+  }
+  __syncthreads();
+  // bitmask reads clamped into [0, c1) and the rule in bitwise form: no
+  // branch separates the reads, so they are waited for together
+  auto glob = [&](int k) { return ((s_gbits[min(k, c1 - 1) >> 5] >> (k & 31)) & 1u) != 0u; };
+  const bool kg = p.keep_global != 0;
+  const float thr = p.threshold;
+  // kept tokens, and kept global tokens, before the chunk
+  int cnt = 0, gcnt = 0;
+  const int lim = min(c0, L);
+#pragma unroll
+  for (int i = 0; i < kPre; ++i) {
+    const int k = tid + kPcThreads * i;
+    const bool gl = glob(k);
+    const bool kp = (k < lim) & ((v[i] > thr) | (kg & gl));
+    cnt += kp;
+    gcnt += kp & gl;
+  }
+  for (int base = kPre * kPcThreads; base < lim; base += 8 * kPcThreads) {  // longer sequences
+    float u[8];
+#pragma unroll
+    for (int i = 0; i < 8; ++i) u[i] = s[min(base + tid + kPcThreads * i, lim - 1)];  // clamped, past lim discarded
+#pragma unroll
+    for (int i = 0; i < 8; ++i) {
+      const int k = base + tid + kPcThreads * i;
+      const bool gl = glob(k);
+      const bool kp = (k < lim) & ((u[i] > thr) | (kg & gl));
+      cnt += kp;
+      gcnt += kp & gl;
+    }
+  }
+#pragma unroll
+  for (int off = 32; off > 0; off >>= 1) {
+    cnt += __shfl_xor(cnt, off, 64);
+    gcnt += __shfl_xor(gcnt, off, 64);
+  }
+  if (lane == 0) {
+    s_red[0][w] = cnt;
+    s_red[1][w] = gcnt;
+  }
+  __syncthreads();
+  int before = 0, gbefore = 0;
+#pragma unroll
+  for (int i = 0; i < kPcThreads / 64; ++i) {
+    before += s_red[0][i];
+    gbefore += s_red[1][i];
+  }
+  int* kidx = p.keep_idx + (long long)b * n;
+  const int* oin = p.orig_in ? p.orig_in + (long long)b * n : nullptr;
+  int* oout = p.orig_out ? p.orig_out + (long long)b * n : nullptr;
+  int* ngp = (p.new_gpos && gp) ? p.new_gpos + (long long)b * p.G : nullptr;
+  if (w == 0) {  // the chunk's own tokens, one per lane
+    const int k = c0 + lane;
+    const bool gl = glob(k);
+    const bool kp = (k < c1) & (k < L) & ((own > thr) | (kg & gl));
+    const bool gk = kp & gl;
+    int tot, gtot;
+    const int r = wave_rank(kp, tot);
+    const int gr = wave_rank(gk, gtot);
+    if (kp) {
+      const int pos = before + r;
+      kidx[pos] = k;
+      if (oout) oout[pos] = oin ? oin[k] : k;
+      s_k[r] = k;
+      s_pos[r] = pos;
+      // surviving global tokens keep their ascending order
+      if (gk && ngp) ngp[gbefore + gr] = pos;
+    }
+    if (lane == 0) {
+      s_nk = tot;
+      s_gchunk = gtot;
+    }
+  }
+  __syncthreads();
+  const int nk = s_nk;
+  if (last) {  // this workgroup's count spans the sequence
+    const int total = before + nk;
+    if (tid == 0) {
+      p.new_len[b] = total;
+      if (p.len_copy) p.len_copy[b] = total;
+    }
+    for (int j = total + tid; j < n; j += kPcThreads) {
+      kidx[j] = -1;
+      if (oout) oout[j] = -1;
+    }
+    if (ngp)
+      for (int j = gbefore + s_gchunk + tid; j < p.G; j += kPcThreads) ngp[j] = -1;
+  }
+  // rows of the kept tokens: wave w copies rows w, w + 4, ..., four rows at a
+  // time, each lane two 16-byte units per row and round.  Rows and units past
+  // the end are clamped to the last valid ones for both the load and the
+  // store (a second, identical write), so that no branch separates the eight
+  // loads or the eight stores.
+  for (int t = 0; t < g.nt; ++t) {
+    const long long rb = g.row_bytes[t];
+    const int nu = (int)(rb >> 4);
+    const char* src = g.src[t] + (long long)b * n * rb;
+    char* dst = g.dst[t] + (long long)b * n * rb;
+    for (int i0 = w; i0 < nk; i0 += 16)
+      for (int u0 = 0; u0 < nu; u0 += 128) {
+        const int r0 = min(i0, nk - 1), r1 = min(i0 + 4, nk - 1), r2 = min(i0 + 8, nk - 1),
+                  r3 = min(i0 + 12, nk - 1);
+        const long long ua = 16LL * min(u0 + lane, nu - 1), ub = 16LL * min(u0 + lane + 64, nu - 1);
+        const char *s0 = src + s_k[r0] * rb, *s1 = src + s_k[r1] * rb, *s2 = src + s_k[r2] * rb,
+                   *s3 = src + s_k[r3] * rb;
+        const uint4 v0a = *reinterpret_cast<const uint4*>(s0 + ua), v0b = *reinterpret_cast<const uint4*>(s0 + ub);
+        const uint4 v1a = *reinterpret_cast<const uint4*>(s1 + ua), v1b = *reinterpret_cast<const uint4*>(s1 + ub);
+        const uint4 v2a = *reinterpret_cast<const uint4*>(s2 + ua), v2b = *reinterpret_cast<const uint4*>(s2 + ub);
+        const uint4 v3a = *reinterpret_cast<const uint4*>(s3 + ua), v3b = *reinterpret_cast<const uint4*>(s3 + ub);
+        char *d0 = dst + s_pos[r0] * rb, *d1 = dst + s_pos[r1] * rb, *d2 = dst + s_pos[r2] * rb,
+             *d3 = dst + s_pos[r3] * rb;
+        *reinterpret_cast<uint4*>(d0 + ua) = v0a;
+        *reinterpret_cast<uint4*>(d0 + ub) = v0b;
+        *reinterpret_cast<uint4*>(d1 + ua) = v1a;
+        *reinterpret_cast<uint4*>(d1 + ub) = v1b;
+        *reinterpret_cast<uint4*>(d2 + ua) = v2a;
+        *reinterpret_cast<uint4*>(d2 + ub) = v2b;
+        *reinterpret_cast<uint4*>(d3 + ua) = v3a;
+        *reinterpret_cast<uint4*>(d3 + ub) = v3b;
+      }
+  }
+}
+
 // One wavefront per (sequence, output row); blockIdx.z selects the tensor.
 __global__ __launch_bounds__(256) void k_gather_rows(GatherArgs a) {
   const int t = blockIdx.z, b = blockIdx.y;
@@ -264,6 +428,19 @@ __global__ void k_iota_orig(const int* valid_len, int* orig, int B, int n) {
 hipError_t launch_prune(const PruneArgs& p, hipStream_t s) {
   const size_t dyn = sizeof(uint32_t) * (((size_t)p.n + 31) / 32 + 1);
   hipLaunchKernelGGL(k_prune_scan, dim3(p.B), dim3(kScanThreads), dyn, s, p);
+  return hipGetLastError();
+}
+
+hipError_t launch_prune_gather(const PruneArgs& p, const GatherArgs& g, hipStream_t s) {
+  bool aligned = !p.topk;
+  for (int t = 0; t < g.nt; ++t)
+    aligned = aligned && ((g.row_bytes[t] | (long long)(uintptr_t)g.src[t] | (long long)(uintptr_t)g.dst[t]) & 15) == 0;
+  if (!aligned) {
+    hipError_t e = launch_prune(p, s);
+    return e != hipSuccess ? e : launch_gather(g, s);
+  }
+  const size_t dyn = sizeof(uint32_t) * (((size_t)p.n + 31) / 32 + 1);
+  hipLaunchKernelGGL(k_prune_compact, dim3((p.n + kChunk - 1) / kChunk, p.B), dim3(kPcThreads), dyn, s, p, g);
   return hipGetLastError();
 }
 
