@@ -574,7 +574,8 @@ def measure(sc, si, torch, np, inp, theta, steps, warmup, dev="cuda:0", keep_rat
     prune_bytes = 4 * B * n * 3 + 2 * sum(kept) * H * dd * 2
     roof = roofline(flops, bytes_, median(fwd), median(cols), pairs,
                     score=(score_kernels, score_us, score_bytes),
-                    prune=("k_prune_scan + k_gather_rows", prune_us, prune_bytes))
+                    prune=("k_prune_compact" if keep_ratio is None else "k_prune_scan + k_gather_rows", prune_us,
+                           prune_bytes))
     return dict(ms=median(per), mean_ms=mean_ms, wall_ms=wall_ms, fwd_ms=median(fwd), cols_ms=median(cols),
                 tokens=tokens, kept=kept, flops=flops, bytes=bytes_, roof=roof, theta=theta, pairs=pairs,
                 other_ms=median(per_other))
