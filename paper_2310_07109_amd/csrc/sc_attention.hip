@@ -35,6 +35,7 @@ constexpr int kBQ = kQueryBlock;
 constexpr int kBK = kKeyTile;
 constexpr float kTau = 8.0f;       // lazy-rescale slack in log2 units
 constexpr float kNegBig = -1e30f;  // running-max sentinel (finite: avoids inf - inf)
+constexpr float kRaiseSum = 256.0f;  // 2^kTau: a lane's sum of P above it triggers a raise
 
 // Minimum resident waves per SIMD the register allocation must allow.
 #define SC_OCC(w) __attribute__((amdgpu_waves_per_eu(w)))
@@ -758,20 +759,10 @@ SC_DEV void lane_max2(const f32x4 (&s)[kSub1][4], float (&lmax)[kSub1]) {
   }
 }
 
-// Whether any lane's running max must be raised: some logit of the lane's
-// own keys above the running max by kTau.  The running max of a query is the
-// same in the 4 lane groups that hold its keys, so the lane's own maximum
-// decides; only a raise needs the maximum over the groups (raise2).
-SC_DEV bool need_raise2(const float (&lmax)[kSub1], const float (&m_use)[kSub1], float c2) {
-  bool up = false;
-#pragma unroll
-  for (int j = 0; j < kSub1; ++j) up |= lmax[j] * c2 > m_use[j] + kTau;
-  return __builtin_amdgcn_ballot_w64(up) != 0ull;
-}
-
-// Raises the running maxima that need it and rescales their sums and
-// accumulators (lanes that do not need it scale by 1).  lmax: the lanes' own
-// maxima; the tile maximum of a query is taken over its 4 lane groups here.
+// Raises every running maximum below its tile maximum to it and rescales the
+// sums and accumulators (lanes that do not need it scale by 1).  lmax: the
+// lanes' own maxima; the tile maximum of a query is taken over its 4 lane
+// groups here.
 SC_DEV void raise2(const float (&lmax)[kSub1], float c2, float (&m_use)[kSub1], float (&l_run)[kSub1],
                    f32x4 (&o)[kSub1][4]) {
   float tmax[kSub1];
@@ -779,7 +770,7 @@ SC_DEV void raise2(const float (&lmax)[kSub1], float c2, float (&m_use)[kSub1], 
   for (int j = 0; j < kSub1; ++j) tmax[j] = group_max(lmax[j]) * c2;
 #pragma unroll
   for (int j = 0; j < kSub1; ++j) {
-    const bool up = tmax[j] > m_use[j] + kTau;
+    const bool up = tmax[j] > m_use[j];
     const float f = up ? fast_exp2(m_use[j] - tmax[j]) : 1.0f;
     m_use[j] = up ? tmax[j] : m_use[j];
     l_run[j] *= f;
@@ -788,31 +779,35 @@ SC_DEV void raise2(const float (&lmax)[kSub1], float c2, float (&m_use)[kSub1], 
   }
 }
 
-// P = exp2(S c2 - m) (summed into l) and O^T += V^T P^T for one tile.
-template <bool kMasked, int kNst = 4>
-SC_DEV void pv_tile2(const f32x4 (&s)[kSub1][4], const __bf16* sV, float c2, int, int, const float (&m_use)[kSub1],
-                     float (&l_run)[kSub1], f32x4 (&o)[kSub1][4], unsigned live) {
-  using TR = Tr<1>;
-  auto is_live = [&](int st) { return !kMasked || ((live >> st) & 1u); };
-  const int ln = threadIdx.x & 63, lr = ln & 15, g = ln >> 4;
-  bf16x8 pb[kSub1][2];
+// P = exp2(S c2 - m) as bf16 MFMA operands, and each query's sum of the
+// lane's own P (float32, before rounding).
+template <int kNst = 4>
+SC_DEV void exp_tile2(const f32x4 (&s)[kSub1][4], float c2, const float (&m_use)[kSub1], bf16x8 (&pb)[kSub1][2],
+                      float (&part)[kSub1]) {
 #pragma unroll
   for (int j = 0; j < kSub1; ++j) {
-    float part[4];
+    float ps[4];
 #pragma unroll
     for (int st = 0; st < kNst; ++st) {
       float p[4];
 #pragma unroll
       for (int i = 0; i < 4; ++i) p[i] = fast_exp2(fmaf(s[j][st][i], c2, -m_use[j]));
-      part[st] = (p[0] + p[1]) + (p[2] + p[3]);
+      ps[st] = (p[0] + p[1]) + (p[2] + p[3]);
 #pragma unroll
       for (int i = 0; i < 4; ++i) pb[j][st >> 1][4 * (st & 1) + i] = (__bf16)p[i];
     }
-    l_run[j] += kNst == 4 ? (part[0] + part[1]) + (part[2] + part[3]) : part[0] + part[1];
+    part[j] = kNst == 4 ? (ps[0] + ps[1]) + (ps[2] + ps[3]) : ps[0] + ps[1];
   }
-  // O^T += V^T P^T: the V operand comes from transposed reads of the
-  // row-major tile; lane (g, lr) supplies dims 16dt + 4(lr&3) .. +3 of rows
-  // 32kc + 4g + lr/4 and 32kc + 16 + 4g + lr/4 (keys in MFMA order)
+}
+
+// O^T += V^T P^T for one tile: the V operand comes from transposed reads of
+// the row-major tile; lane (g, lr) supplies dims 16dt + 4(lr&3) .. +3 of rows
+// 32kc + 4g + lr/4 and 32kc + 16 + 4g + lr/4 (keys in MFMA order)
+template <bool kMasked, int kNst = 4>
+SC_DEV void pv_tile2(const bf16x8 (&pb)[kSub1][2], const __bf16* sV, f32x4 (&o)[kSub1][4], unsigned live) {
+  using TR = Tr<1>;
+  auto is_live = [&](int st) { return !kMasked || ((live >> st) & 1u); };
+  const int ln = threadIdx.x & 63, lr = ln & 15, g = ln >> 4;
 #pragma unroll
   for (int kc = 0; kc < kNst / 2; ++kc) {
     if (!is_live(2 * kc) && !is_live(2 * kc + 1)) continue;
@@ -832,8 +827,11 @@ SC_DEV void pv_tile2(const f32x4 (&s)[kSub1][4], const __bf16* sV, float c2, int
 // (wave-uniform) says whether 16-key sub-tile st can hold an allowed pair; in
 // masked tiles ok(j, st, i) decides the pair (sub-block j's query, key
 // 16 st + 4g + i).  Disallowed logits become -inf, which exp2 maps to 0
-// (c2 > 0 is guaranteed by the host).  The running max is raised only when
-// the tile max exceeds it by kTau (for the whole wave when any lane needs it).
+// (c2 > 0 is guaranteed by the host).  P is computed with the running max
+// first; a logit more than kTau above it makes the lane's sum of P exceed
+// 2^kTau, and only then (for the whole wave, when any lane's sum does) are
+// the tile maxima taken, the running maxima raised to them and P recomputed.
+// So every P stays below 2^kTau, and the maxima are needed only on a raise.
 template <bool kMasked, typename OkFn, int kNst = 4>
 SC_DEV void softmax_tile2(const bf16x8 (&qf)[kSub1][2], const __bf16* sK, const __bf16* sV, float c2, int lr,
                           int g, float (&m_use)[kSub1], float (&l_run)[kSub1], f32x4 (&o)[kSub1][4], unsigned live,
@@ -849,10 +847,21 @@ SC_DEV void softmax_tile2(const bf16x8 (&qf)[kSub1][2], const __bf16* sK, const 
         for (int i = 0; i < 4; ++i)
           s[j][st][i] = (((live >> st) & 1u) && ok(j, st, i)) ? s[j][st][i] : -INFINITY;
   }
-  float lmax[kSub1];
-  lane_max2<kNst>(s, lmax);
-  if (need_raise2(lmax, m_use, c2)) raise2(lmax, c2, m_use, l_run, o);
-  pv_tile2<kMasked, kNst>(s, sV, c2, lr, g, m_use, l_run, o, live);
+  bf16x8 pb[kSub1][2];
+  float part[kSub1];
+  exp_tile2<kNst>(s, c2, m_use, pb, part);
+  bool over = false;
+#pragma unroll
+  for (int j = 0; j < kSub1; ++j) over |= part[j] > kRaiseSum;
+  if (__builtin_amdgcn_ballot_w64(over) != 0ull) {
+    float lmax[kSub1];
+    lane_max2<kNst>(s, lmax);
+    raise2(lmax, c2, m_use, l_run, o);
+    exp_tile2<kNst>(s, c2, m_use, pb, part);
+  }
+#pragma unroll
+  for (int j = 0; j < kSub1; ++j) l_run[j] += part[j];
+  pv_tile2<kMasked, kNst>(pb, sV, o, live);
 }
 
 // Pass 1 for bf16: O, LSE and the log2 LSE of the block's kBQ2 queries.
@@ -1647,7 +1656,7 @@ struct ScorePartialsOut {
 // global-row sums (chunk by chunk), score_head_global then adds, for a global
 // key in slot `slot` (-1: not global), its global-column sums over the nqrv
 // query ranges in use.  kNgc >= 0 fixes the number of global-row chunks at
-// compile time (it must equal sp.ngc).
+// compile time (it must equal sp.ngc; 0, 1 or 2, else -1).
 template <int kNgc>
 SC_DEV float score_head_local(const ScorePartials& sp, long long bh, int k) {
   float v = sp.band[bh * sp.n + k];
@@ -1675,7 +1684,7 @@ constexpr int kScorePre = 4;  // heads per group whose band / global-row terms a
 // global-row terms of the group's first kScorePre heads are loaded before the
 // length and the global positions arrive (they need neither), so the
 // workgroup waits on memory about once.  kNgc: the number of global-row
-// chunks when fixed at compile time (0 or 1), else -1.
+// chunks when fixed at compile time (0, 1 or 2), else -1.
 template <int kNgc>
 __global__ __launch_bounds__(kScoreKeys * kScoreGroups) void k_score_from_partials(ScorePartials sp,
                                                                                     const int* valid_len,
@@ -1705,11 +1714,27 @@ __global__ __launch_bounds__(kScoreKeys * kScoreGroups) void k_score_from_partia
   if (k < L) {
     const int slot = smap[lane];
     const int nqrv = (L + kGlobalKeySpan - 1) / kGlobalKeySpan;
+    // a global key's column terms of the first kScorePre heads, eight query
+    // ranges at a time with all their loads issued together (ranges past
+    // nqrv and heads past H read clamped entries that are discarded), added
+    // to each head's band / global-row term in range order
+    if (slot >= 0)
+      for (int q0 = 0; q0 < nqrv; q0 += 8) {
+        float t[kScorePre][8];
 #pragma unroll
-    for (int i = 0; i < kScorePre; ++i) {
-      const int h = hg + kScoreGroups * i;
-      if (h < H) acc += score_head_global(sp, (long long)b * H + h, slot, nqrv, pre[i]);
-    }
+        for (int i = 0; i < kScorePre; ++i) {
+          const long long bh = (long long)b * H + min(hg + kScoreGroups * i, H - 1);
+#pragma unroll
+          for (int u = 0; u < 8; ++u) t[i][u] = sp.gcol[(bh * sp.nqr + min(q0 + u, nqrv - 1)) * sp.G + slot];
+        }
+#pragma unroll
+        for (int i = 0; i < kScorePre; ++i)
+#pragma unroll
+          for (int u = 0; u < 8; ++u) pre[i] = q0 + u < nqrv ? pre[i] + t[i][u] : pre[i];
+      }
+#pragma unroll
+    for (int i = 0; i < kScorePre; ++i)
+      if (hg + kScoreGroups * i < H) acc += pre[i];
     for (int h = hg + kScoreGroups * kScorePre; h < H; h += kScoreGroups) {
       const long long bh = (long long)b * H + h;
       acc += score_head_global(sp, bh, slot, nqrv, score_head_local<kNgc>(sp, bh, k));
@@ -1953,6 +1978,9 @@ hipError_t launch_score_from_partials(const float* partials, const int* valid_le
                        scores);
   else if (g.ngc == 1)
     hipLaunchKernelGGL(k_score_from_partials<1>, grid, dim3(kScoreKeys * kScoreGroups), 0, s, sp, valid_len, gp,
+                       scores);
+  else if (g.ngc == 2)
+    hipLaunchKernelGGL(k_score_from_partials<2>, grid, dim3(kScoreKeys * kScoreGroups), 0, s, sp, valid_len, gp,
                        scores);
   else
     hipLaunchKernelGGL(k_score_from_partials<-1>, grid, dim3(kScoreKeys * kScoreGroups), 0, s, sp, valid_len, gp,
