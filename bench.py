@@ -647,6 +647,32 @@ def measure_passes(sc, si, torch, np, cfg, steps, warmup, dev="cuda:0", graph=Tr
                 lens=lens_h, gps=gps_h, other_ms=median(per_other))
 
 
+def probe_valu():
+    """Issue rate of v_fma_f32 and v_exp_f32 per SIMD: 2048 workgroups (8 waves per SIMD on 256 CUs), each
+    thread 8 independent chains, so that the time is set by issue, not latency.  Cycles at the 2.4 GHz peak
+    clock; the ratio does not depend on the clock."""
+    import ctypes
+    path = os.path.join(os.path.dirname(os.path.abspath(__file__)), "paper_2310_07109_amd", "libsc_probe.so")
+    lib = ctypes.CDLL(path)
+    lib.sc_probe_valu_rate.argtypes = [ctypes.c_int, ctypes.c_int, ctypes.c_int, ctypes.POINTER(ctypes.c_double),
+                                       ctypes.POINTER(ctypes.c_double)]
+    simds, clock = 256 * 4, 2.4e9
+    res = {}
+    for op, name in ((0, "v_fma_f32"), (1, "v_exp_f32")):
+        runs = []
+        for _ in range(3):
+            ms, wi = ctypes.c_double(), ctypes.c_double()
+            rc = lib.sc_probe_valu_rate(op, 2048, 2048, ctypes.byref(ms), ctypes.byref(wi))
+            if rc != 0:
+                raise RuntimeError(f"probe failed: {rc}")
+            runs.append(ms.value * 1e-3 * clock * simds / wi.value)
+        res[name] = round(median(runs), 3)
+    print(json.dumps({"probe": "VALU issue rate per SIMD (wave64 instructions)", "cycles_per_instruction": res,
+                      "exp_over_fma": round(res["v_exp_f32"] / res["v_fma_f32"], 3), "clock_ghz": clock / 1e9,
+                      "setup": "2048 workgroups x 256 threads (8 waves per SIMD), 8 independent chains per thread, "
+                               "65536 instructions per thread, median of 3 timed launches"}))
+
+
 def sweep(args, sc, si, torch, np):
     """Window and length sweeps of the same step (one JSON line per point).  Window sweep: B8 n4096;
     length sweep: window 512 and B = 32768 / n padded tokens; both H12 bf16, 32 global tokens, valid lengths
@@ -694,6 +720,9 @@ def main():
     ap.add_argument("--score", choices=("partials", "band"), default="partials",
                     help="partials: the fused column-sum partials (default); band: the paper's score path, every "
                          "probability stored in the band layout and summed from it (Sec. 5.5)")
+    ap.add_argument("--probe-valu", action="store_true",
+                    help="instead of the step, measure the SIMD issue rate of v_fma_f32 and v_exp_f32 (the two VALU "
+                         "forms the window attention's VALU floor counts), one JSON line")
     ap.add_argument("--sweep", action="store_true",
                     help="instead of the single measurement, sweep the window (n 4096) and the length (window "
                          "512), one JSON line per point")
@@ -711,6 +740,9 @@ def main():
 
     torch.cuda.set_device(0)
     dev = "cuda:0"
+    if args.probe_valu:
+        probe_valu()
+        return
     if args.sweep:
         sweep(args, sc, si, torch, np)
         return
