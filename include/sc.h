@@ -283,9 +283,10 @@ size_t sc_encoder_attn_stack_workspace_size(const sc_attn_desc *desc, int32_t n_
  *   keep, compaction as sc_ltp_prune_compact with thresholds[l]
  *   x   = bf16(LayerNorm(x + O . Wo[l]))     on the survivors; Wo [D, D];
  *                                            LayerNorm gamma 1, beta 0, eps ln_eps
- * desc gives the layer-0 geometry (dtype must be SC_BF16, causal 0, D = H*d); lengths and
- * global positions shrink on the device from layer to layer, with no host
- * synchronisation.
+ * desc gives the layer-0 geometry (dtype must be SC_BF16, causal 0, D = H*d,
+ * B <= 8192: the products pack the surviving rows of all sequences, larger
+ * batches return SC_EUNSUPPORTED); lengths and global positions shrink on the
+ * device from layer to layer, with no host synchronisation.
  *   x_in            bf16 [B, n, D]; x_out bf16 [B, n, D] (survivors first).
  *   Wqkv, Wo        HOST arrays of n_layers device pointers (bf16).
  *   thresholds      HOST float [n_layers].

@@ -237,6 +237,10 @@ def test_score_and_stack_validation():
                                    0x300000, None, None, 0x900000, 1 << 30, None) == B.SC_EINVAL
     assert L.sc_encoder_attn_stack(ctypes.byref(cd), 1, 0x100000, w, w, th, 1, ctypes.c_float(1e-5), 0x200000,
                                    0x300000, None, None, None, 0, None) == B.SC_EWORKSPACE
+    # the products pack the surviving rows of all sequences with a per-workgroup prefix table: B <= 8192
+    wide = desc(B=8193, n=16, H=2, window=4, G=0)
+    assert L.sc_encoder_attn_stack(ctypes.byref(wide.c()), 1, 0x100000, w, w, th, 1, ctypes.c_float(1e-5),
+                                   0x200000, 0x300000, None, None, 0x900000, 1 << 30, None) == B.SC_EUNSUPPORTED
 
 
 def test_noalloc_rejects_oversized_problems_on_the_host():

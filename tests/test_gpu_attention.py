@@ -315,3 +315,40 @@ def test_causal_config4_attention_scores_and_pruning():
     compare_keep(keep.cpu().numpy(), nl.cpu().numpy(), rs, theta, inp["valid_len"], inp["global_pos"],
                  tag="causal config 4 keep")
     log(f"causal config 4: max |dO| {err:.3g}, worst score rel err {worst:.3g}, kept {nl.cpu().tolist()}")
+
+
+@pytest.mark.parametrize("kg", [1, 0])
+def test_prune_compact_fused_and_fallback_paths(kg):
+    """The one-launch threshold prune (16-byte aligned rows, up to four tensors) and the two-kernel path it
+    falls back to (any row that is not 16-byte aligned) give identical survivor lists, lengths, renumbered
+    globals and composed indices, equal to the oracle's, and copy the same rows.  Ragged lengths (an empty
+    sequence), n not a multiple of the 64-token chunk, unused global slots, ties at the threshold."""
+    B, n, G = 3, 1000, 40
+    vl = np.array([0, 537, 1000], np.int32)
+    gp = si.global_positions(11, vl, G, "random")
+    gp[2, -5:] = -1  # unused slots at the end of one row
+    u = si.uniform(11, 5, B * n).reshape(B, n)
+    scores = (u * 2e-3).astype(np.float32)
+    theta = float(np.float32(scores[2, 123]))  # a score equal to the threshold is pruned
+    d = sc.Desc(B, n, 2, 64, dev_i32(vl), dev_i32(gp), 0.125, sc.SC_BF16)
+    s_dev = torch.from_numpy(scores).cuda()
+    oin = torch.from_numpy(si.randint(11, 6, B * n, 0, 1 << 20).reshape(B, n).astype(np.int32)).cuda()
+    # four aligned tensors (rows of 16, 48, 256 and 1536 bytes) take the one-launch path
+    aligned = [torch.from_numpy(si.randint(11, 7 + i, B * n * w, -30000, 30000).reshape(B, n, w).astype(np.int16)).cuda()
+               for i, w in enumerate((8, 24, 128, 768))]
+    ka, nla, gpa, oa, da = sc.sc_ltp_prune_compact(d, s_dev, theta, kg, aligned, orig_idx_in=oin)
+    # one 6-byte row makes the call take the scan + gather kernels
+    odd = torch.from_numpy(si.randint(11, 12, B * n * 3, -30000, 30000).reshape(B, n, 3).astype(np.int16)).cuda()
+    kb, nlb, gpb, ob, db = sc.sc_ltp_prune_compact(d, s_dev, theta, kg, [aligned[0], odd], orig_idx_in=oin)
+    rk, rnl, rngp, rorig = oracle.ltp_prune(scores, vl, gp, theta, kg, orig_in=oin.cpu().numpy())
+    assert 0 < rnl[1] < vl[1] and 0 < rnl[2] < vl[2] and rnl[0] == 0
+    for k_, nl_, gp_, o_ in ((ka, nla, gpa, oa), (kb, nlb, gpb, ob)):
+        assert np.array_equal(k_.cpu().numpy(), rk) and np.array_equal(nl_.cpu().numpy(), rnl)
+        assert np.array_equal(gp_.cpu().numpy(), rngp)
+        assert np.array_equal(o_.cpu().numpy(), rorig)
+    for src, dst in list(zip(aligned, da)) + [(odd, db[1]), (aligned[0], db[0])]:
+        s_np, d_np = src.cpu().numpy(), dst.cpu().numpy()
+        for b in range(B):
+            assert np.array_equal(d_np[b, :rnl[b]], s_np[b, rk[b, :rnl[b]]])
+    log(f"fused / fallback prune (keep_global={kg}): kept {rnl.tolist()}, globals kept "
+        f"{[(int((rngp[b] >= 0).sum())) for b in range(B)]}")
