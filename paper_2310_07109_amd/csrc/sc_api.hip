@@ -34,8 +34,12 @@ sc_status check_desc(const sc_attn_desc* d) {
   if (d->causal != 0 && d->causal != 1) return SC_EINVAL;
   if (d->d != 64) return SC_EUNSUPPORTED;
   if (d->causal && d->dtype != SC_BF16) return SC_EUNSUPPORTED;
-  // grid sizes must fit the launch limits
-  const long long blocks = (long long)((d->n + 63) / 64) * d->H * d->B;
+  // grid sizes must fit the launch limits: 64-row blocks, and the attention
+  // launches' per-span work (at most 8 window or band-column blocks and two
+  // blocks per 32 global slots in every key span)
+  const long long nspan = (d->n + sc::kGlobalKeySpan - 1) / sc::kGlobalKeySpan;
+  const long long ngc = (d->G + sc::kGlobalChunk - 1) / sc::kGlobalChunk;
+  const long long blocks = std::max((long long)((d->n + 63) / 64), nspan * (8 + 2 * ngc)) * d->H * d->B;
   if (blocks >= (1LL << 31)) return SC_EUNSUPPORTED;
   if ((long long)d->B * d->n >= (1LL << 31)) return SC_EUNSUPPORTED;
   // tile loads address one sequence's rows with 32-bit byte offsets

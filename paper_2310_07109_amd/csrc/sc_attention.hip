@@ -258,9 +258,10 @@ struct WinBlock {
 };
 
 template <int QB = kBQ>
-SC_DEV WinBlock win_block(const AttnArgs& a, int blk) {
+SC_DEV WinBlock win_block(const AttnArgs& a, int bh, int qb) {
   WinBlock wb;
-  xcd_pair_map(blk, a.nqb, a.H * a.B, wb.bh, wb.qb);
+  wb.bh = bh;
+  wb.qb = qb;
   wb.h = wb.bh % a.H;
   wb.b = wb.bh / a.H;
   wb.L = clampi(a.valid_len[wb.b], 0, a.n);
@@ -420,12 +421,12 @@ struct WinLoader {
 // Pass 1: O, LSE (and the log2 LSE used by the column sums) for the
 // non-global queries of the block; zero rows for padding queries.
 template <int DT>
-SC_DEV void window_fwd_block(const AttnArgs& a, int blk, Smem<DT>& sm, uint32_t* sDyn) {
+SC_DEV void window_fwd_block(const AttnArgs& a, int bh, int qb, Smem<DT>& sm, uint32_t* sDyn) {
   using TR = Tr<DT>;
   using T = typename TR::T;
   using Frag = typename TR::Frag;
   constexpr int P = TR::kPitch;
-  const WinBlock wb = win_block(a, blk);
+  const WinBlock wb = win_block(a, bh, qb);
   const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6, g = lane >> 4, lr = lane & 15;
   const int n = a.n, r = a.r, L = wb.L, q0 = wb.q0, kt0 = wb.kt0, kt1 = wb.kt1, nkt = wb.nkt;
   const T* Qg = static_cast<const T*>(a.q) + wb.b * a.bs_in + wb.h * kHeadDim;
@@ -865,9 +866,9 @@ SC_DEV void softmax_tile2(const bf16x8 (&qf)[kSub1][2], const __bf16* sK, const 
 }
 
 // Pass 1 for bf16: O, LSE and the log2 LSE of the block's kBQ2 queries.
-SC_DEV void window_fwd_v2(const AttnArgs& a, int blk, Smem<1>& sm, uint32_t* sDyn) {
+SC_DEV void window_fwd_v2(const AttnArgs& a, int bh, int qb, Smem<1>& sm, uint32_t* sDyn) {
   using T = __bf16;
-  const WinBlock wb = win_block<kBQ2>(a, blk);
+  const WinBlock wb = win_block<kBQ2>(a, bh, qb);
   const int tid = threadIdx.x, lane = tid & 63, w = __builtin_amdgcn_readfirstlane(tid >> 6), g = lane >> 4,
             lr = lane & 15;
   const int n = a.n, r = a.r, L = wb.L, q0 = wb.q0, kt0 = wb.kt0, kt1 = wb.kt1, nkt = wb.nkt;
@@ -1138,21 +1139,39 @@ SC_DEV void window_fwd_v2(const AttnArgs& a, int blk, Smem<1>& sm, uint32_t* sDy
   }
 }
 
-// Launch 1: the window pass-1 blocks, then the global-row forward blocks
-// (when there are global tokens).
+// Work of launch 1 per (sequence, head) pair and key span: kSpanQB window
+// blocks, then the span's global-row blocks (one per 32-slot group).
+static_assert(kBQ == kBQ2 && kGlobalKeySpan % kBQ == 0, "window blocks tile the key span");
+constexpr int kSpanQB = kGlobalKeySpan / kBQ;
+struct FwdSpan {
+  int per;  // blocks per span
+};
+__host__ __device__ inline FwdSpan fwd_span(const AttnArgs& a) { return {kSpanQB + (a.n_gr > 0 ? a.ngc : 0)}; }
+
+// Launch 1: the window pass-1 blocks and the global-row forward blocks (when
+// there are global tokens).  Each (sequence, head) pair's work runs in key
+// span order: for span c (kGlobalKeySpan keys), the window blocks of its
+// queries, then the global-row blocks of its keys, which the window blocks
+// just read (they are still in the XCD's L2).  Pairs are dealt round-robin
+// to the XCDs and a pair's work stays on one XCD, in order (xcd_pair_map).
 template <int DT>
 __global__ __launch_bounds__(kThreads) SC_OCC(DT == 1 ? 3 : 2) void k_attn_fwd(AttnArgs a) {
   __shared__ Smem<DT> sm;
   extern __shared__ uint32_t sDyn[];
-  // window blocks first (their XCD mapping assumes they start at block 0);
-  // the global-row blocks come last and fill the window blocks' uneven tail
-  const int nwin = a.nqb * a.H * a.B;
-  if ((int)blockIdx.x >= nwin)
-    gr_fwd_block<DT>(a, blockIdx.x - nwin, sm);
-  else if constexpr (DT == 1)
-    window_fwd_v2(a, blockIdx.x, sm, sDyn);
+  const FwdSpan f = fwd_span(a);
+  int bh, j;
+  xcd_pair_map(blockIdx.x, a.nkc * f.per, a.H * a.B, bh, j);
+  const int c = j / f.per, o = j - c * f.per;
+  if (o >= kSpanQB) {
+    gr_fwd_block<DT>(a, (bh * a.ngc + (o - kSpanQB)) * a.nkc + c, sm);
+    return;
+  }
+  const int qb = c * kSpanQB + o;
+  if (qb >= a.nqb) return;  // the last span's missing query blocks
+  if constexpr (DT == 1)
+    window_fwd_v2(a, bh, qb, sm, sDyn);
   else
-    window_fwd_block<DT>(a, blockIdx.x, sm, sDyn);
+    window_fwd_block<DT>(a, bh, qb, sm, sDyn);
 }
 
 // -------------------------------------------------------- column sums ------
@@ -1165,12 +1184,10 @@ __global__ __launch_bounds__(kThreads) SC_OCC(DT == 1 ? 3 : 2) void k_attn_fwd(A
 // Query rows come with their log2-LSE from pass 1 (+inf for global and
 // padding rows, whose own probabilities are counted by the global-row blocks).
 template <int DT, bool kBandProbs>
-SC_DEV void band_col_block(const AttnArgs& a, int blk, SmemCol<DT>& sm) {
+SC_DEV void band_col_block(const AttnArgs& a, int bh, int kb, SmemCol<DT>& sm) {
   using TR = Tr<DT>;
   using T = typename TR::T;
   constexpr int P = TR::kPitch;
-  int kb, bh;
-  xcd_pair_map(blk, a.nkb, a.H * a.B, bh, kb);
   const int h = bh % a.H, b = bh / a.H;
   const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6, g = lane >> 4, lr = lane & 15;
   const int n = a.n, r = a.r, G = a.G;
@@ -1292,11 +1309,9 @@ SC_DEV void col_tile2(const bf16x8 (&kf)[2][2], const __bf16* sQ, const float* s
   }
 }
 
-SC_DEV void band_col_v2(const AttnArgs& a, int blk, SmemCol<1>& sm) {
+SC_DEV void band_col_v2(const AttnArgs& a, int bh, int kb, SmemCol<1>& sm) {
   using TR = Tr<1>;
   using T = __bf16;
-  int kb, bh;
-  xcd_pair_map(blk, a.nkb, a.H * a.B, bh, kb);
   const int h = bh % a.H, b = bh / a.H;
   const int tid = threadIdx.x, lane = tid & 63, w = __builtin_amdgcn_readfirstlane(tid >> 6), g = lane >> 4,
             lr = lane & 15;
@@ -1481,7 +1496,6 @@ SC_DEV void gr_col_block(const AttnArgs& a, int lin, SmemCol<DT>& sm) {
   using TR = Tr<DT>;
   using T = typename TR::T;
   constexpr int P = TR::kPitch;
-  if (lin >= a.n_gr) return;  // padding of the block count to a multiple of 8
   const GrBlock blk = gr_block(a, lin);
   const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6, g = lane >> 4, lr = lane & 15;
   const int L = clampi(a.valid_len[blk.b], 0, a.n);
@@ -1607,29 +1621,54 @@ SC_DEV void gr_col_block(const AttnArgs& a, int lin, SmemCol<DT>& sm) {
   }
 }
 
-// Launch 2: global-row column blocks, then band-column and global-column
-// blocks (both only when score partials or the band layout are asked for).
+// Work of launch 2 per (sequence, head) pair and key span: nbc band-column
+// blocks, ngr global-row blocks, ngcol global-column blocks.
+static_assert(kGlobalKeySpan % kBK2 == 0 && kGlobalKeySpan % kBK == 0, "column blocks tile the key span");
+struct ColSpan {
+  int nbc, ngr, ngcol, per;
+};
+template <int DT, bool kBandProbs>
+__host__ __device__ inline ColSpan col_span(const AttnArgs& a) {
+  constexpr int keys = (DT == 1 && !kBandProbs) ? kBK2 : kBK;  // keys per band-column block
+  ColSpan f;
+  f.nbc = a.n_bcol > 0 ? kGlobalKeySpan / keys : 0;
+  f.ngr = a.n_gr > 0 ? a.ngc : 0;
+  f.ngcol = a.n_gcol > 0 ? a.ngc : 0;
+  f.per = f.nbc + f.ngr + f.ngcol;
+  return f;
+}
+
+// Launch 2: global-row column blocks, band-column and global-column blocks
+// (the last two only when score partials or the band layout are asked for).
+// Each (sequence, head) pair's work runs in span order: for span c
+// (kGlobalKeySpan keys), the band-column blocks of its keys, the global-row
+// blocks of the same keys, then the global-column blocks of its queries (the
+// band-column blocks just read those).  Pairs are dealt round-robin to the
+// XCDs, a pair's work on one XCD in order (xcd_pair_map).
 template <int DT, bool kBandProbs>
 __global__ __launch_bounds__(kThreads) SC_OCC(kBandProbs ? 2 : 4) void k_attn_cols(AttnArgs a) {
   __shared__ SmemCol<DT> sm;
-  // global-row column blocks first (long; started early they overlap the
-  // rest), their count padded to a multiple of 8 so that the band-column
-  // blocks start on XCD 0 as their mapping assumes; then band-column and
-  // global-column blocks
-  int blk = blockIdx.x;
-  if (blk < a.n_grc) {
-    gr_col_block<DT, kBandProbs>(a, blk, sm);
-    return;
-  }
-  blk -= a.n_grc;
-  if (blk < a.n_bcol) {
+  const ColSpan f = col_span<DT, kBandProbs>(a);
+  int bh, j;
+  xcd_pair_map(blockIdx.x, a.nkc * f.per, a.H * a.B, bh, j);
+  const int c = j / f.per;
+  int o = j - c * f.per;
+  if (o < f.nbc) {
+    const int kb = c * f.nbc + o;
+    if (kb >= a.nkb) return;  // the last span's missing key blocks
     if constexpr (DT == 1 && !kBandProbs)
-      band_col_v2(a, blk, sm);
+      band_col_v2(a, bh, kb, sm);
     else
-      band_col_block<DT, kBandProbs>(a, blk, sm);
+      band_col_block<DT, kBandProbs>(a, bh, kb, sm);
     return;
   }
-  gcol_block<DT, kBandProbs>(a, blk - a.n_bcol, sm);
+  o -= f.nbc;
+  if (o < f.ngr) {
+    gr_col_block<DT, kBandProbs>(a, (bh * a.ngc + o) * a.nkc + c, sm);
+    return;
+  }
+  o -= f.ngr;
+  gcol_block<DT, kBandProbs>(a, (bh * a.ngc + o) * a.nqr + c, sm);
 }
 
 // ------------------------------------------------------ score reduction ----
@@ -1925,7 +1964,6 @@ static hipError_t launch_window_t(const AttnArgs& a0, hipStream_t s) {
   const bool glob = a.G > 0 && a.gpos;
   const bool cols = a.part_band || a.bp_band;
   a.n_gr = glob ? a.nkc * a.ngc * a.H * a.B : 0;
-  a.n_grc = (a.n_gr + 7) & ~7;
   if (DT == 1 && !a.bp_band) a.nkb = (a.n + kBK2 - 1) / kBK2;  // 128-key column blocks
   a.n_bcol = cols ? a.nkb * a.H * a.B : 0;
   a.n_gcol = (cols && glob) ? a.nqr * a.ngc * a.H * a.B : 0;
@@ -1936,8 +1974,11 @@ static hipError_t launch_window_t(const AttnArgs& a0, hipStream_t s) {
     a.rwp = (int)(rw < a.n ? rw : a.n);
   }
   const size_t dyn = sizeof(uint32_t) * ((size_t)a.rwp / 32 + 2 + nxc + 1);
-  const unsigned fwd_blocks = (unsigned)(a.n_gr + a.nqb * a.H * a.B);
-  const unsigned col_blocks = (unsigned)(a.n_grc + a.n_bcol + a.n_gcol);
+  // the spans' block counts (the host checks that they fit the grid limits)
+  const long long pairs = (long long)a.H * a.B;
+  const unsigned fwd_blocks = (unsigned)(a.nkc * fwd_span(a).per * pairs);
+  const int col_per = a.bp_band ? col_span<DT, true>(a).per : col_span<DT, false>(a).per;
+  const unsigned col_blocks = (unsigned)(a.nkc * col_per * pairs);
   if (!a.no_profile) profile_mark(s, 0);
   hipLaunchKernelGGL(k_attn_fwd<DT>, dim3(fwd_blocks), dim3(kThreads), dyn, s, a);
   if (!a.no_profile) profile_mark(s, 1);

@@ -34,7 +34,6 @@ struct AttnArgs {
   float* part_grow;       // [B, H, ngc, n] column sums over the global rows
   int nqb, rwp, ngc, nkc, Gp, nkb, nqr;
   int n_gr, n_bcol, n_gcol;  // block counts of the global-row, band-column and global-column parts
-  int n_grc;                 // global-row blocks of the column launch (n_gr padded to a multiple of 8)
   // global-row split partials (workspace)
   float* gr_ml;           // [B, H, nkc, Gp, 2]
   float* gr_o;            // [B, H, nkc, Gp, 64]
