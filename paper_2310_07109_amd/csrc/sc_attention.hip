@@ -1146,22 +1146,39 @@ constexpr int kSpanQB = kGlobalKeySpan / kBQ;
 struct FwdSpan {
   int per;  // blocks per span
 };
+
+// Block -> (pair, span c, block o of the span) for `per` blocks per span.
+// Pair by pair suits sequences that fill most of n (a pair's spans share K/V
+// rows at their borders in the L2); span by span starts every pair's first
+// spans before any pair's later ones, so after pruning, when the sequences
+// hold a few spans, the live blocks are dispatched first and the blocks past
+// the sequence ends last.
+SC_DEV void span_block(const AttnArgs& a, int per, int& bh, int& c, int& o) {
+  if (a.span_major) {
+    xcd_span_map(blockIdx.x, a.nkc, per, a.H * a.B, bh, c, o);
+  } else {
+    int j;
+    xcd_pair_map(blockIdx.x, a.nkc * per, a.H * a.B, bh, j);
+    c = j / per;
+    o = j - c * per;
+  }
+}
 __host__ __device__ inline FwdSpan fwd_span(const AttnArgs& a) { return {kSpanQB + (a.n_gr > 0 ? a.ngc : 0)}; }
 
 // Launch 1: the window pass-1 blocks and the global-row forward blocks (when
-// there are global tokens).  Each (sequence, head) pair's work runs in key
-// span order: for span c (kGlobalKeySpan keys), the window blocks of its
-// queries, then the global-row blocks of its keys, which the window blocks
-// just read (they are still in the XCD's L2).  Pairs are dealt round-robin
-// to the XCDs and a pair's work stays on one XCD, in order (xcd_pair_map).
+// there are global tokens).  A (sequence, head) pair's work of key span c
+// (kGlobalKeySpan keys) is the window blocks of its queries, then the
+// global-row blocks of its keys, which the window blocks just read (they are
+// still in the XCD's L2).  Pairs are dealt round-robin to the XCDs, and a
+// pair's work stays on one XCD: pair by pair, each in span order
+// (xcd_pair_map), or span by span (xcd_span_map, a.span_major).
 template <int DT>
 __global__ __launch_bounds__(kThreads) SC_OCC(DT == 1 ? 3 : 2) void k_attn_fwd(AttnArgs a) {
   __shared__ Smem<DT> sm;
   extern __shared__ uint32_t sDyn[];
   const FwdSpan f = fwd_span(a);
-  int bh, j;
-  xcd_pair_map(blockIdx.x, a.nkc * f.per, a.H * a.B, bh, j);
-  const int c = j / f.per, o = j - c * f.per;
+  int bh, c, o;
+  span_block(a, f.per, bh, c, o);
   if (o >= kSpanQB) {
     gr_fwd_block<DT>(a, (bh * a.ngc + (o - kSpanQB)) * a.nkc + c, sm);
     return;
@@ -1640,19 +1657,16 @@ __host__ __device__ inline ColSpan col_span(const AttnArgs& a) {
 
 // Launch 2: global-row column blocks, band-column and global-column blocks
 // (the last two only when score partials or the band layout are asked for).
-// Each (sequence, head) pair's work runs in span order: for span c
-// (kGlobalKeySpan keys), the band-column blocks of its keys, the global-row
-// blocks of the same keys, then the global-column blocks of its queries (the
-// band-column blocks just read those).  Pairs are dealt round-robin to the
-// XCDs, a pair's work on one XCD in order (xcd_pair_map).
+// A (sequence, head) pair's work of span c (kGlobalKeySpan keys) is the
+// band-column blocks of its keys, the global-row blocks of the same keys,
+// then the global-column blocks of its queries (the band-column blocks just
+// read those).  Pairs are dealt to the XCDs as in launch 1.
 template <int DT, bool kBandProbs>
 __global__ __launch_bounds__(kThreads) SC_OCC(kBandProbs ? 2 : 4) void k_attn_cols(AttnArgs a) {
   __shared__ SmemCol<DT> sm;
   const ColSpan f = col_span<DT, kBandProbs>(a);
-  int bh, j;
-  xcd_pair_map(blockIdx.x, a.nkc * f.per, a.H * a.B, bh, j);
-  const int c = j / f.per;
-  int o = j - c * f.per;
+  int bh, c, o;
+  span_block(a, f.per, bh, c, o);
   if (o < f.nbc) {
     const int kb = c * f.nbc + o;
     if (kb >= a.nkb) return;  // the last span's missing key blocks

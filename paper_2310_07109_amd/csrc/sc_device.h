@@ -119,6 +119,30 @@ SC_DEV void xcd_pair_map(int i, int inner, int pairs, int& pair, int& idx) {
   }
 }
 
+// The same dealing of pairs to XCDs for work split into nspan spans of `per`
+// blocks per pair, but span-major: an XCD runs span 0 of all its pairs, then
+// span 1 of all of them, and so on, with a pair's blocks of one span in order.
+// Work at the start of the sequences (all there is once pruning has shortened
+// them) is dispatched first, and the blocks that only find a span beyond
+// their sequence's length come last.  Block i -> (pair, span c, block o of
+// the span).  The last pairs % 8 pairs follow, span-major among themselves.
+SC_DEV void xcd_span_map(int i, int nspan, int per, int pairs, int& pair, int& c, int& o) {
+  const int full = pairs & ~7;
+  if (i < full * nspan * per) {
+    const int x = i & 7, j = i >> 3, row = (full >> 3) * per;  // blocks per span on one XCD
+    c = j / row;
+    const int r = j - c * row;
+    pair = 8 * (r / per) + x;
+    o = r % per;
+  } else {
+    const int rest = i - full * nspan * per, row = (pairs - full) * per;
+    c = rest / row;
+    const int r = rest - c * row;
+    pair = full + r / per;
+    o = r % per;
+  }
+}
+
 template <int DT>
 struct Tr;
 

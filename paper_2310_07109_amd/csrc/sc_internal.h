@@ -27,6 +27,8 @@ struct AttnArgs {
   int causal;             // 1: keys after the query are never attended
   int skip_pad_out;       // 1: output rows of padding-only query blocks are left unwritten
   int no_profile;         // 1: never record benchmark events for this call
+  int span_major;         // 1: dispatch the attention blocks span-major (xcd_span_map), for
+                          //    sequences much shorter than n; 0: pair by pair (xcd_pair_map)
   float c2;               // softmax scale * log2(e)
   // score partials (null: skip the exact-probability column sums)
   float* part_band;       // [B, H, n]      band column sums of non-global keys
