@@ -546,8 +546,11 @@ hipError_t launch_residual_layernorm(const void* x_res, const float* t, void* y,
   const long long rows = (long long)B * n;
   if (!gemm_v3_ok(B, n, K, D)) part = nullptr;  // the product took the path without a split
   auto* kern = D <= 1024 ? k_residual_ln<16> : k_residual_ln<32>;  // D <= 2048 (checked by the caller)
-  // one wave per row, at most 4096 workgroups (later rows loop)
-  const long long blocks = std::min<long long>((rows + 3) / 4, 4096);
+  // one wave per row, at most 1024 workgroups (later rows loop; with the
+  // grid sized by the lengths' upper bound n, a pruned layer's few rows would
+  // otherwise come with thousands of workgroups that only build the prefix
+  // table: 7.5 -> 6.3 us in the stack's late layers)
+  const long long blocks = std::min<long long>((rows + 3) / 4, 1024);
   hipLaunchKernelGGL(kern, dim3((unsigned)blocks), dim3(256), sizeof(int) * (B + 1), s,
                      static_cast<const __bf16*>(x_res), t, static_cast<__bf16*>(y), B, n, D, eps, len, part, K);
   return hipGetLastError();
