@@ -40,7 +40,7 @@ sc_status check_desc(const sc_attn_desc* d) {
   const long long nspan = (d->n + sc::kGlobalKeySpan - 1) / sc::kGlobalKeySpan;
   const long long ngc = (d->G + sc::kGlobalChunk - 1) / sc::kGlobalChunk;
   const long long blocks = std::max((long long)((d->n + 63) / 64), nspan * (8 + 2 * ngc)) * d->H * d->B;
-  if (blocks >= (1LL << 31)) return SC_EUNSUPPORTED;
+  if (blocks + 8 >= (1LL << 31)) return SC_EUNSUPPORTED;  // + padding of a block count to a multiple of 8
   if ((long long)d->B * d->n >= (1LL << 31)) return SC_EUNSUPPORTED;
   // tile loads address one sequence's rows with 32-bit byte offsets
   if ((long long)d->n * d->H * d->d * (long long)elem_size(d->dtype) >= (1LL << 32)) return SC_EUNSUPPORTED;

@@ -1166,16 +1166,35 @@ SC_DEV void span_block(const AttnArgs& a, int per, int& bh, int& c, int& o) {
 __host__ __device__ inline FwdSpan fwd_span(const AttnArgs& a) { return {kSpanQB + (a.n_gr > 0 ? a.ngc : 0)}; }
 
 // Launch 1: the window pass-1 blocks and the global-row forward blocks (when
-// there are global tokens).  A (sequence, head) pair's work of key span c
-// (kGlobalKeySpan keys) is the window blocks of its queries, then the
-// global-row blocks of its keys, which the window blocks just read (they are
-// still in the XCD's L2).  Pairs are dealt round-robin to the XCDs, and a
-// pair's work stays on one XCD: pair by pair, each in span order
-// (xcd_pair_map), or span by span (xcd_span_map, a.span_major).
+// there are global tokens).  Span by span (a.span_major, pruned layers): a
+// (sequence, head) pair's work of key span c (kGlobalKeySpan keys) is the
+// window blocks of its queries, then the global-row blocks of its keys,
+// which the window blocks just read (they are still in the XCD's L2); the
+// pairs are dealt round-robin to the XCDs, a pair's work on one XCD
+// (xcd_span_map).  Otherwise the window blocks come first, pair by pair
+// (xcd_pair_map), and the global-row blocks last, where they fill the window
+// blocks' uneven tail.  The span order used for every call cut the launch's
+// HBM traffic at seq 4096 from 221 to 154 MB and its time by 1.5 %, but
+// cost 5 % at the other single-layer shapes (n 1024, and n 8192 with 64
+// global slots).
 template <int DT>
 __global__ __launch_bounds__(kThreads) SC_OCC(DT == 1 ? 3 : 2) void k_attn_fwd(AttnArgs a) {
   __shared__ Smem<DT> sm;
   extern __shared__ uint32_t sDyn[];
+  if (!a.span_major) {
+    const int nwin = a.nqb * a.H * a.B;
+    if ((int)blockIdx.x >= nwin) {
+      gr_fwd_block<DT>(a, blockIdx.x - nwin, sm);
+      return;
+    }
+    int bh, qb;
+    xcd_pair_map(blockIdx.x, a.nqb, a.H * a.B, bh, qb);
+    if constexpr (DT == 1)
+      window_fwd_v2(a, bh, qb, sm, sDyn);
+    else
+      window_fwd_block<DT>(a, bh, qb, sm, sDyn);
+    return;
+  }
   const FwdSpan f = fwd_span(a);
   int bh, c, o;
   span_block(a, f.per, bh, c, o);
@@ -1657,13 +1676,40 @@ __host__ __device__ inline ColSpan col_span(const AttnArgs& a) {
 
 // Launch 2: global-row column blocks, band-column and global-column blocks
 // (the last two only when score partials or the band layout are asked for).
-// A (sequence, head) pair's work of span c (kGlobalKeySpan keys) is the
-// band-column blocks of its keys, the global-row blocks of the same keys,
-// then the global-column blocks of its queries (the band-column blocks just
-// read those).  Pairs are dealt to the XCDs as in launch 1.
+// Span by span (a.span_major, pruned layers): a (sequence, head) pair's work
+// of span c (kGlobalKeySpan keys) is the band-column blocks of its keys, the
+// global-row blocks of the same keys, then the global-column blocks of its
+// queries, the pairs dealt to the XCDs as in launch 1.  Otherwise the
+// global-row blocks come first (long; started early they overlap the rest;
+// their count padded to a multiple of 8), then the band-column blocks pair
+// by pair (xcd_pair_map), then the global-column blocks.  The span order
+// used for every call lets the global-row and global-column blocks find the
+// span's rows in the L2 (the launch's HBM traffic at seq 4096: 151 -> 86 MB)
+// at the same time there, but was 10-13 % slower at the other single-layer
+// shapes (n 1024, and n 8192 with 64 global slots).
 template <int DT, bool kBandProbs>
 __global__ __launch_bounds__(kThreads) SC_OCC(kBandProbs ? 2 : 4) void k_attn_cols(AttnArgs a) {
   __shared__ SmemCol<DT> sm;
+  if (!a.span_major) {
+    const int ngrp = (a.n_gr + 7) & ~7;
+    int blk = blockIdx.x;
+    if (blk < ngrp) {
+      if (blk < a.n_gr) gr_col_block<DT, kBandProbs>(a, blk, sm);
+      return;
+    }
+    blk -= ngrp;
+    if (blk < a.n_bcol) {
+      int bh, kb;
+      xcd_pair_map(blk, a.nkb, a.H * a.B, bh, kb);
+      if constexpr (DT == 1 && !kBandProbs)
+        band_col_v2(a, bh, kb, sm);
+      else
+        band_col_block<DT, kBandProbs>(a, bh, kb, sm);
+      return;
+    }
+    gcol_block<DT, kBandProbs>(a, blk - a.n_bcol, sm);
+    return;
+  }
   const ColSpan f = col_span<DT, kBandProbs>(a);
   int bh, c, o;
   span_block(a, f.per, bh, c, o);
@@ -1990,9 +2036,10 @@ static hipError_t launch_window_t(const AttnArgs& a0, hipStream_t s) {
   const size_t dyn = sizeof(uint32_t) * ((size_t)a.rwp / 32 + 2 + nxc + 1);
   // the spans' block counts (the host checks that they fit the grid limits)
   const long long pairs = (long long)a.H * a.B;
-  const unsigned fwd_blocks = (unsigned)(a.nkc * fwd_span(a).per * pairs);
+  const unsigned fwd_blocks = (unsigned)(a.span_major ? a.nkc * fwd_span(a).per * pairs : a.n_gr + a.nqb * pairs);
   const int col_per = a.bp_band ? col_span<DT, true>(a).per : col_span<DT, false>(a).per;
-  const unsigned col_blocks = (unsigned)(a.nkc * col_per * pairs);
+  const unsigned col_blocks = (unsigned)(a.span_major ? a.nkc * col_per * pairs
+                                                      : ((a.n_gr + 7) & ~7) + a.n_bcol + a.n_gcol);
   if (!a.no_profile) profile_mark(s, 0);
   hipLaunchKernelGGL(k_attn_fwd<DT>, dim3(fwd_blocks), dim3(kThreads), dyn, s, a);
   if (!a.no_profile) profile_mark(s, 1);
