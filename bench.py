@@ -673,6 +673,33 @@ def probe_valu():
                                "65536 instructions per thread, median of 3 timed launches"}))
 
 
+def probe_lds():
+    """LDS read throughput per CU of ds_read_b128 and ds_read_b64_tr_b16: 1024 workgroups (4 of 4 waves per CU on
+    256 CUs, the window attention's residency), 32 KB of LDS each, groups of 8 independent reads.  Bytes per
+    cycle at the 2.4 GHz peak clock."""
+    import ctypes
+    path = os.path.join(os.path.dirname(os.path.abspath(__file__)), "paper_2310_07109_amd", "libsc_probe.so")
+    lib = ctypes.CDLL(path)
+    lib.sc_probe_lds_rate.argtypes = [ctypes.c_int, ctypes.c_int, ctypes.c_int, ctypes.POINTER(ctypes.c_double),
+                                      ctypes.POINTER(ctypes.c_double)]
+    cus, clock = 256, 2.4e9
+    res = {}
+    for op, name in ((0, "ds_read_b128"), (1, "ds_read_b64_tr_b16")):
+        runs = []
+        for _ in range(3):
+            ms, nb = ctypes.c_double(), ctypes.c_double()
+            rc = lib.sc_probe_lds_rate(op, 1024, 4096, ctypes.byref(ms), ctypes.byref(nb))
+            if rc != 0:
+                raise RuntimeError(f"probe failed: {rc}")
+            runs.append(nb.value / cus / (ms.value * 1e-3 * clock))
+        res[name] = round(median(runs), 1)
+    print(json.dumps({"probe": "LDS read throughput per CU (bytes per cycle)", "bytes_per_cycle": res,
+                      "tr_over_b128": round(res["ds_read_b64_tr_b16"] / res["ds_read_b128"], 3),
+                      "clock_ghz": clock / 1e9,
+                      "setup": "1024 workgroups x 256 threads (4 per CU), 32 KB LDS each, groups of 8 independent "
+                               "reads, 4096 groups per thread, median of 3 timed launches"}))
+
+
 def sweep(args, sc, si, torch, np):
     """Window and length sweeps of the same step (one JSON line per point).  Window sweep: B8 n4096;
     length sweep: window 512 and B = 32768 / n padded tokens; both H12 bf16, 32 global tokens, valid lengths
@@ -723,6 +750,8 @@ def main():
     ap.add_argument("--probe-valu", action="store_true",
                     help="instead of the step, measure the SIMD issue rate of v_fma_f32 and v_exp_f32 (the two VALU "
                          "forms the window attention's VALU floor counts), one JSON line")
+    ap.add_argument("--probe-lds", action="store_true",
+                    help="measure the LDS read throughput of the attention's fragment reads and exit")
     ap.add_argument("--sweep", action="store_true",
                     help="instead of the single measurement, sweep the window (n 4096) and the length (window "
                          "512), one JSON line per point")
@@ -742,6 +771,9 @@ def main():
     dev = "cuda:0"
     if args.probe_valu:
         probe_valu()
+        return
+    if args.probe_lds:
+        probe_lds()
         return
     if args.sweep:
         sweep(args, sc, si, torch, np)

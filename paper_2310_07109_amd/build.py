@@ -14,7 +14,7 @@ CSRC = os.path.join(HERE, "csrc")
 OUT = os.path.join(HERE, "libsc.so")
 # the VALU issue-rate probe behind the roofline figures (bench.py --probe-valu), a library of its own
 PROBE_OUT = os.path.join(HERE, "libsc_probe.so")
-PROBE_SOURCES = ["probe_valu.hip"]
+PROBE_SOURCES = ["probe_valu.hip", "probe_lds.hip"]
 BUILD_DIR = os.path.join(HERE, "_build")
 SOURCES = ["sc_attention.hip", "sc_prune.hip", "sc_stack.hip", "sc_backward.hip", "sc_api.hip"]
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
