@@ -1147,22 +1147,6 @@ struct FwdSpan {
   int per;  // blocks per span
 };
 
-// Block -> (pair, span c, block o of the span) for `per` blocks per span.
-// Pair by pair suits sequences that fill most of n (a pair's spans share K/V
-// rows at their borders in the L2); span by span starts every pair's first
-// spans before any pair's later ones, so after pruning, when the sequences
-// hold a few spans, the live blocks are dispatched first and the blocks past
-// the sequence ends last.
-SC_DEV void span_block(const AttnArgs& a, int per, int& bh, int& c, int& o) {
-  if (a.span_major) {
-    xcd_span_map(blockIdx.x, a.nkc, per, a.H * a.B, bh, c, o);
-  } else {
-    int j;
-    xcd_pair_map(blockIdx.x, a.nkc * per, a.H * a.B, bh, j);
-    c = j / per;
-    o = j - c * per;
-  }
-}
 __host__ __device__ inline FwdSpan fwd_span(const AttnArgs& a) { return {kSpanQB + (a.n_gr > 0 ? a.ngc : 0)}; }
 
 // Launch 1: the window pass-1 blocks and the global-row forward blocks (when
@@ -1197,7 +1181,7 @@ __global__ __launch_bounds__(kThreads) SC_OCC(DT == 1 ? 3 : 2) void k_attn_fwd(A
   }
   const FwdSpan f = fwd_span(a);
   int bh, c, o;
-  span_block(a, f.per, bh, c, o);
+  xcd_span_map(blockIdx.x, a.nkc, f.per, a.H * a.B, bh, c, o);
   if (o >= kSpanQB) {
     gr_fwd_block<DT>(a, (bh * a.ngc + (o - kSpanQB)) * a.nkc + c, sm);
     return;
@@ -1712,7 +1696,7 @@ __global__ __launch_bounds__(kThreads) SC_OCC(kBandProbs ? 2 : 4) void k_attn_co
   }
   const ColSpan f = col_span<DT, kBandProbs>(a);
   int bh, c, o;
-  span_block(a, f.per, bh, c, o);
+  xcd_span_map(blockIdx.x, a.nkc, f.per, a.H * a.B, bh, c, o);
   if (o < f.nbc) {
     const int kb = c * f.nbc + o;
     if (kb >= a.nkb) return;  // the last span's missing key blocks
