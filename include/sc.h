@@ -44,6 +44,8 @@
  *     Device-resident arguments (valid_len, global_pos) cannot be checked on
  *     the host: values outside their documented range are clamped or ignored
  *     by the kernels (memory-safe), with unspecified numerical results.
+ *     sc_validate_desc checks them on the device; the debug build of the
+ *     library (libsc_debug.so) does so before every call and refuses it.
  *   - Activations are token-major: [B, n, H, d] with d contiguous, so one token
  *     of one sequence is one contiguous row of H*d elements.
  *   - Sequence b holds valid_len[b] real tokens followed by padding.  Padding
@@ -344,6 +346,30 @@ sc_status sc_encoder_stack(const sc_attn_desc *desc, int32_t n_layers, const int
 sc_status sc_window_attention_noalloc(const sc_attn_desc *desc, const void *q, const void *k, const void *v,
                                       void *out, float *lse, float *score_partials, float *band_probs,
                                       void *stream);
+
+/*
+ * Checks the device-resident parts of a descriptor, which the host cannot
+ * read and the kernels clamp or ignore when out of range: for callers that
+ * want such inputs reported rather than computed on (and the library's debug
+ * build, below).  Enqueues on `stream` the setting of *err (a device int32
+ * owned by the caller) to the OR of the SC_VALID_* bits of the violations
+ * found, 0 when valid_len and global_pos are as sc_attn_desc documents them;
+ * the value is there once the enqueued work completes.  Capture-safe (no
+ * memset node).  Errors: those of the descriptor's host-side check, and
+ * SC_EINVAL for a null err.
+ *
+ * Debug build.  paper_2310_07109_amd/libsc_debug.so is the same library built
+ * with SC_DEBUG: every entry point that takes a descriptor first runs this
+ * check and waits for it, returning SC_EINVAL (nothing else enqueued) when a
+ * bit is set, and waits for its own work before returning, reporting a failed
+ * launch or execution as SC_EHIP.  It synchronises the stream, so it is not
+ * capture-safe; its results are the release library's.
+ */
+#define SC_VALID_LEN 1              /* a valid_len[b] outside [0, n]                      */
+#define SC_VALID_POS_RANGE 2        /* a global position below -1 or >= its valid_len[b]  */
+#define SC_VALID_POS_ORDER 4        /* used global positions not strictly ascending       */
+#define SC_VALID_POS_UNUSED_FIRST 8 /* a used slot after an unused (-1) one               */
+sc_status sc_validate_desc(const sc_attn_desc *desc, int32_t *err, void *stream);
 
 /*
  * Kernel timing for benchmarks.  While enabled, every window-attention call

@@ -15,7 +15,8 @@ from ._binding import (SC_BF16, SC_F32, SC_SCORE_FROM_BAND_PROBS, SC_SCORE_FROM_
                        sc_ltp_soft_backward_workspace_size, sc_ltp_soft_mask, sc_profile_window_kernel, sc_profile_window_kernel_read,
                        sc_score_partials_size, sc_status_str, sc_topk_prune_compact, sc_window_attention,
                        sc_window_attention_noalloc, sc_window_attention_workspace_size, SC_NOALLOC_SCRATCH_BYTES,
-                       SC_ENOSCRATCH)
+                       SC_ENOSCRATCH, SC_VALID_LEN, SC_VALID_POS_RANGE, SC_VALID_POS_ORDER,
+                       SC_VALID_POS_UNUSED_FIRST, debug_lib_path, load_debug, sc_validate_desc)
 
 __all__ = [
     "SC_BF16", "SC_F32", "SC_SCORE_FROM_PARTIALS", "SC_SCORE_FROM_BAND_PROBS", "Desc", "ScError", "load",
@@ -25,5 +26,7 @@ __all__ = [
     "sc_ltp_soft_mask", "sc_ltp_soft_backward_workspace_size", "sc_ltp_soft_backward",
     "sc_encoder_attn_stack_workspace_size", "sc_encoder_attn_stack", "sc_encoder_stack_workspace_size",
     "sc_encoder_stack", "sc_profile_window_kernel", "sc_profile_window_kernel_read",
-    "sc_window_attention_noalloc", "SC_NOALLOC_SCRATCH_BYTES", "SC_ENOSCRATCH",
+    "sc_window_attention_noalloc", "SC_NOALLOC_SCRATCH_BYTES", "SC_ENOSCRATCH", "SC_VALID_LEN",
+    "SC_VALID_POS_RANGE", "SC_VALID_POS_ORDER", "SC_VALID_POS_UNUSED_FIRST", "debug_lib_path", "load_debug",
+    "sc_validate_desc",
 ]

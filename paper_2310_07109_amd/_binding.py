@@ -7,13 +7,18 @@ import os
 
 _HERE = os.path.dirname(os.path.abspath(__file__))
 _LIB_PATH = os.path.join(_HERE, "libsc.so")
+# the same library built with SC_DEBUG (device-side argument checks, a synchronisation per call)
+_DEBUG_LIB_PATH = os.path.join(_HERE, "libsc_debug.so")
 
 SC_OK, SC_EINVAL, SC_EUNSUPPORTED, SC_EWORKSPACE, SC_EHIP, SC_ENOSCRATCH = 0, -1, -2, -3, -4, -5
 SC_NOALLOC_SCRATCH_BYTES = 16 << 20
+# bits of sc_validate_desc's result
+SC_VALID_LEN, SC_VALID_POS_RANGE, SC_VALID_POS_ORDER, SC_VALID_POS_UNUSED_FIRST = 1, 2, 4, 8
 SC_F32, SC_BF16 = 0, 1
 SC_SCORE_FROM_PARTIALS, SC_SCORE_FROM_BAND_PROBS = 0, 1
 
 _lib = None
+_debug_lib = None
 
 
 class ScError(RuntimeError):
@@ -33,14 +38,30 @@ def lib_path() -> str:
     return _LIB_PATH
 
 
+def debug_lib_path() -> str:
+    return _DEBUG_LIB_PATH
+
+
 def load():
     """Load libsc.so; raises if it has not been built (no fallback path exists)."""
     global _lib
-    if _lib is not None:
-        return _lib
-    if not os.path.exists(_LIB_PATH):
-        raise RuntimeError(f"{_LIB_PATH} is missing: build it with `python -m paper_2310_07109_amd.build`")
-    L = ctypes.CDLL(_LIB_PATH)
+    if _lib is None:
+        _lib = _open(_LIB_PATH)
+    return _lib
+
+
+def load_debug():
+    """Load libsc_debug.so, the SC_DEBUG build (same entry points and signatures); raises if it is missing."""
+    global _debug_lib
+    if _debug_lib is None:
+        _debug_lib = _open(_DEBUG_LIB_PATH)
+    return _debug_lib
+
+
+def _open(path):
+    if not os.path.exists(path):
+        raise RuntimeError(f"{path} is missing: build it with `python -m paper_2310_07109_amd.build`")
+    L = ctypes.CDLL(path)
     vp, sz, i32, f32 = ctypes.c_void_p, ctypes.c_size_t, ctypes.c_int32, ctypes.c_float
     dp = ctypes.POINTER(_Desc)
     sig = {
@@ -62,6 +83,7 @@ def load():
         "sc_encoder_attn_stack": (i32, [dp, i32, vp, vp, vp, vp, i32, f32, vp, vp, vp, vp, vp, sz, vp]),
         "sc_encoder_stack_workspace_size": (sz, [dp, i32, i32]),
         "sc_encoder_stack": (i32, [dp, i32, vp, vp, vp, vp, vp, vp, i32, vp, i32, f32, vp, vp, vp, vp, vp, sz, vp]),
+        "sc_validate_desc": (i32, [dp, vp, vp]),
         "sc_profile_window_kernel": (i32, [i32]),
         "sc_profile_window_kernel_read": (i32, [ctypes.POINTER(ctypes.c_double), ctypes.POINTER(ctypes.c_double),
                                                  ctypes.c_int64, ctypes.POINTER(ctypes.c_int64)]),
@@ -70,7 +92,6 @@ def load():
         f = getattr(L, name)
         f.restype = res
         f.argtypes = args
-    _lib = L
     return L
 
 
@@ -466,6 +487,20 @@ def sc_encoder_stack(desc: Desc, x_in, wqkv, wo, w1, w2, thresholds, windows=Non
                               int(bool(keep_global)), ctypes.c_float(ln_eps), _ptr(x_out), _ptr(final_len),
                               _ptr(orig), _ptr(kpl), _ptr(ws), wsb, _stream(stream)), "sc_encoder_stack")
     return x_out, final_len, orig, kpl
+
+
+@_on_stream
+def sc_validate_desc(desc: Desc, err=None, stream=None):
+    """Enqueues the check of the descriptor's device arrays (valid_len, global_pos); returns the int32 [1]
+    device tensor that receives the OR of the SC_VALID_* bits of the violations found (0: none)."""
+    import torch
+    L = load()
+    cd = desc.c()
+    if err is None:
+        err = torch.empty(1, dtype=torch.int32, device=desc.valid_len.device)
+    _tensor(err, "err", torch.int32, (1,))
+    _check(L.sc_validate_desc(ctypes.byref(cd), _ptr(err), _stream(stream)), "sc_validate_desc")
+    return err
 
 
 def sc_profile_window_kernel(enable: bool):

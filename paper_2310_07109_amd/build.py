@@ -12,6 +12,9 @@ from concurrent.futures import ThreadPoolExecutor
 HERE = os.path.dirname(os.path.abspath(__file__))
 CSRC = os.path.join(HERE, "csrc")
 OUT = os.path.join(HERE, "libsc.so")
+# the same library with SC_DEBUG: device-side argument checks and a synchronisation per call (include/sc.h)
+DEBUG_OUT = os.path.join(HERE, "libsc_debug.so")
+DEBUG_SOURCE = "sc_api.hip"  # the only source SC_DEBUG changes
 # the VALU issue-rate probe behind the roofline figures (bench.py --probe-valu), a library of its own
 PROBE_OUT = os.path.join(HERE, "libsc_probe.so")
 PROBE_SOURCES = ["probe_valu.hip", "probe_lds.hip"]
@@ -31,9 +34,9 @@ FLAGS = [
 ]
 
 
-def _compile(src: str) -> str:
-    obj = os.path.join(BUILD_DIR, os.path.splitext(src)[0] + ".o")
-    cmd = [HIPCC, *FLAGS, "-c", os.path.join(CSRC, src), "-o", obj]
+def _compile(src: str, debug: bool = False) -> str:
+    obj = os.path.join(BUILD_DIR, os.path.splitext(src)[0] + ("_debug.o" if debug else ".o"))
+    cmd = [HIPCC, *FLAGS, *(["-DSC_DEBUG"] if debug else []), "-c", os.path.join(CSRC, src), "-o", obj]
     r = subprocess.run(cmd, capture_output=True, text=True)
     if r.returncode != 0:
         raise RuntimeError(f"hipcc failed on {src}:\n{r.stderr}")
@@ -51,12 +54,14 @@ def _link(objs: list, out: str) -> None:
 
 def build(verbose: bool = False) -> str:
     os.makedirs(BUILD_DIR, exist_ok=True)
-    with ThreadPoolExecutor(max_workers=len(SOURCES) + len(PROBE_SOURCES)) as ex:
+    with ThreadPoolExecutor(max_workers=len(SOURCES) + len(PROBE_SOURCES) + 1) as ex:
         objs = list(ex.map(_compile, SOURCES + PROBE_SOURCES))
+        debug_obj = ex.submit(_compile, DEBUG_SOURCE, True).result()
     _link(objs[:len(SOURCES)], OUT)
+    _link([debug_obj if s == DEBUG_SOURCE else o for s, o in zip(SOURCES, objs)], DEBUG_OUT)
     _link(objs[len(SOURCES):], PROBE_OUT)
     if verbose:
-        print("built", OUT, "and", PROBE_OUT)
+        print("built", OUT, DEBUG_OUT, "and", PROBE_OUT)
     return OUT
 
 

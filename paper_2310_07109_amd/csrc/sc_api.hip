@@ -120,6 +120,52 @@ size_t attn_ws_size(const sc_attn_desc* d) {
 
 }  // namespace
 
+#ifdef SC_DEBUG
+// Debug build: the device word of the descriptor check.
+static __device__ int32_t g_debug_err;
+#endif
+
+namespace {
+#ifdef SC_DEBUG
+// Debug build: before an entry point enqueues anything, its descriptor's
+// device-resident arrays are checked and the stream drained; then the entry
+// point's own work is waited for and a failed launch or execution reported.
+sc_status debug_pre(const sc_attn_desc* d, void* stream) {
+  if (check_desc(d) != SC_OK) return SC_OK;  // the entry point reports it
+  int32_t* err = nullptr;
+  if (hipGetSymbolAddress(reinterpret_cast<void**>(&err), HIP_SYMBOL(g_debug_err)) != hipSuccess || !err)
+    return SC_EHIP;
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  if (sc::launch_validate_desc(d->valid_len, d->G > 0 ? d->global_pos : nullptr, d->B, d->n, d->G, err, s) !=
+      hipSuccess)
+    return SC_EHIP;
+  int32_t bits = 0;
+  if (hipMemcpyAsync(&bits, err, sizeof(bits), hipMemcpyDeviceToHost, s) != hipSuccess ||
+      hipStreamSynchronize(s) != hipSuccess)
+    return SC_EHIP;
+  return bits != 0 ? SC_EINVAL : SC_OK;
+}
+
+sc_status debug_post(sc_status st, void* stream) {
+  if (st != SC_OK) return st;
+  if (hipStreamSynchronize(static_cast<hipStream_t>(stream)) != hipSuccess || hipGetLastError() != hipSuccess)
+    return SC_EHIP;
+  return SC_OK;
+}
+#endif
+}  // namespace
+
+#ifdef SC_DEBUG
+#define SC_DEBUG_CALL(d, stream, call)          \
+  do {                                          \
+    const sc_status pre_ = debug_pre(d, stream); \
+    if (pre_ != SC_OK) return pre_;             \
+    return debug_post(call, stream);            \
+  } while (0)
+#else
+#define SC_DEBUG_CALL(d, stream, call) return call
+#endif
+
 extern "C" {
 
 const char* sc_status_str(sc_status s) {
@@ -234,14 +280,23 @@ sc_status scratch_address(void* stream, void** addr) {
 
 extern "C" {
 
-sc_status sc_window_attention(const sc_attn_desc* d, const void* q, const void* k, const void* v, void* out,
-                              float* lse, float* score_partials, float* band_probs, void* workspace,
-                              size_t ws_bytes, void* stream) {
+static sc_status sc_window_attention_impl(const sc_attn_desc* d, const void* q, const void* k, const void* v, void* out,
+                                          float* lse, float* score_partials, float* band_probs, void* workspace,
+                                          size_t ws_bytes, void* stream) {
   return window_attention(d, q, k, v, out, lse, score_partials, band_probs, workspace, ws_bytes, stream, false);
 }
 
-sc_status sc_window_attention_noalloc(const sc_attn_desc* d, const void* q, const void* k, const void* v, void* out,
-                                      float* lse, float* score_partials, float* band_probs, void* stream) {
+sc_status sc_window_attention(const sc_attn_desc* d, const void* q, const void* k, const void* v, void* out, float* lse,
+                              float* score_partials, float* band_probs, void* workspace, size_t ws_bytes,
+                              void* stream) {
+  SC_DEBUG_CALL(d, stream,
+                sc_window_attention_impl(d, q, k, v, out, lse, score_partials, band_probs, workspace, ws_bytes,
+                                         stream));
+}
+
+static sc_status sc_window_attention_noalloc_impl(const sc_attn_desc* d, const void* q, const void* k, const void* v,
+                                                  void* out, float* lse, float* score_partials, float* band_probs,
+                                                  void* stream) {
   sc_status st = check_desc(d);
   if (st != SC_OK) return st;
   if (attn_ws_size(d) > (size_t)SC_NOALLOC_SCRATCH_BYTES) return SC_ENOSCRATCH;
@@ -252,14 +307,20 @@ sc_status sc_window_attention_noalloc(const sc_attn_desc* d, const void* q, cons
                           stream, true);
 }
 
+sc_status sc_window_attention_noalloc(const sc_attn_desc* d, const void* q, const void* k, const void* v, void* out,
+                                      float* lse, float* score_partials, float* band_probs, void* stream) {
+  SC_DEBUG_CALL(d, stream,
+                sc_window_attention_noalloc_impl(d, q, k, v, out, lse, score_partials, band_probs, stream));
+}
+
 size_t sc_ltp_score_workspace_size(const sc_attn_desc* d, int32_t mode) {
   // the band layout is first reduced to the partials of the fused path
   if (mode != SC_SCORE_FROM_BAND_PROBS || check_desc(d) != SC_OK) return 0;
   return sc_score_partials_size(d);
 }
 
-sc_status sc_ltp_score(const sc_attn_desc* d, int32_t mode, const float* src, float* scores, void* workspace,
-                       size_t ws_bytes, void* stream) {
+static sc_status sc_ltp_score_impl(const sc_attn_desc* d, int32_t mode, const float* src, float* scores,
+                                   void* workspace, size_t ws_bytes, void* stream) {
   sc_status st = check_desc(d);
   if (st != SC_OK) return st;
   if (!src || !scores) return SC_EINVAL;
@@ -280,6 +341,12 @@ sc_status sc_ltp_score(const sc_attn_desc* d, int32_t mode, const float* src, fl
                      : sc::launch_score_from_band(src, d->valid_len, d->global_pos, d->B, d->n, d->H, d->G, geo,
                                                   static_cast<float*>(workspace), scores, s);
   return e == hipSuccess ? SC_OK : SC_EHIP;
+}
+
+sc_status sc_ltp_score(const sc_attn_desc* d, int32_t mode, const float* src, float* scores, void* workspace,
+                       size_t ws_bytes, void* stream) {
+  SC_DEBUG_CALL(d, stream,
+                sc_ltp_score_impl(d, mode, src, scores, workspace, ws_bytes, stream));
 }
 
 size_t sc_ltp_prune_compact_workspace_size(const sc_attn_desc* d) {
@@ -347,12 +414,32 @@ sc_status prune_compact(const sc_attn_desc* d, const float* scores, float thresh
 
 }  // namespace
 
+static sc_status sc_ltp_prune_compact_impl(const sc_attn_desc* d, const float* scores, float threshold,
+                                           int32_t keep_global, int32_t n_tensors, const void* const* src,
+                                           void* const* dst, const int64_t* row_bytes, int32_t* keep_idx,
+                                           int32_t* new_len, int32_t* new_global_pos, const int32_t* orig_idx_in,
+                                           int32_t* orig_idx_out, void* workspace, size_t ws_bytes, void* stream) {
+  return prune_compact(d, scores, threshold, 0, 0.f, keep_global, n_tensors, src, dst, row_bytes, keep_idx, new_len,
+                       new_global_pos, orig_idx_in, orig_idx_out, workspace, ws_bytes, stream);
+}
+
 sc_status sc_ltp_prune_compact(const sc_attn_desc* d, const float* scores, float threshold, int32_t keep_global,
                                int32_t n_tensors, const void* const* src, void* const* dst, const int64_t* row_bytes,
-                               int32_t* keep_idx, int32_t* new_len, int32_t* new_global_pos,
-                               const int32_t* orig_idx_in, int32_t* orig_idx_out, void* workspace, size_t ws_bytes,
-                               void* stream) {
-  return prune_compact(d, scores, threshold, 0, 0.f, keep_global, n_tensors, src, dst, row_bytes, keep_idx, new_len,
+                               int32_t* keep_idx, int32_t* new_len, int32_t* new_global_pos, const int32_t* orig_idx_in,
+                               int32_t* orig_idx_out, void* workspace, size_t ws_bytes, void* stream) {
+  SC_DEBUG_CALL(d, stream,
+                sc_ltp_prune_compact_impl(d, scores, threshold, keep_global, n_tensors, src, dst, row_bytes,
+                                          keep_idx, new_len, new_global_pos, orig_idx_in, orig_idx_out, workspace,
+                                          ws_bytes, stream));
+}
+
+static sc_status sc_topk_prune_compact_impl(const sc_attn_desc* d, const float* scores, float keep_ratio,
+                                            int32_t keep_global, int32_t n_tensors, const void* const* src,
+                                            void* const* dst, const int64_t* row_bytes, int32_t* keep_idx,
+                                            int32_t* new_len, int32_t* new_global_pos, const int32_t* orig_idx_in,
+                                            int32_t* orig_idx_out, void* workspace, size_t ws_bytes, void* stream) {
+  if (!(keep_ratio >= 0.f && keep_ratio <= 1.f)) return SC_EINVAL;  // also rejects NaN
+  return prune_compact(d, scores, 0.f, 1, keep_ratio, keep_global, n_tensors, src, dst, row_bytes, keep_idx, new_len,
                        new_global_pos, orig_idx_in, orig_idx_out, workspace, ws_bytes, stream);
 }
 
@@ -361,9 +448,10 @@ sc_status sc_topk_prune_compact(const sc_attn_desc* d, const float* scores, floa
                                 int32_t* keep_idx, int32_t* new_len, int32_t* new_global_pos,
                                 const int32_t* orig_idx_in, int32_t* orig_idx_out, void* workspace, size_t ws_bytes,
                                 void* stream) {
-  if (!(keep_ratio >= 0.f && keep_ratio <= 1.f)) return SC_EINVAL;  // also rejects NaN
-  return prune_compact(d, scores, 0.f, 1, keep_ratio, keep_global, n_tensors, src, dst, row_bytes, keep_idx, new_len,
-                       new_global_pos, orig_idx_in, orig_idx_out, workspace, ws_bytes, stream);
+  SC_DEBUG_CALL(d, stream,
+                sc_topk_prune_compact_impl(d, scores, keep_ratio, keep_global, n_tensors, src, dst, row_bytes,
+                                           keep_idx, new_len, new_global_pos, orig_idx_in, orig_idx_out, workspace,
+                                           ws_bytes, stream));
 }
 
 // ------------------------------------------------------------ soft pruning --
@@ -415,8 +503,8 @@ sc::SoftArgs soft_args(const sc_attn_desc* d) {
 
 }  // namespace
 
-sc_status sc_ltp_soft_mask(const sc_attn_desc* d, const float* scores, float theta, float temperature,
-                           int32_t keep_global, const void* out, float* mask, void* y, void* stream) {
+static sc_status sc_ltp_soft_mask_impl(const sc_attn_desc* d, const float* scores, float theta, float temperature,
+                                       int32_t keep_global, const void* out, float* mask, void* y, void* stream) {
   sc_status st;
   if (!soft_desc_ok(d, &st)) return st;
   if (!scores || !out || !mask || !y) return SC_EINVAL;
@@ -436,6 +524,12 @@ sc_status sc_ltp_soft_mask(const sc_attn_desc* d, const float* scores, float the
   return sc::launch_soft_mask(a, static_cast<hipStream_t>(stream)) == hipSuccess ? SC_OK : SC_EHIP;
 }
 
+sc_status sc_ltp_soft_mask(const sc_attn_desc* d, const float* scores, float theta, float temperature,
+                           int32_t keep_global, const void* out, float* mask, void* y, void* stream) {
+  SC_DEBUG_CALL(d, stream,
+                sc_ltp_soft_mask_impl(d, scores, theta, temperature, keep_global, out, mask, y, stream));
+}
+
 size_t sc_ltp_soft_backward_workspace_size(const sc_attn_desc* d) {
   sc_status st;
   if (!soft_desc_ok(d, &st)) return 0;
@@ -443,10 +537,10 @@ size_t sc_ltp_soft_backward_workspace_size(const sc_attn_desc* d) {
   return carve_soft(d, nullptr, &a);
 }
 
-sc_status sc_ltp_soft_backward(const sc_attn_desc* d, const void* q, const void* k, const void* v, const void* out,
-                               const float* lse, const float* mask, float temperature, int32_t keep_global,
-                               const void* dy, const float* dmask, void* dq, void* dk, void* dv, float* dtheta,
-                               void* workspace, size_t ws_bytes, void* stream) {
+static sc_status sc_ltp_soft_backward_impl(const sc_attn_desc* d, const void* q, const void* k, const void* v,
+                                           const void* out, const float* lse, const float* mask, float temperature,
+                                           int32_t keep_global, const void* dy, const float* dmask, void* dq, void* dk,
+                                           void* dv, float* dtheta, void* workspace, size_t ws_bytes, void* stream) {
   sc_status st;
   if (!soft_desc_ok(d, &st)) return st;
   if (!q || !k || !v || !out || !lse || !mask || !dy || !dq || !dk || !dv || !dtheta) return SC_EINVAL;
@@ -487,6 +581,15 @@ sc_status sc_ltp_soft_backward(const sc_attn_desc* d, const void* q, const void*
   a.inv_t = 1.f / temperature;
   a.keep_global = keep_global ? 1 : 0;
   return sc::launch_soft_backward(a, static_cast<hipStream_t>(stream)) == hipSuccess ? SC_OK : SC_EHIP;
+}
+
+sc_status sc_ltp_soft_backward(const sc_attn_desc* d, const void* q, const void* k, const void* v, const void* out,
+                               const float* lse, const float* mask, float temperature, int32_t keep_global,
+                               const void* dy, const float* dmask, void* dq, void* dk, void* dv, float* dtheta,
+                               void* workspace, size_t ws_bytes, void* stream) {
+  SC_DEBUG_CALL(d, stream,
+                sc_ltp_soft_backward_impl(d, q, k, v, out, lse, mask, temperature, keep_global, dy, dmask, dq, dk,
+                                          dv, dtheta, workspace, ws_bytes, stream));
 }
 
 // ------------------------------------------------------------------ stack --
@@ -671,13 +774,22 @@ size_t sc_encoder_attn_stack_workspace_size(const sc_attn_desc* d, int32_t n_lay
   return carve_stack(d, 0, nullptr, nullptr);
 }
 
-sc_status sc_encoder_attn_stack(const sc_attn_desc* d, int32_t n_layers, const void* x_in,
-                                const void* const* Wqkv, const void* const* Wo, const float* thresholds,
-                                int32_t keep_global, float ln_eps, void* x_out, int32_t* final_len,
-                                int32_t* orig_idx, int32_t* kept_per_layer, void* workspace, size_t ws_bytes,
-                                void* stream) {
+static sc_status sc_encoder_attn_stack_impl(const sc_attn_desc* d, int32_t n_layers, const void* x_in,
+                                            const void* const* Wqkv, const void* const* Wo, const float* thresholds,
+                                            int32_t keep_global, float ln_eps, void* x_out, int32_t* final_len,
+                                            int32_t* orig_idx, int32_t* kept_per_layer, void* workspace,
+                                            size_t ws_bytes, void* stream) {
   return run_stack(d, n_layers, nullptr, x_in, Wqkv, Wo, nullptr, nullptr, 0, thresholds, keep_global, ln_eps, x_out,
                    final_len, orig_idx, kept_per_layer, workspace, ws_bytes, stream);
+}
+
+sc_status sc_encoder_attn_stack(const sc_attn_desc* d, int32_t n_layers, const void* x_in, const void* const* Wqkv,
+                                const void* const* Wo, const float* thresholds, int32_t keep_global, float ln_eps,
+                                void* x_out, int32_t* final_len, int32_t* orig_idx, int32_t* kept_per_layer,
+                                void* workspace, size_t ws_bytes, void* stream) {
+  SC_DEBUG_CALL(d, stream,
+                sc_encoder_attn_stack_impl(d, n_layers, x_in, Wqkv, Wo, thresholds, keep_global, ln_eps, x_out,
+                                           final_len, orig_idx, kept_per_layer, workspace, ws_bytes, stream));
 }
 
 size_t sc_encoder_stack_workspace_size(const sc_attn_desc* d, int32_t n_layers, int32_t ffn_dim) {
@@ -685,14 +797,36 @@ size_t sc_encoder_stack_workspace_size(const sc_attn_desc* d, int32_t n_layers, 
   return carve_stack(d, ffn_dim, nullptr, nullptr);
 }
 
-sc_status sc_encoder_stack(const sc_attn_desc* d, int32_t n_layers, const int32_t* windows, const void* x_in,
-                           const void* const* Wqkv, const void* const* Wo, const void* const* W1,
-                           const void* const* W2, int32_t ffn_dim, const float* thresholds, int32_t keep_global,
-                           float ln_eps, void* x_out, int32_t* final_len, int32_t* orig_idx, int32_t* kept_per_layer,
-                           void* workspace, size_t ws_bytes, void* stream) {
+static sc_status sc_encoder_stack_impl(const sc_attn_desc* d, int32_t n_layers, const int32_t* windows,
+                                       const void* x_in, const void* const* Wqkv, const void* const* Wo,
+                                       const void* const* W1, const void* const* W2, int32_t ffn_dim,
+                                       const float* thresholds, int32_t keep_global, float ln_eps, void* x_out,
+                                       int32_t* final_len, int32_t* orig_idx, int32_t* kept_per_layer, void* workspace,
+                                       size_t ws_bytes, void* stream) {
   if (!W1 || !W2) return SC_EINVAL;
   return run_stack(d, n_layers, windows, x_in, Wqkv, Wo, W1, W2, ffn_dim, thresholds, keep_global, ln_eps, x_out,
                    final_len, orig_idx, kept_per_layer, workspace, ws_bytes, stream);
+}
+
+sc_status sc_encoder_stack(const sc_attn_desc* d, int32_t n_layers, const int32_t* windows, const void* x_in,
+                           const void* const* Wqkv, const void* const* Wo, const void* const* W1, const void* const* W2,
+                           int32_t ffn_dim, const float* thresholds, int32_t keep_global, float ln_eps, void* x_out,
+                           int32_t* final_len, int32_t* orig_idx, int32_t* kept_per_layer, void* workspace,
+                           size_t ws_bytes, void* stream) {
+  SC_DEBUG_CALL(d, stream,
+                sc_encoder_stack_impl(d, n_layers, windows, x_in, Wqkv, Wo, W1, W2, ffn_dim, thresholds, keep_global,
+                                      ln_eps, x_out, final_len, orig_idx, kept_per_layer, workspace, ws_bytes,
+                                      stream));
+}
+
+sc_status sc_validate_desc(const sc_attn_desc* d, int32_t* err, void* stream) {
+  const sc_status st = check_desc(d);
+  if (st != SC_OK) return st;
+  if (!err) return SC_EINVAL;
+  return sc::launch_validate_desc(d->valid_len, d->G > 0 ? d->global_pos : nullptr, d->B, d->n, d->G, err,
+                                  static_cast<hipStream_t>(stream)) == hipSuccess
+             ? SC_OK
+             : SC_EHIP;
 }
 
 sc_status sc_profile_window_kernel(int32_t enable) {

@@ -154,6 +154,14 @@ hipError_t launch_gemm_bf16(const void* x, const void* w, void* y, int mode, int
 hipError_t launch_residual_layernorm(const void* x_res, const float* t, void* y, int B, int n, int D, float eps,
                                      const int* len, const float* part, int K, hipStream_t s);
 hipError_t launch_fill_zero(void* p, size_t bytes, hipStream_t s);
+// Bits of the device-side descriptor check (the same values as SC_VALID_* in
+// sc.h): a length outside [0, n]; a global position below -1 or not below
+// its sequence's length; used positions not strictly ascending; a used slot
+// after an unused one.
+constexpr int kValidLen = 1, kValidPosRange = 2, kValidPosOrder = 4, kValidPosUnusedFirst = 8;
+// *err = 0, then the bits of the violations found in valid_len [B] and
+// gpos [B, G] (NULL when G == 0).
+hipError_t launch_validate_desc(const int* valid_len, const int* gpos, int B, int n, int G, int* err, hipStream_t s);
 hipError_t launch_copy_i32(const int* src, int* dst, long long count, hipStream_t s);
 hipError_t launch_iota_orig(const int* valid_len, int* orig, int B, int n, hipStream_t s);
 

@@ -411,6 +411,30 @@ __global__ void k_fill_zero(uint32_t* p, long long words) {
   }
 }
 
+// Device-resident preconditions of one sequence's descriptor arrays (one
+// wave per sequence): 0 <= valid_len[b] <= n; global slots hold ascending,
+// distinct positions below valid_len[b], then only unused (-1) slots.  The
+// violations found are OR-ed into *err as SC_VALID_* bits.
+__global__ __launch_bounds__(64) void k_validate_desc(const int* valid_len, const int* gpos, int n, int G,
+                                                      int* err) {
+  const int b = blockIdx.x, lane = threadIdx.x;
+  const int L = valid_len[b];
+  int bits = 0;
+  if (lane == 0 && (L < 0 || L > n)) bits |= kValidLen;
+  if (gpos) {
+    const int* gp = gpos + (long long)b * G;
+    for (int j = lane; j < G; j += 64) {
+      const int p = gp[j], prev = j > 0 ? gp[j - 1] : -2;
+      if (p < -1 || p >= L) bits |= kValidPosRange;
+      if (p >= 0 && prev == -1) bits |= kValidPosUnusedFirst;
+      if (p >= 0 && prev >= 0 && prev >= p) bits |= kValidPosOrder;
+    }
+  }
+  // one atomic per kind of violation and wave (vector memory atomics)
+  for (int bit = 1; bit <= kValidPosUnusedFirst; bit <<= 1)
+    if (__ballot((bits & bit) != 0) != 0ull && lane == 0) atomicOr(err, bit);
+}
+
 __global__ void k_copy_i32(const int* src, int* dst, long long count) {
   const long long i = (long long)blockIdx.x * blockDim.x + threadIdx.x;
   if (i < count) dst[i] = src[i];
@@ -456,6 +480,13 @@ hipError_t launch_fill_zero(void* p, size_t bytes, hipStream_t s) {
   const long long threads = (reinterpret_cast<uintptr_t>(p) & 15) == 0 ? std::max(words >> 2, 3LL) : words;
   hipLaunchKernelGGL(k_fill_zero, dim3((unsigned)((threads + 255) / 256)), dim3(256), 0, s, static_cast<uint32_t*>(p),
                      words);
+  return hipGetLastError();
+}
+
+hipError_t launch_validate_desc(const int* valid_len, const int* gpos, int B, int n, int G, int* err, hipStream_t s) {
+  const hipError_t e = launch_fill_zero(err, sizeof(int), s);
+  if (e != hipSuccess) return e;
+  hipLaunchKernelGGL(k_validate_desc, dim3((unsigned)B), dim3(64), 0, s, valid_len, gpos, n, G, err);
   return hipGetLastError();
 }
 

@@ -25,9 +25,31 @@ def declared_functions():
 def test_exports_every_declared_symbol():
     L = sc.load()
     names = declared_functions()
-    assert len(names) == 20
+    assert len(names) == 21
     for name in names:
         assert hasattr(L, name), name
+
+
+@pytest.mark.skipif(not os.path.exists(sc.debug_lib_path()), reason="libsc_debug.so not built")
+def test_debug_library_exports_the_same_entry_points():
+    L = sc.load_debug()
+    for name in declared_functions():
+        assert hasattr(L, name), name
+    # its host-side checks are the release library's (nothing reaches the device-side check or a launch)
+    assert L.sc_window_attention(ctypes.byref(desc(d=32).c()), 0x100000, 0x200000, 0x300000, 0x400000, None, None,
+                                 None, None, 0, None) == B.SC_EUNSUPPORTED
+    assert L.sc_window_attention(ctypes.byref(desc().c()), None, 0x200000, 0x300000, 0x400000, None, None, None,
+                                 None, 0, None) in (B.SC_EINVAL, B.SC_EHIP)
+
+
+def test_validate_desc_host_checks():
+    """sc_validate_desc rejects on the host (no launch) a null result word and an invalid descriptor."""
+    L = sc.load()
+    assert L.sc_validate_desc(ctypes.byref(desc().c()), None, None) == B.SC_EINVAL
+    assert L.sc_validate_desc(ctypes.byref(desc(B=0).c()), 0x700000, None) == B.SC_EINVAL
+    assert L.sc_validate_desc(ctypes.byref(desc(G=3).c()), 0x700000, None) == B.SC_EINVAL
+    assert L.sc_validate_desc(ctypes.byref(desc(d=32).c()), 0x700000, None) == B.SC_EUNSUPPORTED
+    assert L.sc_validate_desc(None, 0x700000, None) == B.SC_EINVAL
 
 
 def test_status_strings():
