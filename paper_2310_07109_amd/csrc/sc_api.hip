@@ -705,7 +705,7 @@ sc_status run_stack(const sc_attn_desc* d, int32_t n_layers, const int32_t* wind
     a.bs_out = a.ld_out * n;
     a.lse = nullptr;
     a.skip_pad_out = 1;  // O is read only at the kept rows (the gather below)
-    a.span_major = l > 0 ? 1 : 0;  // pruned layers: short sequences in an n-row batch
+    a.span_major = l > 0 ? 1 : 0;  // pruned layers: short sequences in an n-row batch (n up to 4096: always)
     a.valid_len = len_cur;
     a.gpos = G > 0 ? gp_cur : nullptr;
     set_partials(a, w.partials);

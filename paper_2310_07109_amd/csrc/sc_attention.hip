@@ -1150,17 +1150,15 @@ struct FwdSpan {
 __host__ __device__ inline FwdSpan fwd_span(const AttnArgs& a) { return {kSpanQB + (a.n_gr > 0 ? a.ngc : 0)}; }
 
 // Launch 1: the window pass-1 blocks and the global-row forward blocks (when
-// there are global tokens).  Span by span (a.span_major, pruned layers): a
-// (sequence, head) pair's work of key span c (kGlobalKeySpan keys) is the
-// window blocks of its queries, then the global-row blocks of its keys,
-// which the window blocks just read (they are still in the XCD's L2); the
-// pairs are dealt round-robin to the XCDs, a pair's work on one XCD
-// (xcd_span_map).  Otherwise the window blocks come first, pair by pair
+// there are global tokens).  Span by span (a.span_major: sequences up to
+// kSpanOrderMaxN tokens, and the pruned layers of a stack): a (sequence,
+// head) pair's work of key span c (kGlobalKeySpan keys) is the window blocks
+// of its queries, then the global-row blocks of its keys, which the window
+// blocks just read (they are still in the XCD's L2); the pairs are dealt
+// round-robin to the XCDs, a pair's work on one XCD (xcd_span_map).
+// Otherwise (longer sequences) the window blocks come first, pair by pair
 // (xcd_pair_map), and the global-row blocks last, where they fill the window
-// blocks' uneven tail.  The span order used for every call cut the launch's
-// HBM traffic at seq 4096 from 221 to 154 MB and its time by 1.5 %, but
-// cost 5 % at the other single-layer shapes (n 1024, and n 8192 with 64
-// global slots).
+// blocks' uneven tail.
 template <int DT>
 __global__ __launch_bounds__(kThreads) SC_OCC(DT == 1 ? 3 : 2) void k_attn_fwd(AttnArgs a) {
   __shared__ Smem<DT> sm;
@@ -1660,17 +1658,14 @@ __host__ __device__ inline ColSpan col_span(const AttnArgs& a) {
 
 // Launch 2: global-row column blocks, band-column and global-column blocks
 // (the last two only when score partials or the band layout are asked for).
-// Span by span (a.span_major, pruned layers): a (sequence, head) pair's work
+// Span by span (a.span_major, as in launch 1): a (sequence, head) pair's work
 // of span c (kGlobalKeySpan keys) is the band-column blocks of its keys, the
 // global-row blocks of the same keys, then the global-column blocks of its
-// queries, the pairs dealt to the XCDs as in launch 1.  Otherwise the
+// queries, the pairs dealt to the XCDs as in launch 1; the global-row and
+// global-column blocks find the span's rows in the L2.  Otherwise the
 // global-row blocks come first (long; started early they overlap the rest;
 // their count padded to a multiple of 8), then the band-column blocks pair
-// by pair (xcd_pair_map), then the global-column blocks.  The span order
-// used for every call lets the global-row and global-column blocks find the
-// span's rows in the L2 (the launch's HBM traffic at seq 4096: 151 -> 86 MB)
-// at the same time there, but was 10-13 % slower at the other single-layer
-// shapes (n 1024, and n 8192 with 64 global slots).
+// by pair (xcd_pair_map), then the global-column blocks.
 template <int DT, bool kBandProbs>
 __global__ __launch_bounds__(kThreads) SC_OCC(kBandProbs ? 2 : 4) void k_attn_cols(AttnArgs a) {
   __shared__ SmemCol<DT> sm;
@@ -2002,9 +1997,21 @@ int profile_read(double* fwd_ms, double* cols_ms, long long cap, long long* call
   return 0;
 }
 
+// Sequences up to this length are dispatched span by span.  Measured against
+// the pair-by-pair order (both launches, bf16, H12 unless noted): as fast or
+// faster at every shape up to seq 4096 (B8 n4096 window 512, 32 global
+// slots: launch 2 -1 %, HBM traffic 371 -> 245 MB; window 256: launch 2 -6 %;
+// 64 slots: -9 %; B64 n1024 window 256 with paper-shaped lengths: -7.5 % and
+// -15 %; B8 n1024, B16 n2048: within 1 %), slower at n 8192 (B4 window 512:
+// +2 % and +3 %; B2 H16 window 1024 with 64 slots: +5 % and +11 %), where a
+// pair's window blocks alone fill an XCD and its K and V stay in that XCD's
+// L2 in the pair order.
+constexpr int kSpanOrderMaxN = 4096;
+
 template <int DT>
 static hipError_t launch_window_t(const AttnArgs& a0, hipStream_t s) {
   AttnArgs a = a0;
+  if (a.n <= kSpanOrderMaxN) a.span_major = 1;
   const bool glob = a.G > 0 && a.gpos;
   const bool cols = a.part_band || a.bp_band;
   a.n_gr = glob ? a.nkc * a.ngc * a.H * a.B : 0;

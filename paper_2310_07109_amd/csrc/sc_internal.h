@@ -29,6 +29,7 @@ struct AttnArgs {
   int no_profile;         // 1: never record benchmark events for this call
   int span_major;         // 1: dispatch the attention blocks span-major (xcd_span_map), for
                           //    sequences much shorter than n; 0: pair by pair (xcd_pair_map)
+                          //    unless n is at most 4096 (the launch then takes the span order)
   float c2;               // softmax scale * log2(e)
   // score partials (null: skip the exact-probability column sums)
   float* part_band;       // [B, H, n]      band column sums of non-global keys
