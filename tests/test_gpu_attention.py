@@ -352,3 +352,57 @@ def test_prune_compact_fused_and_fallback_paths(kg):
             assert np.array_equal(d_np[b, :rnl[b]], s_np[b, rk[b, :rnl[b]]])
     log(f"fused / fallback prune (keep_global={kg}): kept {rnl.tolist()}, globals kept "
         f"{[(int((rngp[b] >= 0).sum())) for b in range(B)]}")
+
+
+# Batches of sequences longer than 4096 tokens take the pair-by-pair dispatch of the attention blocks (shorter ones
+# the span order, which every case above runs); these cases run the pair order against the oracle.
+PAIR_ORDER = [
+    # name, dtype, B, n, H, window, G, len range, causal
+    ("pair order bf16 two slot chunks", "bf16", 2, 4224, 2, 256, 40, (3000, 4224), False),
+    ("pair order fp32", "f32", 1, 4160, 2, 128, 3, (4100, 4160), False),
+    ("pair order causal", "bf16", 2, 4160, 2, 512, 33, (2500, 4160), True),
+]
+
+
+@pytest.mark.parametrize("case", PAIR_ORDER, ids=[c[0] for c in PAIR_ORDER])
+def test_pair_order_cases(case):
+    name, dtype, B, n, H, window, G, lr, causal = case
+    log(f"case {name}")
+    inp = small_case(name, dtype, B, n, H, window, G, lr)
+    ro, rl, rs = oracle.sparse_attention(inp["q64"], inp["k64"], inp["v64"], inp["valid_len"], inp["global_pos"],
+                                         window, inp["alpha"], causal=causal)
+    d = make_desc(inp)
+    d.causal = int(causal)
+    q, k, v = (to_dev_storage(inp[x], dtype) for x in ("q", "k", "v"))
+    out, lse, sp, _ = sc.sc_window_attention(d, q, k, v, lse=True, score_partials=True)
+    scores = sc.sc_ltp_score(d, sp)
+    torch.cuda.synchronize()
+    check_out(out.float().cpu().numpy(), ro, dtype)
+    check_lse(lse.cpu().numpy(), rl, inp["valid_len"])
+    check_scores(scores.cpu().numpy(), rs, inp["valid_len"])
+
+
+@pytest.mark.parametrize("causal", [0, 1])
+def test_dispatch_order_invariance(causal):
+    """The same sequences in an n = 4096 batch (span order) and, padded, in an n = 4160 batch (pair order) give
+    bit-identical outputs, LSE and scores on their valid rows: every block computes the same values, in the same
+    order, whichever order the blocks are dispatched in."""
+    inp = small_case("order", "bf16", 3, 4096, 2, 512, 32, (1000, 4096), lens=[4096, 2345, 1000])
+    n2 = 4160
+    res = []
+    for n in (4096, n2):
+        q, k, v = (np.zeros((inp["B"], n) + inp[x].shape[2:], inp[x].dtype) for x in ("q", "k", "v"))
+        q[:, :4096], k[:, :4096], v[:, :4096] = inp["q"], inp["k"], inp["v"]
+        d = sc.Desc(inp["B"], n, inp["H"], inp["window"], dev_i32(inp["valid_len"]), dev_i32(inp["global_pos"]),
+                    inp["alpha"], sc.SC_BF16)
+        d.causal = causal
+        out, lse, sp, _ = sc.sc_window_attention(d, *(to_dev_storage(x, "bf16") for x in (q, k, v)), lse=True,
+                                                 score_partials=True)
+        scores = sc.sc_ltp_score(d, sp)
+        torch.cuda.synchronize()
+        res.append((out.view(torch.int16).cpu().numpy(), lse.cpu().numpy(), scores.cpu().numpy()))
+    for b, L in enumerate(inp["valid_len"]):
+        assert np.array_equal(res[0][0][b, :L], res[1][0][b, :L]), f"output of sequence {b} differs"
+        assert np.array_equal(res[0][1][b, :, :L], res[1][1][b, :, :L]), f"lse of sequence {b} differs"
+        assert np.array_equal(res[0][2][b, :L], res[1][2][b, :L]), f"scores of sequence {b} differ"
+    log(f"dispatch orders bit-identical (causal {causal})")
