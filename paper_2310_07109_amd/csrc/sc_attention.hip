@@ -533,6 +533,23 @@ SC_DEV void window_fwd_block(const AttnArgs& a, int bh, int qb, Smem<DT>& sm, ui
   if (g == 0 && l2g && qrow < n) l2g[qrow] = qvalid ? lse2 : INFINITY;
 }
 
+// Rows 16w .. 16w+15 of a 64-row bf16 tile (two wave loads of 8 rows); tile
+// row R holds global row rowfn(R), which must be a valid row.  Byte offsets
+// from the slice base fit in 32 bits (checked by the host).
+template <typename RowFn>
+SC_DEV void tile_dma(const __bf16* g, unsigned ld_bytes, __bf16* tile, int w, int, RowFn rowfn) {
+  const int lane = threadIdx.x & 63;
+#pragma unroll
+  for (int j = 0; j < 2; ++j) {
+    const int R0 = 16 * w + 8 * j, R = R0 + (lane >> 3);
+    const unsigned u = (lane & 7) ^ (lane >> 3);  // slot (lane & 7) of row R holds unit slot ^ (R & 7)
+    // the LDS base is the same for the whole wave; readfirstlane lets the
+    // compiler keep it in a scalar register when it derives from a loaded value
+    lds_dma16(g, (unsigned)rowfn(R) * ld_bytes + 16u * u,
+              __builtin_amdgcn_readfirstlane(lds_addr(tile + R0 * Tr<1>::kPitch)));
+  }
+}
+
 // ------------------------------------------------------ global rows -------
 // Global query rows attend to every valid key: a dense strip, split over key
 // ranges of kGlobalKeySpan.  Block = 64 global slots x one key range.
@@ -582,67 +599,91 @@ SC_DEV void gr_fwd_block(const AttnArgs& a, int lin, Smem<DT>& sm) {
   const T* Kg = static_cast<const T*>(a.k) + blk.b * a.bs_in + blk.h * kHeadDim;
   const T* Vg = static_cast<const T*>(a.v) + blk.b * a.bs_in + blk.h * kHeadDim;
   const int ntile = (kend - kbeg + kBK - 1) / kBK;
-  Stage<DT> stk, stv;
+  // Round r computes key tiles 2r (buffer 0) and 2r + 1 (buffer 1), one per
+  // pair of waves: four round trips to memory per 512 keys instead of eight
+  // with one tile per step (the blocks are latency-bound: little math per tile).
+  // bf16: the pair goes straight into LDS by direct loads once the previous
+  // round has read it (rows past kend repeat the last key; they are masked);
+  // fp32: through registers, loaded during the previous round.
+  constexpr bool kDma = DT == 1;
+  Stage<DT> sk[kDma ? 1 : 2], sv[kDma ? 1 : 2];
+  auto load_pair = [&](int t0) {  // fp32
+#pragma unroll
+    for (int x = 0; x < 2; ++x)
+      if (t0 + x < ntile) {
+        sk[kDma ? 0 : x].load_range(Kg, a.ld_in, kbeg + (t0 + x) * kBK, kend);
+        sv[kDma ? 0 : x].load_range(Vg, a.ld_in, kbeg + (t0 + x) * kBK, kend);
+      }
+  };
+  auto store_pair = [&](int t0) {  // fp32: registers -> LDS; bf16: direct loads, waited for
+    if constexpr (kDma) {
+      const unsigned ldb = (unsigned)(2 * a.ld_in);
+#pragma unroll
+      for (int x = 0; x < 2; ++x)
+        if (t0 + x < ntile) {
+          const int k0 = kbeg + (t0 + x) * kBK;
+          tile_dma(reinterpret_cast<const __bf16*>(Kg), ldb, reinterpret_cast<__bf16*>(sm.b[x]), w, lane,
+                   [=](int R) { return min(k0 + R, kend - 1); });
+          tile_dma(reinterpret_cast<const __bf16*>(Vg), ldb, reinterpret_cast<__bf16*>(sm.c[x]), w, lane,
+                   [=](int R) { return min(k0 + R, kend - 1); });
+        }
+      wait_dma();
+    } else {
+#pragma unroll
+      for (int x = 0; x < 2; ++x)
+        if (t0 + x < ntile) {
+          sk[x].store(sm.b[x]);
+          sv[x].template store<true>(sm.c[x]);
+        }
+    }
+  };
   {
     Stage<DT> sq;
     const int* sp = sm.pos[0];
     sq.load_rows(Qg, a.ld_in, [&](int row) { return sp[row]; });
+    if constexpr (!kDma) load_pair(0);
     sq.store(sm.b[1]);
   }
-  stk.load_range(Kg, a.ld_in, kbeg, kend);
-  stv.load_range(Vg, a.ld_in, kbeg, kend);
-  stk.store(sm.b[0]);
-  stv.template store<true>(sm.c[0]);
   __syncthreads();
-  // wave w serves the 16 slots of group sg = w & 1 over the key half kh = w >> 1
-  // of every tile; the two halves are merged at the end
+  // wave w serves the 16 slots of group sg = w & 1 over the tiles of parity
+  // kh = w >> 1; the two parities are merged at the end
   const int sg = w & 1, kh = w >> 1;
   typename TR::Frag qf[TR::kChunks];
   TR::load_frags(sm.b[1], 16 * sg + lr, g, qf);
   const bool wlive = __ballot(sm.pos[0][16 * sg + lr] >= 0) != 0ull;  // some slot of the group is used
   const int rowpos = sm.pos[0][16 * sg + lr];                           // the lane's global row (-1: unused)
   __syncthreads();  // every wave holds its query fragments before b[1] is reused
+  store_pair(0);
+  __syncthreads();
   float m_use = kNegBig, l_run = 0.f;
   f32x4 o[4];
 #pragma unroll
   for (int dt = 0; dt < 4; ++dt) o[dt] = f32x4{0.f, 0.f, 0.f, 0.f};
-  for (int t = 0; t < ntile; ++t) {
-    const int buf = t & 1, k0 = kbeg + t * kBK;
-    if (t + 1 < ntile) {
-      stk.load_range(Kg, a.ld_in, k0 + kBK, kend);
-      stv.load_range(Vg, a.ld_in, k0 + kBK, kend);
-    }
-    if (wlive && k0 + 32 * kh < kend) {
+  for (int t0 = 0; t0 < ntile; t0 += 2) {
+    const bool more = t0 + 2 < ntile;
+    if (!kDma && more) load_pair(t0 + 2);
+    const int t = t0 + kh, k0 = kbeg + t * kBK;
+    if (wlive && t < ntile) {
       if (a.causal) {  // the lane's global row attends keys up to its own position
         const int hi = min(kend - 1, rowpos) - k0;
-        auto upto = [&](int s4, int i) { return 16 * s4 + 4 * g + i <= hi; };
-        if (kh == 0)
-          softmax_tile<DT, true, 0>(qf, sm.b[buf], sm.c[buf], a.c2, lr, g, m_use, l_run, o, upto);
-        else
-          softmax_tile<DT, true, 1>(qf, sm.b[buf], sm.c[buf], a.c2, lr, g, m_use, l_run, o, upto);
+        softmax_tile<DT, true>(qf, sm.b[kh], sm.c[kh], a.c2, lr, g, m_use, l_run, o,
+                               [&](int s4, int i) { return 16 * s4 + 4 * g + i <= hi; });
       } else if (k0 + kBK <= kend) {
-        auto all = [](int, int) { return true; };
-        if (kh == 0)
-          softmax_tile<DT, false, 0>(qf, sm.b[buf], sm.c[buf], a.c2, lr, g, m_use, l_run, o, all);
-        else
-          softmax_tile<DT, false, 1>(qf, sm.b[buf], sm.c[buf], a.c2, lr, g, m_use, l_run, o, all);
+        softmax_tile<DT, false>(qf, sm.b[kh], sm.c[kh], a.c2, lr, g, m_use, l_run, o, [](int, int) { return true; });
       } else {
         const int hi = kend - 1 - k0;
-        auto below = [&](int s4, int i) { return 16 * s4 + 4 * g + i <= hi; };
-        if (kh == 0)
-          softmax_tile<DT, true, 0>(qf, sm.b[buf], sm.c[buf], a.c2, lr, g, m_use, l_run, o, below);
-        else
-          softmax_tile<DT, true, 1>(qf, sm.b[buf], sm.c[buf], a.c2, lr, g, m_use, l_run, o, below);
+        softmax_tile<DT, true>(qf, sm.b[kh], sm.c[kh], a.c2, lr, g, m_use, l_run, o,
+                               [&](int s4, int i) { return 16 * s4 + 4 * g + i <= hi; });
       }
     }
-    if (t + 1 < ntile) {
-      stk.store(sm.b[buf ^ 1]);
-      stv.template store<true>(sm.c[buf ^ 1]);
+    if (more) {
+      __syncthreads();  // both tiles read before they are overwritten
+      store_pair(t0 + 2);
     }
     __syncthreads();
   }
   float l_row = group_sum(l_run);
-  // merge the two key halves of each slot group through LDS (the key tiles
+  // merge the two tile parities of each slot group through LDS (the key tiles
   // are no longer needed): the kh = 1 wave publishes its row state, the
   // kh = 0 wave combines, in that fixed order
   constexpr int kXRow = 68;  // floats per row: 64 dims, max, sum (16-byte aligned rows)
@@ -689,23 +730,6 @@ SC_DEV void gr_fwd_block(const AttnArgs& a, int lin, Smem<DT>& sm) {
 // 118 (4 waves per SIMD), which measured 3-5 % faster.
 constexpr int kSub1 = 1;
 constexpr int kBQ2 = 64 * kSub1;  // queries per block
-
-// Rows 16w .. 16w+15 of a 64-row bf16 tile (two wave loads of 8 rows); tile
-// row R holds global row rowfn(R), which must be a valid row.  Byte offsets
-// from the slice base fit in 32 bits (checked by the host).
-template <typename RowFn>
-SC_DEV void tile_dma(const __bf16* g, unsigned ld_bytes, __bf16* tile, int w, int, RowFn rowfn) {
-  const int lane = threadIdx.x & 63;
-#pragma unroll
-  for (int j = 0; j < 2; ++j) {
-    const int R0 = 16 * w + 8 * j, R = R0 + (lane >> 3);
-    const unsigned u = (lane & 7) ^ (lane >> 3);  // slot (lane & 7) of row R holds unit slot ^ (R & 7)
-    // the LDS base is the same for the whole wave; readfirstlane lets the
-    // compiler keep it in a scalar register when it derives from a loaded value
-    lds_dma16(g, (unsigned)rowfn(R) * ld_bytes + 16u * u,
-              __builtin_amdgcn_readfirstlane(lds_addr(tile + R0 * Tr<1>::kPitch)));
-  }
-}
 
 // One 64-key tile for the query sub-blocks of a wave.  Bit st of `live`
 // (wave-uniform) says whether 16-key sub-tile st can hold an allowed pair; in
