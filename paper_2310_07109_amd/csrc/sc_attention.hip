@@ -594,7 +594,6 @@ SC_DEV void gr_fwd_block(const AttnArgs& a, int lin, Smem<DT>& sm) {
   const int kbeg = blk.kc * kGlobalKeySpan;
   if (kbeg >= L) return;
   const int kend = min(L, kbeg + kGlobalKeySpan);
-  if (!gr_slots(a, blk, L, sm.pos[0])) return;
   const T* Qg = static_cast<const T*>(a.q) + blk.b * a.bs_in + blk.h * kHeadDim;
   const T* Kg = static_cast<const T*>(a.k) + blk.b * a.bs_in + blk.h * kHeadDim;
   const T* Vg = static_cast<const T*>(a.v) + blk.b * a.bs_in + blk.h * kHeadDim;
@@ -615,7 +614,7 @@ SC_DEV void gr_fwd_block(const AttnArgs& a, int lin, Smem<DT>& sm) {
         sv[kDma ? 0 : x].load_range(Vg, a.ld_in, kbeg + (t0 + x) * kBK, kend);
       }
   };
-  auto store_pair = [&](int t0) {  // fp32: registers -> LDS; bf16: direct loads, waited for
+  auto issue_pair = [&](int t0) {  // bf16: direct loads into the tile buffers
     if constexpr (kDma) {
       const unsigned ldb = (unsigned)(2 * a.ld_in);
 #pragma unroll
@@ -627,6 +626,11 @@ SC_DEV void gr_fwd_block(const AttnArgs& a, int lin, Smem<DT>& sm) {
           tile_dma(reinterpret_cast<const __bf16*>(Vg), ldb, reinterpret_cast<__bf16*>(sm.c[x]), w, lane,
                    [=](int R) { return min(k0 + R, kend - 1); });
         }
+    }
+  };
+  auto store_pair = [&](int t0) {  // fp32: registers -> LDS; bf16: direct loads, waited for
+    if constexpr (kDma) {
+      issue_pair(t0);
       wait_dma();
     } else {
 #pragma unroll
@@ -637,24 +641,41 @@ SC_DEV void gr_fwd_block(const AttnArgs& a, int lin, Smem<DT>& sm) {
         }
     }
   };
-  {
-    Stage<DT> sq;
-    const int* sp = sm.pos[0];
-    sq.load_rows(Qg, a.ld_in, [&](int row) { return sp[row]; });
-    if constexpr (!kDma) load_pair(0);
-    sq.store(sm.b[1]);
+  // bf16: the first pair is in flight while the slots and the query rows load
+  issue_pair(0);
+  if (!gr_slots(a, blk, L, sm.pos[0])) {
+    if constexpr (kDma) wait_dma();  // no direct load may land after the block has left
+    return;
   }
-  __syncthreads();
   // wave w serves the 16 slots of group sg = w & 1 over the tiles of parity
   // kh = w >> 1; the two parities are merged at the end
   const int sg = w & 1, kh = w >> 1;
+  const int rowpos = sm.pos[0][16 * sg + lr];                  // the lane's global row (-1: unused)
+  const bool wlive = __ballot(rowpos >= 0) != 0ull;            // some slot of the group is used
   typename TR::Frag qf[TR::kChunks];
-  TR::load_frags(sm.b[1], 16 * sg + lr, g, qf);
-  const bool wlive = __ballot(sm.pos[0][16 * sg + lr] >= 0) != 0ull;  // some slot of the group is used
-  const int rowpos = sm.pos[0][16 * sg + lr];                           // the lane's global row (-1: unused)
-  __syncthreads();  // every wave holds its query fragments before b[1] is reused
-  store_pair(0);
-  __syncthreads();
+  if constexpr (kDma) {
+    // query fragments straight from memory (the same dims per lane group as
+    // the key fragments; unused slots zero)
+    const T* qrow = Qg + (long long)max(rowpos, 0) * a.ld_in;
+    const bf16x8 z = {};
+    qf[0] = rowpos >= 0 ? *reinterpret_cast<const bf16x8*>(qrow + 8 * g) : z;
+    qf[1] = rowpos >= 0 ? *reinterpret_cast<const bf16x8*>(qrow + 32 + 8 * g) : z;
+    wait_dma();
+    __syncthreads();
+  } else {
+    {
+      Stage<DT> sq;
+      const int* sp = sm.pos[0];
+      sq.load_rows(Qg, a.ld_in, [&](int row) { return sp[row]; });
+      load_pair(0);
+      sq.store(sm.b[1]);
+    }
+    __syncthreads();
+    TR::load_frags(sm.b[1], 16 * sg + lr, g, qf);
+    __syncthreads();  // every wave holds its query fragments before b[1] is reused
+    store_pair(0);
+    __syncthreads();
+  }
   float m_use = kNegBig, l_run = 0.f;
   f32x4 o[4];
 #pragma unroll
