@@ -455,10 +455,24 @@ def capture(step, torch):
     return replay
 
 
+# Seconds of untimed load before the warmup steps of every timed run (--settle).  After idling, the GPU runs at
+# a lower clock for its first few hundred milliseconds of load: the seq-4096 step measured 0.155-0.160 ms per step
+# after 5 or 10 warmup steps and 0.141-0.143 ms after 3000 (0.5 s), in one process, and fell back to 0.160 after
+# a 2-second pause.
+SETTLE_S = 0.5
+TWO_STREAMS = None  # created first thing in main (see there)
+
+
 def timed(step, steps, warmup, torch):
-    """Runs `warmup` untimed steps, then `steps` timed ones bracketed by synchronisations, with an event on the
-    launch stream before every step and after the last.  step(i) gets the step index (None when untimed).
-    Returns (per-step milliseconds, mean milliseconds over the bracket, wall milliseconds per step)."""
+    """Runs the step untimed for SETTLE_S seconds and `warmup` times, then `steps` timed ones bracketed by
+    synchronisations, with an event on the launch stream before every step and after the last.  step(i) gets
+    the step index (None when untimed).  Returns (per-step milliseconds, mean milliseconds over the bracket,
+    wall milliseconds per step)."""
+    t_end = time.perf_counter() + SETTLE_S
+    while time.perf_counter() < t_end:
+        for _ in range(8):
+            step(None)
+        torch.cuda.synchronize()
     for _ in range(warmup):
         step(None)
     torch.cuda.synchronize()
@@ -579,6 +593,78 @@ def measure(sc, si, torch, np, inp, theta, steps, warmup, dev="cuda:0", keep_rat
     return dict(ms=median(per), mean_ms=mean_ms, wall_ms=wall_ms, fwd_ms=median(fwd), cols_ms=median(cols),
                 tokens=tokens, kept=kept, flops=flops, bytes=bytes_, roof=roof, theta=theta, pairs=pairs,
                 other_ms=median(per_other))
+
+
+def two_streams(sc, torch, np, inp, theta, steps, warmup, dev="cuda:0", causal=False):
+    """The same step with the batch's sequences split into two halves (even and odd indices), each half's
+    window attention, scores and prune + compaction enqueued on a stream of its own (default priority), the
+    halves alternating.  Results are identical to the single call's; the halves' kernels overlap each other's
+    launch tails.  Returns milliseconds per step of the whole batch, between an event before the first step
+    (both streams wait on it) and one after both streams' last."""
+    B, n, H, G = inp["B"], inp["n"], inp["H"], inp["G"]
+
+    def half(rows):
+        sel = np.array(rows)
+        d = sc.Desc(len(rows), n, H, inp["window"],
+                    torch.from_numpy(np.ascontiguousarray(inp["valid_len"][sel], dtype=np.int32)).to(dev),
+                    torch.from_numpy(np.ascontiguousarray(inp["global_pos"][sel], dtype=np.int32)).to(dev),
+                    inp["alpha"], sc.SC_BF16, causal=causal)
+        t = dict(d=d)
+        for x in ("q", "k", "v"):
+            t[x] = torch.from_numpy(np.ascontiguousarray(inp[x][sel]).view(np.int16)).to(dev).view(torch.bfloat16)
+        t["out"], t["oc"] = torch.empty_like(t["q"]), torch.empty_like(t["q"])
+        t["lse"] = torch.empty((len(rows), H, n), dtype=torch.float32, device=dev)
+        t["sp"] = torch.empty(sc.sc_score_partials_size(d) // 4, dtype=torch.float32, device=dev)
+        t["ws_attn"] = torch.empty(max(sc.sc_window_attention_workspace_size(d), 1), dtype=torch.uint8, device=dev)
+        t["scores"] = torch.empty((len(rows), n), dtype=torch.float32, device=dev)
+        t["outs"] = dict(keep_idx=torch.empty((len(rows), n), dtype=torch.int32, device=dev),
+                         new_len=torch.empty((len(rows),), dtype=torch.int32, device=dev),
+                         new_global_pos=torch.empty((len(rows), max(G, 1)), dtype=torch.int32, device=dev),
+                         orig_idx_out=torch.empty((len(rows), n), dtype=torch.int32, device=dev))
+        t["ws_prune"] = torch.empty(sc.sc_ltp_prune_compact_workspace_size(d), dtype=torch.uint8, device=dev)
+        return t
+
+    halves = [half(list(range(0, B, 2))), half(list(range(1, B, 2)))]
+    streams = TWO_STREAMS or [torch.cuda.Stream(), torch.cuda.Stream()]
+    for t, st in zip(halves, streams):
+        t["stream"] = st
+
+    def run(t):
+        d, st = t["d"], t["stream"]
+        sc.sc_window_attention(d, t["q"], t["k"], t["v"], out=t["out"], lse=t["lse"], score_partials=t["sp"],
+                               workspace=t["ws_attn"], stream=st)
+        sc.sc_ltp_score(d, t["sp"], scores=t["scores"], stream=st)
+        sc.sc_ltp_prune_compact(d, t["scores"], theta, True, [t["out"]], dsts=[t["oc"]], outs=t["outs"],
+                                workspace=t["ws_prune"], stream=st)
+
+    def step():
+        for t in halves:
+            run(t)
+
+    t_end = time.perf_counter() + SETTLE_S
+    while time.perf_counter() < t_end:
+        for _ in range(8):
+            step()
+        torch.cuda.synchronize()
+    for _ in range(warmup):
+        step()
+    torch.cuda.synchronize()
+    main = torch.cuda.current_stream()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    w0 = time.perf_counter()
+    e0.record(main)
+    for t in halves:
+        t["stream"].wait_event(e0)
+    for _ in range(steps):
+        step()
+    for t in halves:
+        e = torch.cuda.Event()
+        e.record(t["stream"])
+        main.wait_event(e)
+    e1.record(main)
+    torch.cuda.synchronize()
+    wall = (time.perf_counter() - w0) * 1e3 / max(steps, 1)
+    return e0.elapsed_time(e1) / max(steps, 1), wall
 
 
 def measure_passes(sc, si, torch, np, cfg, steps, warmup, dev="cuda:0", graph=True):
@@ -721,11 +807,18 @@ def sweep(args, sc, si, torch, np):
 
 
 def main():
+    global SETTLE_S, TWO_STREAMS
     ap = argparse.ArgumentParser(description=__doc__)
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=50)
     ap.add_argument("--warmup", type=int, default=5)
+    ap.add_argument("--settle", type=float, default=SETTLE_S, metavar="SECONDS",
+                    help="untimed load before each timed run's warmup steps, so that the GPU runs at its sustained "
+                         "clock (0: none)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-two-streams", action="store_true",
+                    help="skip the extra measurement of the batch as two halves on two streams (kernel traces: it "
+                         "overlaps kernels)")
     ap.add_argument("--graph", action="store_true",
                     help="time steps replayed from a HIP graph captured once (default: eager launches; the other "
                          "mode's time is reported beside it either way)")
@@ -756,6 +849,7 @@ def main():
                     help="instead of the single measurement, sweep the window (n 4096) and the length (window "
                          "512), one JSON line per point")
     args = ap.parse_args()
+    SETTLE_S = max(args.settle, 0.0)
     if args.gpus != 1:
         print(f"bench.py measures one GPU only: the hot path runs on a single MI355X; --gpus {args.gpus} is not "
               "supported (sharding across GPUs is described, not built).", file=sys.stderr)
@@ -768,6 +862,15 @@ def main():
     import sc_inputs as si
 
     torch.cuda.set_device(0)
+    # the two-stream measurement's streams, created and given work before anything else runs: a stream takes
+    # one of the device's hardware queues at its first work, and two streams first used late in the run (after
+    # the single-stream measurement) ran one after the other, as if on one queue (0.170 against 0.122 ms per
+    # step)
+    TWO_STREAMS = [torch.cuda.Stream(), torch.cuda.Stream()]
+    for st in TWO_STREAMS:
+        with torch.cuda.stream(st):
+            torch.zeros(1, device="cuda:0")
+    torch.cuda.synchronize()
     dev = "cuda:0"
     if args.probe_valu:
         probe_valu()
@@ -779,8 +882,8 @@ def main():
         sweep(args, sc, si, torch, np)
         return
     cid, desc = WORKLOADS[args.workload]
-    common = {"n_gpus": 1, "steps": args.steps, "warmup": args.warmup, "higher_is_better": True, "scaling": "weak",
-              "vs_baseline": None, "dtype": "bf16", "data": "synthetic"}
+    common = {"n_gpus": 1, "steps": args.steps, "warmup": args.warmup, "settle_s": SETTLE_S, "higher_is_better": True,
+              "scaling": "weak", "vs_baseline": None, "dtype": "bf16", "data": "synthetic"}
     launch = "HIP graph replay (one capture of the step)" if args.graph else "eager launches"
     if cid == "soft":
         m = measure_soft(args, sc, si, torch, np, dev)
@@ -879,6 +982,13 @@ def main():
         "kept_per_sequence": m["kept"],
         "wall_ms_per_step": round(m["wall_ms"], 4),
     }
+    if args.workload == "seq4096" and args.score == "partials" and keep_ratio is None and not args.no_two_streams:
+        ms2, wall2 = two_streams(sc, torch, np, inp, theta, args.steps, args.warmup, dev, causal=args.causal)
+        result["two_streams"] = {"ms_per_step": round(ms2, 4), "wall_ms_per_step": round(wall2, 4),
+                                 "value": round(tokens / (ms2 * 1e-3), 1),
+                                 "unit": "kept-token-layers/s",
+                                 "how": "the same 8 sequences as two halves (even and odd indices), each half's three "
+                                        "calls on a stream of its own; not the headline"}
     if not args.no_cpu_baseline:
         import oracle
 
