@@ -38,7 +38,12 @@
  *     size is returned by the matching *_workspace_size() call (may be 0, in
  *     which case workspace may be NULL).
  *   - `stream` is a hipStream_t passed as void* (NULL = the default stream).
- *     All work is enqueued asynchronously on it; nothing synchronises.
+ *     All work is enqueued asynchronously on it; nothing synchronises.  Calls
+ *     on different streams may overlap when each has its own outputs and
+ *     workspace (the library keeps no state between calls, apart from
+ *     sc_window_attention_noalloc's device array and the benchmark events of
+ *     sc_profile_window_kernel); e.g. a batch split into two halves on two
+ *     streams gives the single call's results.
  *   - Arguments are validated on the host before anything is enqueued.  On any
  *     error nothing is enqueued and a negative sc_status is returned.
  *     Device-resident arguments (valid_len, global_pos) cannot be checked on
