@@ -584,7 +584,7 @@ def measure(sc, si, torch, np, inp, theta, steps, warmup, dev="cuda:0", keep_rat
         r = inp["window"] // 2
         g_used = sum(len([p for p in inp["global_pos"][b] if 0 <= p < inp["valid_len"][b]]) for b in range(B))
         score_bytes = 4 * H * (tokens * (min(2 * r + 1, n)) + 2 * g_used * n) + 4 * B * n
-        score_kernels = "k_band_partials + k_score_from_partials"
+        score_kernels = "k_band_rows + k_band_keys + k_score_from_partials"
     prune_bytes = 4 * B * n * 3 + 2 * sum(kept) * H * dd * 2
     roof = roofline(flops, bytes_, median(fwd), median(cols), pairs,
                     score=(score_kernels, score_us, score_bytes),

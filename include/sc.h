@@ -167,7 +167,9 @@ sc_status sc_window_attention(const sc_attn_desc *desc, const void *q, const voi
 
 /* Workspace of sc_ltp_score: 0 for SC_SCORE_FROM_PARTIALS; for
  * SC_SCORE_FROM_BAND_PROBS, sc_score_partials_size(desc) bytes (the band layout
- * is first reduced to the same partials).  0 on an invalid descriptor. */
+ * is reduced to the same partials) plus one float per (sequence, head, block of
+ * 128 rows, key the block reaches, rounded up to 256 keys).  0 on an invalid
+ * descriptor. */
 size_t sc_ltp_score_workspace_size(const sc_attn_desc *desc, int32_t mode);
 
 /*

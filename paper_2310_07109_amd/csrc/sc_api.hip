@@ -314,9 +314,10 @@ sc_status sc_window_attention_noalloc(const sc_attn_desc* d, const void* q, cons
 }
 
 size_t sc_ltp_score_workspace_size(const sc_attn_desc* d, int32_t mode) {
-  // the band layout is first reduced to the partials of the fused path
+  // the band layout is first reduced to per-row-block partial sums, then to
+  // the partials of the fused path
   if (mode != SC_SCORE_FROM_BAND_PROBS || check_desc(d) != SC_OK) return 0;
-  return sc_score_partials_size(d);
+  return sc_score_partials_size(d) + sizeof(float) * sc::band_parts_floats(d->B, d->H, d->n, d->window, d->G);
 }
 
 static sc_status sc_ltp_score_impl(const sc_attn_desc* d, int32_t mode, const float* src, float* scores,
@@ -339,7 +340,9 @@ static sc_status sc_ltp_score_impl(const sc_attn_desc* d, int32_t mode, const fl
                      ? sc::launch_score_from_partials(src, d->valid_len, d->global_pos, d->B, d->n, d->H, d->G, geo,
                                                       scores, s)
                      : sc::launch_score_from_band(src, d->valid_len, d->global_pos, d->B, d->n, d->H, d->G, geo,
-                                                  static_cast<float*>(workspace), scores, s);
+                                                  static_cast<float*>(workspace),
+                                                  static_cast<float*>(workspace) + sc_score_partials_size(d) / 4,
+                                                  scores, s);
   return e == hipSuccess ? SC_OK : SC_EHIP;
 }
 

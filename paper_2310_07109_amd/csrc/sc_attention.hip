@@ -1767,7 +1767,7 @@ struct ScorePartials {
   const float* grow;  // [B, H, ngc, n] column sums over the global rows
   int n, H, G, ngc, nqr;
 };
-// the same pieces, written by k_band_partials
+// the same pieces, written by k_band_keys and k_band_rows
 struct ScorePartialsOut {
   float* band;
   float* gcol;
@@ -1877,28 +1877,40 @@ __global__ __launch_bounds__(kScoreKeys * kScoreGroups) void k_score_from_partia
 // reduction is k_score_from_partials.  The score of key k is its band
 // sub-diagonal (entries (i, j) with i - r + j = k; zero at global keys), its
 // global column (zero at global rows) and its entries of the global rows.
-//   band blocks    (sequence, head, 256 keys): thread = key; the sub-diagonal
-//                  over the rows that reach the block (for a fixed row, the
-//                  threads read consecutive entries), eight rows in flight
-//                  with their own accumulators; then the global-row entries
-//                  of the key, per 32-slot chunk.
-//   column blocks  (sequence, head, 512-row range): the global-column block
-//                  of the range summed per slot, 8 row groups x 32 slots, the
-//                  row groups added in order through LDS.
-constexpr int kBandKeys = 256;
+// Entry (i, j) of a head's band sits at i * (2r + 1) + j = 2r * i + k + r, so
+// for a fixed row the entries of consecutive keys are consecutive floats.
+// Two launches, both in a fixed order with no atomics:
+//   k_band_rows    column blocks (sequence, head, 512-row range), dispatched
+//                  first: the global-column block of the range summed per
+//                  slot, one row group per 32 threads, the row groups added in
+//                  order through LDS.  Row blocks (sequence, head, 128 rows):
+//                  each block reads its rows once, front to back; the keys
+//                  they reach, [i0 - r, i0 + 128 + r), are cut into segments
+//                  of 64 * VEC keys, one per wave at a time, and the wave walks
+//                  the segment's rows with kU rows in flight, a lane summing
+//                  VEC consecutive keys in row order.  VEC = 4 (16-byte loads)
+//                  needs r and n multiples of 4 and a 16-byte aligned layout.
+//                  Output: one partial sum per (row block, key of its span).
+//   k_band_keys    thread = key: the partials of the row blocks that reach it,
+//                  in row-block order, then its global-row entries per 32-slot
+//                  chunk.
+constexpr int kBandRows = 128;
 constexpr int kBandUnroll = 16;
 
-__global__ __launch_bounds__(256) void k_band_partials(const float* bp, const int* valid_len, int B, int n, int H,
-                                                       int G, AttnGeom geo, ScorePartialsOut po) {
-  __shared__ float red[8][32];
-  const int tid = threadIdx.x;
-  const int nkb = (n + kBandKeys - 1) / kBandKeys;
+int band_segments(int rb, int vec) { return (kBandRows + 2 * rb + 64 * vec - 1) / (64 * vec); }
+
+template <int VEC>
+__global__ __launch_bounds__(256) void k_band_rows(const float* bp, const int* valid_len, int B, int n, int H, int G,
+                                                   AttnGeom geo, int nseg, float* parts, ScorePartialsOut po) {
+  constexpr int kU = 16;  // rows in flight per wave
+  constexpr int kSeg = 64 * VEC;
+  __shared__ float red[8 * 32];
+  const int tid = threadIdx.x, nthr = blockDim.x;
   const long long ncol = G > 0 ? (long long)B * H * geo.nqr : 0;
   const float* band = bp;
-  const float* gcol = band + (size_t)B * H * n * geo.bw;
-  const float* grow = gcol + (size_t)B * H * n * G;
   if ((long long)blockIdx.x < ncol) {
-    // global-column block (first: it walks its rows in one pass per slot group)
+    const float* gcol = band + (size_t)B * H * n * geo.bw;
+    const int kRG = nthr >> 5;  // row groups (at most 8)
     const int qr = (int)(blockIdx.x % geo.nqr), bh = (int)(blockIdx.x / geo.nqr), b = bh / H;
     const int L = clampi(valid_len[b], 0, n);
     const int rg = tid >> 5, sl = tid & 31;
@@ -1907,66 +1919,107 @@ __global__ __launch_bounds__(256) void k_band_partials(const float* bp, const in
       const int slot = s0 + sl, sc = min(slot, G - 1);  // clamped: in bounds, masked below
       float acc[kBandUnroll] = {};
       int i = r0 + rg;
-      for (; i + 8 * (kBandUnroll - 1) < r1; i += 8 * kBandUnroll) {
+      for (; i + kRG * (kBandUnroll - 1) < r1; i += kRG * kBandUnroll) {
 #pragma unroll
-        for (int u = 0; u < kBandUnroll; ++u) acc[u] += gcol[((size_t)bh * n + i + 8 * u) * G + sc];
+        for (int u = 0; u < kBandUnroll; ++u) acc[u] += gcol[((size_t)bh * n + i + kRG * u) * G + sc];
       }
-      for (int u = 0; i < r1; i += 8, ++u) acc[u] += gcol[((size_t)bh * n + i) * G + sc];
+      for (int u = 0; i < r1; i += kRG, ++u) acc[u] += gcol[((size_t)bh * n + i) * G + sc];
       float t = 0.f;
 #pragma unroll
       for (int u = 0; u < kBandUnroll; ++u) t += acc[u];
-      red[rg][sl] = slot < G ? t : 0.f;
+      red[rg * 32 + sl] = slot < G ? t : 0.f;
       __syncthreads();
       if (rg == 0 && slot < G) {
         float tot = 0.f;
-#pragma unroll
-        for (int j = 0; j < 8; ++j) tot += red[j][sl];
+        for (int j = 0; j < kRG; ++j) tot += red[j * 32 + sl];
         po.gcol[((size_t)bh * geo.nqr + qr) * G + slot] = tot;
       }
       __syncthreads();
     }
     return;
   }
-  // band block: thread = key; each wave walks the rows that reach its own 64
-  // keys
+  const int np = (n + kBandRows - 1) / kBandRows;
   const long long blk = blockIdx.x - ncol;
-  const int kb = (int)(blk % nkb), bh = (int)(blk / nkb), b = bh / H;
+  const int p = (int)(blk % np), bh = (int)(blk / np), b = bh / H;
   const int L = clampi(valid_len[b], 0, n);
-  const int k = kb * kBandKeys + tid;
-  if (k >= n) return;
-  float sum = 0.f;
-  const int kw = kb * kBandKeys + (tid & ~63);  // first key of the wave
-  if (kw < L) {
-    const int rb = geo.rb, bw = geo.bw;
-    const float* rows = band + (size_t)bh * n * bw;
-    const int i0 = max(0, kw - rb), i1 = min(L, kw + 64 + rb);
-    float acc[kBandUnroll] = {};
-    int i = i0;
-    for (; i + kBandUnroll <= i1; i += kBandUnroll) {
-      // the mask multiplies the loaded value (entries are finite): every load
-      // is used, so none is made conditional and all eight are in flight
+  const int rb = geo.rb;
+  const int i0 = p * kBandRows, i1 = min(L, i0 + kBandRows);
+  const int lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6), nw = nthr >> 6;
+  const char* head = reinterpret_cast<const char*>(band + (size_t)bh * n * geo.bw);
+  const size_t rstride = 8ull * (unsigned)rb;  // bytes per row along a sub-diagonal
+  float* out = parts + ((size_t)bh * np + p) * nseg * kSeg;
+  for (int seg = wave; seg < nseg; seg += nw) {
+    const int kseg = i0 - rb + seg * kSeg;  // first key of the segment (may lie outside [0, n))
+    const int kl = kseg + lane * VEC;
+    // the segment's rows: those of the block that reach one of its keys
+    const int r0 = max(i0, kseg - rb), r1 = min(i1, kseg + kSeg + rb);
+    float sum[VEC] = {};
+    if (r0 < r1 && kseg < n && kseg + kSeg > 0) {
+      // entry (i, key) at 2r * i + key + r lies inside the head's layout for
+      // every row i < n and key < n: keys outside [0, n) address a clamped key
+      // and are masked, and so are the clamped rows of the last round
+      const unsigned loff = (unsigned)(clampi(kl, 0, n - VEC) + rb) * 4u;  // below 8 n
+      for (int ib = r0; ib < r1; ib += kU) {
+        float v[kU][VEC];
 #pragma unroll
-      for (int u = 0; u < kBandUnroll; ++u) {
-        const int j = k - (i + u) + rb;
-        const float v = rows[(size_t)(i + u) * bw + clampi(j, 0, bw - 1)];  // in bounds
-        acc[u] = fmaf(v, (j >= 0 && j < bw) ? 1.f : 0.f, acc[u]);
+        for (int u = 0; u < kU; ++u) {
+          const char* row = head + rstride * (size_t)min(ib + u, r1 - 1);
+          if constexpr (VEC == 4) {
+            const f32x4 w = *reinterpret_cast<const f32x4*>(row + loff);
+            v[u][0] = w[0], v[u][1] = w[1], v[u][2] = w[2], v[u][3] = w[3];
+          } else {
+            v[u][0] = *reinterpret_cast<const float*>(row + loff);
+          }
+        }
+#pragma unroll
+        for (int u = 0; u < kU; ++u) {
+          const int i = ib + u;
+#pragma unroll
+          for (int e = 0; e < VEC; ++e) {
+            // entry j = key - i + r of row i exists for 0 <= j <= 2r
+            const bool in = i < r1 && (unsigned)(kl + e) < (unsigned)n &&
+                            (unsigned)(kl + e - i + rb) <= 2u * (unsigned)rb;
+            sum[e] += in ? v[u][e] : 0.f;
+          }
+        }
       }
     }
-    for (int u = 0; i < i1; ++i, ++u) {
-      const int j = k - i + rb;
-      const float v = rows[(size_t)i * bw + clampi(j, 0, bw - 1)];
-      acc[u] = fmaf(v, (j >= 0 && j < bw) ? 1.f : 0.f, acc[u]);
-    }
 #pragma unroll
-    for (int u = 0; u < kBandUnroll; ++u) sum += acc[u];
+    for (int e = 0; e < VEC; ++e) out[seg * kSeg + lane * VEC + e] = sum[e];
   }
-  // keys at or beyond L read rows below L only, where their entries are zero
-  po.band[(size_t)bh * n + k] = k < L ? sum : 0.f;
+}
+
+__global__ __launch_bounds__(256) void k_band_keys(const float* bp, const int* valid_len, int B, int n, int H, int G,
+                                                   AttnGeom geo, int nseg, int seg_keys, const float* parts,
+                                                   ScorePartialsOut po) {
+  const int k = blockIdx.x * 256 + threadIdx.x;
+  const int bh = blockIdx.y, b = bh / H;
+  if (k >= n) return;
+  const int L = clampi(valid_len[b], 0, n);
+  const int np = (n + kBandRows - 1) / kBandRows, span = nseg * seg_keys, rb = geo.rb;
+  float s = 0.f;
+  if (k < L) {
+    // row blocks holding a row of [k - r, k + r] below L; key k is slot
+    // k - (p * 128 - r) < 128 + 2r of block p's span
+    const int pa = max(0, k - rb) / kBandRows, pb = min(L - 1, k + rb) / kBandRows;
+    for (int p = pa; p <= pb; ++p) s += parts[((size_t)bh * np + p) * span + (k - p * kBandRows + rb)];
+  }
+  // keys at or beyond L are reached by rows below L only where the entries
+  // are zero
+  po.band[(size_t)bh * n + k] = k < L ? s : 0.f;
+  const float* grow = bp + (size_t)B * H * n * geo.bw + (size_t)B * H * n * G;
+  // a chunk's slots loaded together (slots past G read the last slot's row
+  // and are dropped), then added in slot order
   for (int c = 0; c < geo.ngc; ++c) {
     float g = 0.f;
     if (k < L) {
-      const int s1 = min(G, (c + 1) * kGlobalChunk);
-      for (int sl = c * kGlobalChunk; sl < s1; ++sl) g += grow[((size_t)bh * G + sl) * n + k];
+      float t[kGlobalChunk];
+#pragma unroll
+      for (int x = 0; x < kGlobalChunk; ++x)
+        t[x] = grow[((size_t)bh * G + min(c * kGlobalChunk + x, G - 1)) * n + k];
+#pragma unroll
+      for (int x = 0; x < kGlobalChunk; ++x) g = c * kGlobalChunk + x < G ? g + t[x] : g;
     }
     po.grow[((size_t)bh * geo.ngc + c) * n + k] = g;
   }
@@ -2126,13 +2179,34 @@ hipError_t launch_score_from_partials(const float* partials, const int* valid_le
   return hipGetLastError();
 }
 
+size_t band_parts_floats(int B, int H, int n, int window, int G) {
+  const AttnGeom g = attn_geom(n, window, G);
+  // the 16-byte variant's span (segments of 256 keys) covers the other's
+  return (size_t)B * H * ((n + kBandRows - 1) / kBandRows) * band_segments(g.rb, 4) * 256;
+}
+
 hipError_t launch_score_from_band(const float* bp, const int* valid_len, const int* gpos, int B, int n, int H, int G,
-                                  const AttnGeom& g, float* partials, float* scores, hipStream_t s) {
+                                  const AttnGeom& g, float* partials, float* parts, float* scores, hipStream_t s) {
   ScorePartials sp = score_partials(partials, B, n, H, G, g);
   ScorePartialsOut po{partials, const_cast<float*>(sp.gcol), const_cast<float*>(sp.grow)};
-  const long long blocks = (long long)B * H * ((n + kBandKeys - 1) / kBandKeys) + (G > 0 ? (long long)B * H * g.nqr : 0);
-  hipLaunchKernelGGL(k_band_partials, dim3((unsigned)blocks), dim3(256), 0, s, bp, valid_len, B, n, H, G, g, po);
-  const hipError_t e = hipGetLastError();
+  // 16-byte loads need every row's first entry for a lane's first key
+  // (2r * i + key + r, plus the head's offset b * H * n * (2r + 1)) on a
+  // 4-float boundary
+  const bool vec4 = g.rb % 4 == 0 && n % 4 == 0 && reinterpret_cast<uintptr_t>(bp) % 16 == 0;
+  const int vec = vec4 ? 4 : 1, nseg = band_segments(g.rb, vec);
+  const int threads = 64 * (nseg < 4 ? nseg : 4);
+  const long long blocks = (long long)B * H * ((n + kBandRows - 1) / kBandRows) + (G > 0 ? (long long)B * H * g.nqr : 0);
+  if (vec4)
+    hipLaunchKernelGGL(k_band_rows<4>, dim3((unsigned)blocks), dim3(threads), 0, s, bp, valid_len, B, n, H, G, g,
+                       nseg, parts, po);
+  else
+    hipLaunchKernelGGL(k_band_rows<1>, dim3((unsigned)blocks), dim3(threads), 0, s, bp, valid_len, B, n, H, G, g,
+                       nseg, parts, po);
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return e;
+  hipLaunchKernelGGL(k_band_keys, dim3((unsigned)((n + 255) / 256), (unsigned)(B * H)), dim3(256), 0, s, bp,
+                     valid_len, B, n, H, G, g, nseg, 64 * vec, parts, po);
+  e = hipGetLastError();
   if (e != hipSuccess) return e;
   return launch_score_from_partials(partials, valid_len, gpos, B, n, H, G, g, scores, s);
 }

@@ -63,8 +63,11 @@ int profile_set(int enable);
 int profile_read(double* fwd_ms, double* cols_ms, long long cap, long long* calls);
 hipError_t launch_score_from_partials(const float* partials, const int* valid_len, const int* gpos, int B, int n,
                                       int H, int G, const AttnGeom& g, float* scores, hipStream_t s);
+// per-row-block partial sums of the band layout, a part of sc_ltp_score's
+// workspace in the band mode
+size_t band_parts_floats(int B, int H, int n, int window, int G);
 hipError_t launch_score_from_band(const float* bp, const int* valid_len, const int* gpos, int B, int n, int H, int G,
-                                  const AttnGeom& g, float* partials, float* scores, hipStream_t s);
+                                  const AttnGeom& g, float* partials, float* parts, float* scores, hipStream_t s);
 
 struct PruneArgs {
   const float* scores;     // [B, n]

@@ -143,6 +143,14 @@ def test_sizes():
     # huge window: r clamps to n - 1 for the band layout
     assert sc.sc_band_probs_size(desc(window=10 ** 6)) == 4 * 2 * 4 * 256 * (2 * 255 + 1)
     assert sc.sc_score_partials_size(desc(d=16)) == 0
+    # band-mode score workspace: the partials plus, per (b, h) and block of 128 rows, the 128 + 2r keys the block
+    # reaches, rounded up to 256
+    assert sc.sc_ltp_score_workspace_size(dg, sc.SC_SCORE_FROM_PARTIALS) == 0
+    assert sc.sc_ltp_score_workspace_size(dg, sc.SC_SCORE_FROM_BAND_PROBS) == \
+        sc.sc_score_partials_size(dg) + 4 * 2 * 4 * 2 * 256
+    wide = desc(window=10 ** 6)
+    assert sc.sc_ltp_score_workspace_size(wide, sc.SC_SCORE_FROM_BAND_PROBS) == \
+        sc.sc_score_partials_size(wide) + 4 * 2 * 4 * 2 * 768
     assert sc.sc_encoder_attn_stack_workspace_size(desc(), 3) > 0
     assert sc.sc_encoder_attn_stack_workspace_size(desc(), 0) == 0
 

@@ -99,7 +99,7 @@ def config_run(cid):
         ref = oracle.sparse_attention(inp["q64"], inp["k64"], inp["v64"], inp["valid_len"], inp["global_pos"],
                                       inp["window"], inp["alpha"])
         log(f"config {cid}: gpu")
-        g = run_attention(inp)
+        g = run_attention(inp, band=True)
         _CACHE[cid] = (inp, ref, g)
     return _CACHE[cid]
 
@@ -110,7 +110,9 @@ def test_config_attention_and_scores(cid):
     err = check_out(g["out"], ro, inp["dtype"])
     check_lse(g["lse"], rl, inp["valid_len"])
     worst = check_scores(g["scores"], rs, inp["valid_len"])
-    log(f"config {cid}: max |dO| {err:.3g}, worst score rel err {worst:.3g}")
+    # the paper's path: every probability stored in the band layout, scores summed from it
+    worst_band = check_scores(g["band_scores"], rs, inp["valid_len"])
+    log(f"config {cid}: max |dO| {err:.3g}, worst score rel err {worst:.3g} (band layout {worst_band:.3g})")
 
 
 @pytest.mark.parametrize("cid", [1, 2, 4, 6])
