@@ -16,7 +16,10 @@
 //                K-th largest score is found exactly by a radix select on the
 //                order-preserving 32-bit image of the float (four 8-bit digits,
 //                an LDS histogram and a 256-bin suffix scan per digit); tied
-//                scores are ranked in index order by the same block scan.
+//                scores are ranked in index order by the same block scan.  Up
+//                to 8192 tokens a thread owns 8 consecutive tokens, keeps
+//                their keys in registers through the digit passes, and two
+//                block-wide scans (ties, then kept tokens) rank the sequence.
 // k_gather_rows  one wavefront per output row copies the kept input row with
 //                16-byte lanes (coalesced), for up to four tensors at once.
 // k_prune_compact the threshold rule and the compaction in one launch, for
@@ -37,6 +40,7 @@ namespace {
 
 constexpr int kScanThreads = 1024;
 constexpr int kScanWaves = kScanThreads / 64;
+constexpr int kTopkE = 8;  // tokens per thread held in registers by the top-k path
 
 
 // Exclusive rank of this lane among the lanes of its wave whose flag is set,
@@ -69,6 +73,36 @@ SC_DEV int block_rank(bool flag, int* s_wave, int& total) {
   __syncthreads();
   total = s_wave[2 * kScanWaves];
   const int off = s_wave[kScanWaves + w] + r;
+  __syncthreads();  // s_wave is reused by the next call
+  return off;
+}
+
+// Block-wide exclusive sum of one count per thread; returns this thread's
+// offset and writes the block total to `total`.  Contains barriers.
+SC_DEV int block_excl_sum(int v, int* s_wave, int& total) {
+  const int w = threadIdx.x >> 6, lane = threadIdx.x & 63;
+  int incl = v;
+#pragma unroll
+  for (int off = 1; off < 64; off <<= 1) {
+    const int u = __shfl_up(incl, off, 64);
+    if (lane >= off) incl += u;
+  }
+  if (lane == 63) s_wave[w] = incl;
+  __syncthreads();
+  if (w == 0) {
+    const int x = lane < kScanWaves ? s_wave[lane] : 0;
+    int winc = x;
+#pragma unroll
+    for (int off = 1; off < kScanWaves; off <<= 1) {
+      const int u = __shfl_up(winc, off, 64);
+      if (lane >= off) winc += u;
+    }
+    if (lane < kScanWaves) s_wave[kScanWaves + lane] = winc - x;
+    if (lane == kScanWaves - 1) s_wave[2 * kScanWaves] = winc;
+  }
+  __syncthreads();
+  total = s_wave[2 * kScanWaves];
+  const int off = s_wave[kScanWaves + w] + incl - v;
   __syncthreads();  // s_wave is reused by the next call
   return off;
 }
@@ -128,11 +162,31 @@ __global__ __launch_bounds__(kScanThreads) void k_prune_scan(PruneArgs p) {
   uint32_t T = 0u;
   int want = 0;
   bool none = true;  // no candidate is kept by rank
+  // top-k over at most kTopkE * kScanThreads tokens: thread t owns the E
+  // consecutive tokens [t E, t E + E) and keeps their keys in registers for
+  // the count, the four digit passes and the ranking
+  const bool own = p.topk && n <= kTopkE * kScanThreads;
+  const int E = (n + kScanThreads - 1) / kScanThreads, k0 = tid * E;
+  uint32_t okey[kTopkE];
+  unsigned ogk = 0u;  // bit e: token k0 + e is kept as a global token
+  if (own) {
+#pragma unroll
+    for (int e = 0; e < kTopkE; ++e) {
+      const int k = k0 + e;
+      ogk |= (unsigned)(e < E && k < L && p.keep_global && is_glob(k)) << e;
+      okey[e] = e < E ? cand_key(k) : 0u;
+    }
+  }
   if (p.topk) {
     if (tid == 0) s_sel[0] = 0;
     __syncthreads();
     int cnt = 0;
-    for (int k = tid; k < L; k += kScanThreads) cnt += cand_key(k) != 0u;
+    if (own) {
+#pragma unroll
+      for (int e = 0; e < kTopkE; ++e) cnt += okey[e] != 0u;
+    } else {
+      for (int k = tid; k < L; k += kScanThreads) cnt += cand_key(k) != 0u;
+    }
     // candidate count: per-wave sums, one LDS atomic per wave
 #pragma unroll
     for (int off = 32; off > 0; off >>= 1) cnt += __shfl_xor(cnt, off, 64);
@@ -148,9 +202,17 @@ __global__ __launch_bounds__(kScanThreads) void k_prune_scan(PruneArgs p) {
       if (tid < 256) s_hist[tid] = 0;
       __syncthreads();
       const uint32_t hmask = shift == 24 ? 0u : ~0u << (shift + 8);
-      for (int k = tid; k < L; k += kScanThreads) {
-        const uint32_t key = cand_key(k);
-        if (key != 0u && (key & hmask) == (T & hmask)) atomicAdd(&s_hist[(key >> shift) & 255u], 1);
+      if (own) {
+#pragma unroll
+        for (int e = 0; e < kTopkE; ++e) {
+          const uint32_t key = okey[e];
+          if (key != 0u && (key & hmask) == (T & hmask)) atomicAdd(&s_hist[(key >> shift) & 255u], 1);
+        }
+      } else {
+        for (int k = tid; k < L; k += kScanThreads) {
+          const uint32_t key = cand_key(k);
+          if (key != 0u && (key & hmask) == (T & hmask)) atomicAdd(&s_hist[(key >> shift) & 255u], 1);
+        }
       }
       __syncthreads();
       // bins from the top: the digit whose bin holds the want-th largest key
@@ -171,7 +233,42 @@ __global__ __launch_bounds__(kScanThreads) void k_prune_scan(PruneArgs p) {
   const int* oin = p.orig_in ? p.orig_in + (long long)b * n : nullptr;
   int* oout = p.orig_out ? p.orig_out + (long long)b * n : nullptr;
   int carry = 0, tie_carry = 0;
-  for (int base = 0; base < n; base += kScanThreads) {
+  if (own) {
+    // ties before a token, in token order, then the kept tokens before it:
+    // two block scans for the whole sequence
+    int nt = 0;
+#pragma unroll
+    for (int e = 0; e < kTopkE; ++e) nt += !none && okey[e] != 0u && okey[e] == T;
+    int ties;
+    int tr = block_excl_sum(nt, s_wave, ties);
+    unsigned keepm = 0u;
+    int nk = 0;
+#pragma unroll
+    for (int e = 0; e < kTopkE; ++e) {
+      const uint32_t key = okey[e];
+      const bool cand = key != 0u && !none;
+      const bool tie = cand && key == T;
+      const bool kp = ((ogk >> e) & 1u) || (cand && (key > T || (tie && tr < want)));
+      tr += tie;
+      keepm |= (unsigned)kp << e;
+      nk += kp;
+    }
+    int pos = block_excl_sum(nk, s_wave, carry);
+#pragma unroll
+    for (int e = 0; e < kTopkE; ++e) {
+      const int k = k0 + e;
+      if (e < E && k < n) {
+        if ((keepm >> e) & 1u) {
+          kidx[pos] = k;
+          if (oout) oout[pos] = oin ? oin[k] : k;
+          nidx[k] = pos++;
+        } else {
+          nidx[k] = -1;
+        }
+      }
+    }
+  }
+  for (int base = 0; base < n && !own; base += kScanThreads) {
     const int k = base + tid;
     bool keep = false;
     if (!p.topk) {

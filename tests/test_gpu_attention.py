@@ -242,11 +242,13 @@ def test_config_topk_prune(cid):
     log(f"config {cid}: top-k ratio 1.0 keeps {nl.tolist()}")
 
 
-def test_topk_ties_signs_and_lengths():
+@pytest.mark.parametrize("n", [2600, 9000], ids=["registers", "chunked"])
+def test_topk_ties_signs_and_lengths(n):
     """Ties everywhere (scores on 3 levels), negative scores and both zeros, lengths 0 / 1 / n / ragged over
-    several 1024-token chunks."""
+    several 1024-token chunks; n = 2600 takes the path that holds a thread's tokens in registers (up to 8192
+    tokens), n = 9000 the chunked one."""
     rng = np.random.default_rng(5)
-    B, n, G = 6, 2600, 5
+    B, G = 6, 5
     vl = np.array([0, 1, n, 1500, 2047, 999], np.int32)
     gp = np.full((B, G), -1, np.int32)
     for b in range(B):
