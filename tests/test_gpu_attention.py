@@ -39,6 +39,10 @@ SMALL = [
      dict(gp_override=[[0, 159], [5, 159]])),
     ("unused slots", "f32", 2, 140, 2, 40, 4, (140, 140), dict(gp_override=[[3, 77, -1, -1], [-1, -1, -1, -1]])),
     ("600 global tokens", "bf16", 1, 1200, 2, 64, 600, (1100, 1200), {}),
+    # the band-layout scores' one-key loads: n not a multiple of 4, and r = 259 not a multiple of 4, over many
+    # 128-row blocks
+    ("n 2050 window 512", "bf16", 1, 2050, 2, 512, 4, (1900, 2050), {}),
+    ("r 259 fp32", "f32", 1, 2048, 2, 518, 3, (1800, 2048), {}),
 ]
 
 
